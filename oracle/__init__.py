@@ -1,0 +1,357 @@
+"""CPU oracle for Lloyd k-means on compressed vectors -- TEST INFRASTRUCTURE ONLY.
+
+Only the test-suite, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  The product library never calls it.
+
+Thin numpy/ctypes layer over ``libkmq_oracle.so`` (plain C, fp64 sums, exact
+integer paths; see ``kmq_oracle.h`` for the definition each routine follows) plus
+the Lloyd driver (Sec. 2.3: STEP 1 random init, T x (STEP 2 assign, STEP 3
+update), then one more STEP 2) and the PCA eigensolve (numpy ``eigh``).
+"""
+from __future__ import annotations
+
+import ctypes as ct
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(HERE, "libkmq_oracle.so")
+_lib = None
+
+EMPTY_SPLIT = 0
+EMPTY_KEEP = 1
+
+_f32p = np.ctypeslib.ndpointer(np.float32, flags="C_CONTIGUOUS")
+_f64p = np.ctypeslib.ndpointer(np.float64, flags="C_CONTIGUOUS")
+_u8p = np.ctypeslib.ndpointer(np.uint8, flags="C_CONTIGUOUS")
+_i8p = np.ctypeslib.ndpointer(np.int8, flags="C_CONTIGUOUS")
+_u32p = np.ctypeslib.ndpointer(np.uint32, flags="C_CONTIGUOUS")
+_i32p = np.ctypeslib.ndpointer(np.int32, flags="C_CONTIGUOUS")
+_i64p = np.ctypeslib.ndpointer(np.int64, flags="C_CONTIGUOUS")
+_i64 = ct.c_int64
+_i32 = ct.c_int32
+
+
+def _null(dtype):
+    return np.ctypeslib.ndpointer(dtype, flags="C_CONTIGUOUS")
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            from . import build as _b
+            _b.build()
+        L = ct.CDLL(_LIB_PATH)
+        sig = {
+            "orc_sq8_fit": [_f32p, _i64, _i32, _f32p, _f32p],
+            "orc_sq8_encode": [_f32p, _i64, _i32, _f32p, _f32p, _u8p],
+            "orc_col_mean": [_f32p, _i64, _i32, _f32p],
+            "orc_sign1_encode": [_f32p, _i64, _i32, _f32p, _i32, _u32p, _f32p],
+            "orc_sign1_decode": [_u32p, _f32p, _i64, _i32, _i32, _f32p, _f32p, _i64],
+            "orc_pca_cov": [_f32p, _i64, _i32, _f64p, _f64p],
+            "orc_pca_cov_entry": [_f32p, _i64, _i32, _f64p, _i32, _i32],
+            "orc_project": [_f32p, _i64, _i32, _f32p, _f32p, _i32, _f32p],
+            "orc_assign_f32": [_f32p, _i64, _i32, _i64, _f32p, _i32, _i32p, _f64p],
+            "orc_assign_sq8": [_u8p, _i64, _i32, _u8p, _i32, _i32p, _i64p],
+            "orc_sign1_prep": [_f32p, _i32, _i32, _f32p, _i32, _i8p, _f32p, _i32p, _i32p, _f32p],
+            "orc_assign_sign1": [_u32p, _f32p, _i64, _i32, _i32, _i8p, _f32p, _i32p, _f32p, _i32, _i32p,
+                                 _f32p, _f64p],
+            "orc_assign_hybrid": [_f32p, _u32p, _f32p, _i64, _i32, _i32, _f32p, _i8p, _f32p, _i32p, _f32p,
+                                  _i32, _i32p, _f64p],
+            "orc_update_f32": [_f32p, _i64, _i32, _i64, _i32p, _i32, _f32p, _i64p, _i32],
+            "orc_update_sq8": [_u8p, _i64, _i32, _i32p, _i32, _u8p, _i64p, _i32],
+            "orc_update_sign1": [ct.c_void_p, _u32p, _f32p, _i64, _i32, _i32, _f32p, _i32p, _i32, _f32p, _i64p,
+                                 _i32],
+            "orc_cost_f32": [_f32p, _i64, _i32, _i64, _f32p, _i32p],
+            "orc_partition_cost": [_f32p, _i64, _i32, _i32p, _i32],
+            "orc_num_threads": [],
+        }
+        for name, args in sig.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = None
+        L.orc_pca_cov_entry.restype = ct.c_double
+        L.orc_cost_f32.restype = ct.c_double
+        L.orc_partition_cost.restype = ct.c_double
+        L.orc_num_threads.restype = ct.c_int
+        _lib = L
+    return _lib
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def num_threads() -> int:
+    return lib().orc_num_threads()
+
+
+# --------------------------------------------------------------------------
+# Preprocessing (Sec. 3.1)
+
+def sq8_fit(X):
+    X = _c(X, np.float32)
+    n, d = X.shape
+    lo = np.empty(d, np.float32)
+    hi = np.empty(d, np.float32)
+    lib().orc_sq8_fit(X, n, d, lo, hi)
+    return lo, hi
+
+
+def sq8_encode(X, lo, hi):
+    X = _c(X, np.float32)
+    n, d = X.shape
+    codes = np.empty((n, d), np.uint8)
+    lib().orc_sq8_encode(X, n, d, _c(lo, np.float32), _c(hi, np.float32), codes)
+    return codes
+
+
+def col_mean(X):
+    X = _c(X, np.float32)
+    n, d = X.shape
+    m = np.empty(d, np.float32)
+    lib().orc_col_mean(X, n, d, m)
+    return m
+
+
+def sign1_encode(X, m, d0: int = 0):
+    """Bits of x - m for all d dims (n x d/32 uint32, LSB first) and alpha over dims [d0, d)."""
+    X = _c(X, np.float32)
+    n, d = X.shape
+    assert d % 32 == 0 and d0 % 32 == 0
+    bits = np.empty((n, d // 32), np.uint32)
+    alpha = np.empty(n, np.float32)
+    lib().orc_sign1_encode(X, n, d, _c(m, np.float32), d0, bits, alpha)
+    return bits, alpha
+
+
+def sign1_decode(bits, alpha, d: int, m, d0: int = 0):
+    """Decoded vectors m + alpha (2b - 1) on dims [d0, d) (fp32, n x d; front dims left 0)."""
+    bits = _c(bits, np.uint32)
+    n = bits.shape[0]
+    out = np.zeros((n, d), np.float32)
+    lib().orc_sign1_decode(bits, _c(alpha, np.float32), n, d, d0, _c(m, np.float32), out, d)
+    return out
+
+
+def pca_cov(X):
+    X = _c(X, np.float32)
+    n, d = X.shape
+    mean = np.empty(d, np.float64)
+    cov = np.empty((d, d), np.float64)
+    lib().orc_pca_cov(X, n, d, mean, cov)
+    return mean, cov
+
+
+def col_mean64(X):
+    """fp64 column mean (for sampled covariance entries)."""
+    return np.asarray(X, dtype=np.float64).mean(axis=0)
+
+
+def pca_cov_entry(X, mean64, i: int, j: int) -> float:
+    X = _c(X, np.float32)
+    n, d = X.shape
+    return lib().orc_pca_cov_entry(X, n, d, _c(mean64, np.float64), i, j)
+
+
+def pca_basis(cov, d_out: int):
+    """Top-d_out eigenvectors of the covariance as columns (d x d_out, fp32), eigenvalues
+    sorted descending; each eigenvector's largest-|.| entry is made positive."""
+    w, V = np.linalg.eigh(np.asarray(cov, dtype=np.float64))
+    order = np.argsort(w)[::-1]
+    w = w[order]
+    V = V[:, order]
+    piv = np.argmax(np.abs(V), axis=0)
+    sgn = np.sign(V[piv, np.arange(V.shape[1])])
+    sgn[sgn == 0] = 1.0
+    V = V * sgn
+    return np.ascontiguousarray(V[:, :d_out], dtype=np.float32), w
+
+
+def project(X, mean, W):
+    X = _c(X, np.float32)
+    W = _c(W, np.float32)
+    n, d = X.shape
+    dout = W.shape[1]
+    Y = np.empty((n, dout), np.float32)
+    lib().orc_project(X, n, d, _c(mean, np.float32), W, dout, Y)
+    return Y
+
+
+# --------------------------------------------------------------------------
+# STEP 2
+
+def assign_f32(X, C):
+    X = _c(X, np.float32)
+    C = _c(C, np.float32)
+    n, d = X.shape
+    a = np.empty(n, np.int32)
+    dist = np.empty(n, np.float64)
+    lib().orc_assign_f32(X, n, d, d, C, C.shape[0], a, dist)
+    return a, dist
+
+
+def assign_sq8(codes, Cc):
+    codes = _c(codes, np.uint8)
+    Cc = _c(Cc, np.uint8)
+    n, d = codes.shape
+    a = np.empty(n, np.int32)
+    dist = np.empty(n, np.int64)
+    lib().orc_assign_sq8(codes, n, d, Cc, Cc.shape[0], a, dist)
+    return a, dist
+
+
+def sign1_prep(C, m, d0: int = 0):
+    """Per-centroid symmetric int8 quantisation of the residual C - m on dims [d0, d)."""
+    C = _c(C, np.float32)
+    k, d = C.shape
+    q = np.empty((k, d - d0), np.int8)
+    sigma = np.empty(k, np.float32)
+    T = np.empty(k, np.int32)
+    Q = np.empty(k, np.int32)
+    u = np.empty(k, np.float32)
+    lib().orc_sign1_prep(C, k, d, _c(m, np.float32), d0, q, sigma, T, Q, u)
+    return q, sigma, T, Q, u
+
+
+def assign_sign1(bits, alpha, C, m, d0: int = 0):
+    bits = _c(bits, np.uint32)
+    C = _c(C, np.float32)
+    n = bits.shape[0]
+    k, d = C.shape
+    q, sigma, T, Q, u = sign1_prep(C, m, d0)
+    a = np.empty(n, np.int32)
+    score = np.empty(n, np.float32)
+    dist = np.empty(n, np.float64)
+    lib().orc_assign_sign1(bits, _c(alpha, np.float32), n, d, d0, q, sigma, T, u, k, a, score, dist)
+    return a, score, dist
+
+
+def assign_hybrid(front, bits, alpha, C, m, d0: int):
+    front = _c(front, np.float32)
+    bits = _c(bits, np.uint32)
+    C = _c(C, np.float32)
+    n = bits.shape[0]
+    k, d = C.shape
+    assert front.shape == (n, d0)
+    q, sigma, T, Q, u = sign1_prep(C, m, d0)
+    a = np.empty(n, np.int32)
+    dist = np.empty(n, np.float64)
+    lib().orc_assign_hybrid(front, bits, _c(alpha, np.float32), n, d, d0, C, q, sigma, T, u, k, a, dist)
+    return a, dist
+
+
+# --------------------------------------------------------------------------
+# STEP 3
+
+def update_f32(X, a, k: int, C_old, policy: int = EMPTY_SPLIT):
+    X = _c(X, np.float32)
+    n, d = X.shape
+    C = np.array(C_old, dtype=np.float32, copy=True, order="C")
+    counts = np.empty(k, np.int64)
+    lib().orc_update_f32(X, n, d, d, _c(a, np.int32), k, C, counts, policy)
+    return C, counts
+
+
+def update_sq8(codes, a, k: int, C_old, policy: int = EMPTY_SPLIT):
+    codes = _c(codes, np.uint8)
+    n, d = codes.shape
+    C = np.array(C_old, dtype=np.uint8, copy=True, order="C")
+    counts = np.empty(k, np.int64)
+    lib().orc_update_sq8(codes, n, d, _c(a, np.int32), k, C, counts, policy)
+    return C, counts
+
+
+def update_sign1(bits, alpha, d: int, m, a, k: int, C_old, policy: int = EMPTY_SPLIT, front=None, d0: int = 0):
+    bits = _c(bits, np.uint32)
+    n = bits.shape[0]
+    C = np.array(C_old, dtype=np.float32, copy=True, order="C")
+    counts = np.empty(k, np.int64)
+    fp = None
+    if d0 > 0:
+        front = _c(front, np.float32)
+        assert front.shape == (n, d0)
+        fp = front.ctypes.data_as(ct.c_void_p)
+    lib().orc_update_sign1(fp, bits, _c(alpha, np.float32), n, d, d0, _c(m, np.float32), _c(a, np.int32), k, C,
+                           counts, policy)
+    return C, counts
+
+
+# --------------------------------------------------------------------------
+# Objective
+
+def cost_f32(X, C, a) -> float:
+    X = _c(X, np.float32)
+    n, d = X.shape
+    return lib().orc_cost_f32(X, n, d, d, _c(C, np.float32), _c(a, np.int32))
+
+
+def partition_cost(X, a, k: int) -> float:
+    """Full-precision cost of a partition: sum ||x - mean of x's cluster||^2 (fp64)."""
+    X = _c(X, np.float32)
+    n, d = X.shape
+    return lib().orc_partition_cost(X, n, d, _c(a, np.int32), k)
+
+
+# --------------------------------------------------------------------------
+# Lloyd driver (Sec. 2.3)
+
+def init_centroids(P: dict, idx):
+    """STEP 1: clustering-space representation of the sampled rows."""
+    idx = np.asarray(idx, dtype=np.int64)
+    fmt = P["fmt"]
+    if fmt == "f32":
+        return np.ascontiguousarray(P["X"][idx], dtype=np.float32)
+    if fmt == "sq8":
+        return np.ascontiguousarray(P["codes"][idx], dtype=np.uint8)
+    if fmt == "sign1":
+        return sign1_decode(P["bits"][idx], P["alpha"][idx], P["d"], P["m"], 0)
+    if fmt == "hybrid":
+        d0 = P["d0"]
+        C = sign1_decode(P["bits"][idx], P["alpha"][idx], P["d"], P["m"], d0)
+        C[:, :d0] = P["front"][idx]
+        return C
+    raise ValueError(fmt)
+
+
+def assign(P: dict, C):
+    """(assignments, per-point in-space distance) for one STEP 2."""
+    fmt = P["fmt"]
+    if fmt == "f32":
+        return assign_f32(P["X"], C)
+    if fmt == "sq8":
+        return assign_sq8(P["codes"], C)
+    if fmt == "sign1":
+        a, _, dist = assign_sign1(P["bits"], P["alpha"], C, P["m"], 0)
+        return a, dist
+    if fmt == "hybrid":
+        return assign_hybrid(P["front"], P["bits"], P["alpha"], C, P["m"], P["d0"])
+    raise ValueError(fmt)
+
+
+def update(P: dict, a, k: int, C, policy: int = EMPTY_SPLIT):
+    fmt = P["fmt"]
+    if fmt == "f32":
+        return update_f32(P["X"], a, k, C, policy)
+    if fmt == "sq8":
+        return update_sq8(P["codes"], a, k, C, policy)
+    if fmt == "sign1":
+        return update_sign1(P["bits"], P["alpha"], P["d"], P["m"], a, k, C, policy)
+    if fmt == "hybrid":
+        return update_sign1(P["bits"], P["alpha"], P["d"], P["m"], a, k, C, policy, front=P["front"], d0=P["d0"])
+    raise ValueError(fmt)
+
+
+def fit(P: dict, k: int, iters: int, init_idx, policy: int = EMPTY_SPLIT, C0=None):
+    """Lloyd: T x (assign, update), then a final assign.  Returns (C, a, J[0..T])."""
+    C = init_centroids(P, init_idx) if C0 is None else np.array(C0, copy=True)
+    J = []
+    for _ in range(iters):
+        a, dist = assign(P, C)
+        J.append(float(np.sum(dist, dtype=np.float64)))
+        C, _ = update(P, a, k, C, policy)
+    a, dist = assign(P, C)
+    J.append(float(np.sum(dist, dtype=np.float64)))
+    return C, a, J

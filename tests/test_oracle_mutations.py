@@ -1,0 +1,76 @@
+"""The pins have teeth: plant plausible mistakes in a private copy of the oracle's
+C source (on the CPU only), rebuild it, and check that at least one pin fails for
+each planted mistake.  The real oracle is never modified.
+"""
+import importlib.util
+import os
+import subprocess
+
+import pytest
+
+import test_oracle_pins as pins
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "kmq_oracle.c")
+
+MUTATIONS = {
+    "sign1_wrong_sign_of_T": ("int32_t s = 2 * D - T;", "int32_t s = 2 * D + T;"),
+    "bit_order_msb_first": ("(row[i >> 5] >> (i & 31))", "(row[i >> 5] >> (31 - (i & 31)))"),
+    "f32_dropped_factor_2": ("double s = cn[j] - 2.0 * dot;", "double s = cn[j] - dot;"),
+    "sq8_mean_floor": ("(2 * S[(int64_t)j * d + i] + cnt[j]) / (2 * cnt[j])", "S[(int64_t)j * d + i] / cnt[j]"),
+    "split_sign_of_p": ("Z[(int64_t)j * d + i] = t * (even ? up : dn);", "Z[(int64_t)j * d + i] = t * (even ? dn : up);"),
+    "sq8_truncating_round": ("float t = rintf((X[r * d + i] - lo[i]) * inv);",
+                             "float t = floorf((X[r * d + i] - lo[i]) * inv);"),
+    "alpha_inverted": ("(float)(s2 / s1)", "(float)(s1 / s2)"),
+    "sign_bit_at_zero": ("if (ri > 0.0f)", "if (ri >= 0.0f)"),
+    "project_transposed_W": ("(double)W[(int64_t)i * dout + o]", "(double)W[(int64_t)o * d + i]"),
+    "ties_to_largest": ("if (j == 0 || s < bs) {\n        bs = s;\n        best = j;\n      }\n    }\n    a[r] = best;\n"
+                        "    if (dist) {\n      double e",
+                        "if (j == 0 || s <= bs) {\n        bs = s;\n        best = j;\n      }\n    }\n    a[r] = best;\n"
+                        "    if (dist) {\n      double e"),
+    "sign1_prep_no_centering": ("float t = fabsf(c[i] - m[i]);", "float t = fabsf(c[i]);"),
+    "update_sign1_drops_minus": ("-(double)alpha[r]", "0.0"),
+}
+
+PINS = [name for name in dir(pins) if name.startswith("test_")]
+
+
+def _load_mutant(tmp_path, name, old, new):
+    src = open(SRC).read()
+    assert src.count(old) >= 1, name
+    mutated = src.replace(old, new)
+    cfile = tmp_path / f"{name}.c"
+    cfile.write_text(mutated)
+    hdr = os.path.join(ROOT, "oracle")
+    so = tmp_path / f"{name}.so"
+    subprocess.check_call(["gcc", "-O1", "-std=c11", "-fopenmp", "-ffp-contract=off", "-fPIC", "-shared",
+                           "-I", hdr, "-o", str(so), str(cfile), "-lm"])
+    spec = importlib.util.spec_from_file_location(f"oracle_mutant_{name}", os.path.join(ROOT, "oracle", "__init__.py"))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    mod._LIB_PATH = str(so)
+    mod._lib = None
+    return mod
+
+
+def _run_pin(fn, mod):
+    import inspect
+    params = inspect.signature(fn).parameters
+    if "fmt" in params:
+        for fmt in ("f32", "sq8"):
+            fn(mod, fmt)
+    else:
+        fn(mod)
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_planted_mistake_is_caught(tmp_path, name):
+    old, new = MUTATIONS[name]
+    mod = _load_mutant(tmp_path, name, old, new)
+    failed = []
+    for pin in PINS:
+        try:
+            _run_pin(getattr(pins, pin), mod)
+        except Exception:  # noqa: BLE001 - any failure of a pin counts as caught
+            failed.append(pin)
+    assert failed, f"no pin caught the planted mistake {name}"

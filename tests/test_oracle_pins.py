@@ -1,0 +1,440 @@
+"""Pins for the CPU oracle: hand-computed examples, closed forms, invariants and
+brute force on tiny inputs.  Each check is independent of the oracle's own code
+path (numpy evaluations of a different formula, or values worked out by hand),
+so a dropped term, a wrong sign or index, or a transposed operand fails one.
+"""
+import numpy as np
+import pytest
+from hypothesis import given, settings, strategies as st
+
+from conftest import load_golden
+
+EPS = 2.0 ** -10
+
+
+# --------------------------------------------------------------------------
+# Hand-computed examples (tests/golden)
+
+def test_lloyd_1d_example(orc):
+    g = load_golden("lloyd_1d.json")
+    X = np.array(g["X"], np.float32)
+    P = {"fmt": "f32", "X": X}
+    a0, dist0 = orc.assign(P, X[g["init_idx"]])
+    assert a0.tolist() == g["assign0"]
+    assert dist0.sum() == g["J0"]
+    C, a, J = orc.fit(P, 2, g["iters"], g["init_idx"], orc.EMPTY_KEEP)
+    np.testing.assert_array_equal(C, np.array(g["C1"], np.float32))
+    assert a.tolist() == g["assign1"]
+    assert J == [g["J0"], g["J1"]]
+
+
+def test_tie_goes_to_smallest_index(orc):
+    g = load_golden("tie_smallest_index.json")
+    a, _ = orc.assign_f32(np.array(g["X"], np.float32), np.array(g["C"], np.float32))
+    assert a.tolist() == g["assign"]
+    a, dist = orc.assign_sq8(np.array(g["sq8_codes"], np.uint8), np.array(g["sq8_C"], np.uint8))
+    assert a.tolist() == g["sq8_assign"] and dist.tolist() == [25]
+    # identical centroids: every point goes to the first copy
+    rng = np.random.default_rng(3)
+    X = rng.standard_normal((50, 8)).astype(np.float32)
+    C = np.repeat(rng.standard_normal((1, 8)).astype(np.float32), 4, axis=0)
+    assert (orc.assign_f32(X, C)[0] == 0).all()
+
+
+def test_sign1_identity_example(orc):
+    g = load_golden("sign1_identity.json")
+    # a 32-dim vector whose first word is the fixture's; remaining bits 0, remaining q 0
+    d = 32
+    bits = np.array([[g["bits_word"]]], np.uint32)
+    q = np.zeros(d, np.int64)
+    q[:4] = g["centroid_residual"]
+    b = np.array([(g["bits_word"] >> i) & 1 for i in range(d)])
+    assert int(q[b == 1].sum()) == g["set_bit_sum"] and int(q.sum()) == g["total_sum"]
+    assert int(np.dot(2 * b - 1, q)) == g["signed_dot"]
+    # The oracle's 1-bit score must equal sigma^2 Q - 2 alpha sigma <2b-1, q>.
+    # Centroid residual with max |.| = 127 gives sigma = 1 and q = residual exactly.
+    m = np.zeros(d, np.float32)
+    C = np.zeros((1, d), np.float32)
+    C[0, :4] = g["centroid_residual"]
+    C[0, 4] = 127.0
+    q[4] = 127
+    alpha = np.array([0.5], np.float32)
+    a, score, _ = orc.assign_sign1(bits, alpha, C, m)
+    expect = float((q * q).sum()) - 2 * 0.5 * 1.0 * float(np.dot(2 * b - 1, q))
+    assert score[0] == np.float32(expect)
+
+
+def test_sign1_encode_example(orc):
+    g = load_golden("sign1_encode.json")
+    d = g["d"]
+    x = np.zeros((1, d), np.float32)
+    x[0, :4] = g["x_head"]
+    bits, alpha = orc.sign1_encode(x, np.zeros(d, np.float32))
+    assert bits[0, 0] == g["bits_word"]
+    assert alpha[0] == np.float32(g["alpha_num"] / g["alpha_den"])
+    dec = orc.sign1_decode(bits, alpha, d, np.zeros(d, np.float32))
+    r = x[0].astype(np.float64)
+    # <xhat - m, r> = ||r||^2 (the quantisation error is orthogonal to r)
+    assert np.dot(dec[0].astype(np.float64), r) == pytest.approx(float(r @ r), rel=1e-6)
+    # radius alpha sqrt(d) >= ||r|| (Cauchy-Schwarz)
+    assert np.linalg.norm(dec[0]) >= np.linalg.norm(r)
+
+
+def test_sq8_codes_example(orc):
+    g = load_golden("sq8_codes.json")
+    X = np.array(g["column"], np.float32)[:, None]
+    lo, hi = orc.sq8_fit(X)
+    assert lo[0] == g["lo"] and hi[0] == g["hi"]
+    assert np.float32(255.0) / (hi[0] - lo[0]) == g["inv"]
+    assert orc.sq8_encode(X, lo, hi)[:, 0].tolist() == g["codes"]
+    Xc = np.array(g["constant_column"], np.float32)[:, None]
+    lo, hi = orc.sq8_fit(Xc)
+    assert orc.sq8_encode(Xc, lo, hi)[:, 0].tolist() == g["constant_codes"]
+
+
+def test_sq8_centroid_rounding_example(orc):
+    g = load_golden("sq8_centroid_round.json")
+    for case in g["cases"]:
+        codes = np.array(case["members"], np.uint8)[:, None]
+        a = np.zeros(len(case["members"]), np.int32)
+        C, cnt = orc.update_sq8(codes, a, 1, np.zeros((1, 1), np.uint8))
+        assert int(C[0, 0]) == case["centroid"], case
+        assert cnt.tolist() == [len(case["members"])]
+
+
+def test_empty_split_example(orc):
+    g = load_golden("empty_split.json")
+    X = np.array(g["X"], np.float32)
+    C, cnt = orc.update_f32(X, np.array(g["assign"], np.int32), g["k"], np.array(g["C_old"], np.float32))
+    np.testing.assert_array_equal(C, np.array(g["C_new"], np.float32))
+    assert cnt.tolist() == g["counts"]
+    # KEEP leaves the empty centroid untouched
+    C, _ = orc.update_f32(X, np.array(g["assign"], np.int32), g["k"], np.array(g["C_old"], np.float32),
+                          orc.EMPTY_KEEP)
+    np.testing.assert_array_equal(C[2], np.array(g["C_old"][2], np.float32))
+
+
+def test_empty_split_donor_sequence(orc):
+    # two empties: the first takes half of cluster 0 (count 8 -> 4/4), the second then
+    # sees counts (4, 3, 4, 0): largest is 4, smallest index 0 again.
+    X = np.arange(11 * 2, dtype=np.float32).reshape(11, 2)
+    a = np.array([0] * 8 + [1] * 3, np.int32)
+    C, cnt = orc.update_f32(X, a, 4, np.zeros((4, 2), np.float32))
+    mean0 = X[:8].mean(0)
+    up, dn = np.float32(1 + EPS), np.float32(1 - EPS)
+    p_up = np.array([up, dn], np.float32)
+    p_dn = np.array([dn, up], np.float32)
+    c0 = mean0.astype(np.float32)
+    c2 = c0 * p_up
+    c0 = c0 * p_dn
+    c3 = c0 * p_up
+    c0 = c0 * p_dn
+    np.testing.assert_array_equal(C[2], c2)
+    np.testing.assert_array_equal(C[3], c3)
+    np.testing.assert_array_equal(C[0], c0)
+    assert cnt.tolist() == [8, 3, 0, 0]
+
+
+def test_empty_split_sq8_steps(orc):
+    codes = np.array([[0, 255, 10], [0, 255, 10]], np.uint8)
+    a = np.zeros(2, np.int32)
+    C, _ = orc.update_sq8(codes, a, 2, np.full((2, 3), 77, np.uint8))
+    # p = (+1, -1, +1): new = clamp(c + p), donor = clamp(c - p)
+    assert C[1].tolist() == [1, 254, 11]
+    assert C[0].tolist() == [0, 255, 9]
+
+
+# --------------------------------------------------------------------------
+# Closed forms and invariants
+
+def _blobs(n=600, d=16, comps=6, seed=0, sigma=0.2):
+    rng = np.random.default_rng(seed)
+    mu = rng.standard_normal((comps, d)) * 2
+    lab = rng.integers(0, comps, n)
+    return (mu[lab] + sigma * rng.standard_normal((n, d))).astype(np.float32)
+
+
+def test_centroid_is_member_mean(orc):
+    X = _blobs()
+    rng = np.random.default_rng(1)
+    k = 7
+    a = rng.integers(0, k, len(X)).astype(np.int32)
+    C, cnt = orc.update_f32(X, a, k, np.zeros((k, X.shape[1]), np.float32))
+    onehot = np.zeros((len(X), k))
+    onehot[np.arange(len(X)), a] = 1
+    expect = (onehot.T @ X.astype(np.float64)) / onehot.sum(0)[:, None]
+    np.testing.assert_allclose(C, expect, rtol=1e-6, atol=1e-7)
+    assert cnt.tolist() == np.bincount(a, minlength=k).tolist()
+
+
+@pytest.mark.parametrize("fmt", ["f32", "sq8"])
+def test_lloyd_monotone(orc, fmt):
+    X = _blobs(n=800, d=32, comps=10)
+    if fmt == "f32":
+        P = {"fmt": "f32", "X": X}
+    else:
+        lo, hi = orc.sq8_fit(X)
+        P = {"fmt": "sq8", "codes": orc.sq8_encode(X, lo, hi)}
+    idx = np.random.default_rng(5).choice(len(X), 12, replace=False)
+    _, _, J = orc.fit(P, 12, 8, idx, orc.EMPTY_KEEP)
+    for j0, j1 in zip(J, J[1:]):
+        if fmt == "sq8":
+            assert j1 <= j0  # exact integers: rounding the mean to the nearest code keeps descent
+        else:
+            assert j1 <= j0 * (1 + 1e-9)
+    assert J[-1] < J[0]
+
+
+def test_sign1_lloyd_roughly_monotone(orc):
+    X = _blobs(n=800, d=64, comps=8, sigma=0.5)
+    m = orc.col_mean(X)
+    bits, alpha = orc.sign1_encode(X, m)
+    P = {"fmt": "sign1", "bits": bits, "alpha": alpha, "m": m, "d": 64}
+    idx = np.random.default_rng(2).choice(len(X), 8, replace=False)
+    _, _, J = orc.fit(P, 8, 6, idx, orc.EMPTY_KEEP)
+    # int8 centroid rounding makes this approximate; it must not drift upward materially
+    assert J[-1] <= J[0]
+    for j0, j1 in zip(J, J[1:]):
+        assert j1 <= j0 * 1.01
+
+
+def test_k1_is_global_mean_and_kn_is_zero(orc):
+    X = _blobs(n=40, d=8)
+    P = {"fmt": "f32", "X": X}
+    C, a, J = orc.fit(P, 1, 3, [7])
+    np.testing.assert_allclose(C[0], X.astype(np.float64).mean(0), rtol=1e-6, atol=1e-7)
+    C, a, J = orc.fit(P, len(X), 2, np.arange(len(X)))
+    assert J[-1] == 0.0 and a.tolist() == list(range(len(X)))
+
+
+def test_alpha_matches_rabitq_factor(orc):
+    # alpha = (1/sqrt d) ||r|| / <x_bar, x> with x_bar = sign(r)/sqrt d, x = r/||r||
+    rng = np.random.default_rng(4)
+    d = 96
+    X = rng.standard_normal((50, d)).astype(np.float32)
+    m = orc.col_mean(X)
+    bits, alpha = orc.sign1_encode(X, m)
+    r = X.astype(np.float64) - m.astype(np.float64)
+    xbar = np.where(r > 0, 1.0, -1.0) / np.sqrt(d)
+    cosine = np.einsum("ij,ij->i", xbar, r / np.linalg.norm(r, axis=1, keepdims=True))
+    np.testing.assert_allclose(alpha, np.linalg.norm(r, axis=1) / cosine / np.sqrt(d), rtol=2e-6)
+    # bits: bit i of row in word i//32 at position i%32
+    b = (bits[:, :, None] >> np.arange(32, dtype=np.uint32)) & 1
+    np.testing.assert_array_equal(b.reshape(len(X), d).astype(bool), (X - m) > 0)
+    # decoded residual: orthogonal error and radius >= ||r||
+    dec = orc.sign1_decode(bits, alpha, d, m).astype(np.float64) - m
+    np.testing.assert_allclose(np.einsum("ij,ij->i", dec, r), np.einsum("ij,ij->i", r, r), rtol=1e-5)
+    assert (np.linalg.norm(dec, axis=1) >= np.linalg.norm(r, axis=1) * (1 - 1e-6)).all()
+
+
+def test_sign1_alpha_zero_at_mean(orc):
+    m = np.linspace(-1, 1, 32).astype(np.float32)
+    X = np.tile(m, (3, 1))
+    bits, alpha = orc.sign1_encode(X, m)
+    assert (alpha == 0).all() and (bits == 0).all()
+
+
+def test_sign1_tail_alpha(orc):
+    rng = np.random.default_rng(9)
+    X = rng.standard_normal((20, 64)).astype(np.float32)
+    m = orc.col_mean(X)
+    bits_full, _ = orc.sign1_encode(X, m, 0)
+    bits, alpha = orc.sign1_encode(X, m, 32)
+    np.testing.assert_array_equal(bits, bits_full)
+    r = (X - m).astype(np.float64)[:, 32:]
+    np.testing.assert_allclose(alpha, (r * r).sum(1) / np.abs(r).sum(1), rtol=1e-6)
+
+
+def test_sq8_codes_match_definition(orc):
+    rng = np.random.default_rng(11)
+    X = rng.standard_normal((300, 24)).astype(np.float32) * rng.uniform(0.1, 3, 24).astype(np.float32)
+    lo, hi = orc.sq8_fit(X)
+    np.testing.assert_array_equal(lo, X.min(0))
+    np.testing.assert_array_equal(hi, X.max(0))
+    codes = orc.sq8_encode(X, lo, hi)
+    s = (hi.astype(np.float64) - lo) / 255.0
+    approx = np.clip(np.round((X - lo) / s), 0, 255)
+    # fp32 (x-lo)*inv vs fp64 (x-lo)/s may differ only at exact .5 boundaries: at most one code
+    assert np.abs(codes.astype(int) - approx).max() <= 1
+    assert (codes.astype(int) == approx).mean() > 0.999
+    assert codes.min(0).tolist() == [0] * 24 and codes.max(0).tolist() == [255] * 24
+    # reconstruction error within half a step
+    rec = codes * s + lo
+    assert (np.abs(rec - X) <= s * 0.5 + 1e-6).all()
+
+
+def test_pca_cov_and_basis(orc):
+    rng = np.random.default_rng(12)
+    d = 24
+    lam = np.arange(1, d + 1) ** -0.5
+    X = (rng.standard_normal((500, d)) * np.sqrt(lam) + 3.0).astype(np.float32)
+    mean, cov = orc.pca_cov(X)
+    np.testing.assert_allclose(mean, X.astype(np.float64).mean(0), rtol=1e-12)
+    np.testing.assert_allclose(cov, np.cov(X.astype(np.float64).T, bias=True), rtol=1e-10, atol=1e-12)
+    assert orc.pca_cov_entry(X, mean, 3, 5) == pytest.approx(cov[3, 5], rel=1e-12)
+    W, w = orc.pca_basis(cov, d)
+    np.testing.assert_allclose(W.T.astype(np.float64) @ W, np.eye(d), atol=1e-5)
+    assert (w >= -1e-12).all() and (np.diff(w) <= 0).all()
+    # each column: A w = lambda w and largest-|.| entry positive
+    for c in range(d):
+        np.testing.assert_allclose(cov @ W[:, c], w[c] * W[:, c], atol=1e-5)
+        assert W[np.argmax(np.abs(W[:, c])), c] > 0
+    Y = orc.project(X, mean.astype(np.float32), W[:, :5])
+    np.testing.assert_allclose(Y, (X.astype(np.float64) - mean.astype(np.float32)) @ W[:, :5].astype(np.float64),
+                               rtol=1e-5, atol=1e-6)
+    # variance captured by the first components is the eigenvalue sum
+    assert Y.astype(np.float64).var(0).sum() == pytest.approx(w[:5].sum(), rel=1e-4)
+
+
+def test_full_rank_pca_keeps_partition(orc):
+    # rotation + translation preserve every distance, so Lloyd partitions agree
+    X = _blobs(n=500, d=12, comps=5, sigma=0.3)
+    mean, cov = orc.pca_cov(X)
+    W, _ = orc.pca_basis(cov, 12)
+    Y = orc.project(X, mean.astype(np.float32), W)
+    idx = np.random.default_rng(7).choice(500, 5, replace=False)
+    _, a1, J1 = orc.fit({"fmt": "f32", "X": X}, 5, 6, idx)
+    _, a2, J2 = orc.fit({"fmt": "f32", "X": Y}, 5, 6, idx)
+    np.testing.assert_array_equal(a1, a2)
+    np.testing.assert_allclose(J1, J2, rtol=1e-5)
+
+
+def test_partition_cost(orc):
+    X = _blobs(n=100, d=6)
+    a = (np.arange(100) % 4).astype(np.int32)
+    mu = np.stack([X[a == j].astype(np.float64).mean(0) for j in range(4)])
+    expect = sum(((X[a == j] - mu[j]) ** 2).sum() for j in range(4))
+    assert orc.partition_cost(X, a, 4) == pytest.approx(expect, rel=1e-10)
+    C = mu.astype(np.float32)
+    assert orc.cost_f32(X, C, a) == pytest.approx(
+        float(((X.astype(np.float64) - C.astype(np.float64)[a]) ** 2).sum()), rel=1e-12)
+
+
+def test_hybrid_segment_decomposition(orc):
+    # front part exact L2, tail the 1-bit decoded distance: dist = ||x'-c'||^2 + tail
+    rng = np.random.default_rng(13)
+    n, d, d0, k = 60, 96, 32, 5
+    X = rng.standard_normal((n, d)).astype(np.float32)
+    m = orc.col_mean(X)
+    bits, alpha = orc.sign1_encode(X, m, d0)
+    front = np.ascontiguousarray(X[:, :d0])
+    C = rng.standard_normal((k, d)).astype(np.float32) * 0.5
+    a, dist = orc.assign_hybrid(front, bits, alpha, C, m, d0)
+    q, sigma, T, Q, u = orc.sign1_prep(C, m, d0)
+    sgn = np.where(((bits[:, :, None] >> np.arange(32, dtype=np.uint32)) & 1).reshape(n, d), 1.0, -1.0)[:, d0:]
+    xt = alpha[:, None].astype(np.float64) * sgn
+    ct = sigma[:, None].astype(np.float64) * q
+    full = ((front[:, None, :].astype(np.float64) - C[None, :, :d0]) ** 2).sum(-1) + \
+        ((xt[:, None, :] - ct[None]) ** 2).sum(-1)
+    np.testing.assert_array_equal(a, full.argmin(1))
+    np.testing.assert_allclose(dist, full.min(1), rtol=1e-9)
+
+
+def test_sign1_prep_definition(orc):
+    rng = np.random.default_rng(14)
+    k, d = 6, 64
+    C = rng.standard_normal((k, d)).astype(np.float32)
+    m = rng.standard_normal(d).astype(np.float32) * 0.1
+    C[3] = m  # a centroid at the mean: sigma 1, q 0
+    q, sigma, T, Q, u = orc.sign1_prep(C, m, 0)
+    res = C - m
+    for j in range(k):
+        mx = np.abs(res[j]).max()
+        if mx == 0:
+            assert sigma[j] == 1 and (q[j] == 0).all()
+            continue
+        assert sigma[j] == np.float32(mx) / np.float32(127)
+        assert np.abs(q[j]).max() == 127
+        np.testing.assert_allclose(q[j] * np.float64(sigma[j]), res[j], atol=float(sigma[j]) * 0.5 + 1e-7)
+    assert T.tolist() == q.sum(1).tolist() and Q.tolist() == (q.astype(int) ** 2).sum(1).tolist()
+    assert u.tolist() == [np.float32(np.float32(s * s) * np.float32(qq)) for s, qq in zip(sigma, Q)]
+
+
+# --------------------------------------------------------------------------
+# Brute force on tiny inputs (hypothesis)
+
+@settings(max_examples=40, deadline=None)
+@given(n=st.integers(1, 64), d=st.integers(1, 64), k=st.integers(1, 8), seed=st.integers(0, 2**31 - 1))
+def test_assign_f32_bruteforce(orc, n, d, k, seed):
+    rng = np.random.default_rng(seed)
+    X = rng.standard_normal((n, d)).astype(np.float32)
+    C = rng.standard_normal((k, d)).astype(np.float32)
+    a, dist = orc.assign_f32(X, C)
+    D = ((X[:, None, :].astype(np.float64) - C[None].astype(np.float64)) ** 2).sum(-1)
+    np.testing.assert_array_equal(a, D.argmin(1))
+    np.testing.assert_allclose(dist, D.min(1), rtol=1e-12, atol=1e-12)
+
+
+@settings(max_examples=40, deadline=None)
+@given(n=st.integers(1, 64), d=st.integers(1, 64), k=st.integers(1, 8), seed=st.integers(0, 2**31 - 1))
+def test_assign_sq8_bruteforce(orc, n, d, k, seed):
+    rng = np.random.default_rng(seed)
+    X = rng.integers(0, 256, (n, d)).astype(np.uint8)
+    C = rng.integers(0, 256, (k, d)).astype(np.uint8)
+    if k > 1 and seed % 3 == 0:
+        C[-1] = C[0]  # exact ties must resolve to the smallest index
+    a, dist = orc.assign_sq8(X, C)
+    D = ((X[:, None, :].astype(np.int64) - C[None].astype(np.int64)) ** 2).sum(-1)
+    np.testing.assert_array_equal(a, D.argmin(1))
+    np.testing.assert_array_equal(dist, D.min(1))
+
+
+@settings(max_examples=40, deadline=None)
+@given(n=st.integers(1, 64), w=st.integers(1, 2), k=st.integers(1, 8), seed=st.integers(0, 2**31 - 1))
+def test_assign_sign1_bruteforce(orc, n, w, k, seed):
+    d = 32 * w
+    rng = np.random.default_rng(seed)
+    X = rng.standard_normal((n, d)).astype(np.float32)
+    m = orc.col_mean(X)
+    bits, alpha = orc.sign1_encode(X, m)
+    C = (m + rng.standard_normal((k, d)) * 0.3).astype(np.float32)
+    a, score, dist = orc.assign_sign1(bits, alpha, C, m)
+    q, sigma, T, Q, u = orc.sign1_prep(C, m)
+    sgn = np.where(((bits[:, :, None] >> np.arange(32, dtype=np.uint32)) & 1).reshape(n, d), 1.0, -1.0)
+    xhat = alpha[:, None].astype(np.float64) * sgn      # decoded residual of the point
+    chat = sigma[:, None].astype(np.float64) * q         # decoded residual of the centroid
+    D = ((xhat[:, None, :] - chat[None]) ** 2).sum(-1)
+    # the fp32 score is the decoded distance minus the point-only term alpha^2 d
+    S = D - (alpha.astype(np.float64) ** 2 * d)[:, None]
+    best = S.min(1)
+    np.testing.assert_allclose(score, best, rtol=1e-5, atol=1e-5 * (1 + np.abs(S).max()))
+    # the oracle's choice is optimal up to fp32 rounding of the score
+    chosen = S[np.arange(n), a]
+    assert (chosen <= best + 1e-5 * (1 + np.abs(S).max(1))).all()
+    np.testing.assert_allclose(dist, D[np.arange(n), a], rtol=1e-12)
+
+
+@settings(max_examples=25, deadline=None)
+@given(n=st.integers(1, 40), d=st.integers(1, 16), k=st.integers(1, 6), seed=st.integers(0, 2**31 - 1))
+def test_update_f32_bruteforce(orc, n, d, k, seed):
+    rng = np.random.default_rng(seed)
+    X = rng.standard_normal((n, d)).astype(np.float32)
+    a = rng.integers(0, k, n).astype(np.int32)
+    C0 = rng.standard_normal((k, d)).astype(np.float32)
+    C, cnt = orc.update_f32(X, a, k, C0, orc.EMPTY_KEEP)
+    for j in range(k):
+        if (a == j).any():
+            np.testing.assert_allclose(C[j], X[a == j].astype(np.float64).mean(0), rtol=1e-6, atol=1e-7)
+        else:
+            np.testing.assert_array_equal(C[j], C0[j])
+    assert cnt.tolist() == np.bincount(a, minlength=k).tolist()
+
+
+@settings(max_examples=25, deadline=None)
+@given(n=st.integers(1, 40), w=st.integers(1, 2), k=st.integers(1, 6), seed=st.integers(0, 2**31 - 1))
+def test_update_sign1_bruteforce(orc, n, w, k, seed):
+    d = 32 * w
+    rng = np.random.default_rng(seed)
+    X = rng.standard_normal((n, d)).astype(np.float32)
+    m = orc.col_mean(X)
+    bits, alpha = orc.sign1_encode(X, m)
+    a = rng.integers(0, k, n).astype(np.int32)
+    C0 = rng.standard_normal((k, d)).astype(np.float32)
+    C, cnt = orc.update_sign1(bits, alpha, d, m, a, k, C0, orc.EMPTY_KEEP)
+    dec = orc.sign1_decode(bits, alpha, d, m).astype(np.float64)  # m + alpha(2b-1)
+    for j in range(k):
+        if (a == j).any():
+            # fused decode-average == average of decoded points (m is common)
+            np.testing.assert_allclose(C[j], dec[a == j].mean(0), rtol=1e-5, atol=1e-6)
+        else:
+            np.testing.assert_array_equal(C[j], C0[j])
