@@ -1,0 +1,194 @@
+/*
+ * kmq.h -- C ABI of the MI355X (gfx950) library for Lloyd k-means on vectors
+ * compressed before clustering ("approximate first, then cluster", Sec. 3).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Buffers are caller-owned DEVICE pointers (memory of the current HIP
+ *   device) unless a parameter says "host".  The library never frees or keeps
+ *   a caller pointer after the call returns.
+ * - Every call is asynchronous on `stream` (a hipStream_t; NULL = the legacy
+ *   default stream): results are valid once the stream has synchronised.
+ * - All argument checks run on the host before any allocation or launch, so a
+ *   non-OK status means nothing was written.  Assignment values read from
+ *   device memory are range-checked inside the kernels: an index outside
+ *   [0, k) makes that point belong to no cluster (it is skipped).
+ * - Internal scratch memory is taken from the device's stream-ordered pool
+ *   (hipMallocAsync on `stream`) and given back on the same stream before the
+ *   call returns; km_release() trims the pool.  Calls on different streams
+ *   do not share scratch.
+ * - No exception crosses the ABI.  km_last_error() gives a thread-local
+ *   message for the last non-OK status of the calling thread.
+ * - Layouts are row-major.  1-bit codes: bit i of a vector sits in 32-bit
+ *   word i/32 at bit position i%32 (least significant first); a row holds
+ *   d/32 words.
+ */
+#ifndef KMQ_H
+#define KMQ_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+struct ihipStream_t;                     /* = hipStream_t */
+typedef struct ihipStream_t *km_stream;  /* hipStream_t */
+
+typedef enum {
+  KM_OK = 0,
+  KM_EINVAL = -1,       /* bad argument (null pointer, bad size, bad alignment, ...) */
+  KM_EUNSUPPORTED = -2, /* format not valid for this call */
+  KM_ENOMEM = -3,       /* scratch allocation failed */
+  KM_EDEVICE = -4       /* a HIP runtime error (message from hipGetErrorString) */
+} km_status;
+
+typedef enum {
+  KM_F32 = 0,    /* fp32 vectors (raw, PCA-projected or a dimension prefix) */
+  KM_SQ8 = 2,    /* uint8 scalar-quantised codes, one (lo, hi) pair per dimension */
+  KM_SIGN1 = 3,  /* 1-bit sign codes of x - m plus one fp32 scale alpha per vector */
+  KM_HYBRID = 4  /* fp32 front dims [0, d_front) + 1-bit codes on the tail [d_front, d) */
+} km_format;
+
+typedef enum {
+  KM_EMPTY_SPLIT = 0, /* an empty cluster takes half of the largest cluster */
+  KM_EMPTY_KEEP = 1   /* an empty cluster keeps its previous centroid */
+} km_empty_policy;
+
+/* quantize() flags */
+#define KM_Q_FIT_PARAMS 1 /* compute the parameters from X; otherwise use those passed in */
+
+/*
+ * The points being clustered, in their compressed form.
+ *   KM_F32:    data = float[n][ld], d <= ld, ld % 4 == 0, data 16-byte aligned, d % 4 == 0.
+ *   KM_SQ8:    data = uint8[n][ld] codes, ld % 16 == 0, d % 16 == 0, 16-byte aligned.
+ *   KM_SIGN1:  data = uint32[n][d/32] bits, d % 32 == 0; alpha = float[n];
+ *              center = m, float[d] (the mean the codes were taken around).
+ *   KM_HYBRID: data = uint32[n][d/32] bits of the FULL d dims (only words
+ *              d_front/32 .. d/32-1 are read); alpha = float[n] computed over the
+ *              tail dims; center = float[d]; front = float[n][d_front];
+ *              d_front % 32 == 0, 0 < d_front < d.
+ * `ld` is ignored for the 1-bit formats.
+ */
+typedef struct km_points {
+  int32_t fmt;          /* km_format */
+  int32_t d;            /* logical dimensionality */
+  int64_t n;            /* number of points, 1 <= n < 2^31 */
+  const void *data;
+  int64_t ld;           /* row stride in elements (F32: floats, SQ8: bytes) */
+  const float *alpha;
+  const float *center;
+  const float *front;
+  int32_t d_front;
+  int32_t reserved;     /* must be 0 */
+} km_points;
+
+/*
+ * quantize -- compress fp32 points before clustering (Sec. 3.1).
+ *   X: float[n][ldx] (ldx % 4 == 0, 16-byte aligned).
+ *   fmt == KM_SQ8 (Sec. 3.1 "SQ8"): per-dimension bias lo_i and scale
+ *     (hi_i - lo_i)/255; codes = uint8[n][d] with
+ *     code = clip(rint((x - lo) * (255 / (hi - lo))), 0, 255) in fp32 (0 where hi == lo);
+ *     params = float[2*d]: lo[0..d) then hi[0..d).  d % 16 == 0.
+ *   fmt == KM_SIGN1 (Sec. 3.1 "RabitQ", without the random rotation):
+ *     params = m, float[d] (column mean, fp64 sums); codes = uint32[n][d/32] with
+ *     bit i = [x_i - m_i > 0]; alpha = float[n], alpha = sum r_i^2 / sum |r_i| over
+ *     dims [d_front, d) with r = x - m (fp64 sums; 0 when x == m on those dims).
+ *     alpha equals (1/sqrt(d')) ||r|| / <x_bar, x> of Eq. 4, the decoding radius.
+ *     If d_front > 0 and front != NULL, front = float[n][d_front] receives a copy
+ *     of the first d_front dims (the hybrid layout).  d % 32 == 0, d_front % 32 == 0.
+ *   flags & KM_Q_FIT_PARAMS: compute params from X first (one extra pass over X);
+ *     otherwise params are inputs.
+ */
+km_status quantize(const float *X, int64_t n, int32_t d, int64_t ldx, int32_t fmt, void *codes,
+                   float *params, float *alpha, int32_t d_front, float *front, int32_t flags,
+                   km_stream stream);
+
+/*
+ * pca_fit_cov -- PCA statistics (Sec. 3.1 PCA; Sec. 4.2): mean = float[d] column
+ * mean, cov = float[d][d] = (1/n) sum (x - mean)(x - mean)^T (symmetric, both
+ * halves written).  X: float[n][d], d % 4 == 0.  The eigendecomposition of cov
+ * (d x d, small) is done by the caller on the host.
+ */
+km_status pca_fit_cov(const float *X, int64_t n, int32_t d, float *mean, float *cov, km_stream stream);
+
+/*
+ * pca_project -- Y = (X - mean) W: X float[n][d], mean float[d], W float[d][d_out]
+ * (columns = principal directions), Y float[n][d_out].  d % 4 == 0, d_out % 4 == 0.
+ */
+km_status pca_project(const float *X, int64_t n, int32_t d, const float *mean, const float *W,
+                      int32_t d_out, float *Y, km_stream stream);
+
+/*
+ * kmeans_assign -- STEP 2 (Sec. 2.3): for every point, the index of the nearest
+ * centroid (ties to the smallest index), without materialising the n x k
+ * distance matrix.
+ *   C: centroids in the clustering space, k x d, row-major:
+ *      KM_F32: float; KM_SQ8: uint8 codes; KM_SIGN1 / KM_HYBRID: float in the
+ *      original space (the 1-bit part is compared against int8 residual codes
+ *      q = rint((c - m)/sigma), sigma = max|c - m|/127, rebuilt on each call).
+ *   assign: int32[n].  score (nullable): float[n], the winning score, i.e. the
+ *      in-space squared distance minus the point-only term:
+ *      F32: ||c||^2 - 2<x,c>;  SQ8: ||c~||^2 - 2<x~,c~> with x~ = code - 128;
+ *      SIGN1: fmaf(-alpha*2*sigma, <2b-1, q>, sigma^2 ||q||^2);
+ *      HYBRID: front F32 score + tail SIGN1 score.
+ *   objective (nullable): double[1], receives sum over points of the in-space
+ *      distance (score plus the point-only term), fp64.
+ *   1 <= k.
+ */
+km_status kmeans_assign(const km_points *P, const void *C, int32_t k, int32_t *assign, float *score,
+                        double *objective, km_stream stream);
+
+/*
+ * kmeans_update -- STEP 3 (Sec. 2.3): each centroid becomes the mean of its
+ * members, in the clustering space:
+ *   KM_F32: fp32 mean; KM_SQ8: floor((2 S + n_j) / (2 n_j)) with S the exact code sum
+ *   (averaging in the quantised domain, Sec. 3.1); KM_SIGN1: m + (1/n_j) sum alpha (2b - 1)
+ *   (fused decode-averaging, Sec. 3.1); KM_HYBRID: front mean and tail decode-average.
+ *   C: in = previous centroids, out = new ones (same type as kmeans_assign).
+ *   counts (nullable): int64[k] member counts of `assign`.
+ *   policy KM_EMPTY_SPLIT: empty clusters, in ascending order, take a split of the
+ *   cluster with the largest current count (ties to the smallest index) when that
+ *   count is >= 2: c_j = c_b (1 + eps p), c_b = c_b (1 - eps p), p_i = (-1)^i,
+ *   eps = 2^-10, on the clustering-space vector (1-bit dims: the residual c - m;
+ *   SQ8: c_j = clip(c_b + p), c_b = clip(c_b - p)); the donor's count is halved
+ *   for later choices.  KM_EMPTY_KEEP leaves empty clusters unchanged.
+ *   Deterministic: the result does not depend on scheduling.
+ */
+km_status kmeans_update(const km_points *P, const int32_t *assign, int32_t k, void *C, int64_t *counts,
+                        int32_t policy, km_stream stream);
+
+/*
+ * kmeans_fit -- Lloyd's algorithm (Sec. 2.3): STEP 1 (C = the points at
+ * init_idx), then `iters` x (STEP 2, STEP 3), then a final STEP 2.
+ *   init_idx: HOST int64[k], distinct, in [0, n); NULL = C already holds the
+ *     initial centroids (resume from saved centroids).
+ *   C: out (and in when init_idx is NULL), as in kmeans_assign.
+ *   assign: int32[n], the final assignment.
+ *   objective (nullable): DEVICE double[iters + 1]; entry t is the in-space
+ *     objective of the t-th assignment pass (sum of in-space distances to the
+ *     centroids that pass used).
+ *   Nothing is synchronised: the call only enqueues work on `stream`.
+ */
+km_status kmeans_fit(const km_points *P, int32_t k, int32_t iters, const int64_t *init_idx, void *C,
+                     int32_t *assign, double *objective, int32_t policy, km_stream stream);
+
+/*
+ * kmeans_cost -- sum over points of ||x - c_{assign(x)}||^2 in fp64 for fp32
+ * points (the full-precision partition cost when C holds the member means of the
+ * raw vectors, Sec. 4.2 "recompute").  X float[n][ldx], C float[k][d],
+ * out: DEVICE double[1].  Points with an assignment outside [0, k) are skipped.
+ */
+km_status kmeans_cost(const float *X, int64_t n, int32_t d, int64_t ldx, const float *C, int32_t k,
+                      const int32_t *assign, double *out, km_stream stream);
+
+/* Thread-local message for the last non-OK status ("" if none). */
+const char *km_last_error(void);
+
+/* Return pooled scratch memory of the current device to the system. */
+km_status km_release(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* KMQ_H */

@@ -1,0 +1,278 @@
+"""ctypes binding of libkmq (include/kmq.h): argument marshalling only.
+
+Every call takes torch tensors on the current HIP device, checks dtype, device
+and contiguity, and passes raw device pointers plus the current stream to the
+C ABI.  All arithmetic runs in the library's HIP kernels; there is no fallback:
+a missing library or a non-OK status raises.
+"""
+from __future__ import annotations
+
+import ctypes as ct
+import os
+
+import numpy as np
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libkmq.so")
+
+KM_F32, KM_SQ8, KM_SIGN1, KM_HYBRID = 0, 2, 3, 4
+KM_EMPTY_SPLIT, KM_EMPTY_KEEP = 0, 1
+KM_Q_FIT_PARAMS = 1
+STATUS = {0: "KM_OK", -1: "KM_EINVAL", -2: "KM_EUNSUPPORTED", -3: "KM_ENOMEM", -4: "KM_EDEVICE"}
+EXPORTS = ("quantize", "pca_fit_cov", "pca_project", "kmeans_assign", "kmeans_update", "kmeans_fit",
+           "kmeans_cost", "km_last_error", "km_release")
+
+
+class KmqError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class KmPoints(ct.Structure):
+    _fields_ = [("fmt", ct.c_int32), ("d", ct.c_int32), ("n", ct.c_int64), ("data", ct.c_void_p),
+                ("ld", ct.c_int64), ("alpha", ct.c_void_p), ("center", ct.c_void_p), ("front", ct.c_void_p),
+                ("d_front", ct.c_int32), ("reserved", ct.c_int32)]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libkmq.so; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"libkmq.so not found at {LIB_PATH}: build it with "
+                               "`python -m paper_2608_14648_amd.build` (hipcc, gfx950)")
+        L = ct.CDLL(LIB_PATH)
+        vp, i32, i64 = ct.c_void_p, ct.c_int32, ct.c_int64
+        sig = {
+            "quantize": [vp, i64, i32, i64, i32, vp, vp, vp, i32, vp, i32, vp],
+            "pca_fit_cov": [vp, i64, i32, vp, vp, vp],
+            "pca_project": [vp, i64, i32, vp, vp, i32, vp, vp],
+            "kmeans_assign": [ct.POINTER(KmPoints), vp, i32, vp, vp, vp, vp],
+            "kmeans_update": [ct.POINTER(KmPoints), vp, i32, vp, vp, i32, vp],
+            "kmeans_fit": [ct.POINTER(KmPoints), i32, i32, vp, vp, vp, vp, i32, vp],
+            "kmeans_cost": [vp, i64, i32, i64, vp, i32, vp, vp, vp],
+            "km_release": [],
+        }
+        for name, args in sig.items():
+            f = getattr(L, name)
+            f.argtypes = args
+            f.restype = ct.c_int
+        L.km_last_error.argtypes = []
+        L.km_last_error.restype = ct.c_char_p
+        _lib = L
+    return _lib
+
+
+def _check(status: int):
+    if status != 0:
+        raise KmqError(status, lib().km_last_error().decode(errors="replace"))
+
+
+def _stream():
+    return ct.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _ptr(t):
+    return None if t is None else ct.c_void_p(t.data_ptr())
+
+
+def _dev(t: torch.Tensor, dtype, name: str, ndim=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on the GPU (got {t.device})")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype} (got {t.dtype})")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+class Points:
+    """Compressed points handed to the clustering calls (mirrors ``km_points``)."""
+
+    def __init__(self, fmt: int, data: torch.Tensor, d: int, alpha=None, center=None, front=None, d_front: int = 0):
+        self.fmt, self.data, self.d = fmt, data, d
+        self.alpha, self.center, self.front, self.d_front = alpha, center, front, d_front
+        self.n = data.shape[0]
+        ld = data.stride(0) if fmt in (KM_F32, KM_SQ8) else d // 32
+        self._c = KmPoints(fmt, d, self.n, data.data_ptr(), ld, _ptr(alpha) or None, _ptr(center) or None,
+                           _ptr(front) or None, d_front, 0)
+
+    @property
+    def ref(self):
+        return ct.byref(self._c)
+
+    @property
+    def device(self):
+        return self.data.device
+
+    def centroid_dtype(self):
+        return torch.uint8 if self.fmt == KM_SQ8 else torch.float32
+
+
+def _rows(t: torch.Tensor, dtype, name: str):
+    """A 2-D tensor whose rows are contiguous (row stride may exceed the row length)."""
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda" or t.dtype != dtype or t.dim() != 2:
+        raise ValueError(f"{name} must be a 2-D {dtype} tensor on the GPU")
+    if t.stride(1) != 1 or t.stride(0) < t.shape[1]:
+        raise ValueError(f"{name} rows must be contiguous")
+    return t
+
+
+def points_f32(X: torch.Tensor) -> Points:
+    """fp32 points; rows must be contiguous, the row stride may be larger than d."""
+    _rows(X, torch.float32, "X")
+    return Points(KM_F32, X, X.shape[1])
+
+
+def points_sq8(codes: torch.Tensor) -> Points:
+    _dev(codes, torch.uint8, "codes", 2)
+    return Points(KM_SQ8, codes, codes.shape[1])
+
+
+def points_sign1(bits: torch.Tensor, alpha: torch.Tensor, center: torch.Tensor, d: int) -> Points:
+    _dev(bits, torch.int32, "bits", 2)
+    _dev(alpha, torch.float32, "alpha", 1)
+    _dev(center, torch.float32, "center", 1)
+    if bits.shape[1] != d // 32:
+        raise ValueError("bits must have d/32 words per row")
+    return Points(KM_SIGN1, bits, d, alpha=alpha, center=center)
+
+
+def points_hybrid(front: torch.Tensor, bits: torch.Tensor, alpha: torch.Tensor, center: torch.Tensor,
+                  d: int) -> Points:
+    _dev(front, torch.float32, "front", 2)
+    _dev(bits, torch.int32, "bits", 2)
+    _dev(alpha, torch.float32, "alpha", 1)
+    _dev(center, torch.float32, "center", 1)
+    if bits.shape[1] != d // 32:
+        raise ValueError("bits must have d/32 words per row")
+    return Points(KM_HYBRID, bits, d, alpha=alpha, center=center, front=front, d_front=front.shape[1])
+
+
+# --------------------------------------------------------------------------
+
+def quantize_sq8(X: torch.Tensor, params: torch.Tensor | None = None):
+    """SQ8 codes (uint8 n x d) and params (lo[d] then hi[d]); fits params unless given."""
+    _dev(X, torch.float32, "X", 2)
+    n, d = X.shape
+    codes = torch.empty((n, d), dtype=torch.uint8, device=X.device)
+    flags = 0
+    if params is None:
+        params = torch.empty(2 * d, dtype=torch.float32, device=X.device)
+        flags = KM_Q_FIT_PARAMS
+    else:
+        _dev(params, torch.float32, "params", 1)
+    _check(lib().quantize(_ptr(X), n, d, X.stride(0), KM_SQ8, _ptr(codes), _ptr(params), None, 0, None, flags,
+                          _stream()))
+    return codes, params
+
+
+def quantize_sign1(X: torch.Tensor, center: torch.Tensor | None = None, d_front: int = 0, want_front: bool = False):
+    """1-bit codes (int32 n x d/32), mean m, alpha over dims [d_front, d) and optional fp32 front copy."""
+    _dev(X, torch.float32, "X", 2)
+    n, d = X.shape
+    bits = torch.empty((n, d // 32), dtype=torch.int32, device=X.device)
+    alpha = torch.empty(n, dtype=torch.float32, device=X.device)
+    flags = 0
+    if center is None:
+        center = torch.empty(d, dtype=torch.float32, device=X.device)
+        flags = KM_Q_FIT_PARAMS
+    else:
+        _dev(center, torch.float32, "center", 1)
+    front = torch.empty((n, d_front), dtype=torch.float32, device=X.device) if (want_front and d_front) else None
+    _check(lib().quantize(_ptr(X), n, d, X.stride(0), KM_SIGN1, _ptr(bits), _ptr(center), _ptr(alpha), d_front,
+                          _ptr(front), flags, _stream()))
+    return bits, center, alpha, front
+
+
+def pca_fit_cov(X: torch.Tensor):
+    _dev(X, torch.float32, "X", 2)
+    n, d = X.shape
+    mean = torch.empty(d, dtype=torch.float32, device=X.device)
+    cov = torch.empty((d, d), dtype=torch.float32, device=X.device)
+    _check(lib().pca_fit_cov(_ptr(X), n, d, _ptr(mean), _ptr(cov), _stream()))
+    return mean, cov
+
+
+def pca_project(X: torch.Tensor, mean: torch.Tensor, W: torch.Tensor, out: torch.Tensor | None = None):
+    _dev(X, torch.float32, "X", 2)
+    _dev(mean, torch.float32, "mean", 1)
+    _dev(W, torch.float32, "W", 2)
+    n, d = X.shape
+    d_out = W.shape[1]
+    if W.shape[0] != d:
+        raise ValueError("W must be d x d_out")
+    Y = torch.empty((n, d_out), dtype=torch.float32, device=X.device) if out is None else out
+    _check(lib().pca_project(_ptr(X), n, d, _ptr(mean), _ptr(W), d_out, _ptr(Y), _stream()))
+    return Y
+
+
+def _check_C(P: Points, C: torch.Tensor):
+    _dev(C, P.centroid_dtype(), "C", 2)
+    if C.shape[1] != P.d:
+        raise ValueError("C must be k x d")
+    return C.shape[0]
+
+
+def kmeans_assign(P: Points, C: torch.Tensor, score: bool = True, objective: bool = False):
+    """(assign int32[n], score float[n] or None, objective double[1] on device or None)."""
+    k = _check_C(P, C)
+    a = torch.empty(P.n, dtype=torch.int32, device=P.device)
+    sc = torch.empty(P.n, dtype=torch.float32, device=P.device) if score else None
+    obj = torch.empty(1, dtype=torch.float64, device=P.device) if objective else None
+    _check(lib().kmeans_assign(P.ref, _ptr(C), k, _ptr(a), _ptr(sc), _ptr(obj), _stream()))
+    return a, sc, obj
+
+
+def kmeans_update(P: Points, assign: torch.Tensor, C: torch.Tensor, policy: int = KM_EMPTY_SPLIT,
+                  counts: bool = True):
+    """Updates C in place; returns (C, counts int64[k] or None)."""
+    k = _check_C(P, C)
+    _dev(assign, torch.int32, "assign", 1)
+    cnt = torch.empty(k, dtype=torch.int64, device=P.device) if counts else None
+    _check(lib().kmeans_update(P.ref, _ptr(assign), k, _ptr(C), _ptr(cnt), policy, _stream()))
+    return C, cnt
+
+
+def kmeans_fit(P: Points, k: int, iters: int, init_idx=None, C: torch.Tensor | None = None,
+               policy: int = KM_EMPTY_SPLIT, objective: bool = True, assign: torch.Tensor | None = None):
+    """Lloyd's algorithm on the device.  init_idx: host int64[k] (or None with C holding the start).
+    Returns (C, assign, objective double[iters+1] on device or None)."""
+    if C is None:
+        C = torch.empty((k, P.d), dtype=P.centroid_dtype(), device=P.device)
+    else:
+        _check_C(P, C)
+    a = torch.empty(P.n, dtype=torch.int32, device=P.device) if assign is None else assign
+    obj = torch.empty(iters + 1, dtype=torch.float64, device=P.device) if objective else None
+    idx_p = None
+    if init_idx is not None:
+        idx = np.ascontiguousarray(np.asarray(init_idx, dtype=np.int64))
+        if idx.shape != (k,):
+            raise ValueError("init_idx must hold k indices")
+        idx_p = idx.ctypes.data_as(ct.c_void_p)
+    _check(lib().kmeans_fit(P.ref, k, iters, idx_p, _ptr(C), _ptr(a), _ptr(obj), policy, _stream()))
+    return C, a, obj
+
+
+def kmeans_cost(X: torch.Tensor, C: torch.Tensor, assign: torch.Tensor):
+    """sum ||x - c_a||^2 (fp64, device tensor of 1)."""
+    _dev(X, torch.float32, "X", 2)
+    _dev(C, torch.float32, "C", 2)
+    _dev(assign, torch.int32, "assign", 1)
+    out = torch.empty(1, dtype=torch.float64, device=X.device)
+    _check(lib().kmeans_cost(_ptr(X), X.shape[0], X.shape[1], X.stride(0), _ptr(C), C.shape[0], _ptr(assign),
+                             _ptr(out), _stream()))
+    return out
+
+
+def release():
+    _check(lib().km_release())

@@ -1,0 +1,351 @@
+// C ABI entry points of libkmq: argument validation (host only, before any HIP
+// call), stream-ordered scratch memory, and the Lloyd loop of Sec. 2.3.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <mutex>
+#include <new>
+#include <vector>
+
+#include "common.hpp"
+
+namespace kmq {
+
+static thread_local char g_err[512] = "";
+
+void set_error(const char *fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+}
+
+km_status hip_fail(hipError_t e, const char *what) {
+  set_error("%s: %s", what, hipGetErrorString(e));
+  return KM_EDEVICE;
+}
+
+#define KMQ_CHECK(cond, code, ...) \
+  do {                             \
+    if (!(cond)) {                 \
+      set_error(__VA_ARGS__);      \
+      return (code);               \
+    }                              \
+  } while (0)
+
+static bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Keep freed scratch in each device's default pool instead of returning it to
+// the driver after every synchronisation.
+static km_status prepare_pool() {
+  static std::mutex mu;
+  static bool done[64] = {false};
+  int dev = 0;
+  KMQ_HIP(hipGetDevice(&dev));
+  std::lock_guard<std::mutex> g(mu);
+  if (dev >= 0 && dev < 64 && !done[dev]) {
+    hipMemPool_t pool;
+    KMQ_HIP(hipDeviceGetDefaultMemPool(&pool, dev));
+    uint64_t thr = ~0ull;
+    KMQ_HIP(hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &thr));
+    done[dev] = true;
+  }
+  return KM_OK;
+}
+
+// Scratch taken from the stream-ordered pool and handed back on the same stream.
+class Scratch {
+ public:
+  explicit Scratch(hipStream_t s) : s_(s) {}
+  ~Scratch() {
+    if (p_) (void)hipFreeAsync(p_, s_);
+  }
+  km_status alloc(size_t bytes) {
+    km_status st = prepare_pool();
+    if (st != KM_OK) return st;
+    hipError_t e = hipMallocAsync(&p_, std::max<size_t>(bytes, 256), s_);
+    if (e == hipErrorOutOfMemory) {
+      p_ = nullptr;
+      set_error("scratch allocation of %zu bytes failed: %s", bytes, hipGetErrorString(e));
+      return KM_ENOMEM;
+    }
+    if (e != hipSuccess) {
+      p_ = nullptr;
+      return hip_fail(e, "hipMallocAsync");
+    }
+    return KM_OK;
+  }
+  uint8_t *get() const { return static_cast<uint8_t *>(p_); }
+
+ private:
+  void *p_ = nullptr;
+  hipStream_t s_;
+};
+
+static size_t al(size_t x) { return (x + 255) & ~(size_t)255; }
+
+static km_status check_points(const km_points *P, Points *out) {
+  KMQ_CHECK(P != nullptr, KM_EINVAL, "points descriptor is NULL");
+  const int fmt = P->fmt;
+  KMQ_CHECK(fmt == KM_F32 || fmt == KM_SQ8 || fmt == KM_SIGN1 || fmt == KM_HYBRID, KM_EUNSUPPORTED,
+            "unknown point format %d", fmt);
+  KMQ_CHECK(P->reserved == 0, KM_EINVAL, "reserved field must be 0");
+  KMQ_CHECK(P->n >= 1 && P->n < (int64_t)INT32_MAX, KM_EINVAL, "n = %lld outside [1, 2^31)", (long long)P->n);
+  KMQ_CHECK(P->d >= 1, KM_EINVAL, "d = %d must be >= 1", P->d);
+  KMQ_CHECK(P->data != nullptr, KM_EINVAL, "points data is NULL");
+  KMQ_CHECK(aligned16(P->data), KM_EINVAL, "points data must be 16-byte aligned");
+  Points p{};
+  p.fmt = fmt;
+  p.d = P->d;
+  p.n = P->n;
+  p.data = P->data;
+  p.ld = P->ld;
+  p.alpha = P->alpha;
+  p.center = P->center;
+  p.front = P->front;
+  p.d_front = P->d_front;
+  if (fmt == KM_F32) {
+    KMQ_CHECK(P->d % 4 == 0, KM_EINVAL, "fp32 points need d %% 4 == 0 (d = %d)", P->d);
+    KMQ_CHECK(P->ld >= P->d && P->ld % 4 == 0, KM_EINVAL, "fp32 points need ld >= d and ld %% 4 == 0");
+    KMQ_CHECK(P->d_front == 0, KM_EINVAL, "d_front must be 0 for this format");
+  } else if (fmt == KM_SQ8) {
+    KMQ_CHECK(P->d % 16 == 0, KM_EINVAL, "SQ8 codes need d %% 16 == 0 (d = %d)", P->d);
+    KMQ_CHECK(P->ld >= P->d && P->ld % 16 == 0, KM_EINVAL, "SQ8 codes need ld >= d and ld %% 16 == 0");
+    KMQ_CHECK(P->d_front == 0, KM_EINVAL, "d_front must be 0 for this format");
+  } else {
+    KMQ_CHECK(P->d % 32 == 0, KM_EINVAL, "1-bit codes need d %% 32 == 0 (d = %d)", P->d);
+    KMQ_CHECK(P->alpha != nullptr, KM_EINVAL, "alpha is NULL");
+    KMQ_CHECK(P->center != nullptr, KM_EINVAL, "center is NULL");
+    p.ld = P->d / 32;
+    if (fmt == KM_HYBRID) {
+      KMQ_CHECK(P->d_front > 0 && P->d_front < P->d && P->d_front % 32 == 0, KM_EINVAL,
+                "hybrid needs 0 < d_front < d and d_front %% 32 == 0 (d_front = %d)", P->d_front);
+      KMQ_CHECK(P->front != nullptr && aligned16(P->front), KM_EINVAL, "hybrid front must be a 16-byte aligned pointer");
+    } else {
+      KMQ_CHECK(P->d_front == 0, KM_EINVAL, "d_front must be 0 for this format");
+    }
+  }
+  *out = p;
+  return KM_OK;
+}
+
+static km_status check_centroids(const Points &p, const void *C, int k) {
+  KMQ_CHECK(k >= 1, KM_EINVAL, "k = %d must be >= 1", k);
+  KMQ_CHECK(C != nullptr, KM_EINVAL, "centroids pointer is NULL");
+  KMQ_CHECK(aligned16(C), KM_EINVAL, "centroids must be 16-byte aligned");
+  (void)p;
+  return KM_OK;
+}
+
+static size_t centroid_bytes(const Points &p, int k) {
+  return (size_t)k * p.d * (p.fmt == KM_SQ8 ? 1 : sizeof(float));
+}
+
+}  // namespace kmq
+
+using namespace kmq;
+
+extern "C" {
+
+const char *km_last_error(void) { return g_err; }
+
+km_status km_release(void) {
+  int dev = 0;
+  KMQ_HIP(hipGetDevice(&dev));
+  hipMemPool_t pool;
+  KMQ_HIP(hipDeviceGetDefaultMemPool(&pool, dev));
+  KMQ_HIP(hipMemPoolTrimTo(pool, 0));
+  return KM_OK;
+}
+
+km_status quantize(const float *X, int64_t n, int32_t d, int64_t ldx, int32_t fmt, void *codes, float *params,
+                   float *alpha, int32_t d_front, float *front, int32_t flags, km_stream stream) {
+  g_err[0] = 0;
+  KMQ_CHECK(fmt == KM_SQ8 || fmt == KM_SIGN1, KM_EUNSUPPORTED, "quantize supports SQ8 and SIGN1 (fmt = %d)", fmt);
+  KMQ_CHECK(X != nullptr && codes != nullptr && params != nullptr, KM_EINVAL, "NULL argument");
+  KMQ_CHECK(n >= 1 && n < (int64_t)INT32_MAX, KM_EINVAL, "n = %lld outside [1, 2^31)", (long long)n);
+  KMQ_CHECK(d >= 1 && ldx >= d && ldx % 4 == 0, KM_EINVAL, "need d >= 1, ldx >= d, ldx %% 4 == 0");
+  KMQ_CHECK(aligned16(X) && aligned16(codes), KM_EINVAL, "X and codes must be 16-byte aligned");
+  KMQ_CHECK((flags & ~KM_Q_FIT_PARAMS) == 0, KM_EINVAL, "unknown flags 0x%x", flags);
+  if (fmt == KM_SQ8) {
+    KMQ_CHECK(d % 16 == 0, KM_EINVAL, "SQ8 needs d %% 16 == 0 (d = %d)", d);
+    KMQ_CHECK(d_front == 0 && front == nullptr, KM_EINVAL, "d_front/front are for 1-bit codes only");
+  } else {
+    KMQ_CHECK(d % 32 == 0, KM_EINVAL, "1-bit codes need d %% 32 == 0 (d = %d)", d);
+    KMQ_CHECK(alpha != nullptr, KM_EINVAL, "alpha is NULL");
+    KMQ_CHECK(d_front >= 0 && d_front < d && d_front % 32 == 0, KM_EINVAL,
+              "need 0 <= d_front < d and d_front %% 32 == 0 (d_front = %d)", d_front);
+    KMQ_CHECK(front == nullptr || d_front > 0, KM_EINVAL, "front copy needs d_front > 0");
+  }
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  Scratch ws(s);
+  km_status st = ws.alloc(quantize_bytes(n, d, fmt));
+  if (st != KM_OK) return st;
+  return launch_quantize(X, n, d, ldx, fmt, codes, params, alpha, d_front, front, flags, ws.get(), s);
+}
+
+km_status pca_fit_cov(const float *X, int64_t n, int32_t d, float *mean, float *cov, km_stream stream) {
+  g_err[0] = 0;
+  KMQ_CHECK(X != nullptr && mean != nullptr && cov != nullptr, KM_EINVAL, "NULL argument");
+  KMQ_CHECK(n >= 1 && n < (int64_t)INT32_MAX, KM_EINVAL, "n = %lld outside [1, 2^31)", (long long)n);
+  KMQ_CHECK(d >= 1 && d % 4 == 0, KM_EINVAL, "pca_fit_cov needs d %% 4 == 0 (d = %d)", d);
+  KMQ_CHECK(aligned16(X) && aligned16(mean), KM_EINVAL, "X and mean must be 16-byte aligned");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  Scratch ws(s);
+  km_status st = ws.alloc(pca_cov_bytes(n, d));
+  if (st != KM_OK) return st;
+  return launch_pca_cov(X, n, d, mean, cov, ws.get(), s);
+}
+
+km_status pca_project(const float *X, int64_t n, int32_t d, const float *mean, const float *W, int32_t d_out,
+                      float *Y, km_stream stream) {
+  g_err[0] = 0;
+  KMQ_CHECK(X != nullptr && mean != nullptr && W != nullptr && Y != nullptr, KM_EINVAL, "NULL argument");
+  KMQ_CHECK(n >= 1 && n < (int64_t)INT32_MAX, KM_EINVAL, "n = %lld outside [1, 2^31)", (long long)n);
+  KMQ_CHECK(d >= 1 && d % 4 == 0, KM_EINVAL, "pca_project needs d %% 4 == 0 (d = %d)", d);
+  KMQ_CHECK(d_out >= 1, KM_EINVAL, "d_out = %d must be >= 1", d_out);
+  KMQ_CHECK(aligned16(X) && aligned16(mean), KM_EINVAL, "X and mean must be 16-byte aligned");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  Scratch ws(s);
+  km_status st = ws.alloc(pca_project_bytes(d, d_out));
+  if (st != KM_OK) return st;
+  return launch_pca_project(X, n, d, mean, W, d_out, Y, ws.get(), s);
+}
+
+km_status kmeans_assign(const km_points *P, const void *C, int32_t k, int32_t *assign, float *score,
+                        double *objective, km_stream stream) {
+  g_err[0] = 0;
+  Points p;
+  km_status st = check_points(P, &p);
+  if (st != KM_OK) return st;
+  st = check_centroids(p, C, k);
+  if (st != KM_OK) return st;
+  KMQ_CHECK(assign != nullptr, KM_EINVAL, "assign is NULL");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const size_t b_prep = al(prep_bytes(p, k));
+  const bool need_score = objective != nullptr && score == nullptr;
+  const size_t b_score = need_score ? al(sizeof(float) * (size_t)p.n) : 0;
+  const size_t b_xc = objective ? al(sizeof(float) * (size_t)p.n) : 0;
+  const size_t b_part = objective ? al(sizeof(double) * (size_t)objective_blocks(p.n)) : 0;
+  Scratch ws(s);
+  st = ws.alloc(b_prep + b_score + b_xc + b_part);
+  if (st != KM_OK) return st;
+  uint8_t *w = ws.get();
+  float *sc = need_score ? reinterpret_cast<float *>(w + b_prep) : score;
+  float *xc = reinterpret_cast<float *>(w + b_prep + b_score);
+  double *part = reinterpret_cast<double *>(w + b_prep + b_score + b_xc);
+  CentroidPrep cp;
+  st = launch_prep(p, C, k, w, &cp, s);
+  if (st != KM_OK) return st;
+  st = launch_assign(p, C, cp, k, assign, sc, s);
+  if (st != KM_OK) return st;
+  if (objective) {
+    st = launch_xconst(p, xc, s);
+    if (st != KM_OK) return st;
+    st = launch_objective(p, xc, sc, p.n, objective, part, objective_blocks(p.n), s);
+  }
+  return st;
+}
+
+km_status kmeans_update(const km_points *P, const int32_t *assign, int32_t k, void *C, int64_t *counts, int32_t policy,
+                        km_stream stream) {
+  g_err[0] = 0;
+  Points p;
+  km_status st = check_points(P, &p);
+  if (st != KM_OK) return st;
+  st = check_centroids(p, C, k);
+  if (st != KM_OK) return st;
+  KMQ_CHECK(assign != nullptr, KM_EINVAL, "assign is NULL");
+  KMQ_CHECK(policy == KM_EMPTY_SPLIT || policy == KM_EMPTY_KEEP, KM_EINVAL, "unknown empty-cluster policy %d", policy);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  Scratch ws(s);
+  st = ws.alloc(update_bytes(p, k));
+  if (st != KM_OK) return st;
+  return launch_update(p, assign, k, C, counts, policy, ws.get(), s);
+}
+
+km_status kmeans_fit(const km_points *P, int32_t k, int32_t iters, const int64_t *init_idx, void *C, int32_t *assign,
+                     double *objective, int32_t policy, km_stream stream) {
+  g_err[0] = 0;
+  Points p;
+  km_status st = check_points(P, &p);
+  if (st != KM_OK) return st;
+  st = check_centroids(p, C, k);
+  if (st != KM_OK) return st;
+  KMQ_CHECK(assign != nullptr, KM_EINVAL, "assign is NULL");
+  KMQ_CHECK(k <= p.n, KM_EINVAL, "k = %d exceeds n = %lld", k, (long long)p.n);
+  KMQ_CHECK(iters >= 0, KM_EINVAL, "iters = %d must be >= 0", iters);
+  KMQ_CHECK(policy == KM_EMPTY_SPLIT || policy == KM_EMPTY_KEEP, KM_EINVAL, "unknown empty-cluster policy %d", policy);
+  if (init_idx) {
+    try {
+      std::vector<int64_t> v(init_idx, init_idx + k);
+      std::sort(v.begin(), v.end());
+      KMQ_CHECK(v.front() >= 0 && v.back() < p.n, KM_EINVAL, "init_idx outside [0, n)");
+      KMQ_CHECK(std::adjacent_find(v.begin(), v.end()) == v.end(), KM_EINVAL, "init_idx holds duplicates");
+    } catch (const std::bad_alloc &) {
+      set_error("host allocation failed");
+      return KM_ENOMEM;
+    }
+  }
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const size_t b_prep = al(prep_bytes(p, k));
+  const size_t b_upd = al(update_bytes(p, k));
+  const size_t b_score = objective ? al(sizeof(float) * (size_t)p.n) : 0;
+  const size_t b_xc = objective ? al(sizeof(float) * (size_t)p.n) : 0;
+  const size_t b_part = objective ? al(sizeof(double) * (size_t)objective_blocks(p.n)) : 0;
+  const size_t b_idx = init_idx ? al(sizeof(int64_t) * (size_t)k) : 0;
+  Scratch ws(s);
+  st = ws.alloc(b_prep + b_upd + b_score + b_xc + b_part + b_idx);
+  if (st != KM_OK) return st;
+  uint8_t *w = ws.get();
+  uint8_t *wprep = w;
+  uint8_t *wupd = w + b_prep;
+  float *sc = objective ? reinterpret_cast<float *>(w + b_prep + b_upd) : nullptr;
+  float *xc = reinterpret_cast<float *>(w + b_prep + b_upd + b_score);
+  double *part = reinterpret_cast<double *>(w + b_prep + b_upd + b_score + b_xc);
+  int64_t *didx = reinterpret_cast<int64_t *>(w + b_prep + b_upd + b_score + b_xc + b_part);
+  (void)centroid_bytes;
+
+  if (init_idx) {
+    KMQ_HIP(hipMemcpyAsync(didx, init_idx, sizeof(int64_t) * (size_t)k, hipMemcpyHostToDevice, s));
+    st = launch_gather_init(p, didx, k, C, s);
+    if (st != KM_OK) return st;
+  }
+  if (objective) {
+    st = launch_xconst(p, xc, s);
+    if (st != KM_OK) return st;
+  }
+  CentroidPrep cp;
+  for (int it = 0; it <= iters; ++it) {
+    st = launch_prep(p, C, k, wprep, &cp, s);
+    if (st != KM_OK) return st;
+    st = launch_assign(p, C, cp, k, assign, sc, s);
+    if (st != KM_OK) return st;
+    if (objective) {
+      st = launch_objective(p, xc, sc, p.n, objective + it, part, objective_blocks(p.n), s);
+      if (st != KM_OK) return st;
+    }
+    if (it == iters) break;  // the last pass only assigns (the final STEP 2)
+    st = launch_update(p, assign, k, C, nullptr, policy, wupd, s);
+    if (st != KM_OK) return st;
+  }
+  return KM_OK;
+}
+
+km_status kmeans_cost(const float *X, int64_t n, int32_t d, int64_t ldx, const float *C, int32_t k,
+                      const int32_t *assign, double *out, km_stream stream) {
+  g_err[0] = 0;
+  KMQ_CHECK(X != nullptr && C != nullptr && assign != nullptr && out != nullptr, KM_EINVAL, "NULL argument");
+  KMQ_CHECK(n >= 1 && n < (int64_t)INT32_MAX, KM_EINVAL, "n = %lld outside [1, 2^31)", (long long)n);
+  KMQ_CHECK(d >= 1 && ldx >= d, KM_EINVAL, "need d >= 1 and ldx >= d");
+  KMQ_CHECK(k >= 1, KM_EINVAL, "k = %d must be >= 1", k);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  Scratch ws(s);
+  km_status st = ws.alloc(sizeof(double) * 1024);
+  if (st != KM_OK) return st;
+  return launch_cost(X, n, d, ldx, C, k, assign, out, reinterpret_cast<double *>(ws.get()), s);
+}
+
+}  // extern "C"

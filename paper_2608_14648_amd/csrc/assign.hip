@@ -1,0 +1,714 @@
+// STEP 2 (Sec. 2.3): nearest-centroid assignment as a fused MFMA contraction with
+// an in-register running argmin, plus the small kernels around it (centroid
+// preparation, point-only terms, objective sum, initial gather, partition cost).
+//
+// Fused assignment kernel
+// -----------------------
+// One workgroup (256 threads, 4 waves) owns 128 points and sweeps every centroid
+// in tiles of 128.  For a (centroid tile, point tile) pair the dot products
+// <c, x> are accumulated over d on the matrix cores with the CENTROIDS as the
+// MFMA row operand and the POINTS as the column operand, so each lane of the
+// 32x32 output block holds 16 centroid rows of ONE point column: the argmin over
+// centroids is then a lane-local compare-select, never a cross-lane shuffle,
+// and the n x k score matrix never leaves registers.
+//   - fp32 points (raw / PCA / hybrid front): v_mfma_f32_32x32x2_f32.
+//   - SQ8 codes: code - 128 as int8 on both sides, v_mfma_i32_32x32x32_i8;
+//     score = ||c~||^2 - 2 <x~, c~> is an exact int32.
+//   - 1-bit codes: each bit is widened to a {0,1} byte while the tile is staged
+//     in LDS, and multiplied with the centroid's int8 residual codes q on the
+//     int8 matrix cores: D = sum of q on set bits, and <2b-1, q> = 2D - T (Eq. 5
+//     with x_bar in {0,1}).  The fp32 epilogue follows Eq. 4 with the point's
+//     cached scale alpha: score = fmaf(-(alpha * 2 sigma), 2D - T, sigma^2 Q).
+//   - hybrid: an fp32 phase over the front dims and an int8 phase over the
+//     1-bit tail accumulate separately; the scores add (segment decomposition
+//     of the squared L2 distance, Sec. 3.1 SuperKMeans).
+// Stages are 128 bytes of every row (32 floats or 128 int8 lanes), staged
+// global -> registers -> LDS with double buffering and one barrier per stage.
+// Both operands of an MFMA read 16 contiguous bytes per lane from the same
+// LDS column offset, so the k-index permutation inside the instruction is the
+// same on both sides and cancels in the dot product.
+// Ties: within a lane candidates arrive in increasing centroid index and are
+// taken only on a strict improvement; lanes and waves merge on (score, index),
+// so the smallest index wins every exact tie.
+#include <float.h>
+#include <limits.h>
+
+#include <algorithm>
+#include <type_traits>
+
+#include "common.hpp"
+
+namespace kmq {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kTile = 128;                      // centroids per tile and points per workgroup
+constexpr int kRowBytes = 128;                  // bytes of one row per stage
+constexpr int kLdsStride = kRowBytes + 16;      // padded to spread LDS banks
+constexpr int kTileBytes = kTile * kLdsStride;  // 18432
+constexpr int kStageBytes = 2 * kTileBytes;     // centroid tile + point tile
+
+struct AssignArgs {
+  // fp32 phase: F32 points, hybrid front
+  const float *pf;
+  int64_t pfld;
+  const float *cf;
+  int64_t cfld;
+  int df;
+  // integer phase: SQ8 codes or 1-bit tail
+  const uint8_t *pi8;
+  int64_t pild;
+  const uint32_t *pbits;
+  int64_t pbw;  // words per 1-bit row
+  int pbw0;     // first word of the integer phase
+  const int8_t *ci8;
+  int64_t cild;
+  int di;
+  const float *alpha;
+  CentroidPrep cp;
+  int64_t n;
+  int k;
+  int32_t *assign;
+  float *score;
+};
+
+__device__ __forceinline__ uint32_t spread4(uint32_t b4) {
+  // 4 bits -> 4 bytes holding 0 or 1 (bit j -> byte j)
+  return (b4 * 0x00204081u) & 0x01010101u;
+}
+
+template <int FMT>
+struct Cfg {
+  static constexpr bool kFp = (FMT == KM_F32 || FMT == KM_HYBRID);
+  static constexpr bool kInt = (FMT != KM_F32);
+  static constexpr bool kBits = (FMT == KM_SIGN1 || FMT == KM_HYBRID);
+  static constexpr bool kIntScore = (FMT == KM_SQ8);
+};
+
+struct StageRegs {
+  uint4 c[4];
+  uint4 p[4];
+};
+
+template <int FMT>
+__device__ __forceinline__ void load_stage(const AssignArgs &A, int s, int SF, int64_t c0, int64_t p0,
+                                           StageRegs &R) {
+  const int t = threadIdx.x;
+  const uint4 z = make_uint4(0, 0, 0, 0);
+  if (Cfg<FMT>::kFp && s < SF) {
+    const int dim0 = 32 * s;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int cidx = t + kThreads * i;
+      const int row = cidx >> 3, col = cidx & 7;
+      const int dim = dim0 + 4 * col;
+      const bool ok = dim < A.df;
+      const int64_t cr = min<int64_t>(c0 + row, A.k - 1);
+      const int64_t pr = min<int64_t>(p0 + row, A.n - 1);
+      R.c[i] = ok ? *reinterpret_cast<const uint4 *>(A.cf + cr * A.cfld + dim) : z;
+      R.p[i] = ok ? *reinterpret_cast<const uint4 *>(A.pf + pr * A.pfld + dim) : z;
+    }
+    return;
+  }
+  if constexpr (Cfg<FMT>::kInt) {
+    const int si = s - (Cfg<FMT>::kFp ? SF : 0);
+    const int b0 = kRowBytes * si;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int cidx = t + kThreads * i;
+      const int row = cidx >> 3, col = cidx & 7;
+      const int b = b0 + 16 * col;
+      const bool ok = b < A.di;
+      const int64_t cr = min<int64_t>(c0 + row, A.k - 1);
+      uint4 v = ok ? *reinterpret_cast<const uint4 *>(A.ci8 + cr * A.cild + b) : z;
+      if (FMT == KM_SQ8 && ok) {
+        v.x ^= 0x80808080u; v.y ^= 0x80808080u; v.z ^= 0x80808080u; v.w ^= 0x80808080u;
+      }
+      R.c[i] = v;
+      if (FMT == KM_SQ8) {
+        const int64_t pr = min<int64_t>(p0 + row, A.n - 1);
+        uint4 w = ok ? *reinterpret_cast<const uint4 *>(A.pi8 + pr * A.pild + b) : z;
+        if (ok) {
+          w.x ^= 0x80808080u; w.y ^= 0x80808080u; w.z ^= 0x80808080u; w.w ^= 0x80808080u;
+        }
+        R.p[i] = w;
+      }
+    }
+    if (Cfg<FMT>::kBits) {
+      // 128 points x 4 words of this stage: two words per thread, each widened to 32 bytes
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int w = t + kThreads * i;
+        const int row = w >> 2, wi = w & 3;
+        const int word = 4 * si + wi;
+        const bool ok = 32 * word < A.di;
+        const int64_t pr = min<int64_t>(p0 + row, A.n - 1);
+        const uint32_t bits = ok ? A.pbits[pr * A.pbw + A.pbw0 + word] : 0u;
+        R.p[2 * i] = make_uint4(spread4(bits & 15u), spread4((bits >> 4) & 15u), spread4((bits >> 8) & 15u),
+                                spread4((bits >> 12) & 15u));
+        R.p[2 * i + 1] = make_uint4(spread4((bits >> 16) & 15u), spread4((bits >> 20) & 15u),
+                                    spread4((bits >> 24) & 15u), spread4(bits >> 28));
+      }
+    }
+  }
+}
+
+template <int FMT>
+__device__ __forceinline__ void store_stage(int s, int SF, const StageRegs &R, uint8_t *buf) {
+  const int t = threadIdx.x;
+  uint8_t *ct = buf;
+  uint8_t *pt = buf + kTileBytes;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int cidx = t + kThreads * i;
+    const int row = cidx >> 3, col = cidx & 7;
+    *reinterpret_cast<uint4 *>(ct + row * kLdsStride + 16 * col) = R.c[i];
+  }
+  const bool bitstage = Cfg<FMT>::kBits && !(Cfg<FMT>::kFp && s < SF);
+  if (bitstage) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int w = t + kThreads * i;
+      const int row = w >> 2, wi = w & 3;
+      *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 32 * wi) = R.p[2 * i];
+      *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 32 * wi + 16) = R.p[2 * i + 1];
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int cidx = t + kThreads * i;
+      const int row = cidx >> 3, col = cidx & 7;
+      *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 16 * col) = R.p[i];
+    }
+  }
+}
+
+template <int FMT>
+__global__ __launch_bounds__(kThreads) void assign_kernel(AssignArgs A) {
+  __shared__ __align__(16) uint8_t lds[2 * kStageBytes];
+  typedef typename std::conditional<Cfg<FMT>::kIntScore, int, float>::type score_t;
+
+  const int t = threadIdx.x;
+  const int lane = t & 63, wave = t >> 6;
+  const int r = lane & 31, h = lane >> 5;
+  const int wc = wave & 1, wp = wave >> 1;
+  const int64_t p0 = (int64_t)blockIdx.x * kTile;
+
+  const int SF = Cfg<FMT>::kFp ? (A.df + 31) / 32 : 0;
+  const int SI = Cfg<FMT>::kInt ? (A.di + kRowBytes - 1) / kRowBytes : 0;
+  const int S = SF + SI;
+  const int nct = (A.k + kTile - 1) / kTile;
+  const int total = nct * S;
+
+  float al[2] = {0.f, 0.f};
+  if (Cfg<FMT>::kBits) {
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb) al[pb] = A.alpha[min<int64_t>(p0 + wp * 64 + pb * 32 + r, A.n - 1)];
+  }
+
+  f32x16 facc[2][2];
+  i32x16 iacc[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        facc[a][b][i] = 0.f;
+        iacc[a][b][i] = 0;
+      }
+    }
+
+  score_t best[2];
+  int bidx[2] = {INT_MAX, INT_MAX};
+  if (Cfg<FMT>::kIntScore) {
+    best[0] = best[1] = (score_t)INT_MAX;
+  } else {
+    best[0] = best[1] = (score_t)INFINITY;
+  }
+
+  StageRegs R;
+  load_stage<FMT>(A, 0, SF, 0, p0, R);
+  store_stage<FMT>(0, SF, R, lds);
+  __syncthreads();
+
+  for (int it = 0; it < total; ++it) {
+    const int ct = it / S;
+    const int s = it - ct * S;
+    const bool has_next = it + 1 < total;
+    if (has_next) {
+      const int nct_ = (it + 1) / S;
+      load_stage<FMT>(A, (it + 1) - nct_ * S, SF, (int64_t)nct_ * kTile, p0, R);
+    }
+    const uint8_t *buf = lds + (it & 1) * kStageBytes;
+    const uint8_t *cbuf = buf;
+    const uint8_t *pbuf = buf + kTileBytes;
+    const bool fpstage = Cfg<FMT>::kFp && s < SF;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      uint4 av[2], bv[2];
+#pragma unroll
+      for (int cb = 0; cb < 2; ++cb)
+        av[cb] = *reinterpret_cast<const uint4 *>(cbuf + (wc * 64 + cb * 32 + r) * kLdsStride + 32 * g + 16 * h);
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb)
+        bv[pb] = *reinterpret_cast<const uint4 *>(pbuf + (wp * 64 + pb * 32 + r) * kLdsStride + 32 * g + 16 * h);
+      if (fpstage) {
+        if constexpr (Cfg<FMT>::kFp) {
+#pragma unroll
+          for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+            for (int pb = 0; pb < 2; ++pb) {
+              facc[cb][pb] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(av[cb].x), __uint_as_float(bv[pb].x),
+                                                                  facc[cb][pb], 0, 0, 0);
+              facc[cb][pb] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(av[cb].y), __uint_as_float(bv[pb].y),
+                                                                  facc[cb][pb], 0, 0, 0);
+              facc[cb][pb] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(av[cb].z), __uint_as_float(bv[pb].z),
+                                                                  facc[cb][pb], 0, 0, 0);
+              facc[cb][pb] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(av[cb].w), __uint_as_float(bv[pb].w),
+                                                                  facc[cb][pb], 0, 0, 0);
+            }
+        }
+      } else {
+        if constexpr (Cfg<FMT>::kInt) {
+#pragma unroll
+          for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+            for (int pb = 0; pb < 2; ++pb) {
+              i32x4 a4 = {(int)av[cb].x, (int)av[cb].y, (int)av[cb].z, (int)av[cb].w};
+              i32x4 b4 = {(int)bv[pb].x, (int)bv[pb].y, (int)bv[pb].z, (int)bv[pb].w};
+              iacc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a4, b4, iacc[cb][pb], 0, 0, 0);
+            }
+        }
+      }
+    }
+
+    if (s == S - 1) {
+      // epilogue for centroid tile ct: scores and running argmin, lane-local
+      const int64_t c0 = (int64_t)ct * kTile;
+#pragma unroll
+      for (int cb = 0; cb < 2; ++cb) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int crow = wc * 64 + cb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
+          const int64_t j = c0 + crow;
+          if (j < A.k) {
+            float cn = 0.f, u = 0.f, s2 = 0.f;
+            int qs = 0;
+            if (Cfg<FMT>::kFp) cn = A.cp.cn[j];
+            if (Cfg<FMT>::kInt) qs = A.cp.qsum[j];
+            if (Cfg<FMT>::kBits) {
+              u = A.cp.u[j];
+              s2 = A.cp.sig2[j];
+            }
+#pragma unroll
+            for (int pb = 0; pb < 2; ++pb) {
+              score_t sc;
+              if constexpr (FMT == KM_F32) {
+                sc = fmaf(-2.0f, facc[cb][pb][i], cn);
+              } else if constexpr (FMT == KM_SQ8) {
+                sc = qs - 2 * iacc[cb][pb][i];
+              } else if constexpr (FMT == KM_SIGN1) {
+                const int sd = 2 * iacc[cb][pb][i] - qs;
+                const float v = al[pb] * s2;
+                sc = fmaf(-v, (float)sd, u);
+              } else {
+                const int sd = 2 * iacc[cb][pb][i] - qs;
+                const float v = al[pb] * s2;
+                const float ts = fmaf(-v, (float)sd, u);
+                const float fs = fmaf(-2.0f, facc[cb][pb][i], cn);
+                sc = fs + ts;
+              }
+              if (sc < best[pb]) {
+                best[pb] = sc;
+                bidx[pb] = (int)j;
+              }
+            }
+          }
+        }
+      }
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            facc[a][b][i] = 0.f;
+            iacc[a][b][i] = 0;
+          }
+        }
+    }
+
+    if (has_next) store_stage<FMT>((it + 1) % S, SF, R, lds + ((it + 1) & 1) * kStageBytes);
+    __syncthreads();
+  }
+
+  // merge the two lane halves (rows 4h..), then the two centroid waves
+#pragma unroll
+  for (int pb = 0; pb < 2; ++pb) {
+    score_t os = __shfl_xor(best[pb], 32);
+    int oi = __shfl_xor(bidx[pb], 32);
+    if (os < best[pb] || (os == best[pb] && oi < bidx[pb])) {
+      best[pb] = os;
+      bidx[pb] = oi;
+    }
+  }
+  score_t *ms = reinterpret_cast<score_t *>(lds);
+  int *mi = reinterpret_cast<int *>(lds + kTile * sizeof(score_t));
+  if (wc == 1 && h == 0) {
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb) {
+      ms[wp * 64 + pb * 32 + r] = best[pb];
+      mi[wp * 64 + pb * 32 + r] = bidx[pb];
+    }
+  }
+  __syncthreads();
+  if (wc == 0 && h == 0) {
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb) {
+      const int pc = wp * 64 + pb * 32 + r;
+      const score_t os = ms[pc];
+      const int oi = mi[pc];
+      if (os < best[pb] || (os == best[pb] && oi < bidx[pb])) {
+        best[pb] = os;
+        bidx[pb] = oi;
+      }
+      const int64_t p = p0 + pc;
+      if (p < A.n) {
+        A.assign[p] = bidx[pb];
+        if (A.score) A.score[p] = (float)best[pb];
+      }
+    }
+  }
+}
+
+// ---- centroid preparation: one workgroup per centroid ----------------------
+
+template <int FMT>
+__global__ __launch_bounds__(256) void prep_kernel(const void *Cv, int k, int d, int d0, const float *m,
+                                                   float *cn, int *qsum, float *u, float *sig2, int8_t *q) {
+  __shared__ double shd[256];
+  __shared__ float shf[256];
+  __shared__ int shi[256];
+  const int j = blockIdx.x;
+  const int t = threadIdx.x;
+  if (FMT == KM_F32 || FMT == KM_HYBRID) {
+    const float *c = static_cast<const float *>(Cv) + (int64_t)j * d;
+    const int dd = FMT == KM_F32 ? d : d0;
+    double s = 0.0;
+    for (int i = t; i < dd; i += 256) s += (double)c[i] * (double)c[i];
+    s = block_sum_f64(s, shd);
+    if (t == 0) cn[j] = (float)s;
+  }
+  if (FMT == KM_SQ8) {
+    const uint8_t *c = static_cast<const uint8_t *>(Cv) + (int64_t)j * d;
+    int s = 0;
+    for (int i = t; i < d; i += 256) {
+      const int v = (int)c[i] - 128;
+      s += v * v;
+    }
+    shi[t] = s;
+    __syncthreads();
+    for (int st = 128; st > 0; st >>= 1) {
+      if (t < st) shi[t] += shi[t + st];
+      __syncthreads();
+    }
+    if (t == 0) qsum[j] = shi[0];
+  }
+  if (FMT == KM_SIGN1 || FMT == KM_HYBRID) {
+    const float *c = static_cast<const float *>(Cv) + (int64_t)j * d;
+    const int dt = d - d0;
+    float mx = 0.f;
+    for (int i = d0 + t; i < d; i += 256) mx = fmaxf(mx, fabsf(c[i] - m[i]));
+    shf[t] = mx;
+    __syncthreads();
+    for (int st = 128; st > 0; st >>= 1) {
+      if (t < st) shf[t] = fmaxf(shf[t], shf[t + st]);
+      __syncthreads();
+    }
+    mx = shf[0];
+    const float sg = mx > 0.f ? mx / 127.0f : 1.0f;
+    int ts = 0, qq = 0;
+    for (int i = d0 + t; i < d; i += 256) {
+      float v = mx > 0.f ? rintf((c[i] - m[i]) / sg) : 0.f;
+      v = fminf(fmaxf(v, -127.f), 127.f);
+      const int qi = (int)v;
+      q[(int64_t)j * dt + (i - d0)] = (int8_t)qi;
+      ts += qi;
+      qq += qi * qi;
+    }
+    __syncthreads();
+    shi[t] = ts;
+    __syncthreads();
+    for (int st = 128; st > 0; st >>= 1) {
+      if (t < st) shi[t] += shi[t + st];
+      __syncthreads();
+    }
+    const int T = shi[0];
+    __syncthreads();
+    shi[t] = qq;
+    __syncthreads();
+    for (int st = 128; st > 0; st >>= 1) {
+      if (t < st) shi[t] += shi[t + st];
+      __syncthreads();
+    }
+    if (t == 0) {
+      const int Q = shi[0];
+      qsum[j] = T;
+      u[j] = (sg * sg) * (float)Q;
+      sig2[j] = 2.0f * sg;
+    }
+  }
+}
+
+// ---- point-only terms of the in-space distance ------------------------------
+// F32: ||x||^2 ; SQ8: ||code-128||^2 ; SIGN1: alpha^2 d ; HYBRID: ||x'||^2 + alpha^2 (d - d0)
+// One wave per point.
+template <int FMT>
+__global__ __launch_bounds__(256) void xconst_kernel(Points P, float *xc) {
+  const int lane = threadIdx.x & 63;
+  const int64_t p = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (p >= P.n) return;
+  double s = 0.0;
+  if (FMT == KM_F32 || FMT == KM_HYBRID) {
+    const float *x = FMT == KM_F32 ? static_cast<const float *>(P.data) + p * P.ld : P.front + p * P.d_front;
+    const int dd = FMT == KM_F32 ? P.d : P.d_front;
+    for (int i = lane; i < dd; i += 64) s += (double)x[i] * (double)x[i];
+  } else if (FMT == KM_SQ8) {
+    const uint8_t *x = static_cast<const uint8_t *>(P.data) + p * P.ld;
+    for (int i = lane; i < P.d; i += 64) {
+      const int v = (int)x[i] - 128;
+      s += (double)(v * v);
+    }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+  if (lane == 0) {
+    if (FMT == KM_SIGN1 || FMT == KM_HYBRID) {
+      const double a = P.alpha[p];
+      s += a * a * (double)(P.d - (FMT == KM_HYBRID ? P.d_front : 0));
+    }
+    xc[p] = (float)s;
+  }
+}
+
+// ---- objective: sum of (point term + score), deterministic two-level sum ----
+__global__ __launch_bounds__(256) void objective_partial_kernel(const float *xc, const float *score, int64_t n,
+                                                                double *partials) {
+  __shared__ double sh[256];
+  double s = 0.0;
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  for (int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x; p < n; p += stride)
+    s += (double)xc[p] + (double)score[p];
+  s = block_sum_f64(s, sh);
+  if (threadIdx.x == 0) partials[blockIdx.x] = s;
+}
+
+__global__ __launch_bounds__(256) void sum_partials_kernel(const double *partials, int np, double *out) {
+  __shared__ double sh[256];
+  double s = 0.0;
+  for (int i = threadIdx.x; i < np; i += 256) s += partials[i];
+  s = block_sum_f64(s, sh);
+  if (threadIdx.x == 0) *out = s;
+}
+
+// ---- STEP 1: gather the sampled points as initial centroids -----------------
+template <int FMT>
+__global__ __launch_bounds__(256) void gather_kernel(Points P, const int64_t *idx, void *Cv) {
+  const int j = blockIdx.x;
+  const int64_t row = idx[j];  // validated on the host
+  const int d = P.d;
+  if (FMT == KM_F32) {
+    const float *x = static_cast<const float *>(P.data) + row * P.ld;
+    float *c = static_cast<float *>(Cv) + (int64_t)j * d;
+    for (int i = threadIdx.x; i < d; i += 256) c[i] = x[i];
+  } else if (FMT == KM_SQ8) {
+    const uint8_t *x = static_cast<const uint8_t *>(P.data) + row * P.ld;
+    uint8_t *c = static_cast<uint8_t *>(Cv) + (int64_t)j * d;
+    for (int i = threadIdx.x; i < d; i += 256) c[i] = x[i];
+  } else {
+    const int d0 = FMT == KM_HYBRID ? P.d_front : 0;
+    const uint32_t *b = static_cast<const uint32_t *>(P.data) + row * (d / 32);
+    const float a = P.alpha[row];
+    float *c = static_cast<float *>(Cv) + (int64_t)j * d;
+    for (int i = threadIdx.x; i < d; i += 256) {
+      if (i < d0) {
+        c[i] = P.front[row * d0 + i];
+      } else {
+        const float sg = ((b[i >> 5] >> (i & 31)) & 1u) ? a : -a;
+        c[i] = P.center[i] + sg;  // decoded point m + alpha (2b - 1)
+      }
+    }
+  }
+}
+
+// ---- full-precision cost of a partition: sum ||x - c_a||^2 in fp64 ----------
+__global__ __launch_bounds__(256) void cost_kernel(const float *X, int64_t n, int d, int64_t ldx, const float *C,
+                                                   int k, const int32_t *assign, double *partials) {
+  __shared__ double sh[256];
+  const int lane = threadIdx.x & 63;
+  const int wv = threadIdx.x >> 6;
+  double s = 0.0;
+  const int64_t stride = (int64_t)gridDim.x * 4;
+  for (int64_t p = (int64_t)blockIdx.x * 4 + wv; p < n; p += stride) {
+    const int a = assign[p];
+    if (a < 0 || a >= k) continue;
+    const float *x = X + p * ldx;
+    const float *c = C + (int64_t)a * d;
+    for (int i = lane; i < d; i += 64) {
+      const double e = (double)x[i] - (double)c[i];
+      s += e * e;
+    }
+  }
+  s = block_sum_f64(s, sh);
+  if (threadIdx.x == 0) partials[blockIdx.x] = s;
+}
+
+constexpr int kObjBlocks = 1024;
+
+template <int FMT>
+km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp, int k, int32_t *assign,
+                          float *score, hipStream_t s) {
+  AssignArgs A{};
+  A.n = P.n;
+  A.k = k;
+  A.assign = assign;
+  A.score = score;
+  A.cp = cp;
+  A.alpha = P.alpha;
+  if (FMT == KM_F32) {
+    A.pf = static_cast<const float *>(P.data);
+    A.pfld = P.ld;
+    A.cf = static_cast<const float *>(C);
+    A.cfld = P.d;
+    A.df = P.d;
+  } else if (FMT == KM_SQ8) {
+    A.pi8 = static_cast<const uint8_t *>(P.data);
+    A.pild = P.ld;
+    A.ci8 = static_cast<const int8_t *>(C);
+    A.cild = P.d;
+    A.di = P.d;
+  } else {
+    const int d0 = FMT == KM_HYBRID ? P.d_front : 0;
+    if (FMT == KM_HYBRID) {
+      A.pf = P.front;
+      A.pfld = d0;
+      A.cf = static_cast<const float *>(C);
+      A.cfld = P.d;
+      A.df = d0;
+    }
+    A.pbits = static_cast<const uint32_t *>(P.data);
+    A.pbw = P.d / 32;
+    A.pbw0 = d0 / 32;
+    A.ci8 = cp.q;
+    A.cild = P.d - d0;
+    A.di = P.d - d0;
+  }
+  const int64_t nblk = cdiv(P.n, kTile);
+  hipLaunchKernelGGL(assign_kernel<FMT>, dim3((unsigned)nblk), dim3(kThreads), 0, s, A);
+  KMQ_LAUNCH_CHECK("assign_kernel");
+  return KM_OK;
+}
+
+}  // namespace
+
+size_t prep_bytes(const Points &P, int k) {
+  const int d0 = P.fmt == KM_HYBRID ? P.d_front : 0;
+  size_t b = 4 * (size_t)k * sizeof(float) + 256;
+  if (P.fmt == KM_SIGN1 || P.fmt == KM_HYBRID) b += (size_t)k * (size_t)(P.d - d0) + 256;
+  return b;
+}
+
+km_status launch_prep(const Points &P, const void *C, int k, void *ws, CentroidPrep *out, hipStream_t s) {
+  uint8_t *w = static_cast<uint8_t *>(ws);
+  float *cn = reinterpret_cast<float *>(w);
+  int *qsum = reinterpret_cast<int *>(w + (size_t)k * 4);
+  float *u = reinterpret_cast<float *>(w + (size_t)k * 8);
+  float *sig2 = reinterpret_cast<float *>(w + (size_t)k * 12);
+  int8_t *q = reinterpret_cast<int8_t *>(w + (((size_t)k * 16 + 255) & ~(size_t)255));
+  out->cn = cn;
+  out->qsum = qsum;
+  out->u = u;
+  out->sig2 = sig2;
+  out->q = q;
+  const int d0 = P.fmt == KM_HYBRID ? P.d_front : 0;
+  switch (P.fmt) {
+    case KM_F32:
+      hipLaunchKernelGGL(prep_kernel<KM_F32>, dim3(k), dim3(256), 0, s, C, k, P.d, 0, nullptr, cn, qsum, u, sig2, q);
+      break;
+    case KM_SQ8:
+      hipLaunchKernelGGL(prep_kernel<KM_SQ8>, dim3(k), dim3(256), 0, s, C, k, P.d, 0, nullptr, cn, qsum, u, sig2, q);
+      break;
+    case KM_SIGN1:
+      hipLaunchKernelGGL(prep_kernel<KM_SIGN1>, dim3(k), dim3(256), 0, s, C, k, P.d, 0, P.center, cn, qsum, u, sig2,
+                         q);
+      break;
+    case KM_HYBRID:
+      hipLaunchKernelGGL(prep_kernel<KM_HYBRID>, dim3(k), dim3(256), 0, s, C, k, P.d, d0, P.center, cn, qsum, u,
+                         sig2, q);
+      break;
+    default:
+      return KM_EUNSUPPORTED;
+  }
+  KMQ_LAUNCH_CHECK("prep_kernel");
+  return KM_OK;
+}
+
+km_status launch_assign(const Points &P, const void *C, const CentroidPrep &cp, int k, int32_t *assign,
+                        float *score, hipStream_t s) {
+  switch (P.fmt) {
+    case KM_F32: return launch_assign_t<KM_F32>(P, C, cp, k, assign, score, s);
+    case KM_SQ8: return launch_assign_t<KM_SQ8>(P, C, cp, k, assign, score, s);
+    case KM_SIGN1: return launch_assign_t<KM_SIGN1>(P, C, cp, k, assign, score, s);
+    case KM_HYBRID: return launch_assign_t<KM_HYBRID>(P, C, cp, k, assign, score, s);
+    default: return KM_EUNSUPPORTED;
+  }
+}
+
+km_status launch_xconst(const Points &P, float *xc, hipStream_t s) {
+  const dim3 g((unsigned)cdiv(P.n, 4));
+  switch (P.fmt) {
+    case KM_F32: hipLaunchKernelGGL(xconst_kernel<KM_F32>, g, dim3(256), 0, s, P, xc); break;
+    case KM_SQ8: hipLaunchKernelGGL(xconst_kernel<KM_SQ8>, g, dim3(256), 0, s, P, xc); break;
+    case KM_SIGN1: hipLaunchKernelGGL(xconst_kernel<KM_SIGN1>, g, dim3(256), 0, s, P, xc); break;
+    case KM_HYBRID: hipLaunchKernelGGL(xconst_kernel<KM_HYBRID>, g, dim3(256), 0, s, P, xc); break;
+    default: return KM_EUNSUPPORTED;
+  }
+  KMQ_LAUNCH_CHECK("xconst_kernel");
+  return KM_OK;
+}
+
+int objective_blocks(int64_t n) { return (int)std::min<int64_t>(kObjBlocks, std::max<int64_t>(1, cdiv(n, 256))); }
+
+km_status launch_objective(const Points &P, const float *xc, const float *score, int64_t n, double *out,
+                           double *partials, int nblk_max, hipStream_t s) {
+  (void)P;
+  const int nb = std::min(nblk_max, objective_blocks(n));
+  hipLaunchKernelGGL(objective_partial_kernel, dim3(nb), dim3(256), 0, s, xc, score, n, partials);
+  hipLaunchKernelGGL(sum_partials_kernel, dim3(1), dim3(256), 0, s, partials, nb, out);
+  KMQ_LAUNCH_CHECK("objective");
+  return KM_OK;
+}
+
+km_status launch_gather_init(const Points &P, const int64_t *idx, int k, void *C, hipStream_t s) {
+  switch (P.fmt) {
+    case KM_F32: hipLaunchKernelGGL(gather_kernel<KM_F32>, dim3(k), dim3(256), 0, s, P, idx, C); break;
+    case KM_SQ8: hipLaunchKernelGGL(gather_kernel<KM_SQ8>, dim3(k), dim3(256), 0, s, P, idx, C); break;
+    case KM_SIGN1: hipLaunchKernelGGL(gather_kernel<KM_SIGN1>, dim3(k), dim3(256), 0, s, P, idx, C); break;
+    case KM_HYBRID: hipLaunchKernelGGL(gather_kernel<KM_HYBRID>, dim3(k), dim3(256), 0, s, P, idx, C); break;
+    default: return KM_EUNSUPPORTED;
+  }
+  KMQ_LAUNCH_CHECK("gather_kernel");
+  return KM_OK;
+}
+
+km_status launch_cost(const float *X, int64_t n, int d, int64_t ldx, const float *C, int k, const int32_t *assign,
+                      double *out, double *partials, hipStream_t s) {
+  const int nb = (int)std::min<int64_t>(kObjBlocks, std::max<int64_t>(1, cdiv(n, 4)));
+  hipLaunchKernelGGL(cost_kernel, dim3(nb), dim3(256), 0, s, X, n, d, ldx, C, k, assign, partials);
+  hipLaunchKernelGGL(sum_partials_kernel, dim3(1), dim3(256), 0, s, partials, nb, out);
+  KMQ_LAUNCH_CHECK("cost_kernel");
+  return KM_OK;
+}
+
+}  // namespace kmq

@@ -1,0 +1,117 @@
+// Internal helpers shared by the HIP sources of libkmq (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+
+#include "../../include/kmq.h"
+
+namespace kmq {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int kWave = 64;
+
+// Launch-facing description of the points (validated copy of km_points).
+struct Points {
+  int fmt;
+  int d;          // logical dims
+  int64_t n;
+  const void *data;
+  int64_t ld;     // F32: floats, SQ8: bytes, 1-bit: words (= d/32)
+  const float *alpha;
+  const float *center;
+  const float *front;  // hybrid: n x d_front
+  int d_front;
+};
+
+// Per-centroid data rebuilt before each assignment pass.
+struct CentroidPrep {
+  const float *cn;     // F32/HYBRID: ||c'||^2 over the fp32 dims
+  const int *qsum;     // SQ8: ||c~||^2 ; SIGN1/HYBRID: T_j = sum q
+  const float *u;      // SIGN1/HYBRID: (sigma*sigma)*Q
+  const float *sig2;   // SIGN1/HYBRID: 2*sigma
+  const int8_t *q;     // SIGN1/HYBRID: int8 residual codes, k x dt
+};
+
+// Host-side error plumbing.
+void set_error(const char *fmt, ...);
+km_status hip_fail(hipError_t e, const char *what);
+
+#define KMQ_HIP(call)                                         \
+  do {                                                        \
+    hipError_t _e = (call);                                   \
+    if (_e != hipSuccess) return ::kmq::hip_fail(_e, #call);  \
+  } while (0)
+
+#define KMQ_LAUNCH_CHECK(what)                                \
+  do {                                                        \
+    hipError_t _e = hipGetLastError();                        \
+    if (_e != hipSuccess) return ::kmq::hip_fail(_e, what);   \
+  } while (0)
+
+__host__ __device__ static inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// ---- launchers implemented in the kernel sources ---------------------------
+
+// assign.hip
+km_status launch_prep(const Points &P, const void *C, int k, void *ws_prep, CentroidPrep *out,
+                      hipStream_t s);
+size_t prep_bytes(const Points &P, int k);
+km_status launch_assign(const Points &P, const void *C, const CentroidPrep &cp, int k, int32_t *assign,
+                        float *score, hipStream_t s);
+km_status launch_xconst(const Points &P, float *xc, hipStream_t s);
+km_status launch_objective(const Points &P, const float *xc, const float *score, int64_t n, double *out,
+                           double *partials, int nblk_max, hipStream_t s);
+int objective_blocks(int64_t n);
+km_status launch_gather_init(const Points &P, const int64_t *idx, int k, void *C, hipStream_t s);
+km_status launch_cost(const float *X, int64_t n, int d, int64_t ldx, const float *C, int k,
+                      const int32_t *assign, double *out, double *partials, hipStream_t s);
+
+// update.hip
+size_t update_bytes(const Points &P, int k);
+km_status launch_update(const Points &P, const int32_t *assign, int k, void *C, int64_t *counts,
+                        int policy, void *ws, hipStream_t s);
+
+// quantize.hip
+size_t quantize_bytes(int64_t n, int d, int fmt);
+km_status launch_quantize(const float *X, int64_t n, int d, int64_t ldx, int fmt, void *codes,
+                          float *params, float *alpha, int d_front, float *front, int flags, void *ws,
+                          hipStream_t s);
+
+size_t colmean_bytes(int64_t n, int d);
+km_status launch_colmean(const float *X, int64_t n, int d, int64_t ldx, float *m, void *ws, hipStream_t s);
+
+// pca.hip
+size_t pca_cov_bytes(int64_t n, int d);
+km_status launch_pca_cov(const float *X, int64_t n, int d, float *mean, float *cov, void *ws,
+                         hipStream_t s);
+km_status launch_pca_project(const float *X, int64_t n, int d, const float *mean, const float *W,
+                             int d_out, float *Y, void *ws, hipStream_t s);
+size_t pca_project_bytes(int d, int d_out);
+
+// ---- device helpers ---------------------------------------------------------
+
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+// Deterministic block-wide sum of doubles (fixed tree order). blockDim.x == 256.
+__device__ __forceinline__ double block_sum_f64(double v, double *sh) {
+  const int t = threadIdx.x;
+  sh[t] = v;
+  __syncthreads();
+#pragma unroll
+  for (int s = 128; s > 0; s >>= 1) {
+    if (t < s) sh[t] += sh[t + s];
+    __syncthreads();
+  }
+  double r = sh[0];
+  __syncthreads();
+  return r;
+}
+
+}  // namespace kmq

@@ -1,0 +1,191 @@
+// Compression before clustering (Sec. 3.1): SQ8 with per-dimension (lo, hi) and
+// 1-bit sign codes around the dataset mean with a per-vector scale.
+//
+// Column statistics (min/max, fp64 sums) are two-level reductions: 256-thread
+// blocks own a run of rows and read them as coalesced float4 rows, writing one
+// partial per column; a second kernel folds the partials in block order.
+// SQ8 encode: one thread per 16 codes (4 float4 loads, one 16-byte store).
+// 1-bit encode: one wave per row, one dim per lane; a wave ballot of (x - m > 0)
+// is directly two 32-bit code words (bit i of the vector = lane i % 32 of word
+// i / 32), and the fp64 sums of r^2 and |r| give alpha.
+#include <algorithm>
+
+#include "common.hpp"
+
+namespace kmq {
+namespace {
+
+constexpr int kRowsPerBlock = 1024;
+
+__global__ __launch_bounds__(256) void colminmax_partial_kernel(const float *X, int64_t n, int d, int64_t ldx,
+                                                                float *pmin, float *pmax) {
+  const int64_t r0 = (int64_t)blockIdx.x * kRowsPerBlock;
+  const int64_t r1 = min<int64_t>(n, r0 + kRowsPerBlock);
+  for (int g = threadIdx.x; g < d / 4; g += 256) {
+    f32x4 mn = *reinterpret_cast<const f32x4 *>(X + r0 * ldx + 4 * g);
+    f32x4 mx = mn;
+    for (int64_t r = r0 + 1; r < r1; ++r) {
+      const f32x4 v = *reinterpret_cast<const f32x4 *>(X + r * ldx + 4 * g);
+      mn.x = fminf(mn.x, v.x); mn.y = fminf(mn.y, v.y); mn.z = fminf(mn.z, v.z); mn.w = fminf(mn.w, v.w);
+      mx.x = fmaxf(mx.x, v.x); mx.y = fmaxf(mx.y, v.y); mx.z = fmaxf(mx.z, v.z); mx.w = fmaxf(mx.w, v.w);
+    }
+    *reinterpret_cast<f32x4 *>(pmin + (int64_t)blockIdx.x * d + 4 * g) = mn;
+    *reinterpret_cast<f32x4 *>(pmax + (int64_t)blockIdx.x * d + 4 * g) = mx;
+  }
+}
+
+__global__ void colminmax_final_kernel(const float *pmin, const float *pmax, int nb, int d, float *lo, float *hi) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= d) return;
+  float mn = pmin[i], mx = pmax[i];
+  for (int b = 1; b < nb; ++b) {
+    mn = fminf(mn, pmin[(int64_t)b * d + i]);
+    mx = fmaxf(mx, pmax[(int64_t)b * d + i]);
+  }
+  lo[i] = mn;
+  hi[i] = mx;
+}
+
+__global__ __launch_bounds__(256) void colsum_partial_kernel(const float *X, int64_t n, int d, int64_t ldx,
+                                                             double *psum) {
+  const int64_t r0 = (int64_t)blockIdx.x * kRowsPerBlock;
+  const int64_t r1 = min<int64_t>(n, r0 + kRowsPerBlock);
+  for (int g = threadIdx.x; g < d / 4; g += 256) {
+    double s0 = 0, s1 = 0, s2 = 0, s3 = 0;
+    for (int64_t r = r0; r < r1; ++r) {
+      const f32x4 v = *reinterpret_cast<const f32x4 *>(X + r * ldx + 4 * g);
+      s0 += v.x; s1 += v.y; s2 += v.z; s3 += v.w;
+    }
+    double *o = psum + (int64_t)blockIdx.x * d + 4 * g;
+    o[0] = s0; o[1] = s1; o[2] = s2; o[3] = s3;
+  }
+}
+
+__global__ void colmean_final_kernel(const double *psum, int nb, int d, int64_t n, float *m) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= d) return;
+  double s = 0.0;
+  for (int b = 0; b < nb; ++b) s += psum[(int64_t)b * d + i];
+  m[i] = (float)(s / (double)n);
+}
+
+__global__ void sq8_inv_kernel(const float *lo, const float *hi, int d, float *inv) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= d) return;
+  const float range = hi[i] - lo[i];
+  inv[i] = range > 0.0f ? 255.0f / range : 0.0f;
+}
+
+__global__ __launch_bounds__(256) void sq8_encode_kernel(const float *X, int64_t n, int d, int64_t ldx,
+                                                         const float *lo, const float *inv, uint8_t *codes) {
+  const int per = d / 16;
+  const int64_t total = n * per;
+  for (int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x; g < total; g += (int64_t)gridDim.x * 256) {
+    const int64_t r = g / per;
+    const int c = (int)(g - r * per) * 16;
+    const float *x = X + r * ldx + c;
+    uint32_t w[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const f32x4 v = *reinterpret_cast<const f32x4 *>(x + 4 * q);
+      uint32_t packed = 0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int i = c + 4 * q + e;
+        float t = rintf((v[e] - lo[i]) * inv[i]);
+        t = fminf(fmaxf(t, 0.0f), 255.0f);
+        packed |= (uint32_t)t << (8 * e);
+      }
+      w[q] = packed;
+    }
+    *reinterpret_cast<uint4 *>(codes + r * d + c) = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+}
+
+// one wave per row
+__global__ __launch_bounds__(256) void sign1_encode_kernel(const float *X, int64_t n, int d, int64_t ldx,
+                                                           const float *m, int d0, uint32_t *bits, float *alpha,
+                                                           float *front) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= n) return;
+  const float *x = X + row * ldx;
+  uint32_t *b = bits + row * (d / 32);
+  double s2 = 0.0, s1 = 0.0;
+  for (int base = 0; base < d; base += 64) {
+    const int i = base + lane;
+    const bool in = i < d;
+    const float xi = in ? x[i] : 0.0f;
+    const float r = in ? xi - m[i] : 0.0f;
+    const uint64_t mask = __ballot(in && r > 0.0f);
+    if (in && i >= d0) {
+      s2 += (double)r * (double)r;
+      s1 += fabs((double)r);
+    }
+    if (front && in && i < d0) front[row * d0 + i] = xi;
+    if (lane == 0) b[base >> 5] = (uint32_t)mask;
+    if (lane == 1 && base + 32 < d) b[(base >> 5) + 1] = (uint32_t)(mask >> 32);
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    s2 += __shfl_xor(s2, off);
+    s1 += __shfl_xor(s1, off);
+  }
+  if (lane == 0) alpha[row] = s1 > 0.0 ? (float)(s2 / s1) : 0.0f;
+}
+
+}  // namespace
+
+size_t colmean_bytes(int64_t n, int d) { return (size_t)cdiv(n, kRowsPerBlock) * d * sizeof(double) + 256; }
+
+km_status launch_colmean(const float *X, int64_t n, int d, int64_t ldx, float *m, void *ws, hipStream_t s) {
+  const int nb = (int)cdiv(n, kRowsPerBlock);
+  double *psum = static_cast<double *>(ws);
+  hipLaunchKernelGGL(colsum_partial_kernel, dim3(nb), dim3(256), 0, s, X, n, d, ldx, psum);
+  hipLaunchKernelGGL(colmean_final_kernel, dim3((unsigned)cdiv(d, 256)), dim3(256), 0, s, psum, nb, d, n, m);
+  KMQ_LAUNCH_CHECK("column mean");
+  return KM_OK;
+}
+
+size_t quantize_bytes(int64_t n, int d, int fmt) {
+  const int64_t nb = cdiv(n, kRowsPerBlock);
+  if (fmt == KM_SQ8) return (size_t)nb * d * 2 * sizeof(float) + (size_t)d * sizeof(float) + 512;
+  return (size_t)nb * d * sizeof(double) + 256;
+}
+
+km_status launch_quantize(const float *X, int64_t n, int d, int64_t ldx, int fmt, void *codes, float *params,
+                          float *alpha, int d_front, float *front, int flags, void *ws, hipStream_t s) {
+  const int nb = (int)cdiv(n, kRowsPerBlock);
+  const dim3 gd((unsigned)cdiv(d, 256));
+  if (fmt == KM_SQ8) {
+    float *lo = params, *hi = params + d;
+    float *pmin = static_cast<float *>(ws);
+    float *pmax = pmin + (size_t)nb * d;
+    float *inv = pmax + (size_t)nb * d;
+    if (flags & KM_Q_FIT_PARAMS) {
+      hipLaunchKernelGGL(colminmax_partial_kernel, dim3(nb), dim3(256), 0, s, X, n, d, ldx, pmin, pmax);
+      hipLaunchKernelGGL(colminmax_final_kernel, gd, dim3(256), 0, s, pmin, pmax, nb, d, lo, hi);
+    }
+    hipLaunchKernelGGL(sq8_inv_kernel, gd, dim3(256), 0, s, lo, hi, d, inv);
+    const int64_t work = n * (d / 16);
+    const unsigned g = (unsigned)std::min<int64_t>(cdiv(work, 256), 65536);
+    hipLaunchKernelGGL(sq8_encode_kernel, dim3(g), dim3(256), 0, s, X, n, d, ldx, lo, inv,
+                       static_cast<uint8_t *>(codes));
+    KMQ_LAUNCH_CHECK("quantize sq8");
+    return KM_OK;
+  }
+  if (fmt == KM_SIGN1) {
+    float *m = params;
+    if (flags & KM_Q_FIT_PARAMS) {
+      km_status st = launch_colmean(X, n, d, ldx, m, ws, s);
+      if (st != KM_OK) return st;
+    }
+    hipLaunchKernelGGL(sign1_encode_kernel, dim3((unsigned)cdiv(n, 4)), dim3(256), 0, s, X, n, d, ldx, m, d_front,
+                       static_cast<uint32_t *>(codes), alpha, d_front > 0 ? front : nullptr);
+    KMQ_LAUNCH_CHECK("quantize sign1");
+    return KM_OK;
+  }
+  return KM_EUNSUPPORTED;
+}
+
+}  // namespace kmq

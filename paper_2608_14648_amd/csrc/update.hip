@@ -1,0 +1,562 @@
+// STEP 3 (Sec. 2.3): centroid update as a deterministic segmented sum.
+//
+//   1. hist     per block of 4096 points, member counts of every cluster
+//               (LDS-privatised histogram), stored cluster-major [k][nblk].
+//   2. scan     exclusive scan of that table: entry (j, b) is where block b's
+//               first member of cluster j goes in the cluster-sorted order.
+//   3. scatter  stable counting sort: points are ranked inside each wave by a
+//               match loop over equal cluster ids and the four waves take
+//               their slots in order, so members stay in point order.
+//   4. segsum   fixed-size chunks (<= 512 members, never crossing a cluster)
+//               are summed by one workgroup per (chunk, column slice): each
+//               wave adds every 4th member's slice of the row (coalesced
+//               1 KiB reads of fp32 rows, 256 B of codes, 128 B of bits); the
+//               four wave sums are combined in LDS in a fixed order.
+//               1-bit members are decoded on the fly: alpha_x (2b - 1) (fused
+//               decode-averaging, Sec. 3.1 RabitQ); SQ8 codes are summed as
+//               exact integers (averaging in the quantised domain, Sec. 3.1).
+//   5. finalize per cluster, chunk sums in chunk order in fp64, divided by
+//               the count: fp32 mean / 1-bit residual mean / rounded code mean.
+//   6. split    empty clusters in ascending order take a split of the cluster
+//               with the largest current count (one workgroup, sequential).
+//   7. compose  write the new centroids (1-bit dims: m + residual).
+// Every sum has a fixed order, so results are bit-identical run to run.
+#include <algorithm>
+
+#include "common.hpp"
+
+namespace kmq {
+namespace {
+
+constexpr int kHistPts = 4096;     // points per histogram / scatter block
+constexpr int kChunk = 512;        // members per segmented-sum chunk
+constexpr int kLdsCursorMax = 16384;
+constexpr int kScanSeg = 4096;     // elements per scan block (256 threads x 16)
+
+struct UpdWs {
+  int nblk;      // histogram blocks
+  int64_t L;     // k * nblk
+  int nsb;       // scan blocks
+  int maxchunks;
+  int dp;        // row length of partial sums / Z (F32: d, SQ8: d, SIGN1/HYBRID: d)
+  int *offs;     // [L]
+  int *bsum;     // [nsb + 1]
+  int *total;    // [4]
+  int *cnt;      // [k]
+  int *cstart;   // [k]
+  int *choff;    // [k + 1]
+  int *perm;     // [n]
+  void *partial; // [maxchunks * dp] float or int
+  void *Z;       // [k * dp] float or uint8
+  uint8_t *fresh;  // [k]
+  int64_t *cntw;   // [k]
+};
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+UpdWs carve(const Points &P, int k, void *base, size_t *bytes_out) {
+  UpdWs w{};
+  w.nblk = (int)cdiv(P.n, kHistPts);
+  w.L = (int64_t)k * w.nblk;
+  w.nsb = (int)cdiv(w.L, kScanSeg);
+  w.maxchunks = (int)(cdiv(P.n, kChunk) + k);
+  w.dp = P.d;
+  uint8_t *b = static_cast<uint8_t *>(base);
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    void *p = b ? b + o : nullptr;
+    o += align256(bytes);
+    return p;
+  };
+  w.offs = (int *)take(sizeof(int) * (size_t)w.L);
+  w.bsum = (int *)take(sizeof(int) * (size_t)(w.nsb + 1));
+  w.total = (int *)take(sizeof(int) * 4);
+  w.cnt = (int *)take(sizeof(int) * (size_t)k);
+  w.cstart = (int *)take(sizeof(int) * (size_t)k);
+  w.choff = (int *)take(sizeof(int) * (size_t)(k + 1));
+  w.perm = (int *)take(sizeof(int) * (size_t)P.n);
+  w.partial = take(sizeof(float) * (size_t)w.maxchunks * (size_t)w.dp);
+  w.Z = take(sizeof(float) * (size_t)k * (size_t)w.dp);
+  w.fresh = (uint8_t *)take((size_t)k);
+  w.cntw = (int64_t *)take(sizeof(int64_t) * (size_t)k);
+  if (bytes_out) *bytes_out = o;
+  return w;
+}
+
+// ---- 1. histogram ------------------------------------------------------------
+__global__ __launch_bounds__(256) void hist_kernel(const int32_t *assign, int64_t n, int k, int nblk, int *offs,
+                                                   int use_lds) {
+  extern __shared__ int lc[];
+  const int b = blockIdx.x, t = threadIdx.x;
+  const int64_t lo = (int64_t)b * kHistPts;
+  const int64_t hi = min<int64_t>(n, lo + kHistPts);
+  if (use_lds) {
+    for (int j = t; j < k; j += 256) lc[j] = 0;
+    __syncthreads();
+    for (int64_t p = lo + t; p < hi; p += 256) {
+      const int a = assign[p];
+      if (a >= 0 && a < k) atomicAdd(&lc[a], 1);
+    }
+    __syncthreads();
+    for (int j = t; j < k; j += 256) offs[(int64_t)j * nblk + b] = lc[j];
+  } else {
+    for (int64_t p = lo + t; p < hi; p += 256) {
+      const int a = assign[p];
+      if (a >= 0 && a < k) atomicAdd(&offs[(int64_t)a * nblk + b], 1);
+    }
+  }
+}
+
+__global__ void fill_int_kernel(int *p, int64_t n, int v) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) p[i] = v;
+}
+
+// ---- 2. scan -----------------------------------------------------------------
+__device__ __forceinline__ int block_excl_scan_int(int v, int *sh, int *total) {
+  // Hillis-Steele inclusive scan over 256 thread values, returned exclusive.
+  const int t = threadIdx.x;
+  sh[t] = v;
+  __syncthreads();
+  for (int off = 1; off < 256; off <<= 1) {
+    int add = t >= off ? sh[t - off] : 0;
+    __syncthreads();
+    sh[t] += add;
+    __syncthreads();
+  }
+  const int incl = sh[t];
+  if (total) *total = sh[255];
+  __syncthreads();
+  return incl - v;
+}
+
+__global__ __launch_bounds__(256) void scan_reduce_kernel(const int *x, int64_t L, int *bsum) {
+  __shared__ int sh[256];
+  const int64_t base = (int64_t)blockIdx.x * kScanSeg;
+  int s = 0;
+  for (int i = threadIdx.x; i < kScanSeg; i += 256) {
+    const int64_t g = base + i;
+    if (g < L) s += x[g];
+  }
+  sh[threadIdx.x] = s;
+  __syncthreads();
+  for (int st = 128; st > 0; st >>= 1) {
+    if (threadIdx.x < st) sh[threadIdx.x] += sh[threadIdx.x + st];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) bsum[blockIdx.x] = sh[0];
+}
+
+// Single-workgroup exclusive scan of n ints in place (each thread a contiguous run).
+// mode 1 scans ceil(x / kChunk) instead of x.  *total receives the grand total.
+__global__ __launch_bounds__(256) void scan_single_kernel(const int *in, int *out, int n, int *total, int mode) {
+  __shared__ int sh[256];
+  const int t = threadIdx.x;
+  const int per = (n + 255) / 256;
+  const int lo = min(n, t * per), hi = min(n, lo + per);
+  int s = 0;
+  for (int i = lo; i < hi; ++i) s += mode ? (in[i] + kChunk - 1) / kChunk : in[i];
+  int tot;
+  int run = block_excl_scan_int(s, sh, &tot);
+  for (int i = lo; i < hi; ++i) {
+    const int v = mode ? (in[i] + kChunk - 1) / kChunk : in[i];
+    out[i] = run;
+    run += v;
+  }
+  if (t == 0 && total) *total = tot;
+}
+
+__global__ __launch_bounds__(256) void scan_down_kernel(int *x, int64_t L, const int *bsum) {
+  __shared__ int sh[256];
+  const int64_t base = (int64_t)blockIdx.x * kScanSeg + (int64_t)threadIdx.x * 16;
+  int v[16];
+  int s = 0;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    v[e] = base + e < L ? x[base + e] : 0;
+    s += v[e];
+  }
+  int run = block_excl_scan_int(s, sh, nullptr) + bsum[blockIdx.x];
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    if (base + e < L) x[base + e] = run;
+    run += v[e];
+  }
+}
+
+// counts and start offsets of each cluster from the scanned table
+__global__ void counts_kernel(const int *offs, int nblk, int k, const int *total, int *cnt, int *cstart) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= k) return;
+  const int s = offs[(int64_t)j * nblk];
+  const int e = j + 1 < k ? offs[(int64_t)(j + 1) * nblk] : total[0];
+  cnt[j] = e - s;
+  cstart[j] = s;
+}
+
+// ---- 3. stable scatter -------------------------------------------------------
+__global__ __launch_bounds__(256) void scatter_kernel(const int32_t *assign, int64_t n, int k, int nblk, int *offs,
+                                                      int use_lds, int *perm) {
+  extern __shared__ int cur[];
+  const int b = blockIdx.x, t = threadIdx.x;
+  const int lane = t & 63, wave = t >> 6;
+  const int64_t lo = (int64_t)b * kHistPts;
+  const int64_t hi = min<int64_t>(n, lo + kHistPts);
+  if (use_lds) {
+    for (int j = t; j < k; j += 256) cur[j] = offs[(int64_t)j * nblk + b];
+    __syncthreads();
+  }
+  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int64_t base = lo; base < hi; base += 256) {
+    const int64_t p = base + t;
+    int a = p < hi ? assign[p] : -1;
+    const bool valid = a >= 0 && a < k;
+    // rank among equal ids in this wave (lanes below), group size, group leader
+    int rank = 0, cnt = 0, leader = 0;
+    uint64_t todo = __ballot(valid);
+    while (todo) {
+      const int ld = __ffsll((unsigned long long)todo) - 1;
+      const int v = __shfl(a, ld);
+      const bool mine = valid && a == v;
+      const uint64_t m = __ballot(mine);
+      if (mine) {
+        rank = __popcll(m & lt_mask);
+        cnt = __popcll(m);
+        leader = ld;
+      }
+      todo &= ~m;
+    }
+    for (int w = 0; w < 4; ++w) {
+      __syncthreads();
+      if (wave == w) {
+        int old = 0;
+        if (valid && lane == leader) {
+          old = use_lds ? atomicAdd(&cur[a], cnt) : atomicAdd(&offs[(int64_t)a * nblk + b], cnt);
+        }
+        const int basepos = __shfl(old, leader);
+        if (valid) perm[basepos + rank] = (int)p;
+      }
+    }
+  }
+}
+
+// ---- 4. chunked segmented sums ----------------------------------------------
+__device__ __forceinline__ int find_cluster(const int *choff, int k, int c) {
+  // largest j with choff[j] <= c (clusters with no chunks have equal neighbours)
+  int lo = 0, hi = k;  // invariant: choff[lo] <= c < choff[hi]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (choff[mid] <= c) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
+// fp32 rows: one slice of 256 columns per workgroup
+__global__ __launch_bounds__(256) void segsum_f32_kernel(const float *X, int64_t ld, int df, const int *perm,
+                                                         const int *cnt, const int *cstart, const int *choff, int k,
+                                                         float *partial, int dp) {
+  __shared__ f32x4 red[4][64];
+  const int c = blockIdx.x;
+  if (c >= choff[k]) return;
+  const int j = find_cluster(choff, k, c);
+  const int ci = c - choff[j];
+  const int m0 = cstart[j] + ci * kChunk;
+  const int m1 = cstart[j] + min(cnt[j], (ci + 1) * kChunk);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int col = blockIdx.y * 256 + 4 * lane;
+  const bool ok = col < df;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  int m = m0 + wave;
+  for (; m + 12 < m1; m += 16) {
+    const int p0 = perm[m], p1 = perm[m + 4], p2 = perm[m + 8], p3 = perm[m + 12];
+    if (ok) {
+      const f32x4 v0 = *reinterpret_cast<const f32x4 *>(X + (int64_t)p0 * ld + col);
+      const f32x4 v1 = *reinterpret_cast<const f32x4 *>(X + (int64_t)p1 * ld + col);
+      const f32x4 v2 = *reinterpret_cast<const f32x4 *>(X + (int64_t)p2 * ld + col);
+      const f32x4 v3 = *reinterpret_cast<const f32x4 *>(X + (int64_t)p3 * ld + col);
+      acc += v0;
+      acc += v1;
+      acc += v2;
+      acc += v3;
+    }
+  }
+  for (; m < m1; m += 4) {
+    const int p = perm[m];
+    if (ok) acc += *reinterpret_cast<const f32x4 *>(X + (int64_t)p * ld + col);
+  }
+  red[wave][lane] = acc;
+  __syncthreads();
+  if (wave == 0 && ok) {
+    f32x4 s = red[0][lane];
+    s += red[1][lane];
+    s += red[2][lane];
+    s += red[3][lane];
+    *reinterpret_cast<f32x4 *>(partial + (int64_t)c * dp + col) = s;
+  }
+}
+
+// 1-bit rows: one slice of 1024 tail dims per workgroup; lane = 16 dims (half a word)
+__global__ __launch_bounds__(256) void segsum_bits_kernel(const uint32_t *bits, int64_t wpr, int w0, int dt,
+                                                          const float *alpha, const int *perm, const int *cnt,
+                                                          const int *cstart, const int *choff, int k,
+                                                          float *partial, int dp, int coff) {
+  __shared__ float red[4][64 * 17];
+  const int c = blockIdx.x;
+  if (c >= choff[k]) return;
+  const int j = find_cluster(choff, k, c);
+  const int ci = c - choff[j];
+  const int m0 = cstart[j] + ci * kChunk;
+  const int m1 = cstart[j] + min(cnt[j], (ci + 1) * kChunk);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int hw = blockIdx.y * 64 + lane;  // half-word index within the tail
+  const bool ok = 16 * hw < dt;
+  float acc[16];
+#pragma unroll
+  for (int e = 0; e < 16; ++e) acc[e] = 0.f;
+  for (int m = m0 + wave; m < m1; m += 4) {
+    const int p = perm[m];
+    const float a = alpha[p];
+    const uint32_t w = ok ? bits[(int64_t)p * wpr + w0 + (hw >> 1)] : 0u;
+    const uint32_t hb = w >> (16 * (hw & 1));
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[e] += ((hb >> e) & 1u) ? a : -a;
+  }
+#pragma unroll
+  for (int e = 0; e < 16; ++e) red[wave][lane * 17 + e] = acc[e];
+  __syncthreads();
+  if (wave == 0 && ok) {
+    float *out = partial + (int64_t)c * dp + coff + 16 * hw;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      float s = red[0][lane * 17 + e];
+      s += red[1][lane * 17 + e];
+      s += red[2][lane * 17 + e];
+      s += red[3][lane * 17 + e];
+      out[e] = s;
+    }
+  }
+}
+
+// SQ8 codes: one slice of 256 bytes per workgroup, exact int32 sums
+__global__ __launch_bounds__(256) void segsum_sq8_kernel(const uint8_t *codes, int64_t ld, int d, const int *perm,
+                                                         const int *cnt, const int *cstart, const int *choff, int k,
+                                                         int *partial) {
+  __shared__ int red[4][64 * 5];
+  const int c = blockIdx.x;
+  if (c >= choff[k]) return;
+  const int j = find_cluster(choff, k, c);
+  const int ci = c - choff[j];
+  const int m0 = cstart[j] + ci * kChunk;
+  const int m1 = cstart[j] + min(cnt[j], (ci + 1) * kChunk);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int col = blockIdx.y * 256 + 4 * lane;
+  const bool ok = col < d;
+  int acc[4] = {0, 0, 0, 0};
+  for (int m = m0 + wave; m < m1; m += 4) {
+    const int p = perm[m];
+    const uint32_t w = ok ? *reinterpret_cast<const uint32_t *>(codes + (int64_t)p * ld + col) : 0u;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc[e] += (int)((w >> (8 * e)) & 255u);
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) red[wave][lane * 5 + e] = acc[e];
+  __syncthreads();
+  if (wave == 0 && ok) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      partial[(int64_t)c * d + col + e] =
+          red[0][lane * 5 + e] + red[1][lane * 5 + e] + red[2][lane * 5 + e] + red[3][lane * 5 + e];
+  }
+}
+
+// ---- 5. finalize ---------------------------------------------------------------
+__global__ __launch_bounds__(256) void finalize_f32_kernel(const float *partial, int dp, const int *cnt,
+                                                           const int *choff, float *Z, uint8_t *fresh) {
+  const int j = blockIdx.x;
+  const int col = blockIdx.y * 256 + threadIdx.x;
+  const int nj = cnt[j];
+  if (blockIdx.y == 0 && threadIdx.x == 0) fresh[j] = nj > 0;
+  if (nj == 0 || col >= dp) return;
+  double s = 0.0;
+  for (int c = choff[j]; c < choff[j + 1]; ++c) s += (double)partial[(int64_t)c * dp + col];
+  Z[(int64_t)j * dp + col] = (float)(s / (double)nj);
+}
+
+__global__ __launch_bounds__(256) void finalize_sq8_kernel(const int *partial, int d, const int *cnt,
+                                                           const int *choff, uint8_t *Z, uint8_t *fresh) {
+  const int j = blockIdx.x;
+  const int col = blockIdx.y * 256 + threadIdx.x;
+  const int nj = cnt[j];
+  if (blockIdx.y == 0 && threadIdx.x == 0) fresh[j] = nj > 0;
+  if (nj == 0 || col >= d) return;
+  int64_t S = 0;
+  for (int c = choff[j]; c < choff[j + 1]; ++c) S += partial[(int64_t)c * d + col];
+  // mean of the codes rounded half up: floor((2S + n) / (2n))
+  Z[(int64_t)j * d + col] = (uint8_t)((2 * S + nj) / (2 * (int64_t)nj));
+}
+
+// ---- 6. empty-cluster split (one workgroup) -----------------------------------
+template <bool CODES>
+__global__ __launch_bounds__(256) void split_kernel(void *Zv, int k, int dp, const int *cnt, int64_t *cntw,
+                                                    uint8_t *fresh) {
+  __shared__ int64_t sv[256];
+  __shared__ int si[256];
+  const int t = threadIdx.x;
+  for (int j = t; j < k; j += 256) cntw[j] = cnt[j];
+  __syncthreads();
+  const float up = 1.0f + 0x1p-10f, dn = 1.0f - 0x1p-10f;
+  for (int j = 0; j < k; ++j) {
+    if (cnt[j] != 0) continue;  // uniform
+    int64_t bv = -1;
+    int bi = 0;
+    for (int i = t; i < k; i += 256) {
+      const int64_t v = cntw[i];
+      if (v > bv) {
+        bv = v;
+        bi = i;
+      }
+    }
+    sv[t] = bv;
+    si[t] = bi;
+    __syncthreads();
+    for (int st = 128; st > 0; st >>= 1) {
+      if (t < st) {
+        const int64_t ov = sv[t + st];
+        const int oi = si[t + st];
+        if (ov > sv[t] || (ov == sv[t] && oi < si[t])) {
+          sv[t] = ov;
+          si[t] = oi;
+        }
+      }
+      __syncthreads();
+    }
+    const int b = si[0];
+    const int64_t nb = sv[0];
+    __syncthreads();
+    if (nb < 2) continue;  // uniform
+    if (CODES) {
+      uint8_t *Z = static_cast<uint8_t *>(Zv);
+      for (int i = t; i < dp; i += 256) {
+        const int v = Z[(int64_t)b * dp + i];
+        const int p = (i & 1) ? -1 : 1;
+        Z[(int64_t)j * dp + i] = (uint8_t)min(255, max(0, v + p));
+        Z[(int64_t)b * dp + i] = (uint8_t)min(255, max(0, v - p));
+      }
+    } else {
+      float *Z = static_cast<float *>(Zv);
+      for (int i = t; i < dp; i += 256) {
+        const float v = Z[(int64_t)b * dp + i];
+        const bool even = (i & 1) == 0;
+        Z[(int64_t)j * dp + i] = v * (even ? up : dn);
+        Z[(int64_t)b * dp + i] = v * (even ? dn : up);
+      }
+    }
+    __syncthreads();
+    if (t == 0) {
+      const int64_t half = nb / 2;
+      cntw[j] = half;
+      cntw[b] = nb - half;
+      fresh[j] = 1;
+    }
+    __syncthreads();
+  }
+}
+
+// ---- 7. compose -----------------------------------------------------------------
+template <int FMT>
+__global__ __launch_bounds__(256) void compose_kernel(const void *Zv, int k, int d, int d0, const float *m,
+                                                      const uint8_t *fresh, const int *cnt, void *Cv,
+                                                      int64_t *counts) {
+  const int j = blockIdx.x;
+  const int col = blockIdx.y * 256 + threadIdx.x;
+  if (counts && blockIdx.y == 0 && threadIdx.x == 0) counts[j] = cnt[j];
+  if (!fresh[j] || col >= d) return;
+  if (FMT == KM_SQ8) {
+    static_cast<uint8_t *>(Cv)[(int64_t)j * d + col] = static_cast<const uint8_t *>(Zv)[(int64_t)j * d + col];
+  } else {
+    const float z = static_cast<const float *>(Zv)[(int64_t)j * d + col];
+    const bool bitdim = (FMT == KM_SIGN1 || FMT == KM_HYBRID) && col >= d0;
+    static_cast<float *>(Cv)[(int64_t)j * d + col] = bitdim ? m[col] + z : z;
+  }
+}
+
+}  // namespace
+
+size_t update_bytes(const Points &P, int k) {
+  size_t b = 0;
+  carve(P, k, nullptr, &b);
+  return b;
+}
+
+km_status launch_update(const Points &P, const int32_t *assign, int k, void *C, int64_t *counts, int policy,
+                        void *ws, hipStream_t s) {
+  UpdWs w = carve(P, k, ws, nullptr);
+  const bool lds = k <= kLdsCursorMax;
+  const size_t lds_bytes = lds ? sizeof(int) * (size_t)k : 0;
+  if (!lds) hipLaunchKernelGGL(fill_int_kernel, dim3(1024), dim3(256), 0, s, w.offs, w.L, 0);
+  hipLaunchKernelGGL(hist_kernel, dim3(w.nblk), dim3(256), lds_bytes, s, assign, P.n, k, w.nblk, w.offs, (int)lds);
+  hipLaunchKernelGGL(scan_reduce_kernel, dim3(w.nsb), dim3(256), 0, s, w.offs, w.L, w.bsum);
+  hipLaunchKernelGGL(scan_single_kernel, dim3(1), dim3(256), 0, s, w.bsum, w.bsum, w.nsb, w.total, 0);
+  hipLaunchKernelGGL(scan_down_kernel, dim3(w.nsb), dim3(256), 0, s, w.offs, w.L, w.bsum);
+  hipLaunchKernelGGL(counts_kernel, dim3((unsigned)cdiv(k, 256)), dim3(256), 0, s, w.offs, w.nblk, k, w.total, w.cnt,
+                     w.cstart);
+  hipLaunchKernelGGL(scan_single_kernel, dim3(1), dim3(256), 0, s, w.cnt, w.choff, k, w.choff + k, 1);
+  hipLaunchKernelGGL(scatter_kernel, dim3(w.nblk), dim3(256), lds_bytes, s, assign, P.n, k, w.nblk, w.offs, (int)lds,
+                     w.perm);
+  KMQ_LAUNCH_CHECK("update: sort");
+
+  const int d = P.d;
+  if (P.fmt == KM_SQ8) {
+    hipLaunchKernelGGL(segsum_sq8_kernel, dim3(w.maxchunks, (unsigned)cdiv(d, 256)), dim3(256), 0, s,
+                       static_cast<const uint8_t *>(P.data), P.ld, d, w.perm, w.cnt, w.cstart, w.choff, k,
+                       static_cast<int *>(w.partial));
+    hipLaunchKernelGGL(finalize_sq8_kernel, dim3(k, (unsigned)cdiv(d, 256)), dim3(256), 0, s,
+                       static_cast<const int *>(w.partial), d, w.cnt, w.choff, static_cast<uint8_t *>(w.Z), w.fresh);
+  } else {
+    int df = 0;
+    const float *F = nullptr;
+    int64_t fld = 0;
+    if (P.fmt == KM_F32) {
+      df = d;
+      F = static_cast<const float *>(P.data);
+      fld = P.ld;
+    } else if (P.fmt == KM_HYBRID) {
+      df = P.d_front;
+      F = P.front;
+      fld = P.d_front;
+    }
+    if (df > 0)
+      hipLaunchKernelGGL(segsum_f32_kernel, dim3(w.maxchunks, (unsigned)cdiv(df, 256)), dim3(256), 0, s, F, fld, df,
+                         w.perm, w.cnt, w.cstart, w.choff, k, static_cast<float *>(w.partial), w.dp);
+    if (P.fmt == KM_SIGN1 || P.fmt == KM_HYBRID) {
+      const int d0 = P.fmt == KM_HYBRID ? P.d_front : 0;
+      const int dt = d - d0;
+      hipLaunchKernelGGL(segsum_bits_kernel, dim3(w.maxchunks, (unsigned)cdiv(dt, 1024)), dim3(256), 0, s,
+                         static_cast<const uint32_t *>(P.data), (int64_t)(d / 32), d0 / 32, dt, P.alpha, w.perm,
+                         w.cnt, w.cstart, w.choff, k, static_cast<float *>(w.partial), w.dp, d0);
+    }
+    hipLaunchKernelGGL(finalize_f32_kernel, dim3(k, (unsigned)cdiv(w.dp, 256)), dim3(256), 0, s,
+                       static_cast<const float *>(w.partial), w.dp, w.cnt, w.choff, static_cast<float *>(w.Z),
+                       w.fresh);
+  }
+  KMQ_LAUNCH_CHECK("update: segmented sums");
+
+  if (policy == KM_EMPTY_SPLIT) {
+    if (P.fmt == KM_SQ8)
+      hipLaunchKernelGGL(split_kernel<true>, dim3(1), dim3(256), 0, s, w.Z, k, w.dp, w.cnt, w.cntw, w.fresh);
+    else
+      hipLaunchKernelGGL(split_kernel<false>, dim3(1), dim3(256), 0, s, w.Z, k, w.dp, w.cnt, w.cntw, w.fresh);
+  }
+  const dim3 g(k, (unsigned)cdiv(d, 256));
+  const int d0 = P.fmt == KM_HYBRID ? P.d_front : 0;
+  switch (P.fmt) {
+    case KM_F32: hipLaunchKernelGGL(compose_kernel<KM_F32>, g, dim3(256), 0, s, w.Z, k, d, d0, P.center, w.fresh, w.cnt, C, counts); break;
+    case KM_SQ8: hipLaunchKernelGGL(compose_kernel<KM_SQ8>, g, dim3(256), 0, s, w.Z, k, d, d0, P.center, w.fresh, w.cnt, C, counts); break;
+    case KM_SIGN1: hipLaunchKernelGGL(compose_kernel<KM_SIGN1>, g, dim3(256), 0, s, w.Z, k, d, d0, P.center, w.fresh, w.cnt, C, counts); break;
+    case KM_HYBRID: hipLaunchKernelGGL(compose_kernel<KM_HYBRID>, g, dim3(256), 0, s, w.Z, k, d, d0, P.center, w.fresh, w.cnt, C, counts); break;
+    default: return KM_EUNSUPPORTED;
+  }
+  KMQ_LAUNCH_CHECK("update: split/compose");
+  return KM_OK;
+}
+
+}  // namespace kmq

@@ -4,6 +4,6 @@ This package holds no arithmetic of the clustering method: it only draws points
 (Gaussian mixtures shaped like embedding collections), initial-centroid indices
 and the named workload configurations.
 """
-from .mixture import MixtureSpec, CONFIGS, make_points, make_chunk, init_indices, config
+from .mixture import CONFIGS, MixtureSpec, config, for_each_chunk, init_indices, make_chunk, make_points
 
-__all__ = ["MixtureSpec", "CONFIGS", "make_points", "make_chunk", "init_indices", "config"]
+__all__ = ["MixtureSpec", "CONFIGS", "make_points", "make_chunk", "for_each_chunk", "init_indices", "config"]

@@ -4,7 +4,7 @@ Recipe (stated once so both sides of every parity test draw identical inputs):
 
 * ``default_rng(seed)`` draws the K component means (``N(0, 1)`` per dim, scaled
   by ``sqrt(lam_i)``) and then one uniform label in ``[0, K)`` per point.
-* Points are produced in chunks of ``CHUNK`` rows; chunk ``c`` draws its noise
+* Points are produced in chunks of ``CHUNK`` (131072) rows; chunk ``c`` draws its noise
   from ``default_rng(SeedSequence(seed).spawn(n_chunks)[c])`` so any chunk can be
   regenerated on its own.  ``x = mu[label] + sigma * sqrt(lam) * z``.
 * Optional row normalisation to unit L2 norm, applied after scaling.
@@ -23,7 +23,7 @@ from dataclasses import dataclass, replace
 
 import numpy as np
 
-CHUNK = 1_000_000
+CHUNK = 1 << 17  # 131072 rows
 
 
 @dataclass(frozen=True)
@@ -57,20 +57,32 @@ def n_chunks(spec: MixtureSpec) -> int:
     return max(1, -(-spec.n // CHUNK))
 
 
-def make_chunk(spec: MixtureSpec, c: int, _ml=None) -> np.ndarray:
+SUB = 16384  # rows drawn per call; consecutive draws continue the same stream
+
+
+def make_chunk(spec: MixtureSpec, c: int, _ml=None, out: np.ndarray | None = None) -> np.ndarray:
     """Rows [c*CHUNK, min(n, (c+1)*CHUNK)) as float32, regenerated independently."""
     means, labels, scale = _ml if _ml is not None else _means_labels(spec)
     lo = c * CHUNK
     hi = min(spec.n, lo + CHUNK)
     ss = np.random.SeedSequence(spec.seed).spawn(n_chunks(spec))[c]
     rng = np.random.default_rng(ss)
-    z = rng.standard_normal((hi - lo, spec.d))
-    x = means[labels[lo:hi]] + (spec.sigma * scale) * z
-    if spec.normalize:
-        nrm = np.sqrt(np.einsum("ij,ij->i", x, x))
-        nrm[nrm == 0] = 1.0
-        x /= nrm[:, None]
-    return x.astype(np.float32)
+    if out is None:
+        out = np.empty((hi - lo, spec.d), dtype=np.float32)
+    buf = np.empty((min(SUB, hi - lo), spec.d))
+    for s0 in range(0, hi - lo, SUB):
+        s1 = min(hi - lo, s0 + SUB)
+        z = rng.standard_normal((s1 - s0, spec.d))
+        z *= spec.sigma * scale
+        g = buf[:s1 - s0]
+        np.take(means, labels[lo + s0:lo + s1], axis=0, out=g)
+        z += g
+        if spec.normalize:
+            nrm = np.sqrt(np.einsum("ij,ij->i", z, z))
+            nrm[nrm == 0] = 1.0
+            z /= nrm[:, None]
+        out[s0:s1] = z
+    return out
 
 
 def make_points(spec: MixtureSpec, out: np.ndarray | None = None, threads: int | None = None) -> np.ndarray:
@@ -82,8 +94,7 @@ def make_points(spec: MixtureSpec, out: np.ndarray | None = None, threads: int |
 
     def work(c):
         lo = c * CHUNK
-        blk = make_chunk(spec, c, ml)
-        out[lo:lo + blk.shape[0]] = blk
+        make_chunk(spec, c, ml, out=out[lo:min(spec.n, lo + CHUNK)])
 
     threads = threads or min(16, os.cpu_count() or 1, nc)
     if threads <= 1 or nc == 1:
@@ -93,6 +104,23 @@ def make_points(spec: MixtureSpec, out: np.ndarray | None = None, threads: int |
         with _cf.ThreadPoolExecutor(threads) as ex:
             list(ex.map(work, range(nc)))
     return out
+
+
+def for_each_chunk(spec: MixtureSpec, fn, threads: int | None = None):
+    """Call fn(row0, rows_f32) for every chunk (in parallel threads), without holding all rows."""
+    ml = _means_labels(spec)
+    nc = n_chunks(spec)
+
+    def work(c):
+        fn(c * CHUNK, make_chunk(spec, c, ml))
+
+    threads = threads or min(8, os.cpu_count() or 1, nc)
+    if threads <= 1 or nc == 1:
+        for c in range(nc):
+            work(c)
+    else:
+        with _cf.ThreadPoolExecutor(threads) as ex:
+            list(ex.map(work, range(nc)))
 
 
 def init_indices(n: int, k: int, seed: int = 0) -> np.ndarray:

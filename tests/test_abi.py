@@ -1,0 +1,155 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry point
+declared in include/kmq.h, and rejects bad arguments on the host with the
+documented status before touching the device.  No compute call is made here.
+"""
+import ctypes as ct
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "kmq.h")
+LIB = os.path.join(ROOT, "paper_2608_14648_amd", "libkmq.so")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(LIB), reason="libkmq.so not built (run __graft_entry__.build())")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:km_status|const char \*)\s*(\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ("quantize", "pca_fit_cov", "pca_project", "kmeans_assign", "kmeans_update", "kmeans_fit",
+              "kmeans_cost", "km_last_error", "km_release"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    out = subprocess.run(["nm", "-D", "--defined-only", LIB], capture_output=True, text=True, check=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if " T " in line}
+    missing = [n for n in declared_functions() if n not in exported]
+    assert not missing, missing
+    L = ct.CDLL(LIB)
+    for n in declared_functions():
+        assert hasattr(L, n)
+
+
+def test_header_compiles_as_c():
+    src = '#include "kmq.h"\nint main(void){ km_points p = {0}; (void)p; return (int)sizeof(km_points); }\n'
+    r = subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-I", os.path.dirname(HEADER), "-x", "c", "-", "-o",
+                        "/dev/null"], input=src, text=True, capture_output=True)
+    assert r.returncode == 0, r.stderr
+
+
+@pytest.fixture(scope="module")
+def kmq():
+    from paper_2608_14648_amd import _kmq
+    return _kmq
+
+
+def _pts(kmq, **kw):
+    base = dict(fmt=kmq.KM_F32, d=128, n=100, data=0x1000, ld=128, alpha=None, center=None, front=None, d_front=0,
+                reserved=0)
+    base.update(kw)
+    return kmq.KmPoints(base["fmt"], base["d"], base["n"], base["data"], base["ld"], base["alpha"], base["center"],
+                        base["front"], base["d_front"], base["reserved"])
+
+
+FAKE = ct.c_void_p(0x10000)  # never dereferenced: validation fails first
+
+
+@pytest.mark.parametrize("kw,status,msg", [
+    (dict(fmt=7), -2, "format"),
+    (dict(n=0), -1, "n ="),
+    (dict(d=0), -1, "d ="),
+    (dict(d=126, ld=128), -1, "d % 4"),
+    (dict(ld=64), -1, "ld"),
+    (dict(data=None), -1, "NULL"),
+    (dict(data=0x1004), -1, "aligned"),
+    (dict(reserved=1), -1, "reserved"),
+    (dict(fmt=2, d=40, ld=48), -1, "d % 16"),
+    (dict(fmt=3, d=100, alpha=0x2000, center=0x3000), -1, "d % 32"),
+    (dict(fmt=3, d=128, alpha=None, center=0x3000), -1, "alpha"),
+    (dict(fmt=3, d=128, alpha=0x2000, center=None), -1, "center"),
+    (dict(fmt=4, d=128, alpha=0x2000, center=0x3000, front=0x4000, d_front=0), -1, "d_front"),
+    (dict(fmt=4, d=128, alpha=0x2000, center=0x3000, front=0x4000, d_front=48), -1, "d_front"),
+    (dict(fmt=4, d=128, alpha=0x2000, center=0x3000, front=None, d_front=64), -1, "front"),
+    (dict(fmt=0, d_front=32), -1, "d_front"),
+])
+def test_points_validation(kmq, kw, status, msg):
+    L = kmq.lib()
+    P = _pts(kmq, **kw)
+    st = L.kmeans_assign(ct.byref(P), FAKE, 4, FAKE, None, None, None)
+    assert st == status
+    assert msg in L.km_last_error().decode()
+    st = L.kmeans_update(ct.byref(P), FAKE, 4, FAKE, None, 0, None)
+    assert st == status
+
+
+def test_entry_point_argument_checks(kmq):
+    L = kmq.lib()
+    P = _pts(kmq)
+    assert L.kmeans_assign(None, FAKE, 4, FAKE, None, None, None) == -1
+    assert L.kmeans_assign(ct.byref(P), FAKE, 0, FAKE, None, None, None) == -1
+    assert L.kmeans_assign(ct.byref(P), None, 4, FAKE, None, None, None) == -1
+    assert L.kmeans_assign(ct.byref(P), ct.c_void_p(0x10004), 4, FAKE, None, None, None) == -1
+    assert L.kmeans_assign(ct.byref(P), FAKE, 4, None, None, None, None) == -1
+    assert L.kmeans_update(ct.byref(P), FAKE, 4, FAKE, None, 5, None) == -1
+    assert "policy" in L.km_last_error().decode()
+    # fit: k > n, negative iters, bad init indices (host memory)
+    assert L.kmeans_fit(ct.byref(P), 101, 3, None, FAKE, FAKE, None, 0, None) == -1
+    assert L.kmeans_fit(ct.byref(P), 4, -1, None, FAKE, FAKE, None, 0, None) == -1
+    dup = (ct.c_int64 * 4)(0, 5, 5, 7)
+    assert L.kmeans_fit(ct.byref(P), 4, 3, dup, FAKE, FAKE, None, 0, None) == -1
+    assert "duplicates" in L.km_last_error().decode()
+    oob = (ct.c_int64 * 4)(0, 5, 100, 7)
+    assert L.kmeans_fit(ct.byref(P), 4, 3, oob, FAKE, FAKE, None, 0, None) == -1
+    neg = (ct.c_int64 * 4)(0, -1, 2, 7)
+    assert L.kmeans_fit(ct.byref(P), 4, 3, neg, FAKE, FAKE, None, 0, None) == -1
+
+
+def test_quantize_and_pca_argument_checks(kmq):
+    L = kmq.lib()
+    # unsupported format, bad d, misaligned, unknown flags
+    assert L.quantize(FAKE, 10, 64, 64, 0, FAKE, FAKE, FAKE, 0, None, 1, None) == -2
+    assert L.quantize(FAKE, 10, 40, 40, 2, FAKE, FAKE, None, 0, None, 1, None) == -1
+    assert L.quantize(FAKE, 10, 64, 64, 3, FAKE, FAKE, None, 0, None, 1, None) == -1  # alpha NULL
+    assert L.quantize(FAKE, 10, 64, 64, 3, FAKE, FAKE, FAKE, 16, None, 1, None) == -1  # d_front % 32
+    assert L.quantize(FAKE, 10, 64, 64, 3, FAKE, FAKE, FAKE, 64, None, 1, None) == -1  # d_front == d
+    assert L.quantize(FAKE, 10, 64, 64, 2, FAKE, FAKE, None, 0, None, 4, None) == -1  # flags
+    assert L.quantize(ct.c_void_p(0x10002), 10, 64, 64, 2, FAKE, FAKE, None, 0, None, 1, None) == -1
+    assert L.quantize(FAKE, 0, 64, 64, 2, FAKE, FAKE, None, 0, None, 1, None) == -1
+    assert L.pca_fit_cov(FAKE, 10, 30, FAKE, FAKE, None) == -1
+    assert L.pca_fit_cov(None, 10, 32, FAKE, FAKE, None) == -1
+    assert L.pca_project(FAKE, 10, 32, FAKE, FAKE, 0, FAKE, None) == -1
+    assert L.pca_project(FAKE, 10, 32, FAKE, None, 8, FAKE, None) == -1
+    assert L.kmeans_cost(FAKE, 10, 32, 16, FAKE, 4, FAKE, FAKE, None) == -1
+    assert L.kmeans_cost(FAKE, 10, 32, 32, FAKE, 0, FAKE, FAKE, None) == -1
+
+
+def test_last_error_is_per_thread(kmq):
+    import threading
+    L = kmq.lib()
+    P = _pts(kmq, n=0)
+    assert L.kmeans_assign(ct.byref(P), FAKE, 4, FAKE, None, None, None) == -1
+    seen = {}
+
+    def other():
+        seen["msg"] = L.km_last_error().decode()
+
+    th = threading.Thread(target=other)
+    th.start()
+    th.join()
+    assert seen["msg"] == ""
+    assert "n =" in L.km_last_error().decode()
+
+
+def test_binding_rejects_host_tensors(kmq):
+    import torch
+    with pytest.raises(ValueError):
+        kmq.points_f32(torch.zeros(4, 8))
