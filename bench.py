@@ -1,0 +1,360 @@
+#!/usr/bin/env python3
+"""Benchmark of the hot path on one MI355X: Lloyd k-means on compressed vectors.
+
+Default workload (N=1): 1,000,000 x 768 unit-normalised Gaussian mixture of
+1,000 components (sigma 0.15), k = 1,000, 20 Lloyd iterations, clustered twice:
+as fp32 vectors and as per-dimension SQ8 codes.  One step =
+  quantize (SQ8 parameters + codes)
+  + kmeans_fit fp32 (init, 20 x (assign, update), final assign, objectives)
+  + kmeans_fit SQ8  (same)
+  + full-precision partition cost of both final partitions (raw-vector means).
+Inputs are resident in HBM before the timed region.  `value` is Lloyd
+iterations per second over the whole step (20 fp32 + 20 SQ8 iterations).
+
+Other workloads (--workload 1|3|4|5) time the other configurations for
+measurement; they are not the headline line.
+
+The JSON line carries the roofline of the dominant kernel (the fused fp32
+assignment kernel, on fp32 MFMA), measured from HIP events recorded by the
+library around each launch of that kernel on its stream, and the oracle timed on
+this host on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "Lloyd iters/s + point×centroid distances/s; objective ratio vs fp32 oracle"
+PEAK = {"fp32_mfma_tflops": 157.3, "int8_mfma_tops": 5000.0, "hbm_gbs": 8000.0}
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def upload(spec, torch):
+    """Generate the mixture chunk by chunk straight into a device tensor."""
+    import synth
+    X = torch.empty((spec.n, spec.d), dtype=torch.float32, device="cuda")
+
+    def put(r0, blk):
+        X[r0:r0 + blk.shape[0]].copy_(torch.from_numpy(blk), non_blocking=False)
+    synth.for_each_chunk(spec, put)
+    torch.cuda.synchronize()
+    return X
+
+
+class Timer:
+    def __init__(self):
+        self.stats = {}
+
+    def add(self, name, st):
+        d = self.stats.setdefault(name, {"assign_ms": 0.0, "prep_ms": 0.0, "update_ms": 0.0, "other_ms": 0.0,
+                                         "assign_passes": 0, "updates": 0})
+        for key, v in st.as_dict().items():
+            d[key] += v
+
+
+def stage_summary(s):
+    return {"assign_ms_per_pass": s["assign_ms"] / max(1, s["assign_passes"]),
+            "update_ms_per_iter": s["update_ms"] / max(1, s["updates"]),
+            "prep_ms_per_pass": s["prep_ms"] / max(1, s["assign_passes"]),
+            "other_ms_total": s["other_ms"]}
+
+
+# ------------------------------------------------------------------------- workloads
+
+def workload_c2(cfg, torch, km, args):
+    spec = cfg["spec"] if args.n is None else cfg["spec"].with_n(args.n)
+    k, T = cfg["k"], cfg["iters"]
+    import synth
+    log(f"generating {spec.n} x {spec.d} mixture")
+    X = upload(spec, torch)
+    idx = synth.init_indices(spec.n, k)
+    P32 = km.points_f32(X)
+    mu = torch.empty((k, spec.d), dtype=torch.float32, device="cuda")
+
+    def step(timer):
+        codes, params = km.quantize_sq8(X)
+        P8 = km.points_sq8(codes)
+        s32, s8 = km.KmFitStats(), km.KmFitStats()
+        C32, a32, J32 = km.kmeans_fit(P32, k, T, idx, stats=s32)
+        C8, a8, J8 = km.kmeans_fit(P8, k, T, idx, stats=s8)
+        out = {}
+        for name, a in (("f32", a32), ("sq8", a8)):  # full-precision cost of the final partition
+            km.kmeans_update(P32, a, mu, km.KM_EMPTY_KEEP, counts=False)
+            out[name] = km.kmeans_cost(X, mu, a)
+        if timer is not None:
+            timer.add("f32", s32)
+            timer.add("sq8", s8)
+        return out, (J32, J8)
+
+    def finish(out, timer, elapsed, K):
+        c32 = float(out["f32"].item())
+        c8 = float(out["sq8"].item())
+        f = timer.stats["f32"]
+        q = timer.stats["sq8"]
+        a_ms = f["assign_ms"] / f["assign_passes"]
+        flop = 2.0 * spec.n * k * spec.d
+        achieved = flop / (a_ms * 1e-3) / 1e12
+        q_ms = q["assign_ms"] / q["assign_passes"]
+        iters = 2 * T * K
+        res = {
+            "value": iters / elapsed,
+            "unit": "Lloyd iters/s",
+            "dtype": "f32+i8",
+            "config": {"workload": cfg["name"], "N": spec.n, "d": spec.d, "k": k, "iters": T,
+                       "formats": ["f32", "sq8"], "components": spec.components, "sigma": spec.sigma},
+            "distances_per_s": 2 * (T + 1) * spec.n * k * K / elapsed,
+            "objective_ratio_sq8_vs_f32": c8 / c32,
+            "partition_cost": {"f32": c32, "sq8": c8},
+            "roofline": {"bound": "mfma", "kernel": "assign_kernel<fp32>", "achieved": achieved,
+                         "peak": PEAK["fp32_mfma_tflops"], "unit": "TFLOP/s",
+                         "frac": achieved / PEAK["fp32_mfma_tflops"], "traffic": None,
+                         "avg_launch_ms": a_ms, "flop_per_launch": flop},
+            "roofline_sq8_assign": {"bound": "mfma", "achieved": 2.0 * spec.n * k * spec.d / (q_ms * 1e-3) / 1e12,
+                                    "peak": PEAK["int8_mfma_tops"], "unit": "TOP/s",
+                                    "frac": 2.0 * spec.n * k * spec.d / (q_ms * 1e-3) / 1e12 / PEAK["int8_mfma_tops"],
+                                    "avg_launch_ms": q_ms},
+            "update_f32_hbm": {"bytes_per_update": spec.n * (4 * spec.d + 4),
+                               "achieved_gbs": spec.n * (4 * spec.d + 4) / (f["update_ms"] / f["updates"] * 1e-3) / 1e9,
+                               "peak_gbs": PEAK["hbm_gbs"]},
+            "stages": {"f32": stage_summary(f), "sq8": stage_summary(q)},
+        }
+        res["update_f32_hbm"]["frac"] = res["update_f32_hbm"]["achieved_gbs"] / PEAK["hbm_gbs"]
+        return res
+
+    def cpu_baseline():
+        import oracle as orc
+        Xh = synth.make_points(spec.with_n(min(spec.n, 200_000)))
+        C = np.ascontiguousarray(Xh[:k])
+        lo, hi = orc.sq8_fit(Xh)
+
+        def one_iter(ns):
+            xs = Xh[:ns]
+            codes = orc.sq8_encode(xs, lo, hi)
+            t0 = time.perf_counter()
+            a, _ = orc.assign_f32(xs, C)
+            orc.update_f32(xs, a, k, C)
+            t1 = time.perf_counter()
+            a8, _ = orc.assign_sq8(codes, codes[:k])
+            orc.update_sq8(codes, a8, k, codes[:k])
+            t2 = time.perf_counter()
+            return t1 - t0, t2 - t1
+
+        c32, c8 = one_iter(1000)
+        ns = int(min(len(Xh), max(1000, 1000 * args.cpu_seconds / max(c32 + c8, 1e-6))))
+        t32, t8 = one_iter(ns)
+        scale = spec.n / ns
+        per_iter = (t32 + t8) * scale / 2  # one fp32 and one SQ8 iteration, extrapolated to N
+        return {"value": 1.0 / per_iter, "unit": "Lloyd iters/s", "cores": orc.num_threads(), "kind": "oracle",
+                "sample": f"one fp32 and one SQ8 Lloyd iteration (assign + update) on the first {ns} of the "
+                          f"{spec.n} points, k={k}, d={spec.d}, timed {t32 + t8:.2f} s, extrapolated linearly to N"}
+
+    return step, finish, cpu_baseline
+
+
+def workload_sign1(cfg, torch, km, args):
+    spec = cfg["spec"] if args.n is None else cfg["spec"].with_n(args.n)
+    k, T = cfg["k"], cfg["iters"]
+    import synth
+    log(f"generating {spec.n} x {spec.d} mixture")
+    X = upload(spec, torch)
+    idx = synth.init_indices(spec.n, k)
+    P32 = km.points_f32(X)
+    mu = torch.empty((k, spec.d), dtype=torch.float32, device="cuda")
+
+    def step(timer):
+        bits, m, alpha, _ = km.quantize_sign1(X)
+        P = km.points_sign1(bits, alpha, m, spec.d)
+        st = km.KmFitStats()
+        C, a, J = km.kmeans_fit(P, k, T, idx, stats=st)
+        km.kmeans_update(P32, a, mu, km.KM_EMPTY_KEEP, counts=False)
+        cost = km.kmeans_cost(X, mu, a)
+        if timer is not None:
+            timer.add("sign1", st)
+        return {"sign1": cost}, J
+
+    def finish(out, timer, elapsed, K):
+        s = timer.stats["sign1"]
+        a_ms = s["assign_ms"] / s["assign_passes"]
+        ops = 2.0 * spec.n * k * spec.d
+        ach = ops / (a_ms * 1e-3) / 1e12
+        return {"value": T * K / elapsed, "unit": "Lloyd iters/s", "dtype": "i8",
+                "config": {"workload": cfg["name"], "N": spec.n, "d": spec.d, "k": k, "iters": T,
+                           "formats": ["sign1"]},
+                "distances_per_s": (T + 1) * spec.n * k * K / elapsed,
+                "partition_cost": {"sign1": float(out["sign1"].item())},
+                "roofline": {"bound": "mfma", "kernel": "assign_kernel<1-bit>", "achieved": ach,
+                             "peak": PEAK["int8_mfma_tops"], "unit": "TOP/s", "frac": ach / PEAK["int8_mfma_tops"],
+                             "traffic": None, "avg_launch_ms": a_ms},
+                "stages": {"sign1": stage_summary(s)}}
+
+    return step, finish, None
+
+
+def workload_pca(cfg, torch, km, args):
+    spec = cfg["spec"] if args.n is None else cfg["spec"].with_n(args.n)
+    k, T, dout = cfg["k"], cfg["iters"], cfg["d_out"]
+    import synth
+    log(f"generating {spec.n} x {spec.d} mixture")
+    X = upload(spec, torch)
+    idx = synth.init_indices(spec.n, k)
+    Y = torch.empty((spec.n, dout), dtype=torch.float32, device="cuda")
+
+    def step(timer):
+        mean, cov = km.pca_fit_cov(X)
+        # host eigensolve of the d x d covariance (harness step)
+        w, V = np.linalg.eigh(cov.double().cpu().numpy())
+        order = np.argsort(w)[::-1][:dout]
+        W = torch.from_numpy(np.ascontiguousarray(V[:, order], dtype=np.float32)).cuda()
+        km.pca_project(X, mean, W, out=Y)
+        st = km.KmFitStats()
+        C, a, J = km.kmeans_fit(km.points_f32(Y), k, T, idx, stats=st)
+        if timer is not None:
+            timer.add("pca", st)
+        return {}, J
+
+    def finish(out, timer, elapsed, K):
+        s = timer.stats["pca"]
+        a_ms = s["assign_ms"] / s["assign_passes"]
+        flop = 2.0 * spec.n * k * dout
+        ach = flop / (a_ms * 1e-3) / 1e12
+        return {"value": T * K / elapsed, "unit": "Lloyd iters/s", "dtype": "f32",
+                "config": {"workload": cfg["name"], "N": spec.n, "d": spec.d, "d_out": dout, "k": k, "iters": T},
+                "distances_per_s": (T + 1) * spec.n * k * K / elapsed,
+                "roofline": {"bound": "mfma", "kernel": "assign_kernel<fp32>", "achieved": ach,
+                             "peak": PEAK["fp32_mfma_tflops"], "unit": "TFLOP/s",
+                             "frac": ach / PEAK["fp32_mfma_tflops"], "traffic": None, "avg_launch_ms": a_ms},
+                "stages": {"pca": stage_summary(s)}}
+
+    return step, finish, None
+
+
+def workload_hybrid(cfg, torch, km, args):
+    spec = cfg["spec"] if args.n is None else cfg["spec"].with_n(args.n)
+    k, T, d0 = cfg["k"], cfg["iters"], cfg["d_front"]
+    import synth
+    log(f"generating {spec.n} x {spec.d} mixture")
+    X = upload(spec, torch)
+    idx = synth.init_indices(spec.n, k)
+    P32 = km.points_f32(X)
+    mu = torch.empty((k, spec.d), dtype=torch.float32, device="cuda")
+
+    def step(timer):
+        bits, m, alpha, front = km.quantize_sign1(X, d_front=d0, want_front=True)
+        P = km.points_hybrid(front, bits, alpha, m, spec.d)
+        st = km.KmFitStats()
+        C, a, J = km.kmeans_fit(P, k, T, idx, stats=st)
+        del front
+        km.kmeans_update(P32, a, mu, km.KM_EMPTY_KEEP, counts=False)
+        cost = km.kmeans_cost(X, mu, a)
+        if timer is not None:
+            timer.add("hybrid", st)
+        return {"hybrid": cost}, J
+
+    def finish(out, timer, elapsed, K):
+        s = timer.stats["hybrid"]
+        a_ms = s["assign_ms"] / s["assign_passes"]
+        flop = 2.0 * spec.n * k * d0
+        ach = flop / (a_ms * 1e-3) / 1e12
+        return {"value": T * K / elapsed, "unit": "Lloyd iters/s", "dtype": "f32+i8",
+                "config": {"workload": cfg["name"], "N": spec.n, "d": spec.d, "d_front": d0, "k": k, "iters": T},
+                "distances_per_s": (T + 1) * spec.n * k * K / elapsed,
+                "partition_cost": {"hybrid": float(out["hybrid"].item())},
+                "roofline": {"bound": "mfma", "kernel": "assign_kernel<hybrid>", "achieved_front": ach,
+                             "peak": PEAK["fp32_mfma_tflops"], "unit": "TFLOP/s",
+                             "frac": ach / PEAK["fp32_mfma_tflops"], "traffic": None, "avg_launch_ms": a_ms},
+                "stages": {"hybrid": stage_summary(s)}}
+
+    return step, finish, None
+
+
+def workload_c1(cfg, torch, km, args):
+    spec = cfg["spec"] if args.n is None else cfg["spec"].with_n(args.n)
+    k, T = cfg["k"], cfg["iters"]
+    import synth
+    X = upload(spec, torch)
+    idx = synth.init_indices(spec.n, k)
+    P = km.points_f32(X)
+
+    def step(timer):
+        st = km.KmFitStats()
+        C, a, J = km.kmeans_fit(P, k, T, idx, stats=st)
+        if timer is not None:
+            timer.add("f32", st)
+        return {}, J
+
+    def finish(out, timer, elapsed, K):
+        s = timer.stats["f32"]
+        return {"value": T * K / elapsed, "unit": "Lloyd iters/s", "dtype": "f32",
+                "config": {"workload": cfg["name"], "N": spec.n, "d": spec.d, "k": k, "iters": T},
+                "distances_per_s": (T + 1) * spec.n * k * K / elapsed, "stages": {"f32": stage_summary(s)}}
+
+    return step, finish, None
+
+
+WORKLOADS = {1: workload_c1, 2: workload_c2, 3: workload_sign1, 4: workload_pca, 5: workload_hybrid}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", type=int, default=2, choices=sorted(WORKLOADS))
+    ap.add_argument("--n", type=int, default=None, help="override the number of points (measurement only)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle's CPU-baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path (the sharding design is "
+              "described in DESIGN.md); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2608_14648_amd as km
+    import synth
+    km.lib()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+
+    cfg = synth.config(args.workload)
+    step, finish, cpu_baseline = WORKLOADS[args.workload](cfg, torch, km, args)
+    for i in range(args.warmup):
+        step(None)
+        torch.cuda.synchronize()
+        log(f"warmup step {i + 1}/{args.warmup} done")
+    timer = Timer()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    out = None
+    for i in range(args.steps):
+        out, _ = step(timer)
+        log(f"timed step {i + 1}/{args.steps} issued")
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    res = finish(out, timer, elapsed, args.steps)
+    line = {"metric": METRIC, "value": res.pop("value"), "unit": res.pop("unit"), "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": elapsed / args.steps * 1e3, "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": res.pop("dtype"),
+            "data": "synthetic (seeded Gaussian mixture shaped like the paper's embedding workloads)",
+            "config": res.pop("config")}
+    line.update(res)
+    if cpu_baseline is not None and not args.no_cpu_baseline:
+        log("timing the CPU oracle on a bounded sample")
+        line["cpu_baseline"] = cpu_baseline()
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -158,6 +158,17 @@ km_status kmeans_assign(const km_points *P, const void *C, int32_t k, int32_t *a
 km_status kmeans_update(const km_points *P, const int32_t *assign, int32_t k, void *C, int64_t *counts,
                         int32_t policy, km_stream stream);
 
+/* Per-stage device times of one kmeans_fit call (milliseconds, from HIP events
+ * recorded on the call's stream around each launch). */
+typedef struct km_fit_stats {
+  double assign_ms;      /* fused assignment kernels only, summed over the passes */
+  double prep_ms;        /* centroid preparation before each pass */
+  double update_ms;      /* complete update step (sort, sums, split, compose) */
+  double other_ms;       /* initial gather, point-only terms, objective sums */
+  int32_t assign_passes; /* iters + 1 */
+  int32_t updates;       /* iters */
+} km_fit_stats;
+
 /*
  * kmeans_fit -- Lloyd's algorithm (Sec. 2.3): STEP 1 (C = the points at
  * init_idx), then `iters` x (STEP 2, STEP 3), then a final STEP 2.
@@ -168,10 +179,13 @@ km_status kmeans_update(const km_points *P, const int32_t *assign, int32_t k, vo
  *   objective (nullable): DEVICE double[iters + 1]; entry t is the in-space
  *     objective of the t-th assignment pass (sum of in-space distances to the
  *     centroids that pass used).
- *   Nothing is synchronised: the call only enqueues work on `stream`.
+ *   stats (nullable, HOST): per-stage device times; when given, the call waits
+ *     for `stream` to finish before returning.  Otherwise nothing is
+ *     synchronised: the call only enqueues work on `stream`.
  */
 km_status kmeans_fit(const km_points *P, int32_t k, int32_t iters, const int64_t *init_idx, void *C,
-                     int32_t *assign, double *objective, int32_t policy, km_stream stream);
+                     int32_t *assign, double *objective, int32_t policy, km_fit_stats *stats,
+                     km_stream stream);
 
 /*
  * kmeans_cost -- sum over points of ||x - c_{assign(x)}||^2 in fp64 for fp32

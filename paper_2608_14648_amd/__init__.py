@@ -5,6 +5,6 @@ Python face of libkmq.so, the HIP library whose C ABI is declared in
 Lloyd steps (assign, update, fit) on fp32, SQ8, 1-bit and hybrid points.
 """
 from ._kmq import (  # noqa: F401
-    KM_EMPTY_KEEP, KM_EMPTY_SPLIT, KM_F32, KM_HYBRID, KM_SIGN1, KM_SQ8, KmqError, Points, kmeans_assign,
+    KM_EMPTY_KEEP, KM_EMPTY_SPLIT, KM_F32, KM_HYBRID, KM_SIGN1, KM_SQ8, KmFitStats, KmqError, Points, kmeans_assign,
     kmeans_cost, kmeans_fit, kmeans_update, lib, pca_fit_cov, pca_project, points_f32, points_hybrid,
     points_sign1, points_sq8, quantize_sign1, quantize_sq8, release)

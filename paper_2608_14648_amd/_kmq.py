@@ -36,6 +36,14 @@ class KmPoints(ct.Structure):
                 ("d_front", ct.c_int32), ("reserved", ct.c_int32)]
 
 
+class KmFitStats(ct.Structure):
+    _fields_ = [("assign_ms", ct.c_double), ("prep_ms", ct.c_double), ("update_ms", ct.c_double),
+                ("other_ms", ct.c_double), ("assign_passes", ct.c_int32), ("updates", ct.c_int32)]
+
+    def as_dict(self):
+        return {f: getattr(self, f) for f, _ in self._fields_}
+
+
 _lib = None
 
 
@@ -54,7 +62,7 @@ def lib():
             "pca_project": [vp, i64, i32, vp, vp, i32, vp, vp],
             "kmeans_assign": [ct.POINTER(KmPoints), vp, i32, vp, vp, vp, vp],
             "kmeans_update": [ct.POINTER(KmPoints), vp, i32, vp, vp, i32, vp],
-            "kmeans_fit": [ct.POINTER(KmPoints), i32, i32, vp, vp, vp, vp, i32, vp],
+            "kmeans_fit": [ct.POINTER(KmPoints), i32, i32, vp, vp, vp, vp, i32, ct.POINTER(KmFitStats), vp],
             "kmeans_cost": [vp, i64, i32, i64, vp, i32, vp, vp, vp],
             "km_release": [],
         }
@@ -244,8 +252,10 @@ def kmeans_update(P: Points, assign: torch.Tensor, C: torch.Tensor, policy: int 
 
 
 def kmeans_fit(P: Points, k: int, iters: int, init_idx=None, C: torch.Tensor | None = None,
-               policy: int = KM_EMPTY_SPLIT, objective: bool = True, assign: torch.Tensor | None = None):
+               policy: int = KM_EMPTY_SPLIT, objective: bool = True, assign: torch.Tensor | None = None,
+               stats: KmFitStats | None = None):
     """Lloyd's algorithm on the device.  init_idx: host int64[k] (or None with C holding the start).
+    stats: optional KmFitStats filled with per-stage device times (the call then waits for the stream).
     Returns (C, assign, objective double[iters+1] on device or None)."""
     if C is None:
         C = torch.empty((k, P.d), dtype=P.centroid_dtype(), device=P.device)
@@ -259,7 +269,8 @@ def kmeans_fit(P: Points, k: int, iters: int, init_idx=None, C: torch.Tensor | N
         if idx.shape != (k,):
             raise ValueError("init_idx must hold k indices")
         idx_p = idx.ctypes.data_as(ct.c_void_p)
-    _check(lib().kmeans_fit(P.ref, k, iters, idx_p, _ptr(C), _ptr(a), _ptr(obj), policy, _stream()))
+    _check(lib().kmeans_fit(P.ref, k, iters, idx_p, _ptr(C), _ptr(a), _ptr(obj), policy,
+                            ct.byref(stats) if stats is not None else None, _stream()))
     return C, a, obj
 
 

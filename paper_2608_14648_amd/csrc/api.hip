@@ -266,8 +266,62 @@ km_status kmeans_update(const km_points *P, const int32_t *assign, int32_t k, vo
   return launch_update(p, assign, k, C, counts, policy, ws.get(), s);
 }
 
+namespace {
+// hipEvent pairs around the launches of one fit (only when stats are requested)
+class StageClock {
+ public:
+  StageClock(bool on, hipStream_t s) : on_(on), s_(s) {}
+  ~StageClock() {
+    for (auto &e : ev_) {
+      (void)hipEventDestroy(e.first);
+      (void)hipEventDestroy(e.second);
+    }
+  }
+  km_status begin(int stage) {
+    if (!on_) return KM_OK;
+    hipEvent_t a, b;
+    KMQ_HIP(hipEventCreate(&a));
+    if (hipEventCreate(&b) != hipSuccess) {
+      (void)hipEventDestroy(a);
+      return hip_fail(hipErrorOutOfMemory, "hipEventCreate");
+    }
+    ev_.push_back({a, b});
+    stage_.push_back(stage);
+    KMQ_HIP(hipEventRecord(a, s_));
+    return KM_OK;
+  }
+  km_status end() {
+    if (!on_) return KM_OK;
+    KMQ_HIP(hipEventRecord(ev_.back().second, s_));
+    return KM_OK;
+  }
+  km_status collect(km_fit_stats *st) {
+    if (!on_) return KM_OK;
+    KMQ_HIP(hipStreamSynchronize(s_));
+    double ms[4] = {0, 0, 0, 0};
+    for (size_t i = 0; i < ev_.size(); ++i) {
+      float t = 0.f;
+      KMQ_HIP(hipEventElapsedTime(&t, ev_[i].first, ev_[i].second));
+      ms[stage_[i]] += t;
+    }
+    st->assign_ms = ms[0];
+    st->prep_ms = ms[1];
+    st->update_ms = ms[2];
+    st->other_ms = ms[3];
+    return KM_OK;
+  }
+
+ private:
+  bool on_;
+  hipStream_t s_;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> ev_;
+  std::vector<int> stage_;
+};
+enum { kStAssign = 0, kStPrep = 1, kStUpdate = 2, kStOther = 3 };
+}  // namespace
+
 km_status kmeans_fit(const km_points *P, int32_t k, int32_t iters, const int64_t *init_idx, void *C, int32_t *assign,
-                     double *objective, int32_t policy, km_stream stream) {
+                     double *objective, int32_t policy, km_fit_stats *stats, km_stream stream) {
   g_err[0] = 0;
   Points p;
   km_status st = check_points(P, &p);
@@ -308,28 +362,41 @@ km_status kmeans_fit(const km_points *P, int32_t k, int32_t iters, const int64_t
   int64_t *didx = reinterpret_cast<int64_t *>(w + b_prep + b_upd + b_score + b_xc + b_part);
   (void)centroid_bytes;
 
-  if (init_idx) {
-    KMQ_HIP(hipMemcpyAsync(didx, init_idx, sizeof(int64_t) * (size_t)k, hipMemcpyHostToDevice, s));
-    st = launch_gather_init(p, didx, k, C, s);
-    if (st != KM_OK) return st;
-  }
-  if (objective) {
-    st = launch_xconst(p, xc, s);
-    if (st != KM_OK) return st;
-  }
-  CentroidPrep cp;
-  for (int it = 0; it <= iters; ++it) {
-    st = launch_prep(p, C, k, wprep, &cp, s);
-    if (st != KM_OK) return st;
-    st = launch_assign(p, C, cp, k, assign, sc, s);
-    if (st != KM_OK) return st;
-    if (objective) {
-      st = launch_objective(p, xc, sc, p.n, objective + it, part, objective_blocks(p.n), s);
-      if (st != KM_OK) return st;
+  try {
+    StageClock clk(stats != nullptr, s);
+#define KMQ_STAGE(stage, expr)            \
+  do {                                    \
+    st = clk.begin(stage);                \
+    if (st != KM_OK) return st;           \
+    st = (expr);                          \
+    if (st != KM_OK) return st;           \
+    st = clk.end();                       \
+    if (st != KM_OK) return st;           \
+  } while (0)
+    if (init_idx) {
+      KMQ_HIP(hipMemcpyAsync(didx, init_idx, sizeof(int64_t) * (size_t)k, hipMemcpyHostToDevice, s));
+      KMQ_STAGE(kStOther, launch_gather_init(p, didx, k, C, s));
     }
-    if (it == iters) break;  // the last pass only assigns (the final STEP 2)
-    st = launch_update(p, assign, k, C, nullptr, policy, wupd, s);
-    if (st != KM_OK) return st;
+    if (objective) KMQ_STAGE(kStOther, launch_xconst(p, xc, s));
+    CentroidPrep cp;
+    for (int it = 0; it <= iters; ++it) {
+      KMQ_STAGE(kStPrep, launch_prep(p, C, k, wprep, &cp, s));
+      KMQ_STAGE(kStAssign, launch_assign(p, C, cp, k, assign, sc, s));
+      if (objective)
+        KMQ_STAGE(kStOther, launch_objective(p, xc, sc, p.n, objective + it, part, objective_blocks(p.n), s));
+      if (it == iters) break;  // the last pass only assigns (the final STEP 2)
+      KMQ_STAGE(kStUpdate, launch_update(p, assign, k, C, nullptr, policy, wupd, s));
+    }
+#undef KMQ_STAGE
+    if (stats) {
+      st = clk.collect(stats);
+      if (st != KM_OK) return st;
+      stats->assign_passes = iters + 1;
+      stats->updates = iters;
+    }
+  } catch (const std::bad_alloc &) {
+    set_error("host allocation failed");
+    return KM_ENOMEM;
   }
   return KM_OK;
 }

@@ -102,15 +102,15 @@ def test_entry_point_argument_checks(kmq):
     assert L.kmeans_update(ct.byref(P), FAKE, 4, FAKE, None, 5, None) == -1
     assert "policy" in L.km_last_error().decode()
     # fit: k > n, negative iters, bad init indices (host memory)
-    assert L.kmeans_fit(ct.byref(P), 101, 3, None, FAKE, FAKE, None, 0, None) == -1
-    assert L.kmeans_fit(ct.byref(P), 4, -1, None, FAKE, FAKE, None, 0, None) == -1
+    assert L.kmeans_fit(ct.byref(P), 101, 3, None, FAKE, FAKE, None, 0, None, None) == -1
+    assert L.kmeans_fit(ct.byref(P), 4, -1, None, FAKE, FAKE, None, 0, None, None) == -1
     dup = (ct.c_int64 * 4)(0, 5, 5, 7)
-    assert L.kmeans_fit(ct.byref(P), 4, 3, dup, FAKE, FAKE, None, 0, None) == -1
+    assert L.kmeans_fit(ct.byref(P), 4, 3, dup, FAKE, FAKE, None, 0, None, None) == -1
     assert "duplicates" in L.km_last_error().decode()
     oob = (ct.c_int64 * 4)(0, 5, 100, 7)
-    assert L.kmeans_fit(ct.byref(P), 4, 3, oob, FAKE, FAKE, None, 0, None) == -1
+    assert L.kmeans_fit(ct.byref(P), 4, 3, oob, FAKE, FAKE, None, 0, None, None) == -1
     neg = (ct.c_int64 * 4)(0, -1, 2, 7)
-    assert L.kmeans_fit(ct.byref(P), 4, 3, neg, FAKE, FAKE, None, 0, None) == -1
+    assert L.kmeans_fit(ct.byref(P), 4, 3, neg, FAKE, FAKE, None, 0, None, None) == -1
 
 
 def test_quantize_and_pca_argument_checks(kmq):

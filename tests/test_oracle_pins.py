@@ -438,3 +438,15 @@ def test_update_sign1_bruteforce(orc, n, w, k, seed):
             np.testing.assert_allclose(C[j], dec[a == j].mean(0), rtol=1e-5, atol=1e-6)
         else:
             np.testing.assert_array_equal(C[j], C0[j])
+
+
+def test_col_mean_and_sq8_fit_special_cases(orc):
+    rng = np.random.default_rng(21)
+    X = (rng.standard_normal((513, 40)) * 3 + 1).astype(np.float32)
+    np.testing.assert_allclose(orc.col_mean(X), X.astype(np.float64).mean(0), rtol=1e-6, atol=1e-7)
+    # a single row is its own mean and its own (lo, hi)
+    x1 = X[:1]
+    np.testing.assert_array_equal(orc.col_mean(x1), x1[0])
+    lo, hi = orc.sq8_fit(x1)
+    np.testing.assert_array_equal(lo, x1[0])
+    np.testing.assert_array_equal(hi, x1[0])
