@@ -85,32 +85,50 @@ struct Cfg {
   static constexpr bool kIntScore = (FMT == KM_SQ8);
 };
 
+// Raw loads of one stage (consumed only when the stage is written to LDS, one MFMA
+// stage later, so the global latency hides under the matrix work).
 struct StageRegs {
   uint4 c[4];
   uint4 p[4];
+  float cpar[4];  // per-centroid constants of the next tile (threads < 128, stage 0 only)
 };
 
+__device__ __forceinline__ uint4 mask4(uint4 v, bool ok) {
+  return make_uint4(ok ? v.x : 0u, ok ? v.y : 0u, ok ? v.z : 0u, ok ? v.w : 0u);
+}
+
+__device__ __forceinline__ uint4 flip4(uint4 v) {
+  // uint8 code -> int8 (code - 128) in every byte
+  return make_uint4(v.x ^ 0x80808080u, v.y ^ 0x80808080u, v.z ^ 0x80808080u, v.w ^ 0x80808080u);
+}
+
+template <int FMT>
+__device__ __forceinline__ bool is_fp_stage(int s, int SF) {
+  if constexpr (FMT == KM_F32) return true;
+  else if constexpr (FMT == KM_HYBRID) return s < SF;
+  else return false;
+}
+
+// Every address is clamped into its buffer; lanes outside the data are zeroed at
+// store time, so the loads are unconditional and branch-free.
 template <int FMT>
 __device__ __forceinline__ void load_stage(const AssignArgs &A, int s, int SF, int64_t c0, int64_t p0,
                                            StageRegs &R) {
   const int t = threadIdx.x;
-  const uint4 z = make_uint4(0, 0, 0, 0);
-  if (Cfg<FMT>::kFp && s < SF) {
+  if (is_fp_stage<FMT>(s, SF)) {
     const int dim0 = 32 * s;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int cidx = t + kThreads * i;
       const int row = cidx >> 3, col = cidx & 7;
       const int dim = dim0 + 4 * col;
-      const bool ok = dim < A.df;
+      const int dimc = dim < A.df ? dim : 0;
       const int64_t cr = min<int64_t>(c0 + row, A.k - 1);
       const int64_t pr = min<int64_t>(p0 + row, A.n - 1);
-      R.c[i] = ok ? *reinterpret_cast<const uint4 *>(A.cf + cr * A.cfld + dim) : z;
-      R.p[i] = ok ? *reinterpret_cast<const uint4 *>(A.pf + pr * A.pfld + dim) : z;
+      R.c[i] = *reinterpret_cast<const uint4 *>(A.cf + cr * A.cfld + dimc);
+      R.p[i] = *reinterpret_cast<const uint4 *>(A.pf + pr * A.pfld + dimc);
     }
-    return;
-  }
-  if constexpr (Cfg<FMT>::kInt) {
+  } else if constexpr (Cfg<FMT>::kInt) {
     const int si = s - (Cfg<FMT>::kFp ? SF : 0);
     const int b0 = kRowBytes * si;
 #pragma unroll
@@ -118,74 +136,155 @@ __device__ __forceinline__ void load_stage(const AssignArgs &A, int s, int SF, i
       const int cidx = t + kThreads * i;
       const int row = cidx >> 3, col = cidx & 7;
       const int b = b0 + 16 * col;
-      const bool ok = b < A.di;
+      const int bc = b < A.di ? b : 0;
       const int64_t cr = min<int64_t>(c0 + row, A.k - 1);
-      uint4 v = ok ? *reinterpret_cast<const uint4 *>(A.ci8 + cr * A.cild + b) : z;
-      if (FMT == KM_SQ8 && ok) {
-        v.x ^= 0x80808080u; v.y ^= 0x80808080u; v.z ^= 0x80808080u; v.w ^= 0x80808080u;
-      }
-      R.c[i] = v;
+      R.c[i] = *reinterpret_cast<const uint4 *>(A.ci8 + cr * A.cild + bc);
       if (FMT == KM_SQ8) {
         const int64_t pr = min<int64_t>(p0 + row, A.n - 1);
-        uint4 w = ok ? *reinterpret_cast<const uint4 *>(A.pi8 + pr * A.pild + b) : z;
-        if (ok) {
-          w.x ^= 0x80808080u; w.y ^= 0x80808080u; w.z ^= 0x80808080u; w.w ^= 0x80808080u;
-        }
-        R.p[i] = w;
+        R.p[i] = *reinterpret_cast<const uint4 *>(A.pi8 + pr * A.pild + bc);
       }
     }
     if (Cfg<FMT>::kBits) {
-      // 128 points x 4 words of this stage: two words per thread, each widened to 32 bytes
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
         const int w = t + kThreads * i;
         const int row = w >> 2, wi = w & 3;
         const int word = 4 * si + wi;
-        const bool ok = 32 * word < A.di;
         const int64_t pr = min<int64_t>(p0 + row, A.n - 1);
-        const uint32_t bits = ok ? A.pbits[pr * A.pbw + A.pbw0 + word] : 0u;
-        R.p[2 * i] = make_uint4(spread4(bits & 15u), spread4((bits >> 4) & 15u), spread4((bits >> 8) & 15u),
-                                spread4((bits >> 12) & 15u));
-        R.p[2 * i + 1] = make_uint4(spread4((bits >> 16) & 15u), spread4((bits >> 20) & 15u),
-                                    spread4((bits >> 24) & 15u), spread4(bits >> 28));
+        R.p[i].x = A.pbits[pr * A.pbw + A.pbw0 + (32 * word < A.di ? word : 0)];
       }
+    }
+  }
+  if (s == 0 && t < kTile) {
+    const int64_t j = min<int64_t>(c0 + t, A.k - 1);
+    if (Cfg<FMT>::kFp) R.cpar[0] = A.cp.cn[j];
+    if (Cfg<FMT>::kInt) R.cpar[1] = __int_as_float(A.cp.qsum[j]);
+    if (Cfg<FMT>::kBits) {
+      R.cpar[2] = A.cp.u[j];
+      R.cpar[3] = A.cp.sig2[j];
     }
   }
 }
 
 template <int FMT>
-__device__ __forceinline__ void store_stage(int s, int SF, const StageRegs &R, uint8_t *buf) {
+__device__ __forceinline__ void store_stage(const AssignArgs &A, int s, int SF, const StageRegs &R, uint8_t *buf,
+                                            float *cpar) {
   const int t = threadIdx.x;
   uint8_t *ct = buf;
   uint8_t *pt = buf + kTileBytes;
+  const bool fp = is_fp_stage<FMT>(s, SF);
+  const int si = s - (Cfg<FMT>::kFp ? SF : 0);
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int cidx = t + kThreads * i;
     const int row = cidx >> 3, col = cidx & 7;
-    *reinterpret_cast<uint4 *>(ct + row * kLdsStride + 16 * col) = R.c[i];
+    bool ok;
+    uint4 cv = R.c[i];
+    if (fp) {
+      ok = 32 * s + 4 * col < A.df;
+    } else {
+      ok = kRowBytes * si + 16 * col < A.di;
+      if (FMT == KM_SQ8) cv = flip4(cv);
+    }
+    *reinterpret_cast<uint4 *>(ct + row * kLdsStride + 16 * col) = mask4(cv, ok);
+    if (fp || FMT == KM_SQ8) {
+      uint4 pv = R.p[i];
+      if (!fp) pv = flip4(pv);
+      *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 16 * col) = mask4(pv, ok);
+    }
   }
-  const bool bitstage = Cfg<FMT>::kBits && !(Cfg<FMT>::kFp && s < SF);
-  if (bitstage) {
+  if (Cfg<FMT>::kBits && !fp) {
+    // each 32-bit code word widened to 32 bytes holding 0 or 1
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int w = t + kThreads * i;
       const int row = w >> 2, wi = w & 3;
-      *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 32 * wi) = R.p[2 * i];
-      *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 32 * wi + 16) = R.p[2 * i + 1];
+      const uint32_t bits = (32 * (4 * si + wi) < A.di) ? R.p[i].x : 0u;
+      *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 32 * wi) =
+          make_uint4(spread4(bits & 15u), spread4((bits >> 4) & 15u), spread4((bits >> 8) & 15u),
+                     spread4((bits >> 12) & 15u));
+      *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 32 * wi + 16) =
+          make_uint4(spread4((bits >> 16) & 15u), spread4((bits >> 20) & 15u), spread4((bits >> 24) & 15u),
+                     spread4(bits >> 28));
     }
-  } else {
+  }
+  if (s == 0 && t < kTile) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int cidx = t + kThreads * i;
-      const int row = cidx >> 3, col = cidx & 7;
-      *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 16 * col) = R.p[i];
-    }
+    for (int q = 0; q < 4; ++q) cpar[q * kTile + t] = R.cpar[q];
   }
 }
 
 template <int FMT>
-__global__ __launch_bounds__(kThreads) void assign_kernel(AssignArgs A) {
+__device__ __forceinline__ void mfma_stage_fp(const uint8_t *cbuf, const uint8_t *pbuf, int wc, int wp, int r, int h,
+                                              f32x16 (&facc)[2][2]) {
+  uint4 av[2][2], bv[2][2];  // [register set][block]
+#pragma unroll
+  for (int cb = 0; cb < 2; ++cb)
+    av[0][cb] = *reinterpret_cast<const uint4 *>(cbuf + (wc * 64 + cb * 32 + r) * kLdsStride + 16 * h);
+#pragma unroll
+  for (int pb = 0; pb < 2; ++pb)
+    bv[0][pb] = *reinterpret_cast<const uint4 *>(pbuf + (wp * 64 + pb * 32 + r) * kLdsStride + 16 * h);
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const int cur = g & 1, nxt = cur ^ 1;
+    if (g + 1 < 4) {
+#pragma unroll
+      for (int cb = 0; cb < 2; ++cb)
+        av[nxt][cb] = *reinterpret_cast<const uint4 *>(cbuf + (wc * 64 + cb * 32 + r) * kLdsStride + 32 * (g + 1) +
+                                                       16 * h);
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb)
+        bv[nxt][pb] = *reinterpret_cast<const uint4 *>(pbuf + (wp * 64 + pb * 32 + r) * kLdsStride + 32 * (g + 1) +
+                                                       16 * h);
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+#pragma unroll
+      for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+        for (int pb = 0; pb < 2; ++pb)
+          facc[cb][pb] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(av[cur][cb][e]),
+                                                              __uint_as_float(bv[cur][pb][e]), facc[cb][pb], 0, 0, 0);
+  }
+}
+
+__device__ __forceinline__ void mfma_stage_int(const uint8_t *cbuf, const uint8_t *pbuf, int wc, int wp, int r, int h,
+                                               i32x16 (&iacc)[2][2]) {
+  uint4 av[2][2], bv[2][2];
+#pragma unroll
+  for (int cb = 0; cb < 2; ++cb)
+    av[0][cb] = *reinterpret_cast<const uint4 *>(cbuf + (wc * 64 + cb * 32 + r) * kLdsStride + 16 * h);
+#pragma unroll
+  for (int pb = 0; pb < 2; ++pb)
+    bv[0][pb] = *reinterpret_cast<const uint4 *>(pbuf + (wp * 64 + pb * 32 + r) * kLdsStride + 16 * h);
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const int cur = g & 1, nxt = cur ^ 1;
+    if (g + 1 < 4) {
+#pragma unroll
+      for (int cb = 0; cb < 2; ++cb)
+        av[nxt][cb] = *reinterpret_cast<const uint4 *>(cbuf + (wc * 64 + cb * 32 + r) * kLdsStride + 32 * (g + 1) +
+                                                       16 * h);
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb)
+        bv[nxt][pb] = *reinterpret_cast<const uint4 *>(pbuf + (wp * 64 + pb * 32 + r) * kLdsStride + 32 * (g + 1) +
+                                                       16 * h);
+    }
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb) {
+        const i32x4 a4 = {(int)av[cur][cb].x, (int)av[cur][cb].y, (int)av[cur][cb].z, (int)av[cur][cb].w};
+        const i32x4 b4 = {(int)bv[cur][pb].x, (int)bv[cur][pb].y, (int)bv[cur][pb].z, (int)bv[cur][pb].w};
+        iacc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a4, b4, iacc[cb][pb], 0, 0, 0);
+      }
+  }
+}
+
+template <int FMT>
+__global__ __launch_bounds__(kThreads, FMT == KM_HYBRID ? 1 : 2) void assign_kernel(AssignArgs A) {
   __shared__ __align__(16) uint8_t lds[2 * kStageBytes];
+  __shared__ float cparl[2][4 * kTile];
   typedef typename std::conditional<Cfg<FMT>::kIntScore, int, float>::type score_t;
 
   const int t = threadIdx.x;
@@ -229,100 +328,58 @@ __global__ __launch_bounds__(kThreads) void assign_kernel(AssignArgs A) {
 
   StageRegs R;
   load_stage<FMT>(A, 0, SF, 0, p0, R);
-  store_stage<FMT>(0, SF, R, lds);
+  store_stage<FMT>(A, 0, SF, R, lds, cparl[0]);
   __syncthreads();
 
+  int ct = 0, s = 0;
   for (int it = 0; it < total; ++it) {
-    const int ct = it / S;
-    const int s = it - ct * S;
     const bool has_next = it + 1 < total;
-    if (has_next) {
-      const int nct_ = (it + 1) / S;
-      load_stage<FMT>(A, (it + 1) - nct_ * S, SF, (int64_t)nct_ * kTile, p0, R);
-    }
+    const int s_n = (s + 1 == S) ? 0 : s + 1;
+    const int ct_n = (s + 1 == S) ? ct + 1 : ct;
+    if (has_next) load_stage<FMT>(A, s_n, SF, (int64_t)ct_n * kTile, p0, R);
     const uint8_t *buf = lds + (it & 1) * kStageBytes;
-    const uint8_t *cbuf = buf;
-    const uint8_t *pbuf = buf + kTileBytes;
-    const bool fpstage = Cfg<FMT>::kFp && s < SF;
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      uint4 av[2], bv[2];
-#pragma unroll
-      for (int cb = 0; cb < 2; ++cb)
-        av[cb] = *reinterpret_cast<const uint4 *>(cbuf + (wc * 64 + cb * 32 + r) * kLdsStride + 32 * g + 16 * h);
-#pragma unroll
-      for (int pb = 0; pb < 2; ++pb)
-        bv[pb] = *reinterpret_cast<const uint4 *>(pbuf + (wp * 64 + pb * 32 + r) * kLdsStride + 32 * g + 16 * h);
-      if (fpstage) {
-        if constexpr (Cfg<FMT>::kFp) {
-#pragma unroll
-          for (int cb = 0; cb < 2; ++cb)
-#pragma unroll
-            for (int pb = 0; pb < 2; ++pb) {
-              facc[cb][pb] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(av[cb].x), __uint_as_float(bv[pb].x),
-                                                                  facc[cb][pb], 0, 0, 0);
-              facc[cb][pb] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(av[cb].y), __uint_as_float(bv[pb].y),
-                                                                  facc[cb][pb], 0, 0, 0);
-              facc[cb][pb] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(av[cb].z), __uint_as_float(bv[pb].z),
-                                                                  facc[cb][pb], 0, 0, 0);
-              facc[cb][pb] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(av[cb].w), __uint_as_float(bv[pb].w),
-                                                                  facc[cb][pb], 0, 0, 0);
-            }
-        }
-      } else {
-        if constexpr (Cfg<FMT>::kInt) {
-#pragma unroll
-          for (int cb = 0; cb < 2; ++cb)
-#pragma unroll
-            for (int pb = 0; pb < 2; ++pb) {
-              i32x4 a4 = {(int)av[cb].x, (int)av[cb].y, (int)av[cb].z, (int)av[cb].w};
-              i32x4 b4 = {(int)bv[pb].x, (int)bv[pb].y, (int)bv[pb].z, (int)bv[pb].w};
-              iacc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a4, b4, iacc[cb][pb], 0, 0, 0);
-            }
-        }
-      }
+    if (is_fp_stage<FMT>(s, SF)) {
+      if constexpr (Cfg<FMT>::kFp) mfma_stage_fp<FMT>(buf, buf + kTileBytes, wc, wp, r, h, facc);
+    } else {
+      if constexpr (Cfg<FMT>::kInt) mfma_stage_int(buf, buf + kTileBytes, wc, wp, r, h, iacc);
     }
 
     if (s == S - 1) {
       // epilogue for centroid tile ct: scores and running argmin, lane-local
       const int64_t c0 = (int64_t)ct * kTile;
+      const float *cp = cparl[ct & 1];
 #pragma unroll
       for (int cb = 0; cb < 2; ++cb) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int crow = wc * 64 + cb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
           const int64_t j = c0 + crow;
-          if (j < A.k) {
-            float cn = 0.f, u = 0.f, s2 = 0.f;
-            int qs = 0;
-            if (Cfg<FMT>::kFp) cn = A.cp.cn[j];
-            if (Cfg<FMT>::kInt) qs = A.cp.qsum[j];
-            if (Cfg<FMT>::kBits) {
-              u = A.cp.u[j];
-              s2 = A.cp.sig2[j];
-            }
+          const bool live = j < A.k;
+          const float cn = cp[crow];
+          const int qs = __float_as_int(cp[kTile + crow]);
+          const float u = cp[2 * kTile + crow];
+          const float s2 = cp[3 * kTile + crow];
 #pragma unroll
-            for (int pb = 0; pb < 2; ++pb) {
-              score_t sc;
-              if constexpr (FMT == KM_F32) {
-                sc = fmaf(-2.0f, facc[cb][pb][i], cn);
-              } else if constexpr (FMT == KM_SQ8) {
-                sc = qs - 2 * iacc[cb][pb][i];
-              } else if constexpr (FMT == KM_SIGN1) {
-                const int sd = 2 * iacc[cb][pb][i] - qs;
-                const float v = al[pb] * s2;
-                sc = fmaf(-v, (float)sd, u);
-              } else {
-                const int sd = 2 * iacc[cb][pb][i] - qs;
-                const float v = al[pb] * s2;
-                const float ts = fmaf(-v, (float)sd, u);
-                const float fs = fmaf(-2.0f, facc[cb][pb][i], cn);
-                sc = fs + ts;
-              }
-              if (sc < best[pb]) {
-                best[pb] = sc;
-                bidx[pb] = (int)j;
-              }
+          for (int pb = 0; pb < 2; ++pb) {
+            score_t sc;
+            if constexpr (FMT == KM_F32) {
+              sc = fmaf(-2.0f, facc[cb][pb][i], cn);
+            } else if constexpr (FMT == KM_SQ8) {
+              sc = qs - 2 * iacc[cb][pb][i];
+            } else if constexpr (FMT == KM_SIGN1) {
+              const int sd = 2 * iacc[cb][pb][i] - qs;
+              const float v = al[pb] * s2;
+              sc = fmaf(-v, (float)sd, u);
+            } else {
+              const int sd = 2 * iacc[cb][pb][i] - qs;
+              const float v = al[pb] * s2;
+              const float ts = fmaf(-v, (float)sd, u);
+              const float fs = fmaf(-2.0f, facc[cb][pb][i], cn);
+              sc = fs + ts;
+            }
+            if (live && sc < best[pb]) {
+              best[pb] = sc;
+              bidx[pb] = (int)j;
             }
           }
         }
@@ -339,8 +396,10 @@ __global__ __launch_bounds__(kThreads) void assign_kernel(AssignArgs A) {
         }
     }
 
-    if (has_next) store_stage<FMT>((it + 1) % S, SF, R, lds + ((it + 1) & 1) * kStageBytes);
+    if (has_next) store_stage<FMT>(A, s_n, SF, R, lds + ((it + 1) & 1) * kStageBytes, cparl[ct_n & 1]);
     __syncthreads();
+    s = s_n;
+    ct = ct_n;
   }
 
   // merge the two lane halves (rows 4h..), then the two centroid waves

@@ -50,6 +50,7 @@ struct UpdWs {
   void *Z;       // [k * dp] float or uint8
   uint8_t *fresh;  // [k]
   int64_t *cntw;   // [k]
+  int *empties;    // [k]
 };
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -79,6 +80,7 @@ UpdWs carve(const Points &P, int k, void *base, size_t *bytes_out) {
   w.Z = take(sizeof(float) * (size_t)k * (size_t)w.dp);
   w.fresh = (uint8_t *)take((size_t)k);
   w.cntw = (int64_t *)take(sizeof(int64_t) * (size_t)k);
+  w.empties = (int *)take(sizeof(int) * (size_t)k);
   if (bytes_out) *bytes_out = o;
   return w;
 }
@@ -395,17 +397,34 @@ __global__ __launch_bounds__(256) void finalize_sq8_kernel(const int *partial, i
 }
 
 // ---- 6. empty-cluster split (one workgroup) -----------------------------------
+// The empty clusters are first listed in ascending order (block scan over the
+// counts); the split itself is inherently sequential (each donor choice sees the
+// counts left by the previous split) and runs over that list only.
 template <bool CODES>
 __global__ __launch_bounds__(256) void split_kernel(void *Zv, int k, int dp, const int *cnt, int64_t *cntw,
-                                                    uint8_t *fresh) {
+                                                    uint8_t *fresh, int *empties) {
   __shared__ int64_t sv[256];
   __shared__ int si[256];
+  __shared__ int shs[256];
+  __shared__ int n_empty;
   const int t = threadIdx.x;
+  const int per = (k + 255) / 256;
+  const int lo = min(k, t * per), hi = min(k, lo + per);
+  int mine = 0;
+  for (int j = lo; j < hi; ++j) mine += cnt[j] == 0;
+  int tot;
+  int pos = block_excl_scan_int(mine, shs, &tot);
+  for (int j = lo; j < hi; ++j)
+    if (cnt[j] == 0) empties[pos++] = j;
+  if (t == 0) n_empty = tot;
+  __syncthreads();
+  const int ne = n_empty;
+  if (ne == 0) return;
   for (int j = t; j < k; j += 256) cntw[j] = cnt[j];
   __syncthreads();
   const float up = 1.0f + 0x1p-10f, dn = 1.0f - 0x1p-10f;
-  for (int j = 0; j < k; ++j) {
-    if (cnt[j] != 0) continue;  // uniform
+  for (int e = 0; e < ne; ++e) {
+    const int j = empties[e];
     int64_t bv = -1;
     int bi = 0;
     for (int i = t; i < k; i += 256) {
@@ -542,9 +561,11 @@ km_status launch_update(const Points &P, const int32_t *assign, int k, void *C, 
 
   if (policy == KM_EMPTY_SPLIT) {
     if (P.fmt == KM_SQ8)
-      hipLaunchKernelGGL(split_kernel<true>, dim3(1), dim3(256), 0, s, w.Z, k, w.dp, w.cnt, w.cntw, w.fresh);
+      hipLaunchKernelGGL(split_kernel<true>, dim3(1), dim3(256), 0, s, w.Z, k, w.dp, w.cnt, w.cntw, w.fresh,
+                         w.empties);
     else
-      hipLaunchKernelGGL(split_kernel<false>, dim3(1), dim3(256), 0, s, w.Z, k, w.dp, w.cnt, w.cntw, w.fresh);
+      hipLaunchKernelGGL(split_kernel<false>, dim3(1), dim3(256), 0, s, w.Z, k, w.dp, w.cnt, w.cntw, w.fresh,
+                         w.empties);
   }
   const dim3 g(k, (unsigned)cdiv(d, 256));
   const int d0 = P.fmt == KM_HYBRID ? P.d_front : 0;
