@@ -331,75 +331,72 @@ __global__ __launch_bounds__(kThreads, FMT == KM_HYBRID ? 1 : 2) void assign_ker
   store_stage<FMT>(A, 0, SF, R, lds, cparl[0]);
   __syncthreads();
 
-  int ct = 0, s = 0;
-  for (int it = 0; it < total; ++it) {
-    const bool has_next = it + 1 < total;
-    const int s_n = (s + 1 == S) ? 0 : s + 1;
-    const int ct_n = (s + 1 == S) ? ct + 1 : ct;
-    if (has_next) load_stage<FMT>(A, s_n, SF, (int64_t)ct_n * kTile, p0, R);
-    const uint8_t *buf = lds + (it & 1) * kStageBytes;
-    if (is_fp_stage<FMT>(s, SF)) {
-      if constexpr (Cfg<FMT>::kFp) mfma_stage_fp<FMT>(buf, buf + kTileBytes, wc, wp, r, h, facc);
-    } else {
-      if constexpr (Cfg<FMT>::kInt) mfma_stage_int(buf, buf + kTileBytes, wc, wp, r, h, iacc);
+  for (int ct = 0; ct < nct; ++ct) {
+    for (int s = 0; s < S; ++s) {
+      const int it = ct * S + s;
+      const bool has_next = it + 1 < total;
+      const int s_n = (s + 1 == S) ? 0 : s + 1;
+      const int ct_n = (s + 1 == S) ? ct + 1 : ct;
+      if (has_next) load_stage<FMT>(A, s_n, SF, (int64_t)ct_n * kTile, p0, R);
+      const uint8_t *buf = lds + (it & 1) * kStageBytes;
+      if (is_fp_stage<FMT>(s, SF)) {
+        if constexpr (Cfg<FMT>::kFp) mfma_stage_fp<FMT>(buf, buf + kTileBytes, wc, wp, r, h, facc);
+      } else {
+        if constexpr (Cfg<FMT>::kInt) mfma_stage_int(buf, buf + kTileBytes, wc, wp, r, h, iacc);
+      }
+      if (has_next) store_stage<FMT>(A, s_n, SF, R, lds + ((it + 1) & 1) * kStageBytes, cparl[ct_n & 1]);
+      __syncthreads();
     }
 
-    if (s == S - 1) {
-      // epilogue for centroid tile ct: scores and running argmin, lane-local
-      const int64_t c0 = (int64_t)ct * kTile;
-      const float *cp = cparl[ct & 1];
+    // epilogue for centroid tile ct: scores and running argmin, lane-local
+    const int64_t c0 = (int64_t)ct * kTile;
+    const float *cp = cparl[ct & 1];
 #pragma unroll
-      for (int cb = 0; cb < 2; ++cb) {
+    for (int cb = 0; cb < 2; ++cb) {
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int crow = wc * 64 + cb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
-          const int64_t j = c0 + crow;
-          const bool live = j < A.k;
-          const float cn = cp[crow];
-          const int qs = __float_as_int(cp[kTile + crow]);
-          const float u = cp[2 * kTile + crow];
-          const float s2 = cp[3 * kTile + crow];
+      for (int i = 0; i < 16; ++i) {
+        const int crow = wc * 64 + cb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
+        const int64_t j = c0 + crow;
+        const bool live = j < A.k;
+        const float cn = cp[crow];
+        const int qs = __float_as_int(cp[kTile + crow]);
+        const float u = cp[2 * kTile + crow];
+        const float s2 = cp[3 * kTile + crow];
 #pragma unroll
-          for (int pb = 0; pb < 2; ++pb) {
-            score_t sc;
-            if constexpr (FMT == KM_F32) {
-              sc = fmaf(-2.0f, facc[cb][pb][i], cn);
-            } else if constexpr (FMT == KM_SQ8) {
-              sc = qs - 2 * iacc[cb][pb][i];
-            } else if constexpr (FMT == KM_SIGN1) {
-              const int sd = 2 * iacc[cb][pb][i] - qs;
-              const float v = al[pb] * s2;
-              sc = fmaf(-v, (float)sd, u);
-            } else {
-              const int sd = 2 * iacc[cb][pb][i] - qs;
-              const float v = al[pb] * s2;
-              const float ts = fmaf(-v, (float)sd, u);
-              const float fs = fmaf(-2.0f, facc[cb][pb][i], cn);
-              sc = fs + ts;
-            }
-            if (live && sc < best[pb]) {
-              best[pb] = sc;
-              bidx[pb] = (int)j;
-            }
+        for (int pb = 0; pb < 2; ++pb) {
+          score_t sc;
+          if constexpr (FMT == KM_F32) {
+            sc = fmaf(-2.0f, facc[cb][pb][i], cn);
+          } else if constexpr (FMT == KM_SQ8) {
+            sc = qs - 2 * iacc[cb][pb][i];
+          } else if constexpr (FMT == KM_SIGN1) {
+            const int sd = 2 * iacc[cb][pb][i] - qs;
+            const float v = al[pb] * s2;
+            sc = fmaf(-v, (float)sd, u);
+          } else {
+            const int sd = 2 * iacc[cb][pb][i] - qs;
+            const float v = al[pb] * s2;
+            const float ts = fmaf(-v, (float)sd, u);
+            const float fs = fmaf(-2.0f, facc[cb][pb][i], cn);
+            sc = fs + ts;
+          }
+          if (live && sc < best[pb]) {
+            best[pb] = sc;
+            bidx[pb] = (int)j;
           }
         }
       }
-#pragma unroll
-      for (int a = 0; a < 2; ++a)
-#pragma unroll
-        for (int b = 0; b < 2; ++b) {
-#pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            facc[a][b][i] = 0.f;
-            iacc[a][b][i] = 0;
-          }
-        }
     }
-
-    if (has_next) store_stage<FMT>(A, s_n, SF, R, lds + ((it + 1) & 1) * kStageBytes, cparl[ct_n & 1]);
-    __syncthreads();
-    s = s_n;
-    ct = ct_n;
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          facc[a][b][i] = 0.f;
+          iacc[a][b][i] = 0;
+        }
+      }
   }
 
   // merge the two lane halves (rows 4h..), then the two centroid waves
@@ -426,6 +423,259 @@ __global__ __launch_bounds__(kThreads, FMT == KM_HYBRID ? 1 : 2) void assign_ker
 #pragma unroll
     for (int pb = 0; pb < 2; ++pb) {
       const int pc = wp * 64 + pb * 32 + r;
+      const score_t os = ms[pc];
+      const int oi = mi[pc];
+      if (os < best[pb] || (os == best[pb] && oi < bidx[pb])) {
+        best[pb] = os;
+        bidx[pb] = oi;
+      }
+      const int64_t p = p0 + pc;
+      if (p < A.n) {
+        A.assign[p] = bidx[pb];
+        if (A.score) A.score[p] = (float)best[pb];
+      }
+    }
+  }
+}
+
+// ---- int8 assignment with 256 x 256 workgroup tiles ---------------------------
+// SQ8 and 1-bit points.  An int8 MFMA (32x32x32) is 32x denser than the fp32 one,
+// so operand bandwidth, not the matrix core, limits the 128-tile kernel.  Here each
+// wave owns 128 centroids x 128 points (4 x 4 blocks, 256 int32 accumulators) and
+// the workgroup 256 x 256: per MFMA a wave reads half the LDS bytes and the
+// workgroup a quarter of the L2 bytes of the 2 x 2 layout.
+constexpr int kT8 = 256;
+constexpr int kTileBytes8 = kT8 * kLdsStride;  // 36864
+constexpr int kStageBytes8 = 2 * kTileBytes8;  // 73728
+
+struct Stage8 {
+  uint4 c[8];
+  uint4 p[8];
+  float cpar[4];
+};
+
+template <int FMT>
+__device__ __forceinline__ void load_stage8(const AssignArgs &A, int s, int64_t c0, int64_t p0, Stage8 &R) {
+  const int t = threadIdx.x;
+  const int b0 = kRowBytes * s;
+  // uniform tile bases + 32-bit per-thread offsets (rows clamped into the data)
+  const int8_t *cbase = A.ci8 + c0 * A.cild;
+  const int crmax = (int)min<int64_t>(A.k - 1 - c0, kT8 - 1);
+  const uint8_t *pbase8 = A.pi8 + p0 * A.pild;
+  const uint32_t *pbaseb = A.pbits + p0 * A.pbw + A.pbw0;
+  const int prmax = (int)min<int64_t>(A.n - 1 - p0, kT8 - 1);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int cidx = t + kThreads * i;
+    const int row = cidx >> 3, col = cidx & 7;
+    const int b = b0 + 16 * col;
+    const int bc = b < A.di ? b : 0;
+    R.c[i] = *reinterpret_cast<const uint4 *>(cbase + (uint32_t)(min(row, crmax) * (int)A.cild + bc));
+    if (FMT == KM_SQ8)
+      R.p[i] = *reinterpret_cast<const uint4 *>(pbase8 + (uint32_t)(min(row, prmax) * (int)A.pild + bc));
+  }
+  if (FMT == KM_SIGN1) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int w = t + kThreads * i;
+      const int row = w >> 2, wi = w & 3;
+      const int word = 4 * s + wi;
+      R.p[i].x = pbaseb[(uint32_t)(min(row, prmax) * (int)A.pbw + (32 * word < A.di ? word : 0))];
+    }
+  }
+  if (s == 0) {
+    const int64_t j = min<int64_t>(c0 + t, A.k - 1);
+    R.cpar[1] = __int_as_float(A.cp.qsum[j]);
+    if (FMT == KM_SIGN1) {
+      R.cpar[2] = A.cp.u[j];
+      R.cpar[3] = A.cp.sig2[j];
+    }
+  }
+}
+
+template <int FMT>
+__device__ __forceinline__ void store_stage8(const AssignArgs &A, int s, const Stage8 &R, uint8_t *buf, float *cpar) {
+  const int t = threadIdx.x;
+  uint8_t *ct = buf;
+  uint8_t *pt = buf + kTileBytes8;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int cidx = t + kThreads * i;
+    const int row = cidx >> 3, col = cidx & 7;
+    const bool ok = kRowBytes * s + 16 * col < A.di;
+    uint4 cv = R.c[i];
+    if (FMT == KM_SQ8) cv = flip4(cv);
+    *reinterpret_cast<uint4 *>(ct + row * kLdsStride + 16 * col) = mask4(cv, ok);
+    if (FMT == KM_SQ8)
+      *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 16 * col) = mask4(flip4(R.p[i]), ok);
+  }
+  if (FMT == KM_SIGN1) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int w = t + kThreads * i;
+      const int row = w >> 2, wi = w & 3;
+      const uint32_t bits = (32 * (4 * s + wi) < A.di) ? R.p[i].x : 0u;
+      *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 32 * wi) =
+          make_uint4(spread4(bits & 15u), spread4((bits >> 4) & 15u), spread4((bits >> 8) & 15u),
+                     spread4((bits >> 12) & 15u));
+      *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 32 * wi + 16) =
+          make_uint4(spread4((bits >> 16) & 15u), spread4((bits >> 20) & 15u), spread4((bits >> 24) & 15u),
+                     spread4(bits >> 28));
+    }
+  }
+  if (s == 0) {
+#pragma unroll
+    for (int q = 1; q < 4; ++q) cpar[q * kT8 + t] = R.cpar[q];
+  }
+}
+
+__device__ __forceinline__ void mfma_stage8(const uint8_t *cbuf, const uint8_t *pbuf, int wc, int wp, int r, int h,
+                                            i32x16 (&acc)[4][4]) {
+  uint4 av[2][4], bv[2][4];
+#pragma unroll
+  for (int cb = 0; cb < 4; ++cb)
+    av[0][cb] = *reinterpret_cast<const uint4 *>(cbuf + (wc * 128 + cb * 32 + r) * kLdsStride + 16 * h);
+#pragma unroll
+  for (int pb = 0; pb < 4; ++pb)
+    bv[0][pb] = *reinterpret_cast<const uint4 *>(pbuf + (wp * 128 + pb * 32 + r) * kLdsStride + 16 * h);
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const int cur = g & 1, nxt = cur ^ 1;
+    if (g + 1 < 4) {
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb)
+        av[nxt][cb] = *reinterpret_cast<const uint4 *>(cbuf + (wc * 128 + cb * 32 + r) * kLdsStride + 32 * (g + 1) +
+                                                       16 * h);
+#pragma unroll
+      for (int pb = 0; pb < 4; ++pb)
+        bv[nxt][pb] = *reinterpret_cast<const uint4 *>(pbuf + (wp * 128 + pb * 32 + r) * kLdsStride + 32 * (g + 1) +
+                                                       16 * h);
+    }
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+      for (int pb = 0; pb < 4; ++pb) {
+        const i32x4 a4 = {(int)av[cur][cb].x, (int)av[cur][cb].y, (int)av[cur][cb].z, (int)av[cur][cb].w};
+        const i32x4 b4 = {(int)bv[cur][pb].x, (int)bv[cur][pb].y, (int)bv[cur][pb].z, (int)bv[cur][pb].w};
+        acc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a4, b4, acc[cb][pb], 0, 0, 0);
+      }
+  }
+}
+
+template <int FMT>
+__global__ __launch_bounds__(kThreads, 1) void assign_i8_kernel(AssignArgs A) {
+  __shared__ __align__(16) uint8_t lds[2 * kStageBytes8];
+  __shared__ float cparl[2][4 * kT8];
+  typedef typename std::conditional<FMT == KM_SQ8, int, float>::type score_t;
+
+  const int t = threadIdx.x;
+  const int lane = t & 63, wave = t >> 6;
+  const int r = lane & 31, h = lane >> 5;
+  const int wc = wave & 1, wp = wave >> 1;
+  const int64_t p0 = (int64_t)blockIdx.x * kT8;
+
+  const int S = (A.di + kRowBytes - 1) / kRowBytes;
+  const int nct = (A.k + kT8 - 1) / kT8;
+  const int total = nct * S;
+
+  float al[4] = {0.f, 0.f, 0.f, 0.f};
+  if (FMT == KM_SIGN1) {
+#pragma unroll
+    for (int pb = 0; pb < 4; ++pb) al[pb] = A.alpha[min<int64_t>(p0 + wp * 128 + pb * 32 + r, A.n - 1)];
+  }
+  i32x16 acc[4][4];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc[a][b][i] = 0;
+
+  score_t best[4];
+  int bidx[4];
+#pragma unroll
+  for (int pb = 0; pb < 4; ++pb) {
+    best[pb] = FMT == KM_SQ8 ? (score_t)INT_MAX : (score_t)INFINITY;
+    bidx[pb] = INT_MAX;
+  }
+
+  Stage8 R;
+  load_stage8<FMT>(A, 0, 0, p0, R);
+  store_stage8<FMT>(A, 0, R, lds, cparl[0]);
+  __syncthreads();
+
+  for (int ct = 0; ct < nct; ++ct) {
+    for (int s = 0; s < S; ++s) {
+      const int it = ct * S + s;
+      const bool has_next = it + 1 < total;
+      const int s_n = (s + 1 == S) ? 0 : s + 1;
+      const int ct_n = (s + 1 == S) ? ct + 1 : ct;
+      if (has_next) load_stage8<FMT>(A, s_n, (int64_t)ct_n * kT8, p0, R);
+      const uint8_t *buf = lds + (it & 1) * kStageBytes8;
+      mfma_stage8(buf, buf + kTileBytes8, wc, wp, r, h, acc);
+      if (has_next) store_stage8<FMT>(A, s_n, R, lds + ((it + 1) & 1) * kStageBytes8, cparl[ct_n & 1]);
+      __syncthreads();
+    }
+    const int64_t c0 = (int64_t)ct * kT8;
+    const float *cp = cparl[ct & 1];
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int crow = wc * 128 + cb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
+        const int64_t j = c0 + crow;
+        const bool live = j < A.k;
+        const int qs = __float_as_int(cp[kT8 + crow]);
+        const float u = cp[2 * kT8 + crow];
+        const float s2 = cp[3 * kT8 + crow];
+#pragma unroll
+        for (int pb = 0; pb < 4; ++pb) {
+          score_t sc;
+          if constexpr (FMT == KM_SQ8) {
+            sc = qs - 2 * acc[cb][pb][i];
+          } else {
+            const int sd = 2 * acc[cb][pb][i] - qs;
+            const float v = al[pb] * s2;
+            sc = fmaf(-v, (float)sd, u);
+          }
+          if (live && sc < best[pb]) {
+            best[pb] = sc;
+            bidx[pb] = (int)j;
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int b = 0; b < 4; ++b)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[a][b][i] = 0;
+  }
+
+#pragma unroll
+  for (int pb = 0; pb < 4; ++pb) {
+    score_t os = __shfl_xor(best[pb], 32);
+    int oi = __shfl_xor(bidx[pb], 32);
+    if (os < best[pb] || (os == best[pb] && oi < bidx[pb])) {
+      best[pb] = os;
+      bidx[pb] = oi;
+    }
+  }
+  score_t *ms = reinterpret_cast<score_t *>(lds);
+  int *mi = reinterpret_cast<int *>(lds + kT8 * sizeof(score_t));
+  if (wc == 1 && h == 0) {
+#pragma unroll
+    for (int pb = 0; pb < 4; ++pb) {
+      ms[wp * 128 + pb * 32 + r] = best[pb];
+      mi[wp * 128 + pb * 32 + r] = bidx[pb];
+    }
+  }
+  __syncthreads();
+  if (wc == 0 && h == 0) {
+#pragma unroll
+    for (int pb = 0; pb < 4; ++pb) {
+      const int pc = wp * 128 + pb * 32 + r;
       const score_t os = ms[pc];
       const int oi = mi[pc];
       if (os < best[pb] || (os == best[pb] && oi < bidx[pb])) {
@@ -663,8 +913,11 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
     A.cild = P.d - d0;
     A.di = P.d - d0;
   }
-  const int64_t nblk = cdiv(P.n, kTile);
-  hipLaunchKernelGGL(assign_kernel<FMT>, dim3((unsigned)nblk), dim3(kThreads), 0, s, A);
+  if constexpr (FMT == KM_SQ8 || FMT == KM_SIGN1) {
+    hipLaunchKernelGGL(assign_i8_kernel<FMT>, dim3((unsigned)cdiv(P.n, kT8)), dim3(kThreads), 0, s, A);
+  } else {
+    hipLaunchKernelGGL(assign_kernel<FMT>, dim3((unsigned)cdiv(P.n, kTile)), dim3(kThreads), 0, s, A);
+  }
   KMQ_LAUNCH_CHECK("assign_kernel");
   return KM_OK;
 }

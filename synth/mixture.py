@@ -114,7 +114,7 @@ def for_each_chunk(spec: MixtureSpec, fn, threads: int | None = None):
     def work(c):
         fn(c * CHUNK, make_chunk(spec, c, ml))
 
-    threads = threads or min(8, os.cpu_count() or 1, nc)
+    threads = threads or min(16, os.cpu_count() or 1, nc)
     if threads <= 1 or nc == 1:
         for c in range(nc):
             work(c)
