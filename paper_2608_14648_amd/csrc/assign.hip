@@ -42,11 +42,8 @@ namespace kmq {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kTile = 128;                      // centroids per tile and points per workgroup
-constexpr int kRowBytes = 128;                  // bytes of one row per stage
-constexpr int kLdsStride = kRowBytes + 16;      // padded to spread LDS banks
-constexpr int kTileBytes = kTile * kLdsStride;  // 18432
-constexpr int kStageBytes = 2 * kTileBytes;     // centroid tile + point tile
+constexpr int kRowBytes = 128;              // bytes of one row per stage
+constexpr int kLdsStride = kRowBytes + 16;  // padded to spread LDS banks
 
 struct AssignArgs {
   // fp32 phase: F32 points, hybrid front
@@ -87,10 +84,26 @@ struct Cfg {
 
 // Raw loads of one stage (consumed only when the stage is written to LDS, one MFMA
 // stage later, so the global latency hides under the matrix work).
+// Tile geometry: waves are 2 (centroid halves) x 2 (point halves); each wave owns
+// CB x PB blocks of 32 x 32, so a tile holds TC = 64 CB centroids and the
+// workgroup TP = 64 PB points.
+template <int CB, int PB>
+struct Geo {
+  static constexpr int TC = 64 * CB;
+  static constexpr int TP = 64 * PB;
+  static constexpr int CBYTES = TC * kLdsStride;
+  static constexpr int PBYTES = TP * kLdsStride;
+  static constexpr int STAGE = CBYTES + PBYTES;
+  static constexpr int NC = TC / 32;  // 16-byte chunks of centroid rows per thread per stage
+  static constexpr int NP = TP / 32;
+  static_assert(TC <= kThreads, "one thread per tile centroid for the per-tile constants");
+};
+
+template <int CB, int PB>
 struct StageRegs {
-  uint4 c[4];
-  uint4 p[4];
-  float cpar[4];  // per-centroid constants of the next tile (threads < 128, stage 0 only)
+  uint4 c[Geo<CB, PB>::NC];
+  uint4 p[Geo<CB, PB>::NP];
+  float cpar[4];  // per-centroid constants of the next tile (stage 0 only)
 };
 
 __device__ __forceinline__ uint4 mask4(uint4 v, bool ok) {
@@ -111,92 +124,117 @@ __device__ __forceinline__ bool is_fp_stage(int s, int SF) {
 
 // Every address is clamped into its buffer; lanes outside the data are zeroed at
 // store time, so the loads are unconditional and branch-free.
-template <int FMT>
+template <int FMT, int CB, int PB>
 __device__ __forceinline__ void load_stage(const AssignArgs &A, int s, int SF, int64_t c0, int64_t p0,
-                                           StageRegs &R) {
+                                           StageRegs<CB, PB> &R) {
+  typedef Geo<CB, PB> G;
   const int t = threadIdx.x;
+  const int crmax = (int)min<int64_t>(A.k - 1 - c0, G::TC - 1);
+  const int prmax = (int)min<int64_t>(A.n - 1 - p0, G::TP - 1);
   if (is_fp_stage<FMT>(s, SF)) {
+    const float *cbase = A.cf + c0 * A.cfld;
+    const float *pbase = A.pf + p0 * A.pfld;
     const int dim0 = 32 * s;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < G::NC; ++i) {
       const int cidx = t + kThreads * i;
       const int row = cidx >> 3, col = cidx & 7;
       const int dim = dim0 + 4 * col;
       const int dimc = dim < A.df ? dim : 0;
-      const int64_t cr = min<int64_t>(c0 + row, A.k - 1);
-      const int64_t pr = min<int64_t>(p0 + row, A.n - 1);
-      R.c[i] = *reinterpret_cast<const uint4 *>(A.cf + cr * A.cfld + dimc);
-      R.p[i] = *reinterpret_cast<const uint4 *>(A.pf + pr * A.pfld + dimc);
+      R.c[i] = *reinterpret_cast<const uint4 *>(cbase + (uint32_t)(min(row, crmax) * (int)A.cfld + dimc));
+    }
+#pragma unroll
+    for (int i = 0; i < G::NP; ++i) {
+      const int cidx = t + kThreads * i;
+      const int row = cidx >> 3, col = cidx & 7;
+      const int dim = dim0 + 4 * col;
+      const int dimc = dim < A.df ? dim : 0;
+      R.p[i] = *reinterpret_cast<const uint4 *>(pbase + (uint32_t)(min(row, prmax) * (int)A.pfld + dimc));
     }
   } else if constexpr (Cfg<FMT>::kInt) {
     const int si = s - (Cfg<FMT>::kFp ? SF : 0);
     const int b0 = kRowBytes * si;
+    const int8_t *cbase = A.ci8 + c0 * A.cild;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < G::NC; ++i) {
       const int cidx = t + kThreads * i;
       const int row = cidx >> 3, col = cidx & 7;
       const int b = b0 + 16 * col;
       const int bc = b < A.di ? b : 0;
-      const int64_t cr = min<int64_t>(c0 + row, A.k - 1);
-      R.c[i] = *reinterpret_cast<const uint4 *>(A.ci8 + cr * A.cild + bc);
-      if (FMT == KM_SQ8) {
-        const int64_t pr = min<int64_t>(p0 + row, A.n - 1);
-        R.p[i] = *reinterpret_cast<const uint4 *>(A.pi8 + pr * A.pild + bc);
+      R.c[i] = *reinterpret_cast<const uint4 *>(cbase + (uint32_t)(min(row, crmax) * (int)A.cild + bc));
+    }
+    if (FMT == KM_SQ8) {
+      const uint8_t *pbase = A.pi8 + p0 * A.pild;
+#pragma unroll
+      for (int i = 0; i < G::NP; ++i) {
+        const int cidx = t + kThreads * i;
+        const int row = cidx >> 3, col = cidx & 7;
+        const int b = b0 + 16 * col;
+        const int bc = b < A.di ? b : 0;
+        R.p[i] = *reinterpret_cast<const uint4 *>(pbase + (uint32_t)(min(row, prmax) * (int)A.pild + bc));
       }
     }
     if (Cfg<FMT>::kBits) {
+      // TP rows x 4 words; NP/2 words per thread, kept in the .x lanes
+      const uint32_t *pbase = A.pbits + p0 * A.pbw + A.pbw0;
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
+      for (int i = 0; i < G::NP / 2; ++i) {
         const int w = t + kThreads * i;
         const int row = w >> 2, wi = w & 3;
         const int word = 4 * si + wi;
-        const int64_t pr = min<int64_t>(p0 + row, A.n - 1);
-        R.p[i].x = A.pbits[pr * A.pbw + A.pbw0 + (32 * word < A.di ? word : 0)];
+        R.p[i].x = pbase[(uint32_t)(min(row, prmax) * (int)A.pbw + (32 * word < A.di ? word : 0))];
       }
     }
   }
-  if (s == 0 && t < kTile) {
-    const int64_t j = min<int64_t>(c0 + t, A.k - 1);
-    if (Cfg<FMT>::kFp) R.cpar[0] = A.cp.cn[j];
-    if (Cfg<FMT>::kInt) R.cpar[1] = __int_as_float(A.cp.qsum[j]);
-    if (Cfg<FMT>::kBits) {
-      R.cpar[2] = A.cp.u[j];
-      R.cpar[3] = A.cp.sig2[j];
+  if (s == 0) {
+#pragma unroll
+    for (int q = 0; q < G::TC / kThreads + (G::TC % kThreads ? 1 : 0); ++q) {
+      const int jt = t + kThreads * q;
+      if (jt < G::TC) {
+        const int64_t j = c0 + min(jt, crmax);
+        if (Cfg<FMT>::kFp) R.cpar[0] = A.cp.cn[j];
+        if (Cfg<FMT>::kInt) R.cpar[1] = __int_as_float(A.cp.qsum[j]);
+        if (Cfg<FMT>::kBits) {
+          R.cpar[2] = A.cp.u[j];
+          R.cpar[3] = A.cp.sig2[j];
+        }
+      }
     }
   }
 }
 
-template <int FMT>
-__device__ __forceinline__ void store_stage(const AssignArgs &A, int s, int SF, const StageRegs &R, uint8_t *buf,
-                                            float *cpar) {
+template <int FMT, int CB, int PB>
+__device__ __forceinline__ void store_stage(const AssignArgs &A, int s, int SF, const StageRegs<CB, PB> &R,
+                                            uint8_t *buf, float *cpar) {
+  typedef Geo<CB, PB> G;
   const int t = threadIdx.x;
   uint8_t *ct = buf;
-  uint8_t *pt = buf + kTileBytes;
+  uint8_t *pt = buf + G::CBYTES;
   const bool fp = is_fp_stage<FMT>(s, SF);
   const int si = s - (Cfg<FMT>::kFp ? SF : 0);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < G::NC; ++i) {
     const int cidx = t + kThreads * i;
     const int row = cidx >> 3, col = cidx & 7;
-    bool ok;
+    const bool ok = fp ? (32 * s + 4 * col < A.df) : (kRowBytes * si + 16 * col < A.di);
     uint4 cv = R.c[i];
-    if (fp) {
-      ok = 32 * s + 4 * col < A.df;
-    } else {
-      ok = kRowBytes * si + 16 * col < A.di;
-      if (FMT == KM_SQ8) cv = flip4(cv);
-    }
+    if (FMT == KM_SQ8) cv = flip4(cv);
     *reinterpret_cast<uint4 *>(ct + row * kLdsStride + 16 * col) = mask4(cv, ok);
-    if (fp || FMT == KM_SQ8) {
+  }
+  if (fp || FMT == KM_SQ8) {
+#pragma unroll
+    for (int i = 0; i < G::NP; ++i) {
+      const int cidx = t + kThreads * i;
+      const int row = cidx >> 3, col = cidx & 7;
+      const bool ok = fp ? (32 * s + 4 * col < A.df) : (kRowBytes * si + 16 * col < A.di);
       uint4 pv = R.p[i];
       if (!fp) pv = flip4(pv);
       *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 16 * col) = mask4(pv, ok);
     }
-  }
-  if (Cfg<FMT>::kBits && !fp) {
+  } else if (Cfg<FMT>::kBits) {
     // each 32-bit code word widened to 32 bytes holding 0 or 1
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < G::NP / 2; ++i) {
       const int w = t + kThreads * i;
       const int row = w >> 2, wi = w & 3;
       const uint32_t bits = (32 * (4 * si + wi) < A.di) ? R.p[i].x : 0u;
@@ -208,109 +246,106 @@ __device__ __forceinline__ void store_stage(const AssignArgs &A, int s, int SF, 
                      spread4(bits >> 28));
     }
   }
-  if (s == 0 && t < kTile) {
+  if (s == 0) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) cpar[q * kTile + t] = R.cpar[q];
-  }
-}
-
-template <int FMT>
-__device__ __forceinline__ void mfma_stage_fp(const uint8_t *cbuf, const uint8_t *pbuf, int wc, int wp, int r, int h,
-                                              f32x16 (&facc)[2][2]) {
-  uint4 av[2][2], bv[2][2];  // [register set][block]
+    for (int q = 0; q < G::TC / kThreads + (G::TC % kThreads ? 1 : 0); ++q) {
+      const int jt = t + kThreads * q;
+      if (jt < G::TC) {
 #pragma unroll
-  for (int cb = 0; cb < 2; ++cb)
-    av[0][cb] = *reinterpret_cast<const uint4 *>(cbuf + (wc * 64 + cb * 32 + r) * kLdsStride + 16 * h);
-#pragma unroll
-  for (int pb = 0; pb < 2; ++pb)
-    bv[0][pb] = *reinterpret_cast<const uint4 *>(pbuf + (wp * 64 + pb * 32 + r) * kLdsStride + 16 * h);
-#pragma unroll
-  for (int g = 0; g < 4; ++g) {
-    const int cur = g & 1, nxt = cur ^ 1;
-    if (g + 1 < 4) {
-#pragma unroll
-      for (int cb = 0; cb < 2; ++cb)
-        av[nxt][cb] = *reinterpret_cast<const uint4 *>(cbuf + (wc * 64 + cb * 32 + r) * kLdsStride + 32 * (g + 1) +
-                                                       16 * h);
-#pragma unroll
-      for (int pb = 0; pb < 2; ++pb)
-        bv[nxt][pb] = *reinterpret_cast<const uint4 *>(pbuf + (wp * 64 + pb * 32 + r) * kLdsStride + 32 * (g + 1) +
-                                                       16 * h);
-    }
-#pragma unroll
-    for (int e = 0; e < 4; ++e)
-#pragma unroll
-      for (int cb = 0; cb < 2; ++cb)
-#pragma unroll
-        for (int pb = 0; pb < 2; ++pb)
-          facc[cb][pb] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(av[cur][cb][e]),
-                                                              __uint_as_float(bv[cur][pb][e]), facc[cb][pb], 0, 0, 0);
-  }
-}
-
-__device__ __forceinline__ void mfma_stage_int(const uint8_t *cbuf, const uint8_t *pbuf, int wc, int wp, int r, int h,
-                                               i32x16 (&iacc)[2][2]) {
-  uint4 av[2][2], bv[2][2];
-#pragma unroll
-  for (int cb = 0; cb < 2; ++cb)
-    av[0][cb] = *reinterpret_cast<const uint4 *>(cbuf + (wc * 64 + cb * 32 + r) * kLdsStride + 16 * h);
-#pragma unroll
-  for (int pb = 0; pb < 2; ++pb)
-    bv[0][pb] = *reinterpret_cast<const uint4 *>(pbuf + (wp * 64 + pb * 32 + r) * kLdsStride + 16 * h);
-#pragma unroll
-  for (int g = 0; g < 4; ++g) {
-    const int cur = g & 1, nxt = cur ^ 1;
-    if (g + 1 < 4) {
-#pragma unroll
-      for (int cb = 0; cb < 2; ++cb)
-        av[nxt][cb] = *reinterpret_cast<const uint4 *>(cbuf + (wc * 64 + cb * 32 + r) * kLdsStride + 32 * (g + 1) +
-                                                       16 * h);
-#pragma unroll
-      for (int pb = 0; pb < 2; ++pb)
-        bv[nxt][pb] = *reinterpret_cast<const uint4 *>(pbuf + (wp * 64 + pb * 32 + r) * kLdsStride + 32 * (g + 1) +
-                                                       16 * h);
-    }
-#pragma unroll
-    for (int cb = 0; cb < 2; ++cb)
-#pragma unroll
-      for (int pb = 0; pb < 2; ++pb) {
-        const i32x4 a4 = {(int)av[cur][cb].x, (int)av[cur][cb].y, (int)av[cur][cb].z, (int)av[cur][cb].w};
-        const i32x4 b4 = {(int)bv[cur][pb].x, (int)bv[cur][pb].y, (int)bv[cur][pb].z, (int)bv[cur][pb].w};
-        iacc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a4, b4, iacc[cb][pb], 0, 0, 0);
+        for (int c = 0; c < 4; ++c) cpar[c * G::TC + jt] = R.cpar[c];
       }
+    }
   }
 }
 
+template <int CB, int PB, bool FP>
+__device__ __forceinline__ void mfma_stage(const uint8_t *cbuf, const uint8_t *pbuf, int wc, int wp, int r, int h,
+                                           f32x16 (&facc)[CB][PB], i32x16 (&iacc)[CB][PB]) {
+  uint4 av[2][CB], bv[2][PB];  // [register set][block]
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb)
+    av[0][cb] = *reinterpret_cast<const uint4 *>(cbuf + (wc * 32 * CB + cb * 32 + r) * kLdsStride + 16 * h);
+#pragma unroll
+  for (int pb = 0; pb < PB; ++pb)
+    bv[0][pb] = *reinterpret_cast<const uint4 *>(pbuf + (wp * 32 * PB + pb * 32 + r) * kLdsStride + 16 * h);
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const int cur = g & 1, nxt = cur ^ 1;
+    if (g + 1 < 4) {
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb)
+        av[nxt][cb] = *reinterpret_cast<const uint4 *>(cbuf + (wc * 32 * CB + cb * 32 + r) * kLdsStride +
+                                                       32 * (g + 1) + 16 * h);
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb)
+        bv[nxt][pb] = *reinterpret_cast<const uint4 *>(pbuf + (wp * 32 * PB + pb * 32 + r) * kLdsStride +
+                                                       32 * (g + 1) + 16 * h);
+    }
+    if constexpr (FP) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+          for (int pb = 0; pb < PB; ++pb)
+            facc[cb][pb] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(av[cur][cb][e]),
+                                                                __uint_as_float(bv[cur][pb][e]), facc[cb][pb], 0, 0, 0);
+    } else {
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+        for (int pb = 0; pb < PB; ++pb) {
+          const i32x4 a4 = {(int)av[cur][cb].x, (int)av[cur][cb].y, (int)av[cur][cb].z, (int)av[cur][cb].w};
+          const i32x4 b4 = {(int)bv[cur][pb].x, (int)bv[cur][pb].y, (int)bv[cur][pb].z, (int)bv[cur][pb].w};
+          iacc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a4, b4, iacc[cb][pb], 0, 0, 0);
+        }
+    }
+  }
+}
+
+// Register blocking per format: 2 x 2 blocks per wave (128-centroid tiles, 128
+// points per workgroup).  fp32 runs two workgroups per CU so that one's barrier
+// and LDS refill hide under the other's MFMAs (measured faster than 4 x 2 blocks
+// at one workgroup per CU); the hybrid kernel carries fp32 and int32
+// accumulators and runs one.
 template <int FMT>
-__global__ __launch_bounds__(kThreads, FMT == KM_HYBRID ? 1 : 2) void assign_kernel(AssignArgs A) {
-  __shared__ __align__(16) uint8_t lds[2 * kStageBytes];
-  __shared__ float cparl[2][4 * kTile];
+struct Blocking {
+  static constexpr int CB = 2;
+  static constexpr int PB = 2;
+  static constexpr int MINB = FMT == KM_HYBRID ? 1 : 2;
+};
+
+template <int FMT>
+__global__ __launch_bounds__(kThreads, Blocking<FMT>::MINB) void assign_kernel(AssignArgs A) {
+  constexpr int CB = Blocking<FMT>::CB, PB = Blocking<FMT>::PB;
+  typedef Geo<CB, PB> G;
+  __shared__ __align__(16) uint8_t lds[2 * G::STAGE];
+  __shared__ float cparl[2][4 * G::TC];
   typedef typename std::conditional<Cfg<FMT>::kIntScore, int, float>::type score_t;
 
   const int t = threadIdx.x;
   const int lane = t & 63, wave = t >> 6;
   const int r = lane & 31, h = lane >> 5;
   const int wc = wave & 1, wp = wave >> 1;
-  const int64_t p0 = (int64_t)blockIdx.x * kTile;
+  const int64_t p0 = (int64_t)blockIdx.x * G::TP;
 
   const int SF = Cfg<FMT>::kFp ? (A.df + 31) / 32 : 0;
   const int SI = Cfg<FMT>::kInt ? (A.di + kRowBytes - 1) / kRowBytes : 0;
   const int S = SF + SI;
-  const int nct = (A.k + kTile - 1) / kTile;
+  const int nct = (A.k + G::TC - 1) / G::TC;
   const int total = nct * S;
 
-  float al[2] = {0.f, 0.f};
-  if (Cfg<FMT>::kBits) {
+  float al[PB];
 #pragma unroll
-    for (int pb = 0; pb < 2; ++pb) al[pb] = A.alpha[min<int64_t>(p0 + wp * 64 + pb * 32 + r, A.n - 1)];
-  }
+  for (int pb = 0; pb < PB; ++pb)
+    al[pb] = Cfg<FMT>::kBits ? A.alpha[min<int64_t>(p0 + wp * 32 * PB + pb * 32 + r, A.n - 1)] : 0.f;
 
-  f32x16 facc[2][2];
-  i32x16 iacc[2][2];
+  f32x16 facc[CB][PB];
+  i32x16 iacc[CB][PB];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < CB; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
+    for (int b = 0; b < PB; ++b) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         facc[a][b][i] = 0.f;
@@ -318,17 +353,17 @@ __global__ __launch_bounds__(kThreads, FMT == KM_HYBRID ? 1 : 2) void assign_ker
       }
     }
 
-  score_t best[2];
-  int bidx[2] = {INT_MAX, INT_MAX};
-  if (Cfg<FMT>::kIntScore) {
-    best[0] = best[1] = (score_t)INT_MAX;
-  } else {
-    best[0] = best[1] = (score_t)INFINITY;
+  score_t best[PB];
+  int bidx[PB];
+#pragma unroll
+  for (int pb = 0; pb < PB; ++pb) {
+    best[pb] = Cfg<FMT>::kIntScore ? (score_t)INT_MAX : (score_t)INFINITY;
+    bidx[pb] = INT_MAX;
   }
 
-  StageRegs R;
-  load_stage<FMT>(A, 0, SF, 0, p0, R);
-  store_stage<FMT>(A, 0, SF, R, lds, cparl[0]);
+  StageRegs<CB, PB> R;
+  load_stage<FMT, CB, PB>(A, 0, SF, 0, p0, R);
+  store_stage<FMT, CB, PB>(A, 0, SF, R, lds, cparl[0]);
   __syncthreads();
 
   for (int ct = 0; ct < nct; ++ct) {
@@ -337,33 +372,33 @@ __global__ __launch_bounds__(kThreads, FMT == KM_HYBRID ? 1 : 2) void assign_ker
       const bool has_next = it + 1 < total;
       const int s_n = (s + 1 == S) ? 0 : s + 1;
       const int ct_n = (s + 1 == S) ? ct + 1 : ct;
-      if (has_next) load_stage<FMT>(A, s_n, SF, (int64_t)ct_n * kTile, p0, R);
-      const uint8_t *buf = lds + (it & 1) * kStageBytes;
+      if (has_next) load_stage<FMT, CB, PB>(A, s_n, SF, (int64_t)ct_n * G::TC, p0, R);
+      const uint8_t *buf = lds + (it & 1) * G::STAGE;
       if (is_fp_stage<FMT>(s, SF)) {
-        if constexpr (Cfg<FMT>::kFp) mfma_stage_fp<FMT>(buf, buf + kTileBytes, wc, wp, r, h, facc);
+        if constexpr (Cfg<FMT>::kFp) mfma_stage<CB, PB, true>(buf, buf + G::CBYTES, wc, wp, r, h, facc, iacc);
       } else {
-        if constexpr (Cfg<FMT>::kInt) mfma_stage_int(buf, buf + kTileBytes, wc, wp, r, h, iacc);
+        if constexpr (Cfg<FMT>::kInt) mfma_stage<CB, PB, false>(buf, buf + G::CBYTES, wc, wp, r, h, facc, iacc);
       }
-      if (has_next) store_stage<FMT>(A, s_n, SF, R, lds + ((it + 1) & 1) * kStageBytes, cparl[ct_n & 1]);
+      if (has_next) store_stage<FMT, CB, PB>(A, s_n, SF, R, lds + ((it + 1) & 1) * G::STAGE, cparl[ct_n & 1]);
       __syncthreads();
     }
 
     // epilogue for centroid tile ct: scores and running argmin, lane-local
-    const int64_t c0 = (int64_t)ct * kTile;
+    const int64_t c0 = (int64_t)ct * G::TC;
     const float *cp = cparl[ct & 1];
 #pragma unroll
-    for (int cb = 0; cb < 2; ++cb) {
+    for (int cb = 0; cb < CB; ++cb) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const int crow = wc * 64 + cb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
+        const int crow = wc * 32 * CB + cb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
         const int64_t j = c0 + crow;
         const bool live = j < A.k;
         const float cn = cp[crow];
-        const int qs = __float_as_int(cp[kTile + crow]);
-        const float u = cp[2 * kTile + crow];
-        const float s2 = cp[3 * kTile + crow];
+        const int qs = __float_as_int(cp[G::TC + crow]);
+        const float u = cp[2 * G::TC + crow];
+        const float s2 = cp[3 * G::TC + crow];
 #pragma unroll
-        for (int pb = 0; pb < 2; ++pb) {
+        for (int pb = 0; pb < PB; ++pb) {
           score_t sc;
           if constexpr (FMT == KM_F32) {
             sc = fmaf(-2.0f, facc[cb][pb][i], cn);
@@ -388,9 +423,9 @@ __global__ __launch_bounds__(kThreads, FMT == KM_HYBRID ? 1 : 2) void assign_ker
       }
     }
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int a = 0; a < CB; ++a)
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
+      for (int b = 0; b < PB; ++b) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           facc[a][b][i] = 0.f;
@@ -401,7 +436,7 @@ __global__ __launch_bounds__(kThreads, FMT == KM_HYBRID ? 1 : 2) void assign_ker
 
   // merge the two lane halves (rows 4h..), then the two centroid waves
 #pragma unroll
-  for (int pb = 0; pb < 2; ++pb) {
+  for (int pb = 0; pb < PB; ++pb) {
     score_t os = __shfl_xor(best[pb], 32);
     int oi = __shfl_xor(bidx[pb], 32);
     if (os < best[pb] || (os == best[pb] && oi < bidx[pb])) {
@@ -410,19 +445,19 @@ __global__ __launch_bounds__(kThreads, FMT == KM_HYBRID ? 1 : 2) void assign_ker
     }
   }
   score_t *ms = reinterpret_cast<score_t *>(lds);
-  int *mi = reinterpret_cast<int *>(lds + kTile * sizeof(score_t));
+  int *mi = reinterpret_cast<int *>(lds + G::TP * sizeof(score_t));
   if (wc == 1 && h == 0) {
 #pragma unroll
-    for (int pb = 0; pb < 2; ++pb) {
-      ms[wp * 64 + pb * 32 + r] = best[pb];
-      mi[wp * 64 + pb * 32 + r] = bidx[pb];
+    for (int pb = 0; pb < PB; ++pb) {
+      ms[wp * 32 * PB + pb * 32 + r] = best[pb];
+      mi[wp * 32 * PB + pb * 32 + r] = bidx[pb];
     }
   }
   __syncthreads();
   if (wc == 0 && h == 0) {
 #pragma unroll
-    for (int pb = 0; pb < 2; ++pb) {
-      const int pc = wp * 64 + pb * 32 + r;
+    for (int pb = 0; pb < PB; ++pb) {
+      const int pc = wp * 32 * PB + pb * 32 + r;
       const score_t os = ms[pc];
       const int oi = mi[pc];
       if (os < best[pb] || (os == best[pb] && oi < bidx[pb])) {
@@ -916,7 +951,8 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
   if constexpr (FMT == KM_SQ8 || FMT == KM_SIGN1) {
     hipLaunchKernelGGL(assign_i8_kernel<FMT>, dim3((unsigned)cdiv(P.n, kT8)), dim3(kThreads), 0, s, A);
   } else {
-    hipLaunchKernelGGL(assign_kernel<FMT>, dim3((unsigned)cdiv(P.n, kTile)), dim3(kThreads), 0, s, A);
+    constexpr int TP = Geo<Blocking<FMT>::CB, Blocking<FMT>::PB>::TP;
+    hipLaunchKernelGGL(assign_kernel<FMT>, dim3((unsigned)cdiv(P.n, TP)), dim3(kThreads), 0, s, A);
   }
   KMQ_LAUNCH_CHECK("assign_kernel");
   return KM_OK;
