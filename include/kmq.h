@@ -96,7 +96,8 @@ typedef struct km_points {
  *     dims [d_front, d) with r = x - m (fp64 sums; 0 when x == m on those dims).
  *     alpha equals (1/sqrt(d')) ||r|| / <x_bar, x> of Eq. 4, the decoding radius.
  *     If d_front > 0 and front != NULL, front = float[n][d_front] receives a copy
- *     of the first d_front dims (the hybrid layout).  d % 32 == 0, d_front % 32 == 0.
+ *     of the first d_front dims (the hybrid layout).  d % 32 == 0, d_front % 32 == 0;
+ *     params and front 16-byte aligned.
  *   flags & KM_Q_FIT_PARAMS: compute params from X first (one extra pass over X);
  *     otherwise params are inputs.
  */

@@ -178,6 +178,8 @@ km_status quantize(const float *X, int64_t n, int32_t d, int64_t ldx, int32_t fm
     KMQ_CHECK(d_front >= 0 && d_front < d && d_front % 32 == 0, KM_EINVAL,
               "need 0 <= d_front < d and d_front %% 32 == 0 (d_front = %d)", d_front);
     KMQ_CHECK(front == nullptr || d_front > 0, KM_EINVAL, "front copy needs d_front > 0");
+    KMQ_CHECK(aligned16(params) && (front == nullptr || aligned16(front)), KM_EINVAL,
+              "params and front must be 16-byte aligned");
   }
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   Scratch ws(s);

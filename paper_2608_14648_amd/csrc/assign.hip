@@ -115,26 +115,35 @@ __device__ __forceinline__ uint4 flip4(uint4 v) {
   return make_uint4(v.x ^ 0x80808080u, v.y ^ 0x80808080u, v.z ^ 0x80808080u, v.w ^ 0x80808080u);
 }
 
+// Stage order inside a centroid tile: fp32 formats have only fp32 stages, the
+// integer formats only int8 stages; the hybrid runs its int8 (1-bit tail) stages
+// first and its fp32 (front) stages after, so the two accumulators are never
+// live together.  SI is the number of int8 stages.
 template <int FMT>
-__device__ __forceinline__ bool is_fp_stage(int s, int SF) {
+__device__ __forceinline__ bool is_fp_stage(int s, int SI) {
   if constexpr (FMT == KM_F32) return true;
-  else if constexpr (FMT == KM_HYBRID) return s < SF;
+  else if constexpr (FMT == KM_HYBRID) return s >= SI;
   else return false;
+}
+
+template <int FMT>
+__device__ __forceinline__ int fp_index(int s, int SI) {
+  return FMT == KM_HYBRID ? s - SI : s;
 }
 
 // Every address is clamped into its buffer; lanes outside the data are zeroed at
 // store time, so the loads are unconditional and branch-free.
 template <int FMT, int CB, int PB>
-__device__ __forceinline__ void load_stage(const AssignArgs &A, int s, int SF, int64_t c0, int64_t p0,
+__device__ __forceinline__ void load_stage(const AssignArgs &A, int s, int SI, int64_t c0, int64_t p0,
                                            StageRegs<CB, PB> &R) {
   typedef Geo<CB, PB> G;
   const int t = threadIdx.x;
   const int crmax = (int)min<int64_t>(A.k - 1 - c0, G::TC - 1);
   const int prmax = (int)min<int64_t>(A.n - 1 - p0, G::TP - 1);
-  if (is_fp_stage<FMT>(s, SF)) {
+  if (is_fp_stage<FMT>(s, SI)) {
     const float *cbase = A.cf + c0 * A.cfld;
     const float *pbase = A.pf + p0 * A.pfld;
-    const int dim0 = 32 * s;
+    const int dim0 = 32 * fp_index<FMT>(s, SI);
 #pragma unroll
     for (int i = 0; i < G::NC; ++i) {
       const int cidx = t + kThreads * i;
@@ -152,7 +161,7 @@ __device__ __forceinline__ void load_stage(const AssignArgs &A, int s, int SF, i
       R.p[i] = *reinterpret_cast<const uint4 *>(pbase + (uint32_t)(min(row, prmax) * (int)A.pfld + dimc));
     }
   } else if constexpr (Cfg<FMT>::kInt) {
-    const int si = s - (Cfg<FMT>::kFp ? SF : 0);
+    const int si = s;
     const int b0 = kRowBytes * si;
     const int8_t *cbase = A.ci8 + c0 * A.cild;
 #pragma unroll
@@ -204,19 +213,20 @@ __device__ __forceinline__ void load_stage(const AssignArgs &A, int s, int SF, i
 }
 
 template <int FMT, int CB, int PB>
-__device__ __forceinline__ void store_stage(const AssignArgs &A, int s, int SF, const StageRegs<CB, PB> &R,
+__device__ __forceinline__ void store_stage(const AssignArgs &A, int s, int SI, const StageRegs<CB, PB> &R,
                                             uint8_t *buf, float *cpar) {
   typedef Geo<CB, PB> G;
   const int t = threadIdx.x;
   uint8_t *ct = buf;
   uint8_t *pt = buf + G::CBYTES;
-  const bool fp = is_fp_stage<FMT>(s, SF);
-  const int si = s - (Cfg<FMT>::kFp ? SF : 0);
+  const bool fp = is_fp_stage<FMT>(s, SI);
+  const int si = s;
+  const int sf = fp_index<FMT>(s, SI);
 #pragma unroll
   for (int i = 0; i < G::NC; ++i) {
     const int cidx = t + kThreads * i;
     const int row = cidx >> 3, col = cidx & 7;
-    const bool ok = fp ? (32 * s + 4 * col < A.df) : (kRowBytes * si + 16 * col < A.di);
+    const bool ok = fp ? (32 * sf + 4 * col < A.df) : (kRowBytes * si + 16 * col < A.di);
     uint4 cv = R.c[i];
     if (FMT == KM_SQ8) cv = flip4(cv);
     *reinterpret_cast<uint4 *>(ct + row * kLdsStride + 16 * col) = mask4(cv, ok);
@@ -226,7 +236,7 @@ __device__ __forceinline__ void store_stage(const AssignArgs &A, int s, int SF, 
     for (int i = 0; i < G::NP; ++i) {
       const int cidx = t + kThreads * i;
       const int row = cidx >> 3, col = cidx & 7;
-      const bool ok = fp ? (32 * s + 4 * col < A.df) : (kRowBytes * si + 16 * col < A.di);
+      const bool ok = fp ? (32 * sf + 4 * col < A.df) : (kRowBytes * si + 16 * col < A.di);
       uint4 pv = R.p[i];
       if (!fp) pv = flip4(pv);
       *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 16 * col) = mask4(pv, ok);
@@ -304,15 +314,14 @@ __device__ __forceinline__ void mfma_stage(const uint8_t *cbuf, const uint8_t *p
 }
 
 // Register blocking per format: 2 x 2 blocks per wave (128-centroid tiles, 128
-// points per workgroup).  fp32 runs two workgroups per CU so that one's barrier
-// and LDS refill hide under the other's MFMAs (measured faster than 4 x 2 blocks
-// at one workgroup per CU); the hybrid kernel carries fp32 and int32
-// accumulators and runs one.
+// points per workgroup), two workgroups per CU so that one's barrier and LDS
+// refill hide under the other's MFMAs (measured faster than 4 x 2 blocks at one
+// workgroup per CU).
 template <int FMT>
 struct Blocking {
   static constexpr int CB = 2;
   static constexpr int PB = 2;
-  static constexpr int MINB = FMT == KM_HYBRID ? 1 : 2;
+  static constexpr int MINB = 2;
 };
 
 template <int FMT>
@@ -340,19 +349,6 @@ __global__ __launch_bounds__(kThreads, Blocking<FMT>::MINB) void assign_kernel(A
   for (int pb = 0; pb < PB; ++pb)
     al[pb] = Cfg<FMT>::kBits ? A.alpha[min<int64_t>(p0 + wp * 32 * PB + pb * 32 + r, A.n - 1)] : 0.f;
 
-  f32x16 facc[CB][PB];
-  i32x16 iacc[CB][PB];
-#pragma unroll
-  for (int a = 0; a < CB; ++a)
-#pragma unroll
-    for (int b = 0; b < PB; ++b) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        facc[a][b][i] = 0.f;
-        iacc[a][b][i] = 0;
-      }
-    }
-
   score_t best[PB];
   int bidx[PB];
 #pragma unroll
@@ -362,30 +358,70 @@ __global__ __launch_bounds__(kThreads, Blocking<FMT>::MINB) void assign_kernel(A
   }
 
   StageRegs<CB, PB> R;
-  load_stage<FMT, CB, PB>(A, 0, SF, 0, p0, R);
-  store_stage<FMT, CB, PB>(A, 0, SF, R, lds, cparl[0]);
+  load_stage<FMT, CB, PB>(A, 0, SI, 0, p0, R);
+  store_stage<FMT, CB, PB>(A, 0, SI, R, lds, cparl[0]);
   __syncthreads();
 
+  // one pipeline step: prefetch stage (it+1) into registers, run the MFMAs of
+  // stage `it` from LDS, write stage (it+1) to the other buffer, barrier
+  auto step = [&](int ct, int s, auto fp_tag, auto &acc_f, auto &acc_i) {
+    constexpr bool FPS = decltype(fp_tag)::value;
+    const int it = ct * S + s;
+    const bool has_next = it + 1 < total;
+    const int s_n = (s + 1 == S) ? 0 : s + 1;
+    const int ct_n = (s + 1 == S) ? ct + 1 : ct;
+    if (has_next) load_stage<FMT, CB, PB>(A, s_n, SI, (int64_t)ct_n * G::TC, p0, R);
+    const uint8_t *buf = lds + (it & 1) * G::STAGE;
+    mfma_stage<CB, PB, FPS>(buf, buf + G::CBYTES, wc, wp, r, h, acc_f, acc_i);
+    if (has_next) store_stage<FMT, CB, PB>(A, s_n, SI, R, lds + ((it + 1) & 1) * G::STAGE, cparl[ct_n & 1]);
+    __syncthreads();
+  };
+
   for (int ct = 0; ct < nct; ++ct) {
-    for (int s = 0; s < S; ++s) {
-      const int it = ct * S + s;
-      const bool has_next = it + 1 < total;
-      const int s_n = (s + 1 == S) ? 0 : s + 1;
-      const int ct_n = (s + 1 == S) ? ct + 1 : ct;
-      if (has_next) load_stage<FMT, CB, PB>(A, s_n, SF, (int64_t)ct_n * G::TC, p0, R);
-      const uint8_t *buf = lds + (it & 1) * G::STAGE;
-      if (is_fp_stage<FMT>(s, SF)) {
-        if constexpr (Cfg<FMT>::kFp) mfma_stage<CB, PB, true>(buf, buf + G::CBYTES, wc, wp, r, h, facc, iacc);
-      } else {
-        if constexpr (Cfg<FMT>::kInt) mfma_stage<CB, PB, false>(buf, buf + G::CBYTES, wc, wp, r, h, facc, iacc);
-      }
-      if (has_next) store_stage<FMT, CB, PB>(A, s_n, SF, R, lds + ((it + 1) & 1) * G::STAGE, cparl[ct_n & 1]);
-      __syncthreads();
+    const int64_t c0 = (int64_t)ct * G::TC;
+    const float *cp = cparl[ct & 1];
+    f32x16 facc[CB][PB];
+    i32x16 iacc[CB][PB];
+    if constexpr (Cfg<FMT>::kInt) {
+#pragma unroll
+      for (int a = 0; a < CB; ++a)
+#pragma unroll
+        for (int b = 0; b < PB; ++b)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) iacc[a][b][i] = 0;
+      for (int s = 0; s < SI; ++s) step(ct, s, std::false_type{}, facc, iacc);
+    }
+    if constexpr (FMT == KM_HYBRID) {
+      // the tail's exact 1-bit score ts becomes the starting value -ts/2 of the
+      // fp32 accumulator, so -2 acc + ||c'||^2 = ||c'||^2 - 2<x',c'> + ts
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int crow = wc * 32 * CB + cb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
+          const int qs = __float_as_int(cp[G::TC + crow]);
+          const float u = cp[2 * G::TC + crow];
+          const float s2 = cp[3 * G::TC + crow];
+#pragma unroll
+          for (int pb = 0; pb < PB; ++pb) {
+            const int sd = 2 * iacc[cb][pb][i] - qs;
+            const float ts = fmaf(-(al[pb] * s2), (float)sd, u);
+            facc[cb][pb][i] = -0.5f * ts;
+          }
+        }
+    } else if constexpr (FMT == KM_F32) {
+#pragma unroll
+      for (int a = 0; a < CB; ++a)
+#pragma unroll
+        for (int b = 0; b < PB; ++b)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) facc[a][b][i] = 0.f;
+    }
+    if constexpr (Cfg<FMT>::kFp) {
+      for (int s = SI; s < S; ++s) step(ct, s, std::true_type{}, facc, iacc);
     }
 
     // epilogue for centroid tile ct: scores and running argmin, lane-local
-    const int64_t c0 = (int64_t)ct * G::TC;
-    const float *cp = cparl[ct & 1];
 #pragma unroll
     for (int cb = 0; cb < CB; ++cb) {
 #pragma unroll
@@ -409,11 +445,7 @@ __global__ __launch_bounds__(kThreads, Blocking<FMT>::MINB) void assign_kernel(A
             const float v = al[pb] * s2;
             sc = fmaf(-v, (float)sd, u);
           } else {
-            const int sd = 2 * iacc[cb][pb][i] - qs;
-            const float v = al[pb] * s2;
-            const float ts = fmaf(-v, (float)sd, u);
-            const float fs = fmaf(-2.0f, facc[cb][pb][i], cn);
-            sc = fs + ts;
+            sc = fmaf(-2.0f, facc[cb][pb][i], cn);  // tail score already folded in
           }
           if (live && sc < best[pb]) {
             best[pb] = sc;
@@ -422,16 +454,6 @@ __global__ __launch_bounds__(kThreads, Blocking<FMT>::MINB) void assign_kernel(A
         }
       }
     }
-#pragma unroll
-    for (int a = 0; a < CB; ++a)
-#pragma unroll
-      for (int b = 0; b < PB; ++b) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          facc[a][b][i] = 0.f;
-          iacc[a][b][i] = 0;
-        }
-      }
   }
 
   // merge the two lane halves (rows 4h..), then the two centroid waves
@@ -807,7 +829,7 @@ __global__ __launch_bounds__(256) void prep_kernel(const void *Cv, int k, int d,
 
 // ---- point-only terms of the in-space distance ------------------------------
 // F32: ||x||^2 ; SQ8: ||code-128||^2 ; SIGN1: alpha^2 d ; HYBRID: ||x'||^2 + alpha^2 (d - d0)
-// One wave per point.
+// One wave per point, 16-byte loads.
 template <int FMT>
 __global__ __launch_bounds__(256) void xconst_kernel(Points P, float *xc) {
   const int lane = threadIdx.x & 63;
@@ -817,13 +839,25 @@ __global__ __launch_bounds__(256) void xconst_kernel(Points P, float *xc) {
   if (FMT == KM_F32 || FMT == KM_HYBRID) {
     const float *x = FMT == KM_F32 ? static_cast<const float *>(P.data) + p * P.ld : P.front + p * P.d_front;
     const int dd = FMT == KM_F32 ? P.d : P.d_front;
-    for (int i = lane; i < dd; i += 64) s += (double)x[i] * (double)x[i];
+    for (int i = 4 * lane; i < dd; i += 256) {
+      const f32x4 v = *reinterpret_cast<const f32x4 *>(x + i);
+      s += (double)v.x * v.x + (double)v.y * v.y + (double)v.z * v.z + (double)v.w * v.w;
+    }
   } else if (FMT == KM_SQ8) {
     const uint8_t *x = static_cast<const uint8_t *>(P.data) + p * P.ld;
-    for (int i = lane; i < P.d; i += 64) {
-      const int v = (int)x[i] - 128;
-      s += (double)(v * v);
+    int acc = 0;
+    for (int i = 16 * lane; i < P.d; i += 1024) {
+      const uint4 w = *reinterpret_cast<const uint4 *>(x + i);
+      const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int v = (int)((ws[q] >> (8 * e)) & 255u) - 128;
+          acc += v * v;
+        }
     }
+    s = (double)acc;
   }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
@@ -887,11 +921,15 @@ __global__ __launch_bounds__(256) void gather_kernel(Points P, const int64_t *id
 }
 
 // ---- full-precision cost of a partition: sum ||x - c_a||^2 in fp64 ----------
+// One wave per point at a time, 16-byte loads of the point and its centroid row.
+// Rows whose length is not a multiple of 4 fall back to scalar loads.
 __global__ __launch_bounds__(256) void cost_kernel(const float *X, int64_t n, int d, int64_t ldx, const float *C,
                                                    int k, const int32_t *assign, double *partials) {
   __shared__ double sh[256];
   const int lane = threadIdx.x & 63;
   const int wv = threadIdx.x >> 6;
+  const bool vec = (d % 4 == 0) && (ldx % 4 == 0) &&
+                   (((reinterpret_cast<uintptr_t>(X) | reinterpret_cast<uintptr_t>(C)) & 15u) == 0);
   double s = 0.0;
   const int64_t stride = (int64_t)gridDim.x * 4;
   for (int64_t p = (int64_t)blockIdx.x * 4 + wv; p < n; p += stride) {
@@ -899,9 +937,21 @@ __global__ __launch_bounds__(256) void cost_kernel(const float *X, int64_t n, in
     if (a < 0 || a >= k) continue;
     const float *x = X + p * ldx;
     const float *c = C + (int64_t)a * d;
-    for (int i = lane; i < d; i += 64) {
-      const double e = (double)x[i] - (double)c[i];
-      s += e * e;
+    if (vec) {
+      for (int i = 4 * lane; i < d; i += 256) {
+        const f32x4 xv = *reinterpret_cast<const f32x4 *>(x + i);
+        const f32x4 cv = *reinterpret_cast<const f32x4 *>(c + i);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const double t = (double)xv[e] - (double)cv[e];
+          s += t * t;
+        }
+      }
+    } else {
+      for (int i = lane; i < d; i += 64) {
+        const double t = (double)x[i] - (double)c[i];
+        s += t * t;
+      }
     }
   }
   s = block_sum_f64(s, sh);

@@ -47,12 +47,23 @@ __global__ void colminmax_final_kernel(const float *pmin, const float *pmax, int
 }
 
 __global__ __launch_bounds__(256) void colsum_partial_kernel(const float *X, int64_t n, int d, int64_t ldx,
-                                                             double *psum) {
-  const int64_t r0 = (int64_t)blockIdx.x * kRowsPerBlock;
-  const int64_t r1 = min<int64_t>(n, r0 + kRowsPerBlock);
+                                                             int64_t rows_per_block, double *psum) {
+  const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
+  const int64_t r1 = min<int64_t>(n, r0 + rows_per_block);
   for (int g = threadIdx.x; g < d / 4; g += 256) {
     double s0 = 0, s1 = 0, s2 = 0, s3 = 0;
-    for (int64_t r = r0; r < r1; ++r) {
+    int64_t r = r0;
+    for (; r + 3 < r1; r += 4) {
+      const f32x4 v0 = *reinterpret_cast<const f32x4 *>(X + r * ldx + 4 * g);
+      const f32x4 v1 = *reinterpret_cast<const f32x4 *>(X + (r + 1) * ldx + 4 * g);
+      const f32x4 v2 = *reinterpret_cast<const f32x4 *>(X + (r + 2) * ldx + 4 * g);
+      const f32x4 v3 = *reinterpret_cast<const f32x4 *>(X + (r + 3) * ldx + 4 * g);
+      s0 += v0.x; s1 += v0.y; s2 += v0.z; s3 += v0.w;
+      s0 += v1.x; s1 += v1.y; s2 += v1.z; s3 += v1.w;
+      s0 += v2.x; s1 += v2.y; s2 += v2.z; s3 += v2.w;
+      s0 += v3.x; s1 += v3.y; s2 += v3.z; s3 += v3.w;
+    }
+    for (; r < r1; ++r) {
       const f32x4 v = *reinterpret_cast<const f32x4 *>(X + r * ldx + 4 * g);
       s0 += v.x; s1 += v.y; s2 += v.z; s3 += v.w;
     }
@@ -61,12 +72,14 @@ __global__ __launch_bounds__(256) void colsum_partial_kernel(const float *X, int
   }
 }
 
-__global__ void colmean_final_kernel(const double *psum, int nb, int d, int64_t n, float *m) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= d) return;
+// one workgroup per column: strided partial sums, then a fixed-order tree
+__global__ __launch_bounds__(256) void colmean_final_kernel(const double *psum, int nb, int d, int64_t n, float *m) {
+  __shared__ double sh[256];
+  const int i = blockIdx.x;
   double s = 0.0;
-  for (int b = 0; b < nb; ++b) s += psum[(int64_t)b * d + i];
-  m[i] = (float)(s / (double)n);
+  for (int b = threadIdx.x; b < nb; b += 256) s += psum[(int64_t)b * d + i];
+  s = block_sum_f64(s, sh);
+  if (threadIdx.x == 0) m[i] = (float)(s / (double)n);
 }
 
 __global__ void sq8_inv_kernel(const float *lo, const float *hi, int d, float *inv) {
@@ -102,7 +115,10 @@ __global__ __launch_bounds__(256) void sq8_encode_kernel(const float *X, int64_t
   }
 }
 
-// one wave per row
+// One wave per row.  Lane l reads dims [base + 4l, base + 4l + 4) as a float4 and
+// forms a 4-bit nibble of sign bits; the 8 lanes that share a 32-dim word OR
+// their shifted nibbles together (3 xor-shuffles) and the first of them stores
+// the word, so a wave stores 8 consecutive words per 256 dims.
 __global__ __launch_bounds__(256) void sign1_encode_kernel(const float *X, int64_t n, int d, int64_t ldx,
                                                            const float *m, int d0, uint32_t *bits, float *alpha,
                                                            float *front) {
@@ -112,19 +128,30 @@ __global__ __launch_bounds__(256) void sign1_encode_kernel(const float *X, int64
   const float *x = X + row * ldx;
   uint32_t *b = bits + row * (d / 32);
   double s2 = 0.0, s1 = 0.0;
-  for (int base = 0; base < d; base += 64) {
-    const int i = base + lane;
-    const bool in = i < d;
-    const float xi = in ? x[i] : 0.0f;
-    const float r = in ? xi - m[i] : 0.0f;
-    const uint64_t mask = __ballot(in && r > 0.0f);
-    if (in && i >= d0) {
-      s2 += (double)r * (double)r;
-      s1 += fabs((double)r);
+  for (int base = 0; base < d; base += 256) {
+    const int i0 = base + 4 * lane;
+    const bool in = i0 < d;  // d % 32 == 0, so a float4 is either wholly in or out
+    f32x4 xv = {0.f, 0.f, 0.f, 0.f}, mv = {0.f, 0.f, 0.f, 0.f};
+    if (in) {
+      xv = *reinterpret_cast<const f32x4 *>(x + i0);
+      mv = *reinterpret_cast<const f32x4 *>(m + i0);
     }
-    if (front && in && i < d0) front[row * d0 + i] = xi;
-    if (lane == 0) b[base >> 5] = (uint32_t)mask;
-    if (lane == 1 && base + 32 < d) b[(base >> 5) + 1] = (uint32_t)(mask >> 32);
+    uint32_t nib = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float r = xv[e] - mv[e];
+      nib |= (in && r > 0.0f) ? (1u << e) : 0u;
+      if (in && i0 + e >= d0) {
+        s2 += (double)r * (double)r;
+        s1 += fabs((double)r);
+      }
+    }
+    uint32_t w = nib << (4 * (lane & 7));
+    w |= __shfl_xor(w, 1);
+    w |= __shfl_xor(w, 2);
+    w |= __shfl_xor(w, 4);
+    if (in && (lane & 7) == 0) b[(i0 >> 5)] = w;
+    if (front && in && i0 < d0) *reinterpret_cast<f32x4 *>(front + row * d0 + i0) = xv;
   }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) {
@@ -136,13 +163,19 @@ __global__ __launch_bounds__(256) void sign1_encode_kernel(const float *X, int64
 
 }  // namespace
 
-size_t colmean_bytes(int64_t n, int d) { return (size_t)cdiv(n, kRowsPerBlock) * d * sizeof(double) + 256; }
+constexpr int kMaxSumBlocks = 1024;
+
+size_t colmean_bytes(int64_t n, int d) {
+  return (size_t)std::min<int64_t>(kMaxSumBlocks, cdiv(n, 64)) * d * sizeof(double) + 256;
+}
 
 km_status launch_colmean(const float *X, int64_t n, int d, int64_t ldx, float *m, void *ws, hipStream_t s) {
-  const int nb = (int)cdiv(n, kRowsPerBlock);
+  const int64_t want = std::min<int64_t>(kMaxSumBlocks, cdiv(n, 64));
+  const int64_t rpb = cdiv(n, want);
+  const int nb = (int)cdiv(n, rpb);
   double *psum = static_cast<double *>(ws);
-  hipLaunchKernelGGL(colsum_partial_kernel, dim3(nb), dim3(256), 0, s, X, n, d, ldx, psum);
-  hipLaunchKernelGGL(colmean_final_kernel, dim3((unsigned)cdiv(d, 256)), dim3(256), 0, s, psum, nb, d, n, m);
+  hipLaunchKernelGGL(colsum_partial_kernel, dim3(nb), dim3(256), 0, s, X, n, d, ldx, rpb, psum);
+  hipLaunchKernelGGL(colmean_final_kernel, dim3(d), dim3(256), 0, s, psum, nb, d, n, m);
   KMQ_LAUNCH_CHECK("column mean");
   return KM_OK;
 }
@@ -150,7 +183,7 @@ km_status launch_colmean(const float *X, int64_t n, int d, int64_t ldx, float *m
 size_t quantize_bytes(int64_t n, int d, int fmt) {
   const int64_t nb = cdiv(n, kRowsPerBlock);
   if (fmt == KM_SQ8) return (size_t)nb * d * 2 * sizeof(float) + (size_t)d * sizeof(float) + 512;
-  return (size_t)nb * d * sizeof(double) + 256;
+  return colmean_bytes(n, d);
 }
 
 km_status launch_quantize(const float *X, int64_t n, int d, int64_t ldx, int fmt, void *codes, float *params,

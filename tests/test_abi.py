@@ -124,6 +124,7 @@ def test_quantize_and_pca_argument_checks(kmq):
     assert L.quantize(FAKE, 10, 64, 64, 2, FAKE, FAKE, None, 0, None, 4, None) == -1  # flags
     assert L.quantize(ct.c_void_p(0x10002), 10, 64, 64, 2, FAKE, FAKE, None, 0, None, 1, None) == -1
     assert L.quantize(FAKE, 0, 64, 64, 2, FAKE, FAKE, None, 0, None, 1, None) == -1
+    assert L.quantize(FAKE, 10, 64, 64, 3, FAKE, ct.c_void_p(0x10008), FAKE, 0, None, 1, None) == -1  # params
     assert L.pca_fit_cov(FAKE, 10, 30, FAKE, FAKE, None) == -1
     assert L.pca_fit_cov(None, 10, 32, FAKE, FAKE, None) == -1
     assert L.pca_project(FAKE, 10, 32, FAKE, FAKE, 0, FAKE, None) == -1
