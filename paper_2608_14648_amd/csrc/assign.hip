@@ -748,6 +748,168 @@ __global__ __launch_bounds__(kThreads, 1) void assign_i8_kernel(AssignArgs A) {
   }
 }
 
+// ---- 1-bit assignment with the points' bits resident in LDS ----------------------
+// A workgroup (8 waves) owns 512 points.  Their code words are loaded once and kept
+// in LDS transposed, word-major ([word][point]), so the 32 lanes of a wave that
+// read the same word of 32 consecutive points hit 32 consecutive banks.  At each
+// MFMA the lane widens its 16 bits (one half-word) to 16 {0,1} bytes in
+// registers.  The centroids' int8 residual codes stream through LDS in stages of
+// 128 centroids x 128 bytes; every wave multiplies its 64 points by all 128
+// centroids of the tile (4 x 2 blocks of 32 x 32 x 32), so no cross-wave merge is
+// needed and the workgroup sweeps the centroids once per 512 points.
+constexpr int kBT = 512;            // threads (8 waves)
+constexpr int kBTP = 512;           // points per workgroup
+constexpr int kBTC = 128;           // centroids per tile
+constexpr int kBMaxWords = 40;      // d - d0 <= 1280 dims for the resident codes
+constexpr int kBStageBytes = kBTC * kLdsStride;
+
+__device__ __forceinline__ i32x4 widen16(uint32_t hb) {
+  return i32x4{(int)spread4(hb & 15u), (int)spread4((hb >> 4) & 15u), (int)spread4((hb >> 8) & 15u),
+               (int)spread4((hb >> 12) & 15u)};
+}
+
+__global__ __launch_bounds__(kBT, 1) void assign_bits_kernel(AssignArgs A) {
+  __shared__ uint32_t bitsT[kBMaxWords * kBTP];  // 80 KB
+  __shared__ __align__(16) uint8_t cst[2][kBStageBytes];
+  __shared__ float cparl[2][3 * kBTC];
+  const int t = threadIdx.x;
+  const int lane = t & 63, wave = t >> 6;
+  const int r = lane & 31, h = lane >> 5;
+  const int64_t p0 = (int64_t)blockIdx.x * kBTP;
+  const int W = A.di / 32;  // words of the 1-bit part
+  const int S = (A.di + kRowBytes - 1) / kRowBytes;
+  const int nct = (A.k + kBTC - 1) / kBTC;
+  const int total = nct * S;
+  const int prmax = (int)min<int64_t>(A.n - 1 - p0, kBTP - 1);
+
+  // resident codes: thread t loads point t's words, 4 at a time when aligned
+  {
+    const uint32_t *row = A.pbits + (p0 + min(t, prmax)) * A.pbw + A.pbw0;
+    for (int w = 0; w < W; ++w) bitsT[w * kBTP + t] = row[w];
+  }
+  float al[2];
+#pragma unroll
+  for (int pb = 0; pb < 2; ++pb) al[pb] = A.alpha[p0 + min(wave * 64 + pb * 32 + r, prmax)];
+
+  // centroid stage loads: 128 rows x 8 chunks of 16 B = 2 chunks per thread
+  uint4 cr[2];
+  float cpv[3] = {0.f, 0.f, 0.f};
+  auto load = [&](int ct, int s) {
+    const int64_t c0 = (int64_t)ct * kBTC;
+    const int crmax = (int)min<int64_t>(A.k - 1 - c0, kBTC - 1);
+    const int8_t *cbase = A.ci8 + c0 * A.cild;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int cidx = t + kBT * i;
+      const int row = cidx >> 3, col = cidx & 7;
+      const int b = kRowBytes * s + 16 * col;
+      cr[i] = *reinterpret_cast<const uint4 *>(cbase + (uint32_t)(min(row, crmax) * (int)A.cild + (b < A.di ? b : 0)));
+    }
+    if (s == 0 && t < kBTC) {
+      const int64_t j = c0 + min(t, crmax);
+      cpv[0] = __int_as_float(A.cp.qsum[j]);
+      cpv[1] = A.cp.u[j];
+      cpv[2] = A.cp.sig2[j];
+    }
+  };
+  auto store = [&](int ct, int s, uint8_t *buf) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int cidx = t + kBT * i;
+      const int row = cidx >> 3, col = cidx & 7;
+      const bool ok = kRowBytes * s + 16 * col < A.di;
+      *reinterpret_cast<uint4 *>(buf + row * kLdsStride + 16 * col) = mask4(cr[i], ok);
+    }
+    if (s == 0 && t < kBTC) {
+#pragma unroll
+      for (int q = 0; q < 3; ++q) cparl[ct & 1][q * kBTC + t] = cpv[q];
+    }
+  };
+
+  float best[2] = {INFINITY, INFINITY};
+  int bidx[2] = {INT_MAX, INT_MAX};
+
+  load(0, 0);
+  store(0, 0, cst[0]);
+  __syncthreads();
+
+  for (int ct = 0; ct < nct; ++ct) {
+    i32x16 acc[4][2];
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[a][b][i] = 0;
+    for (int s = 0; s < S; ++s) {
+      const int it = ct * S + s;
+      const bool has_next = it + 1 < total;
+      const int s_n = (s + 1 == S) ? 0 : s + 1;
+      const int ct_n = (s + 1 == S) ? ct + 1 : ct;
+      if (has_next) load(ct_n, s_n);
+      const uint8_t *buf = cst[it & 1];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int w = min(4 * s + g, W - 1);  // past the end the centroid chunk is zero
+        i32x4 bv[2];
+#pragma unroll
+        for (int pb = 0; pb < 2; ++pb) {
+          const uint32_t word = bitsT[w * kBTP + wave * 64 + pb * 32 + r];
+          bv[pb] = widen16((word >> (16 * h)) & 0xFFFFu);
+        }
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) {
+          const uint4 av = *reinterpret_cast<const uint4 *>(buf + (cb * 32 + r) * kLdsStride + 32 * g + 16 * h);
+          const i32x4 a4 = {(int)av.x, (int)av.y, (int)av.z, (int)av.w};
+#pragma unroll
+          for (int pb = 0; pb < 2; ++pb)
+            acc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a4, bv[pb], acc[cb][pb], 0, 0, 0);
+        }
+      }
+      if (has_next) store(ct_n, s_n, cst[(it + 1) & 1]);
+      __syncthreads();
+    }
+    // epilogue: exact integer dot 2D - T, fp32 score in the fixed order of Eq. 4
+    const int64_t c0 = (int64_t)ct * kBTC;
+    const float *cp = cparl[ct & 1];
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int crow = cb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
+        const int64_t j = c0 + crow;
+        const bool live = j < A.k;
+        const int qs = __float_as_int(cp[crow]);
+        const float u = cp[kBTC + crow];
+        const float s2 = cp[2 * kBTC + crow];
+#pragma unroll
+        for (int pb = 0; pb < 2; ++pb) {
+          const int sd = 2 * acc[cb][pb][i] - qs;
+          const float v = al[pb] * s2;
+          const float sc = fmaf(-v, (float)sd, u);
+          if (live && sc < best[pb]) {
+            best[pb] = sc;
+            bidx[pb] = (int)j;
+          }
+        }
+      }
+  }
+#pragma unroll
+  for (int pb = 0; pb < 2; ++pb) {
+    const float os = __shfl_xor(best[pb], 32);
+    const int oi = __shfl_xor(bidx[pb], 32);
+    if (os < best[pb] || (os == best[pb] && oi < bidx[pb])) {
+      best[pb] = os;
+      bidx[pb] = oi;
+    }
+    const int64_t p = p0 + wave * 64 + pb * 32 + r;
+    if (h == 0 && p < A.n) {
+      A.assign[p] = bidx[pb];
+      if (A.score) A.score[p] = best[pb];
+    }
+  }
+}
+
 // ---- centroid preparation: one workgroup per centroid ----------------------
 
 template <int FMT>
@@ -998,7 +1160,13 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
     A.cild = P.d - d0;
     A.di = P.d - d0;
   }
-  if constexpr (FMT == KM_SQ8 || FMT == KM_SIGN1) {
+  if constexpr (FMT == KM_SIGN1) {
+    if (P.d <= 32 * kBMaxWords) {
+      hipLaunchKernelGGL(assign_bits_kernel, dim3((unsigned)cdiv(P.n, kBTP)), dim3(kBT), 0, s, A);
+    } else {
+      hipLaunchKernelGGL(assign_i8_kernel<FMT>, dim3((unsigned)cdiv(P.n, kT8)), dim3(kThreads), 0, s, A);
+    }
+  } else if constexpr (FMT == KM_SQ8) {
     hipLaunchKernelGGL(assign_i8_kernel<FMT>, dim3((unsigned)cdiv(P.n, kT8)), dim3(kThreads), 0, s, A);
   } else {
     constexpr int TP = Geo<Blocking<FMT>::CB, Blocking<FMT>::PB>::TP;
