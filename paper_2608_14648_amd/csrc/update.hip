@@ -1,6 +1,6 @@
 // STEP 3 (Sec. 2.3): centroid update as a deterministic segmented sum.
 //
-//   1. hist     per block of 4096 points, member counts of every cluster
+//   1. hist     per block of points (about 1024 blocks), member counts of every cluster
 //               (LDS-privatised histogram), stored cluster-major [k][nblk].
 //   2. scan     exclusive scan of that table: entry (j, b) is where block b's
 //               first member of cluster j goes in the cluster-sorted order.
@@ -28,12 +28,13 @@
 namespace kmq {
 namespace {
 
-constexpr int kHistPts = 4096;     // points per histogram / scatter block
+constexpr int kHistBlocks = 1024;  // target number of histogram / scatter blocks
 constexpr int kChunk = 512;        // members per segmented-sum chunk
 constexpr int kLdsCursorMax = 16384;
 constexpr int kScanSeg = 4096;     // elements per scan block (256 threads x 16)
 
 struct UpdWs {
+  int ppb;       // points per histogram / scatter block (multiple of 256)
   int nblk;      // histogram blocks
   int64_t L;     // k * nblk
   int nsb;       // scan blocks
@@ -57,7 +58,8 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 UpdWs carve(const Points &P, int k, void *base, size_t *bytes_out) {
   UpdWs w{};
-  w.nblk = (int)cdiv(P.n, kHistPts);
+  w.ppb = (int)std::max<int64_t>(256, cdiv(cdiv(P.n, kHistBlocks), 256) * 256);
+  w.nblk = (int)cdiv(P.n, w.ppb);
   w.L = (int64_t)k * w.nblk;
   w.nsb = (int)cdiv(w.L, kScanSeg);
   w.maxchunks = (int)(cdiv(P.n, kChunk) + k);
@@ -86,12 +88,12 @@ UpdWs carve(const Points &P, int k, void *base, size_t *bytes_out) {
 }
 
 // ---- 1. histogram ------------------------------------------------------------
-__global__ __launch_bounds__(256) void hist_kernel(const int32_t *assign, int64_t n, int k, int nblk, int *offs,
-                                                   int use_lds) {
+__global__ __launch_bounds__(256) void hist_kernel(const int32_t *assign, int64_t n, int k, int nblk, int ppb,
+                                                   int *offs, int use_lds) {
   extern __shared__ int lc[];
   const int b = blockIdx.x, t = threadIdx.x;
-  const int64_t lo = (int64_t)b * kHistPts;
-  const int64_t hi = min<int64_t>(n, lo + kHistPts);
+  const int64_t lo = (int64_t)b * ppb;
+  const int64_t hi = min<int64_t>(n, lo + ppb);
   if (use_lds) {
     for (int j = t; j < k; j += 256) lc[j] = 0;
     __syncthreads();
@@ -196,13 +198,13 @@ __global__ void counts_kernel(const int *offs, int nblk, int k, const int *total
 }
 
 // ---- 3. stable scatter -------------------------------------------------------
-__global__ __launch_bounds__(256) void scatter_kernel(const int32_t *assign, int64_t n, int k, int nblk, int *offs,
-                                                      int use_lds, int *perm) {
+__global__ __launch_bounds__(256) void scatter_kernel(const int32_t *assign, int64_t n, int k, int nblk, int ppb,
+                                                      int *offs, int use_lds, int *perm) {
   extern __shared__ int cur[];
   const int b = blockIdx.x, t = threadIdx.x;
   const int lane = t & 63, wave = t >> 6;
-  const int64_t lo = (int64_t)b * kHistPts;
-  const int64_t hi = min<int64_t>(n, lo + kHistPts);
+  const int64_t lo = (int64_t)b * ppb;
+  const int64_t hi = min<int64_t>(n, lo + ppb);
   if (use_lds) {
     for (int j = t; j < k; j += 256) cur[j] = offs[(int64_t)j * nblk + b];
     __syncthreads();
@@ -268,17 +270,16 @@ __global__ __launch_bounds__(256) void segsum_f32_kernel(const float *X, int64_t
   const bool ok = col < df;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   int m = m0 + wave;
-  for (; m + 12 < m1; m += 16) {
-    const int p0 = perm[m], p1 = perm[m + 4], p2 = perm[m + 8], p3 = perm[m + 12];
+  for (; m + 28 < m1; m += 32) {
+    int pp[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) pp[e] = perm[m + 4 * e];
     if (ok) {
-      const f32x4 v0 = *reinterpret_cast<const f32x4 *>(X + (int64_t)p0 * ld + col);
-      const f32x4 v1 = *reinterpret_cast<const f32x4 *>(X + (int64_t)p1 * ld + col);
-      const f32x4 v2 = *reinterpret_cast<const f32x4 *>(X + (int64_t)p2 * ld + col);
-      const f32x4 v3 = *reinterpret_cast<const f32x4 *>(X + (int64_t)p3 * ld + col);
-      acc += v0;
-      acc += v1;
-      acc += v2;
-      acc += v3;
+      f32x4 v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = *reinterpret_cast<const f32x4 *>(X + (int64_t)pp[e] * ld + col);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc += v[e];
     }
   }
   for (; m < m1; m += 4) {
@@ -338,11 +339,11 @@ __global__ __launch_bounds__(256) void segsum_bits_kernel(const uint32_t *bits, 
   }
 }
 
-// SQ8 codes: one slice of 256 bytes per workgroup, exact int32 sums
+// SQ8 codes: one slice of 1024 bytes (16 per lane) per workgroup, exact int32 sums
 __global__ __launch_bounds__(256) void segsum_sq8_kernel(const uint8_t *codes, int64_t ld, int d, const int *perm,
                                                          const int *cnt, const int *cstart, const int *choff, int k,
                                                          int *partial) {
-  __shared__ int red[4][64 * 5];
+  __shared__ int red[4][64 * 17];
   const int c = blockIdx.x;
   if (c >= choff[k]) return;
   const int j = find_cluster(choff, k, c);
@@ -350,23 +351,49 @@ __global__ __launch_bounds__(256) void segsum_sq8_kernel(const uint8_t *codes, i
   const int m0 = cstart[j] + ci * kChunk;
   const int m1 = cstart[j] + min(cnt[j], (ci + 1) * kChunk);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int col = blockIdx.y * 256 + 4 * lane;
+  const int col = blockIdx.y * 1024 + 16 * lane;
   const bool ok = col < d;
-  int acc[4] = {0, 0, 0, 0};
-  for (int m = m0 + wave; m < m1; m += 4) {
-    const int p = perm[m];
-    const uint32_t w = ok ? *reinterpret_cast<const uint32_t *>(codes + (int64_t)p * ld + col) : 0u;
+  int acc[16];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) acc[e] += (int)((w >> (8 * e)) & 255u);
+  for (int e = 0; e < 16; ++e) acc[e] = 0;
+  int m = m0 + wave;
+  for (; m + 12 < m1; m += 16) {
+    int pp[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) pp[e] = perm[m + 4 * e];
+    if (ok) {
+      uint4 v[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = *reinterpret_cast<const uint4 *>(codes + (int64_t)pp[e] * ld + col);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t ws[4] = {v[e].x, v[e].y, v[e].z, v[e].w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int b = 0; b < 4; ++b) acc[4 * q + b] += (int)((ws[q] >> (8 * b)) & 255u);
+      }
+    }
+  }
+  for (; m < m1; m += 4) {
+    const int p = perm[m];
+    if (ok) {
+      const uint4 v = *reinterpret_cast<const uint4 *>(codes + (int64_t)p * ld + col);
+      const uint32_t ws[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) acc[4 * q + b] += (int)((ws[q] >> (8 * b)) & 255u);
+    }
   }
 #pragma unroll
-  for (int e = 0; e < 4; ++e) red[wave][lane * 5 + e] = acc[e];
+  for (int e = 0; e < 16; ++e) red[wave][lane * 17 + e] = acc[e];
   __syncthreads();
   if (wave == 0 && ok) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
+    for (int e = 0; e < 16; ++e)
       partial[(int64_t)c * d + col + e] =
-          red[0][lane * 5 + e] + red[1][lane * 5 + e] + red[2][lane * 5 + e] + red[3][lane * 5 + e];
+          red[0][lane * 17 + e] + red[1][lane * 17 + e] + red[2][lane * 17 + e] + red[3][lane * 17 + e];
   }
 }
 
@@ -512,20 +539,21 @@ km_status launch_update(const Points &P, const int32_t *assign, int k, void *C, 
   const bool lds = k <= kLdsCursorMax;
   const size_t lds_bytes = lds ? sizeof(int) * (size_t)k : 0;
   if (!lds) hipLaunchKernelGGL(fill_int_kernel, dim3(1024), dim3(256), 0, s, w.offs, w.L, 0);
-  hipLaunchKernelGGL(hist_kernel, dim3(w.nblk), dim3(256), lds_bytes, s, assign, P.n, k, w.nblk, w.offs, (int)lds);
+  hipLaunchKernelGGL(hist_kernel, dim3(w.nblk), dim3(256), lds_bytes, s, assign, P.n, k, w.nblk, w.ppb, w.offs,
+                     (int)lds);
   hipLaunchKernelGGL(scan_reduce_kernel, dim3(w.nsb), dim3(256), 0, s, w.offs, w.L, w.bsum);
   hipLaunchKernelGGL(scan_single_kernel, dim3(1), dim3(256), 0, s, w.bsum, w.bsum, w.nsb, w.total, 0);
   hipLaunchKernelGGL(scan_down_kernel, dim3(w.nsb), dim3(256), 0, s, w.offs, w.L, w.bsum);
   hipLaunchKernelGGL(counts_kernel, dim3((unsigned)cdiv(k, 256)), dim3(256), 0, s, w.offs, w.nblk, k, w.total, w.cnt,
                      w.cstart);
   hipLaunchKernelGGL(scan_single_kernel, dim3(1), dim3(256), 0, s, w.cnt, w.choff, k, w.choff + k, 1);
-  hipLaunchKernelGGL(scatter_kernel, dim3(w.nblk), dim3(256), lds_bytes, s, assign, P.n, k, w.nblk, w.offs, (int)lds,
-                     w.perm);
+  hipLaunchKernelGGL(scatter_kernel, dim3(w.nblk), dim3(256), lds_bytes, s, assign, P.n, k, w.nblk, w.ppb, w.offs,
+                     (int)lds, w.perm);
   KMQ_LAUNCH_CHECK("update: sort");
 
   const int d = P.d;
   if (P.fmt == KM_SQ8) {
-    hipLaunchKernelGGL(segsum_sq8_kernel, dim3(w.maxchunks, (unsigned)cdiv(d, 256)), dim3(256), 0, s,
+    hipLaunchKernelGGL(segsum_sq8_kernel, dim3(w.maxchunks, (unsigned)cdiv(d, 1024)), dim3(256), 0, s,
                        static_cast<const uint8_t *>(P.data), P.ld, d, w.perm, w.cnt, w.cstart, w.choff, k,
                        static_cast<int *>(w.partial));
     hipLaunchKernelGGL(finalize_sq8_kernel, dim3(k, (unsigned)cdiv(d, 256)), dim3(256), 0, s,
