@@ -25,6 +25,7 @@ EMPTY_KEEP = 1
 _f32p = np.ctypeslib.ndpointer(np.float32, flags="C_CONTIGUOUS")
 _f64p = np.ctypeslib.ndpointer(np.float64, flags="C_CONTIGUOUS")
 _u8p = np.ctypeslib.ndpointer(np.uint8, flags="C_CONTIGUOUS")
+_u16p = np.ctypeslib.ndpointer(np.uint16, flags="C_CONTIGUOUS")
 _i8p = np.ctypeslib.ndpointer(np.int8, flags="C_CONTIGUOUS")
 _u32p = np.ctypeslib.ndpointer(np.uint32, flags="C_CONTIGUOUS")
 _i32p = np.ctypeslib.ndpointer(np.int32, flags="C_CONTIGUOUS")
@@ -48,6 +49,7 @@ def lib():
             "orc_sq8_fit": [_f32p, _i64, _i32, _f32p, _f32p],
             "orc_sq8_encode": [_f32p, _i64, _i32, _f32p, _f32p, _u8p],
             "orc_col_mean": [_f32p, _i64, _i32, _f32p],
+            "orc_bf16_round": [_f32p, _i64, _u16p],
             "orc_sign1_encode": [_f32p, _i64, _i32, _f32p, _i32, _u32p, _f32p],
             "orc_sign1_decode": [_u32p, _f32p, _i64, _i32, _i32, _f32p, _f32p, _i64],
             "orc_pca_cov": [_f32p, _i64, _i32, _f64p, _f64p],
@@ -136,6 +138,20 @@ def sign1_decode(bits, alpha, d: int, m, d0: int = 0):
     return out
 
 
+def bf16_round(X):
+    """Nearest bfloat16 of every value (ties to even), as uint16 bit patterns of X's shape."""
+    X = _c(X, np.float32)
+    out = np.empty(X.shape, np.uint16)
+    lib().orc_bf16_round(X.reshape(-1), X.size, out.reshape(-1))
+    return out
+
+
+def bf16_decode(codes):
+    """fp32 values of bfloat16 bit patterns (the pattern is the top half of the fp32 one)."""
+    codes = np.asarray(codes, dtype=np.uint16)
+    return (codes.astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
 def pca_cov(X):
     X = _c(X, np.float32)
     n, d = X.shape
@@ -191,6 +207,12 @@ def assign_f32(X, C):
     dist = np.empty(n, np.float64)
     lib().orc_assign_f32(X, n, d, d, C, C.shape[0], a, dist)
     return a, dist
+
+
+def assign_bf16(codes, C):
+    """bfloat16 points: the fp32 step on the stored values and on the centroids rounded
+    to bfloat16 (products of bfloat16 values are exact in fp64)."""
+    return assign_f32(bf16_decode(codes), bf16_decode(bf16_round(C)))
 
 
 def assign_sq8(codes, Cc):
@@ -255,6 +277,11 @@ def update_f32(X, a, k: int, C_old, policy: int = EMPTY_SPLIT):
     return C, counts
 
 
+def update_bf16(codes, a, k: int, C_old, policy: int = EMPTY_SPLIT):
+    """bfloat16 points: fp32 centroids = mean of the stored (decoded) member values."""
+    return update_f32(bf16_decode(codes), a, k, C_old, policy)
+
+
 def update_sq8(codes, a, k: int, C_old, policy: int = EMPTY_SPLIT):
     codes = _c(codes, np.uint8)
     n, d = codes.shape
@@ -306,6 +333,8 @@ def init_centroids(P: dict, idx):
         return np.ascontiguousarray(P["X"][idx], dtype=np.float32)
     if fmt == "sq8":
         return np.ascontiguousarray(P["codes"][idx], dtype=np.uint8)
+    if fmt == "bf16":
+        return np.ascontiguousarray(bf16_decode(P["codes"][idx]))
     if fmt == "sign1":
         return sign1_decode(P["bits"][idx], P["alpha"][idx], P["d"], P["m"], 0)
     if fmt == "hybrid":
@@ -323,6 +352,8 @@ def assign(P: dict, C):
         return assign_f32(P["X"], C)
     if fmt == "sq8":
         return assign_sq8(P["codes"], C)
+    if fmt == "bf16":
+        return assign_bf16(P["codes"], C)
     if fmt == "sign1":
         a, _, dist = assign_sign1(P["bits"], P["alpha"], C, P["m"], 0)
         return a, dist
@@ -337,6 +368,8 @@ def update(P: dict, a, k: int, C, policy: int = EMPTY_SPLIT):
         return update_f32(P["X"], a, k, C, policy)
     if fmt == "sq8":
         return update_sq8(P["codes"], a, k, C, policy)
+    if fmt == "bf16":
+        return update_bf16(P["codes"], a, k, C, policy)
     if fmt == "sign1":
         return update_sign1(P["bits"], P["alpha"], P["d"], P["m"], a, k, C, policy)
     if fmt == "hybrid":

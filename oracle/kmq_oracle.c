@@ -60,6 +60,36 @@ void orc_sq8_encode(const float *X, int64_t n, int32_t d, const float *lo, const
 }
 
 /* ------------------------------------------------------------------------ */
+/* bfloat16 storage (Sec. 2.4 names 16-bit full-precision vectors).  A finite
+ * value x = f * 2^e with 0.5 <= |f| < 1 has bfloat16 neighbours spaced
+ * 2^(e-8) apart (never finer than the subnormal spacing 2^-133).  x / spacing is
+ * exact in fp64, rint() rounds it to the nearest integer with ties to even (the
+ * default rounding mode), and scaling back is exact again; the rounded value is
+ * an fp32 number whose low 16 bits are zero. */
+static uint16_t bf16_of(float x) {
+  uint32_t u;
+  if (isnan(x)) {
+    memcpy(&u, &x, 4);
+    return (uint16_t)((u >> 16) | 0x0040u); /* keep sign and payload top, force quiet */
+  }
+  float r = x;
+  if (x != 0.0f && !isinf(x)) {
+    int e;
+    (void)frexp((double)x, &e);
+    int se = e - 8 < -133 ? -133 : e - 8;
+    double q = rint(ldexp((double)x, -se));
+    r = (float)ldexp(q, se); /* exact unless it passes the fp32 range (then +-inf) */
+  }
+  memcpy(&u, &r, 4);
+  return (uint16_t)(u >> 16);
+}
+
+void orc_bf16_round(const float *X, int64_t n, uint16_t *out) {
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < n; ++i) out[i] = bf16_of(X[i]);
+}
+
+/* ------------------------------------------------------------------------ */
 /* 1-bit sign codes (Sec. 3.1, RabitQ without rotation). */
 
 void orc_col_mean(const float *X, int64_t n, int32_t d, float *m) {

@@ -51,6 +51,13 @@ double orc_pca_cov_entry(const float *X, int64_t n, int32_t d, const double *mea
 void orc_project(const float *X, int64_t n, int32_t d, const float *mean, const float *W,
                  int32_t dout, float *Y);
 
+/* 16-bit storage of full-precision vectors (Sec. 2.4): bfloat16, i.e. the fp32
+ * exponent range with 8 significant bits.  Each value is rounded to the nearest
+ * bfloat16, ties to the even significand; the result is returned as its 16-bit
+ * pattern (the top half of the rounded value's fp32 pattern).  NaN stays NaN;
+ * magnitudes that round past the largest bfloat16 become infinities. */
+void orc_bf16_round(const float *X, int64_t n, uint16_t *out);
+
 /* ---- STEP 2: assignment (ties go to the smallest centroid index) ------- */
 
 /* fp32 points: a = argmin_j ||c_j||^2 - 2<x,c_j> (fp64), dist = ||x - c_a||^2 (fp64). */

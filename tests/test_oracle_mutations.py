@@ -30,6 +30,9 @@ MUTATIONS = {
                         "    if (dist) {\n      double e"),
     "sign1_prep_no_centering": ("float t = fabsf(c[i] - m[i]);", "float t = fabsf(c[i]);"),
     "update_sign1_drops_minus": ("-(double)alpha[r]", "0.0"),
+    "bf16_truncates": ("double q = rint(ldexp((double)x, -se));", "double q = trunc(ldexp((double)x, -se));"),
+    "bf16_ties_away_from_zero": ("double q = rint(ldexp((double)x, -se));", "double q = round(ldexp((double)x, -se));"),
+    "bf16_keeps_9_bits": ("int se = e - 8 < -133 ? -133 : e - 8;", "int se = e - 9 < -133 ? -133 : e - 9;"),
 }
 
 PINS = [name for name in dir(pins) if name.startswith("test_")]

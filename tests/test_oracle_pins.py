@@ -450,3 +450,77 @@ def test_col_mean_and_sq8_fit_special_cases(orc):
     lo, hi = orc.sq8_fit(x1)
     np.testing.assert_array_equal(lo, x1[0])
     np.testing.assert_array_equal(hi, x1[0])
+
+
+# --------------------------------------------------------------------------
+# bfloat16 storage (16-bit full-precision vectors, Sec. 2.4)
+
+def _f32(bits):
+    return np.array([bits], np.uint32).view(np.float32)[0]
+
+
+def test_bf16_rounding_hand_examples(orc):
+    """Nearest bfloat16 with ties to the even significand, worked out by hand:
+    bfloat16 keeps the top 16 bits of the fp32 pattern, so the discarded half is
+    compared with 0x8000 (exactly 0x8000 = a tie)."""
+    cases = [
+        (1.0, 0x3F80),
+        (1.0 + 2.0 ** -8, 0x3F80),            # tie, 0x3F80 is even
+        (1.0 + 3 * 2.0 ** -8, 0x3F82),        # tie between 0x3F81 (odd) and 0x3F82
+        (1.0 + 2.0 ** -8 + 2.0 ** -23, 0x3F81),  # just above the tie
+        (-2.5, 0xC020),
+        (-0.0, 0x8000),
+        (2.0 ** -133, 0x0001),                # smallest bfloat16 subnormal
+        (3 * 2.0 ** -134, 0x0002),            # tie between 1 and 2 units of 2^-133
+        (2.0 ** -134, 0x0000),                # tie between 0 and 1 unit
+        (2.0 ** -149, 0x0000),
+        (_f32(0x7F7F7FFF), 0x7F7F),           # below the tie: largest finite bfloat16
+        (_f32(0x7F7FFFFF), 0x7F80),           # largest fp32 rounds past it: +inf
+        (np.inf, 0x7F80),
+        (-np.inf, 0xFF80),
+    ]
+    X = np.array([c[0] for c in cases], np.float32)
+    got = orc.bf16_round(X)
+    assert [int(g) for g in got] == [c[1] for c in cases]
+    nan = orc.bf16_round(np.array([np.nan], np.float32))[0]
+    assert (int(nan) & 0x7F80) == 0x7F80 and (int(nan) & 0x7F) != 0
+
+
+def test_bf16_rounding_matches_library(orc):
+    """Special case that reduces to a library routine: torch's fp32 -> bfloat16
+    conversion on the CPU (round to nearest, ties to even) on values spanning the
+    whole exponent range, exact ties included."""
+    import torch
+    rng = np.random.default_rng(31)
+    u = rng.integers(0, 2 ** 32, 200_000, dtype=np.uint64).astype(np.uint32)
+    u = u[(u & 0x7F800000) != 0x7F800000]                   # finite patterns, subnormals included
+    ties = (u & 0xFFFF0000) | 0x8000                          # exact ties
+    X = np.concatenate([u, ties]).view(np.float32)
+    ref = torch.from_numpy(X.copy()).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    np.testing.assert_array_equal(orc.bf16_round(X), ref)
+
+
+def test_bf16_steps_on_representable_data_equal_f32(orc):
+    """Points and centroids that are already bfloat16 values: the bfloat16 steps
+    must give exactly the fp32 steps (rounding is the identity on them), and the
+    rounding error bound |x - bf16(x)| <= 2^-8 |x| (unit roundoff of 8 significant
+    bits) holds on normal values."""
+    rng = np.random.default_rng(32)
+    X = rng.standard_normal((300, 48)).astype(np.float32)
+    codes = orc.bf16_round(X)
+    Xb = orc.bf16_decode(codes)
+    assert np.all(np.abs(Xb.astype(np.float64) - X) <= 2.0 ** -8 * np.abs(X.astype(np.float64)))
+    np.testing.assert_array_equal(orc.bf16_round(Xb), codes)  # idempotent
+    C = Xb[[3, 70, 150, 220, 299]].copy()
+    a16, d16 = orc.assign_bf16(codes, C)
+    a32, d32 = orc.assign_f32(Xb, C)
+    np.testing.assert_array_equal(a16, a32)
+    np.testing.assert_array_equal(d16, d32)
+    C16, n16 = orc.update_bf16(codes, a16, 5, C)
+    C32, n32 = orc.update_f32(Xb, a32, 5, C)
+    np.testing.assert_array_equal(C16, C32)
+    np.testing.assert_array_equal(n16, n32)
+    # a cluster whose members all hold one value keeps exactly that value
+    same = np.repeat(codes[:1], 7, axis=0)
+    Cm, _ = orc.update_bf16(same, np.zeros(7, np.int32), 1, np.zeros((1, 48), np.float32))
+    np.testing.assert_array_equal(Cm[0], Xb[0])
