@@ -45,6 +45,7 @@ typedef enum {
 
 typedef enum {
   KM_F32 = 0,    /* fp32 vectors (raw, PCA-projected or a dimension prefix) */
+  KM_BF16 = 1,   /* bfloat16 vectors (16-bit storage of full-precision vectors, Sec. 2.4) */
   KM_SQ8 = 2,    /* uint8 scalar-quantised codes, one (lo, hi) pair per dimension */
   KM_SIGN1 = 3,  /* 1-bit sign codes of x - m plus one fp32 scale alpha per vector */
   KM_HYBRID = 4  /* fp32 front dims [0, d_front) + 1-bit codes on the tail [d_front, d) */
@@ -61,6 +62,8 @@ typedef enum {
 /*
  * The points being clustered, in their compressed form.
  *   KM_F32:    data = float[n][ld], d <= ld, ld % 4 == 0, data 16-byte aligned, d % 4 == 0.
+ *   KM_BF16:   data = bfloat16 (uint16 bit patterns)[n][ld], d <= ld, ld % 8 == 0,
+ *              d % 8 == 0, 16-byte aligned.
  *   KM_SQ8:    data = uint8[n][ld] codes, ld % 16 == 0, d % 16 == 0, 16-byte aligned.
  *   KM_SIGN1:  data = uint32[n][d/32] bits, d % 32 == 0; alpha = float[n];
  *              center = m, float[d] (the mean the codes were taken around).
@@ -75,7 +78,7 @@ typedef struct km_points {
   int32_t d;            /* logical dimensionality */
   int64_t n;            /* number of points, 1 <= n < 2^31 */
   const void *data;
-  int64_t ld;           /* row stride in elements (F32: floats, SQ8: bytes) */
+  int64_t ld;           /* row stride in elements (F32: floats, BF16: 16-bit values, SQ8: bytes) */
   const float *alpha;
   const float *center;
   const float *front;
@@ -98,6 +101,10 @@ typedef struct km_points {
  *     If d_front > 0 and front != NULL, front = float[n][d_front] receives a copy
  *     of the first d_front dims (the hybrid layout).  d % 32 == 0, d_front % 32 == 0;
  *     params and front 16-byte aligned.
+ *   fmt == KM_BF16 (16-bit storage, Sec. 2.4): codes = bfloat16[n][d], each value
+ *     rounded to the nearest bfloat16 with ties to the even significand (NaN stays
+ *     NaN, overflow gives infinities).  params, alpha, front: unused (may be NULL);
+ *     d % 8 == 0, d_front == 0, flags ignored.
  *   flags & KM_Q_FIT_PARAMS: compute params from X first (one extra pass over X);
  *     otherwise params are inputs.
  */
@@ -125,12 +132,15 @@ km_status pca_project(const float *X, int64_t n, int32_t d, const float *mean, c
  * centroid (ties to the smallest index), without materialising the n x k
  * distance matrix.
  *   C: centroids in the clustering space, k x d, row-major:
- *      KM_F32: float; KM_SQ8: uint8 codes; KM_SIGN1 / KM_HYBRID: float in the
- *      original space (the 1-bit part is compared against int8 residual codes
+ *      KM_F32 / KM_BF16: float; KM_SQ8: uint8 codes; KM_SIGN1 / KM_HYBRID: float in
+ *      the original space (the 1-bit part is compared against int8 residual codes
  *      q = rint((c - m)/sigma), sigma = max|c - m|/127, rebuilt on each call).
+ *      KM_BF16 compares the points with the centroids rounded to bfloat16 (nearest,
+ *      ties to even), products exact, fp32 accumulation.
  *   assign: int32[n].  score (nullable): float[n], the winning score, i.e. the
  *      in-space squared distance minus the point-only term:
- *      F32: ||c||^2 - 2<x,c>;  SQ8: ||c~||^2 - 2<x~,c~> with x~ = code - 128;
+ *      F32: ||c||^2 - 2<x,c>;  BF16: the same on the bfloat16 values;
+ *      SQ8: ||c~||^2 - 2<x~,c~> with x~ = code - 128;
  *      SIGN1: fmaf(-alpha*2*sigma, <2b-1, q>, sigma^2 ||q||^2);
  *      HYBRID: front F32 score + tail SIGN1 score.
  *   objective (nullable): double[1], receives sum over points of the in-space
@@ -143,7 +153,8 @@ km_status kmeans_assign(const km_points *P, const void *C, int32_t k, int32_t *a
 /*
  * kmeans_update -- STEP 3 (Sec. 2.3): each centroid becomes the mean of its
  * members, in the clustering space:
- *   KM_F32: fp32 mean; KM_SQ8: floor((2 S + n_j) / (2 n_j)) with S the exact code sum
+ *   KM_F32: fp32 mean; KM_BF16: fp32 mean of the stored bfloat16 values;
+ *   KM_SQ8: floor((2 S + n_j) / (2 n_j)) with S the exact code sum
  *   (averaging in the quantised domain, Sec. 3.1); KM_SIGN1: m + (1/n_j) sum alpha (2b - 1)
  *   (fused decode-averaging, Sec. 3.1); KM_HYBRID: front mean and tail decode-average.
  *   C: in = previous centroids, out = new ones (same type as kmeans_assign).

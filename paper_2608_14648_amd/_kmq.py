@@ -16,7 +16,7 @@ import torch
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libkmq.so")
 
-KM_F32, KM_SQ8, KM_SIGN1, KM_HYBRID = 0, 2, 3, 4
+KM_F32, KM_BF16, KM_SQ8, KM_SIGN1, KM_HYBRID = 0, 1, 2, 3, 4
 KM_EMPTY_SPLIT, KM_EMPTY_KEEP = 0, 1
 KM_Q_FIT_PARAMS = 1
 STATUS = {0: "KM_OK", -1: "KM_EINVAL", -2: "KM_EUNSUPPORTED", -3: "KM_ENOMEM", -4: "KM_EDEVICE"}
@@ -110,7 +110,7 @@ class Points:
         self.fmt, self.data, self.d = fmt, data, d
         self.alpha, self.center, self.front, self.d_front = alpha, center, front, d_front
         self.n = data.shape[0]
-        ld = data.stride(0) if fmt in (KM_F32, KM_SQ8) else d // 32
+        ld = data.stride(0) if fmt in (KM_F32, KM_BF16, KM_SQ8) else d // 32
         self._c = KmPoints(fmt, d, self.n, data.data_ptr(), ld, _ptr(alpha) or None, _ptr(center) or None,
                            _ptr(front) or None, d_front, 0)
 
@@ -139,6 +139,12 @@ def points_f32(X: torch.Tensor) -> Points:
     """fp32 points; rows must be contiguous, the row stride may be larger than d."""
     _rows(X, torch.float32, "X")
     return Points(KM_F32, X, X.shape[1])
+
+
+def points_bf16(X: torch.Tensor) -> Points:
+    """bfloat16 points (torch.bfloat16); rows must be contiguous, the row stride may be larger than d."""
+    _rows(X, torch.bfloat16, "X")
+    return Points(KM_BF16, X, X.shape[1])
 
 
 def points_sq8(codes: torch.Tensor) -> Points:
@@ -182,6 +188,15 @@ def quantize_sq8(X: torch.Tensor, params: torch.Tensor | None = None):
     _check(lib().quantize(_ptr(X), n, d, X.stride(0), KM_SQ8, _ptr(codes), _ptr(params), None, 0, None, flags,
                           _stream()))
     return codes, params
+
+
+def quantize_bf16(X: torch.Tensor) -> torch.Tensor:
+    """bfloat16 copy of fp32 points (nearest, ties to even), n x d torch.bfloat16."""
+    _dev(X, torch.float32, "X", 2)
+    n, d = X.shape
+    out = torch.empty((n, d), dtype=torch.bfloat16, device=X.device)
+    _check(lib().quantize(_ptr(X), n, d, X.stride(0), KM_BF16, _ptr(out), None, None, 0, None, 0, _stream()))
+    return out
 
 
 def quantize_sign1(X: torch.Tensor, center: torch.Tensor | None = None, d_front: int = 0, want_front: bool = False):

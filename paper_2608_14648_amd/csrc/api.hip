@@ -89,7 +89,7 @@ static size_t al(size_t x) { return (x + 255) & ~(size_t)255; }
 static km_status check_points(const km_points *P, Points *out) {
   KMQ_CHECK(P != nullptr, KM_EINVAL, "points descriptor is NULL");
   const int fmt = P->fmt;
-  KMQ_CHECK(fmt == KM_F32 || fmt == KM_SQ8 || fmt == KM_SIGN1 || fmt == KM_HYBRID, KM_EUNSUPPORTED,
+  KMQ_CHECK(fmt == KM_F32 || fmt == KM_BF16 || fmt == KM_SQ8 || fmt == KM_SIGN1 || fmt == KM_HYBRID, KM_EUNSUPPORTED,
             "unknown point format %d", fmt);
   KMQ_CHECK(P->reserved == 0, KM_EINVAL, "reserved field must be 0");
   KMQ_CHECK(P->n >= 1 && P->n < (int64_t)INT32_MAX, KM_EINVAL, "n = %lld outside [1, 2^31)", (long long)P->n);
@@ -109,6 +109,10 @@ static km_status check_points(const km_points *P, Points *out) {
   if (fmt == KM_F32) {
     KMQ_CHECK(P->d % 4 == 0, KM_EINVAL, "fp32 points need d %% 4 == 0 (d = %d)", P->d);
     KMQ_CHECK(P->ld >= P->d && P->ld % 4 == 0, KM_EINVAL, "fp32 points need ld >= d and ld %% 4 == 0");
+    KMQ_CHECK(P->d_front == 0, KM_EINVAL, "d_front must be 0 for this format");
+  } else if (fmt == KM_BF16) {
+    KMQ_CHECK(P->d % 8 == 0, KM_EINVAL, "bfloat16 points need d %% 8 == 0 (d = %d)", P->d);
+    KMQ_CHECK(P->ld >= P->d && P->ld % 8 == 0, KM_EINVAL, "bfloat16 points need ld >= d and ld %% 8 == 0");
     KMQ_CHECK(P->d_front == 0, KM_EINVAL, "d_front must be 0 for this format");
   } else if (fmt == KM_SQ8) {
     KMQ_CHECK(P->d % 16 == 0, KM_EINVAL, "SQ8 codes need d %% 16 == 0 (d = %d)", P->d);
@@ -139,7 +143,7 @@ static km_status check_centroids(const Points &p, const void *C, int k) {
   return KM_OK;
 }
 
-static size_t centroid_bytes(const Points &p, int k) {
+static size_t centroid_bytes(const Points &p, int k) {  // BF16 centroids are fp32
   return (size_t)k * p.d * (p.fmt == KM_SQ8 ? 1 : sizeof(float));
 }
 
@@ -163,14 +167,18 @@ km_status km_release(void) {
 km_status quantize(const float *X, int64_t n, int32_t d, int64_t ldx, int32_t fmt, void *codes, float *params,
                    float *alpha, int32_t d_front, float *front, int32_t flags, km_stream stream) {
   g_err[0] = 0;
-  KMQ_CHECK(fmt == KM_SQ8 || fmt == KM_SIGN1, KM_EUNSUPPORTED, "quantize supports SQ8 and SIGN1 (fmt = %d)", fmt);
-  KMQ_CHECK(X != nullptr && codes != nullptr && params != nullptr, KM_EINVAL, "NULL argument");
+  KMQ_CHECK(fmt == KM_SQ8 || fmt == KM_SIGN1 || fmt == KM_BF16, KM_EUNSUPPORTED,
+            "quantize supports SQ8, SIGN1 and BF16 (fmt = %d)", fmt);
+  KMQ_CHECK(X != nullptr && codes != nullptr && (params != nullptr || fmt == KM_BF16), KM_EINVAL, "NULL argument");
   KMQ_CHECK(n >= 1 && n < (int64_t)INT32_MAX, KM_EINVAL, "n = %lld outside [1, 2^31)", (long long)n);
   KMQ_CHECK(d >= 1 && ldx >= d && ldx % 4 == 0, KM_EINVAL, "need d >= 1, ldx >= d, ldx %% 4 == 0");
   KMQ_CHECK(aligned16(X) && aligned16(codes), KM_EINVAL, "X and codes must be 16-byte aligned");
   KMQ_CHECK((flags & ~KM_Q_FIT_PARAMS) == 0, KM_EINVAL, "unknown flags 0x%x", flags);
   if (fmt == KM_SQ8) {
     KMQ_CHECK(d % 16 == 0, KM_EINVAL, "SQ8 needs d %% 16 == 0 (d = %d)", d);
+    KMQ_CHECK(d_front == 0 && front == nullptr, KM_EINVAL, "d_front/front are for 1-bit codes only");
+  } else if (fmt == KM_BF16) {
+    KMQ_CHECK(d % 8 == 0, KM_EINVAL, "BF16 needs d %% 8 == 0 (d = %d)", d);
     KMQ_CHECK(d_front == 0 && front == nullptr, KM_EINVAL, "d_front/front are for 1-bit codes only");
   } else {
     KMQ_CHECK(d % 32 == 0, KM_EINVAL, "1-bit codes need d %% 32 == 0 (d = %d)", d);

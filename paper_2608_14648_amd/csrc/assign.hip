@@ -528,7 +528,7 @@ __device__ __forceinline__ void load_stage8(const AssignArgs &A, int s, int64_t 
     const int b = b0 + 16 * col;
     const int bc = b < A.di ? b : 0;
     R.c[i] = *reinterpret_cast<const uint4 *>(cbase + (uint32_t)(min(row, crmax) * (int)A.cild + bc));
-    if (FMT == KM_SQ8)
+    if (FMT == KM_SQ8 || FMT == KM_BF16)
       R.p[i] = *reinterpret_cast<const uint4 *>(pbase8 + (uint32_t)(min(row, prmax) * (int)A.pild + bc));
   }
   if (FMT == KM_SIGN1) {
@@ -542,7 +542,7 @@ __device__ __forceinline__ void load_stage8(const AssignArgs &A, int s, int64_t 
   }
   if (s == 0) {
     const int64_t j = min<int64_t>(c0 + t, A.k - 1);
-    R.cpar[1] = __int_as_float(A.cp.qsum[j]);
+    R.cpar[1] = FMT == KM_BF16 ? A.cp.cn[j] : __int_as_float(A.cp.qsum[j]);
     if (FMT == KM_SIGN1) {
       R.cpar[2] = A.cp.u[j];
       R.cpar[3] = A.cp.sig2[j];
@@ -565,6 +565,7 @@ __device__ __forceinline__ void store_stage8(const AssignArgs &A, int s, const S
     *reinterpret_cast<uint4 *>(ct + row * kLdsStride + 16 * col) = mask4(cv, ok);
     if (FMT == KM_SQ8)
       *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 16 * col) = mask4(flip4(R.p[i]), ok);
+    if (FMT == KM_BF16) *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 16 * col) = mask4(R.p[i], ok);
   }
   if (FMT == KM_SIGN1) {
 #pragma unroll
@@ -586,8 +587,16 @@ __device__ __forceinline__ void store_stage8(const AssignArgs &A, int s, const S
   }
 }
 
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+// 16 bytes per lane are one operand of either matrix instruction: 16 int8 codes of
+// v_mfma_i32_32x32x32_i8 or 8 bfloat16 values of v_mfma_f32_32x32x16_bf16.
+template <bool BF>
+using Acc8 = typename std::conditional<BF, f32x16, i32x16>::type;
+
+template <bool BF>
 __device__ __forceinline__ void mfma_stage8(const uint8_t *cbuf, const uint8_t *pbuf, int wc, int wp, int r, int h,
-                                            i32x16 (&acc)[4][4]) {
+                                            Acc8<BF> (&acc)[4][4]) {
   uint4 av[2][4], bv[2][4];
 #pragma unroll
   for (int cb = 0; cb < 4; ++cb)
@@ -612,9 +621,15 @@ __device__ __forceinline__ void mfma_stage8(const uint8_t *cbuf, const uint8_t *
     for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
       for (int pb = 0; pb < 4; ++pb) {
-        const i32x4 a4 = {(int)av[cur][cb].x, (int)av[cur][cb].y, (int)av[cur][cb].z, (int)av[cur][cb].w};
-        const i32x4 b4 = {(int)bv[cur][pb].x, (int)bv[cur][pb].y, (int)bv[cur][pb].z, (int)bv[cur][pb].w};
-        acc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a4, b4, acc[cb][pb], 0, 0, 0);
+        if constexpr (BF) {
+          const bf16x8 a8 = __builtin_bit_cast(bf16x8, av[cur][cb]);
+          const bf16x8 b8 = __builtin_bit_cast(bf16x8, bv[cur][pb]);
+          acc[cb][pb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a8, b8, acc[cb][pb], 0, 0, 0);
+        } else {
+          const i32x4 a4 = {(int)av[cur][cb].x, (int)av[cur][cb].y, (int)av[cur][cb].z, (int)av[cur][cb].w};
+          const i32x4 b4 = {(int)bv[cur][pb].x, (int)bv[cur][pb].y, (int)bv[cur][pb].z, (int)bv[cur][pb].w};
+          acc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a4, b4, acc[cb][pb], 0, 0, 0);
+        }
       }
   }
 }
@@ -640,7 +655,8 @@ __global__ __launch_bounds__(kThreads, 1) void assign_i8_kernel(AssignArgs A) {
 #pragma unroll
     for (int pb = 0; pb < 4; ++pb) al[pb] = A.alpha[min<int64_t>(p0 + wp * 128 + pb * 32 + r, A.n - 1)];
   }
-  i32x16 acc[4][4];
+  constexpr bool BF = FMT == KM_BF16;
+  Acc8<BF> acc[4][4];
 #pragma unroll
   for (int a = 0; a < 4; ++a)
 #pragma unroll
@@ -669,7 +685,7 @@ __global__ __launch_bounds__(kThreads, 1) void assign_i8_kernel(AssignArgs A) {
       const int ct_n = (s + 1 == S) ? ct + 1 : ct;
       if (has_next) load_stage8<FMT>(A, s_n, (int64_t)ct_n * kT8, p0, R);
       const uint8_t *buf = lds + (it & 1) * kStageBytes8;
-      mfma_stage8(buf, buf + kTileBytes8, wc, wp, r, h, acc);
+      mfma_stage8<BF>(buf, buf + kTileBytes8, wc, wp, r, h, acc);
       if (has_next) store_stage8<FMT>(A, s_n, R, lds + ((it + 1) & 1) * kStageBytes8, cparl[ct_n & 1]);
       __syncthreads();
     }
@@ -690,6 +706,8 @@ __global__ __launch_bounds__(kThreads, 1) void assign_i8_kernel(AssignArgs A) {
           score_t sc;
           if constexpr (FMT == KM_SQ8) {
             sc = qs - 2 * acc[cb][pb][i];
+          } else if constexpr (FMT == KM_BF16) {
+            sc = fmaf(-2.0f, acc[cb][pb][i], __int_as_float(qs));  // ||c||^2 - 2<x,c>
           } else {
             const int sd = 2 * acc[cb][pb][i] - qs;
             const float v = al[pb] * s2;
@@ -914,7 +932,8 @@ __global__ __launch_bounds__(kBT, 1) void assign_bits_kernel(AssignArgs A) {
 
 template <int FMT>
 __global__ __launch_bounds__(256) void prep_kernel(const void *Cv, int k, int d, int d0, const float *m,
-                                                   float *cn, int *qsum, float *u, float *sig2, int8_t *q) {
+                                                   float *cn, int *qsum, float *u, float *sig2, int8_t *q,
+                                                   uint16_t *cb) {
   __shared__ double shd[256];
   __shared__ float shf[256];
   __shared__ int shi[256];
@@ -925,6 +944,18 @@ __global__ __launch_bounds__(256) void prep_kernel(const void *Cv, int k, int d,
     const int dd = FMT == KM_F32 ? d : d0;
     double s = 0.0;
     for (int i = t; i < dd; i += 256) s += (double)c[i] * (double)c[i];
+    s = block_sum_f64(s, shd);
+    if (t == 0) cn[j] = (float)s;
+  }
+  if (FMT == KM_BF16) {  // round the fp32 centroid to bfloat16; ||c||^2 of the rounded values
+    const float *c = static_cast<const float *>(Cv) + (int64_t)j * d;
+    double s = 0.0;
+    for (int i = t; i < d; i += 256) {
+      const uint32_t b = bf16_bits(c[i]);
+      cb[(int64_t)j * d + i] = (uint16_t)b;
+      const double v = bf16_value(b);
+      s += v * v;
+    }
     s = block_sum_f64(s, shd);
     if (t == 0) cn[j] = (float)s;
   }
@@ -990,7 +1021,7 @@ __global__ __launch_bounds__(256) void prep_kernel(const void *Cv, int k, int d,
 }
 
 // ---- point-only terms of the in-space distance ------------------------------
-// F32: ||x||^2 ; SQ8: ||code-128||^2 ; SIGN1: alpha^2 d ; HYBRID: ||x'||^2 + alpha^2 (d - d0)
+// F32, BF16: ||x||^2 ; SQ8: ||code-128||^2 ; SIGN1: alpha^2 d ; HYBRID: ||x'||^2 + alpha^2 (d - d0)
 // One wave per point, 16-byte loads.
 template <int FMT>
 __global__ __launch_bounds__(256) void xconst_kernel(Points P, float *xc) {
@@ -1004,6 +1035,17 @@ __global__ __launch_bounds__(256) void xconst_kernel(Points P, float *xc) {
     for (int i = 4 * lane; i < dd; i += 256) {
       const f32x4 v = *reinterpret_cast<const f32x4 *>(x + i);
       s += (double)v.x * v.x + (double)v.y * v.y + (double)v.z * v.z + (double)v.w * v.w;
+    }
+  } else if (FMT == KM_BF16) {
+    const uint16_t *x = static_cast<const uint16_t *>(P.data) + p * P.ld;
+    for (int i = 8 * lane; i < P.d; i += 512) {
+      const uint4 w = *reinterpret_cast<const uint4 *>(x + i);
+      const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const double lo = bf16_value(ws[q] & 0xffffu), hi = bf16_value(ws[q] >> 16);
+        s += lo * lo + hi * hi;
+      }
     }
   } else if (FMT == KM_SQ8) {
     const uint8_t *x = static_cast<const uint8_t *>(P.data) + p * P.ld;
@@ -1062,6 +1104,10 @@ __global__ __launch_bounds__(256) void gather_kernel(Points P, const int64_t *id
     const float *x = static_cast<const float *>(P.data) + row * P.ld;
     float *c = static_cast<float *>(Cv) + (int64_t)j * d;
     for (int i = threadIdx.x; i < d; i += 256) c[i] = x[i];
+  } else if (FMT == KM_BF16) {
+    const uint16_t *x = static_cast<const uint16_t *>(P.data) + row * P.ld;
+    float *c = static_cast<float *>(Cv) + (int64_t)j * d;
+    for (int i = threadIdx.x; i < d; i += 256) c[i] = bf16_value(x[i]);
   } else if (FMT == KM_SQ8) {
     const uint8_t *x = static_cast<const uint8_t *>(P.data) + row * P.ld;
     uint8_t *c = static_cast<uint8_t *>(Cv) + (int64_t)j * d;
@@ -1144,6 +1190,12 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
     A.ci8 = static_cast<const int8_t *>(C);
     A.cild = P.d;
     A.di = P.d;
+  } else if (FMT == KM_BF16) {  // byte-addressed rows of 16-bit values
+    A.pi8 = static_cast<const uint8_t *>(P.data);
+    A.pild = 2 * P.ld;
+    A.ci8 = reinterpret_cast<const int8_t *>(cp.cb);
+    A.cild = 2 * (int64_t)P.d;
+    A.di = 2 * P.d;
   } else {
     const int d0 = FMT == KM_HYBRID ? P.d_front : 0;
     if (FMT == KM_HYBRID) {
@@ -1166,7 +1218,7 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
     } else {
       hipLaunchKernelGGL(assign_i8_kernel<FMT>, dim3((unsigned)cdiv(P.n, kT8)), dim3(kThreads), 0, s, A);
     }
-  } else if constexpr (FMT == KM_SQ8) {
+  } else if constexpr (FMT == KM_SQ8 || FMT == KM_BF16) {
     hipLaunchKernelGGL(assign_i8_kernel<FMT>, dim3((unsigned)cdiv(P.n, kT8)), dim3(kThreads), 0, s, A);
   } else {
     constexpr int TP = Geo<Blocking<FMT>::CB, Blocking<FMT>::PB>::TP;
@@ -1182,6 +1234,7 @@ size_t prep_bytes(const Points &P, int k) {
   const int d0 = P.fmt == KM_HYBRID ? P.d_front : 0;
   size_t b = 4 * (size_t)k * sizeof(float) + 256;
   if (P.fmt == KM_SIGN1 || P.fmt == KM_HYBRID) b += (size_t)k * (size_t)(P.d - d0) + 256;
+  if (P.fmt == KM_BF16) b += 2 * (size_t)k * (size_t)P.d + 256;
   return b;
 }
 
@@ -1192,26 +1245,32 @@ km_status launch_prep(const Points &P, const void *C, int k, void *ws, CentroidP
   float *u = reinterpret_cast<float *>(w + (size_t)k * 8);
   float *sig2 = reinterpret_cast<float *>(w + (size_t)k * 12);
   int8_t *q = reinterpret_cast<int8_t *>(w + (((size_t)k * 16 + 255) & ~(size_t)255));
+  uint16_t *cb = reinterpret_cast<uint16_t *>(q);  // BF16 uses the same region for its rows
   out->cn = cn;
   out->qsum = qsum;
   out->u = u;
   out->sig2 = sig2;
   out->q = q;
+  out->cb = cb;
   const int d0 = P.fmt == KM_HYBRID ? P.d_front : 0;
   switch (P.fmt) {
     case KM_F32:
-      hipLaunchKernelGGL(prep_kernel<KM_F32>, dim3(k), dim3(256), 0, s, C, k, P.d, 0, nullptr, cn, qsum, u, sig2, q);
+      hipLaunchKernelGGL(prep_kernel<KM_F32>, dim3(k), dim3(256), 0, s, C, k, P.d, 0, nullptr, cn, qsum, u, sig2, q, cb);
+      break;
+    case KM_BF16:
+      hipLaunchKernelGGL(prep_kernel<KM_BF16>, dim3(k), dim3(256), 0, s, C, k, P.d, 0, nullptr, cn, qsum, u, sig2, q,
+                         cb);
       break;
     case KM_SQ8:
-      hipLaunchKernelGGL(prep_kernel<KM_SQ8>, dim3(k), dim3(256), 0, s, C, k, P.d, 0, nullptr, cn, qsum, u, sig2, q);
+      hipLaunchKernelGGL(prep_kernel<KM_SQ8>, dim3(k), dim3(256), 0, s, C, k, P.d, 0, nullptr, cn, qsum, u, sig2, q, cb);
       break;
     case KM_SIGN1:
       hipLaunchKernelGGL(prep_kernel<KM_SIGN1>, dim3(k), dim3(256), 0, s, C, k, P.d, 0, P.center, cn, qsum, u, sig2,
-                         q);
+                         q, cb);
       break;
     case KM_HYBRID:
       hipLaunchKernelGGL(prep_kernel<KM_HYBRID>, dim3(k), dim3(256), 0, s, C, k, P.d, d0, P.center, cn, qsum, u,
-                         sig2, q);
+                         sig2, q, cb);
       break;
     default:
       return KM_EUNSUPPORTED;
@@ -1224,6 +1283,7 @@ km_status launch_assign(const Points &P, const void *C, const CentroidPrep &cp, 
                         float *score, hipStream_t s) {
   switch (P.fmt) {
     case KM_F32: return launch_assign_t<KM_F32>(P, C, cp, k, assign, score, s);
+    case KM_BF16: return launch_assign_t<KM_BF16>(P, C, cp, k, assign, score, s);
     case KM_SQ8: return launch_assign_t<KM_SQ8>(P, C, cp, k, assign, score, s);
     case KM_SIGN1: return launch_assign_t<KM_SIGN1>(P, C, cp, k, assign, score, s);
     case KM_HYBRID: return launch_assign_t<KM_HYBRID>(P, C, cp, k, assign, score, s);
@@ -1235,6 +1295,7 @@ km_status launch_xconst(const Points &P, float *xc, hipStream_t s) {
   const dim3 g((unsigned)cdiv(P.n, 4));
   switch (P.fmt) {
     case KM_F32: hipLaunchKernelGGL(xconst_kernel<KM_F32>, g, dim3(256), 0, s, P, xc); break;
+    case KM_BF16: hipLaunchKernelGGL(xconst_kernel<KM_BF16>, g, dim3(256), 0, s, P, xc); break;
     case KM_SQ8: hipLaunchKernelGGL(xconst_kernel<KM_SQ8>, g, dim3(256), 0, s, P, xc); break;
     case KM_SIGN1: hipLaunchKernelGGL(xconst_kernel<KM_SIGN1>, g, dim3(256), 0, s, P, xc); break;
     case KM_HYBRID: hipLaunchKernelGGL(xconst_kernel<KM_HYBRID>, g, dim3(256), 0, s, P, xc); break;
@@ -1259,6 +1320,7 @@ km_status launch_objective(const Points &P, const float *xc, const float *score,
 km_status launch_gather_init(const Points &P, const int64_t *idx, int k, void *C, hipStream_t s) {
   switch (P.fmt) {
     case KM_F32: hipLaunchKernelGGL(gather_kernel<KM_F32>, dim3(k), dim3(256), 0, s, P, idx, C); break;
+    case KM_BF16: hipLaunchKernelGGL(gather_kernel<KM_BF16>, dim3(k), dim3(256), 0, s, P, idx, C); break;
     case KM_SQ8: hipLaunchKernelGGL(gather_kernel<KM_SQ8>, dim3(k), dim3(256), 0, s, P, idx, C); break;
     case KM_SIGN1: hipLaunchKernelGGL(gather_kernel<KM_SIGN1>, dim3(k), dim3(256), 0, s, P, idx, C); break;
     case KM_HYBRID: hipLaunchKernelGGL(gather_kernel<KM_HYBRID>, dim3(k), dim3(256), 0, s, P, idx, C); break;

@@ -37,6 +37,7 @@ struct CentroidPrep {
   const float *u;      // SIGN1/HYBRID: (sigma*sigma)*Q
   const float *sig2;   // SIGN1/HYBRID: 2*sigma
   const int8_t *q;     // SIGN1/HYBRID: int8 residual codes, k x dt
+  const uint16_t *cb;  // BF16: centroids rounded to bfloat16, k x d
 };
 
 // Host-side error plumbing.
@@ -98,6 +99,20 @@ size_t pca_project_bytes(int d, int d_out);
 // ---- device helpers ---------------------------------------------------------
 
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+// Nearest bfloat16 of x, ties to the even significand, as its 16-bit pattern.
+// bfloat16 keeps the top 16 bits of the fp32 pattern; adding 0x7FFF plus the
+// lowest kept bit carries into the kept half exactly when the discarded half
+// exceeds 0x8000, or equals it and the kept half is odd.  A carry out of the
+// significand steps the exponent (up to infinity), which is the correct result.
+// NaN keeps its sign and top payload bits and is made quiet.
+__device__ __forceinline__ uint32_t bf16_bits(float x) {
+  const uint32_t u = __float_as_uint(x);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+__device__ __forceinline__ float bf16_value(uint32_t b) { return __uint_as_float(b << 16); }
 
 // Deterministic block-wide sum of doubles (fixed tree order). blockDim.x == 256.
 __device__ __forceinline__ double block_sum_f64(double v, double *sh) {

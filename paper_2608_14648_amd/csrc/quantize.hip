@@ -115,6 +115,22 @@ __global__ __launch_bounds__(256) void sq8_encode_kernel(const float *X, int64_t
   }
 }
 
+// 8 values per thread: two float4 loads, one 16-byte store of bfloat16 patterns.
+__global__ __launch_bounds__(256) void bf16_encode_kernel(const float *X, int64_t n, int d, int64_t ldx,
+                                                          uint16_t *codes) {
+  const int per = d / 8;
+  const int64_t total = n * per;
+  for (int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x; g < total; g += (int64_t)gridDim.x * 256) {
+    const int64_t r = g / per;
+    const int c = (int)(g - r * per) * 8;
+    const f32x4 a = *reinterpret_cast<const f32x4 *>(X + r * ldx + c);
+    const f32x4 b = *reinterpret_cast<const f32x4 *>(X + r * ldx + c + 4);
+    const uint4 w = make_uint4(bf16_bits(a[0]) | (bf16_bits(a[1]) << 16), bf16_bits(a[2]) | (bf16_bits(a[3]) << 16),
+                               bf16_bits(b[0]) | (bf16_bits(b[1]) << 16), bf16_bits(b[2]) | (bf16_bits(b[3]) << 16));
+    *reinterpret_cast<uint4 *>(codes + r * d + c) = w;
+  }
+}
+
 // One wave per row.  Lane l reads dims [base + 4l, base + 4l + 4) as a float4 and
 // forms a 4-bit nibble of sign bits; the 8 lanes that share a 32-dim word OR
 // their shifted nibbles together (3 xor-shuffles) and the first of them stores
@@ -181,6 +197,7 @@ km_status launch_colmean(const float *X, int64_t n, int d, int64_t ldx, float *m
 }
 
 size_t quantize_bytes(int64_t n, int d, int fmt) {
+  if (fmt == KM_BF16) return 0;
   const int64_t nb = cdiv(n, kRowsPerBlock);
   if (fmt == KM_SQ8) return (size_t)nb * d * 2 * sizeof(float) + (size_t)d * sizeof(float) + 512;
   return colmean_bytes(n, d);
@@ -205,6 +222,13 @@ km_status launch_quantize(const float *X, int64_t n, int d, int64_t ldx, int fmt
     hipLaunchKernelGGL(sq8_encode_kernel, dim3(g), dim3(256), 0, s, X, n, d, ldx, lo, inv,
                        static_cast<uint8_t *>(codes));
     KMQ_LAUNCH_CHECK("quantize sq8");
+    return KM_OK;
+  }
+  if (fmt == KM_BF16) {
+    const int64_t work = n * (d / 8);
+    const unsigned g = (unsigned)std::min<int64_t>(cdiv(work, 256), 65536);
+    hipLaunchKernelGGL(bf16_encode_kernel, dim3(g), dim3(256), 0, s, X, n, d, ldx, static_cast<uint16_t *>(codes));
+    KMQ_LAUNCH_CHECK("quantize bf16");
     return KM_OK;
   }
   if (fmt == KM_SIGN1) {

@@ -297,6 +297,58 @@ __global__ __launch_bounds__(256) void segsum_f32_kernel(const float *X, int64_t
   }
 }
 
+// bfloat16 rows: one slice of 512 columns per workgroup; lane = 8 values (16 bytes),
+// decoded to fp32 and summed in fp32 within a chunk (as for fp32 rows)
+__global__ __launch_bounds__(256) void segsum_bf16_kernel(const uint16_t *X, int64_t ld, int d, const int *perm,
+                                                          const int *cnt, const int *cstart, const int *choff, int k,
+                                                          float *partial, int dp) {
+  __shared__ f32x4 red[4][2][64];
+  const int c = blockIdx.x;
+  if (c >= choff[k]) return;
+  const int j = find_cluster(choff, k, c);
+  const int ci = c - choff[j];
+  const int m0 = cstart[j] + ci * kChunk;
+  const int m1 = cstart[j] + min(cnt[j], (ci + 1) * kChunk);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int col = blockIdx.y * 512 + 8 * lane;
+  const bool ok = col < d;
+  f32x4 lo = {0.f, 0.f, 0.f, 0.f}, hi = {0.f, 0.f, 0.f, 0.f};
+  auto add = [&](uint4 w) {
+    lo += f32x4{bf16_value(w.x & 0xffffu), bf16_value(w.x >> 16), bf16_value(w.y & 0xffffu), bf16_value(w.y >> 16)};
+    hi += f32x4{bf16_value(w.z & 0xffffu), bf16_value(w.z >> 16), bf16_value(w.w & 0xffffu), bf16_value(w.w >> 16)};
+  };
+  int m = m0 + wave;
+  for (; m + 28 < m1; m += 32) {
+    int pp[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) pp[e] = perm[m + 4 * e];
+    if (ok) {
+      uint4 v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = *reinterpret_cast<const uint4 *>(X + (int64_t)pp[e] * ld + col);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) add(v[e]);
+    }
+  }
+  for (; m < m1; m += 4) {
+    const int p = perm[m];
+    if (ok) add(*reinterpret_cast<const uint4 *>(X + (int64_t)p * ld + col));
+  }
+  red[wave][0][lane] = lo;
+  red[wave][1][lane] = hi;
+  __syncthreads();
+  if (wave == 0 && ok) {
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      f32x4 t = red[0][hh][lane];
+      t += red[1][hh][lane];
+      t += red[2][hh][lane];
+      t += red[3][hh][lane];
+      *reinterpret_cast<f32x4 *>(partial + (int64_t)c * dp + col + 4 * hh) = t;
+    }
+  }
+}
+
 // 1-bit rows: one slice of 1024 tail dims per workgroup; lane = 16 dims (half a word)
 __global__ __launch_bounds__(256) void segsum_bits_kernel(const uint32_t *bits, int64_t wpr, int w0, int dt,
                                                           const float *alpha, const int *perm, const int *cnt,
@@ -571,6 +623,10 @@ km_status launch_update(const Points &P, const int32_t *assign, int k, void *C, 
       F = P.front;
       fld = P.d_front;
     }
+    if (P.fmt == KM_BF16)
+      hipLaunchKernelGGL(segsum_bf16_kernel, dim3(w.maxchunks, (unsigned)cdiv(d, 512)), dim3(256), 0, s,
+                         static_cast<const uint16_t *>(P.data), P.ld, d, w.perm, w.cnt, w.cstart, w.choff, k,
+                         static_cast<float *>(w.partial), w.dp);
     if (df > 0)
       hipLaunchKernelGGL(segsum_f32_kernel, dim3(w.maxchunks, (unsigned)cdiv(df, 256)), dim3(256), 0, s, F, fld, df,
                          w.perm, w.cnt, w.cstart, w.choff, k, static_cast<float *>(w.partial), w.dp);
@@ -598,7 +654,8 @@ km_status launch_update(const Points &P, const int32_t *assign, int k, void *C, 
   const dim3 g(k, (unsigned)cdiv(d, 256));
   const int d0 = P.fmt == KM_HYBRID ? P.d_front : 0;
   switch (P.fmt) {
-    case KM_F32: hipLaunchKernelGGL(compose_kernel<KM_F32>, g, dim3(256), 0, s, w.Z, k, d, d0, P.center, w.fresh, w.cnt, C, counts); break;
+    case KM_F32:
+    case KM_BF16: hipLaunchKernelGGL(compose_kernel<KM_F32>, g, dim3(256), 0, s, w.Z, k, d, d0, P.center, w.fresh, w.cnt, C, counts); break;
     case KM_SQ8: hipLaunchKernelGGL(compose_kernel<KM_SQ8>, g, dim3(256), 0, s, w.Z, k, d, d0, P.center, w.fresh, w.cnt, C, counts); break;
     case KM_SIGN1: hipLaunchKernelGGL(compose_kernel<KM_SIGN1>, g, dim3(256), 0, s, w.Z, k, d, d0, P.center, w.fresh, w.cnt, C, counts); break;
     case KM_HYBRID: hipLaunchKernelGGL(compose_kernel<KM_HYBRID>, g, dim3(256), 0, s, w.Z, k, d, d0, P.center, w.fresh, w.cnt, C, counts); break;

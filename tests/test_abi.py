@@ -73,6 +73,9 @@ FAKE = ct.c_void_p(0x10000)  # never dereferenced: validation fails first
     (dict(data=0x1004), -1, "aligned"),
     (dict(reserved=1), -1, "reserved"),
     (dict(fmt=2, d=40, ld=48), -1, "d % 16"),
+    (dict(fmt=1, d=12, ld=16), -1, "d % 8"),
+    (dict(fmt=1, d=64, ld=68), -1, "ld % 8"),
+    (dict(fmt=1, d=64, ld=64, d_front=32), -1, "d_front"),
     (dict(fmt=3, d=100, alpha=0x2000, center=0x3000), -1, "d % 32"),
     (dict(fmt=3, d=128, alpha=None, center=0x3000), -1, "alpha"),
     (dict(fmt=3, d=128, alpha=0x2000, center=None), -1, "center"),
@@ -125,6 +128,10 @@ def test_quantize_and_pca_argument_checks(kmq):
     assert L.quantize(ct.c_void_p(0x10002), 10, 64, 64, 2, FAKE, FAKE, None, 0, None, 1, None) == -1
     assert L.quantize(FAKE, 0, 64, 64, 2, FAKE, FAKE, None, 0, None, 1, None) == -1
     assert L.quantize(FAKE, 10, 64, 64, 3, FAKE, ct.c_void_p(0x10008), FAKE, 0, None, 1, None) == -1  # params
+    assert L.quantize(FAKE, 10, 12, 12, 1, FAKE, None, None, 0, None, 0, None) == -1  # bf16: d % 8
+    assert "d % 8" in L.km_last_error().decode()
+    assert L.quantize(FAKE, 10, 64, 64, 1, FAKE, None, None, 32, None, 0, None) == -1  # bf16: no front
+    assert L.quantize(FAKE, 10, 64, 64, 1, None, None, None, 0, None, 0, None) == -1  # bf16: codes NULL
     assert L.pca_fit_cov(FAKE, 10, 30, FAKE, FAKE, None) == -1
     assert L.pca_fit_cov(None, 10, 32, FAKE, FAKE, None) == -1
     assert L.pca_project(FAKE, 10, 32, FAKE, FAKE, 0, FAKE, None) == -1
