@@ -12,18 +12,28 @@ Inputs are resident in HBM before the timed region.  `value` is Lloyd
 iterations per second over the whole step (20 fp32 + 20 SQ8 iterations).
 
 Other workloads (--workload 1|3|4|5) time the other configurations for
-measurement; they are not the headline line.
+measurement; they are not the headline line.  --workload 6 runs the default
+workload's data stored as bfloat16.
 
 The JSON line carries the roofline of the dominant kernel (the fused fp32
 assignment kernel, on fp32 MFMA), measured from HIP events recorded by the
 library around each launch of that kernel on its stream, and the oracle timed on
-this host on a bounded sample of the same workload.
+this host on a bounded sample of the same workload.  `roofline.traffic` (bytes
+the kernel moves between L2 and memory per launch) comes from the committed
+rocprofv3 counter summary under profiles/; it is null when that summary is
+missing, covers another workload, or was taken from a different source of the
+kernel than the one built here.
+
+--copy-probe runs a 1 GiB fill and a 1 GiB negating copy before the workload:
+kernels of known traffic against which FETCH_SIZE / WRITE_SIZE are scaled.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -33,7 +43,10 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "Lloyd iters/s + point×centroid distances/s; objective ratio vs fp32 oracle"
-PEAK = {"fp32_mfma_tflops": 157.3, "int8_mfma_tops": 5000.0, "hbm_gbs": 8000.0}
+PEAK = {"fp32_mfma_tflops": 157.3, "bf16_mfma_tflops": 2500.0, "int8_mfma_tops": 5000.0, "hbm_gbs": 8000.0}
+COUNTERS = os.path.join(ROOT, "profiles", "counters__assign_kernel_fp32__gmm1m_d768_k1000.md")
+KERNEL_SOURCES = ("paper_2608_14648_amd/csrc/assign.hip", "paper_2608_14648_amd/csrc/common.hpp")
+COPY_PROBE_FLOATS = 256 << 20  # 1 GiB of fp32
 
 
 def log(msg):
@@ -68,6 +81,45 @@ def stage_summary(s):
             "update_ms_per_iter": s["update_ms"] / max(1, s["updates"]),
             "prep_ms_per_pass": s["prep_ms"] / max(1, s["assign_passes"]),
             "other_ms_total": s["other_ms"]}
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def counted_traffic(workload):
+    """Calibrated L2<->memory bytes per launch of the fp32 assignment kernel.
+
+    Read from the JSON block of the committed counter summary; None when the
+    summary is absent, was taken on another workload, or the kernel's sources
+    have changed since the counters were collected."""
+    try:
+        with open(COUNTERS) as f:
+            text = f.read()
+    except OSError:
+        return None
+    m = re.search(r"```json\n(.*?)\n```", text, re.S)
+    if m is None:
+        return None
+    rec = json.loads(m.group(1))
+    if rec.get("workload") != workload or rec.get("source_sha256") != kernel_source_hash():
+        return None
+    return rec.get("traffic_bytes_per_launch")
+
+
+def copy_probe(torch):
+    """Kernels of known traffic for counter calibration: a fill that writes
+    1 GiB, then a negating copy that reads 1 GiB and writes 1 GiB."""
+    src = torch.ones(COPY_PROBE_FLOATS, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    del src, dst
+    log(f"copy probe done ({COPY_PROBE_FLOATS * 4} bytes)")
 
 
 # ------------------------------------------------------------------------- workloads
@@ -118,7 +170,8 @@ def workload_c2(cfg, torch, km, args):
             "partition_cost": {"f32": c32, "sq8": c8},
             "roofline": {"bound": "mfma", "kernel": "assign_kernel<fp32>", "achieved": achieved,
                          "peak": PEAK["fp32_mfma_tflops"], "unit": "TFLOP/s",
-                         "frac": achieved / PEAK["fp32_mfma_tflops"], "traffic": None,
+                         "frac": achieved / PEAK["fp32_mfma_tflops"],
+                         "traffic": counted_traffic(cfg["name"]) if args.n is None else None,
                          "avg_launch_ms": a_ms, "flop_per_launch": flop},
             "roofline_sq8_assign": {"bound": "mfma", "achieved": 2.0 * spec.n * k * spec.d / (q_ms * 1e-3) / 1e12,
                                     "peak": PEAK["int8_mfma_tops"], "unit": "TOP/s",
@@ -160,6 +213,45 @@ def workload_c2(cfg, torch, km, args):
                           f"{spec.n} points, k={k}, d={spec.d}, timed {t32 + t8:.2f} s, extrapolated linearly to N"}
 
     return step, finish, cpu_baseline
+
+
+def workload_bf16(cfg, torch, km, args):
+    """The 1M x 768, k=1000 mixture stored as bfloat16 (measurement only)."""
+    spec = cfg["spec"] if args.n is None else cfg["spec"].with_n(args.n)
+    k, T = cfg["k"], cfg["iters"]
+    import synth
+    log(f"generating {spec.n} x {spec.d} mixture")
+    X = upload(spec, torch)
+    idx = synth.init_indices(spec.n, k)
+    P32 = km.points_f32(X)
+    mu = torch.empty((k, spec.d), dtype=torch.float32, device="cuda")
+
+    def step(timer):
+        Xb = km.quantize_bf16(X)
+        st = km.KmFitStats()
+        C, a, J = km.kmeans_fit(km.points_bf16(Xb), k, T, idx, stats=st)
+        km.kmeans_update(P32, a, mu, km.KM_EMPTY_KEEP, counts=False)
+        cost = km.kmeans_cost(X, mu, a)
+        if timer is not None:
+            timer.add("bf16", st)
+        return {"bf16": cost}, J
+
+    def finish(out, timer, elapsed, K):
+        s = timer.stats["bf16"]
+        a_ms = s["assign_ms"] / s["assign_passes"]
+        flop = 2.0 * spec.n * k * spec.d
+        ach = flop / (a_ms * 1e-3) / 1e12
+        return {"value": T * K / elapsed, "unit": "Lloyd iters/s", "dtype": "bf16",
+                "config": {"workload": "gmm1m_d768_k1000_bf16", "N": spec.n, "d": spec.d, "k": k, "iters": T,
+                           "formats": ["bf16"]},
+                "distances_per_s": (T + 1) * spec.n * k * K / elapsed,
+                "partition_cost": {"bf16": float(out["bf16"].item())},
+                "roofline": {"bound": "mfma", "kernel": "assign_i8_kernel<bf16>", "achieved": ach,
+                             "peak": PEAK["bf16_mfma_tflops"], "unit": "TFLOP/s",
+                             "frac": ach / PEAK["bf16_mfma_tflops"], "traffic": None, "avg_launch_ms": a_ms},
+                "stages": {"bf16": stage_summary(s)}}
+
+    return step, finish, None
 
 
 def workload_sign1(cfg, torch, km, args):
@@ -302,7 +394,9 @@ def workload_c1(cfg, torch, km, args):
     return step, finish, None
 
 
-WORKLOADS = {1: workload_c1, 2: workload_c2, 3: workload_sign1, 4: workload_pca, 5: workload_hybrid}
+WORKLOADS = {1: workload_c1, 2: workload_c2, 3: workload_sign1, 4: workload_pca, 5: workload_hybrid,
+             6: workload_bf16}
+CONFIG_OF = {6: 2}  # measurement-only workloads and the configuration whose data they use
 
 
 def main():
@@ -314,6 +408,7 @@ def main():
     ap.add_argument("--n", type=int, default=None, help="override the number of points (measurement only)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle's CPU-baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true", help="run the counter-calibration copy kernels first")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -328,7 +423,9 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
 
-    cfg = synth.config(args.workload)
+    if args.copy_probe:
+        copy_probe(torch)
+    cfg = synth.config(CONFIG_OF.get(args.workload, args.workload))
     step, finish, cpu_baseline = WORKLOADS[args.workload](cfg, torch, km, args)
     for i in range(args.warmup):
         step(None)
