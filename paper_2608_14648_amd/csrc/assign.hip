@@ -67,7 +67,28 @@ struct AssignArgs {
   int k;
   int32_t *assign;
   float *score;
+  // centroid-tile groups: workgroup (pt, g) scans centroid tiles g, g + ngroups, ...
+  // of point tile pt and merges its argmin into keys[] (used when ngroups > 1)
+  int ngroups;
+  int64_t n_ptiles;
+  unsigned long long *keys;
 };
+
+// (score, index) as one 64-bit key whose unsigned order is the lexicographic
+// order of (score, index): the fp32 pattern is mapped to an order-preserving
+// unsigned integer (negative values complemented, positive ones offset by the
+// sign bit), -0 taken as +0 so that equal scores tie on the index.
+__device__ __forceinline__ unsigned long long score_key(float sc, int idx) {
+  uint32_t u = __float_as_uint(sc == 0.0f ? 0.0f : sc);
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ((unsigned long long)u << 32) | (uint32_t)idx;
+}
+
+__device__ __forceinline__ float key_score(unsigned long long key) {
+  uint32_t u = (uint32_t)(key >> 32);
+  u = (u & 0x80000000u) ? (u & 0x7fffffffu) : ~u;
+  return __uint_as_float(u);
+}
 
 __device__ __forceinline__ uint32_t spread4(uint32_t b4) {
   // 4 bits -> 4 bytes holding 0 or 1 (bit j -> byte j)
@@ -201,7 +222,8 @@ __device__ __forceinline__ void load_stage(const AssignArgs &A, int s, int SI, i
       const int jt = t + kThreads * q;
       if (jt < G::TC) {
         const int64_t j = c0 + min(jt, crmax);
-        if (Cfg<FMT>::kFp) R.cpar[0] = A.cp.cn[j];
+        // rows past k get an infinite norm: their fp scores are +inf and never win
+        if (Cfg<FMT>::kFp) R.cpar[0] = jt <= crmax ? A.cp.cn[j] : INFINITY;
         if (Cfg<FMT>::kInt) R.cpar[1] = __int_as_float(A.cp.qsum[j]);
         if (Cfg<FMT>::kBits) {
           R.cpar[2] = A.cp.u[j];
@@ -329,20 +351,34 @@ __global__ __launch_bounds__(kThreads, Blocking<FMT>::MINB) void assign_kernel(A
   constexpr int CB = Blocking<FMT>::CB, PB = Blocking<FMT>::PB;
   typedef Geo<CB, PB> G;
   __shared__ __align__(16) uint8_t lds[2 * G::STAGE];
-  __shared__ float cparl[2][4 * G::TC];
+  __shared__ __align__(16) float cparl[2][4 * G::TC];
   typedef typename std::conditional<Cfg<FMT>::kIntScore, int, float>::type score_t;
 
   const int t = threadIdx.x;
   const int lane = t & 63, wave = t >> 6;
   const int r = lane & 31, h = lane >> 5;
   const int wc = wave & 1, wp = wave >> 1;
-  const int64_t p0 = (int64_t)blockIdx.x * G::TP;
+  // With ngroups > 1 the ngroups workgroups of one point tile are consecutive
+  // among the workgroups of one XCD (dispatch deals workgroup ids round-robin to
+  // the 8 XCDs), so the re-reads of the point tile, one per centroid tile, are
+  // served by that XCD's L2.
+  const int NG = A.ngroups;
+  int64_t pt = blockIdx.x;
+  int g = 0;
+  if (NG > 1) {
+    const int64_t l = blockIdx.x >> 3;
+    pt = (l / NG) * 8 + (blockIdx.x & 7);
+    g = (int)(l % NG);
+    if (pt >= A.n_ptiles) return;  // whole workgroup, before any barrier
+  }
+  const int64_t p0 = pt * G::TP;
 
   const int SF = Cfg<FMT>::kFp ? (A.df + 31) / 32 : 0;
   const int SI = Cfg<FMT>::kInt ? (A.di + kRowBytes - 1) / kRowBytes : 0;
   const int S = SF + SI;
   const int nct = (A.k + G::TC - 1) / G::TC;
-  const int total = nct * S;
+  const int nmy = (nct - g + NG - 1) / NG;  // centroid tiles of this workgroup (>= 1: NG <= nct)
+  const int total = nmy * S;
 
   float al[PB];
 #pragma unroll
@@ -357,29 +393,37 @@ __global__ __launch_bounds__(kThreads, Blocking<FMT>::MINB) void assign_kernel(A
     bidx[pb] = INT_MAX;
   }
 
+  // Pipeline: at the start of step `it` the registers hold stage it+1 (loaded
+  // during step it-1).  They are written to the free LDS buffer first (every wave
+  // has finished reading it: barrier of step it-1), then reloaded with stage it+2,
+  // then the MFMAs of stage `it` run from the other buffer.  Each global load thus
+  // has a whole step to arrive.  q counts this workgroup's centroid tiles
+  // (tile g + q * NG).
   StageRegs<CB, PB> R;
-  load_stage<FMT, CB, PB>(A, 0, SI, 0, p0, R);
+  load_stage<FMT, CB, PB>(A, 0, SI, (int64_t)g * G::TC, p0, R);
   store_stage<FMT, CB, PB>(A, 0, SI, R, lds, cparl[0]);
+  if (total > 1) load_stage<FMT, CB, PB>(A, S > 1 ? 1 : 0, SI, (int64_t)(g + (S > 1 ? 0 : NG)) * G::TC, p0, R);
   __syncthreads();
 
-  // one pipeline step: prefetch stage (it+1) into registers, run the MFMAs of
-  // stage `it` from LDS, write stage (it+1) to the other buffer, barrier
-  auto step = [&](int ct, int s, auto fp_tag, auto &acc_f, auto &acc_i) {
+  auto step = [&](int q, int s, auto fp_tag, auto &acc_f, auto &acc_i) {
     constexpr bool FPS = decltype(fp_tag)::value;
-    const int it = ct * S + s;
-    const bool has_next = it + 1 < total;
+    const int it = q * S + s;
     const int s_n = (s + 1 == S) ? 0 : s + 1;
-    const int ct_n = (s + 1 == S) ? ct + 1 : ct;
-    if (has_next) load_stage<FMT, CB, PB>(A, s_n, SI, (int64_t)ct_n * G::TC, p0, R);
+    const int q_n = (s + 1 == S) ? q + 1 : q;
+    const int s_nn = (s_n + 1 == S) ? 0 : s_n + 1;
+    const int q_nn = (s_n + 1 == S) ? q_n + 1 : q_n;
+    if (it + 1 < total) store_stage<FMT, CB, PB>(A, s_n, SI, R, lds + ((it + 1) & 1) * G::STAGE, cparl[q_n & 1]);
+    if (it + 2 < total) load_stage<FMT, CB, PB>(A, s_nn, SI, (int64_t)(g + q_nn * NG) * G::TC, p0, R);
     const uint8_t *buf = lds + (it & 1) * G::STAGE;
+    __builtin_amdgcn_s_setprio(1);  // favour the wave that is feeding the matrix core
     mfma_stage<CB, PB, FPS>(buf, buf + G::CBYTES, wc, wp, r, h, acc_f, acc_i);
-    if (has_next) store_stage<FMT, CB, PB>(A, s_n, SI, R, lds + ((it + 1) & 1) * G::STAGE, cparl[ct_n & 1]);
+    __builtin_amdgcn_s_setprio(0);
     __syncthreads();
   };
 
-  for (int ct = 0; ct < nct; ++ct) {
-    const int64_t c0 = (int64_t)ct * G::TC;
-    const float *cp = cparl[ct & 1];
+  for (int q = 0; q < nmy; ++q) {
+    const int64_t c0 = (int64_t)(g + q * NG) * G::TC;
+    const float *cp = cparl[q & 1];
     f32x16 facc[CB][PB];
     i32x16 iacc[CB][PB];
     if constexpr (Cfg<FMT>::kInt) {
@@ -389,7 +433,7 @@ __global__ __launch_bounds__(kThreads, Blocking<FMT>::MINB) void assign_kernel(A
         for (int b = 0; b < PB; ++b)
 #pragma unroll
           for (int i = 0; i < 16; ++i) iacc[a][b][i] = 0;
-      for (int s = 0; s < SI; ++s) step(ct, s, std::false_type{}, facc, iacc);
+      for (int s = 0; s < SI; ++s) step(q, s, std::false_type{}, facc, iacc);
     }
     if constexpr (FMT == KM_HYBRID) {
       // the tail's exact 1-bit score ts becomes the starting value -ts/2 of the
@@ -418,10 +462,38 @@ __global__ __launch_bounds__(kThreads, Blocking<FMT>::MINB) void assign_kernel(A
           for (int i = 0; i < 16; ++i) facc[a][b][i] = 0.f;
     }
     if constexpr (Cfg<FMT>::kFp) {
-      for (int s = SI; s < S; ++s) step(ct, s, std::true_type{}, facc, iacc);
+      for (int s = SI; s < S; ++s) step(q, s, std::true_type{}, facc, iacc);
     }
 
-    // epilogue for centroid tile ct: scores and running argmin, lane-local
+    // epilogue for this centroid tile: scores and running argmin, lane-local.
+    // fp formats: branch-free selects; lane rows ascend with (cb, i), so the strict
+    // comparison keeps the smallest index among equal scores.
+    if constexpr (FMT == KM_F32 || FMT == KM_HYBRID) {
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb) {
+        const int crow0 = wc * 32 * CB + cb * 32 + 4 * h;
+#pragma unroll
+        for (int i4 = 0; i4 < 4; ++i4) {
+          const f32x4 cn4 = *reinterpret_cast<const f32x4 *>(&cp[crow0 + 8 * i4]);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int i = 4 * i4 + e;
+            const int j = (int)c0 + crow0 + 8 * i4 + e;
+#pragma unroll
+            for (int pb = 0; pb < PB; ++pb) {
+              const float sc = fmaf(-2.0f, facc[cb][pb][i], cn4[e]);  // tail score folded in for HYBRID
+              const bool take = sc < best[pb];
+              best[pb] = take ? sc : best[pb];
+              bidx[pb] = take ? j : bidx[pb];
+            }
+          }
+        }
+      }
+      // With one stage per tile, the next step already writes the constants of tile
+      // q + 2 into cparl[q & 1]: every wave must be done reading them first.
+      if (S == 1) __syncthreads();
+      continue;
+    }
 #pragma unroll
     for (int cb = 0; cb < CB; ++cb) {
 #pragma unroll
@@ -488,11 +560,29 @@ __global__ __launch_bounds__(kThreads, Blocking<FMT>::MINB) void assign_kernel(A
       }
       const int64_t p = p0 + pc;
       if (p < A.n) {
-        A.assign[p] = bidx[pb];
-        if (A.score) A.score[p] = (float)best[pb];
+        if (A.keys) {
+          if constexpr (!Cfg<FMT>::kIntScore) atomicMin(A.keys + p, score_key(best[pb], bidx[pb]));
+        } else {
+          A.assign[p] = bidx[pb];
+          if (A.score) A.score[p] = (float)best[pb];
+        }
       }
     }
   }
+}
+
+__global__ __launch_bounds__(256) void keys_init_kernel(unsigned long long *keys, int64_t n) {
+  const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (p < n) keys[p] = ~0ull;
+}
+
+__global__ __launch_bounds__(256) void keys_unpack_kernel(const unsigned long long *keys, int64_t n, int32_t *assign,
+                                                          float *score) {
+  const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (p >= n) return;
+  const unsigned long long key = keys[p];
+  assign[p] = (int32_t)(uint32_t)key;
+  if (score) score[p] = key_score(key);
 }
 
 // ---- int8 assignment with 256 x 256 workgroup tiles ---------------------------
@@ -726,6 +816,9 @@ __global__ __launch_bounds__(kThreads, 1) void assign_i8_kernel(AssignArgs A) {
       for (int b = 0; b < 4; ++b)
 #pragma unroll
         for (int i = 0; i < 16; ++i) acc[a][b][i] = 0;
+    // one stage per tile: the next stage writes tile ct + 2's constants into
+    // cparl[ct & 1], which every wave must have finished reading
+    if (S == 1) __syncthreads();
   }
 
 #pragma unroll
@@ -911,6 +1004,9 @@ __global__ __launch_bounds__(kBT, 1) void assign_bits_kernel(AssignArgs A) {
           }
         }
       }
+    // one stage per tile: the next stage writes tile ct + 2's constants into
+    // cparl[ct & 1], which every wave must have finished reading
+    if (S == 1) __syncthreads();
   }
 #pragma unroll
   for (int pb = 0; pb < 2; ++pb) {
@@ -1168,10 +1264,19 @@ __global__ __launch_bounds__(256) void cost_kernel(const float *X, int64_t n, in
 
 constexpr int kObjBlocks = 1024;
 
+// Centroid-tile groups of the fp32 kernel: up to 8 workgroups share a point tile,
+// each scanning every 8th centroid tile.
+int assign_groups(const Points &P, int k) {
+  if (P.fmt != KM_F32 && P.fmt != KM_HYBRID) return 1;
+  constexpr int TC = Geo<Blocking<KM_F32>::CB, Blocking<KM_F32>::PB>::TC;
+  return (int)std::min<int64_t>(8, cdiv(k, TC));
+}
+
 template <int FMT>
 km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp, int k, int32_t *assign,
                           float *score, hipStream_t s) {
   AssignArgs A{};
+  A.ngroups = 1;
   A.n = P.n;
   A.k = k;
   A.assign = assign;
@@ -1222,7 +1327,19 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
     hipLaunchKernelGGL(assign_i8_kernel<FMT>, dim3((unsigned)cdiv(P.n, kT8)), dim3(kThreads), 0, s, A);
   } else {
     constexpr int TP = Geo<Blocking<FMT>::CB, Blocking<FMT>::PB>::TP;
-    hipLaunchKernelGGL(assign_kernel<FMT>, dim3((unsigned)cdiv(P.n, TP)), dim3(kThreads), 0, s, A);
+    const int64_t npt = cdiv(P.n, TP);
+    const int ng = assign_groups(P, k);
+    const dim3 gp((unsigned)cdiv(P.n, 256));
+    A.n_ptiles = npt;
+    if (ng > 1) {
+      A.ngroups = ng;
+      A.keys = cp.keys;
+      hipLaunchKernelGGL(keys_init_kernel, gp, dim3(256), 0, s, cp.keys, P.n);
+      hipLaunchKernelGGL(assign_kernel<FMT>, dim3((unsigned)(cdiv(npt, 8) * 8 * ng)), dim3(kThreads), 0, s, A);
+      hipLaunchKernelGGL(keys_unpack_kernel, gp, dim3(256), 0, s, cp.keys, P.n, assign, score);
+    } else {
+      hipLaunchKernelGGL(assign_kernel<FMT>, dim3((unsigned)npt), dim3(kThreads), 0, s, A);
+    }
   }
   KMQ_LAUNCH_CHECK("assign_kernel");
   return KM_OK;
@@ -1230,11 +1347,19 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
 
 }  // namespace
 
-size_t prep_bytes(const Points &P, int k) {
+// prep workspace: cn, qsum, u, sig2 (k each) | residual codes or bf16 rows | keys (n)
+static size_t prep_codes_bytes(const Points &P, int k) {
   const int d0 = P.fmt == KM_HYBRID ? P.d_front : 0;
-  size_t b = 4 * (size_t)k * sizeof(float) + 256;
-  if (P.fmt == KM_SIGN1 || P.fmt == KM_HYBRID) b += (size_t)k * (size_t)(P.d - d0) + 256;
-  if (P.fmt == KM_BF16) b += 2 * (size_t)k * (size_t)P.d + 256;
+  if (P.fmt == KM_SIGN1 || P.fmt == KM_HYBRID) return (size_t)k * (size_t)(P.d - d0);
+  if (P.fmt == KM_BF16) return 2 * (size_t)k * (size_t)P.d;
+  return 0;
+}
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+size_t prep_bytes(const Points &P, int k) {
+  size_t b = align256(16 * (size_t)k) + align256(prep_codes_bytes(P, k));
+  if (assign_groups(P, k) > 1) b += align256(8 * (size_t)P.n);
   return b;
 }
 
@@ -1244,8 +1369,11 @@ km_status launch_prep(const Points &P, const void *C, int k, void *ws, CentroidP
   int *qsum = reinterpret_cast<int *>(w + (size_t)k * 4);
   float *u = reinterpret_cast<float *>(w + (size_t)k * 8);
   float *sig2 = reinterpret_cast<float *>(w + (size_t)k * 12);
-  int8_t *q = reinterpret_cast<int8_t *>(w + (((size_t)k * 16 + 255) & ~(size_t)255));
+  int8_t *q = reinterpret_cast<int8_t *>(w + align256(16 * (size_t)k));
   uint16_t *cb = reinterpret_cast<uint16_t *>(q);  // BF16 uses the same region for its rows
+  out->keys = assign_groups(P, k) > 1 ? reinterpret_cast<unsigned long long *>(
+                                            w + align256(16 * (size_t)k) + align256(prep_codes_bytes(P, k)))
+                                      : nullptr;
   out->cn = cn;
   out->qsum = qsum;
   out->u = u;

@@ -38,6 +38,7 @@ struct CentroidPrep {
   const float *sig2;   // SIGN1/HYBRID: 2*sigma
   const int8_t *q;     // SIGN1/HYBRID: int8 residual codes, k x dt
   const uint16_t *cb;  // BF16: centroids rounded to bfloat16, k x d
+  unsigned long long *keys;  // F32/HYBRID with centroid-tile groups: per-point (score, index) keys
 };
 
 // Host-side error plumbing.

@@ -72,7 +72,7 @@ def test_quantize_bf16_bit_exact(km, torch, n, d):
 
 
 ASSIGN_SHAPES = [(1, 8, 1), (5, 16, 3), (300, 32, 3), (1000, 128, 64), (2049, 96, 130), (517, 768, 257),
-                 (700, 136, 129), (130, 64, 300), (600, 1000, 70), (64, 8, 5)]
+                 (700, 136, 129), (130, 64, 300), (600, 1000, 70), (64, 8, 5), (600, 64, 900)]
 
 
 @pytest.mark.parametrize("n,d,k", ASSIGN_SHAPES)

@@ -47,7 +47,9 @@ ASSIGN_SHAPES = [(1, 32, 1), (5, 32, 3), (300, 32, 3), (1000, 128, 64), (2049, 9
 
 # --------------------------------------------------------------------------- assign
 
-@pytest.mark.parametrize("n,d,k", ASSIGN_SHAPES + [(700, 36, 129), (64, 4, 5)])
+# (600, 32, 2500) and (500, 4, 2100): one stage per centroid tile, three tiles per workgroup
+@pytest.mark.parametrize("n,d,k", ASSIGN_SHAPES + [(700, 36, 129), (64, 4, 5), (3000, 64, 1024), (1500, 32, 1100),
+                                                   (200, 96, 2000), (600, 32, 2500), (500, 4, 2100)])
 def test_assign_f32(km, torch, n, d, k):
     say(f"assign f32 n={n} d={d} k={k}")
     X = blobs(n, d, max(2, k // 2), seed=n + d + k)
@@ -82,7 +84,7 @@ def test_assign_f32_strided_rows(km, torch):
 
 
 @pytest.mark.parametrize("n,d,k", [(1, 16, 1), (5, 16, 3), (300, 32, 3), (1000, 128, 64), (2049, 96, 130),
-                                   (517, 768, 257), (130, 48, 300)])
+                                   (517, 768, 257), (130, 48, 300), (700, 16, 900)])
 def test_assign_sq8_bit_exact(km, torch, n, d, k):
     say(f"assign sq8 n={n} d={d} k={k}")
     rng = np.random.default_rng(n * 7 + d + k)
@@ -114,7 +116,7 @@ def sign1_inputs(n, d, k, seed, d0=0):
 
 
 @pytest.mark.parametrize("n,d,k", [(1, 32, 1), (5, 64, 3), (300, 96, 3), (1000, 128, 64), (2049, 256, 130),
-                                   (517, 1024, 257), (700, 160, 129), (130, 64, 300)])
+                                   (517, 1024, 257), (700, 160, 129), (130, 64, 300), (700, 64, 600)])
 def test_assign_sign1_bit_exact(km, torch, n, d, k):
     say(f"assign sign1 n={n} d={d} k={k}")
     X, m, bits, alpha, C = sign1_inputs(n, d, k, seed=n + d + k)
@@ -130,7 +132,7 @@ def test_assign_sign1_bit_exact(km, torch, n, d, k):
 
 
 @pytest.mark.parametrize("n,d,d0,k", [(300, 64, 32, 3), (1000, 128, 32, 64), (2049, 256, 96, 130),
-                                      (517, 1024, 384, 257), (50, 96, 64, 7)])
+                                      (517, 1024, 384, 257), (50, 96, 64, 7), (600, 128, 32, 1100)])
 def test_assign_hybrid(km, torch, n, d, d0, k):
     say(f"assign hybrid n={n} d={d} d0={d0} k={k}")
     X, m, bits, alpha, C = sign1_inputs(n, d, k, seed=n + d + k + d0, d0=d0)
