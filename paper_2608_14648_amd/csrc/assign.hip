@@ -711,14 +711,15 @@ __device__ __forceinline__ void mfma_stage8(const uint8_t *cbuf, const uint8_t *
     for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
       for (int pb = 0; pb < 4; ++pb) {
+        const Acc8<BF> cin = acc[cb][pb];
         if constexpr (BF) {
           const bf16x8 a8 = __builtin_bit_cast(bf16x8, av[cur][cb]);
           const bf16x8 b8 = __builtin_bit_cast(bf16x8, bv[cur][pb]);
-          acc[cb][pb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a8, b8, acc[cb][pb], 0, 0, 0);
+          acc[cb][pb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a8, b8, cin, 0, 0, 0);
         } else {
           const i32x4 a4 = {(int)av[cur][cb].x, (int)av[cur][cb].y, (int)av[cur][cb].z, (int)av[cur][cb].w};
           const i32x4 b4 = {(int)bv[cur][pb].x, (int)bv[cur][pb].y, (int)bv[cur][pb].z, (int)bv[cur][pb].w};
-          acc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a4, b4, acc[cb][pb], 0, 0, 0);
+          acc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a4, b4, cin, 0, 0, 0);
         }
       }
   }
@@ -727,7 +728,7 @@ __device__ __forceinline__ void mfma_stage8(const uint8_t *cbuf, const uint8_t *
 template <int FMT>
 __global__ __launch_bounds__(kThreads, 1) void assign_i8_kernel(AssignArgs A) {
   __shared__ __align__(16) uint8_t lds[2 * kStageBytes8];
-  __shared__ float cparl[2][4 * kT8];
+  __shared__ __align__(16) float cparl[2][4 * kT8];
   typedef typename std::conditional<FMT == KM_SQ8, int, float>::type score_t;
 
   const int t = threadIdx.x;
@@ -779,46 +780,57 @@ __global__ __launch_bounds__(kThreads, 1) void assign_i8_kernel(AssignArgs A) {
       if (has_next) store_stage8<FMT>(A, s_n, R, lds + ((it + 1) & 1) * kStageBytes8, cparl[ct_n & 1]);
       __syncthreads();
     }
-    const int64_t c0 = (int64_t)ct * kT8;
+    // epilogue: one 32-row block at a time (a scheduling barrier keeps the
+    // compiler from pulling all 256 accumulators into VGPRs at once); per-row
+    // constants read 4 at a time; branch-free selects.  Rows ascend with (cb, i)
+    // in a lane, so the strict comparison keeps the smallest index among ties.
+    const int c0 = ct * kT8;
     const float *cp = cparl[ct & 1];
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb) {
+      const int crow0 = wc * 128 + cb * 32 + 4 * h;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int crow = wc * 128 + cb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
-        const int64_t j = c0 + crow;
-        const bool live = j < A.k;
-        const int qs = __float_as_int(cp[kT8 + crow]);
-        const float u = cp[2 * kT8 + crow];
-        const float s2 = cp[3 * kT8 + crow];
+      for (int i4 = 0; i4 < 4; ++i4) {
+        const int cr = crow0 + 8 * i4;
+        const f32x4 q4 = *reinterpret_cast<const f32x4 *>(&cp[kT8 + cr]);
+        f32x4 u4 = {0.f, 0.f, 0.f, 0.f}, s4 = {0.f, 0.f, 0.f, 0.f};
+        if constexpr (FMT == KM_SIGN1) {
+          u4 = *reinterpret_cast<const f32x4 *>(&cp[2 * kT8 + cr]);
+          s4 = *reinterpret_cast<const f32x4 *>(&cp[3 * kT8 + cr]);
+        }
 #pragma unroll
-        for (int pb = 0; pb < 4; ++pb) {
-          score_t sc;
-          if constexpr (FMT == KM_SQ8) {
-            sc = qs - 2 * acc[cb][pb][i];
-          } else if constexpr (FMT == KM_BF16) {
-            sc = fmaf(-2.0f, acc[cb][pb][i], __int_as_float(qs));  // ||c||^2 - 2<x,c>
-          } else {
-            const int sd = 2 * acc[cb][pb][i] - qs;
-            const float v = al[pb] * s2;
-            sc = fmaf(-v, (float)sd, u);
-          }
-          if (live && sc < best[pb]) {
-            best[pb] = sc;
-            bidx[pb] = (int)j;
+        for (int e = 0; e < 4; ++e) {
+          const int i = 4 * i4 + e;
+          const int j = c0 + cr + e;
+          const bool live = j < A.k;
+#pragma unroll
+          for (int pb = 0; pb < 4; ++pb) {
+            score_t sc;
+            if constexpr (FMT == KM_SQ8) {
+              sc = __float_as_int(q4[e]) - 2 * acc[cb][pb][i];
+            } else if constexpr (FMT == KM_BF16) {
+              sc = fmaf(-2.0f, acc[cb][pb][i], q4[e]);  // ||c||^2 - 2<x,c>
+            } else {
+              const int sd = 2 * acc[cb][pb][i] - __float_as_int(q4[e]);
+              const float v = al[pb] * s4[e];
+              sc = fmaf(-v, (float)sd, u4[e]);
+            }
+            const bool take = live && sc < best[pb];
+            best[pb] = take ? sc : best[pb];
+            bidx[pb] = take ? j : bidx[pb];
           }
         }
       }
+#pragma unroll
+      for (int pb = 0; pb < 4; ++pb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[cb][pb][i] = 0;
+      __builtin_amdgcn_sched_barrier(0);
     }
-#pragma unroll
-    for (int a = 0; a < 4; ++a)
-#pragma unroll
-      for (int b = 0; b < 4; ++b)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) acc[a][b][i] = 0;
-    // one stage per tile: the next stage writes tile ct + 2's constants into
-    // cparl[ct & 1], which every wave must have finished reading
-    if (S == 1) __syncthreads();
+    // the next tile's steps write tile ct + 2's constants into cparl[ct & 1]; with
+    // one stage per tile no other barrier would order that after these reads.
+    // (Unconditional: a branch here splits the loop and costs register spills.)
+    __syncthreads();
   }
 
 #pragma unroll
@@ -1004,9 +1016,10 @@ __global__ __launch_bounds__(kBT, 1) void assign_bits_kernel(AssignArgs A) {
           }
         }
       }
-    // one stage per tile: the next stage writes tile ct + 2's constants into
-    // cparl[ct & 1], which every wave must have finished reading
-    if (S == 1) __syncthreads();
+    // the next tile's steps write tile ct + 2's constants into cparl[ct & 1]; with
+    // one stage per tile no other barrier would order that after these reads.
+    // (Unconditional: a branch here splits the loop and costs register spills.)
+    __syncthreads();
   }
 #pragma unroll
   for (int pb = 0; pb < 2; ++pb) {
