@@ -585,19 +585,23 @@ __global__ __launch_bounds__(256) void keys_unpack_kernel(const unsigned long lo
   if (score) score[p] = key_score(key);
 }
 
-// ---- int8 assignment with 256 x 256 workgroup tiles ---------------------------
-// SQ8 and 1-bit points.  An int8 MFMA (32x32x32) is 32x denser than the fp32 one,
-// so operand bandwidth, not the matrix core, limits the 128-tile kernel.  Here each
-// wave owns 128 centroids x 128 points (4 x 4 blocks, 256 int32 accumulators) and
-// the workgroup 256 x 256: per MFMA a wave reads half the LDS bytes and the
-// workgroup a quarter of the L2 bytes of the 2 x 2 layout.
+// ---- int8 / bf16 assignment with 256 x 256 workgroup tiles -------------------
+// SQ8, bf16 and (wide) 1-bit points.  An int8 or bf16 MFMA is 16-32x denser than
+// the fp32 one, so operand bandwidth decides the tiling: the workgroup owns 256
+// centroids x 256 points per stage (a quarter of the L2 bytes per MFMA of a 128
+// tile) and each of its 8 waves 128 centroids x 64 points (4 x 2 blocks of
+// 32 x 32, 0.75 LDS reads of 1 KB per MFMA).  128 accumulators per wave leave
+// room for two waves per SIMD, so one wave's stage boundary (LDS writes, barrier)
+// overlaps the other's matrix work.
 constexpr int kT8 = 256;
+constexpr int k8Threads = 512;                 // 8 waves: 2 centroid halves x 4 point quarters
+constexpr int k8PB = 2;                        // 32-point blocks per wave
 constexpr int kTileBytes8 = kT8 * kLdsStride;  // 36864
 constexpr int kStageBytes8 = 2 * kTileBytes8;  // 73728
 
 struct Stage8 {
-  uint4 c[8];
-  uint4 p[8];
+  uint4 c[4];
+  uint4 p[4];
   float cpar[4];
 };
 
@@ -612,8 +616,8 @@ __device__ __forceinline__ void load_stage8(const AssignArgs &A, int s, int64_t 
   const uint32_t *pbaseb = A.pbits + p0 * A.pbw + A.pbw0;
   const int prmax = (int)min<int64_t>(A.n - 1 - p0, kT8 - 1);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int cidx = t + kThreads * i;
+  for (int i = 0; i < 4; ++i) {  // 256 rows x 8 chunks of 16 bytes over 512 threads
+    const int cidx = t + k8Threads * i;
     const int row = cidx >> 3, col = cidx & 7;
     const int b = b0 + 16 * col;
     const int bc = b < A.di ? b : 0;
@@ -623,15 +627,15 @@ __device__ __forceinline__ void load_stage8(const AssignArgs &A, int s, int64_t 
   }
   if (FMT == KM_SIGN1) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int w = t + kThreads * i;
+    for (int i = 0; i < 2; ++i) {  // 256 rows x 4 words
+      const int w = t + k8Threads * i;
       const int row = w >> 2, wi = w & 3;
       const int word = 4 * s + wi;
       R.p[i].x = pbaseb[(uint32_t)(min(row, prmax) * (int)A.pbw + (32 * word < A.di ? word : 0))];
     }
   }
-  if (s == 0) {
-    const int64_t j = min<int64_t>(c0 + t, A.k - 1);
+  if (s == 0) {  // per-centroid constants: threads t < kT8 (the others load a valid duplicate)
+    const int64_t j = min<int64_t>(c0 + (t & (kT8 - 1)), A.k - 1);
     R.cpar[1] = FMT == KM_BF16 ? A.cp.cn[j] : __int_as_float(A.cp.qsum[j]);
     if (FMT == KM_SIGN1) {
       R.cpar[2] = A.cp.u[j];
@@ -646,8 +650,8 @@ __device__ __forceinline__ void store_stage8(const AssignArgs &A, int s, const S
   uint8_t *ct = buf;
   uint8_t *pt = buf + kTileBytes8;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int cidx = t + kThreads * i;
+  for (int i = 0; i < 4; ++i) {
+    const int cidx = t + k8Threads * i;
     const int row = cidx >> 3, col = cidx & 7;
     const bool ok = kRowBytes * s + 16 * col < A.di;
     uint4 cv = R.c[i];
@@ -659,8 +663,8 @@ __device__ __forceinline__ void store_stage8(const AssignArgs &A, int s, const S
   }
   if (FMT == KM_SIGN1) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int w = t + kThreads * i;
+    for (int i = 0; i < 2; ++i) {
+      const int w = t + k8Threads * i;
       const int row = w >> 2, wi = w & 3;
       const uint32_t bits = (32 * (4 * s + wi) < A.di) ? R.p[i].x : 0u;
       *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 32 * wi) =
@@ -671,7 +675,7 @@ __device__ __forceinline__ void store_stage8(const AssignArgs &A, int s, const S
                      spread4(bits >> 28));
     }
   }
-  if (s == 0) {
+  if (s == 0 && t < kT8) {
 #pragma unroll
     for (int q = 1; q < 4; ++q) cpar[q * kT8 + t] = R.cpar[q];
   }
@@ -686,14 +690,14 @@ using Acc8 = typename std::conditional<BF, f32x16, i32x16>::type;
 
 template <bool BF>
 __device__ __forceinline__ void mfma_stage8(const uint8_t *cbuf, const uint8_t *pbuf, int wc, int wp, int r, int h,
-                                            Acc8<BF> (&acc)[4][4]) {
-  uint4 av[2][4], bv[2][4];
+                                            Acc8<BF> (&acc)[4][k8PB]) {
+  uint4 av[2][4], bv[2][k8PB];
 #pragma unroll
   for (int cb = 0; cb < 4; ++cb)
     av[0][cb] = *reinterpret_cast<const uint4 *>(cbuf + (wc * 128 + cb * 32 + r) * kLdsStride + 16 * h);
 #pragma unroll
-  for (int pb = 0; pb < 4; ++pb)
-    bv[0][pb] = *reinterpret_cast<const uint4 *>(pbuf + (wp * 128 + pb * 32 + r) * kLdsStride + 16 * h);
+  for (int pb = 0; pb < k8PB; ++pb)
+    bv[0][pb] = *reinterpret_cast<const uint4 *>(pbuf + (wp * 32 * k8PB + pb * 32 + r) * kLdsStride + 16 * h);
 #pragma unroll
   for (int g = 0; g < 4; ++g) {
     const int cur = g & 1, nxt = cur ^ 1;
@@ -703,14 +707,14 @@ __device__ __forceinline__ void mfma_stage8(const uint8_t *cbuf, const uint8_t *
         av[nxt][cb] = *reinterpret_cast<const uint4 *>(cbuf + (wc * 128 + cb * 32 + r) * kLdsStride + 32 * (g + 1) +
                                                        16 * h);
 #pragma unroll
-      for (int pb = 0; pb < 4; ++pb)
-        bv[nxt][pb] = *reinterpret_cast<const uint4 *>(pbuf + (wp * 128 + pb * 32 + r) * kLdsStride + 32 * (g + 1) +
-                                                       16 * h);
+      for (int pb = 0; pb < k8PB; ++pb)
+        bv[nxt][pb] = *reinterpret_cast<const uint4 *>(pbuf + (wp * 32 * k8PB + pb * 32 + r) * kLdsStride +
+                                                       32 * (g + 1) + 16 * h);
     }
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
-      for (int pb = 0; pb < 4; ++pb) {
+      for (int pb = 0; pb < k8PB; ++pb) {
         const Acc8<BF> cin = acc[cb][pb];
         if constexpr (BF) {
           const bf16x8 a8 = __builtin_bit_cast(bf16x8, av[cur][cb]);
@@ -726,7 +730,7 @@ __device__ __forceinline__ void mfma_stage8(const uint8_t *cbuf, const uint8_t *
 }
 
 template <int FMT>
-__global__ __launch_bounds__(kThreads, 1) void assign_i8_kernel(AssignArgs A) {
+__global__ __launch_bounds__(k8Threads, 1) void assign_i8_kernel(AssignArgs A) {
   __shared__ __align__(16) uint8_t lds[2 * kStageBytes8];
   __shared__ __align__(16) float cparl[2][4 * kT8];
   typedef typename std::conditional<FMT == KM_SQ8, int, float>::type score_t;
@@ -741,24 +745,24 @@ __global__ __launch_bounds__(kThreads, 1) void assign_i8_kernel(AssignArgs A) {
   const int nct = (A.k + kT8 - 1) / kT8;
   const int total = nct * S;
 
-  float al[4] = {0.f, 0.f, 0.f, 0.f};
+  float al[k8PB] = {};
   if (FMT == KM_SIGN1) {
 #pragma unroll
-    for (int pb = 0; pb < 4; ++pb) al[pb] = A.alpha[min<int64_t>(p0 + wp * 128 + pb * 32 + r, A.n - 1)];
+    for (int pb = 0; pb < k8PB; ++pb) al[pb] = A.alpha[min<int64_t>(p0 + wp * 32 * k8PB + pb * 32 + r, A.n - 1)];
   }
   constexpr bool BF = FMT == KM_BF16;
-  Acc8<BF> acc[4][4];
+  Acc8<BF> acc[4][k8PB];
 #pragma unroll
   for (int a = 0; a < 4; ++a)
 #pragma unroll
-    for (int b = 0; b < 4; ++b)
+    for (int b = 0; b < k8PB; ++b)
 #pragma unroll
       for (int i = 0; i < 16; ++i) acc[a][b][i] = 0;
 
-  score_t best[4];
-  int bidx[4];
+  score_t best[k8PB];
+  int bidx[k8PB];
 #pragma unroll
-  for (int pb = 0; pb < 4; ++pb) {
+  for (int pb = 0; pb < k8PB; ++pb) {
     best[pb] = FMT == KM_SQ8 ? (score_t)INT_MAX : (score_t)INFINITY;
     bidx[pb] = INT_MAX;
   }
@@ -804,7 +808,7 @@ __global__ __launch_bounds__(kThreads, 1) void assign_i8_kernel(AssignArgs A) {
           const int j = c0 + cr + e;
           const bool live = j < A.k;
 #pragma unroll
-          for (int pb = 0; pb < 4; ++pb) {
+          for (int pb = 0; pb < k8PB; ++pb) {
             score_t sc;
             if constexpr (FMT == KM_SQ8) {
               sc = __float_as_int(q4[e]) - 2 * acc[cb][pb][i];
@@ -822,7 +826,7 @@ __global__ __launch_bounds__(kThreads, 1) void assign_i8_kernel(AssignArgs A) {
         }
       }
 #pragma unroll
-      for (int pb = 0; pb < 4; ++pb)
+      for (int pb = 0; pb < k8PB; ++pb)
 #pragma unroll
         for (int i = 0; i < 16; ++i) acc[cb][pb][i] = 0;
       __builtin_amdgcn_sched_barrier(0);
@@ -834,7 +838,7 @@ __global__ __launch_bounds__(kThreads, 1) void assign_i8_kernel(AssignArgs A) {
   }
 
 #pragma unroll
-  for (int pb = 0; pb < 4; ++pb) {
+  for (int pb = 0; pb < k8PB; ++pb) {
     score_t os = __shfl_xor(best[pb], 32);
     int oi = __shfl_xor(bidx[pb], 32);
     if (os < best[pb] || (os == best[pb] && oi < bidx[pb])) {
@@ -846,16 +850,16 @@ __global__ __launch_bounds__(kThreads, 1) void assign_i8_kernel(AssignArgs A) {
   int *mi = reinterpret_cast<int *>(lds + kT8 * sizeof(score_t));
   if (wc == 1 && h == 0) {
 #pragma unroll
-    for (int pb = 0; pb < 4; ++pb) {
-      ms[wp * 128 + pb * 32 + r] = best[pb];
-      mi[wp * 128 + pb * 32 + r] = bidx[pb];
+    for (int pb = 0; pb < k8PB; ++pb) {
+      ms[wp * 32 * k8PB + pb * 32 + r] = best[pb];
+      mi[wp * 32 * k8PB + pb * 32 + r] = bidx[pb];
     }
   }
   __syncthreads();
   if (wc == 0 && h == 0) {
 #pragma unroll
-    for (int pb = 0; pb < 4; ++pb) {
-      const int pc = wp * 128 + pb * 32 + r;
+    for (int pb = 0; pb < k8PB; ++pb) {
+      const int pc = wp * 32 * k8PB + pb * 32 + r;
       const score_t os = ms[pc];
       const int oi = mi[pc];
       if (os < best[pb] || (os == best[pb] && oi < bidx[pb])) {
@@ -1334,10 +1338,10 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
     if (P.d <= 32 * kBMaxWords) {
       hipLaunchKernelGGL(assign_bits_kernel, dim3((unsigned)cdiv(P.n, kBTP)), dim3(kBT), 0, s, A);
     } else {
-      hipLaunchKernelGGL(assign_i8_kernel<FMT>, dim3((unsigned)cdiv(P.n, kT8)), dim3(kThreads), 0, s, A);
+      hipLaunchKernelGGL(assign_i8_kernel<FMT>, dim3((unsigned)cdiv(P.n, kT8)), dim3(k8Threads), 0, s, A);
     }
   } else if constexpr (FMT == KM_SQ8 || FMT == KM_BF16) {
-    hipLaunchKernelGGL(assign_i8_kernel<FMT>, dim3((unsigned)cdiv(P.n, kT8)), dim3(kThreads), 0, s, A);
+    hipLaunchKernelGGL(assign_i8_kernel<FMT>, dim3((unsigned)cdiv(P.n, kT8)), dim3(k8Threads), 0, s, A);
   } else {
     constexpr int TP = Geo<Blocking<FMT>::CB, Blocking<FMT>::PB>::TP;
     const int64_t npt = cdiv(P.n, TP);
