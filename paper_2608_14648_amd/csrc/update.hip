@@ -364,16 +364,36 @@ __global__ __launch_bounds__(256) void segsum_bits_kernel(const uint32_t *bits, 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int hw = blockIdx.y * 64 + lane;  // half-word index within the tail
   const bool ok = 16 * hw < dt;
+  const int wo = w0 + ((ok ? hw : 0) >> 1);  // clamped: every load is valid
+  const int sh = 16 * (hw & 1);
   float acc[16];
 #pragma unroll
   for (int e = 0; e < 16; ++e) acc[e] = 0.f;
-  for (int m = m0 + wave; m < m1; m += 4) {
-    const int p = perm[m];
-    const float a = alpha[p];
-    const uint32_t w = ok ? bits[(int64_t)p * wpr + w0 + (hw >> 1)] : 0u;
-    const uint32_t hb = w >> (16 * (hw & 1));
+  auto add = [&](float a, uint32_t w) {
+    const uint32_t hb = ok ? (w >> sh) : 0u;
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc[e] += ((hb >> e) & 1u) ? a : -a;
+  };
+  // 8 members in flight per wave (their loads issued together); each lane still
+  // adds the members in the order m, m + 4, m + 8, ...
+  int m = m0 + wave;
+  for (; m + 28 < m1; m += 32) {
+    int pp[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) pp[e] = perm[m + 4 * e];
+    float aa[8];
+    uint32_t ww[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      aa[e] = alpha[pp[e]];
+      ww[e] = bits[(int64_t)pp[e] * wpr + wo];
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) add(aa[e], ww[e]);
+  }
+  for (; m < m1; m += 4) {
+    const int p = perm[m];
+    add(alpha[p], bits[(int64_t)p * wpr + wo]);
   }
 #pragma unroll
   for (int e = 0; e < 16; ++e) red[wave][lane * 17 + e] = acc[e];
@@ -409,16 +429,16 @@ __global__ __launch_bounds__(256) void segsum_sq8_kernel(const uint8_t *codes, i
 #pragma unroll
   for (int e = 0; e < 16; ++e) acc[e] = 0;
   int m = m0 + wave;
-  for (; m + 12 < m1; m += 16) {
-    int pp[4];
+  for (; m + 28 < m1; m += 32) {
+    int pp[8];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) pp[e] = perm[m + 4 * e];
+    for (int e = 0; e < 8; ++e) pp[e] = perm[m + 4 * e];
     if (ok) {
-      uint4 v[4];
+      uint4 v[8];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = *reinterpret_cast<const uint4 *>(codes + (int64_t)pp[e] * ld + col);
+      for (int e = 0; e < 8; ++e) v[e] = *reinterpret_cast<const uint4 *>(codes + (int64_t)pp[e] * ld + col);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
+      for (int e = 0; e < 8; ++e) {
         const uint32_t ws[4] = {v[e].x, v[e].y, v[e].z, v[e].w};
 #pragma unroll
         for (int q = 0; q < 4; ++q)
