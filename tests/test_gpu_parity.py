@@ -70,6 +70,36 @@ def test_assign_f32(km, torch, n, d, k):
     assert abs(J - dist_o.sum()) <= OBJ_REL * dist_o.sum() + 1e-3
 
 
+@pytest.mark.parametrize("fmt", ["f32", "hybrid"])
+def test_assign_ties_across_centroid_groups(km, torch, fmt):
+    """k = 1100 spreads the centroid tiles over 8 workgroups per point tile; copies
+    of centroids 5 and 130 placed in other groups' tiles must never win."""
+    n, d, k = 3000, 96, 1100
+    X = blobs(n, d, 40, seed=17)
+    C = X[pick(n, k, 17)].copy()
+    C[900] = C[5]    # tile 7 vs tile 0
+    C[1050] = C[130]  # tile 8 vs tile 1
+    C[640] = C[5]
+    if fmt == "f32":
+        a_o, _ = orc.assign_f32(X, C)
+        a, _, _ = km.kmeans_assign(km.points_f32(to_dev(X, torch)), to_dev(C, torch), score=False)
+        a = host(a)
+        assert_fp_assign(a, a_o, f32_dist(X, C), "f32 groups")
+    else:
+        d0 = 32
+        m = orc.col_mean(X)
+        bits, alpha = orc.sign1_encode(X, m, d0)
+        front = np.ascontiguousarray(X[:, :d0])
+        a_o, _ = orc.assign_hybrid(front, bits, alpha, C, m, d0)
+        P = km.points_hybrid(to_dev(front, torch), to_dev(bits.view(np.int32), torch), to_dev(alpha, torch),
+                             to_dev(m, torch), d)
+        a, _, _ = km.kmeans_assign(P, to_dev(C, torch), score=False)
+        a = host(a)
+    if fmt == "f32":  # each centroid is a data point, which picks it (or an equal copy)
+        assert (a == 5).any() and (a == 130).any()
+    assert not np.isin(a, [640, 900, 1050]).any()
+
+
 def test_assign_f32_strided_rows(km, torch):
     n, d, k = 777, 64, 70
     W = blobs(n, 96, 20, seed=4)
@@ -115,8 +145,10 @@ def sign1_inputs(n, d, k, seed, d0=0):
     return X, m, bits, alpha, C
 
 
+# d > 1280 takes the 256 x 256 int8 kernel instead of the resident-bits one
 @pytest.mark.parametrize("n,d,k", [(1, 32, 1), (5, 64, 3), (300, 96, 3), (1000, 128, 64), (2049, 256, 130),
-                                   (517, 1024, 257), (700, 160, 129), (130, 64, 300), (700, 64, 600)])
+                                   (517, 1024, 257), (700, 160, 129), (130, 64, 300), (700, 64, 600),
+                                   (300, 1536, 70), (700, 2048, 300), (1, 1312, 3)])
 def test_assign_sign1_bit_exact(km, torch, n, d, k):
     say(f"assign sign1 n={n} d={d} k={k}")
     X, m, bits, alpha, C = sign1_inputs(n, d, k, seed=n + d + k)
@@ -170,8 +202,9 @@ def rand_assign(n, k, seed, empties=(), invalid=0):
     return a
 
 
+# (60000, 32, 20000): k above the LDS cursor limit of the scatter (global cursors)
 UPDATE_SHAPES = [(1, 32, 1, ()), (300, 32, 5, (1, 3)), (5000, 128, 64, (0, 7, 63)), (3001, 768, 130, (5,)),
-                 (2000, 96, 300, ()), (40, 64, 50, ())]
+                 (2000, 96, 300, ()), (40, 64, 50, ()), (60000, 32, 20000, (0, 19999))]
 
 
 @pytest.mark.parametrize("n,d,k,empties", UPDATE_SHAPES)
