@@ -15,6 +15,11 @@ Other workloads (--workload 1|3|4|5) time the other configurations for
 measurement; they are not the headline line.  --workload 6 runs the default
 workload's data stored as bfloat16.
 
+After the timed region, `quality` reports each final partition's full-precision
+cost (raw-vector member means), its cluster-size spread and, for the compressed
+formats other than SQ8, the ratio to an fp32 Lloyd run on the raw vectors with
+the same initial centroids and iteration count (--no-quality skips it).
+
 The JSON line carries the roofline of the dominant kernel (the fused fp32
 assignment kernel, on fp32 MFMA), measured from HIP events recorded by the
 library around each launch of that kernel on its stream, and the oracle timed on
@@ -122,6 +127,28 @@ def copy_probe(torch):
     log(f"copy probe done ({COPY_PROBE_FLOATS * 4} bytes)")
 
 
+def partition_stats(km, X, a, mu):
+    """Full-precision cost of a partition (raw-vector member means) and the spread
+    of its cluster sizes."""
+    _, cnt = km.kmeans_update(km.points_f32(X), a, mu, km.KM_EMPTY_KEEP, counts=True)
+    cost = float(km.kmeans_cost(X, mu, a).item())
+    c = cnt.cpu().numpy()
+    return {"cost": cost, "cluster_size_std": float(c.std()), "empty_clusters": int((c == 0).sum())}
+
+
+def f32_reference(km, X, k, T, idx, mu):
+    """The quality baseline: fp32 Lloyd on the raw vectors, same init and T."""
+    _, a, _ = km.kmeans_fit(km.points_f32(X), k, T, idx, objective=False)
+    return partition_stats(km, X, a, mu)
+
+
+def quality_vs_f32(km, X, k, T, idx, mu, name, a):
+    log("quality: fp32 reference fit (outside the timed region)")
+    q = {name: partition_stats(km, X, a, mu), "f32": f32_reference(km, X, k, T, idx, mu)}
+    q[f"objective_ratio_{name}_vs_f32"] = q[name]["cost"] / q["f32"]["cost"]
+    return q
+
+
 # ------------------------------------------------------------------------- workloads
 
 def workload_c2(cfg, torch, km, args):
@@ -140,7 +167,7 @@ def workload_c2(cfg, torch, km, args):
         s32, s8 = km.KmFitStats(), km.KmFitStats()
         C32, a32, J32 = km.kmeans_fit(P32, k, T, idx, stats=s32)
         C8, a8, J8 = km.kmeans_fit(P8, k, T, idx, stats=s8)
-        out = {}
+        out = {"a_f32": a32, "a_sq8": a8}
         for name, a in (("f32", a32), ("sq8", a8)):  # full-precision cost of the final partition
             km.kmeans_update(P32, a, mu, km.KM_EMPTY_KEEP, counts=False)
             out[name] = km.kmeans_cost(X, mu, a)
@@ -148,6 +175,9 @@ def workload_c2(cfg, torch, km, args):
             timer.add("f32", s32)
             timer.add("sq8", s8)
         return out, (J32, J8)
+
+    def quality(out):
+        return {name: partition_stats(km, X, out["a_" + name], mu) for name in ("f32", "sq8")}
 
     def finish(out, timer, elapsed, K):
         c32 = float(out["f32"].item())
@@ -212,7 +242,7 @@ def workload_c2(cfg, torch, km, args):
                 "sample": f"one fp32 and one SQ8 Lloyd iteration (assign + update) on the first {ns} of the "
                           f"{spec.n} points, k={k}, d={spec.d}, timed {t32 + t8:.2f} s, extrapolated linearly to N"}
 
-    return step, finish, cpu_baseline
+    return step, finish, cpu_baseline, quality
 
 
 def workload_bf16(cfg, torch, km, args):
@@ -234,7 +264,10 @@ def workload_bf16(cfg, torch, km, args):
         cost = km.kmeans_cost(X, mu, a)
         if timer is not None:
             timer.add("bf16", st)
-        return {"bf16": cost}, J
+        return {"bf16": cost, "a": a}, J
+
+    def quality(out):
+        return quality_vs_f32(km, X, k, T, idx, mu, "bf16", out["a"])
 
     def finish(out, timer, elapsed, K):
         s = timer.stats["bf16"]
@@ -251,7 +284,7 @@ def workload_bf16(cfg, torch, km, args):
                              "frac": ach / PEAK["bf16_mfma_tflops"], "traffic": None, "avg_launch_ms": a_ms},
                 "stages": {"bf16": stage_summary(s)}}
 
-    return step, finish, None
+    return step, finish, None, quality
 
 
 def workload_sign1(cfg, torch, km, args):
@@ -273,7 +306,10 @@ def workload_sign1(cfg, torch, km, args):
         cost = km.kmeans_cost(X, mu, a)
         if timer is not None:
             timer.add("sign1", st)
-        return {"sign1": cost}, J
+        return {"sign1": cost, "a": a}, J
+
+    def quality(out):
+        return quality_vs_f32(km, X, k, T, idx, mu, "sign1", out["a"])
 
     def finish(out, timer, elapsed, K):
         s = timer.stats["sign1"]
@@ -290,7 +326,7 @@ def workload_sign1(cfg, torch, km, args):
                              "traffic": None, "avg_launch_ms": a_ms},
                 "stages": {"sign1": stage_summary(s)}}
 
-    return step, finish, None
+    return step, finish, None, quality
 
 
 def workload_pca(cfg, torch, km, args):
@@ -301,6 +337,7 @@ def workload_pca(cfg, torch, km, args):
     X = upload(spec, torch)
     idx = synth.init_indices(spec.n, k)
     Y = torch.empty((spec.n, dout), dtype=torch.float32, device="cuda")
+    mu = torch.empty((k, spec.d), dtype=torch.float32, device="cuda")
 
     def step(timer):
         mean, cov = km.pca_fit_cov(X)
@@ -313,7 +350,10 @@ def workload_pca(cfg, torch, km, args):
         C, a, J = km.kmeans_fit(km.points_f32(Y), k, T, idx, stats=st)
         if timer is not None:
             timer.add("pca", st)
-        return {}, J
+        return {"a": a}, J
+
+    def quality(out):
+        return quality_vs_f32(km, X, k, T, idx, mu, "pca", out["a"])
 
     def finish(out, timer, elapsed, K):
         s = timer.stats["pca"]
@@ -328,7 +368,7 @@ def workload_pca(cfg, torch, km, args):
                              "frac": ach / PEAK["fp32_mfma_tflops"], "traffic": None, "avg_launch_ms": a_ms},
                 "stages": {"pca": stage_summary(s)}}
 
-    return step, finish, None
+    return step, finish, None, quality
 
 
 def workload_hybrid(cfg, torch, km, args):
@@ -351,7 +391,10 @@ def workload_hybrid(cfg, torch, km, args):
         cost = km.kmeans_cost(X, mu, a)
         if timer is not None:
             timer.add("hybrid", st)
-        return {"hybrid": cost}, J
+        return {"hybrid": cost, "a": a}, J
+
+    def quality(out):
+        return quality_vs_f32(km, X, k, T, idx, mu, "hybrid", out["a"])
 
     def finish(out, timer, elapsed, K):
         s = timer.stats["hybrid"]
@@ -367,7 +410,7 @@ def workload_hybrid(cfg, torch, km, args):
                              "frac": ach / PEAK["fp32_mfma_tflops"], "traffic": None, "avg_launch_ms": a_ms},
                 "stages": {"hybrid": stage_summary(s)}}
 
-    return step, finish, None
+    return step, finish, None, quality
 
 
 def workload_c1(cfg, torch, km, args):
@@ -377,13 +420,17 @@ def workload_c1(cfg, torch, km, args):
     X = upload(spec, torch)
     idx = synth.init_indices(spec.n, k)
     P = km.points_f32(X)
+    mu = torch.empty((k, spec.d), dtype=torch.float32, device="cuda")
 
     def step(timer):
         st = km.KmFitStats()
         C, a, J = km.kmeans_fit(P, k, T, idx, stats=st)
         if timer is not None:
             timer.add("f32", st)
-        return {}, J
+        return {"a": a}, J
+
+    def quality(out):
+        return {"f32": partition_stats(km, X, out["a"], mu)}
 
     def finish(out, timer, elapsed, K):
         s = timer.stats["f32"]
@@ -391,7 +438,7 @@ def workload_c1(cfg, torch, km, args):
                 "config": {"workload": cfg["name"], "N": spec.n, "d": spec.d, "k": k, "iters": T},
                 "distances_per_s": (T + 1) * spec.n * k * K / elapsed, "stages": {"f32": stage_summary(s)}}
 
-    return step, finish, None
+    return step, finish, None, quality
 
 
 WORKLOADS = {1: workload_c1, 2: workload_c2, 3: workload_sign1, 4: workload_pca, 5: workload_hybrid,
@@ -409,6 +456,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle's CPU-baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true", help="run the counter-calibration copy kernels first")
+    ap.add_argument("--no-quality", action="store_true",
+                    help="skip the partition-quality figures computed after the timed region")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -426,7 +475,7 @@ def main():
     if args.copy_probe:
         copy_probe(torch)
     cfg = synth.config(CONFIG_OF.get(args.workload, args.workload))
-    step, finish, cpu_baseline = WORKLOADS[args.workload](cfg, torch, km, args)
+    step, finish, cpu_baseline, quality = WORKLOADS[args.workload](cfg, torch, km, args)
     for i in range(args.warmup):
         step(None)
         torch.cuda.synchronize()
@@ -447,6 +496,8 @@ def main():
             "data": "synthetic (seeded Gaussian mixture shaped like the paper's embedding workloads)",
             "config": res.pop("config")}
     line.update(res)
+    if quality is not None and not args.no_quality:
+        line["quality"] = quality(out)
     if cpu_baseline is not None and not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
         line["cpu_baseline"] = cpu_baseline()
