@@ -60,6 +60,9 @@ def lib():
             "orc_sign1_prep": [_f32p, _i32, _i32, _f32p, _i32, _i8p, _f32p, _i32p, _i32p, _f32p],
             "orc_assign_sign1": [_u32p, _f32p, _i64, _i32, _i32, _i8p, _f32p, _i32p, _f32p, _i32, _i32p,
                                  _f32p, _f64p],
+            "orc_rabitq_prep": [_f32p, _i32, _i32, _i8p, _f32p, _f32p, _i32p, _f32p],
+            "orc_assign_rabitq": [_u32p, _f32p, _i64, _i32, _i8p, _f32p, _f32p, _i32p, _f32p, _i32, _i32p, _f32p,
+                                  _f64p],
             "orc_assign_hybrid": [_f32p, _u32p, _f32p, _i64, _i32, _i32, _f32p, _i8p, _f32p, _i32p, _f32p,
                                   _i32, _i32p, _f64p],
             "orc_update_f32": [_f32p, _i64, _i32, _i64, _i32p, _i32, _f32p, _i64p, _i32],
@@ -251,6 +254,33 @@ def assign_sign1(bits, alpha, C, m, d0: int = 0):
     return a, score, dist
 
 
+def rabitq_prep(C):
+    """Per-centroid SQ4 code of the centroid residuals (rotated space, centre 0)."""
+    C = _c(C, np.float32)
+    k, d = C.shape
+    q = np.empty((k, d), np.int8)
+    s = np.empty(k, np.float32)
+    b = np.empty(k, np.float32)
+    T = np.empty(k, np.int32)
+    N = np.empty(k, np.float32)
+    lib().orc_rabitq_prep(C, k, d, q, s, b, T, N)
+    return q, s, b, T, N
+
+
+def assign_rabitq(bits, alpha, C):
+    """(assignments, winning fp32 scores, alpha^2 d + score in fp64)."""
+    bits = _c(bits, np.uint32)
+    C = _c(C, np.float32)
+    n = bits.shape[0]
+    k, d = C.shape
+    q, s, b, T, N = rabitq_prep(C)
+    a = np.empty(n, np.int32)
+    score = np.empty(n, np.float32)
+    dist = np.empty(n, np.float64)
+    lib().orc_assign_rabitq(bits, _c(alpha, np.float32), n, d, q, s, b, T, N, k, a, score, dist)
+    return a, score, dist
+
+
 def assign_hybrid(front, bits, alpha, C, m, d0: int):
     front = _c(front, np.float32)
     bits = _c(bits, np.uint32)
@@ -337,6 +367,8 @@ def init_centroids(P: dict, idx):
         return np.ascontiguousarray(bf16_decode(P["codes"][idx]))
     if fmt == "sign1":
         return sign1_decode(P["bits"][idx], P["alpha"][idx], P["d"], P["m"], 0)
+    if fmt == "rabitq":
+        return sign1_decode(P["bits"][idx], P["alpha"][idx], P["d"], np.zeros(P["d"], np.float32), 0)
     if fmt == "hybrid":
         d0 = P["d0"]
         C = sign1_decode(P["bits"][idx], P["alpha"][idx], P["d"], P["m"], d0)
@@ -357,6 +389,9 @@ def assign(P: dict, C):
     if fmt == "sign1":
         a, _, dist = assign_sign1(P["bits"], P["alpha"], C, P["m"], 0)
         return a, dist
+    if fmt == "rabitq":
+        a, _, dist = assign_rabitq(P["bits"], P["alpha"], C)
+        return a, dist
     if fmt == "hybrid":
         return assign_hybrid(P["front"], P["bits"], P["alpha"], C, P["m"], P["d0"])
     raise ValueError(fmt)
@@ -372,19 +407,28 @@ def update(P: dict, a, k: int, C, policy: int = EMPTY_SPLIT):
         return update_bf16(P["codes"], a, k, C, policy)
     if fmt == "sign1":
         return update_sign1(P["bits"], P["alpha"], P["d"], P["m"], a, k, C, policy)
+    if fmt == "rabitq":
+        return update_sign1(P["bits"], P["alpha"], P["d"], np.zeros(P["d"], np.float32), a, k, C, policy)
     if fmt == "hybrid":
         return update_sign1(P["bits"], P["alpha"], P["d"], P["m"], a, k, C, policy, front=P["front"], d0=P["d0"])
     raise ValueError(fmt)
 
 
 def fit(P: dict, k: int, iters: int, init_idx, policy: int = EMPTY_SPLIT, C0=None):
-    """Lloyd: T x (assign, update), then a final assign.  Returns (C, a, J[0..T])."""
+    """Lloyd: T x (assign, update), then a final assign.  Returns (C, a, J[0..T]).
+
+    If P holds "raw" (fp32 rows in the clustering space), the last update averages
+    those instead of the compressed points (the raw-vector last iteration of
+    Sec. 4.1 that removes the outward bias of decoded 1-bit codes)."""
     C = init_centroids(P, init_idx) if C0 is None else np.array(C0, copy=True)
     J = []
-    for _ in range(iters):
+    for t in range(iters):
         a, dist = assign(P, C)
         J.append(float(np.sum(dist, dtype=np.float64)))
-        C, _ = update(P, a, k, C, policy)
+        if t == iters - 1 and P.get("raw") is not None:
+            C, _ = update_f32(P["raw"], a, k, C, policy)
+        else:
+            C, _ = update(P, a, k, C, policy)
     a, dist = assign(P, C)
     J.append(float(np.sum(dist, dtype=np.float64)))
     return C, a, J

@@ -308,6 +308,71 @@ void orc_assign_sign1(const uint32_t *bits, const float *alpha, int64_t n, int32
   }
 }
 
+/* ------------------------------------------------------------------------ */
+/* RabitQ with SQ4 centroid codes (Sec. 3.1, Eq. 3-5). */
+
+void orc_rabitq_prep(const float *C, int32_t k, int32_t d, int8_t *q, float *s, float *b, int32_t *T,
+                     float *N) {
+  for (int32_t j = 0; j < k; ++j) {
+    const float *c = C + (int64_t)j * d;
+    float lo = c[0], hi = c[0];
+    double nn = 0.0;
+    for (int32_t i = 0; i < d; ++i) {
+      if (c[i] < lo) lo = c[i];
+      if (c[i] > hi) hi = c[i];
+      nn += (double)c[i] * (double)c[i];
+    }
+    const float sc = hi > lo ? (hi - lo) / 15.0f : 1.0f;
+    int32_t tsum = 0;
+    for (int32_t i = 0; i < d; ++i) {
+      float t = rintf((c[i] - lo) / sc);
+      if (t < 0.0f) t = 0.0f;
+      if (t > 15.0f) t = 15.0f;
+      q[(int64_t)j * d + i] = (int8_t)t;
+      tsum += (int32_t)t;
+    }
+    s[j] = sc;
+    b[j] = lo;
+    T[j] = tsum;
+    N[j] = (float)nn;
+  }
+}
+
+/* Eq. 5: <2 xbar - 1, b + s q> = s (2 D - T) + b (2 P - d), D = sum of q on set bits. */
+static inline float rabitq_score(const uint32_t *row, float alpha, int32_t d, const int8_t *qj, float s,
+                                 float b, int32_t T, float N) {
+  int32_t D = 0, P = 0;
+  for (int32_t i = 0; i < d; ++i)
+    if (bit_of(row, i)) {
+      D += qj[i];
+      P += 1;
+    }
+  const float inner = fmaf(s, (float)(2 * D - T), b * (float)(2 * P - d));
+  return fmaf(-(2.0f * alpha), inner, N);
+}
+
+void orc_assign_rabitq(const uint32_t *bits, const float *alpha, int64_t n, int32_t d, const int8_t *q,
+                       const float *s, const float *b, const int32_t *T, const float *N, int32_t k,
+                       int32_t *a, float *score, double *dist) {
+  const int32_t W = d / 32;
+#pragma omp parallel for schedule(static)
+  for (int64_t r = 0; r < n; ++r) {
+    const uint32_t *row = bits + r * W;
+    int32_t best = 0;
+    float bs = 0.0f;
+    for (int32_t j = 0; j < k; ++j) {
+      const float sc = rabitq_score(row, alpha[r], d, q + (int64_t)j * d, s[j], b[j], T[j], N[j]);
+      if (j == 0 || sc < bs) {
+        bs = sc;
+        best = j;
+      }
+    }
+    a[r] = best;
+    if (score) score[r] = bs;
+    if (dist) dist[r] = (double)alpha[r] * (double)alpha[r] * (double)d + (double)bs;
+  }
+}
+
 void orc_assign_hybrid(const float *front, const uint32_t *bits, const float *alpha, int64_t n,
                        int32_t d, int32_t d0, const float *C, const int8_t *q, const float *sigma,
                        const int32_t *T, const float *u, int32_t k, int32_t *a, double *dist) {

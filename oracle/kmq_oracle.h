@@ -84,6 +84,22 @@ void orc_assign_hybrid(const float *front, const uint32_t *bits, const float *al
                        int32_t d, int32_t d0, const float *C, const int8_t *q, const float *sigma,
                        const int32_t *T, const float *u, int32_t k, int32_t *a, double *dist);
 
+/* RabitQ as the paper runs it (Sec. 3.1, Eq. 3-5), on 1-bit codes of the rotated,
+ * centred residual (centre 0 in the rotated space).  Centroid residuals are coded
+ * with a per-centroid SQ4: b_j = min_i c_ji, s_j = (max_i c_ji - b_j) / 15 (1 when
+ * the range is 0), q_ji = clip(rint((c_ji - b_j) / s_j), 0, 15) in fp32;
+ * T_j = sum q, N_j = ||c_j||^2 (fp64 sum, fp32 result). */
+void orc_rabitq_prep(const float *C, int32_t k, int32_t d, int8_t *q, float *s, float *b, int32_t *T,
+                     float *N);
+/* Eq. 4-5: with D = sum of q on set bits, P = number of set bits,
+ * inner = fmaf(s_j, 2D - T_j, b_j * (2P - d)) and score = fmaf(-(2 alpha), inner, N_j),
+ * fp32 in this order (alpha = ||x_r - m|| / (sqrt(d) <xbar, x>)).  Ties go to the
+ * smallest index.  dist (nullable) = alpha^2 d + score in fp64, the estimated squared
+ * distance with the decoded point's norm in place of ||x_r - m||^2. */
+void orc_assign_rabitq(const uint32_t *bits, const float *alpha, int64_t n, int32_t d, const int8_t *q,
+                       const float *s, const float *b, const int32_t *T, const float *N, int32_t k,
+                       int32_t *a, float *score, double *dist);
+
 /* ---- STEP 3: update (mean of members, empty-cluster split) ------------- */
 
 /* fp32 points: c_j = mean of members (fp64 sums, fp32 result).  counts = member counts. */

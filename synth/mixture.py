@@ -123,6 +123,16 @@ def for_each_chunk(spec: MixtureSpec, fn, threads: int | None = None):
             list(ex.map(work, range(nc)))
 
 
+def random_rotation(d: int, seed: int = 7) -> np.ndarray:
+    """A seeded random orthogonal d x d matrix (Haar measure: QR of a Gaussian matrix
+    with the signs of R's diagonal folded into Q), fp32.  The random rotation the
+    1-bit codes are taken after is an input drawn here, shared by both sides."""
+    g = np.random.default_rng(seed).standard_normal((d, d))
+    q, r = np.linalg.qr(g)
+    q *= np.sign(np.diag(r))[None, :]
+    return np.ascontiguousarray(q, dtype=np.float32)
+
+
 def init_indices(n: int, k: int, seed: int = 0) -> np.ndarray:
     """k distinct row indices drawn at random (Forgy initialisation)."""
     return np.random.default_rng(seed + 1).choice(n, k, replace=False).astype(np.int64)

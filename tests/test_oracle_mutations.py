@@ -33,6 +33,9 @@ MUTATIONS = {
     "bf16_truncates": ("double q = rint(ldexp((double)x, -se));", "double q = trunc(ldexp((double)x, -se));"),
     "bf16_ties_away_from_zero": ("double q = rint(ldexp((double)x, -se));", "double q = round(ldexp((double)x, -se));"),
     "bf16_keeps_9_bits": ("int se = e - 8 < -133 ? -133 : e - 8;", "int se = e - 9 < -133 ? -133 : e - 9;"),
+    "rabitq_bias_term_sign": ("b * (float)(2 * P - d)", "b * (float)(d - 2 * P)"),
+    "rabitq_sq4_16_levels": ("(hi - lo) / 15.0f", "(hi - lo) / 16.0f"),
+    "rabitq_drops_T": ("(float)(2 * D - T)", "(float)(2 * D)"),
 }
 
 PINS = [name for name in dir(pins) if name.startswith("test_")]

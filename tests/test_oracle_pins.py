@@ -524,3 +524,123 @@ def test_bf16_steps_on_representable_data_equal_f32(orc):
     same = np.repeat(codes[:1], 7, axis=0)
     Cm, _ = orc.update_bf16(same, np.zeros(7, np.int32), 1, np.zeros((1, 48), np.float32))
     np.testing.assert_array_equal(Cm[0], Xb[0])
+
+
+# --------------------------------------------------------------------------
+# RabitQ with SQ4 centroid codes (Sec. 3.1, Eq. 3-5) and the raw-vector last update
+
+def test_rabitq_eq5_example(orc):
+    """Hand-worked Eq. 5 example: codes, sums and the estimator, evaluated directly as
+    sum_i (2 xbar_i - 1)(b + s ybar_i) over the 32 dims."""
+    g = load_golden("rabitq_eq5.json")
+    d = g["d"]
+    C = np.zeros((1, d), np.float32)
+    C[0, :4] = g["centroid_residual_head"]
+    q, s, b, T, N = orc.rabitq_prep(C)
+    s32 = np.float32(g["scale_fraction"][0]) / np.float32(g["scale_fraction"][1])
+    assert b[0] == g["bias"] and s[0] == s32
+    assert q[0, :4].tolist() == g["codes_head"] and (q[0, 4:] == g["code_of_zero"]).all()
+    assert int(T[0]) == g["T"] and float(N[0]) == g["centroid_norm_sq"]
+    bits = np.zeros((1, 1), np.uint32)
+    bits[0, 0] = g["bits_word"]
+    xb = np.array([(g["bits_word"] >> i) & 1 for i in range(d)])
+    assert int(q[0][xb == 1].sum()) == g["D"] and int(xb.sum()) == g["popcount"]
+    direct = float(np.sum((2.0 * xb - 1.0) * (float(b[0]) + float(s[0]) * q[0].astype(np.float64))))
+    hand = g["estimator_constant"] + g["estimator_s_coefficient"] * float(s[0])
+    assert abs(direct - hand) < 1e-6
+    alpha = np.array([0.5], np.float32)
+    a, score, dist = orc.assign_rabitq(bits, alpha, C)
+    # score = N - 2 alpha <2xbar - 1, b + s q>, to fp32 rounding
+    assert abs(float(score[0]) - (g["centroid_norm_sq"] - 2 * 0.5 * hand)) < 1e-5
+    assert abs(dist[0] - (0.25 * d + float(score[0]))) < 1e-9
+
+
+def test_rabitq_sq4_code_properties(orc):
+    """Per-centroid SQ4: bias = min, 15 s = max - min, codes in [0, 15] with the min
+    at 0 and the max at 15, reconstruction within half a step; a constant centroid
+    codes to 0 with s = 1 and reconstructs exactly."""
+    rng = np.random.default_rng(41)
+    C = (rng.standard_normal((20, 64)) * rng.uniform(0.1, 3.0, (20, 1))).astype(np.float32)
+    C[3] = 0.75
+    q, s, b, T, N = orc.rabitq_prep(C)
+    C64 = C.astype(np.float64)
+    np.testing.assert_array_equal(b, C.min(1))
+    live = np.arange(20) != 3
+    np.testing.assert_allclose(15.0 * s[live], C64.max(1)[live] - C64.min(1)[live], rtol=1e-6)
+    assert q.min() >= 0 and q.max() <= 15
+    assert (q[live].min(1) == 0).all() and (q[live].max(1) == 15).all()
+    rec = b[:, None].astype(np.float64) + s[:, None].astype(np.float64) * q
+    assert (np.abs(rec - C64) <= 0.5 * s[:, None] * (1 + 1e-5)).all()
+    assert s[3] == 1.0 and (q[3] == 0).all() and rec[3, 0] == 0.75
+    np.testing.assert_array_equal(T, q.astype(np.int64).sum(1))
+    np.testing.assert_allclose(N, (C64 ** 2).sum(1), rtol=1e-6)
+
+
+def test_rabitq_estimator_unbiased_over_rotations(orc):
+    """RabitQ's estimator of <x_r - m, y_r - m> (Eq. 4-5) is unbiased over random
+    rotations: averaging alpha <2 xbar - 1, SQ4(P y)> over many seeded rotations P
+    recovers the exact inner product within a few standard errors (the SQ4 rounding
+    of the rotated centroid behaves as zero-mean noise).  A dropped bias term, a
+    wrong sign or a wrong scale of alpha moves the mean far outside."""
+    import synth
+    d = 64
+    rng = np.random.default_rng(43)
+    r = rng.standard_normal(d).astype(np.float32)
+    y = (0.6 * r + 0.8 * rng.standard_normal(d)).astype(np.float32)
+    exact = float(np.dot(r.astype(np.float64), y.astype(np.float64)))
+    est = []
+    for t in range(3000):
+        P = synth.random_rotation(d, seed=1000 + t)
+        rp = (r.astype(np.float64) @ P.astype(np.float64)).astype(np.float32)[None, :]
+        yp = (y.astype(np.float64) @ P.astype(np.float64)).astype(np.float32)[None, :]
+        bits, alpha = orc.sign1_encode(rp, np.zeros(d, np.float32), 0)
+        _, score, _ = orc.assign_rabitq(bits, alpha, yp)
+        _, _, _, _, N = orc.rabitq_prep(yp)
+        est.append((float(N[0]) - float(score[0])) / 2.0)  # alpha * <2xbar - 1, b + s q>
+    est = np.array(est)
+    se = est.std() / np.sqrt(len(est))
+    assert abs(est.mean() - exact) < 5 * se + 1e-3 * abs(exact), (est.mean(), exact, se)
+
+
+@settings(max_examples=25, deadline=None)
+@given(n=st.integers(1, 40), w=st.integers(1, 2), k=st.integers(1, 7), seed=st.integers(0, 10_000))
+def test_assign_rabitq_bruteforce(orc, n, w, k, seed):
+    """Against an explicit fp64 evaluation of N_j - 2 alpha <2 xbar - 1, b_j + s_j q_j>
+    over the decoded sign vectors; disagreements only at fp32 near-ties."""
+    d = 32 * w
+    rng = np.random.default_rng(seed)
+    X = rng.standard_normal((n, d)).astype(np.float32)
+    C = rng.standard_normal((k, d)).astype(np.float32)
+    bits, alpha = orc.sign1_encode(X, np.zeros(d, np.float32), 0)
+    a, score, _ = orc.assign_rabitq(bits, alpha, C)
+    q, s, b, T, N = orc.rabitq_prep(C)
+    sgn = ((bits[:, :, None] >> np.arange(32, dtype=np.uint32)) & 1).reshape(n, d).astype(np.float64) * 2 - 1
+    rec = b[:, None].astype(np.float64) + s[:, None].astype(np.float64) * q
+    est = N[None, :].astype(np.float64) - 2 * alpha[:, None].astype(np.float64) * (sgn @ rec.T)
+    ref = est.argmin(1)
+    gap = est[np.arange(n), a] - est[np.arange(n), ref]
+    assert (gap <= 1e-4 * (1 + np.abs(est).max())).all()
+
+
+def test_fit_raw_last_update(orc):
+    """With raw rows given, the last Lloyd update averages them: the final centroids
+    are the raw-row means of the clusters of the last-but-one assignment pass
+    (explicit one-hot means), and the final pass assigns against them."""
+    import synth
+    rng = np.random.default_rng(47)
+    d, n, k, T = 64, 600, 6, 3
+    Xr = rng.standard_normal((n, d)).astype(np.float32)
+    P = synth.random_rotation(d, seed=5)
+    Y = (Xr.astype(np.float64) @ P.astype(np.float64)).astype(np.float32)
+    bits, alpha = orc.sign1_encode(Y, np.zeros(d, np.float32), 0)
+    Pd = {"fmt": "rabitq", "bits": bits, "alpha": alpha, "d": d, "raw": Y}
+    idx = rng.choice(n, k, replace=False)
+    C, a, J = orc.fit(Pd, k, T, idx)
+    C2, a2, J2 = orc.fit({k_: v for k_, v in Pd.items() if k_ != "raw"}, k, T - 1, idx)
+    a_last, _ = orc.assign(Pd, C2)
+    for j in range(k):
+        mem = Y[a_last == j].astype(np.float64)
+        if len(mem):
+            np.testing.assert_allclose(C[j], mem.mean(0), rtol=1e-6, atol=1e-6)
+    a_fin, _ = orc.assign(Pd, C)
+    np.testing.assert_array_equal(a, a_fin)
