@@ -48,7 +48,8 @@ typedef enum {
   KM_BF16 = 1,   /* bfloat16 vectors (16-bit storage of full-precision vectors, Sec. 2.4) */
   KM_SQ8 = 2,    /* uint8 scalar-quantised codes, one (lo, hi) pair per dimension */
   KM_SIGN1 = 3,  /* 1-bit sign codes of x - m plus one fp32 scale alpha per vector */
-  KM_HYBRID = 4  /* fp32 front dims [0, d_front) + 1-bit codes on the tail [d_front, d) */
+  KM_HYBRID = 4, /* fp32 front dims [0, d_front) + 1-bit codes on the tail [d_front, d) */
+  KM_RABITQ = 5  /* 1-bit codes of the randomly rotated, centred residual; SQ4 centroid codes */
 } km_format;
 
 typedef enum {
@@ -71,7 +72,17 @@ typedef enum {
  *              d_front/32 .. d/32-1 are read); alpha = float[n] computed over the
  *              tail dims; center = float[d]; front = float[n][d_front];
  *              d_front % 32 == 0, 0 < d_front < d.
+ *   KM_RABITQ: data = uint32[n][d/32] bits of y = (x - m) P, the centred residual
+ *              rotated by an orthogonal d x d matrix P (Sec. 3.1 RabitQ; see
+ *              rabitq_encode), alpha = float[n] = ||y||^2 / ||y||_1, center must be
+ *              NULL (the codes are of the residual: the clustering space is the
+ *              rotated residual space, centre 0).  d % 32 == 0.
  * `ld` is ignored for the 1-bit formats.
+ * raw (nullable): fp32 rows of the same points in the clustering space (the
+ *   original vectors for KM_SIGN1 / KM_HYBRID / KM_BF16, the rotated residual y for
+ *   KM_RABITQ), float[n][raw_ld], raw_ld >= d, raw_ld % 4 == 0, d % 4 == 0,
+ *   16-byte aligned.  kmeans_fit then computes its last update from these rows
+ *   (the raw-vector last iteration of Sec. 4.1).  Not allowed for KM_SQ8.
  */
 typedef struct km_points {
   int32_t fmt;          /* km_format */
@@ -84,6 +95,8 @@ typedef struct km_points {
   const float *front;
   int32_t d_front;
   int32_t reserved;     /* must be 0 */
+  const float *raw;     /* nullable, see above */
+  int64_t raw_ld;       /* row stride of raw in floats */
 } km_points;
 
 /*
@@ -113,6 +126,19 @@ km_status quantize(const float *X, int64_t n, int32_t d, int64_t ldx, int32_t fm
                    km_stream stream);
 
 /*
+ * rabitq_encode -- RabitQ codes (Sec. 3.1 RabitQ): y = (x - m) P for an orthogonal
+ * P, then bit i = [y_i > 0] and alpha = ||y||^2 / ||y||_1 (fp64 sums; 0 when y = 0),
+ * which is ||x - m|| / (sqrt(d) <xbar, x>) of Eq. 4.
+ *   X: float[n][ldx] (ldx % 4 == 0, 16-byte aligned); P: float[d][d] row-major (the
+ *   caller draws it; the library does not check orthogonality); m: float[d], the
+ *   centre: computed as the column mean (fp64 sums) when flags & KM_Q_FIT_PARAMS,
+ *   else an input.  bits: uint32[n][d/32]; alpha: float[n].  d % 32 == 0.
+ *   Scratch: the rotated rows (n x d floats) for the duration of the call.
+ */
+km_status rabitq_encode(const float *X, int64_t n, int32_t d, int64_t ldx, const float *P, float *m,
+                        uint32_t *bits, float *alpha, int32_t flags, km_stream stream);
+
+/*
  * pca_fit_cov -- PCA statistics (Sec. 3.1 PCA; Sec. 4.2): mean = float[d] column
  * mean, cov = float[d][d] = (1/n) sum (x - mean)(x - mean)^T (symmetric, both
  * halves written).  X: float[n][d], d % 4 == 0.  The eigendecomposition of cov
@@ -134,7 +160,10 @@ km_status pca_project(const float *X, int64_t n, int32_t d, const float *mean, c
  *   C: centroids in the clustering space, k x d, row-major:
  *      KM_F32 / KM_BF16: float; KM_SQ8: uint8 codes; KM_SIGN1 / KM_HYBRID: float in
  *      the original space (the 1-bit part is compared against int8 residual codes
- *      q = rint((c - m)/sigma), sigma = max|c - m|/127, rebuilt on each call).
+ *      q = rint((c - m)/sigma), sigma = max|c - m|/127, rebuilt on each call);
+ *      KM_RABITQ: float in the rotated residual space, coded on each call with a
+ *      per-centroid SQ4 (Eq. 5): b = min_i c_i, s = (max_i c_i - b)/15 (1 when the
+ *      range is 0), q = clip(rint((c - b)/s), 0, 15).
  *      KM_BF16 compares the points with the centroids rounded to bfloat16 (nearest,
  *      ties to even), products exact, fp32 accumulation.
  *   assign: int32[n].  score (nullable): float[n], the winning score, i.e. the
@@ -142,9 +171,13 @@ km_status pca_project(const float *X, int64_t n, int32_t d, const float *mean, c
  *      F32: ||c||^2 - 2<x,c>;  BF16: the same on the bfloat16 values;
  *      SQ8: ||c~||^2 - 2<x~,c~> with x~ = code - 128;
  *      SIGN1: fmaf(-alpha*2*sigma, <2b-1, q>, sigma^2 ||q||^2);
- *      HYBRID: front F32 score + tail SIGN1 score.
+ *      HYBRID: front F32 score + tail SIGN1 score;
+ *      RABITQ (Eq. 4-5): fmaf(-2 alpha, fmaf(s, 2D - T, b (2P - d)), ||c||^2) with
+ *      D = sum of q on set bits, T = sum of q, P = number of set bits (fp32, in this
+ *      order).
  *   objective (nullable): double[1], receives sum over points of the in-space
- *      distance (score plus the point-only term), fp64.
+ *      distance (score plus the point-only term), fp64.  For the 1-bit formats the
+ *      point-only term is the decoded point's squared norm alpha^2 d.
  *   1 <= k.
  */
 km_status kmeans_assign(const km_points *P, const void *C, int32_t k, int32_t *assign, float *score,
@@ -156,7 +189,8 @@ km_status kmeans_assign(const km_points *P, const void *C, int32_t k, int32_t *a
  *   KM_F32: fp32 mean; KM_BF16: fp32 mean of the stored bfloat16 values;
  *   KM_SQ8: floor((2 S + n_j) / (2 n_j)) with S the exact code sum
  *   (averaging in the quantised domain, Sec. 3.1); KM_SIGN1: m + (1/n_j) sum alpha (2b - 1)
- *   (fused decode-averaging, Sec. 3.1); KM_HYBRID: front mean and tail decode-average.
+ *   (fused decode-averaging, Sec. 3.1); KM_HYBRID: front mean and tail decode-average;
+ *   KM_RABITQ: (1/n_j) sum alpha (2b - 1) in the rotated residual space.
  *   C: in = previous centroids, out = new ones (same type as kmeans_assign).
  *   counts (nullable): int64[k] member counts of `assign`.
  *   policy KM_EMPTY_SPLIT: empty clusters, in ascending order, take a split of the
@@ -183,7 +217,8 @@ typedef struct km_fit_stats {
 
 /*
  * kmeans_fit -- Lloyd's algorithm (Sec. 2.3): STEP 1 (C = the points at
- * init_idx), then `iters` x (STEP 2, STEP 3), then a final STEP 2.
+ * init_idx), then `iters` x (STEP 2, STEP 3), then a final STEP 2.  When
+ * P->raw is set, the last STEP 3 averages the raw rows instead of the codes.
  *   init_idx: HOST int64[k], distinct, in [0, n); NULL = C already holds the
  *     initial centroids (resume from saved centroids).
  *   C: out (and in when init_idx is NULL), as in kmeans_assign.

@@ -16,12 +16,12 @@ import torch
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libkmq.so")
 
-KM_F32, KM_BF16, KM_SQ8, KM_SIGN1, KM_HYBRID = 0, 1, 2, 3, 4
+KM_F32, KM_BF16, KM_SQ8, KM_SIGN1, KM_HYBRID, KM_RABITQ = 0, 1, 2, 3, 4, 5
 KM_EMPTY_SPLIT, KM_EMPTY_KEEP = 0, 1
 KM_Q_FIT_PARAMS = 1
 STATUS = {0: "KM_OK", -1: "KM_EINVAL", -2: "KM_EUNSUPPORTED", -3: "KM_ENOMEM", -4: "KM_EDEVICE"}
-EXPORTS = ("quantize", "pca_fit_cov", "pca_project", "kmeans_assign", "kmeans_update", "kmeans_fit",
-           "kmeans_cost", "km_last_error", "km_release")
+EXPORTS = ("quantize", "rabitq_encode", "pca_fit_cov", "pca_project", "kmeans_assign", "kmeans_update",
+           "kmeans_fit", "kmeans_cost", "km_last_error", "km_release")
 
 
 class KmqError(RuntimeError):
@@ -33,7 +33,7 @@ class KmqError(RuntimeError):
 class KmPoints(ct.Structure):
     _fields_ = [("fmt", ct.c_int32), ("d", ct.c_int32), ("n", ct.c_int64), ("data", ct.c_void_p),
                 ("ld", ct.c_int64), ("alpha", ct.c_void_p), ("center", ct.c_void_p), ("front", ct.c_void_p),
-                ("d_front", ct.c_int32), ("reserved", ct.c_int32)]
+                ("d_front", ct.c_int32), ("reserved", ct.c_int32), ("raw", ct.c_void_p), ("raw_ld", ct.c_int64)]
 
 
 class KmFitStats(ct.Structure):
@@ -58,6 +58,7 @@ def lib():
         vp, i32, i64 = ct.c_void_p, ct.c_int32, ct.c_int64
         sig = {
             "quantize": [vp, i64, i32, i64, i32, vp, vp, vp, i32, vp, i32, vp],
+            "rabitq_encode": [vp, i64, i32, i64, vp, vp, vp, vp, i32, vp],
             "pca_fit_cov": [vp, i64, i32, vp, vp, vp],
             "pca_project": [vp, i64, i32, vp, vp, i32, vp, vp],
             "kmeans_assign": [ct.POINTER(KmPoints), vp, i32, vp, vp, vp, vp],
@@ -106,13 +107,18 @@ def _dev(t: torch.Tensor, dtype, name: str, ndim=None):
 class Points:
     """Compressed points handed to the clustering calls (mirrors ``km_points``)."""
 
-    def __init__(self, fmt: int, data: torch.Tensor, d: int, alpha=None, center=None, front=None, d_front: int = 0):
+    def __init__(self, fmt: int, data: torch.Tensor, d: int, alpha=None, center=None, front=None, d_front: int = 0,
+                 raw=None):
         self.fmt, self.data, self.d = fmt, data, d
-        self.alpha, self.center, self.front, self.d_front = alpha, center, front, d_front
+        self.alpha, self.center, self.front, self.d_front, self.raw = alpha, center, front, d_front, raw
         self.n = data.shape[0]
         ld = data.stride(0) if fmt in (KM_F32, KM_BF16, KM_SQ8) else d // 32
+        if raw is not None:
+            _rows(raw, torch.float32, "raw")
+            if raw.shape[0] != self.n or raw.shape[1] != d:
+                raise ValueError("raw must hold the same n points with d dims")
         self._c = KmPoints(fmt, d, self.n, data.data_ptr(), ld, _ptr(alpha) or None, _ptr(center) or None,
-                           _ptr(front) or None, d_front, 0)
+                           _ptr(front) or None, d_front, 0, _ptr(raw) or None, raw.stride(0) if raw is not None else 0)
 
     @property
     def ref(self):
@@ -141,10 +147,11 @@ def points_f32(X: torch.Tensor) -> Points:
     return Points(KM_F32, X, X.shape[1])
 
 
-def points_bf16(X: torch.Tensor) -> Points:
-    """bfloat16 points (torch.bfloat16); rows must be contiguous, the row stride may be larger than d."""
+def points_bf16(X: torch.Tensor, raw: torch.Tensor | None = None) -> Points:
+    """bfloat16 points (torch.bfloat16); rows must be contiguous, the row stride may be larger than d.
+    raw: optional fp32 rows for the last update of kmeans_fit."""
     _rows(X, torch.bfloat16, "X")
-    return Points(KM_BF16, X, X.shape[1])
+    return Points(KM_BF16, X, X.shape[1], raw=raw)
 
 
 def points_sq8(codes: torch.Tensor) -> Points:
@@ -152,24 +159,35 @@ def points_sq8(codes: torch.Tensor) -> Points:
     return Points(KM_SQ8, codes, codes.shape[1])
 
 
-def points_sign1(bits: torch.Tensor, alpha: torch.Tensor, center: torch.Tensor, d: int) -> Points:
+def points_sign1(bits: torch.Tensor, alpha: torch.Tensor, center: torch.Tensor, d: int,
+                 raw: torch.Tensor | None = None) -> Points:
     _dev(bits, torch.int32, "bits", 2)
     _dev(alpha, torch.float32, "alpha", 1)
     _dev(center, torch.float32, "center", 1)
     if bits.shape[1] != d // 32:
         raise ValueError("bits must have d/32 words per row")
-    return Points(KM_SIGN1, bits, d, alpha=alpha, center=center)
+    return Points(KM_SIGN1, bits, d, alpha=alpha, center=center, raw=raw)
+
+
+def points_rabitq(bits: torch.Tensor, alpha: torch.Tensor, d: int, raw: torch.Tensor | None = None) -> Points:
+    """RabitQ points (codes of the rotated residual, from rabitq_encode); raw: optional
+    fp32 rotated residual rows (X - m) P for the last update of kmeans_fit."""
+    _dev(bits, torch.int32, "bits", 2)
+    _dev(alpha, torch.float32, "alpha", 1)
+    if bits.shape[1] != d // 32:
+        raise ValueError("bits must have d/32 words per row")
+    return Points(KM_RABITQ, bits, d, alpha=alpha, raw=raw)
 
 
 def points_hybrid(front: torch.Tensor, bits: torch.Tensor, alpha: torch.Tensor, center: torch.Tensor,
-                  d: int) -> Points:
+                  d: int, raw: torch.Tensor | None = None) -> Points:
     _dev(front, torch.float32, "front", 2)
     _dev(bits, torch.int32, "bits", 2)
     _dev(alpha, torch.float32, "alpha", 1)
     _dev(center, torch.float32, "center", 1)
     if bits.shape[1] != d // 32:
         raise ValueError("bits must have d/32 words per row")
-    return Points(KM_HYBRID, bits, d, alpha=alpha, center=center, front=front, d_front=front.shape[1])
+    return Points(KM_HYBRID, bits, d, alpha=alpha, center=center, front=front, d_front=front.shape[1], raw=raw)
 
 
 # --------------------------------------------------------------------------
@@ -188,6 +206,28 @@ def quantize_sq8(X: torch.Tensor, params: torch.Tensor | None = None):
     _check(lib().quantize(_ptr(X), n, d, X.stride(0), KM_SQ8, _ptr(codes), _ptr(params), None, 0, None, flags,
                           _stream()))
     return codes, params
+
+
+def rabitq_encode(X: torch.Tensor, rotation: torch.Tensor, center: torch.Tensor | None = None):
+    """RabitQ codes of X: (bits int32 n x d/32, centre m, alpha).  rotation: float32
+    d x d orthogonal P (row-major); the codes are of (X - m) P.  Fits m (column mean)
+    unless given."""
+    _dev(X, torch.float32, "X", 2)
+    _dev(rotation, torch.float32, "rotation", 2)
+    n, d = X.shape
+    if rotation.shape != (d, d):
+        raise ValueError("rotation must be d x d")
+    bits = torch.empty((n, d // 32), dtype=torch.int32, device=X.device)
+    alpha = torch.empty(n, dtype=torch.float32, device=X.device)
+    flags = 0
+    if center is None:
+        center = torch.empty(d, dtype=torch.float32, device=X.device)
+        flags = KM_Q_FIT_PARAMS
+    else:
+        _dev(center, torch.float32, "center", 1)
+    _check(lib().rabitq_encode(_ptr(X), n, d, X.stride(0), _ptr(rotation), _ptr(center), _ptr(bits), _ptr(alpha),
+                               flags, _stream()))
+    return bits, center, alpha
 
 
 def quantize_bf16(X: torch.Tensor) -> torch.Tensor:

@@ -89,8 +89,9 @@ static size_t al(size_t x) { return (x + 255) & ~(size_t)255; }
 static km_status check_points(const km_points *P, Points *out) {
   KMQ_CHECK(P != nullptr, KM_EINVAL, "points descriptor is NULL");
   const int fmt = P->fmt;
-  KMQ_CHECK(fmt == KM_F32 || fmt == KM_BF16 || fmt == KM_SQ8 || fmt == KM_SIGN1 || fmt == KM_HYBRID, KM_EUNSUPPORTED,
-            "unknown point format %d", fmt);
+  KMQ_CHECK(fmt == KM_F32 || fmt == KM_BF16 || fmt == KM_SQ8 || fmt == KM_SIGN1 || fmt == KM_HYBRID ||
+                fmt == KM_RABITQ,
+            KM_EUNSUPPORTED, "unknown point format %d", fmt);
   KMQ_CHECK(P->reserved == 0, KM_EINVAL, "reserved field must be 0");
   KMQ_CHECK(P->n >= 1 && P->n < (int64_t)INT32_MAX, KM_EINVAL, "n = %lld outside [1, 2^31)", (long long)P->n);
   KMQ_CHECK(P->d >= 1, KM_EINVAL, "d = %d must be >= 1", P->d);
@@ -106,6 +107,13 @@ static km_status check_points(const km_points *P, Points *out) {
   p.center = P->center;
   p.front = P->front;
   p.d_front = P->d_front;
+  p.raw = P->raw;
+  p.raw_ld = P->raw_ld;
+  if (P->raw) {
+    KMQ_CHECK(fmt != KM_SQ8, KM_EINVAL, "raw rows are not allowed for SQ8 points (their centroids are codes)");
+    KMQ_CHECK(P->d % 4 == 0 && P->raw_ld >= P->d && P->raw_ld % 4 == 0 && aligned16(P->raw), KM_EINVAL,
+              "raw rows need d %% 4 == 0, raw_ld >= d, raw_ld %% 4 == 0 and 16-byte alignment");
+  }
   if (fmt == KM_F32) {
     KMQ_CHECK(P->d % 4 == 0, KM_EINVAL, "fp32 points need d %% 4 == 0 (d = %d)", P->d);
     KMQ_CHECK(P->ld >= P->d && P->ld % 4 == 0, KM_EINVAL, "fp32 points need ld >= d and ld %% 4 == 0");
@@ -121,7 +129,10 @@ static km_status check_points(const km_points *P, Points *out) {
   } else {
     KMQ_CHECK(P->d % 32 == 0, KM_EINVAL, "1-bit codes need d %% 32 == 0 (d = %d)", P->d);
     KMQ_CHECK(P->alpha != nullptr, KM_EINVAL, "alpha is NULL");
-    KMQ_CHECK(P->center != nullptr, KM_EINVAL, "center is NULL");
+    if (fmt == KM_RABITQ)
+      KMQ_CHECK(P->center == nullptr, KM_EINVAL, "RabitQ codes are of the rotated residual: center must be NULL");
+    else
+      KMQ_CHECK(P->center != nullptr, KM_EINVAL, "center is NULL");
     p.ld = P->d / 32;
     if (fmt == KM_HYBRID) {
       KMQ_CHECK(P->d_front > 0 && P->d_front < P->d && P->d_front % 32 == 0, KM_EINVAL,
@@ -141,6 +152,17 @@ static km_status check_centroids(const Points &p, const void *C, int k) {
   KMQ_CHECK(aligned16(C), KM_EINVAL, "centroids must be 16-byte aligned");
   (void)p;
   return KM_OK;
+}
+
+// The raw rows of p as fp32 points (the last update of a fit).
+static Points raw_points(const Points &p) {
+  Points r{};
+  r.fmt = KM_F32;
+  r.d = p.d;
+  r.n = p.n;
+  r.data = p.raw;
+  r.ld = p.raw_ld;
+  return r;
 }
 
 static size_t centroid_bytes(const Points &p, int k) {  // BF16 centroids are fp32
@@ -221,7 +243,24 @@ km_status pca_project(const float *X, int64_t n, int32_t d, const float *mean, c
   Scratch ws(s);
   km_status st = ws.alloc(pca_project_bytes(d, d_out));
   if (st != KM_OK) return st;
-  return launch_pca_project(X, n, d, mean, W, d_out, Y, ws.get(), s);
+  return launch_pca_project(X, n, d, (int64_t)d, mean, W, d_out, Y, ws.get(), s);
+}
+
+km_status rabitq_encode(const float *X, int64_t n, int32_t d, int64_t ldx, const float *P, float *m, uint32_t *bits,
+                        float *alpha, int32_t flags, km_stream stream) {
+  g_err[0] = 0;
+  KMQ_CHECK(X != nullptr && P != nullptr && m != nullptr && bits != nullptr && alpha != nullptr, KM_EINVAL,
+            "NULL argument");
+  KMQ_CHECK(n >= 1 && n < (int64_t)INT32_MAX, KM_EINVAL, "n = %lld outside [1, 2^31)", (long long)n);
+  KMQ_CHECK(d >= 32 && d % 32 == 0, KM_EINVAL, "rabitq_encode needs d %% 32 == 0 (d = %d)", d);
+  KMQ_CHECK(ldx >= d && ldx % 4 == 0, KM_EINVAL, "need ldx >= d and ldx %% 4 == 0");
+  KMQ_CHECK(aligned16(X) && aligned16(m), KM_EINVAL, "X and m must be 16-byte aligned");
+  KMQ_CHECK((flags & ~KM_Q_FIT_PARAMS) == 0, KM_EINVAL, "unknown flags 0x%x", flags);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  Scratch ws(s);
+  km_status st = ws.alloc(rabitq_encode_bytes(n, d));
+  if (st != KM_OK) return st;
+  return launch_rabitq_encode(X, n, d, ldx, P, m, bits, alpha, flags, ws.get(), s);
 }
 
 km_status kmeans_assign(const km_points *P, const void *C, int32_t k, int32_t *assign, float *score,
@@ -355,7 +394,7 @@ km_status kmeans_fit(const km_points *P, int32_t k, int32_t iters, const int64_t
   }
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const size_t b_prep = al(prep_bytes(p, k));
-  const size_t b_upd = al(update_bytes(p, k));
+  const size_t b_upd = al(std::max(update_bytes(p, k), p.raw ? update_bytes(raw_points(p), k) : (size_t)0));
   const size_t b_score = objective ? al(sizeof(float) * (size_t)p.n) : 0;
   const size_t b_xc = objective ? al(sizeof(float) * (size_t)p.n) : 0;
   const size_t b_part = objective ? al(sizeof(double) * (size_t)objective_blocks(p.n)) : 0;
@@ -395,7 +434,11 @@ km_status kmeans_fit(const km_points *P, int32_t k, int32_t iters, const int64_t
       if (objective)
         KMQ_STAGE(kStOther, launch_objective(p, xc, sc, p.n, objective + it, part, objective_blocks(p.n), s));
       if (it == iters) break;  // the last pass only assigns (the final STEP 2)
-      KMQ_STAGE(kStUpdate, launch_update(p, assign, k, C, nullptr, policy, wupd, s));
+      if (p.raw && it == iters - 1) {  // last update from the raw rows (Sec. 4.1)
+        KMQ_STAGE(kStUpdate, launch_update(raw_points(p), assign, k, C, nullptr, policy, wupd, s));
+      } else {
+        KMQ_STAGE(kStUpdate, launch_update(p, assign, k, C, nullptr, policy, wupd, s));
+      }
     }
 #undef KMQ_STAGE
     if (stats) {

@@ -625,7 +625,7 @@ __device__ __forceinline__ void load_stage8(const AssignArgs &A, int s, int64_t 
     if (FMT == KM_SQ8 || FMT == KM_BF16)
       R.p[i] = *reinterpret_cast<const uint4 *>(pbase8 + (uint32_t)(min(row, prmax) * (int)A.pild + bc));
   }
-  if (FMT == KM_SIGN1) {
+  if (FMT == KM_SIGN1 || FMT == KM_RABITQ) {
 #pragma unroll
     for (int i = 0; i < 2; ++i) {  // 256 rows x 4 words
       const int w = t + k8Threads * i;
@@ -637,10 +637,11 @@ __device__ __forceinline__ void load_stage8(const AssignArgs &A, int s, int64_t 
   if (s == 0) {  // per-centroid constants: threads t < kT8 (the others load a valid duplicate)
     const int64_t j = min<int64_t>(c0 + (t & (kT8 - 1)), A.k - 1);
     R.cpar[1] = FMT == KM_BF16 ? A.cp.cn[j] : __int_as_float(A.cp.qsum[j]);
-    if (FMT == KM_SIGN1) {
+    if (FMT == KM_SIGN1 || FMT == KM_RABITQ) {
       R.cpar[2] = A.cp.u[j];
       R.cpar[3] = A.cp.sig2[j];
     }
+    if (FMT == KM_RABITQ) R.cpar[0] = A.cp.cn[j];
   }
 }
 
@@ -661,7 +662,7 @@ __device__ __forceinline__ void store_stage8(const AssignArgs &A, int s, const S
       *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 16 * col) = mask4(flip4(R.p[i]), ok);
     if (FMT == KM_BF16) *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 16 * col) = mask4(R.p[i], ok);
   }
-  if (FMT == KM_SIGN1) {
+  if (FMT == KM_SIGN1 || FMT == KM_RABITQ) {
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int w = t + k8Threads * i;
@@ -677,7 +678,7 @@ __device__ __forceinline__ void store_stage8(const AssignArgs &A, int s, const S
   }
   if (s == 0 && t < kT8) {
 #pragma unroll
-    for (int q = 1; q < 4; ++q) cpar[q * kT8 + t] = R.cpar[q];
+    for (int q = (FMT == KM_RABITQ ? 0 : 1); q < 4; ++q) cpar[q * kT8 + t] = R.cpar[q];
   }
 }
 
@@ -746,9 +747,17 @@ __global__ __launch_bounds__(k8Threads, 1) void assign_i8_kernel(AssignArgs A) {
   const int total = nct * S;
 
   float al[k8PB] = {};
-  if (FMT == KM_SIGN1) {
+  int pop[k8PB] = {};
+  if (FMT == KM_SIGN1 || FMT == KM_RABITQ) {
 #pragma unroll
-    for (int pb = 0; pb < k8PB; ++pb) al[pb] = A.alpha[min<int64_t>(p0 + wp * 32 * k8PB + pb * 32 + r, A.n - 1)];
+    for (int pb = 0; pb < k8PB; ++pb) {
+      const int64_t p = min<int64_t>(p0 + wp * 32 * k8PB + pb * 32 + r, A.n - 1);
+      al[pb] = A.alpha[p];
+      if (FMT == KM_RABITQ) {  // the point's number of set bits
+        const uint32_t *row = A.pbits + p * A.pbw + A.pbw0;
+        for (int w = 0; w < A.di / 32; ++w) pop[pb] += __popc(row[w]);
+      }
+    }
   }
   constexpr bool BF = FMT == KM_BF16;
   Acc8<BF> acc[4][k8PB];
@@ -797,11 +806,12 @@ __global__ __launch_bounds__(k8Threads, 1) void assign_i8_kernel(AssignArgs A) {
       for (int i4 = 0; i4 < 4; ++i4) {
         const int cr = crow0 + 8 * i4;
         const f32x4 q4 = *reinterpret_cast<const f32x4 *>(&cp[kT8 + cr]);
-        f32x4 u4 = {0.f, 0.f, 0.f, 0.f}, s4 = {0.f, 0.f, 0.f, 0.f};
-        if constexpr (FMT == KM_SIGN1) {
+        f32x4 u4 = {0.f, 0.f, 0.f, 0.f}, s4 = {0.f, 0.f, 0.f, 0.f}, b4 = {0.f, 0.f, 0.f, 0.f};
+        if constexpr (FMT == KM_SIGN1 || FMT == KM_RABITQ) {
           u4 = *reinterpret_cast<const f32x4 *>(&cp[2 * kT8 + cr]);
           s4 = *reinterpret_cast<const f32x4 *>(&cp[3 * kT8 + cr]);
         }
+        if constexpr (FMT == KM_RABITQ) b4 = *reinterpret_cast<const f32x4 *>(&cp[cr]);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int i = 4 * i4 + e;
@@ -814,6 +824,10 @@ __global__ __launch_bounds__(k8Threads, 1) void assign_i8_kernel(AssignArgs A) {
               sc = __float_as_int(q4[e]) - 2 * acc[cb][pb][i];
             } else if constexpr (FMT == KM_BF16) {
               sc = fmaf(-2.0f, acc[cb][pb][i], q4[e]);  // ||c||^2 - 2<x,c>
+            } else if constexpr (FMT == KM_RABITQ) {  // Eq. 4-5, fp32 in the oracle's order
+              const int sd = 2 * acc[cb][pb][i] - __float_as_int(q4[e]);
+              const float inner = fmaf(s4[e], (float)sd, b4[e] * (float)(2 * pop[pb] - A.di));
+              sc = fmaf(-(2.0f * al[pb]), inner, u4[e]);
             } else {
               const int sd = 2 * acc[cb][pb][i] - __float_as_int(q4[e]);
               const float v = al[pb] * s4[e];
@@ -895,10 +909,14 @@ __device__ __forceinline__ i32x4 widen16(uint32_t hb) {
                (int)spread4((hb >> 12) & 15u)};
 }
 
+// FMT: KM_SIGN1 (symmetric int8 centroid codes) or KM_RABITQ (SQ4 centroid codes
+// with bias; the epilogue also needs each point's number of set bits).
+template <int FMT>
 __global__ __launch_bounds__(kBT, 1) void assign_bits_kernel(AssignArgs A) {
   __shared__ uint32_t bitsT[kBMaxWords * kBTP];  // 80 KB
   __shared__ __align__(16) uint8_t cst[2][kBStageBytes];
-  __shared__ float cparl[2][3 * kBTC];
+  __shared__ float cparl[2][4 * kBTC];
+  __shared__ int popl[kBTP];
   const int t = threadIdx.x;
   const int lane = t & 63, wave = t >> 6;
   const int r = lane & 31, h = lane >> 5;
@@ -909,10 +927,16 @@ __global__ __launch_bounds__(kBT, 1) void assign_bits_kernel(AssignArgs A) {
   const int total = nct * S;
   const int prmax = (int)min<int64_t>(A.n - 1 - p0, kBTP - 1);
 
-  // resident codes: thread t loads point t's words, 4 at a time when aligned
+  // resident codes: thread t loads point t's words (and counts its set bits)
   {
     const uint32_t *row = A.pbits + (p0 + min(t, prmax)) * A.pbw + A.pbw0;
-    for (int w = 0; w < W; ++w) bitsT[w * kBTP + t] = row[w];
+    int pc = 0;
+    for (int w = 0; w < W; ++w) {
+      const uint32_t v = row[w];
+      bitsT[w * kBTP + t] = v;
+      pc += __popc(v);
+    }
+    popl[t] = pc;
   }
   float al[2];
 #pragma unroll
@@ -920,7 +944,7 @@ __global__ __launch_bounds__(kBT, 1) void assign_bits_kernel(AssignArgs A) {
 
   // centroid stage loads: 128 rows x 8 chunks of 16 B = 2 chunks per thread
   uint4 cr[2];
-  float cpv[3] = {0.f, 0.f, 0.f};
+  float cpv[4] = {0.f, 0.f, 0.f, 0.f};
   auto load = [&](int ct, int s) {
     const int64_t c0 = (int64_t)ct * kBTC;
     const int crmax = (int)min<int64_t>(A.k - 1 - c0, kBTC - 1);
@@ -937,6 +961,7 @@ __global__ __launch_bounds__(kBT, 1) void assign_bits_kernel(AssignArgs A) {
       cpv[0] = __int_as_float(A.cp.qsum[j]);
       cpv[1] = A.cp.u[j];
       cpv[2] = A.cp.sig2[j];
+      if (FMT == KM_RABITQ) cpv[3] = A.cp.cn[j];
     }
   };
   auto store = [&](int ct, int s, uint8_t *buf) {
@@ -949,7 +974,7 @@ __global__ __launch_bounds__(kBT, 1) void assign_bits_kernel(AssignArgs A) {
     }
     if (s == 0 && t < kBTC) {
 #pragma unroll
-      for (int q = 0; q < 3; ++q) cparl[ct & 1][q * kBTC + t] = cpv[q];
+      for (int q = 0; q < 4; ++q) cparl[ct & 1][q * kBTC + t] = cpv[q];
     }
   };
 
@@ -959,6 +984,11 @@ __global__ __launch_bounds__(kBT, 1) void assign_bits_kernel(AssignArgs A) {
   load(0, 0);
   store(0, 0, cst[0]);
   __syncthreads();
+  int pop[2] = {0, 0};
+  if (FMT == KM_RABITQ) {
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb) pop[pb] = popl[wave * 64 + pb * 32 + r];
+  }
 
   for (int ct = 0; ct < nct; ++ct) {
     i32x16 acc[4][2];
@@ -1009,11 +1039,18 @@ __global__ __launch_bounds__(kBT, 1) void assign_bits_kernel(AssignArgs A) {
         const int qs = __float_as_int(cp[crow]);
         const float u = cp[kBTC + crow];
         const float s2 = cp[2 * kBTC + crow];
+        const float bj = cp[3 * kBTC + crow];
 #pragma unroll
         for (int pb = 0; pb < 2; ++pb) {
           const int sd = 2 * acc[cb][pb][i] - qs;
-          const float v = al[pb] * s2;
-          const float sc = fmaf(-v, (float)sd, u);
+          float sc;
+          if constexpr (FMT == KM_RABITQ) {  // Eq. 4-5: fp32 in the oracle's order
+            const float inner = fmaf(s2, (float)sd, bj * (float)(2 * pop[pb] - A.di));
+            sc = fmaf(-(2.0f * al[pb]), inner, u);
+          } else {
+            const float v = al[pb] * s2;
+            sc = fmaf(-v, (float)sd, u);
+          }
           if (live && sc < best[pb]) {
             best[pb] = sc;
             bidx[pb] = (int)j;
@@ -1086,6 +1123,52 @@ __global__ __launch_bounds__(256) void prep_kernel(const void *Cv, int k, int d,
       __syncthreads();
     }
     if (t == 0) qsum[j] = shi[0];
+  }
+  if (FMT == KM_RABITQ) {  // per-centroid SQ4 of the residual (Eq. 5): b = min, s = range / 15
+    const float *c = static_cast<const float *>(Cv) + (int64_t)j * d;
+    float lo = INFINITY, hi = -INFINITY;
+    double nn = 0.0;
+    for (int i = t; i < d; i += 256) {
+      lo = fminf(lo, c[i]);
+      hi = fmaxf(hi, c[i]);
+      nn += (double)c[i] * (double)c[i];
+    }
+    nn = block_sum_f64(nn, shd);
+    shf[t] = lo;
+    __syncthreads();
+    for (int st = 128; st > 0; st >>= 1) {
+      if (t < st) shf[t] = fminf(shf[t], shf[t + st]);
+      __syncthreads();
+    }
+    lo = shf[0];
+    __syncthreads();
+    shf[t] = hi;
+    __syncthreads();
+    for (int st = 128; st > 0; st >>= 1) {
+      if (t < st) shf[t] = fmaxf(shf[t], shf[t + st]);
+      __syncthreads();
+    }
+    hi = shf[0];
+    const float sc = hi > lo ? (hi - lo) / 15.0f : 1.0f;
+    int ts = 0;
+    for (int i = t; i < d; i += 256) {
+      const float v = fminf(fmaxf(rintf((c[i] - lo) / sc), 0.f), 15.f);
+      q[(int64_t)j * d + i] = (int8_t)(int)v;
+      ts += (int)v;
+    }
+    __syncthreads();
+    shi[t] = ts;
+    __syncthreads();
+    for (int st = 128; st > 0; st >>= 1) {
+      if (t < st) shi[t] += shi[t + st];
+      __syncthreads();
+    }
+    if (t == 0) {
+      qsum[j] = shi[0];
+      u[j] = (float)nn;
+      sig2[j] = sc;
+      cn[j] = lo;
+    }
   }
   if (FMT == KM_SIGN1 || FMT == KM_HYBRID) {
     const float *c = static_cast<const float *>(Cv) + (int64_t)j * d;
@@ -1179,7 +1262,7 @@ __global__ __launch_bounds__(256) void xconst_kernel(Points P, float *xc) {
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
   if (lane == 0) {
-    if (FMT == KM_SIGN1 || FMT == KM_HYBRID) {
+    if (is_bits_fmt(FMT)) {
       const double a = P.alpha[p];
       s += a * a * (double)(P.d - (FMT == KM_HYBRID ? P.d_front : 0));
     }
@@ -1235,7 +1318,7 @@ __global__ __launch_bounds__(256) void gather_kernel(Points P, const int64_t *id
         c[i] = P.front[row * d0 + i];
       } else {
         const float sg = ((b[i >> 5] >> (i & 31)) & 1u) ? a : -a;
-        c[i] = P.center[i] + sg;  // decoded point m + alpha (2b - 1)
+        c[i] = (P.center ? P.center[i] : 0.0f) + sg;  // decoded point m + alpha (2b - 1)
       }
     }
   }
@@ -1334,9 +1417,9 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
     A.cild = P.d - d0;
     A.di = P.d - d0;
   }
-  if constexpr (FMT == KM_SIGN1) {
+  if constexpr (FMT == KM_SIGN1 || FMT == KM_RABITQ) {
     if (P.d <= 32 * kBMaxWords) {
-      hipLaunchKernelGGL(assign_bits_kernel, dim3((unsigned)cdiv(P.n, kBTP)), dim3(kBT), 0, s, A);
+      hipLaunchKernelGGL(assign_bits_kernel<FMT>, dim3((unsigned)cdiv(P.n, kBTP)), dim3(kBT), 0, s, A);
     } else {
       hipLaunchKernelGGL(assign_i8_kernel<FMT>, dim3((unsigned)cdiv(P.n, kT8)), dim3(k8Threads), 0, s, A);
     }
@@ -1367,7 +1450,7 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
 // prep workspace: cn, qsum, u, sig2 (k each) | residual codes or bf16 rows | keys (n)
 static size_t prep_codes_bytes(const Points &P, int k) {
   const int d0 = P.fmt == KM_HYBRID ? P.d_front : 0;
-  if (P.fmt == KM_SIGN1 || P.fmt == KM_HYBRID) return (size_t)k * (size_t)(P.d - d0);
+  if (is_bits_fmt(P.fmt)) return (size_t)k * (size_t)(P.d - d0);
   if (P.fmt == KM_BF16) return 2 * (size_t)k * (size_t)P.d;
   return 0;
 }
@@ -1413,6 +1496,10 @@ km_status launch_prep(const Points &P, const void *C, int k, void *ws, CentroidP
       hipLaunchKernelGGL(prep_kernel<KM_SIGN1>, dim3(k), dim3(256), 0, s, C, k, P.d, 0, P.center, cn, qsum, u, sig2,
                          q, cb);
       break;
+    case KM_RABITQ:
+      hipLaunchKernelGGL(prep_kernel<KM_RABITQ>, dim3(k), dim3(256), 0, s, C, k, P.d, 0, nullptr, cn, qsum, u, sig2, q,
+                         cb);
+      break;
     case KM_HYBRID:
       hipLaunchKernelGGL(prep_kernel<KM_HYBRID>, dim3(k), dim3(256), 0, s, C, k, P.d, d0, P.center, cn, qsum, u,
                          sig2, q, cb);
@@ -1432,6 +1519,7 @@ km_status launch_assign(const Points &P, const void *C, const CentroidPrep &cp, 
     case KM_SQ8: return launch_assign_t<KM_SQ8>(P, C, cp, k, assign, score, s);
     case KM_SIGN1: return launch_assign_t<KM_SIGN1>(P, C, cp, k, assign, score, s);
     case KM_HYBRID: return launch_assign_t<KM_HYBRID>(P, C, cp, k, assign, score, s);
+    case KM_RABITQ: return launch_assign_t<KM_RABITQ>(P, C, cp, k, assign, score, s);
     default: return KM_EUNSUPPORTED;
   }
 }
@@ -1444,6 +1532,7 @@ km_status launch_xconst(const Points &P, float *xc, hipStream_t s) {
     case KM_SQ8: hipLaunchKernelGGL(xconst_kernel<KM_SQ8>, g, dim3(256), 0, s, P, xc); break;
     case KM_SIGN1: hipLaunchKernelGGL(xconst_kernel<KM_SIGN1>, g, dim3(256), 0, s, P, xc); break;
     case KM_HYBRID: hipLaunchKernelGGL(xconst_kernel<KM_HYBRID>, g, dim3(256), 0, s, P, xc); break;
+    case KM_RABITQ: hipLaunchKernelGGL(xconst_kernel<KM_RABITQ>, g, dim3(256), 0, s, P, xc); break;
     default: return KM_EUNSUPPORTED;
   }
   KMQ_LAUNCH_CHECK("xconst_kernel");
@@ -1469,6 +1558,7 @@ km_status launch_gather_init(const Points &P, const int64_t *idx, int k, void *C
     case KM_SQ8: hipLaunchKernelGGL(gather_kernel<KM_SQ8>, dim3(k), dim3(256), 0, s, P, idx, C); break;
     case KM_SIGN1: hipLaunchKernelGGL(gather_kernel<KM_SIGN1>, dim3(k), dim3(256), 0, s, P, idx, C); break;
     case KM_HYBRID: hipLaunchKernelGGL(gather_kernel<KM_HYBRID>, dim3(k), dim3(256), 0, s, P, idx, C); break;
+    case KM_RABITQ: hipLaunchKernelGGL(gather_kernel<KM_RABITQ>, dim3(k), dim3(256), 0, s, P, idx, C); break;
     default: return KM_EUNSUPPORTED;
   }
   KMQ_LAUNCH_CHECK("gather_kernel");

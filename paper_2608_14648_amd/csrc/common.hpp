@@ -28,15 +28,22 @@ struct Points {
   const float *center;
   const float *front;  // hybrid: n x d_front
   int d_front;
+  const float *raw;    // nullable: fp32 rows in the clustering space (last update of a fit)
+  int64_t raw_ld;
 };
+
+// 1-bit point formats (codes + one scale per point)
+__host__ __device__ constexpr bool is_bits_fmt(int fmt) {
+  return fmt == KM_SIGN1 || fmt == KM_HYBRID || fmt == KM_RABITQ;
+}
 
 // Per-centroid data rebuilt before each assignment pass.
 struct CentroidPrep {
-  const float *cn;     // F32/HYBRID: ||c'||^2 over the fp32 dims
-  const int *qsum;     // SQ8: ||c~||^2 ; SIGN1/HYBRID: T_j = sum q
-  const float *u;      // SIGN1/HYBRID: (sigma*sigma)*Q
-  const float *sig2;   // SIGN1/HYBRID: 2*sigma
-  const int8_t *q;     // SIGN1/HYBRID: int8 residual codes, k x dt
+  const float *cn;     // F32/HYBRID/BF16: ||c'||^2 over the fp32 dims; RABITQ: SQ4 bias b
+  const int *qsum;     // SQ8: ||c~||^2 ; SIGN1/HYBRID/RABITQ: T_j = sum q
+  const float *u;      // SIGN1/HYBRID: (sigma*sigma)*Q ; RABITQ: ||c||^2
+  const float *sig2;   // SIGN1/HYBRID: 2*sigma ; RABITQ: SQ4 scale s
+  const int8_t *q;     // SIGN1/HYBRID: int8 residual codes, k x dt ; RABITQ: SQ4 codes 0..15, k x d
   const uint16_t *cb;  // BF16: centroids rounded to bfloat16, k x d
   unsigned long long *keys;  // F32/HYBRID with centroid-tile groups: per-point (score, index) keys
 };
@@ -87,13 +94,16 @@ km_status launch_quantize(const float *X, int64_t n, int d, int64_t ldx, int fmt
                           hipStream_t s);
 
 size_t colmean_bytes(int64_t n, int d);
+size_t rabitq_encode_bytes(int64_t n, int d);
+km_status launch_rabitq_encode(const float *X, int64_t n, int d, int64_t ldx, const float *P, float *m,
+                               uint32_t *bits, float *alpha, int flags, void *ws, hipStream_t s);
 km_status launch_colmean(const float *X, int64_t n, int d, int64_t ldx, float *m, void *ws, hipStream_t s);
 
 // pca.hip
 size_t pca_cov_bytes(int64_t n, int d);
 km_status launch_pca_cov(const float *X, int64_t n, int d, float *mean, float *cov, void *ws,
                          hipStream_t s);
-km_status launch_pca_project(const float *X, int64_t n, int d, const float *mean, const float *W,
+km_status launch_pca_project(const float *X, int64_t n, int d, int64_t ldx, const float *mean, const float *W,
                              int d_out, float *Y, void *ws, hipStream_t s);
 size_t pca_project_bytes(int d, int d_out);
 

@@ -171,9 +171,9 @@ constexpr int kPStride = 32 + 4;  // floats per LDS row of a projection stage
 // Workgroups are numbered so that the output tiles of one point tile land on the
 // same XCD one after another (consecutive ids are spread over the 8 XCDs), so the
 // point rows come from HBM once and from that XCD's L2 for the other tiles.
-__global__ __launch_bounds__(256) void project_kernel(const float *X, int64_t n, int d, const float *mean,
-                                                      const float *Wt, int d_out, float *Y, int n_ptiles,
-                                                      int n_otiles) {
+__global__ __launch_bounds__(256) void project_kernel(const float *X, int64_t n, int d, int64_t ldx,
+                                                      const float *mean, const float *Wt, int d_out, float *Y,
+                                                      int n_ptiles, int n_otiles) {
   __shared__ float Xs[2][kT * kPStride];
   __shared__ float Ws[2][kT * kPStride];
   const int64_t b = blockIdx.x;
@@ -206,7 +206,7 @@ __global__ __launch_bounds__(256) void project_kernel(const float *X, int64_t n,
       const int row = idx >> 3, c4 = idx & 7;
       const int dim = 32 * st + 4 * c4;
       const int dimc = dim < d ? dim : 0;
-      rx[q] = *reinterpret_cast<const f32x4 *>(X + (p0 + min(row, prmax)) * (int64_t)d + dimc);
+      rx[q] = *reinterpret_cast<const f32x4 *>(X + (p0 + min(row, prmax)) * ldx + dimc);
       rw[q] = *reinterpret_cast<const f32x4 *>(Wt + (int64_t)(o0 + min(row, ormax)) * d + dimc);
     }
   };
@@ -320,15 +320,15 @@ km_status launch_pca_cov(const float *X, int64_t n, int d, float *mean, float *c
 
 size_t pca_project_bytes(int d, int d_out) { return (size_t)d * d_out * sizeof(float) + 256; }
 
-km_status launch_pca_project(const float *X, int64_t n, int d, const float *mean, const float *W, int d_out, float *Y,
-                             void *ws, hipStream_t s) {
+km_status launch_pca_project(const float *X, int64_t n, int d, int64_t ldx, const float *mean, const float *W,
+                             int d_out, float *Y, void *ws, hipStream_t s) {
   float *Wt = static_cast<float *>(ws);
   const int64_t e = (int64_t)d * d_out;
   hipLaunchKernelGGL(transpose_kernel, dim3((unsigned)cdiv(e, 256)), dim3(256), 0, s, W, d, d_out, Wt);
   const int n_ptiles = (int)cdiv(n, kT), n_otiles = (int)cdiv(d_out, kT);
   const int64_t nblk = cdiv(n_ptiles, 8) * 8 * n_otiles;
-  hipLaunchKernelGGL(project_kernel, dim3((unsigned)nblk), dim3(256), 0, s, X, n, d, mean, Wt, d_out, Y, n_ptiles,
-                     n_otiles);
+  hipLaunchKernelGGL(project_kernel, dim3((unsigned)nblk), dim3(256), 0, s, X, n, d, ldx, mean, Wt, d_out, Y,
+                     n_ptiles, n_otiles);
   KMQ_LAUNCH_CHECK("pca_project");
   return KM_OK;
 }

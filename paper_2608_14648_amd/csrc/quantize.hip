@@ -177,6 +177,11 @@ __global__ __launch_bounds__(256) void sign1_encode_kernel(const float *X, int64
   if (lane == 0) alpha[row] = s1 > 0.0 ? (float)(s2 / s1) : 0.0f;
 }
 
+__global__ __launch_bounds__(256) void fill_zero_kernel(float *v, int n) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i < n) v[i] = 0.0f;
+}
+
 }  // namespace
 
 constexpr int kMaxSumBlocks = 1024;
@@ -201,6 +206,36 @@ size_t quantize_bytes(int64_t n, int d, int fmt) {
   const int64_t nb = cdiv(n, kRowsPerBlock);
   if (fmt == KM_SQ8) return (size_t)nb * d * 2 * sizeof(float) + (size_t)d * sizeof(float) + 512;
   return colmean_bytes(n, d);
+}
+
+static size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// workspace: column-mean partials | transposed P | rotated rows y (n x d) | zero centre (d)
+size_t rabitq_encode_bytes(int64_t n, int d) {
+  return al256(colmean_bytes(n, d)) + al256(pca_project_bytes(d, d)) + al256((size_t)n * d * sizeof(float)) +
+         al256((size_t)d * sizeof(float));
+}
+
+// RabitQ codes (Sec. 3.1): centre (column mean when fitting), rotate with the
+// projection kernel, then sign bits and alpha of the rotated residual (centre 0).
+km_status launch_rabitq_encode(const float *X, int64_t n, int d, int64_t ldx, const float *P, float *m,
+                               uint32_t *bits, float *alpha, int flags, void *ws, hipStream_t s) {
+  uint8_t *w = static_cast<uint8_t *>(ws);
+  void *wmean = w;
+  void *wproj = w + al256(colmean_bytes(n, d));
+  float *Y = reinterpret_cast<float *>(w + al256(colmean_bytes(n, d)) + al256(pca_project_bytes(d, d)));
+  float *zero = Y + ((al256((size_t)n * d * sizeof(float))) / sizeof(float));
+  if (flags & KM_Q_FIT_PARAMS) {
+    km_status st = launch_colmean(X, n, d, ldx, m, wmean, s);
+    if (st != KM_OK) return st;
+  }
+  km_status st = launch_pca_project(X, n, d, ldx, m, P, d, Y, wproj, s);
+  if (st != KM_OK) return st;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)cdiv(d, 256)), dim3(256), 0, s, zero, d);
+  hipLaunchKernelGGL(sign1_encode_kernel, dim3((unsigned)cdiv(n, 4)), dim3(256), 0, s, Y, n, d, (int64_t)d, zero, 0,
+                     bits, alpha, nullptr);
+  KMQ_LAUNCH_CHECK("rabitq encode");
+  return KM_OK;
 }
 
 km_status launch_quantize(const float *X, int64_t n, int d, int64_t ldx, int fmt, void *codes, float *params,

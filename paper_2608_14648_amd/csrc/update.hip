@@ -593,7 +593,8 @@ __global__ __launch_bounds__(256) void compose_kernel(const void *Zv, int k, int
   } else {
     const float z = static_cast<const float *>(Zv)[(int64_t)j * d + col];
     const bool bitdim = (FMT == KM_SIGN1 || FMT == KM_HYBRID) && col >= d0;
-    static_cast<float *>(Cv)[(int64_t)j * d + col] = bitdim ? m[col] + z : z;
+    // (RabitQ centroids live in the rotated residual space: centre 0, composed as SIGN1 with m = NULL)
+    static_cast<float *>(Cv)[(int64_t)j * d + col] = bitdim ? (m ? m[col] : 0.0f) + z : z;
   }
 }
 
@@ -650,7 +651,7 @@ km_status launch_update(const Points &P, const int32_t *assign, int k, void *C, 
     if (df > 0)
       hipLaunchKernelGGL(segsum_f32_kernel, dim3(w.maxchunks, (unsigned)cdiv(df, 256)), dim3(256), 0, s, F, fld, df,
                          w.perm, w.cnt, w.cstart, w.choff, k, static_cast<float *>(w.partial), w.dp);
-    if (P.fmt == KM_SIGN1 || P.fmt == KM_HYBRID) {
+    if (is_bits_fmt(P.fmt)) {
       const int d0 = P.fmt == KM_HYBRID ? P.d_front : 0;
       const int dt = d - d0;
       hipLaunchKernelGGL(segsum_bits_kernel, dim3(w.maxchunks, (unsigned)cdiv(dt, 1024)), dim3(256), 0, s,
@@ -677,7 +678,8 @@ km_status launch_update(const Points &P, const int32_t *assign, int k, void *C, 
     case KM_F32:
     case KM_BF16: hipLaunchKernelGGL(compose_kernel<KM_F32>, g, dim3(256), 0, s, w.Z, k, d, d0, P.center, w.fresh, w.cnt, C, counts); break;
     case KM_SQ8: hipLaunchKernelGGL(compose_kernel<KM_SQ8>, g, dim3(256), 0, s, w.Z, k, d, d0, P.center, w.fresh, w.cnt, C, counts); break;
-    case KM_SIGN1: hipLaunchKernelGGL(compose_kernel<KM_SIGN1>, g, dim3(256), 0, s, w.Z, k, d, d0, P.center, w.fresh, w.cnt, C, counts); break;
+    case KM_SIGN1:
+    case KM_RABITQ: hipLaunchKernelGGL(compose_kernel<KM_SIGN1>, g, dim3(256), 0, s, w.Z, k, d, d0, P.center, w.fresh, w.cnt, C, counts); break;
     case KM_HYBRID: hipLaunchKernelGGL(compose_kernel<KM_HYBRID>, g, dim3(256), 0, s, w.Z, k, d, d0, P.center, w.fresh, w.cnt, C, counts); break;
     default: return KM_EUNSUPPORTED;
   }

@@ -54,10 +54,10 @@ def kmq():
 
 def _pts(kmq, **kw):
     base = dict(fmt=kmq.KM_F32, d=128, n=100, data=0x1000, ld=128, alpha=None, center=None, front=None, d_front=0,
-                reserved=0)
+                reserved=0, raw=None, raw_ld=0)
     base.update(kw)
     return kmq.KmPoints(base["fmt"], base["d"], base["n"], base["data"], base["ld"], base["alpha"], base["center"],
-                        base["front"], base["d_front"], base["reserved"])
+                        base["front"], base["d_front"], base["reserved"], base["raw"], base["raw_ld"])
 
 
 FAKE = ct.c_void_p(0x10000)  # never dereferenced: validation fails first
@@ -83,6 +83,12 @@ FAKE = ct.c_void_p(0x10000)  # never dereferenced: validation fails first
     (dict(fmt=4, d=128, alpha=0x2000, center=0x3000, front=0x4000, d_front=48), -1, "d_front"),
     (dict(fmt=4, d=128, alpha=0x2000, center=0x3000, front=None, d_front=64), -1, "front"),
     (dict(fmt=0, d_front=32), -1, "d_front"),
+    (dict(fmt=5, d=128, alpha=0x2000, center=0x3000), -1, "center must be NULL"),
+    (dict(fmt=5, d=100, alpha=0x2000), -1, "d % 32"),
+    (dict(fmt=5, d=128, alpha=None), -1, "alpha"),
+    (dict(fmt=2, d=128, ld=128, raw=0x5000, raw_ld=128), -1, "not allowed for SQ8"),
+    (dict(fmt=5, d=128, alpha=0x2000, raw=0x5004, raw_ld=128), -1, "raw rows"),
+    (dict(fmt=5, d=128, alpha=0x2000, raw=0x5000, raw_ld=64), -1, "raw rows"),
 ])
 def test_points_validation(kmq, kw, status, msg):
     L = kmq.lib()
@@ -114,6 +120,23 @@ def test_entry_point_argument_checks(kmq):
     assert L.kmeans_fit(ct.byref(P), 4, 3, oob, FAKE, FAKE, None, 0, None, None) == -1
     neg = (ct.c_int64 * 4)(0, -1, 2, 7)
     assert L.kmeans_fit(ct.byref(P), 4, 3, neg, FAKE, FAKE, None, 0, None, None) == -1
+
+
+def test_rabitq_encode_argument_checks(kmq):
+    L = kmq.lib()
+    ok = (FAKE, 10, 64, 64, FAKE, FAKE, FAKE, FAKE, 1, None)
+    bad = [
+        ((None,) + ok[1:], "NULL"),
+        (ok[:2] + (48, 48) + ok[4:], "d % 32"),
+        (ok[:3] + (60,) + ok[4:], "ldx"),
+        (ok[:4] + (None,) + ok[5:], "NULL"),
+        ((ct.c_void_p(0x10004),) + ok[1:], "aligned"),
+        (ok[:8] + (4,) + ok[9:], "flags"),
+        (ok[:1] + (0,) + ok[2:], "n ="),
+    ]
+    for args, msg in bad:
+        assert L.rabitq_encode(*args) == -1, msg
+        assert msg in L.km_last_error().decode(), (msg, L.km_last_error())
 
 
 def test_quantize_and_pca_argument_checks(kmq):
