@@ -13,7 +13,9 @@ iterations per second over the whole step (20 fp32 + 20 SQ8 iterations).
 
 Other workloads (--workload 1|3|4|5) time the other configurations for
 measurement; they are not the headline line.  --workload 6 runs the default
-workload's data stored as bfloat16.
+workload's data stored as bfloat16; --workload 7 runs the 1-bit workload's data
+through the paper's RabitQ pipeline (random rotation, SQ4 centroid codes with
+bias, last update from the raw rotated rows).
 
 After the timed region, `quality` reports each final partition's full-precision
 cost (raw-vector member means), its cluster-size spread and, for the compressed
@@ -329,6 +331,53 @@ def workload_sign1(cfg, torch, km, args):
     return step, finish, None, quality
 
 
+def workload_rabitq(cfg, torch, km, args):
+    """The 1M x 1024, k=1024 mixture through the paper's RabitQ pipeline: centre, random
+    rotation, 1-bit codes; SQ4 centroid codes; last update from the rotated raw rows."""
+    spec = cfg["spec"] if args.n is None else cfg["spec"].with_n(args.n)
+    k, T = cfg["k"], cfg["iters"]
+    import synth
+    log(f"generating {spec.n} x {spec.d} mixture")
+    X = upload(spec, torch)
+    idx = synth.init_indices(spec.n, k)
+    rot = torch.from_numpy(synth.random_rotation(spec.d)).cuda()
+    mu = torch.empty((k, spec.d), dtype=torch.float32, device="cuda")
+
+    def step(timer):
+        bits, m, alpha, Y = km.rabitq_encode(X, rot, want_rotated=True)
+        st = km.KmFitStats()
+        C, a, J = km.kmeans_fit(km.points_rabitq(bits, alpha, spec.d, raw=Y), k, T, idx, stats=st)
+        km.kmeans_update(km.points_f32(X), a, mu, km.KM_EMPTY_KEEP, counts=False)
+        cost = km.kmeans_cost(X, mu, a)
+        if timer is not None:
+            timer.add("rabitq", st)
+        return {"rabitq": cost, "a": a, "bits": bits, "alpha": alpha}, J
+
+    def finish(out, timer, elapsed, K):
+        s = timer.stats["rabitq"]
+        a_ms = s["assign_ms"] / s["assign_passes"]
+        ops = 2.0 * spec.n * k * spec.d
+        ach = ops / (a_ms * 1e-3) / 1e12
+        return {"value": T * K / elapsed, "unit": "Lloyd iters/s", "dtype": "i8",
+                "config": {"workload": "gmm1m_d1024_k1024_rabitq", "N": spec.n, "d": spec.d, "k": k, "iters": T,
+                           "formats": ["rabitq"], "raw_last_update": True},
+                "distances_per_s": (T + 1) * spec.n * k * K / elapsed,
+                "partition_cost": {"rabitq": float(out["rabitq"].item())},
+                "roofline": {"bound": "mfma", "kernel": "assign_bits_kernel<rabitq>", "achieved": ach,
+                             "peak": PEAK["int8_mfma_tops"], "unit": "TOP/s", "frac": ach / PEAK["int8_mfma_tops"],
+                             "traffic": None, "avg_launch_ms": a_ms},
+                "stages": {"rabitq": stage_summary(s)}}
+
+    def quality(out):
+        q = quality_vs_f32(km, X, k, T, idx, mu, "rabitq", out["a"])
+        _, a2, _ = km.kmeans_fit(km.points_rabitq(out["bits"], out["alpha"], spec.d), k, T, idx, objective=False)
+        q["rabitq_codes_only"] = partition_stats(km, X, a2, mu)
+        q["objective_ratio_rabitq_codes_only_vs_f32"] = q["rabitq_codes_only"]["cost"] / q["f32"]["cost"]
+        return q
+
+    return step, finish, None, quality
+
+
 def workload_pca(cfg, torch, km, args):
     spec = cfg["spec"] if args.n is None else cfg["spec"].with_n(args.n)
     k, T, dout = cfg["k"], cfg["iters"], cfg["d_out"]
@@ -442,8 +491,8 @@ def workload_c1(cfg, torch, km, args):
 
 
 WORKLOADS = {1: workload_c1, 2: workload_c2, 3: workload_sign1, 4: workload_pca, 5: workload_hybrid,
-             6: workload_bf16}
-CONFIG_OF = {6: 2}  # measurement-only workloads and the configuration whose data they use
+             6: workload_bf16, 7: workload_rabitq}
+CONFIG_OF = {6: 2, 7: 3}  # measurement-only workloads and the configuration whose data they use
 
 
 def main():

@@ -133,10 +133,11 @@ km_status quantize(const float *X, int64_t n, int32_t d, int64_t ldx, int32_t fm
  *   caller draws it; the library does not check orthogonality); m: float[d], the
  *   centre: computed as the column mean (fp64 sums) when flags & KM_Q_FIT_PARAMS,
  *   else an input.  bits: uint32[n][d/32]; alpha: float[n].  d % 32 == 0.
- *   Scratch: the rotated rows (n x d floats) for the duration of the call.
+ *   Y (nullable): float[n][d], receives the rotated residual rows y (the raw rows
+ *   of a kmeans_fit last update); when NULL they live in scratch for the call.
  */
 km_status rabitq_encode(const float *X, int64_t n, int32_t d, int64_t ldx, const float *P, float *m,
-                        uint32_t *bits, float *alpha, int32_t flags, km_stream stream);
+                        uint32_t *bits, float *alpha, float *Y, int32_t flags, km_stream stream);
 
 /*
  * pca_fit_cov -- PCA statistics (Sec. 3.1 PCA; Sec. 4.2): mean = float[d] column

@@ -58,7 +58,7 @@ def lib():
         vp, i32, i64 = ct.c_void_p, ct.c_int32, ct.c_int64
         sig = {
             "quantize": [vp, i64, i32, i64, i32, vp, vp, vp, i32, vp, i32, vp],
-            "rabitq_encode": [vp, i64, i32, i64, vp, vp, vp, vp, i32, vp],
+            "rabitq_encode": [vp, i64, i32, i64, vp, vp, vp, vp, vp, i32, vp],
             "pca_fit_cov": [vp, i64, i32, vp, vp, vp],
             "pca_project": [vp, i64, i32, vp, vp, i32, vp, vp],
             "kmeans_assign": [ct.POINTER(KmPoints), vp, i32, vp, vp, vp, vp],
@@ -208,10 +208,11 @@ def quantize_sq8(X: torch.Tensor, params: torch.Tensor | None = None):
     return codes, params
 
 
-def rabitq_encode(X: torch.Tensor, rotation: torch.Tensor, center: torch.Tensor | None = None):
-    """RabitQ codes of X: (bits int32 n x d/32, centre m, alpha).  rotation: float32
-    d x d orthogonal P (row-major); the codes are of (X - m) P.  Fits m (column mean)
-    unless given."""
+def rabitq_encode(X: torch.Tensor, rotation: torch.Tensor, center: torch.Tensor | None = None,
+                  want_rotated: bool = False):
+    """RabitQ codes of X: (bits int32 n x d/32, centre m, alpha, rotated rows or None).
+    rotation: float32 d x d orthogonal P (row-major); the codes are of (X - m) P.  Fits
+    m (column mean) unless given; want_rotated also returns y = (X - m) P (n x d)."""
     _dev(X, torch.float32, "X", 2)
     _dev(rotation, torch.float32, "rotation", 2)
     n, d = X.shape
@@ -225,9 +226,10 @@ def rabitq_encode(X: torch.Tensor, rotation: torch.Tensor, center: torch.Tensor 
         flags = KM_Q_FIT_PARAMS
     else:
         _dev(center, torch.float32, "center", 1)
+    Y = torch.empty((n, d), dtype=torch.float32, device=X.device) if want_rotated else None
     _check(lib().rabitq_encode(_ptr(X), n, d, X.stride(0), _ptr(rotation), _ptr(center), _ptr(bits), _ptr(alpha),
-                               flags, _stream()))
-    return bits, center, alpha
+                               _ptr(Y), flags, _stream()))
+    return bits, center, alpha, Y
 
 
 def quantize_bf16(X: torch.Tensor) -> torch.Tensor:

@@ -247,20 +247,21 @@ km_status pca_project(const float *X, int64_t n, int32_t d, const float *mean, c
 }
 
 km_status rabitq_encode(const float *X, int64_t n, int32_t d, int64_t ldx, const float *P, float *m, uint32_t *bits,
-                        float *alpha, int32_t flags, km_stream stream) {
+                        float *alpha, float *Y, int32_t flags, km_stream stream) {
   g_err[0] = 0;
   KMQ_CHECK(X != nullptr && P != nullptr && m != nullptr && bits != nullptr && alpha != nullptr, KM_EINVAL,
             "NULL argument");
   KMQ_CHECK(n >= 1 && n < (int64_t)INT32_MAX, KM_EINVAL, "n = %lld outside [1, 2^31)", (long long)n);
   KMQ_CHECK(d >= 32 && d % 32 == 0, KM_EINVAL, "rabitq_encode needs d %% 32 == 0 (d = %d)", d);
   KMQ_CHECK(ldx >= d && ldx % 4 == 0, KM_EINVAL, "need ldx >= d and ldx %% 4 == 0");
-  KMQ_CHECK(aligned16(X) && aligned16(m), KM_EINVAL, "X and m must be 16-byte aligned");
+  KMQ_CHECK(aligned16(X) && aligned16(m) && (Y == nullptr || aligned16(Y)), KM_EINVAL,
+            "X, m and Y must be 16-byte aligned");
   KMQ_CHECK((flags & ~KM_Q_FIT_PARAMS) == 0, KM_EINVAL, "unknown flags 0x%x", flags);
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   Scratch ws(s);
-  km_status st = ws.alloc(rabitq_encode_bytes(n, d));
+  km_status st = ws.alloc(rabitq_encode_bytes(n, d, Y != nullptr));
   if (st != KM_OK) return st;
-  return launch_rabitq_encode(X, n, d, ldx, P, m, bits, alpha, flags, ws.get(), s);
+  return launch_rabitq_encode(X, n, d, ldx, P, m, bits, alpha, Y, flags, ws.get(), s);
 }
 
 km_status kmeans_assign(const km_points *P, const void *C, int32_t k, int32_t *assign, float *score,

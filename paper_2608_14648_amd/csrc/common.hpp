@@ -94,9 +94,9 @@ km_status launch_quantize(const float *X, int64_t n, int d, int64_t ldx, int fmt
                           hipStream_t s);
 
 size_t colmean_bytes(int64_t n, int d);
-size_t rabitq_encode_bytes(int64_t n, int d);
+size_t rabitq_encode_bytes(int64_t n, int d, bool y_given);
 km_status launch_rabitq_encode(const float *X, int64_t n, int d, int64_t ldx, const float *P, float *m,
-                               uint32_t *bits, float *alpha, int flags, void *ws, hipStream_t s);
+                               uint32_t *bits, float *alpha, float *Y, int flags, void *ws, hipStream_t s);
 km_status launch_colmean(const float *X, int64_t n, int d, int64_t ldx, float *m, void *ws, hipStream_t s);
 
 // pca.hip

@@ -210,21 +210,22 @@ size_t quantize_bytes(int64_t n, int d, int fmt) {
 
 static size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// workspace: column-mean partials | transposed P | rotated rows y (n x d) | zero centre (d)
-size_t rabitq_encode_bytes(int64_t n, int d) {
-  return al256(colmean_bytes(n, d)) + al256(pca_project_bytes(d, d)) + al256((size_t)n * d * sizeof(float)) +
-         al256((size_t)d * sizeof(float));
+// workspace: column-mean partials | transposed P | zero centre (d) | rotated rows y
+// (n x d, only when the caller does not take them)
+size_t rabitq_encode_bytes(int64_t n, int d, bool y_given) {
+  return al256(colmean_bytes(n, d)) + al256(pca_project_bytes(d, d)) + al256((size_t)d * sizeof(float)) +
+         (y_given ? 0 : al256((size_t)n * d * sizeof(float)));
 }
 
 // RabitQ codes (Sec. 3.1): centre (column mean when fitting), rotate with the
 // projection kernel, then sign bits and alpha of the rotated residual (centre 0).
 km_status launch_rabitq_encode(const float *X, int64_t n, int d, int64_t ldx, const float *P, float *m,
-                               uint32_t *bits, float *alpha, int flags, void *ws, hipStream_t s) {
+                               uint32_t *bits, float *alpha, float *Y, int flags, void *ws, hipStream_t s) {
   uint8_t *w = static_cast<uint8_t *>(ws);
   void *wmean = w;
   void *wproj = w + al256(colmean_bytes(n, d));
-  float *Y = reinterpret_cast<float *>(w + al256(colmean_bytes(n, d)) + al256(pca_project_bytes(d, d)));
-  float *zero = Y + ((al256((size_t)n * d * sizeof(float))) / sizeof(float));
+  float *zero = reinterpret_cast<float *>(w + al256(colmean_bytes(n, d)) + al256(pca_project_bytes(d, d)));
+  if (Y == nullptr) Y = zero + al256((size_t)d * sizeof(float)) / sizeof(float);
   if (flags & KM_Q_FIT_PARAMS) {
     km_status st = launch_colmean(X, n, d, ldx, m, wmean, s);
     if (st != KM_OK) return st;

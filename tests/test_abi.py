@@ -124,14 +124,15 @@ def test_entry_point_argument_checks(kmq):
 
 def test_rabitq_encode_argument_checks(kmq):
     L = kmq.lib()
-    ok = (FAKE, 10, 64, 64, FAKE, FAKE, FAKE, FAKE, 1, None)
+    ok = (FAKE, 10, 64, 64, FAKE, FAKE, FAKE, FAKE, None, 1, None)
     bad = [
         ((None,) + ok[1:], "NULL"),
         (ok[:2] + (48, 48) + ok[4:], "d % 32"),
         (ok[:3] + (60,) + ok[4:], "ldx"),
         (ok[:4] + (None,) + ok[5:], "NULL"),
         ((ct.c_void_p(0x10004),) + ok[1:], "aligned"),
-        (ok[:8] + (4,) + ok[9:], "flags"),
+        (ok[:9] + (4,) + ok[10:], "flags"),
+        (ok[:8] + (ct.c_void_p(0x10008),) + ok[9:], "aligned"),
         (ok[:1] + (0,) + ok[2:], "n ="),
     ]
     for args, msg in bad:

@@ -51,8 +51,12 @@ def test_rabitq_encode(km, torch, n, d):
     say(f"rabitq encode n={n} d={d}")
     X = blobs(n, d, 5, seed=n + d)
     m, P, Y, bits_o, alpha_o = rotated(X, seed=d)
-    bits, mg, alpha = km.rabitq_encode(to_dev(X, torch), to_dev(P, torch), center=to_dev(m, torch))
+    bits, mg, alpha, Yg = km.rabitq_encode(to_dev(X, torch), to_dev(P, torch), center=to_dev(m, torch),
+                                           want_rotated=True)
     torch.cuda.synchronize()
+    # fp32 dot products of length d: error bounded relative to the row norm ||x - m||
+    rn = np.linalg.norm(X.astype(np.float64) - m.astype(np.float64), axis=1, keepdims=True)
+    assert (np.abs(host(Yg).astype(np.float64) - Y) <= 2e-6 * rn + 1e-12).all()
     # the GPU rotation (fp32 MFMA) and the oracle's (fp64 sums) differ by rounding:
     # signs may differ only where a rotated coordinate is within rounding of 0
     diff = unpack_bits(host(bits).view(np.uint32), d) != unpack_bits(bits_o, d)
@@ -60,7 +64,7 @@ def test_rabitq_encode(km, torch, n, d):
     assert (np.abs(Y)[diff] <= 1e-5 * np.broadcast_to(scale, Y.shape)[diff]).all()
     np.testing.assert_allclose(host(alpha), alpha_o, rtol=2e-5, atol=1e-7)
     # fitted centre: the column mean
-    _, m2, _ = km.rabitq_encode(to_dev(X, torch), to_dev(P, torch))
+    _, m2, _, _ = km.rabitq_encode(to_dev(X, torch), to_dev(P, torch))
     torch.cuda.synchronize()
     np.testing.assert_allclose(host(m2), m, rtol=2e-7, atol=1e-9)
 
