@@ -63,6 +63,10 @@ def lib():
             "orc_rabitq_prep": [_f32p, _i32, _i32, _i8p, _f32p, _f32p, _i32p, _f32p],
             "orc_assign_rabitq": [_u32p, _f32p, _i64, _i32, _i8p, _f32p, _f32p, _i32p, _f32p, _i32, _i32p, _f32p,
                                   _f64p],
+            "orc_lvq4_encode": [_f32p, _i64, _i32, _u8p, _f32p],
+            "orc_lvq4_decode": [_u8p, _f32p, _i64, _i32, _f32p],
+            "orc_assign_lvq4": [_u8p, _f32p, _i64, _i32, _u8p, _f32p, _i32p, _i32, _i32p, _f32p, _f64p],
+            "orc_update_lvq4": [_u8p, _f32p, _i64, _i32, _i32p, _i32, _f32p, _i64p, _i32],
             "orc_assign_hybrid": [_f32p, _u32p, _f32p, _i64, _i32, _i32, _f32p, _i8p, _f32p, _i32p, _f32p,
                                   _i32, _i32p, _f64p],
             "orc_update_f32": [_f32p, _i64, _i32, _i64, _i32p, _i32, _f32p, _i64p, _i32],
@@ -281,6 +285,43 @@ def assign_rabitq(bits, alpha, C):
     return a, score, dist
 
 
+def lvq4_encode(X):
+    """LVQ4 codes (uint8 n x d, one code per byte) and per-vector (s, b, A, N), float n x 4."""
+    X = _c(X, np.float32)
+    n, d = X.shape
+    codes = np.empty((n, d), np.uint8)
+    par = np.empty((n, 4), np.float32)
+    lib().orc_lvq4_encode(X, n, d, codes, par)
+    return codes, par
+
+
+def lvq4_decode(codes, par):
+    codes = _c(codes, np.uint8)
+    n, d = codes.shape
+    out = np.empty((n, d), np.float32)
+    lib().orc_lvq4_decode(codes, _c(par, np.float32), n, d, out)
+    return out
+
+
+def lvq4_pack(codes):
+    """Two 4-bit codes per byte: dim 2i in the low nibble, dim 2i+1 in the high one."""
+    codes = np.asarray(codes, dtype=np.uint8)
+    return np.ascontiguousarray(codes[:, 0::2] | (codes[:, 1::2] << 4))
+
+
+def assign_lvq4(codes, par, C):
+    """Points as LVQ4 codes; centroids C (fp32) coded with LVQ4 for the pass."""
+    codes = _c(codes, np.uint8)
+    n, d = codes.shape
+    yc, ypar = lvq4_encode(C)
+    yS = yc.astype(np.int32).sum(1).astype(np.int32)
+    a = np.empty(n, np.int32)
+    score = np.empty(n, np.float32)
+    dist = np.empty(n, np.float64)
+    lib().orc_assign_lvq4(codes, _c(par, np.float32), n, d, yc, ypar, yS, len(C), a, score, dist)
+    return a, score, dist
+
+
 def assign_hybrid(front, bits, alpha, C, m, d0: int):
     front = _c(front, np.float32)
     bits = _c(bits, np.uint32)
@@ -310,6 +351,15 @@ def update_f32(X, a, k: int, C_old, policy: int = EMPTY_SPLIT):
 def update_bf16(codes, a, k: int, C_old, policy: int = EMPTY_SPLIT):
     """bfloat16 points: fp32 centroids = mean of the stored (decoded) member values."""
     return update_f32(bf16_decode(codes), a, k, C_old, policy)
+
+
+def update_lvq4(codes, par, a, k: int, C_old, policy: int = EMPTY_SPLIT):
+    codes = _c(codes, np.uint8)
+    n, d = codes.shape
+    C = np.array(C_old, dtype=np.float32, copy=True, order="C")
+    counts = np.empty(k, np.int64)
+    lib().orc_update_lvq4(codes, _c(par, np.float32), n, d, _c(a, np.int32), k, C, counts, policy)
+    return C, counts
 
 
 def update_sq8(codes, a, k: int, C_old, policy: int = EMPTY_SPLIT):
@@ -369,6 +419,8 @@ def init_centroids(P: dict, idx):
         return sign1_decode(P["bits"][idx], P["alpha"][idx], P["d"], P["m"], 0)
     if fmt == "rabitq":
         return sign1_decode(P["bits"][idx], P["alpha"][idx], P["d"], np.zeros(P["d"], np.float32), 0)
+    if fmt == "lvq4":
+        return lvq4_decode(P["codes"][idx], P["par"][idx])
     if fmt == "hybrid":
         d0 = P["d0"]
         C = sign1_decode(P["bits"][idx], P["alpha"][idx], P["d"], P["m"], d0)
@@ -392,6 +444,9 @@ def assign(P: dict, C):
     if fmt == "rabitq":
         a, _, dist = assign_rabitq(P["bits"], P["alpha"], C)
         return a, dist
+    if fmt == "lvq4":
+        a, _, dist = assign_lvq4(P["codes"], P["par"], C)
+        return a, dist
     if fmt == "hybrid":
         return assign_hybrid(P["front"], P["bits"], P["alpha"], C, P["m"], P["d0"])
     raise ValueError(fmt)
@@ -409,6 +464,8 @@ def update(P: dict, a, k: int, C, policy: int = EMPTY_SPLIT):
         return update_sign1(P["bits"], P["alpha"], P["d"], P["m"], a, k, C, policy)
     if fmt == "rabitq":
         return update_sign1(P["bits"], P["alpha"], P["d"], np.zeros(P["d"], np.float32), a, k, C, policy)
+    if fmt == "lvq4":
+        return update_lvq4(P["codes"], P["par"], a, k, C, policy)
     if fmt == "hybrid":
         return update_sign1(P["bits"], P["alpha"], P["d"], P["m"], a, k, C, policy, front=P["front"], d0=P["d0"])
     raise ValueError(fmt)

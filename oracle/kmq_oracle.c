@@ -373,6 +373,70 @@ void orc_assign_rabitq(const uint32_t *bits, const float *alpha, int64_t n, int3
   }
 }
 
+/* ------------------------------------------------------------------------ */
+/* LVQ4 (Sec. 3.1, Eq. 1-2). */
+
+void orc_lvq4_encode(const float *X, int64_t n, int32_t d, uint8_t *codes, float *par) {
+#pragma omp parallel for schedule(static)
+  for (int64_t r = 0; r < n; ++r) {
+    const float *v = X + r * d;
+    float lo = v[0], hi = v[0];
+    for (int32_t i = 1; i < d; ++i) {
+      if (v[i] < lo) lo = v[i];
+      if (v[i] > hi) hi = v[i];
+    }
+    const float s = hi > lo ? (hi - lo) / 15.0f : 1.0f;
+    int32_t S = 0, Q = 0;
+    for (int32_t i = 0; i < d; ++i) {
+      float t = rintf((v[i] - lo) / s);
+      if (t < 0.0f) t = 0.0f;
+      if (t > 15.0f) t = 15.0f;
+      const int32_t c = (int32_t)t;
+      codes[r * d + i] = (uint8_t)c;
+      S += c;
+      Q += c * c;
+    }
+    const float db = (float)d * lo;
+    par[4 * r + 0] = s;
+    par[4 * r + 1] = lo;
+    par[4 * r + 2] = fmaf(s, (float)S, db);
+    par[4 * r + 3] = fmaf(s * s, (float)Q, fmaf(2.0f * lo * s, (float)S, db * lo));
+  }
+}
+
+void orc_lvq4_decode(const uint8_t *codes, const float *par, int64_t n, int32_t d, float *out) {
+#pragma omp parallel for schedule(static)
+  for (int64_t r = 0; r < n; ++r)
+    for (int32_t i = 0; i < d; ++i) out[r * d + i] = fmaf(par[4 * r], (float)codes[r * d + i], par[4 * r + 1]);
+}
+
+void orc_assign_lvq4(const uint8_t *xc, const float *xpar, int64_t n, int32_t d, const uint8_t *yc,
+                     const float *ypar, const int32_t *yS, int32_t k, int32_t *a, float *score, double *dist) {
+#pragma omp parallel for schedule(static)
+  for (int64_t r = 0; r < n; ++r) {
+    const uint8_t *x = xc + r * d;
+    const float sx = xpar[4 * r], bx = xpar[4 * r + 1], Ax = xpar[4 * r + 2];
+    int32_t best = 0;
+    float bs = 0.0f;
+    for (int32_t j = 0; j < k; ++j) {
+      const uint8_t *y = yc + (int64_t)j * d;
+      int32_t dot = 0;
+      for (int32_t i = 0; i < d; ++i) dot += (int32_t)x[i] * (int32_t)y[i];
+      const float sy = ypar[4 * j], by = ypar[4 * j + 1], Ny = ypar[4 * j + 3];
+      /* Eq. 2 without the point-only N_x: N_y - 2 (sx sy <xbar,ybar> + by A_x + bx sy S_y) */
+      const float t = fmaf(bx * sy, (float)yS[j], fmaf(by, Ax, (sx * sy) * (float)dot));
+      const float sc = fmaf(-2.0f, t, Ny);
+      if (j == 0 || sc < bs) {
+        bs = sc;
+        best = j;
+      }
+    }
+    a[r] = best;
+    if (score) score[r] = bs;
+    if (dist) dist[r] = (double)xpar[4 * r + 3] + (double)bs;
+  }
+}
+
 void orc_assign_hybrid(const float *front, const uint32_t *bits, const float *alpha, int64_t n,
                        int32_t d, int32_t d0, const float *C, const int8_t *q, const float *sigma,
                        const int32_t *T, const float *u, int32_t k, int32_t *a, double *dist) {
@@ -486,6 +550,33 @@ void orc_update_f32(const float *X, int64_t n, int32_t d, int64_t ldx, const int
   for (int32_t i = 0; i < d; ++i)
     for (int64_t r = 0; r < n; ++r)
       if (a[r] >= 0 && a[r] < k) S[(int64_t)a[r] * d + i] += (double)X[r * ldx + i];
+  for (int32_t j = 0; j < k; ++j) {
+    fresh[j] = cnt[j] > 0;
+    for (int32_t i = 0; i < d; ++i)
+      Z[(int64_t)j * d + i] = cnt[j] > 0 ? (float)(S[(int64_t)j * d + i] / (double)cnt[j]) : 0.0f;
+  }
+  if (policy == ORC_EMPTY_SPLIT) split_float(Z, k, d, cnt, fresh);
+  for (int32_t j = 0; j < k; ++j)
+    if (fresh[j]) memcpy(C + (int64_t)j * d, Z + (int64_t)j * d, sizeof(float) * (size_t)d);
+  if (counts) memcpy(counts, cnt, sizeof(int64_t) * (size_t)k);
+  free(cnt);
+  free(S);
+  free(Z);
+  free(fresh);
+}
+
+void orc_update_lvq4(const uint8_t *xc, const float *xpar, int64_t n, int32_t d, const int32_t *a, int32_t k,
+                     float *C, int64_t *counts, int32_t policy) {
+  int64_t *cnt = (int64_t *)malloc(sizeof(int64_t) * (size_t)k);
+  double *S = (double *)calloc((size_t)k * (size_t)d, sizeof(double));
+  float *Z = (float *)malloc(sizeof(float) * (size_t)k * (size_t)d);
+  uint8_t *fresh = (uint8_t *)calloc((size_t)k, 1);
+  count_members(a, n, k, cnt);
+#pragma omp parallel for schedule(static)
+  for (int32_t i = 0; i < d; ++i)
+    for (int64_t r = 0; r < n; ++r)
+      if (a[r] >= 0 && a[r] < k)
+        S[(int64_t)a[r] * d + i] += (double)fmaf(xpar[4 * r], (float)xc[r * d + i], xpar[4 * r + 1]);
   for (int32_t j = 0; j < k; ++j) {
     fresh[j] = cnt[j] > 0;
     for (int32_t i = 0; i < d; ++i)

@@ -100,6 +100,25 @@ void orc_assign_rabitq(const uint32_t *bits, const float *alpha, int64_t n, int3
                        const float *s, const float *b, const int32_t *T, const float *N, int32_t k,
                        int32_t *a, float *score, double *dist);
 
+/* LVQ4 (Sec. 3.1 LVQ, Eq. 1-2): each vector (point or centroid) v is coded with its
+ * own bias b = min_i v_i and scale s = (max_i v_i - b) / 15 (1 when the range is 0),
+ * code_i = clip(rint((v_i - b) / s), 0, 15) in fp32; S = sum code, Q = sum code^2
+ * (exact), and in fp32, in this order: A = fmaf(s, S, d * b),
+ * N = fmaf(s * s, Q, fmaf(2 * b * s, S, d * b * b)).  codes: uint8[n][d] (one code per
+ * byte; the product packs two per byte), par: float[n][4] = (s, b, A, N).
+ * Decoding is fmaf(s, code, b). */
+void orc_lvq4_encode(const float *X, int64_t n, int32_t d, uint8_t *codes, float *par);
+/* Decoding: out = fmaf(s, code, b) per value (fp32). */
+void orc_lvq4_decode(const uint8_t *codes, const float *par, int64_t n, int32_t d, float *out);
+/* Eq. 2 for the argmin: score = fmaf(-2, fmaf(bx * sy, Sy, fmaf(by, Ax, (sx * sy) * dot)), Ny)
+ * with dot = <xbar, ybar> exact; fp32 in this order.  dist (nullable) = Nx + score (fp64). */
+void orc_assign_lvq4(const uint8_t *xc, const float *xpar, int64_t n, int32_t d, const uint8_t *yc,
+                     const float *ypar, const int32_t *yS, int32_t k, int32_t *a, float *score, double *dist);
+/* Update: c_j = (1/n_j) sum of the decoded members fmaf(s, code, b) (fp64 sums, fp32 result),
+ * empty-cluster split as for fp32 points. */
+void orc_update_lvq4(const uint8_t *xc, const float *xpar, int64_t n, int32_t d, const int32_t *a, int32_t k,
+                     float *C, int64_t *counts, int32_t policy);
+
 /* ---- STEP 3: update (mean of members, empty-cluster split) ------------- */
 
 /* fp32 points: c_j = mean of members (fp64 sums, fp32 result).  counts = member counts. */

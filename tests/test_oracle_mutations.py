@@ -36,6 +36,11 @@ MUTATIONS = {
     "rabitq_bias_term_sign": ("b * (float)(2 * P - d)", "b * (float)(d - 2 * P)"),
     "rabitq_sq4_16_levels": ("(hi - lo) / 15.0f", "(hi - lo) / 16.0f"),
     "rabitq_drops_T": ("(float)(2 * D - T)", "(float)(2 * D)"),
+    "lvq4_A_sign_of_bias": ("par[4 * r + 2] = fmaf(s, (float)S, db);", "par[4 * r + 2] = fmaf(s, (float)S, -db);"),
+    "lvq4_drops_bx_sy_Sy": ("fmaf(bx * sy, (float)yS[j], fmaf(by, Ax, (sx * sy) * (float)dot))",
+                            "fmaf(by, Ax, (sx * sy) * (float)dot)"),
+    "lvq4_16_levels": ("const float s = hi > lo ? (hi - lo) / 15.0f : 1.0f;",
+                       "const float s = hi > lo ? (hi - lo) / 16.0f : 1.0f;"),
 }
 
 PINS = [name for name in dir(pins) if name.startswith("test_")]

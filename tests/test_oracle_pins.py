@@ -644,3 +644,58 @@ def test_fit_raw_last_update(orc):
             np.testing.assert_allclose(C[j], mem.mean(0), rtol=1e-6, atol=1e-6)
     a_fin, _ = orc.assign(Pd, C)
     np.testing.assert_array_equal(a, a_fin)
+
+
+# --------------------------------------------------------------------------
+# LVQ4 (Sec. 3.1 LVQ, Eq. 1-2)
+
+def test_lvq4_hand_example(orc):
+    """Codes, per-vector terms and the Eq. 2 distance of a hand-worked example with
+    exact scales; the winning score plus N_x is the decoded squared distance."""
+    g = load_golden("lvq4_eq2.json")
+    V = np.array(g["vectors"], np.float32)
+    codes, par = orc.lvq4_encode(V)
+    assert codes.tolist() == g["codes"]
+    assert par[:, 0].tolist() == g["scale"] and par[:, 1].tolist() == g["bias"]
+    assert par[:, 2].tolist() == g["A"] and par[:, 3].tolist() == g["N"]
+    p = g["point"]
+    assert int(codes[p].astype(np.int64) @ codes[2].astype(np.int64)) == g["dot_point_centroid2"]
+    C = V[g["centroids"]]
+    a, score, dist = orc.assign_lvq4(codes[p:p + 1], par[p:p + 1], C)
+    assert int(a[0]) == g["assign"] and float(score[0]) == g["scores"][g["assign"]]
+    assert dist[0] == g["decoded_distance"]
+
+
+def test_lvq4_cached_terms_and_eq2_identity(orc):
+    """A_x is the sum and N_x the squared norm of the decoded vector, and N_x + score is
+    the squared distance between decoded point and decoded centroid (Eq. 2), checked
+    against explicit fp64 evaluations on the decoded vectors."""
+    rng = np.random.default_rng(51)
+    X = (rng.standard_normal((200, 96)) * rng.uniform(0.2, 3, (200, 1)) + rng.normal(0, 1, (200, 1))).astype(np.float32)
+    codes, par = orc.lvq4_encode(X)
+    dec = orc.lvq4_decode(codes, par).astype(np.float64)
+    np.testing.assert_allclose(par[:, 2], dec.sum(1), rtol=2e-6, atol=1e-4)
+    np.testing.assert_allclose(par[:, 3], (dec ** 2).sum(1), rtol=2e-6)
+    assert (np.abs(dec - X) <= 0.5 * par[:, :1] * (1 + 1e-5)).all()  # within half a step
+    C = X[:7] * 1.1
+    a, score, dist = orc.assign_lvq4(codes, par, C)
+    cdec = orc.lvq4_decode(*orc.lvq4_encode(C)).astype(np.float64)
+    full = ((dec[:, None, :] - cdec[None, :, :]) ** 2).sum(-1)
+    np.testing.assert_allclose(dist, full[np.arange(len(X)), a], rtol=1e-5, atol=1e-3)
+    gap = full[np.arange(len(X)), a] - full.min(1)
+    assert (gap <= 1e-5 * (1 + full.max())).all()
+
+
+def test_lvq4_update_is_decoded_mean(orc):
+    rng = np.random.default_rng(53)
+    X = rng.standard_normal((500, 64)).astype(np.float32)
+    codes, par = orc.lvq4_encode(X)
+    dec = orc.lvq4_decode(codes, par).astype(np.float64)
+    k = 9
+    a = rng.integers(0, k - 1, 500).astype(np.int32)  # cluster k-1 stays empty
+    C0 = rng.standard_normal((k, 64)).astype(np.float32)
+    C, cnt = orc.update_lvq4(codes, par, a, k, C0, orc.EMPTY_KEEP)
+    for j in range(k - 1):
+        np.testing.assert_allclose(C[j], dec[a == j].mean(0), rtol=1e-6, atol=1e-6)
+    np.testing.assert_array_equal(C[k - 1], C0[k - 1])
+    np.testing.assert_array_equal(cnt, np.bincount(a, minlength=k))
