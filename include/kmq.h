@@ -49,7 +49,8 @@ typedef enum {
   KM_SQ8 = 2,    /* uint8 scalar-quantised codes, one (lo, hi) pair per dimension */
   KM_SIGN1 = 3,  /* 1-bit sign codes of x - m plus one fp32 scale alpha per vector */
   KM_HYBRID = 4, /* fp32 front dims [0, d_front) + 1-bit codes on the tail [d_front, d) */
-  KM_RABITQ = 5  /* 1-bit codes of the randomly rotated, centred residual; SQ4 centroid codes */
+  KM_RABITQ = 5, /* 1-bit codes of the randomly rotated, centred residual; SQ4 centroid codes */
+  KM_LVQ4 = 6    /* 4-bit codes with a per-vector scale and bias (LVQ) */
 } km_format;
 
 typedef enum {
@@ -77,6 +78,11 @@ typedef enum {
  *              rabitq_encode), alpha = float[n] = ||y||^2 / ||y||_1, center must be
  *              NULL (the codes are of the residual: the clustering space is the
  *              rotated residual space, centre 0).  d % 32 == 0.
+ *   KM_LVQ4:   data = uint8[n][ld] codes, two per byte (dim 2i in the low nibble, dim
+ *              2i+1 in the high one), ld >= d/2, ld % 16 == 0, d % 32 == 0, 16-byte
+ *              aligned; vparams = float[n][4] per vector (s, b, A, N): scale, bias,
+ *              A = fmaf(s, S, d b) and N = fmaf(s s, Q, fmaf(2 b s, S, (d b) b)) with S,
+ *              Q the sum and the sum of squares of its codes (as quantize writes them).
  * `ld` is ignored for the 1-bit formats.
  * raw (nullable): fp32 rows of the same points in the clustering space (the
  *   original vectors for KM_SIGN1 / KM_HYBRID / KM_BF16, the rotated residual y for
@@ -89,7 +95,7 @@ typedef struct km_points {
   int32_t d;            /* logical dimensionality */
   int64_t n;            /* number of points, 1 <= n < 2^31 */
   const void *data;
-  int64_t ld;           /* row stride in elements (F32: floats, BF16: 16-bit values, SQ8: bytes) */
+  int64_t ld;           /* row stride in elements (F32: floats, BF16: 16-bit values, SQ8 and LVQ4: bytes) */
   const float *alpha;
   const float *center;
   const float *front;
@@ -97,6 +103,7 @@ typedef struct km_points {
   int32_t reserved;     /* must be 0 */
   const float *raw;     /* nullable, see above */
   int64_t raw_ld;       /* row stride of raw in floats */
+  const float *vparams; /* KM_LVQ4: per-vector (s, b, A, N), float[n][4]; NULL otherwise */
 } km_points;
 
 /*
@@ -114,6 +121,10 @@ typedef struct km_points {
  *     If d_front > 0 and front != NULL, front = float[n][d_front] receives a copy
  *     of the first d_front dims (the hybrid layout).  d % 32 == 0, d_front % 32 == 0;
  *     params and front 16-byte aligned.
+ *   fmt == KM_LVQ4 (Sec. 3.1 LVQ, B = 4): per vector b = min_i x_i, s = (max_i x_i - b)/15
+ *     (1 when the range is 0), code_i = clip(rint((x_i - b)/s), 0, 15) in fp32; codes =
+ *     uint8[n][d/2] packed as in km_points; params = float[n][4] receives (s, b, A, N).
+ *     d % 32 == 0; alpha, front unused; flags ignored.
  *   fmt == KM_BF16 (16-bit storage, Sec. 2.4): codes = bfloat16[n][d], each value
  *     rounded to the nearest bfloat16 with ties to the even significand (NaN stays
  *     NaN, overflow gives infinities).  params, alpha, front: unused (may be NULL);
@@ -164,7 +175,8 @@ km_status pca_project(const float *X, int64_t n, int32_t d, const float *mean, c
  *      q = rint((c - m)/sigma), sigma = max|c - m|/127, rebuilt on each call);
  *      KM_RABITQ: float in the rotated residual space, coded on each call with a
  *      per-centroid SQ4 (Eq. 5): b = min_i c_i, s = (max_i c_i - b)/15 (1 when the
- *      range is 0), q = clip(rint((c - b)/s), 0, 15).
+ *      range is 0), q = clip(rint((c - b)/s), 0, 15); KM_LVQ4: float, coded on each
+ *      call with LVQ4 like the points.
  *      KM_BF16 compares the points with the centroids rounded to bfloat16 (nearest,
  *      ties to even), products exact, fp32 accumulation.
  *   assign: int32[n].  score (nullable): float[n], the winning score, i.e. the
@@ -173,12 +185,14 @@ km_status pca_project(const float *X, int64_t n, int32_t d, const float *mean, c
  *      SQ8: ||c~||^2 - 2<x~,c~> with x~ = code - 128;
  *      SIGN1: fmaf(-alpha*2*sigma, <2b-1, q>, sigma^2 ||q||^2);
  *      HYBRID: front F32 score + tail SIGN1 score;
+ *      LVQ4 (Eq. 2 without N_x): fmaf(-2, fmaf(b_x s_y, S_y, fmaf(b_y, A_x,
+ *      (s_x s_y) <xbar, ybar>)), N_y), fp32 in this order;
  *      RABITQ (Eq. 4-5): fmaf(-2 alpha, fmaf(s, 2D - T, b (2P - d)), ||c||^2) with
  *      D = sum of q on set bits, T = sum of q, P = number of set bits (fp32, in this
  *      order).
  *   objective (nullable): double[1], receives sum over points of the in-space
  *      distance (score plus the point-only term), fp64.  For the 1-bit formats the
- *      point-only term is the decoded point's squared norm alpha^2 d.
+ *      point-only term is the decoded point's squared norm alpha^2 d; for LVQ4 it is N_x.
  *   1 <= k.
  */
 km_status kmeans_assign(const km_points *P, const void *C, int32_t k, int32_t *assign, float *score,
@@ -191,7 +205,8 @@ km_status kmeans_assign(const km_points *P, const void *C, int32_t k, int32_t *a
  *   KM_SQ8: floor((2 S + n_j) / (2 n_j)) with S the exact code sum
  *   (averaging in the quantised domain, Sec. 3.1); KM_SIGN1: m + (1/n_j) sum alpha (2b - 1)
  *   (fused decode-averaging, Sec. 3.1); KM_HYBRID: front mean and tail decode-average;
- *   KM_RABITQ: (1/n_j) sum alpha (2b - 1) in the rotated residual space.
+ *   KM_RABITQ: (1/n_j) sum alpha (2b - 1) in the rotated residual space;
+ *   KM_LVQ4: the fp32 mean of the decoded members fmaf(s, code, b).
  *   C: in = previous centroids, out = new ones (same type as kmeans_assign).
  *   counts (nullable): int64[k] member counts of `assign`.
  *   policy KM_EMPTY_SPLIT: empty clusters, in ascending order, take a split of the

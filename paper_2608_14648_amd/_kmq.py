@@ -16,7 +16,7 @@ import torch
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libkmq.so")
 
-KM_F32, KM_BF16, KM_SQ8, KM_SIGN1, KM_HYBRID, KM_RABITQ = 0, 1, 2, 3, 4, 5
+KM_F32, KM_BF16, KM_SQ8, KM_SIGN1, KM_HYBRID, KM_RABITQ, KM_LVQ4 = 0, 1, 2, 3, 4, 5, 6
 KM_EMPTY_SPLIT, KM_EMPTY_KEEP = 0, 1
 KM_Q_FIT_PARAMS = 1
 STATUS = {0: "KM_OK", -1: "KM_EINVAL", -2: "KM_EUNSUPPORTED", -3: "KM_ENOMEM", -4: "KM_EDEVICE"}
@@ -33,7 +33,8 @@ class KmqError(RuntimeError):
 class KmPoints(ct.Structure):
     _fields_ = [("fmt", ct.c_int32), ("d", ct.c_int32), ("n", ct.c_int64), ("data", ct.c_void_p),
                 ("ld", ct.c_int64), ("alpha", ct.c_void_p), ("center", ct.c_void_p), ("front", ct.c_void_p),
-                ("d_front", ct.c_int32), ("reserved", ct.c_int32), ("raw", ct.c_void_p), ("raw_ld", ct.c_int64)]
+                ("d_front", ct.c_int32), ("reserved", ct.c_int32), ("raw", ct.c_void_p), ("raw_ld", ct.c_int64),
+                ("vparams", ct.c_void_p)]
 
 
 class KmFitStats(ct.Structure):
@@ -108,17 +109,19 @@ class Points:
     """Compressed points handed to the clustering calls (mirrors ``km_points``)."""
 
     def __init__(self, fmt: int, data: torch.Tensor, d: int, alpha=None, center=None, front=None, d_front: int = 0,
-                 raw=None):
+                 raw=None, vparams=None):
         self.fmt, self.data, self.d = fmt, data, d
         self.alpha, self.center, self.front, self.d_front, self.raw = alpha, center, front, d_front, raw
+        self.vparams = vparams
         self.n = data.shape[0]
-        ld = data.stride(0) if fmt in (KM_F32, KM_BF16, KM_SQ8) else d // 32
+        ld = data.stride(0) if fmt in (KM_F32, KM_BF16, KM_SQ8, KM_LVQ4) else d // 32
         if raw is not None:
             _rows(raw, torch.float32, "raw")
             if raw.shape[0] != self.n or raw.shape[1] != d:
                 raise ValueError("raw must hold the same n points with d dims")
         self._c = KmPoints(fmt, d, self.n, data.data_ptr(), ld, _ptr(alpha) or None, _ptr(center) or None,
-                           _ptr(front) or None, d_front, 0, _ptr(raw) or None, raw.stride(0) if raw is not None else 0)
+                           _ptr(front) or None, d_front, 0, _ptr(raw) or None, raw.stride(0) if raw is not None else 0,
+                           _ptr(vparams) or None)
 
     @property
     def ref(self):
@@ -177,6 +180,17 @@ def points_rabitq(bits: torch.Tensor, alpha: torch.Tensor, d: int, raw: torch.Te
     if bits.shape[1] != d // 32:
         raise ValueError("bits must have d/32 words per row")
     return Points(KM_RABITQ, bits, d, alpha=alpha, raw=raw)
+
+
+def points_lvq4(codes: torch.Tensor, vparams: torch.Tensor, d: int, raw: torch.Tensor | None = None) -> Points:
+    """LVQ4 points: packed 4-bit codes (uint8 n x ld, ld >= d/2, two dims per byte) and
+    per-vector (s, b, A, N) float32 n x 4 as quantize_lvq4 returns them; raw: optional
+    fp32 rows for the last update of kmeans_fit."""
+    _rows(codes, torch.uint8, "codes")
+    _dev(vparams, torch.float32, "vparams", 2)
+    if codes.shape[1] < d // 2 or vparams.shape != (codes.shape[0], 4):
+        raise ValueError("codes must hold d/2 bytes per row and vparams n x 4 floats")
+    return Points(KM_LVQ4, codes, d, raw=raw, vparams=vparams)
 
 
 def points_hybrid(front: torch.Tensor, bits: torch.Tensor, alpha: torch.Tensor, center: torch.Tensor,
@@ -239,6 +253,17 @@ def quantize_bf16(X: torch.Tensor) -> torch.Tensor:
     out = torch.empty((n, d), dtype=torch.bfloat16, device=X.device)
     _check(lib().quantize(_ptr(X), n, d, X.stride(0), KM_BF16, _ptr(out), None, None, 0, None, 0, _stream()))
     return out
+
+
+def quantize_lvq4(X: torch.Tensor):
+    """LVQ4 codes (uint8 n x d/2, two 4-bit codes per byte, low nibble first) and the
+    per-vector (s, b, A, N) as float32 n x 4."""
+    _dev(X, torch.float32, "X", 2)
+    n, d = X.shape
+    codes = torch.empty((n, d // 2), dtype=torch.uint8, device=X.device)
+    par = torch.empty((n, 4), dtype=torch.float32, device=X.device)
+    _check(lib().quantize(_ptr(X), n, d, X.stride(0), KM_LVQ4, _ptr(codes), _ptr(par), None, 0, None, 0, _stream()))
+    return codes, par
 
 
 def quantize_sign1(X: torch.Tensor, center: torch.Tensor | None = None, d_front: int = 0, want_front: bool = False):

@@ -90,7 +90,7 @@ static km_status check_points(const km_points *P, Points *out) {
   KMQ_CHECK(P != nullptr, KM_EINVAL, "points descriptor is NULL");
   const int fmt = P->fmt;
   KMQ_CHECK(fmt == KM_F32 || fmt == KM_BF16 || fmt == KM_SQ8 || fmt == KM_SIGN1 || fmt == KM_HYBRID ||
-                fmt == KM_RABITQ,
+                fmt == KM_RABITQ || fmt == KM_LVQ4,
             KM_EUNSUPPORTED, "unknown point format %d", fmt);
   KMQ_CHECK(P->reserved == 0, KM_EINVAL, "reserved field must be 0");
   KMQ_CHECK(P->n >= 1 && P->n < (int64_t)INT32_MAX, KM_EINVAL, "n = %lld outside [1, 2^31)", (long long)P->n);
@@ -109,6 +109,9 @@ static km_status check_points(const km_points *P, Points *out) {
   p.d_front = P->d_front;
   p.raw = P->raw;
   p.raw_ld = P->raw_ld;
+  p.vparams = P->vparams;
+  KMQ_CHECK((fmt == KM_LVQ4) == (P->vparams != nullptr), KM_EINVAL,
+            "vparams must be given for LVQ4 points and only for them");
   if (P->raw) {
     KMQ_CHECK(fmt != KM_SQ8, KM_EINVAL, "raw rows are not allowed for SQ8 points (their centroids are codes)");
     KMQ_CHECK(P->d % 4 == 0 && P->raw_ld >= P->d && P->raw_ld % 4 == 0 && aligned16(P->raw), KM_EINVAL,
@@ -126,6 +129,11 @@ static km_status check_points(const km_points *P, Points *out) {
     KMQ_CHECK(P->d % 16 == 0, KM_EINVAL, "SQ8 codes need d %% 16 == 0 (d = %d)", P->d);
     KMQ_CHECK(P->ld >= P->d && P->ld % 16 == 0, KM_EINVAL, "SQ8 codes need ld >= d and ld %% 16 == 0");
     KMQ_CHECK(P->d_front == 0, KM_EINVAL, "d_front must be 0 for this format");
+  } else if (fmt == KM_LVQ4) {
+    KMQ_CHECK(P->d % 32 == 0, KM_EINVAL, "LVQ4 codes need d %% 32 == 0 (d = %d)", P->d);
+    KMQ_CHECK(P->ld >= P->d / 2 && P->ld % 16 == 0, KM_EINVAL, "LVQ4 codes need ld >= d/2 and ld %% 16 == 0");
+    KMQ_CHECK(P->d_front == 0 && P->center == nullptr, KM_EINVAL, "LVQ4 points take no front and no center");
+    KMQ_CHECK(aligned16(P->vparams), KM_EINVAL, "vparams must be 16-byte aligned");
   } else {
     KMQ_CHECK(P->d % 32 == 0, KM_EINVAL, "1-bit codes need d %% 32 == 0 (d = %d)", P->d);
     KMQ_CHECK(P->alpha != nullptr, KM_EINVAL, "alpha is NULL");
@@ -189,8 +197,8 @@ km_status km_release(void) {
 km_status quantize(const float *X, int64_t n, int32_t d, int64_t ldx, int32_t fmt, void *codes, float *params,
                    float *alpha, int32_t d_front, float *front, int32_t flags, km_stream stream) {
   g_err[0] = 0;
-  KMQ_CHECK(fmt == KM_SQ8 || fmt == KM_SIGN1 || fmt == KM_BF16, KM_EUNSUPPORTED,
-            "quantize supports SQ8, SIGN1 and BF16 (fmt = %d)", fmt);
+  KMQ_CHECK(fmt == KM_SQ8 || fmt == KM_SIGN1 || fmt == KM_BF16 || fmt == KM_LVQ4, KM_EUNSUPPORTED,
+            "quantize supports SQ8, SIGN1, BF16 and LVQ4 (fmt = %d)", fmt);
   KMQ_CHECK(X != nullptr && codes != nullptr && (params != nullptr || fmt == KM_BF16), KM_EINVAL, "NULL argument");
   KMQ_CHECK(n >= 1 && n < (int64_t)INT32_MAX, KM_EINVAL, "n = %lld outside [1, 2^31)", (long long)n);
   KMQ_CHECK(d >= 1 && ldx >= d && ldx % 4 == 0, KM_EINVAL, "need d >= 1, ldx >= d, ldx %% 4 == 0");
@@ -202,6 +210,10 @@ km_status quantize(const float *X, int64_t n, int32_t d, int64_t ldx, int32_t fm
   } else if (fmt == KM_BF16) {
     KMQ_CHECK(d % 8 == 0, KM_EINVAL, "BF16 needs d %% 8 == 0 (d = %d)", d);
     KMQ_CHECK(d_front == 0 && front == nullptr, KM_EINVAL, "d_front/front are for 1-bit codes only");
+  } else if (fmt == KM_LVQ4) {
+    KMQ_CHECK(d % 32 == 0, KM_EINVAL, "LVQ4 needs d %% 32 == 0 (d = %d)", d);
+    KMQ_CHECK(d_front == 0 && front == nullptr, KM_EINVAL, "d_front/front are for 1-bit codes only");
+    KMQ_CHECK(aligned16(params), KM_EINVAL, "params must be 16-byte aligned");
   } else {
     KMQ_CHECK(d % 32 == 0, KM_EINVAL, "1-bit codes need d %% 32 == 0 (d = %d)", d);
     KMQ_CHECK(alpha != nullptr, KM_EINVAL, "alpha is NULL");

@@ -62,6 +62,7 @@ struct AssignArgs {
   int64_t cild;
   int di;
   const float *alpha;
+  const float *vparams;  // LVQ4: per-point (s, b, A, N)
   CentroidPrep cp;
   int64_t n;
   int k;
@@ -605,6 +606,11 @@ struct Stage8 {
   float cpar[4];
 };
 
+// 4 packed 4-bit codes (a half-word) -> 4 bytes holding the codes (nibble k -> byte k)
+__device__ __forceinline__ uint32_t spread_nib(uint32_t h) {
+  return (h & 0x000Fu) | ((h & 0x00F0u) << 4) | ((h & 0x0F00u) << 8) | ((h & 0xF000u) << 12);
+}
+
 template <int FMT>
 __device__ __forceinline__ void load_stage8(const AssignArgs &A, int s, int64_t c0, int64_t p0, Stage8 &R) {
   const int t = threadIdx.x;
@@ -625,6 +631,16 @@ __device__ __forceinline__ void load_stage8(const AssignArgs &A, int s, int64_t 
     if (FMT == KM_SQ8 || FMT == KM_BF16)
       R.p[i] = *reinterpret_cast<const uint4 *>(pbase8 + (uint32_t)(min(row, prmax) * (int)A.pild + bc));
   }
+  if (FMT == KM_LVQ4) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {  // 256 rows x 4 chunks of 16 packed bytes (32 dims) per stage
+      const int w = t + k8Threads * i;
+      const int row = w >> 2, qc = w & 3;
+      const int dim = kRowBytes * s + 32 * qc;
+      const int bp = dim < A.di ? dim / 2 : 0;
+      R.p[i] = *reinterpret_cast<const uint4 *>(pbase8 + (uint32_t)(min(row, prmax) * (int)A.pild + bp));
+    }
+  }
   if (FMT == KM_SIGN1 || FMT == KM_RABITQ) {
 #pragma unroll
     for (int i = 0; i < 2; ++i) {  // 256 rows x 4 words
@@ -637,11 +653,11 @@ __device__ __forceinline__ void load_stage8(const AssignArgs &A, int s, int64_t 
   if (s == 0) {  // per-centroid constants: threads t < kT8 (the others load a valid duplicate)
     const int64_t j = min<int64_t>(c0 + (t & (kT8 - 1)), A.k - 1);
     R.cpar[1] = FMT == KM_BF16 ? A.cp.cn[j] : __int_as_float(A.cp.qsum[j]);
-    if (FMT == KM_SIGN1 || FMT == KM_RABITQ) {
+    if (FMT == KM_SIGN1 || FMT == KM_RABITQ || FMT == KM_LVQ4) {
       R.cpar[2] = A.cp.u[j];
       R.cpar[3] = A.cp.sig2[j];
     }
-    if (FMT == KM_RABITQ) R.cpar[0] = A.cp.cn[j];
+    if (FMT == KM_RABITQ || FMT == KM_LVQ4) R.cpar[0] = A.cp.cn[j];
   }
 }
 
@@ -662,6 +678,23 @@ __device__ __forceinline__ void store_stage8(const AssignArgs &A, int s, const S
       *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 16 * col) = mask4(flip4(R.p[i]), ok);
     if (FMT == KM_BF16) *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 16 * col) = mask4(R.p[i], ok);
   }
+  if (FMT == KM_LVQ4) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int w = t + k8Threads * i;
+      const int row = w >> 2, qc = w & 3;
+      const bool ok = kRowBytes * s + 32 * qc < A.di;
+      const uint4 v = R.p[i];
+      *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 32 * qc) =
+          mask4(make_uint4(spread_nib(v.x & 0xFFFFu), spread_nib(v.x >> 16), spread_nib(v.y & 0xFFFFu),
+                           spread_nib(v.y >> 16)),
+                ok);
+      *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 32 * qc + 16) =
+          mask4(make_uint4(spread_nib(v.z & 0xFFFFu), spread_nib(v.z >> 16), spread_nib(v.w & 0xFFFFu),
+                           spread_nib(v.w >> 16)),
+                ok);
+    }
+  }
   if (FMT == KM_SIGN1 || FMT == KM_RABITQ) {
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
@@ -678,7 +711,7 @@ __device__ __forceinline__ void store_stage8(const AssignArgs &A, int s, const S
   }
   if (s == 0 && t < kT8) {
 #pragma unroll
-    for (int q = (FMT == KM_RABITQ ? 0 : 1); q < 4; ++q) cpar[q * kT8 + t] = R.cpar[q];
+    for (int q = (FMT == KM_RABITQ || FMT == KM_LVQ4 ? 0 : 1); q < 4; ++q) cpar[q * kT8 + t] = R.cpar[q];
   }
 }
 
@@ -748,6 +781,13 @@ __global__ __launch_bounds__(k8Threads, 1) void assign_i8_kernel(AssignArgs A) {
 
   float al[k8PB] = {};
   int pop[k8PB] = {};
+  f32x4 vp[k8PB] = {};  // LVQ4: (s, b, A, N) of the lane's points
+  if (FMT == KM_LVQ4) {
+#pragma unroll
+    for (int pb = 0; pb < k8PB; ++pb)
+      vp[pb] = *reinterpret_cast<const f32x4 *>(
+          A.vparams + 4 * min<int64_t>(p0 + wp * 32 * k8PB + pb * 32 + r, A.n - 1));
+  }
   if (FMT == KM_SIGN1 || FMT == KM_RABITQ) {
 #pragma unroll
     for (int pb = 0; pb < k8PB; ++pb) {
@@ -811,7 +851,11 @@ __global__ __launch_bounds__(k8Threads, 1) void assign_i8_kernel(AssignArgs A) {
           u4 = *reinterpret_cast<const f32x4 *>(&cp[2 * kT8 + cr]);
           s4 = *reinterpret_cast<const f32x4 *>(&cp[3 * kT8 + cr]);
         }
-        if constexpr (FMT == KM_RABITQ) b4 = *reinterpret_cast<const f32x4 *>(&cp[cr]);
+        if constexpr (FMT == KM_RABITQ || FMT == KM_LVQ4) b4 = *reinterpret_cast<const f32x4 *>(&cp[cr]);
+        if constexpr (FMT == KM_LVQ4) {
+          u4 = *reinterpret_cast<const f32x4 *>(&cp[2 * kT8 + cr]);
+          s4 = *reinterpret_cast<const f32x4 *>(&cp[3 * kT8 + cr]);
+        }
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int i = 4 * i4 + e;
@@ -824,6 +868,11 @@ __global__ __launch_bounds__(k8Threads, 1) void assign_i8_kernel(AssignArgs A) {
               sc = __float_as_int(q4[e]) - 2 * acc[cb][pb][i];
             } else if constexpr (FMT == KM_BF16) {
               sc = fmaf(-2.0f, acc[cb][pb][i], q4[e]);  // ||c||^2 - 2<x,c>
+            } else if constexpr (FMT == KM_LVQ4) {  // Eq. 2 without N_x, fp32 in the oracle's order
+              const float sy = s4[e];
+              const float tt = fmaf(vp[pb][1] * sy, (float)__float_as_int(q4[e]),
+                                    fmaf(b4[e], vp[pb][2], (vp[pb][0] * sy) * (float)acc[cb][pb][i]));
+              sc = fmaf(-2.0f, tt, u4[e]);
             } else if constexpr (FMT == KM_RABITQ) {  // Eq. 4-5, fp32 in the oracle's order
               const int sd = 2 * acc[cb][pb][i] - __float_as_int(q4[e]);
               const float inner = fmaf(s4[e], (float)sd, b4[e] * (float)(2 * pop[pb] - A.di));
@@ -1124,6 +1173,60 @@ __global__ __launch_bounds__(256) void prep_kernel(const void *Cv, int k, int d,
     }
     if (t == 0) qsum[j] = shi[0];
   }
+  if (FMT == KM_LVQ4) {  // LVQ4 of the centroid (Sec. 3.1 LVQ): b = min, s = range / 15, S, Q, N
+    const float *c = static_cast<const float *>(Cv) + (int64_t)j * d;
+    float lo = INFINITY, hi = -INFINITY;
+    for (int i = t; i < d; i += 256) {
+      lo = fminf(lo, c[i]);
+      hi = fmaxf(hi, c[i]);
+    }
+    shf[t] = lo;
+    __syncthreads();
+    for (int st = 128; st > 0; st >>= 1) {
+      if (t < st) shf[t] = fminf(shf[t], shf[t + st]);
+      __syncthreads();
+    }
+    lo = shf[0];
+    __syncthreads();
+    shf[t] = hi;
+    __syncthreads();
+    for (int st = 128; st > 0; st >>= 1) {
+      if (t < st) shf[t] = fmaxf(shf[t], shf[t + st]);
+      __syncthreads();
+    }
+    hi = shf[0];
+    const float sc = hi > lo ? (hi - lo) / 15.0f : 1.0f;
+    int ts = 0, tq = 0;
+    for (int i = t; i < d; i += 256) {
+      const int v = (int)fminf(fmaxf(rintf((c[i] - lo) / sc), 0.f), 15.f);
+      q[(int64_t)j * d + i] = (int8_t)v;
+      ts += v;
+      tq += v * v;
+    }
+    __syncthreads();
+    shi[t] = ts;
+    __syncthreads();
+    for (int st = 128; st > 0; st >>= 1) {
+      if (t < st) shi[t] += shi[t + st];
+      __syncthreads();
+    }
+    const int S = shi[0];
+    __syncthreads();
+    shi[t] = tq;
+    __syncthreads();
+    for (int st = 128; st > 0; st >>= 1) {
+      if (t < st) shi[t] += shi[t + st];
+      __syncthreads();
+    }
+    if (t == 0) {
+      const int Q = shi[0];
+      const float db = (float)d * lo;
+      qsum[j] = S;
+      u[j] = fmaf(sc * sc, (float)Q, fmaf(2.0f * lo * sc, (float)S, db * lo));
+      sig2[j] = sc;
+      cn[j] = lo;
+    }
+  }
   if (FMT == KM_RABITQ) {  // per-centroid SQ4 of the residual (Eq. 5): b = min, s = range / 15
     const float *c = static_cast<const float *>(Cv) + (int64_t)j * d;
     float lo = INFINITY, hi = -INFINITY;
@@ -1232,6 +1335,8 @@ __global__ __launch_bounds__(256) void xconst_kernel(Points P, float *xc) {
       const f32x4 v = *reinterpret_cast<const f32x4 *>(x + i);
       s += (double)v.x * v.x + (double)v.y * v.y + (double)v.z * v.z + (double)v.w * v.w;
     }
+  } else if (FMT == KM_LVQ4) {
+    if (lane == 0) s = P.vparams[4 * p + 3];  // N_x (only lane 0's value is kept)
   } else if (FMT == KM_BF16) {
     const uint16_t *x = static_cast<const uint16_t *>(P.data) + p * P.ld;
     for (int i = 8 * lane; i < P.d; i += 512) {
@@ -1300,6 +1405,11 @@ __global__ __launch_bounds__(256) void gather_kernel(Points P, const int64_t *id
     const float *x = static_cast<const float *>(P.data) + row * P.ld;
     float *c = static_cast<float *>(Cv) + (int64_t)j * d;
     for (int i = threadIdx.x; i < d; i += 256) c[i] = x[i];
+  } else if (FMT == KM_LVQ4) {
+    const uint8_t *x = static_cast<const uint8_t *>(P.data) + row * P.ld;
+    const float sx = P.vparams[4 * row], bx = P.vparams[4 * row + 1];
+    float *c = static_cast<float *>(Cv) + (int64_t)j * d;
+    for (int i = threadIdx.x; i < d; i += 256) c[i] = fmaf(sx, (float)((x[i >> 1] >> (4 * (i & 1))) & 15u), bx);
   } else if (FMT == KM_BF16) {
     const uint16_t *x = static_cast<const uint16_t *>(P.data) + row * P.ld;
     float *c = static_cast<float *>(Cv) + (int64_t)j * d;
@@ -1395,6 +1505,13 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
     A.ci8 = static_cast<const int8_t *>(C);
     A.cild = P.d;
     A.di = P.d;
+  } else if (FMT == KM_LVQ4) {  // packed 4-bit point codes, unpacked centroid codes
+    A.pi8 = static_cast<const uint8_t *>(P.data);
+    A.pild = P.ld;
+    A.ci8 = cp.q;
+    A.cild = P.d;
+    A.di = P.d;
+    A.vparams = P.vparams;
   } else if (FMT == KM_BF16) {  // byte-addressed rows of 16-bit values
     A.pi8 = static_cast<const uint8_t *>(P.data);
     A.pild = 2 * P.ld;
@@ -1423,7 +1540,7 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
     } else {
       hipLaunchKernelGGL(assign_i8_kernel<FMT>, dim3((unsigned)cdiv(P.n, kT8)), dim3(k8Threads), 0, s, A);
     }
-  } else if constexpr (FMT == KM_SQ8 || FMT == KM_BF16) {
+  } else if constexpr (FMT == KM_SQ8 || FMT == KM_BF16 || FMT == KM_LVQ4) {
     hipLaunchKernelGGL(assign_i8_kernel<FMT>, dim3((unsigned)cdiv(P.n, kT8)), dim3(k8Threads), 0, s, A);
   } else {
     constexpr int TP = Geo<Blocking<FMT>::CB, Blocking<FMT>::PB>::TP;
@@ -1451,6 +1568,7 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
 static size_t prep_codes_bytes(const Points &P, int k) {
   const int d0 = P.fmt == KM_HYBRID ? P.d_front : 0;
   if (is_bits_fmt(P.fmt)) return (size_t)k * (size_t)(P.d - d0);
+  if (P.fmt == KM_LVQ4) return (size_t)k * (size_t)P.d;
   if (P.fmt == KM_BF16) return 2 * (size_t)k * (size_t)P.d;
   return 0;
 }
@@ -1496,6 +1614,10 @@ km_status launch_prep(const Points &P, const void *C, int k, void *ws, CentroidP
       hipLaunchKernelGGL(prep_kernel<KM_SIGN1>, dim3(k), dim3(256), 0, s, C, k, P.d, 0, P.center, cn, qsum, u, sig2,
                          q, cb);
       break;
+    case KM_LVQ4:
+      hipLaunchKernelGGL(prep_kernel<KM_LVQ4>, dim3(k), dim3(256), 0, s, C, k, P.d, 0, nullptr, cn, qsum, u, sig2, q,
+                         cb);
+      break;
     case KM_RABITQ:
       hipLaunchKernelGGL(prep_kernel<KM_RABITQ>, dim3(k), dim3(256), 0, s, C, k, P.d, 0, nullptr, cn, qsum, u, sig2, q,
                          cb);
@@ -1520,6 +1642,7 @@ km_status launch_assign(const Points &P, const void *C, const CentroidPrep &cp, 
     case KM_SIGN1: return launch_assign_t<KM_SIGN1>(P, C, cp, k, assign, score, s);
     case KM_HYBRID: return launch_assign_t<KM_HYBRID>(P, C, cp, k, assign, score, s);
     case KM_RABITQ: return launch_assign_t<KM_RABITQ>(P, C, cp, k, assign, score, s);
+    case KM_LVQ4: return launch_assign_t<KM_LVQ4>(P, C, cp, k, assign, score, s);
     default: return KM_EUNSUPPORTED;
   }
 }
@@ -1533,6 +1656,7 @@ km_status launch_xconst(const Points &P, float *xc, hipStream_t s) {
     case KM_SIGN1: hipLaunchKernelGGL(xconst_kernel<KM_SIGN1>, g, dim3(256), 0, s, P, xc); break;
     case KM_HYBRID: hipLaunchKernelGGL(xconst_kernel<KM_HYBRID>, g, dim3(256), 0, s, P, xc); break;
     case KM_RABITQ: hipLaunchKernelGGL(xconst_kernel<KM_RABITQ>, g, dim3(256), 0, s, P, xc); break;
+    case KM_LVQ4: hipLaunchKernelGGL(xconst_kernel<KM_LVQ4>, g, dim3(256), 0, s, P, xc); break;
     default: return KM_EUNSUPPORTED;
   }
   KMQ_LAUNCH_CHECK("xconst_kernel");
@@ -1559,6 +1683,7 @@ km_status launch_gather_init(const Points &P, const int64_t *idx, int k, void *C
     case KM_SIGN1: hipLaunchKernelGGL(gather_kernel<KM_SIGN1>, dim3(k), dim3(256), 0, s, P, idx, C); break;
     case KM_HYBRID: hipLaunchKernelGGL(gather_kernel<KM_HYBRID>, dim3(k), dim3(256), 0, s, P, idx, C); break;
     case KM_RABITQ: hipLaunchKernelGGL(gather_kernel<KM_RABITQ>, dim3(k), dim3(256), 0, s, P, idx, C); break;
+    case KM_LVQ4: hipLaunchKernelGGL(gather_kernel<KM_LVQ4>, dim3(k), dim3(256), 0, s, P, idx, C); break;
     default: return KM_EUNSUPPORTED;
   }
   KMQ_LAUNCH_CHECK("gather_kernel");

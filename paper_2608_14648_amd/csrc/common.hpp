@@ -30,6 +30,7 @@ struct Points {
   int d_front;
   const float *raw;    // nullable: fp32 rows in the clustering space (last update of a fit)
   int64_t raw_ld;
+  const float *vparams;  // LVQ4: per-vector (s, b, A, N)
 };
 
 // 1-bit point formats (codes + one scale per point)
@@ -39,11 +40,11 @@ __host__ __device__ constexpr bool is_bits_fmt(int fmt) {
 
 // Per-centroid data rebuilt before each assignment pass.
 struct CentroidPrep {
-  const float *cn;     // F32/HYBRID/BF16: ||c'||^2 over the fp32 dims; RABITQ: SQ4 bias b
-  const int *qsum;     // SQ8: ||c~||^2 ; SIGN1/HYBRID/RABITQ: T_j = sum q
-  const float *u;      // SIGN1/HYBRID: (sigma*sigma)*Q ; RABITQ: ||c||^2
-  const float *sig2;   // SIGN1/HYBRID: 2*sigma ; RABITQ: SQ4 scale s
-  const int8_t *q;     // SIGN1/HYBRID: int8 residual codes, k x dt ; RABITQ: SQ4 codes 0..15, k x d
+  const float *cn;     // F32/HYBRID/BF16: ||c'||^2 over the fp32 dims; RABITQ, LVQ4: bias b
+  const int *qsum;     // SQ8: ||c~||^2 ; SIGN1/HYBRID/RABITQ: T_j = sum q ; LVQ4: S_j = sum of codes
+  const float *u;      // SIGN1/HYBRID: (sigma*sigma)*Q ; RABITQ: ||c||^2 ; LVQ4: N_j
+  const float *sig2;   // SIGN1/HYBRID: 2*sigma ; RABITQ, LVQ4: scale s
+  const int8_t *q;     // SIGN1/HYBRID: int8 residual codes, k x dt ; RABITQ, LVQ4: codes 0..15, k x d
   const uint16_t *cb;  // BF16: centroids rounded to bfloat16, k x d
   unsigned long long *keys;  // F32/HYBRID with centroid-tile groups: per-point (score, index) keys
 };

@@ -131,6 +131,52 @@ __global__ __launch_bounds__(256) void bf16_encode_kernel(const float *X, int64_
   }
 }
 
+// LVQ4: one wave per row.  Pass 1: the row's min and max (float4 per lane, wave
+// reductions); pass 2: codes, two per byte, and the exact sums S and Q of the codes;
+// lane 0 writes (s, b, A, N) with the fp32 expressions of the format definition.
+__global__ __launch_bounds__(256) void lvq4_encode_kernel(const float *X, int64_t n, int d, int64_t ldx,
+                                                          uint8_t *codes, float *par) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= n) return;
+  const float *x = X + row * ldx;
+  float lo = INFINITY, hi = -INFINITY;
+  for (int i = 4 * lane; i < d; i += 256) {
+    const f32x4 v = *reinterpret_cast<const f32x4 *>(x + i);
+    lo = fminf(fminf(lo, v[0]), fminf(fminf(v[1], v[2]), v[3]));
+    hi = fmaxf(fmaxf(hi, v[0]), fmaxf(fmaxf(v[1], v[2]), v[3]));
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    lo = fminf(lo, __shfl_xor(lo, off));
+    hi = fmaxf(hi, __shfl_xor(hi, off));
+  }
+  const float s = hi > lo ? (hi - lo) / 15.0f : 1.0f;
+  int S = 0, Q = 0;
+  uint8_t *out = codes + row * (int64_t)(d / 2);
+  for (int i = 4 * lane; i < d; i += 256) {  // d % 32 == 0: a float4 is wholly in or out
+    const f32x4 v = *reinterpret_cast<const f32x4 *>(x + i);
+    int c[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      c[e] = (int)fminf(fmaxf(rintf((v[e] - lo) / s), 0.0f), 15.0f);
+      S += c[e];
+      Q += c[e] * c[e];
+    }
+    *reinterpret_cast<uint16_t *>(out + i / 2) = (uint16_t)(c[0] | (c[1] << 4) | (c[2] << 8) | (c[3] << 12));
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    S += __shfl_xor(S, off);
+    Q += __shfl_xor(Q, off);
+  }
+  if (lane == 0) {
+    const float db = (float)d * lo;
+    *reinterpret_cast<f32x4 *>(par + 4 * row) =
+        f32x4{s, lo, fmaf(s, (float)S, db), fmaf(s * s, (float)Q, fmaf(2.0f * lo * s, (float)S, db * lo))};
+  }
+}
+
 // One wave per row.  Lane l reads dims [base + 4l, base + 4l + 4) as a float4 and
 // forms a 4-bit nibble of sign bits; the 8 lanes that share a 32-dim word OR
 // their shifted nibbles together (3 xor-shuffles) and the first of them stores
@@ -202,7 +248,7 @@ km_status launch_colmean(const float *X, int64_t n, int d, int64_t ldx, float *m
 }
 
 size_t quantize_bytes(int64_t n, int d, int fmt) {
-  if (fmt == KM_BF16) return 0;
+  if (fmt == KM_BF16 || fmt == KM_LVQ4) return 0;
   const int64_t nb = cdiv(n, kRowsPerBlock);
   if (fmt == KM_SQ8) return (size_t)nb * d * 2 * sizeof(float) + (size_t)d * sizeof(float) + 512;
   return colmean_bytes(n, d);
@@ -258,6 +304,12 @@ km_status launch_quantize(const float *X, int64_t n, int d, int64_t ldx, int fmt
     hipLaunchKernelGGL(sq8_encode_kernel, dim3(g), dim3(256), 0, s, X, n, d, ldx, lo, inv,
                        static_cast<uint8_t *>(codes));
     KMQ_LAUNCH_CHECK("quantize sq8");
+    return KM_OK;
+  }
+  if (fmt == KM_LVQ4) {
+    hipLaunchKernelGGL(lvq4_encode_kernel, dim3((unsigned)cdiv(n, 4)), dim3(256), 0, s, X, n, d, ldx,
+                       static_cast<uint8_t *>(codes), params);
+    KMQ_LAUNCH_CHECK("quantize lvq4");
     return KM_OK;
   }
   if (fmt == KM_BF16) {

@@ -349,6 +349,69 @@ __global__ __launch_bounds__(256) void segsum_bf16_kernel(const uint16_t *X, int
   }
 }
 
+// LVQ4 rows: one slice of 1024 dims (512 packed bytes) per workgroup; lane = 16
+// dims from 8 packed bytes, each decoded as fmaf(s, code, b) and summed in fp32
+__global__ __launch_bounds__(256) void segsum_lvq4_kernel(const uint8_t *codes, int64_t ld, const float *vparams,
+                                                          int d, const int *perm, const int *cnt, const int *cstart,
+                                                          const int *choff, int k, float *partial, int dp) {
+  __shared__ float red[4][64 * 17];
+  const int c = blockIdx.x;
+  if (c >= choff[k]) return;
+  const int j = find_cluster(choff, k, c);
+  const int ci = c - choff[j];
+  const int m0 = cstart[j] + ci * kChunk;
+  const int m1 = cstart[j] + min(cnt[j], (ci + 1) * kChunk);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int col = blockIdx.y * 1024 + 16 * lane;
+  const bool ok = col < d;  // d % 32 == 0: 16 dims are wholly in or out
+  const int bo = (ok ? col : 0) / 2;
+  float acc[16];
+#pragma unroll
+  for (int e = 0; e < 16; ++e) acc[e] = 0.f;
+  auto add = [&](float sx, float bx, uint2 w) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const uint32_t byte = ((e < 4 ? w.x : w.y) >> (8 * (e & 3))) & 255u;
+      acc[2 * e] += fmaf(sx, (float)(byte & 15u), bx);
+      acc[2 * e + 1] += fmaf(sx, (float)(byte >> 4), bx);
+    }
+  };
+  int m = m0 + wave;
+  for (; m + 28 < m1; m += 32) {
+    int pp[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) pp[e] = perm[m + 4 * e];
+    f32x4 vp[8];
+    uint2 ww[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      vp[e] = *reinterpret_cast<const f32x4 *>(vparams + 4 * (int64_t)pp[e]);
+      ww[e] = *reinterpret_cast<const uint2 *>(codes + (int64_t)pp[e] * ld + bo);
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) add(vp[e][0], vp[e][1], ww[e]);
+  }
+  for (; m < m1; m += 4) {
+    const int p = perm[m];
+    add(vparams[4 * (int64_t)p], vparams[4 * (int64_t)p + 1],
+        *reinterpret_cast<const uint2 *>(codes + (int64_t)p * ld + bo));
+  }
+#pragma unroll
+  for (int e = 0; e < 16; ++e) red[wave][lane * 17 + e] = acc[e];
+  __syncthreads();
+  if (wave == 0 && ok) {
+    float *out = partial + (int64_t)c * dp + col;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      float t = red[0][lane * 17 + e];
+      t += red[1][lane * 17 + e];
+      t += red[2][lane * 17 + e];
+      t += red[3][lane * 17 + e];
+      out[e] = t;
+    }
+  }
+}
+
 // 1-bit rows: one slice of 1024 tail dims per workgroup; lane = 16 dims (half a word)
 __global__ __launch_bounds__(256) void segsum_bits_kernel(const uint32_t *bits, int64_t wpr, int w0, int dt,
                                                           const float *alpha, const int *perm, const int *cnt,
@@ -644,6 +707,10 @@ km_status launch_update(const Points &P, const int32_t *assign, int k, void *C, 
       F = P.front;
       fld = P.d_front;
     }
+    if (P.fmt == KM_LVQ4)
+      hipLaunchKernelGGL(segsum_lvq4_kernel, dim3(w.maxchunks, (unsigned)cdiv(d, 1024)), dim3(256), 0, s,
+                         static_cast<const uint8_t *>(P.data), P.ld, P.vparams, d, w.perm, w.cnt, w.cstart, w.choff,
+                         k, static_cast<float *>(w.partial), w.dp);
     if (P.fmt == KM_BF16)
       hipLaunchKernelGGL(segsum_bf16_kernel, dim3(w.maxchunks, (unsigned)cdiv(d, 512)), dim3(256), 0, s,
                          static_cast<const uint16_t *>(P.data), P.ld, d, w.perm, w.cnt, w.cstart, w.choff, k,
@@ -676,6 +743,7 @@ km_status launch_update(const Points &P, const int32_t *assign, int k, void *C, 
   const int d0 = P.fmt == KM_HYBRID ? P.d_front : 0;
   switch (P.fmt) {
     case KM_F32:
+    case KM_LVQ4:
     case KM_BF16: hipLaunchKernelGGL(compose_kernel<KM_F32>, g, dim3(256), 0, s, w.Z, k, d, d0, P.center, w.fresh, w.cnt, C, counts); break;
     case KM_SQ8: hipLaunchKernelGGL(compose_kernel<KM_SQ8>, g, dim3(256), 0, s, w.Z, k, d, d0, P.center, w.fresh, w.cnt, C, counts); break;
     case KM_SIGN1:

@@ -54,10 +54,11 @@ def kmq():
 
 def _pts(kmq, **kw):
     base = dict(fmt=kmq.KM_F32, d=128, n=100, data=0x1000, ld=128, alpha=None, center=None, front=None, d_front=0,
-                reserved=0, raw=None, raw_ld=0)
+                reserved=0, raw=None, raw_ld=0, vparams=None)
     base.update(kw)
     return kmq.KmPoints(base["fmt"], base["d"], base["n"], base["data"], base["ld"], base["alpha"], base["center"],
-                        base["front"], base["d_front"], base["reserved"], base["raw"], base["raw_ld"])
+                        base["front"], base["d_front"], base["reserved"], base["raw"], base["raw_ld"],
+                        base["vparams"])
 
 
 FAKE = ct.c_void_p(0x10000)  # never dereferenced: validation fails first
@@ -89,6 +90,13 @@ FAKE = ct.c_void_p(0x10000)  # never dereferenced: validation fails first
     (dict(fmt=2, d=128, ld=128, raw=0x5000, raw_ld=128), -1, "not allowed for SQ8"),
     (dict(fmt=5, d=128, alpha=0x2000, raw=0x5004, raw_ld=128), -1, "raw rows"),
     (dict(fmt=5, d=128, alpha=0x2000, raw=0x5000, raw_ld=64), -1, "raw rows"),
+    (dict(fmt=6, d=128, ld=64), -1, "vparams"),
+    (dict(fmt=0, vparams=0x6000), -1, "vparams"),
+    (dict(fmt=6, d=112, ld=64, vparams=0x6000), -1, "d % 32"),
+    (dict(fmt=6, d=128, ld=48, vparams=0x6000), -1, "ld >= d/2"),
+    (dict(fmt=6, d=128, ld=72, vparams=0x6000), -1, "ld % 16"),
+    (dict(fmt=6, d=128, ld=64, vparams=0x6000, center=0x3000), -1, "no center"),
+    (dict(fmt=6, d=128, ld=64, vparams=0x6004), -1, "vparams must be 16-byte"),
 ])
 def test_points_validation(kmq, kw, status, msg):
     L = kmq.lib()
@@ -156,6 +164,10 @@ def test_quantize_and_pca_argument_checks(kmq):
     assert "d % 8" in L.km_last_error().decode()
     assert L.quantize(FAKE, 10, 64, 64, 1, FAKE, None, None, 32, None, 0, None) == -1  # bf16: no front
     assert L.quantize(FAKE, 10, 64, 64, 1, None, None, None, 0, None, 0, None) == -1  # bf16: codes NULL
+    assert L.quantize(FAKE, 10, 48, 48, 6, FAKE, FAKE, None, 0, None, 0, None) == -1  # lvq4: d % 32
+    assert "d % 32" in L.km_last_error().decode()
+    assert L.quantize(FAKE, 10, 64, 64, 6, FAKE, None, None, 0, None, 0, None) == -1  # lvq4: params NULL
+    assert L.quantize(FAKE, 10, 64, 64, 6, FAKE, ct.c_void_p(0x10008), None, 0, None, 0, None) == -1
     assert L.pca_fit_cov(FAKE, 10, 30, FAKE, FAKE, None) == -1
     assert L.pca_fit_cov(None, 10, 32, FAKE, FAKE, None) == -1
     assert L.pca_project(FAKE, 10, 32, FAKE, FAKE, 0, FAKE, None) == -1
