@@ -15,7 +15,8 @@ Other workloads (--workload 1|3|4|5) time the other configurations for
 measurement; they are not the headline line.  --workload 6 runs the default
 workload's data stored as bfloat16; --workload 7 runs the 1-bit workload's data
 through the paper's RabitQ pipeline (random rotation, SQ4 centroid codes with
-bias, last update from the raw rotated rows).
+bias, last update from the raw rotated rows); --workload 8 runs the default
+workload's data as LVQ4 codes.
 
 After the timed region, `quality` reports each final partition's full-precision
 cost (raw-vector member means), its cluster-size spread and, for the compressed
@@ -289,6 +290,50 @@ def workload_bf16(cfg, torch, km, args):
     return step, finish, None, quality
 
 
+def workload_lvq4(cfg, torch, km, args):
+    """The 1M x 768, k=1000 mixture as LVQ4 codes (measurement only).  One step: encode
+    (per-vector bias, scale, packed 4-bit codes, cached A and N), kmeans_fit on the codes
+    (centroids LVQ4-coded per pass, decode-averaging update), partition cost."""
+    spec = cfg["spec"] if args.n is None else cfg["spec"].with_n(args.n)
+    k, T = cfg["k"], cfg["iters"]
+    import synth
+    log(f"generating {spec.n} x {spec.d} mixture")
+    X = upload(spec, torch)
+    idx = synth.init_indices(spec.n, k)
+    P32 = km.points_f32(X)
+    mu = torch.empty((k, spec.d), dtype=torch.float32, device="cuda")
+
+    def step(timer):
+        codes, par = km.quantize_lvq4(X)
+        st = km.KmFitStats()
+        C, a, J = km.kmeans_fit(km.points_lvq4(codes, par, spec.d), k, T, idx, stats=st)
+        km.kmeans_update(P32, a, mu, km.KM_EMPTY_KEEP, counts=False)
+        cost = km.kmeans_cost(X, mu, a)
+        if timer is not None:
+            timer.add("lvq4", st)
+        return {"lvq4": cost, "a": a}, J
+
+    def quality(out):
+        return quality_vs_f32(km, X, k, T, idx, mu, "lvq4", out["a"])
+
+    def finish(out, timer, elapsed, K):
+        s = timer.stats["lvq4"]
+        a_ms = s["assign_ms"] / s["assign_passes"]
+        ops = 2.0 * spec.n * k * spec.d
+        ach = ops / (a_ms * 1e-3) / 1e12
+        return {"value": T * K / elapsed, "unit": "Lloyd iters/s", "dtype": "u4+i8",
+                "config": {"workload": "gmm1m_d768_k1000_lvq4", "N": spec.n, "d": spec.d, "k": k, "iters": T,
+                           "formats": ["lvq4"]},
+                "distances_per_s": (T + 1) * spec.n * k * K / elapsed,
+                "partition_cost": {"lvq4": float(out["lvq4"].item())},
+                "roofline": {"bound": "mfma", "kernel": "assign_i8_kernel<lvq4>", "achieved": ach,
+                             "peak": PEAK["int8_mfma_tops"], "unit": "TOP/s",
+                             "frac": ach / PEAK["int8_mfma_tops"], "traffic": None, "avg_launch_ms": a_ms},
+                "stages": {"lvq4": stage_summary(s)}}
+
+    return step, finish, None, quality
+
+
 def workload_sign1(cfg, torch, km, args):
     spec = cfg["spec"] if args.n is None else cfg["spec"].with_n(args.n)
     k, T = cfg["k"], cfg["iters"]
@@ -491,8 +536,8 @@ def workload_c1(cfg, torch, km, args):
 
 
 WORKLOADS = {1: workload_c1, 2: workload_c2, 3: workload_sign1, 4: workload_pca, 5: workload_hybrid,
-             6: workload_bf16, 7: workload_rabitq}
-CONFIG_OF = {6: 2, 7: 3}  # measurement-only workloads and the configuration whose data they use
+             6: workload_bf16, 7: workload_rabitq, 8: workload_lvq4}
+CONFIG_OF = {6: 2, 7: 3, 8: 2}  # measurement-only workloads and the configuration whose data they use
 
 
 def main():
