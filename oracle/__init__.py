@@ -489,3 +489,115 @@ def fit(P: dict, k: int, iters: int, init_idx, policy: int = EMPTY_SPLIT, C0=Non
     a, dist = assign(P, C)
     J.append(float(np.sum(dist, dtype=np.float64)))
     return C, a, J
+
+
+# --------------------------------------------------------------------------
+# Hierarchical k-means (Sec. 4.4 "Other Accelerators", Table 7): MESO-CLUSTERING
+# of all points into about sqrt(k) clusters, FINE-CLUSTERING by Lloyd inside each
+# meso-cluster, then optional iterations of vanilla Lloyd over all points with all
+# k centroids.  Every Lloyd run is the driver above.
+
+_ROW_KEYS = ("X", "codes", "bits", "alpha", "front", "par", "raw")
+
+
+def n_rows(P: dict) -> int:
+    for key in _ROW_KEYS:
+        if P.get(key) is not None:
+            return len(P[key])
+    raise ValueError("no point rows")
+
+
+def subset(P: dict, rows, keep_raw: bool = False):
+    """The same points' format dict restricted to `rows` (in the given order)."""
+    Q = dict(P)
+    for key in _ROW_KEYS:
+        if P.get(key) is not None:
+            Q[key] = np.ascontiguousarray(P[key][rows])
+    if not keep_raw:
+        Q.pop("raw", None)
+    return Q
+
+
+def meso_count(k: int) -> int:
+    """Number of meso-clusters: the integer nearest to sqrt(k) (never a tie for integer k)."""
+    r = 0
+    while (r + 1) * (r + 1) <= k:
+        r += 1
+    return max(1, r + 1 if k - r * r > r else r)
+
+
+def fine_counts(n_meso, k: int):
+    """Fine clusters per meso-cluster.  One for every non-empty meso-cluster, the
+    remaining k - m split in proportion to n_i - 1 (floor shares, then one more for
+    the largest remainders, ties to the smaller index).  Sums to k; k_i <= n_i."""
+    n_meso = [int(v) for v in n_meso]
+    N = sum(n_meso)
+    m = sum(1 for v in n_meso if v > 0)
+    if not m <= k <= N:
+        raise ValueError("need (non-empty meso-clusters) <= k <= n")
+    rem, cap = k - m, N - m
+    ks, rems = [], []
+    for v in n_meso:
+        w = v - 1 if v > 0 else 0
+        share, r = (divmod(rem * w, cap) if cap > 0 else (0, 0))
+        ks.append((1 if v > 0 else 0) + share)
+        rems.append(r)
+    left = k - sum(ks)
+    for i in sorted(range(len(n_meso)), key=lambda i: (-rems[i], i))[:left]:
+        ks[i] += 1
+    return np.asarray(ks, dtype=np.int32)
+
+
+def fine_init_positions(n_i: int, k_i: int):
+    """Initial fine centroids of a meso-cluster: its members (ascending point index)
+    at positions floor(j n_i / k_i), j = 0 .. k_i - 1 (distinct since k_i <= n_i)."""
+    return (np.arange(k_i, dtype=np.int64) * n_i) // k_i
+
+
+def fit_fine(P: dict, a_meso, k_meso: int, k: int, iters: int, policy: int = EMPTY_SPLIT, C0=None):
+    """FINE-CLUSTERING: Lloyd (T = iters) inside every meso-cluster i on its members,
+    with k_i fine centroids; fine centroid j of meso-cluster i is global centroid
+    off_i + j, off_i = k_0 + ... + k_{i-1}.  C0 (optional, k rows) replaces the
+    initial centroids.  Returns (C, a, k_i, J) with J[t] the in-space objective of
+    pass t summed over the meso-clusters; points with a meso id outside [0, k_meso)
+    get -1."""
+    a_meso = np.asarray(a_meso, dtype=np.int64)
+    valid = (a_meso >= 0) & (a_meso < k_meso)
+    n_i = np.bincount(a_meso[valid], minlength=k_meso)
+    k_i = fine_counts(n_i, k)
+    off = np.concatenate([[0], np.cumsum(k_i)])
+    a = np.full(len(a_meso), -1, dtype=np.int32)
+    C = None
+    J = np.zeros(iters + 1, dtype=np.float64)
+    for i in range(k_meso):
+        if n_i[i] == 0:
+            continue
+        rows = np.nonzero(a_meso == i)[0]
+        sub = subset(P, rows)
+        Ci0 = None if C0 is None else np.asarray(C0)[off[i]:off[i + 1]]
+        Ci, ai, Ji = fit(sub, int(k_i[i]), iters, fine_init_positions(len(rows), int(k_i[i])), policy, C0=Ci0)
+        if C is None:
+            C = np.empty((k, Ci.shape[1]), dtype=Ci.dtype)
+        C[off[i]:off[i + 1]] = Ci
+        a[rows] = off[i] + ai
+        J += np.asarray(Ji)
+    return C, a, k_i, J
+
+
+def fit_hier(P: dict, k: int, iters_meso: int, iters_fine: int, iters_refine: int, init_meso,
+             k_meso: int = 0, policy: int = EMPTY_SPLIT):
+    """Hierarchical k-means.  MESO: Lloyd with k_meso (default meso_count(k))
+    centroids on all points from the rows init_meso; FINE: fit_fine; REFINE:
+    iters_refine vanilla Lloyd iterations over all points with all k centroids
+    (then a final assignment), the last update from P["raw"] if given.  Meso and
+    fine use the compressed points only.  Returns (C, a, J, info) with J the
+    in-space objective of the returned partition."""
+    km = k_meso if k_meso else meso_count(k)
+    Pc = subset(P, slice(None))
+    Cm, am, Jm = fit(Pc, km, iters_meso, init_meso, policy)
+    C, a, k_i, Jf = fit_fine(Pc, am, km, k, iters_fine, policy)
+    J = float(Jf[-1])
+    if iters_refine > 0:
+        C, a, Jr = fit(P, k, iters_refine, None, policy, C0=C)
+        J = float(Jr[-1])
+    return C, a, J, {"k_meso": km, "C_meso": Cm, "a_meso": am, "J_meso": Jm, "k_fine": k_i, "J_fine": Jf}

@@ -1,6 +1,7 @@
 """The pins have teeth: plant plausible mistakes in a private copy of the oracle's
-C source (on the CPU only), rebuild it, and check that at least one pin fails for
-each planted mistake.  The real oracle is never modified.
+C source or of its Python driver (on the CPU only), rebuild or reload it, and
+check that at least one pin fails for each planted mistake.  The real oracle is
+never modified.
 """
 import importlib.util
 import os
@@ -43,7 +44,18 @@ MUTATIONS = {
                        "const float s = hi > lo ? (hi - lo) / 16.0f : 1.0f;"),
 }
 
+# mistakes in the Python driver (hierarchical k-means)
+PY_MUTATIONS = {
+    "fine_init_first_members": ("(np.arange(k_i, dtype=np.int64) * n_i) // k_i", "np.arange(k_i, dtype=np.int64)"),
+    "fine_offsets_without_leading_zero": ("off = np.concatenate([[0], np.cumsum(k_i)])", "off = np.cumsum(k_i)"),
+    "fine_remainder_ties_to_larger_index": ("key=lambda i: (-rems[i], i)", "key=lambda i: (-rems[i], -i)"),
+    "fine_share_by_n_not_n_minus_1": ("w = v - 1 if v > 0 else 0", "w = v"),
+    "refine_skipped": ("    if iters_refine > 0:\n        C, a, Jr", "    if iters_refine > 1:\n        C, a, Jr"),
+    "meso_count_floor": ("return max(1, r + 1 if k - r * r > r else r)", "return max(1, r)"),
+}
+
 PINS = [name for name in dir(pins) if name.startswith("test_")]
+PY_SRC = os.path.join(ROOT, "oracle", "__init__.py")
 
 
 def _load_mutant(tmp_path, name, old, new):
@@ -64,6 +76,19 @@ def _load_mutant(tmp_path, name, old, new):
     return mod
 
 
+def _load_py_mutant(tmp_path, name, old, new):
+    src = open(PY_SRC).read()
+    assert src.count(old) == 1, name
+    pyfile = tmp_path / f"{name}.py"
+    pyfile.write_text(src.replace(old, new))
+    spec = importlib.util.spec_from_file_location(f"oracle_py_mutant_{name}", str(pyfile))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    mod._LIB_PATH = os.path.join(ROOT, "oracle", "libkmq_oracle.so")
+    mod._lib = None
+    return mod
+
+
 def _run_pin(fn, mod):
     import inspect
     params = inspect.signature(fn).parameters
@@ -74,10 +99,12 @@ def _run_pin(fn, mod):
         fn(mod)
 
 
-@pytest.mark.parametrize("name", sorted(MUTATIONS))
+@pytest.mark.parametrize("name", sorted(MUTATIONS) + sorted(PY_MUTATIONS))
 def test_planted_mistake_is_caught(tmp_path, name):
-    old, new = MUTATIONS[name]
-    mod = _load_mutant(tmp_path, name, old, new)
+    if name in MUTATIONS:
+        mod = _load_mutant(tmp_path, name, *MUTATIONS[name])
+    else:
+        mod = _load_py_mutant(tmp_path, name, *PY_MUTATIONS[name])
     failed = []
     for pin in PINS:
         try:

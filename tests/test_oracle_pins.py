@@ -699,3 +699,146 @@ def test_lvq4_update_is_decoded_mean(orc):
         np.testing.assert_allclose(C[j], dec[a == j].mean(0), rtol=1e-6, atol=1e-6)
     np.testing.assert_array_equal(C[k - 1], C0[k - 1])
     np.testing.assert_array_equal(cnt, np.bincount(a, minlength=k))
+
+
+# --------------------------------------------------------------------------
+# Hierarchical k-means (Sec. 4.4, Table 7)
+
+def test_hier_meso_count_and_fine_counts_hand_examples(orc):
+    g = load_golden("hier_fine_counts.json")
+    for k, m in g["meso_count"].items():
+        assert orc.meso_count(int(k)) == m
+    for k in list(range(1, 2000)) + [4096, 10000, 12649, 40000]:
+        assert orc.meso_count(k) == int(np.floor(np.sqrt(k) + 0.5)), k
+    for case in g["cases"]:
+        assert orc.fine_counts(case["n"], case["k"]).tolist() == case["k_fine"], case
+
+
+@settings(max_examples=200, deadline=None)
+@given(n=st.lists(st.integers(0, 40), min_size=1, max_size=12), seed=st.integers(0, 10 ** 6))
+def test_fine_counts_properties(orc, n, seed):
+    m, N = sum(v > 0 for v in n), sum(n)
+    if m == 0:
+        return
+    k = m + seed % (N - m + 1)
+    ks = orc.fine_counts(n, k)
+    assert ks.sum() == k
+    for v, kv in zip(n, ks):
+        assert (kv > 0) == (v > 0) and kv <= v
+        if v > 0 and N > m:  # within one of the exact proportional share
+            assert abs(kv - 1 - (k - m) * (v - 1) / (N - m)) < 1
+    # order-independence of the shares up to the tie rule: a larger meso-cluster never gets fewer
+    for i in range(len(n)):
+        for j in range(len(n)):
+            if n[i] > n[j]:
+                assert ks[i] >= ks[j]
+
+
+def _blob_rows(n, d, seed, comps=6):
+    rng = np.random.default_rng(seed)
+    mu = rng.standard_normal((comps, d)) * 3
+    return (mu[rng.integers(0, comps, n)] + rng.standard_normal((n, d))).astype(np.float32)
+
+
+@pytest.mark.parametrize("fmt", ["f32", "sq8"])
+def test_fine_with_one_meso_cluster_is_plain_lloyd(orc, fmt):
+    """All points in one meso-cluster: the fine phase is Lloyd with k centroids started
+    from the rows floor(j n / k)."""
+    X = _blob_rows(300, 16, 61)
+    P = {"fmt": "f32", "X": X} if fmt == "f32" else {"fmt": "sq8", "codes": orc.sq8_encode(X, *orc.sq8_fit(X))}
+    k, T = 13, 3
+    C, a, ks, J = orc.fit_fine(P, np.zeros(300, np.int32), 1, k, T)
+    idx = np.array([j * 300 // k for j in range(k)])
+    C2, a2, J2 = orc.fit(P, k, T, idx)
+    assert ks.tolist() == [k]
+    np.testing.assert_array_equal(C, C2)
+    np.testing.assert_array_equal(a, a2)
+    assert list(J) == J2
+
+
+def _nearest(X, C, cand):
+    D = ((X[:, None, :].astype(np.float64) - C[None, cand, :].astype(np.float64)) ** 2).sum(-1)
+    return np.asarray(cand)[D.argmin(1)], D.min(1)
+
+
+def test_fine_first_update_brute_force(orc):
+    """One fine iteration (KEEP) worked out with explicit numpy: each meso-cluster's
+    members (ascending index) start from the rows at positions floor(j n_i / k_i),
+    are assigned to the nearest centroid of their own meso-cluster, the centroids
+    become member means (global ids offset by the counts before), and the final
+    assignment is again the nearest within the meso-cluster."""
+    X = _blob_rows(240, 8, 67)
+    rng = np.random.default_rng(68)
+    a_meso = rng.integers(0, 4, 240).astype(np.int32)
+    a_meso[a_meso == 3] = 2  # meso-cluster 3 is empty
+    k = 17
+    C, a, ks, J = orc.fit_fine({"fmt": "f32", "X": X}, a_meso, 4, k, 1, orc.EMPTY_KEEP)
+    n_i = np.bincount(a_meso, minlength=4)
+    assert ks.tolist() == orc.fine_counts(n_i, k).tolist() and ks[3] == 0
+    off = np.concatenate([[0], np.cumsum(ks)])
+    C_exp = np.zeros((k, 8))
+    a_exp = np.zeros(240, np.int64)
+    J_exp = 0.0
+    for i in range(3):
+        rows = np.nonzero(a_meso == i)[0]
+        seg = list(range(off[i], off[i + 1]))
+        C0 = np.zeros((k, 8), np.float32)
+        C0[seg] = X[rows[(np.arange(ks[i]) * len(rows)) // ks[i]]]
+        a0, _ = _nearest(X[rows], C0, seg)
+        for j in seg:
+            C_exp[j] = X[rows[a0 == j]].astype(np.float64).mean(0) if (a0 == j).any() else C0[j]
+        a1, d1 = _nearest(X[rows], C_exp.astype(np.float32), seg)
+        a_exp[rows] = a1
+        J_exp += d1.sum()
+    np.testing.assert_allclose(C, C_exp, rtol=1e-6, atol=1e-6)
+    np.testing.assert_array_equal(a, a_exp)
+    assert abs(J[-1] - J_exp) <= 1e-9 * J_exp
+
+
+def test_hier_refine_ends_at_the_global_nearest(orc):
+    """With refinement the returned assignment is the nearest of all k centroids and
+    J its in-space objective; without it every point stays in its meso-cluster's
+    segment of centroids (on unclustered data, where the two differ)."""
+    X = np.random.default_rng(71).standard_normal((400, 8)).astype(np.float32)
+    P = {"fmt": "f32", "X": X}
+    init = np.random.default_rng(72).choice(400, 4, replace=False)
+    C, a, J, info = orc.fit_hier(P, 16, 3, 2, 1, init)
+    a_exp, d = _nearest(X, C, list(range(16)))
+    np.testing.assert_array_equal(a, a_exp)
+    assert abs(J - d.sum()) <= 1e-9 * d.sum()
+    C0, a0, J0, info0 = orc.fit_hier(P, 16, 3, 2, 0, init)
+    assert info0["k_meso"] == 4 and info0["k_fine"].sum() == 16
+    off = np.concatenate([[0], np.cumsum(info0["k_fine"])])
+    seg_of = np.searchsorted(off, a0, side="right") - 1
+    np.testing.assert_array_equal(seg_of, info0["a_meso"])
+    assert (_nearest(X, C0, list(range(16)))[0] != a0).any()
+
+
+def test_fine_split_donor_stays_in_its_meso_cluster(orc):
+    """Meso-cluster 0: six identical rows and three fine centroids that start equal, so
+    two fine clusters come out empty; meso-cluster 1 holds a 20-member cluster.  The
+    split must take its donor inside meso-cluster 0 (the largest cluster overall is
+    in meso-cluster 1), so all three centroids of meso-cluster 0 stay at the row."""
+    rng = np.random.default_rng(73)
+    v0 = np.array([1.0, 2.0, 3.0, 4.0], np.float32)
+    w = np.array([-5.0, 1.0, 0.0, 2.0], np.float32)
+    X = np.concatenate([np.repeat(v0[None], 6, 0), np.repeat(w[None], 20, 0),
+                        (w + rng.standard_normal((10, 4)) * 0.5).astype(np.float32)])
+    a_meso = np.array([0] * 6 + [1] * 30, np.int32)
+    C, a, ks, J = orc.fit_fine({"fmt": "f32", "X": X}, a_meso, 2, 16, 1, orc.EMPTY_SPLIT)
+    assert ks.tolist() == [3, 13]
+    assert np.all(np.abs(C[:3] - v0) <= 2.0 ** -8 * np.abs(v0))
+    assert set(a[:6].tolist()) <= {0, 1, 2}
+
+
+def test_hier_one_fine_cluster_per_meso_cluster(orc):
+    """k = k_meso with every meso-cluster non-empty: each fine centroid is the mean of
+    its meso-cluster's members and the partition is the meso partition."""
+    X = _blob_rows(300, 8, 79)
+    init = np.random.default_rng(80).choice(300, 5, replace=False)
+    C, a, J, info = orc.fit_hier({"fmt": "f32", "X": X}, 5, 4, 2, 0, init, k_meso=5)
+    am = info["a_meso"]
+    assert info["k_fine"].tolist() == [1] * 5
+    np.testing.assert_array_equal(a, am)
+    for j in range(5):
+        np.testing.assert_allclose(C[j], X[am == j].astype(np.float64).mean(0), rtol=1e-6, atol=1e-6)
