@@ -250,6 +250,62 @@ km_status kmeans_fit(const km_points *P, int32_t k, int32_t iters, const int64_t
                      int32_t *assign, double *objective, int32_t policy, km_fit_stats *stats,
                      km_stream stream);
 
+/* kmeans_fine() flags */
+#define KM_FINE_C_GIVEN 1 /* C holds the initial fine centroids; otherwise they are taken from the points */
+
+/*
+ * kmeans_fine -- FINE-CLUSTERING of hierarchical k-means (Sec. 4.4, Table 7):
+ * Lloyd inside every meso-cluster, on that meso-cluster's points only.
+ *   meso_assign: DEVICE int32[n], the meso-cluster of every point; points with an
+ *     id outside [0, k_meso) take no part and get assign = -1.
+ *   Fine clusters per meso-cluster (k_i; the paper sizes them by the meso-cluster
+ *     size n_i without making them sum to k): one for every non-empty meso-cluster,
+ *     the other k - m (m = number of non-empty meso-clusters) shared in proportion
+ *     to n_i - 1: floor shares, then one more for the largest remainders (ties to
+ *     the smaller meso index).  Fine centroid j of meso-cluster i is centroid
+ *     off_i + j of C, off_i = k_0 + ... + k_{i-1}.  KM_EINVAL unless m <= k <= the
+ *     number of points with a valid meso id.
+ *   STEP 1 (unless flags has KM_FINE_C_GIVEN): centroid off_i + j = the member of
+ *     meso-cluster i at position floor(j n_i / k_i) in ascending point order.
+ *   Then `iters` x (STEP 2 against the point's own meso-cluster's centroids, STEP 3
+ *   as in kmeans_update, where an empty fine cluster takes its split donor from its
+ *   own meso-cluster), and a final STEP 2.
+ *   C: k centroids (in, when KM_FINE_C_GIVEN; out), as in kmeans_assign.
+ *   assign: int32[n] global fine-centroid ids.  k_fine (nullable, HOST int32[k_meso])
+ *   receives k_i.  objective (nullable): DEVICE double[1], the in-space objective of
+ *   the final pass.
+ *   The call waits for `stream` once, to read the meso-cluster sizes; it keeps a
+ *   meso-ordered copy of the points in scratch memory while it runs.
+ */
+km_status kmeans_fine(const km_points *P, const int32_t *meso_assign, int32_t k_meso, int32_t k, int32_t iters,
+                      int32_t flags, void *C, int32_t *assign, int32_t *k_fine, double *objective, int32_t policy,
+                      km_stream stream);
+
+typedef struct km_hier_params {
+  int32_t k_meso;       /* meso-clusters; 0 = the integer nearest to sqrt(k) */
+  int32_t iters_meso;   /* Lloyd iterations of MESO-CLUSTERING */
+  int32_t iters_fine;   /* Lloyd iterations inside every meso-cluster */
+  int32_t iters_refine; /* vanilla Lloyd iterations over all points and all k centroids afterwards; 0 = none */
+} km_hier_params;
+
+/*
+ * kmeans_fit_hier -- hierarchical k-means (Sec. 4.4, Table 7): MESO-CLUSTERING =
+ * kmeans_fit with k_meso centroids from the rows init_meso (HOST int64[k_meso],
+ * distinct) for iters_meso iterations; FINE-CLUSTERING = kmeans_fine with
+ * iters_fine iterations; then, if iters_refine > 0, kmeans_fit from the fine
+ * centroids with iters_refine iterations over all points (its last update from
+ * P->raw when set; the meso and fine phases use the compressed points only).
+ *   C, assign: out, as in kmeans_fit.  k_fine: as in kmeans_fine.
+ *   objective (nullable): DEVICE double[1], the in-space objective of the returned
+ *   partition.  stats (nullable, HOST): stage times summed over the three phases;
+ *   phase_ms (nullable, HOST double[3]): device time of the meso, fine and refine
+ *   phases.  Either makes the call wait for `stream` at the end; the fine phase
+ *   always waits once (see kmeans_fine).
+ */
+km_status kmeans_fit_hier(const km_points *P, int32_t k, const km_hier_params *hp, const int64_t *init_meso, void *C,
+                          int32_t *assign, int32_t *k_fine, double *objective, int32_t policy, km_fit_stats *stats,
+                          double *phase_ms, km_stream stream);
+
 /*
  * kmeans_cost -- sum over points of ||x - c_{assign(x)}||^2 in fp64 for fp32
  * points (the full-precision partition cost when C holds the member means of the

@@ -19,9 +19,10 @@ LIB_PATH = os.path.join(HERE, "libkmq.so")
 KM_F32, KM_BF16, KM_SQ8, KM_SIGN1, KM_HYBRID, KM_RABITQ, KM_LVQ4 = 0, 1, 2, 3, 4, 5, 6
 KM_EMPTY_SPLIT, KM_EMPTY_KEEP = 0, 1
 KM_Q_FIT_PARAMS = 1
+KM_FINE_C_GIVEN = 1
 STATUS = {0: "KM_OK", -1: "KM_EINVAL", -2: "KM_EUNSUPPORTED", -3: "KM_ENOMEM", -4: "KM_EDEVICE"}
 EXPORTS = ("quantize", "rabitq_encode", "pca_fit_cov", "pca_project", "kmeans_assign", "kmeans_update",
-           "kmeans_fit", "kmeans_cost", "km_last_error", "km_release")
+           "kmeans_fit", "kmeans_fine", "kmeans_fit_hier", "kmeans_cost", "km_last_error", "km_release")
 
 
 class KmqError(RuntimeError):
@@ -45,6 +46,11 @@ class KmFitStats(ct.Structure):
         return {f: getattr(self, f) for f, _ in self._fields_}
 
 
+class KmHierParams(ct.Structure):
+    _fields_ = [("k_meso", ct.c_int32), ("iters_meso", ct.c_int32), ("iters_fine", ct.c_int32),
+                ("iters_refine", ct.c_int32)]
+
+
 _lib = None
 
 
@@ -65,6 +71,9 @@ def lib():
             "kmeans_assign": [ct.POINTER(KmPoints), vp, i32, vp, vp, vp, vp],
             "kmeans_update": [ct.POINTER(KmPoints), vp, i32, vp, vp, i32, vp],
             "kmeans_fit": [ct.POINTER(KmPoints), i32, i32, vp, vp, vp, vp, i32, ct.POINTER(KmFitStats), vp],
+            "kmeans_fine": [ct.POINTER(KmPoints), vp, i32, i32, i32, i32, vp, vp, vp, vp, i32, vp],
+            "kmeans_fit_hier": [ct.POINTER(KmPoints), i32, ct.POINTER(KmHierParams), vp, vp, vp, vp, vp, i32,
+                                ct.POINTER(KmFitStats), vp, vp],
             "kmeans_cost": [vp, i64, i32, i64, vp, i32, vp, vp, vp],
             "km_release": [],
         }
@@ -354,6 +363,53 @@ def kmeans_fit(P: Points, k: int, iters: int, init_idx=None, C: torch.Tensor | N
     _check(lib().kmeans_fit(P.ref, k, iters, idx_p, _ptr(C), _ptr(a), _ptr(obj), policy,
                             ct.byref(stats) if stats is not None else None, _stream()))
     return C, a, obj
+
+
+def kmeans_fine(P: Points, meso_assign: torch.Tensor, k_meso: int, k: int, iters: int,
+                C: torch.Tensor | None = None, policy: int = KM_EMPTY_SPLIT, objective: bool = False):
+    """FINE-CLUSTERING inside each meso-cluster (hierarchical k-means).  C given: the
+    initial fine centroids (k rows); otherwise they are taken from the points.
+    Returns (C, assign int32[n], k_fine numpy int32[k_meso], objective double[1] or None)."""
+    _dev(meso_assign, torch.int32, "meso_assign", 1)
+    if meso_assign.shape[0] != P.n:
+        raise ValueError("meso_assign must hold n ids")
+    flags = 0
+    if C is None:
+        C = torch.empty((k, P.d), dtype=P.centroid_dtype(), device=P.device)
+    else:
+        if _check_C(P, C) != k:
+            raise ValueError("C must hold k rows")
+        flags = KM_FINE_C_GIVEN
+    a = torch.empty(P.n, dtype=torch.int32, device=P.device)
+    kf = np.zeros(k_meso, dtype=np.int32)
+    obj = torch.empty(1, dtype=torch.float64, device=P.device) if objective else None
+    _check(lib().kmeans_fine(P.ref, _ptr(meso_assign), k_meso, k, iters, flags, _ptr(C), _ptr(a),
+                             kf.ctypes.data_as(ct.c_void_p), _ptr(obj), policy, _stream()))
+    return C, a, kf, obj
+
+
+def kmeans_fit_hier(P: Points, k: int, init_meso, iters_meso: int, iters_fine: int, iters_refine: int = 0,
+                    k_meso: int = 0, policy: int = KM_EMPTY_SPLIT, objective: bool = True,
+                    stats: KmFitStats | None = None, phases: bool = False):
+    """Hierarchical k-means: meso Lloyd with k_meso (0 = round(sqrt(k))) centroids from
+    the rows init_meso, Lloyd inside every meso-cluster, optional vanilla refinement.
+    Returns (C, assign, k_fine numpy int32[k_meso], objective double[1] or None,
+    phase times [meso, fine, refine] in ms or None)."""
+    idx = np.ascontiguousarray(np.asarray(init_meso, dtype=np.int64))
+    km = k_meso if k_meso else len(idx)
+    if idx.ndim != 1 or len(idx) != km:
+        raise ValueError("init_meso must hold k_meso indices")
+    hp = KmHierParams(k_meso, iters_meso, iters_fine, iters_refine)
+    C = torch.empty((k, P.d), dtype=P.centroid_dtype(), device=P.device)
+    a = torch.empty(P.n, dtype=torch.int32, device=P.device)
+    kf = np.zeros(len(idx), dtype=np.int32)
+    obj = torch.empty(1, dtype=torch.float64, device=P.device) if objective else None
+    ph = np.zeros(3, dtype=np.float64) if phases else None
+    _check(lib().kmeans_fit_hier(P.ref, k, ct.byref(hp), idx.ctypes.data_as(ct.c_void_p), _ptr(C), _ptr(a),
+                                 kf.ctypes.data_as(ct.c_void_p), _ptr(obj), policy,
+                                 ct.byref(stats) if stats is not None else None,
+                                 ph.ctypes.data_as(ct.c_void_p) if phases else None, _stream()))
+    return C, a, kf, obj, ph
 
 
 def kmeans_cost(X: torch.Tensor, C: torch.Tensor, assign: torch.Tensor):

@@ -382,30 +382,34 @@ class StageClock {
 enum { kStAssign = 0, kStPrep = 1, kStUpdate = 2, kStOther = 3 };
 }  // namespace
 
-km_status kmeans_fit(const km_points *P, int32_t k, int32_t iters, const int64_t *init_idx, void *C, int32_t *assign,
-                     double *objective, int32_t policy, km_fit_stats *stats, km_stream stream) {
-  g_err[0] = 0;
-  Points p;
-  km_status st = check_points(P, &p);
-  if (st != KM_OK) return st;
-  st = check_centroids(p, C, k);
-  if (st != KM_OK) return st;
-  KMQ_CHECK(assign != nullptr, KM_EINVAL, "assign is NULL");
-  KMQ_CHECK(k <= p.n, KM_EINVAL, "k = %d exceeds n = %lld", k, (long long)p.n);
-  KMQ_CHECK(iters >= 0, KM_EINVAL, "iters = %d must be >= 0", iters);
-  KMQ_CHECK(policy == KM_EMPTY_SPLIT || policy == KM_EMPTY_KEEP, KM_EINVAL, "unknown empty-cluster policy %d", policy);
-  if (init_idx) {
-    try {
-      std::vector<int64_t> v(init_idx, init_idx + k);
-      std::sort(v.begin(), v.end());
-      KMQ_CHECK(v.front() >= 0 && v.back() < p.n, KM_EINVAL, "init_idx outside [0, n)");
-      KMQ_CHECK(std::adjacent_find(v.begin(), v.end()) == v.end(), KM_EINVAL, "init_idx holds duplicates");
-    } catch (const std::bad_alloc &) {
-      set_error("host allocation failed");
-      return KM_ENOMEM;
-    }
+#define KMQ_STAGE(clk, stage, expr)   \
+  do {                                \
+    st = (clk).begin(stage);          \
+    if (st != KM_OK) return st;       \
+    st = (expr);                      \
+    if (st != KM_OK) return st;       \
+    st = (clk).end();                 \
+    if (st != KM_OK) return st;       \
+  } while (0)
+
+static km_status check_init_idx(const int64_t *init_idx, int k, int64_t n) {
+  try {
+    std::vector<int64_t> v(init_idx, init_idx + k);
+    std::sort(v.begin(), v.end());
+    KMQ_CHECK(v.front() >= 0 && v.back() < n, KM_EINVAL, "init_idx outside [0, n)");
+    KMQ_CHECK(std::adjacent_find(v.begin(), v.end()) == v.end(), KM_EINVAL, "init_idx holds duplicates");
+  } catch (const std::bad_alloc &) {
+    set_error("host allocation failed");
+    return KM_ENOMEM;
   }
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  return KM_OK;
+}
+
+// Lloyd on validated arguments: STEP 1 from init_idx (HOST; NULL = C holds the
+// start), iters x (STEP 2, STEP 3), final STEP 2; objective: DEVICE double[iters + 1].
+static km_status fit_impl(const Points &p, int k, int iters, const int64_t *init_idx, void *C, int32_t *assign,
+                          double *objective, int policy, StageClock &clk, hipStream_t s) {
+  km_status st;
   const size_t b_prep = al(prep_bytes(p, k));
   const size_t b_upd = al(std::max(update_bytes(p, k), p.raw ? update_bytes(raw_points(p), k) : (size_t)0));
   const size_t b_score = objective ? al(sizeof(float) * (size_t)p.n) : 0;
@@ -422,43 +426,292 @@ km_status kmeans_fit(const km_points *P, int32_t k, int32_t iters, const int64_t
   float *xc = reinterpret_cast<float *>(w + b_prep + b_upd + b_score);
   double *part = reinterpret_cast<double *>(w + b_prep + b_upd + b_score + b_xc);
   int64_t *didx = reinterpret_cast<int64_t *>(w + b_prep + b_upd + b_score + b_xc + b_part);
-  (void)centroid_bytes;
+  if (init_idx) {
+    KMQ_HIP(hipMemcpyAsync(didx, init_idx, sizeof(int64_t) * (size_t)k, hipMemcpyHostToDevice, s));
+    KMQ_STAGE(clk, kStOther, launch_gather_init(p, didx, k, C, s));
+  }
+  if (objective) KMQ_STAGE(clk, kStOther, launch_xconst(p, xc, s));
+  CentroidPrep cp;
+  for (int it = 0; it <= iters; ++it) {
+    KMQ_STAGE(clk, kStPrep, launch_prep(p, C, k, wprep, &cp, s));
+    KMQ_STAGE(clk, kStAssign, launch_assign(p, C, cp, k, assign, sc, s));
+    if (objective)
+      KMQ_STAGE(clk, kStOther, launch_objective(p, xc, sc, p.n, objective + it, part, objective_blocks(p.n), s));
+    if (it == iters) break;  // the last pass only assigns (the final STEP 2)
+    if (p.raw && it == iters - 1) {  // last update from the raw rows (Sec. 4.1)
+      KMQ_STAGE(clk, kStUpdate, launch_update(raw_points(p), assign, k, C, nullptr, policy, wupd, s));
+    } else {
+      KMQ_STAGE(clk, kStUpdate, launch_update(p, assign, k, C, nullptr, policy, wupd, s));
+    }
+  }
+  return KM_OK;
+}
 
+// Nearest integer to sqrt(k) (k is never the square of a half-integer).
+static int meso_count(int k) {
+  int r = 0;
+  while ((int64_t)(r + 1) * (r + 1) <= k) ++r;
+  return std::max(1, (int64_t)k - (int64_t)r * r > r ? r + 1 : r);
+}
+
+// Fine clusters per meso-cluster: one per non-empty meso-cluster, the other k - m
+// shared in proportion to n_i - 1 (floor shares, then one more for the largest
+// remainders, ties to the smaller index).  Sums to k, k_i <= n_i, when m <= k <= N.
+static std::vector<int> fine_counts(const std::vector<int64_t> &n_i, int k) {
+  const int km = (int)n_i.size();
+  int64_t N = 0, m = 0;
+  for (int64_t v : n_i) {
+    N += v;
+    m += v > 0;
+  }
+  const int64_t rem = k - m, cap = N - m;
+  std::vector<int> ks(km);
+  std::vector<int64_t> r(km, 0);
+  int64_t given = 0;
+  for (int i = 0; i < km; ++i) {
+    const int64_t w = n_i[i] > 0 ? n_i[i] - 1 : 0;
+    const int64_t share = cap > 0 ? rem * w / cap : 0;
+    r[i] = cap > 0 ? rem * w % cap : 0;
+    ks[i] = (int)((n_i[i] > 0 ? 1 : 0) + share);
+    given += ks[i];
+  }
+  std::vector<int> order(km);
+  for (int i = 0; i < km; ++i) order[i] = i;
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return r[a] > r[b]; });
+  for (int64_t left = k - given, t = 0; left > 0; --left, ++t) ks[order[t]] += 1;
+  return ks;
+}
+
+// FINE-CLUSTERING (Sec. 4.4) on validated arguments.
+static km_status fine_impl(const Points &p, const int32_t *meso, int k_meso, int k, int iters, bool c_given,
+                           void *C, int32_t *assign, int32_t *k_fine, double *objective, int policy, StageClock &clk,
+                           hipStream_t s) {
+  km_status st;
+  // meso-cluster order of the points (stable) and the meso-cluster sizes
+  Scratch wsort(s);
+  st = wsort.alloc(sort_bytes(p.n, k_meso));
+  if (st != KM_OK) return st;
+  SortOut so{};
+  KMQ_STAGE(clk, kStOther, launch_cluster_sort(meso, p.n, k_meso, wsort.get(), &so, s));
+  std::vector<int> cnt(k_meso);
+  KMQ_HIP(hipMemcpyAsync(cnt.data(), so.cnt, sizeof(int) * (size_t)k_meso, hipMemcpyDeviceToHost, s));
+  KMQ_HIP(hipStreamSynchronize(s));
+  std::vector<int64_t> n_i(cnt.begin(), cnt.end());
+  int64_t N = 0, m = 0;
+  for (int64_t v : n_i) {
+    N += v;
+    m += v > 0;
+  }
+  KMQ_CHECK(N >= 1, KM_EINVAL, "no point has a meso-cluster id in [0, %d)", k_meso);
+  KMQ_CHECK(m <= k && k <= N, KM_EINVAL,
+            "k = %d must lie between the number of non-empty meso-clusters (%lld) and the number of points with a "
+            "meso-cluster (%lld)", k, (long long)m, (long long)N);
+  const std::vector<int> kf = fine_counts(n_i, k);
+  std::vector<int64_t> start(k_meso), off(k_meso + 1, 0);
+  for (int i = 0, acc = 0; i < k_meso; ++i) {
+    start[i] = acc;
+    acc += cnt[i];
+    off[i + 1] = off[i] + kf[i];
+  }
+  // host tables: initial rows (in meso order) and each centroid's segment
+  std::vector<int64_t> idx(k);
+  std::vector<int> seg(2 * (size_t)k);
+  for (int i = 0; i < k_meso; ++i)
+    for (int j = 0; j < kf[i]; ++j) {
+      idx[off[i] + j] = start[i] + (int64_t)j * n_i[i] / kf[i];
+      seg[off[i] + j] = (int)off[i];
+      seg[k + off[i] + j] = (int)off[i + 1];
+    }
+  // the points of each meso-cluster as one contiguous run of rows
+  Points q{};
+  const size_t b_perm = al(permuted_bytes(p, N));
+  const size_t b_prep = al(prep_bytes(slice_points(p, 0, N), k));
+  const size_t b_upd = al(update_bytes(slice_points(p, 0, N), k));
+  const size_t b_a = al(sizeof(int32_t) * (size_t)N);
+  const size_t b_score = objective ? al(sizeof(float) * (size_t)N) : 0;
+  const size_t b_xc = objective ? al(sizeof(float) * (size_t)N) : 0;
+  const size_t b_part = objective ? al(sizeof(double) * (size_t)objective_blocks(N)) : 0;
+  const size_t b_idx = al(sizeof(int64_t) * (size_t)k);
+  const size_t b_seg = al(sizeof(int) * 2 * (size_t)k);
+  Scratch ws(s);
+  st = ws.alloc(b_perm + b_prep + b_upd + b_a + b_score + b_xc + b_part + b_idx + b_seg);
+  if (st != KM_OK) return st;
+  uint8_t *w = ws.get();
+  uint8_t *wperm = w;
+  uint8_t *wprep = wperm + b_perm;
+  uint8_t *wupd = wprep + b_prep;
+  int32_t *ap = reinterpret_cast<int32_t *>(wupd + b_upd);
+  float *sc = objective ? reinterpret_cast<float *>(wupd + b_upd + b_a) : nullptr;
+  float *xc = reinterpret_cast<float *>(wupd + b_upd + b_a + b_score);
+  double *part = reinterpret_cast<double *>(wupd + b_upd + b_a + b_score + b_xc);
+  int64_t *didx = reinterpret_cast<int64_t *>(wupd + b_upd + b_a + b_score + b_xc + b_part);
+  int *dseg = reinterpret_cast<int *>(wupd + b_upd + b_a + b_score + b_xc + b_part + b_idx);
+  KMQ_STAGE(clk, kStOther, launch_permute_points(p, so.perm, N, wperm, &q, s));
+  KMQ_HIP(hipMemcpyAsync(dseg, seg.data(), sizeof(int) * seg.size(), hipMemcpyHostToDevice, s));
+  if (!c_given) {
+    KMQ_HIP(hipMemcpyAsync(didx, idx.data(), sizeof(int64_t) * (size_t)k, hipMemcpyHostToDevice, s));
+    KMQ_STAGE(clk, kStOther, launch_gather_init(q, didx, k, C, s));
+  }
+  const size_t crow = p.fmt == KM_SQ8 ? (size_t)p.d : sizeof(float) * (size_t)p.d;
+  CentroidPrep cp;
+  for (int it = 0; it <= iters; ++it) {
+    KMQ_STAGE(clk, kStPrep, launch_prep(q, C, k, wprep, &cp, s));
+    st = clk.begin(kStAssign);
+    if (st != KM_OK) return st;
+    for (int i = 0; i < k_meso; ++i) {  // each meso-cluster against its own fine centroids
+      if (n_i[i] == 0) continue;
+      st = launch_assign(slice_points(q, start[i], n_i[i]), static_cast<const uint8_t *>(C) + off[i] * crow,
+                         prep_slice(q, cp, (int)off[i], start[i]), kf[i], ap + start[i],
+                         sc ? sc + start[i] : nullptr, s, (int)off[i]);
+      if (st != KM_OK) return st;
+    }
+    st = clk.end();
+    if (st != KM_OK) return st;
+    if (it == iters) break;
+    KMQ_STAGE(clk, kStUpdate, launch_update(q, ap, k, C, nullptr, policy, wupd, s, dseg, dseg + k));
+  }
+  if (objective) {
+    KMQ_STAGE(clk, kStOther, launch_xconst(q, xc, s));
+    KMQ_STAGE(clk, kStOther, launch_objective(q, xc, sc, N, objective, part, objective_blocks(N), s));
+  }
+  KMQ_STAGE(clk, kStOther, launch_scatter_assign(so.perm, ap, N, p.n, assign, s));
+  if (k_fine) std::copy(kf.begin(), kf.end(), k_fine);
+  return KM_OK;
+}
+
+
+km_status kmeans_fit(const km_points *P, int32_t k, int32_t iters, const int64_t *init_idx, void *C, int32_t *assign,
+                     double *objective, int32_t policy, km_fit_stats *stats, km_stream stream) {
+  g_err[0] = 0;
+  Points p;
+  km_status st = check_points(P, &p);
+  if (st != KM_OK) return st;
+  st = check_centroids(p, C, k);
+  if (st != KM_OK) return st;
+  KMQ_CHECK(assign != nullptr, KM_EINVAL, "assign is NULL");
+  KMQ_CHECK(k <= p.n, KM_EINVAL, "k = %d exceeds n = %lld", k, (long long)p.n);
+  KMQ_CHECK(iters >= 0, KM_EINVAL, "iters = %d must be >= 0", iters);
+  KMQ_CHECK(policy == KM_EMPTY_SPLIT || policy == KM_EMPTY_KEEP, KM_EINVAL, "unknown empty-cluster policy %d", policy);
+  if (init_idx) {
+    st = check_init_idx(init_idx, k, p.n);
+    if (st != KM_OK) return st;
+  }
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  (void)centroid_bytes;
   try {
     StageClock clk(stats != nullptr, s);
-#define KMQ_STAGE(stage, expr)            \
-  do {                                    \
-    st = clk.begin(stage);                \
-    if (st != KM_OK) return st;           \
-    st = (expr);                          \
-    if (st != KM_OK) return st;           \
-    st = clk.end();                       \
-    if (st != KM_OK) return st;           \
-  } while (0)
-    if (init_idx) {
-      KMQ_HIP(hipMemcpyAsync(didx, init_idx, sizeof(int64_t) * (size_t)k, hipMemcpyHostToDevice, s));
-      KMQ_STAGE(kStOther, launch_gather_init(p, didx, k, C, s));
-    }
-    if (objective) KMQ_STAGE(kStOther, launch_xconst(p, xc, s));
-    CentroidPrep cp;
-    for (int it = 0; it <= iters; ++it) {
-      KMQ_STAGE(kStPrep, launch_prep(p, C, k, wprep, &cp, s));
-      KMQ_STAGE(kStAssign, launch_assign(p, C, cp, k, assign, sc, s));
-      if (objective)
-        KMQ_STAGE(kStOther, launch_objective(p, xc, sc, p.n, objective + it, part, objective_blocks(p.n), s));
-      if (it == iters) break;  // the last pass only assigns (the final STEP 2)
-      if (p.raw && it == iters - 1) {  // last update from the raw rows (Sec. 4.1)
-        KMQ_STAGE(kStUpdate, launch_update(raw_points(p), assign, k, C, nullptr, policy, wupd, s));
-      } else {
-        KMQ_STAGE(kStUpdate, launch_update(p, assign, k, C, nullptr, policy, wupd, s));
-      }
-    }
-#undef KMQ_STAGE
+    st = fit_impl(p, k, iters, init_idx, C, assign, objective, policy, clk, s);
+    if (st != KM_OK) return st;
     if (stats) {
       st = clk.collect(stats);
       if (st != KM_OK) return st;
       stats->assign_passes = iters + 1;
       stats->updates = iters;
+    }
+  } catch (const std::bad_alloc &) {
+    set_error("host allocation failed");
+    return KM_ENOMEM;
+  }
+  return KM_OK;
+}
+
+km_status kmeans_fine(const km_points *P, const int32_t *meso_assign, int32_t k_meso, int32_t k, int32_t iters,
+                      int32_t flags, void *C, int32_t *assign, int32_t *k_fine, double *objective, int32_t policy,
+                      km_stream stream) {
+  g_err[0] = 0;
+  Points p;
+  km_status st = check_points(P, &p);
+  if (st != KM_OK) return st;
+  st = check_centroids(p, C, k);
+  if (st != KM_OK) return st;
+  KMQ_CHECK(meso_assign != nullptr && assign != nullptr, KM_EINVAL, "meso_assign or assign is NULL");
+  KMQ_CHECK(k_meso >= 1, KM_EINVAL, "k_meso = %d must be >= 1", k_meso);
+  KMQ_CHECK(iters >= 0, KM_EINVAL, "iters = %d must be >= 0", iters);
+  KMQ_CHECK((flags & ~KM_FINE_C_GIVEN) == 0, KM_EINVAL, "unknown flags 0x%x", flags);
+  KMQ_CHECK(policy == KM_EMPTY_SPLIT || policy == KM_EMPTY_KEEP, KM_EINVAL, "unknown empty-cluster policy %d", policy);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  try {
+    StageClock clk(false, s);
+    return fine_impl(p, meso_assign, k_meso, k, iters, (flags & KM_FINE_C_GIVEN) != 0, C, assign, k_fine, objective,
+                     policy, clk, s);
+  } catch (const std::bad_alloc &) {
+    set_error("host allocation failed");
+    return KM_ENOMEM;
+  }
+}
+
+km_status kmeans_fit_hier(const km_points *P, int32_t k, const km_hier_params *hp, const int64_t *init_meso, void *C,
+                          int32_t *assign, int32_t *k_fine, double *objective, int32_t policy, km_fit_stats *stats,
+                          double *phase_ms, km_stream stream) {
+  g_err[0] = 0;
+  Points p;
+  km_status st = check_points(P, &p);
+  if (st != KM_OK) return st;
+  st = check_centroids(p, C, k);
+  if (st != KM_OK) return st;
+  KMQ_CHECK(hp != nullptr && init_meso != nullptr && assign != nullptr, KM_EINVAL,
+            "hp, init_meso or assign is NULL");
+  KMQ_CHECK(k <= p.n, KM_EINVAL, "k = %d exceeds n = %lld", k, (long long)p.n);
+  const int km = hp->k_meso ? hp->k_meso : meso_count(k);
+  KMQ_CHECK(km >= 1 && km <= k, KM_EINVAL, "k_meso = %d must lie in [1, k]", km);
+  KMQ_CHECK(hp->iters_meso >= 0 && hp->iters_fine >= 0 && hp->iters_refine >= 0, KM_EINVAL,
+            "iteration counts must be >= 0");
+  KMQ_CHECK(policy == KM_EMPTY_SPLIT || policy == KM_EMPTY_KEEP, KM_EINVAL, "unknown empty-cluster policy %d", policy);
+  st = check_init_idx(init_meso, km, p.n);
+  if (st != KM_OK) return st;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  Points pc = p;  // meso and fine phases cluster the compressed points only
+  pc.raw = nullptr;
+  pc.raw_ld = 0;
+  const int R = hp->iters_refine;
+  const size_t b_cm = al(centroid_bytes(p, km));
+  const size_t b_am = al(sizeof(int32_t) * (size_t)p.n);
+  const size_t b_obj = (objective && R > 0) ? al(sizeof(double) * (size_t)(R + 1)) : 0;
+  Scratch ws(s);
+  st = ws.alloc(b_cm + b_am + b_obj);
+  if (st != KM_OK) return st;
+  void *Cm = ws.get();
+  int32_t *am = reinterpret_cast<int32_t *>(ws.get() + b_cm);
+  double *objr = reinterpret_cast<double *>(ws.get() + b_cm + b_am);
+  try {
+    StageClock clk(stats != nullptr, s);
+    hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
+    struct EvGuard {
+      hipEvent_t *e;
+      ~EvGuard() {
+        for (int i = 0; i < 4; ++i)
+          if (e[i]) (void)hipEventDestroy(e[i]);
+      }
+    } guard{ev};
+    if (phase_ms)
+      for (int i = 0; i < 4; ++i) KMQ_HIP(hipEventCreate(&ev[i]));
+    if (phase_ms) KMQ_HIP(hipEventRecord(ev[0], s));
+    st = fit_impl(pc, km, hp->iters_meso, init_meso, Cm, am, nullptr, policy, clk, s);
+    if (st != KM_OK) return st;
+    if (phase_ms) KMQ_HIP(hipEventRecord(ev[1], s));
+    st = fine_impl(pc, am, km, k, hp->iters_fine, false, C, assign, k_fine, R > 0 ? nullptr : objective, policy, clk,
+                   s);
+    if (st != KM_OK) return st;
+    if (phase_ms) KMQ_HIP(hipEventRecord(ev[2], s));
+    if (R > 0) {
+      st = fit_impl(p, k, R, nullptr, C, assign, objective ? objr : nullptr, policy, clk, s);
+      if (st != KM_OK) return st;
+      if (objective) KMQ_HIP(hipMemcpyAsync(objective, objr + R, sizeof(double), hipMemcpyDeviceToDevice, s));
+    }
+    if (phase_ms) {
+      KMQ_HIP(hipEventRecord(ev[3], s));
+      KMQ_HIP(hipEventSynchronize(ev[3]));
+      for (int i = 0; i < 3; ++i) {
+        float t = 0.f;
+        KMQ_HIP(hipEventElapsedTime(&t, ev[i], ev[i + 1]));
+        phase_ms[i] = t;
+      }
+    }
+    if (stats) {
+      st = clk.collect(stats);
+      if (st != KM_OK) return st;
+      stats->assign_passes = hp->iters_meso + 1 + hp->iters_fine + 1 + (R > 0 ? R + 1 : 0);
+      stats->updates = hp->iters_meso + hp->iters_fine + R;
     }
   } catch (const std::bad_alloc &) {
     set_error("host allocation failed");

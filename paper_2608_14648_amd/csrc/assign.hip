@@ -68,6 +68,7 @@ struct AssignArgs {
   int k;
   int32_t *assign;
   float *score;
+  int aoff;  // added to every stored centroid index (a slice of a larger centroid set)
   // centroid-tile groups: workgroup (pt, g) scans centroid tiles g, g + ngroups, ...
   // of point tile pt and merges its argmin into keys[] (used when ngroups > 1)
   int ngroups;
@@ -564,7 +565,7 @@ __global__ __launch_bounds__(kThreads, Blocking<FMT>::MINB) void assign_kernel(A
         if (A.keys) {
           if constexpr (!Cfg<FMT>::kIntScore) atomicMin(A.keys + p, score_key(best[pb], bidx[pb]));
         } else {
-          A.assign[p] = bidx[pb];
+          A.assign[p] = bidx[pb] + A.aoff;
           if (A.score) A.score[p] = (float)best[pb];
         }
       }
@@ -578,11 +579,11 @@ __global__ __launch_bounds__(256) void keys_init_kernel(unsigned long long *keys
 }
 
 __global__ __launch_bounds__(256) void keys_unpack_kernel(const unsigned long long *keys, int64_t n, int32_t *assign,
-                                                          float *score) {
+                                                          float *score, int aoff) {
   const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (p >= n) return;
   const unsigned long long key = keys[p];
-  assign[p] = (int32_t)(uint32_t)key;
+  assign[p] = (int32_t)(uint32_t)key + aoff;
   if (score) score[p] = key_score(key);
 }
 
@@ -931,7 +932,7 @@ __global__ __launch_bounds__(k8Threads, 1) void assign_i8_kernel(AssignArgs A) {
       }
       const int64_t p = p0 + pc;
       if (p < A.n) {
-        A.assign[p] = bidx[pb];
+        A.assign[p] = bidx[pb] + A.aoff;
         if (A.score) A.score[p] = (float)best[pb];
       }
     }
@@ -1121,7 +1122,7 @@ __global__ __launch_bounds__(kBT, 1) void assign_bits_kernel(AssignArgs A) {
     }
     const int64_t p = p0 + wave * 64 + pb * 32 + r;
     if (h == 0 && p < A.n) {
-      A.assign[p] = bidx[pb];
+      A.assign[p] = bidx[pb] + A.aoff;
       if (A.score) A.score[p] = best[pb];
     }
   }
@@ -1484,8 +1485,9 @@ int assign_groups(const Points &P, int k) {
 
 template <int FMT>
 km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp, int k, int32_t *assign,
-                          float *score, hipStream_t s) {
+                          float *score, hipStream_t s, int aoff) {
   AssignArgs A{};
+  A.aoff = aoff;
   A.ngroups = 1;
   A.n = P.n;
   A.k = k;
@@ -1553,7 +1555,7 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
       A.keys = cp.keys;
       hipLaunchKernelGGL(keys_init_kernel, gp, dim3(256), 0, s, cp.keys, P.n);
       hipLaunchKernelGGL(assign_kernel<FMT>, dim3((unsigned)(cdiv(npt, 8) * 8 * ng)), dim3(kThreads), 0, s, A);
-      hipLaunchKernelGGL(keys_unpack_kernel, gp, dim3(256), 0, s, cp.keys, P.n, assign, score);
+      hipLaunchKernelGGL(keys_unpack_kernel, gp, dim3(256), 0, s, cp.keys, P.n, assign, score, aoff);
     } else {
       hipLaunchKernelGGL(assign_kernel<FMT>, dim3((unsigned)npt), dim3(kThreads), 0, s, A);
     }
@@ -1634,17 +1636,34 @@ km_status launch_prep(const Points &P, const void *C, int k, void *ws, CentroidP
 }
 
 km_status launch_assign(const Points &P, const void *C, const CentroidPrep &cp, int k, int32_t *assign,
-                        float *score, hipStream_t s) {
+                        float *score, hipStream_t s, int aoff) {
   switch (P.fmt) {
-    case KM_F32: return launch_assign_t<KM_F32>(P, C, cp, k, assign, score, s);
-    case KM_BF16: return launch_assign_t<KM_BF16>(P, C, cp, k, assign, score, s);
-    case KM_SQ8: return launch_assign_t<KM_SQ8>(P, C, cp, k, assign, score, s);
-    case KM_SIGN1: return launch_assign_t<KM_SIGN1>(P, C, cp, k, assign, score, s);
-    case KM_HYBRID: return launch_assign_t<KM_HYBRID>(P, C, cp, k, assign, score, s);
-    case KM_RABITQ: return launch_assign_t<KM_RABITQ>(P, C, cp, k, assign, score, s);
-    case KM_LVQ4: return launch_assign_t<KM_LVQ4>(P, C, cp, k, assign, score, s);
+    case KM_F32: return launch_assign_t<KM_F32>(P, C, cp, k, assign, score, s, aoff);
+    case KM_BF16: return launch_assign_t<KM_BF16>(P, C, cp, k, assign, score, s, aoff);
+    case KM_SQ8: return launch_assign_t<KM_SQ8>(P, C, cp, k, assign, score, s, aoff);
+    case KM_SIGN1: return launch_assign_t<KM_SIGN1>(P, C, cp, k, assign, score, s, aoff);
+    case KM_HYBRID: return launch_assign_t<KM_HYBRID>(P, C, cp, k, assign, score, s, aoff);
+    case KM_RABITQ: return launch_assign_t<KM_RABITQ>(P, C, cp, k, assign, score, s, aoff);
+    case KM_LVQ4: return launch_assign_t<KM_LVQ4>(P, C, cp, k, assign, score, s, aoff);
     default: return KM_EUNSUPPORTED;
   }
+}
+
+CentroidPrep prep_slice(const Points &P, const CentroidPrep &cp, int off, int64_t pstart) {
+  CentroidPrep r = cp;
+  r.cn = cp.cn + off;
+  r.qsum = cp.qsum + off;
+  r.u = cp.u + off;
+  r.sig2 = cp.sig2 + off;
+  const int d0 = P.fmt == KM_HYBRID ? P.d_front : 0;
+  if (is_bits_fmt(P.fmt)) r.q = cp.q + (int64_t)off * (P.d - d0);
+  if (P.fmt == KM_LVQ4) r.q = cp.q + (int64_t)off * P.d;
+  if (P.fmt == KM_BF16) {
+    r.cb = cp.cb + (int64_t)off * P.d;
+    r.q = reinterpret_cast<const int8_t *>(r.cb);
+  }
+  if (cp.keys) r.keys = cp.keys + pstart;
+  return r;
 }
 
 km_status launch_xconst(const Points &P, float *xc, hipStream_t s) {

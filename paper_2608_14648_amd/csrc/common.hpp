@@ -73,8 +73,11 @@ __host__ __device__ static inline int64_t cdiv(int64_t a, int64_t b) { return (a
 km_status launch_prep(const Points &P, const void *C, int k, void *ws_prep, CentroidPrep *out,
                       hipStream_t s);
 size_t prep_bytes(const Points &P, int k);
+// aoff is added to every stored centroid index (C and cp may be a slice of a larger set)
 km_status launch_assign(const Points &P, const void *C, const CentroidPrep &cp, int k, int32_t *assign,
-                        float *score, hipStream_t s);
+                        float *score, hipStream_t s, int aoff = 0);
+// cp restricted to centroids [off, ...) and, for the per-point keys, to points [pstart, ...)
+CentroidPrep prep_slice(const Points &P, const CentroidPrep &cp, int off, int64_t pstart);
 km_status launch_xconst(const Points &P, float *xc, hipStream_t s);
 km_status launch_objective(const Points &P, const float *xc, const float *score, int64_t n, double *out,
                            double *partials, int nblk_max, hipStream_t s);
@@ -85,8 +88,26 @@ km_status launch_cost(const float *X, int64_t n, int d, int64_t ldx, const float
 
 // update.hip
 size_t update_bytes(const Points &P, int k);
+// seg_lo / seg_hi (nullable, int[k]): the split takes the donor of empty cluster j
+// from clusters [seg_lo[j], seg_hi[j]) only.
 km_status launch_update(const Points &P, const int32_t *assign, int k, void *C, int64_t *counts,
-                        int policy, void *ws, hipStream_t s);
+                        int policy, void *ws, hipStream_t s, const int *seg_lo = nullptr,
+                        const int *seg_hi = nullptr);
+struct SortOut {
+  const int *perm;    // [n]: point indices ordered by cluster, point order kept inside a cluster
+  const int *cnt;     // [k]: members per cluster (ids outside [0, k) are left out)
+  const int *cstart;  // [k]: first position of each cluster in perm
+};
+size_t sort_bytes(int64_t n, int k);
+km_status launch_cluster_sort(const int32_t *assign, int64_t n, int k, void *ws, SortOut *out, hipStream_t s);
+
+// hier.hip: contiguous per-meso-cluster copies of the points and the write-back
+size_t permuted_bytes(const Points &P, int64_t nrows);
+km_status launch_permute_points(const Points &P, const int *perm, int64_t nrows, void *ws, Points *out,
+                                hipStream_t s);
+Points slice_points(const Points &P, int64_t start, int64_t count);
+km_status launch_scatter_assign(const int *perm, const int32_t *a_perm, int64_t nsel, int64_t n, int32_t *assign,
+                                hipStream_t s);
 
 // quantize.hip
 size_t quantize_bytes(int64_t n, int d, int fmt);

@@ -18,7 +18,9 @@
 //   5. finalize per cluster, chunk sums in chunk order in fp64, divided by
 //               the count: fp32 mean / 1-bit residual mean / rounded code mean.
 //   6. split    empty clusters in ascending order take a split of the cluster
-//               with the largest current count (one workgroup, sequential).
+//               with the largest current count (one workgroup, sequential);
+//               with segments given (hierarchical fine phase), the donor is
+//               searched among the empty cluster's own segment of centroids.
 //   7. compose  write the new centroids (1-bit dims: m + residual).
 // Every sum has a fixed order, so results are bit-identical run to run.
 #include <algorithm>
@@ -564,7 +566,8 @@ __global__ __launch_bounds__(256) void finalize_sq8_kernel(const int *partial, i
 // counts left by the previous split) and runs over that list only.
 template <bool CODES>
 __global__ __launch_bounds__(256) void split_kernel(void *Zv, int k, int dp, const int *cnt, int64_t *cntw,
-                                                    uint8_t *fresh, int *empties) {
+                                                    uint8_t *fresh, int *empties, const int *seg_lo,
+                                                    const int *seg_hi) {
   __shared__ int64_t sv[256];
   __shared__ int si[256];
   __shared__ int shs[256];
@@ -587,9 +590,10 @@ __global__ __launch_bounds__(256) void split_kernel(void *Zv, int k, int dp, con
   const float up = 1.0f + 0x1p-10f, dn = 1.0f - 0x1p-10f;
   for (int e = 0; e < ne; ++e) {
     const int j = empties[e];
+    const int slo = seg_lo ? seg_lo[j] : 0, shi = seg_hi ? seg_hi[j] : k;  // donor candidates
     int64_t bv = -1;
-    int bi = 0;
-    for (int i = t; i < k; i += 256) {
+    int bi = slo;
+    for (int i = slo + t; i < shi; i += 256) {
       const int64_t v = cntw[i];
       if (v > bv) {
         bv = v;
@@ -669,13 +673,12 @@ size_t update_bytes(const Points &P, int k) {
   return b;
 }
 
-km_status launch_update(const Points &P, const int32_t *assign, int k, void *C, int64_t *counts, int policy,
-                        void *ws, hipStream_t s) {
-  UpdWs w = carve(P, k, ws, nullptr);
+// steps 1-3: counts, starts and the stable cluster-sorted order of the points
+static km_status launch_sort(const int32_t *assign, int64_t n, int k, const UpdWs &w, hipStream_t s) {
   const bool lds = k <= kLdsCursorMax;
   const size_t lds_bytes = lds ? sizeof(int) * (size_t)k : 0;
   if (!lds) hipLaunchKernelGGL(fill_int_kernel, dim3(1024), dim3(256), 0, s, w.offs, w.L, 0);
-  hipLaunchKernelGGL(hist_kernel, dim3(w.nblk), dim3(256), lds_bytes, s, assign, P.n, k, w.nblk, w.ppb, w.offs,
+  hipLaunchKernelGGL(hist_kernel, dim3(w.nblk), dim3(256), lds_bytes, s, assign, n, k, w.nblk, w.ppb, w.offs,
                      (int)lds);
   hipLaunchKernelGGL(scan_reduce_kernel, dim3(w.nsb), dim3(256), 0, s, w.offs, w.L, w.bsum);
   hipLaunchKernelGGL(scan_single_kernel, dim3(1), dim3(256), 0, s, w.bsum, w.bsum, w.nsb, w.total, 0);
@@ -683,9 +686,38 @@ km_status launch_update(const Points &P, const int32_t *assign, int k, void *C, 
   hipLaunchKernelGGL(counts_kernel, dim3((unsigned)cdiv(k, 256)), dim3(256), 0, s, w.offs, w.nblk, k, w.total, w.cnt,
                      w.cstart);
   hipLaunchKernelGGL(scan_single_kernel, dim3(1), dim3(256), 0, s, w.cnt, w.choff, k, w.choff + k, 1);
-  hipLaunchKernelGGL(scatter_kernel, dim3(w.nblk), dim3(256), lds_bytes, s, assign, P.n, k, w.nblk, w.ppb, w.offs,
+  hipLaunchKernelGGL(scatter_kernel, dim3(w.nblk), dim3(256), lds_bytes, s, assign, n, k, w.nblk, w.ppb, w.offs,
                      (int)lds, w.perm);
   KMQ_LAUNCH_CHECK("update: sort");
+  return KM_OK;
+}
+
+static Points sort_only_points(int64_t n) {  // the sort's workspace does not depend on the format
+  Points q{};
+  q.n = n;
+  q.d = 4;
+  return q;
+}
+
+size_t sort_bytes(int64_t n, int k) {
+  size_t b = 0;
+  carve(sort_only_points(n), k, nullptr, &b);
+  return b;
+}
+
+km_status launch_cluster_sort(const int32_t *assign, int64_t n, int k, void *ws, SortOut *out, hipStream_t s) {
+  UpdWs w = carve(sort_only_points(n), k, ws, nullptr);
+  out->perm = w.perm;
+  out->cnt = w.cnt;
+  out->cstart = w.cstart;
+  return launch_sort(assign, n, k, w, s);
+}
+
+km_status launch_update(const Points &P, const int32_t *assign, int k, void *C, int64_t *counts, int policy,
+                        void *ws, hipStream_t s, const int *seg_lo, const int *seg_hi) {
+  UpdWs w = carve(P, k, ws, nullptr);
+  km_status sst = launch_sort(assign, P.n, k, w, s);
+  if (sst != KM_OK) return sst;
 
   const int d = P.d;
   if (P.fmt == KM_SQ8) {
@@ -734,10 +766,10 @@ km_status launch_update(const Points &P, const int32_t *assign, int k, void *C, 
   if (policy == KM_EMPTY_SPLIT) {
     if (P.fmt == KM_SQ8)
       hipLaunchKernelGGL(split_kernel<true>, dim3(1), dim3(256), 0, s, w.Z, k, w.dp, w.cnt, w.cntw, w.fresh,
-                         w.empties);
+                         w.empties, seg_lo, seg_hi);
     else
       hipLaunchKernelGGL(split_kernel<false>, dim3(1), dim3(256), 0, s, w.Z, k, w.dp, w.cnt, w.cntw, w.fresh,
-                         w.empties);
+                         w.empties, seg_lo, seg_hi);
   }
   const dim3 g(k, (unsigned)cdiv(d, 256));
   const int d0 = P.fmt == KM_HYBRID ? P.d_front : 0;

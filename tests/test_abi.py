@@ -197,3 +197,48 @@ def test_binding_rejects_host_tensors(kmq):
     import torch
     with pytest.raises(ValueError):
         kmq.points_f32(torch.zeros(4, 8))
+
+
+def test_hierarchical_argument_checks(kmq):
+    """kmeans_fine / kmeans_fit_hier reject bad arguments on the host, before any HIP call."""
+    L = kmq.lib()
+    P = _pts(kmq)
+    ok = (ct.byref(P), FAKE, 4, 10, 2, 0, FAKE, FAKE, None, None, 0, None)
+    bad = [
+        (ok[:1] + (None,) + ok[2:], "NULL"),
+        (ok[:2] + (0,) + ok[3:], "k_meso"),
+        (ok[:4] + (-1,) + ok[5:], "iters"),
+        (ok[:5] + (2,) + ok[6:], "flags"),
+        (ok[:10] + (5,) + ok[11:], "policy"),
+        (ok[:6] + (None,) + ok[7:], "centroids"),
+        (ok[:7] + (None,) + ok[8:], "NULL"),
+    ]
+    for args, msg in bad:
+        assert L.kmeans_fine(*args) == -1, msg
+        assert msg in L.km_last_error().decode(), (msg, L.km_last_error())
+    init = (ct.c_int64 * 3)(0, 5, 9)
+    hp = kmq.KmHierParams(3, 2, 2, 0)
+    base = [ct.byref(P), 10, ct.byref(hp), init, FAKE, FAKE, None, None, 0, None, None, None]
+    for i, v, msg in [(2, None, "NULL"), (3, None, "NULL"), (1, 101, "exceeds"), (8, 7, "policy")]:
+        args = list(base)
+        args[i] = v
+        assert L.kmeans_fit_hier(*args) == -1, msg
+        assert msg in L.km_last_error().decode(), (msg, L.km_last_error())
+    for params, msg in [((11, 2, 2, 0), "k_meso"), ((3, -1, 2, 0), "iteration"), ((3, 2, 2, -2), "iteration")]:
+        hp2 = kmq.KmHierParams(*params)
+        args = list(base)
+        args[2] = ct.byref(hp2)
+        assert L.kmeans_fit_hier(*args) == -1, msg
+        assert msg in L.km_last_error().decode(), (msg, L.km_last_error())
+    dup = (ct.c_int64 * 3)(0, 5, 5)
+    args = list(base)
+    args[3] = dup
+    assert L.kmeans_fit_hier(*args) == -1
+    assert "duplicates" in L.km_last_error().decode()
+    # k_meso = 0 means round(sqrt(k)): 3 for k = 10, so three initial rows are needed and checked
+    hp0 = kmq.KmHierParams(0, 1, 1, 0)
+    oob = (ct.c_int64 * 3)(0, 5, 100)
+    args = list(base)
+    args[2], args[3] = ct.byref(hp0), oob
+    assert L.kmeans_fit_hier(*args) == -1
+    assert "outside" in L.km_last_error().decode()
