@@ -295,7 +295,9 @@ typedef struct km_hier_params {
  * iters_fine iterations; then, if iters_refine > 0, kmeans_fit from the fine
  * centroids with iters_refine iterations over all points (its last update from
  * P->raw when set; the meso and fine phases use the compressed points only).
- *   C, assign: out, as in kmeans_fit.  k_fine: as in kmeans_fine.
+ *   C, assign: out, as in kmeans_fit.  meso_assign (nullable): DEVICE int32[n],
+ *   receives the meso partition (the upper level of the two-level clustering).
+ *   k_fine: as in kmeans_fine.
  *   objective (nullable): DEVICE double[1], the in-space objective of the returned
  *   partition.  stats (nullable, HOST): stage times summed over the three phases;
  *   phase_ms (nullable, HOST double[3]): device time of the meso, fine and refine
@@ -303,8 +305,8 @@ typedef struct km_hier_params {
  *   always waits once (see kmeans_fine).
  */
 km_status kmeans_fit_hier(const km_points *P, int32_t k, const km_hier_params *hp, const int64_t *init_meso, void *C,
-                          int32_t *assign, int32_t *k_fine, double *objective, int32_t policy, km_fit_stats *stats,
-                          double *phase_ms, km_stream stream);
+                          int32_t *assign, int32_t *meso_assign, int32_t *k_fine, double *objective, int32_t policy,
+                          km_fit_stats *stats, double *phase_ms, km_stream stream);
 
 /*
  * kmeans_cost -- sum over points of ||x - c_{assign(x)}||^2 in fp64 for fp32

@@ -72,7 +72,7 @@ def lib():
             "kmeans_update": [ct.POINTER(KmPoints), vp, i32, vp, vp, i32, vp],
             "kmeans_fit": [ct.POINTER(KmPoints), i32, i32, vp, vp, vp, vp, i32, ct.POINTER(KmFitStats), vp],
             "kmeans_fine": [ct.POINTER(KmPoints), vp, i32, i32, i32, i32, vp, vp, vp, vp, i32, vp],
-            "kmeans_fit_hier": [ct.POINTER(KmPoints), i32, ct.POINTER(KmHierParams), vp, vp, vp, vp, vp, i32,
+            "kmeans_fit_hier": [ct.POINTER(KmPoints), i32, ct.POINTER(KmHierParams), vp, vp, vp, vp, vp, vp, i32,
                                 ct.POINTER(KmFitStats), vp, vp],
             "kmeans_cost": [vp, i64, i32, i64, vp, i32, vp, vp, vp],
             "km_release": [],
@@ -390,11 +390,12 @@ def kmeans_fine(P: Points, meso_assign: torch.Tensor, k_meso: int, k: int, iters
 
 def kmeans_fit_hier(P: Points, k: int, init_meso, iters_meso: int, iters_fine: int, iters_refine: int = 0,
                     k_meso: int = 0, policy: int = KM_EMPTY_SPLIT, objective: bool = True,
-                    stats: KmFitStats | None = None, phases: bool = False):
+                    stats: KmFitStats | None = None, phases: bool = False, meso: bool = False):
     """Hierarchical k-means: meso Lloyd with k_meso (0 = round(sqrt(k))) centroids from
     the rows init_meso, Lloyd inside every meso-cluster, optional vanilla refinement.
     Returns (C, assign, k_fine numpy int32[k_meso], objective double[1] or None,
-    phase times [meso, fine, refine] in ms or None)."""
+    phase times [meso, fine, refine] in ms or None); with meso=True the meso
+    assignment (int32[n]) is appended."""
     idx = np.ascontiguousarray(np.asarray(init_meso, dtype=np.int64))
     km = k_meso if k_meso else len(idx)
     if idx.ndim != 1 or len(idx) != km:
@@ -405,11 +406,12 @@ def kmeans_fit_hier(P: Points, k: int, init_meso, iters_meso: int, iters_fine: i
     kf = np.zeros(len(idx), dtype=np.int32)
     obj = torch.empty(1, dtype=torch.float64, device=P.device) if objective else None
     ph = np.zeros(3, dtype=np.float64) if phases else None
-    _check(lib().kmeans_fit_hier(P.ref, k, ct.byref(hp), idx.ctypes.data_as(ct.c_void_p), _ptr(C), _ptr(a),
+    am = torch.empty(P.n, dtype=torch.int32, device=P.device) if meso else None
+    _check(lib().kmeans_fit_hier(P.ref, k, ct.byref(hp), idx.ctypes.data_as(ct.c_void_p), _ptr(C), _ptr(a), _ptr(am),
                                  kf.ctypes.data_as(ct.c_void_p), _ptr(obj), policy,
                                  ct.byref(stats) if stats is not None else None,
                                  ph.ctypes.data_as(ct.c_void_p) if phases else None, _stream()))
-    return C, a, kf, obj, ph
+    return (C, a, kf, obj, ph, am) if meso else (C, a, kf, obj, ph)
 
 
 def kmeans_cost(X: torch.Tensor, C: torch.Tensor, assign: torch.Tensor):

@@ -641,8 +641,8 @@ km_status kmeans_fine(const km_points *P, const int32_t *meso_assign, int32_t k_
 }
 
 km_status kmeans_fit_hier(const km_points *P, int32_t k, const km_hier_params *hp, const int64_t *init_meso, void *C,
-                          int32_t *assign, int32_t *k_fine, double *objective, int32_t policy, km_fit_stats *stats,
-                          double *phase_ms, km_stream stream) {
+                          int32_t *assign, int32_t *meso_assign, int32_t *k_fine, double *objective, int32_t policy,
+                          km_fit_stats *stats, double *phase_ms, km_stream stream) {
   g_err[0] = 0;
   Points p;
   km_status st = check_points(P, &p);
@@ -665,13 +665,13 @@ km_status kmeans_fit_hier(const km_points *P, int32_t k, const km_hier_params *h
   pc.raw_ld = 0;
   const int R = hp->iters_refine;
   const size_t b_cm = al(centroid_bytes(p, km));
-  const size_t b_am = al(sizeof(int32_t) * (size_t)p.n);
+  const size_t b_am = meso_assign ? 0 : al(sizeof(int32_t) * (size_t)p.n);
   const size_t b_obj = (objective && R > 0) ? al(sizeof(double) * (size_t)(R + 1)) : 0;
   Scratch ws(s);
   st = ws.alloc(b_cm + b_am + b_obj);
   if (st != KM_OK) return st;
   void *Cm = ws.get();
-  int32_t *am = reinterpret_cast<int32_t *>(ws.get() + b_cm);
+  int32_t *am = meso_assign ? meso_assign : reinterpret_cast<int32_t *>(ws.get() + b_cm);
   double *objr = reinterpret_cast<double *>(ws.get() + b_cm + b_am);
   try {
     StageClock clk(stats != nullptr, s);

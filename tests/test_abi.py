@@ -218,8 +218,8 @@ def test_hierarchical_argument_checks(kmq):
         assert msg in L.km_last_error().decode(), (msg, L.km_last_error())
     init = (ct.c_int64 * 3)(0, 5, 9)
     hp = kmq.KmHierParams(3, 2, 2, 0)
-    base = [ct.byref(P), 10, ct.byref(hp), init, FAKE, FAKE, None, None, 0, None, None, None]
-    for i, v, msg in [(2, None, "NULL"), (3, None, "NULL"), (1, 101, "exceeds"), (8, 7, "policy")]:
+    base = [ct.byref(P), 10, ct.byref(hp), init, FAKE, FAKE, None, None, None, 0, None, None, None]
+    for i, v, msg in [(2, None, "NULL"), (3, None, "NULL"), (1, 101, "exceeds"), (9, 7, "policy")]:
         args = list(base)
         args[i] = v
         assert L.kmeans_fit_hier(*args) == -1, msg

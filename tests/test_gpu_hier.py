@@ -232,7 +232,7 @@ def test_hier_pipeline_is_its_phases(km, torch):
     kmeso = orc.meso_count(k)
     init = synth.init_indices(len(X), kmeso)
     say("hier f32 pipeline")
-    C, a, kf, obj, ph = km.kmeans_fit_hier(Pg, k, init, 5, 4, 1, phases=True)
+    C, a, kf, obj, ph, am_h = km.kmeans_fit_hier(Pg, k, init, 5, 4, 1, phases=True, meso=True)
     _, am, _ = km.kmeans_fit(Pg, kmeso, 5, init, objective=False)
     Cf, af, kf2, _ = km.kmeans_fine(Pg, am, kmeso, k, 4)
     Cr, ar, Jr = km.kmeans_fit(Pg, k, 1, None, C=Cf.clone())
@@ -242,6 +242,7 @@ def test_hier_pipeline_is_its_phases(km, torch):
     np.testing.assert_array_equal(host(a), host(ar))
     assert host(obj)[0] == host(Jr)[-1]
     assert (ph > 0).all()
+    np.testing.assert_array_equal(host(am_h), host(am))
     am_h = host(am)
     np.testing.assert_array_equal(kf, orc.fine_counts(np.bincount(am_h, minlength=kmeso), k))
     C0_o, a0_o, _, J0_o = orc.fit_fine(Po, am_h, kmeso, k, 0)
