@@ -75,6 +75,11 @@ def lib():
                                  _i32],
             "orc_cost_f32": [_f32p, _i64, _i32, _i64, _f32p, _i32p],
             "orc_partition_cost": [_f32p, _i64, _i32, _i32p, _i32],
+            "orc_prune_factor": [_i32, _i32, ct.c_double],
+            "orc_assign_pruned_f32": [_f32p, _i64, _i32, _f32p, _i32, _i32p, ct.c_double, _i32, _i32, _i32p, _f64p,
+                                      _i64p],
+            "orc_assign_pruned_sq8": [_u8p, _i64, _i32, _u8p, _i32, _i32p, ct.c_double, _i32, _i32, _i32p, _i64p,
+                                      _i64p],
             "orc_num_threads": [],
         }
         for name, args in sig.items():
@@ -85,6 +90,7 @@ def lib():
         L.orc_cost_f32.restype = ct.c_double
         L.orc_partition_cost.restype = ct.c_double
         L.orc_num_threads.restype = ct.c_int
+        L.orc_prune_factor.restype = ct.c_double
         _lib = L
     return _lib
 
@@ -601,3 +607,62 @@ def fit_hier(P: dict, k: int, iters_meso: int, iters_fine: int, iters_refine: in
         C, a, Jr = fit(P, k, iters_refine, None, policy, C0=C)
         J = float(Jr[-1])
     return C, a, J, {"k_meso": km, "C_meso": Cm, "a_meso": am, "J_meso": Jm, "k_fine": k_i, "J_fine": Jf}
+
+
+# --------------------------------------------------------------------------
+# Dimension pruning inside STEP 2 (Sec. 3.1 "SuperKMeans", Table 4): the first
+# pass is a full assignment; every later pass starts each point from its previous
+# centroid and drops other centroids with the ADSampling test on partial distances
+# over the front d' dims and then every `step` dims, comparing the survivors on the
+# full distance.  Meant for randomly rotated points (the test assumes the
+# variance is spread evenly over the dims).
+
+def prune_front_dims(d: int) -> int:
+    """Default d': 12.5 % of d rounded up to a multiple of 32 (at most d)."""
+    return min(d, 32 * ((d + 255) // 256))
+
+
+def prune_factor(D: int, d: int, eps0: float) -> float:
+    return float(lib().orc_prune_factor(D, d, eps0))
+
+
+def assign_pruned(P: dict, C, prev, eps0: float = 2.1, d_front: int = 0, step: int = 64):
+    """One pruned STEP 2 from the previous assignment.  Returns (a, dist, counters) with
+    counters = [candidates tested at d', passed d', compared on the full distance]."""
+    fmt = P["fmt"]
+    prev = _c(prev, np.int32)
+    cnt = np.zeros(3, np.int64)
+    if fmt == "f32":
+        X = _c(P["X"], np.float32)
+        n, d = X.shape
+        D0 = d_front or prune_front_dims(d)
+        a = np.empty(n, np.int32)
+        dist = np.empty(n, np.float64)
+        lib().orc_assign_pruned_f32(X, n, d, _c(C, np.float32), len(C), prev, eps0, D0, step, a, dist, cnt)
+        return a, dist, cnt
+    if fmt == "sq8":
+        X = _c(P["codes"], np.uint8)
+        n, d = X.shape
+        D0 = d_front or prune_front_dims(d)
+        a = np.empty(n, np.int32)
+        dist = np.empty(n, np.int64)
+        lib().orc_assign_pruned_sq8(X, n, d, _c(C, np.uint8), len(C), prev, eps0, D0, step, a, dist, cnt)
+        return a, dist.astype(np.float64), cnt
+    raise ValueError(f"dimension pruning is defined for f32 and sq8 points, not {fmt}")
+
+
+def fit_pruned(P: dict, k: int, iters: int, init_idx, policy: int = EMPTY_SPLIT, eps0: float = 2.1,
+               d_front: int = 0, step: int = 64, C0=None):
+    """Lloyd with pruned assignment passes: STEP 1, a full STEP 2, then iters x
+    (STEP 3, pruned STEP 2 from the previous assignment).  Returns (C, a, J[0..T],
+    counters summed over the pruned passes)."""
+    C = init_centroids(P, init_idx) if C0 is None else np.array(C0, copy=True)
+    a, dist = assign(P, C)
+    J = [float(np.sum(dist, dtype=np.float64))]
+    total = np.zeros(3, np.int64)
+    for _ in range(iters):
+        C, _ = update(P, a, k, C, policy)
+        a, dist, cnt = assign_pruned(P, C, a, eps0, d_front, step)
+        J.append(float(np.sum(dist, dtype=np.float64)))
+        total += cnt
+    return C, a, J, total

@@ -235,6 +235,121 @@ void orc_assign_sq8(const uint8_t *X, int64_t n, int32_t d, const uint8_t *C, in
   }
 }
 
+double orc_prune_factor(int32_t D, int32_t d, double eps0) {
+  const double g = 1.0 + eps0 / sqrt((double)D);
+  return g * g * (double)D / (double)d;
+}
+
+void orc_assign_pruned_f32(const float *X, int64_t n, int32_t d, const float *C, int32_t k, const int32_t *prev,
+                           double eps0, int32_t d_front, int32_t step, int32_t *a, double *dist,
+                           int64_t *counters) {
+  int64_t tested = 0, passed = 0, full = 0;
+#pragma omp parallel for schedule(static) reduction(+ : tested, passed, full)
+  for (int64_t r = 0; r < n; ++r) {
+    const float *x = X + r * d;
+    const int32_t pj = prev[r];
+    double tau = 0.0;
+    for (int32_t i = 0; i < d; ++i) {
+      const double t = (double)x[i] - (double)C[(int64_t)pj * d + i];
+      tau += t * t;
+    }
+    int32_t best = pj;
+    double bd = tau;
+    for (int32_t j = 0; j < k; ++j) {
+      if (j == pj) continue;
+      const float *c = C + (int64_t)j * d;
+      double p = 0.0;
+      int32_t i = 0, alive = 1;
+      for (int32_t D = d_front; D < d; D += step) { /* checkpoints */
+        for (; i < D; ++i) {
+          const double t = (double)x[i] - (double)c[i];
+          p += t * t;
+        }
+        const int first = D == d_front;
+        tested += first;
+        if (p > tau * orc_prune_factor(D, d, eps0)) {
+          alive = 0;
+          break;
+        }
+        passed += first;
+      }
+      if (!alive) continue;
+      for (; i < d; ++i) {
+        const double t = (double)x[i] - (double)c[i];
+        p += t * t;
+      }
+      ++full;
+      if (p < bd || (p == bd && j < best)) {
+        bd = p;
+        best = j;
+      }
+    }
+    a[r] = best;
+    if (dist) dist[r] = bd;
+  }
+  if (counters) {
+    counters[0] = tested;
+    counters[1] = passed;
+    counters[2] = full;
+  }
+}
+
+void orc_assign_pruned_sq8(const uint8_t *X, int64_t n, int32_t d, const uint8_t *C, int32_t k,
+                           const int32_t *prev, double eps0, int32_t d_front, int32_t step, int32_t *a,
+                           int64_t *dist, int64_t *counters) {
+  int64_t tested = 0, passed = 0, full = 0;
+#pragma omp parallel for schedule(static) reduction(+ : tested, passed, full)
+  for (int64_t r = 0; r < n; ++r) {
+    const uint8_t *x = X + r * d;
+    const int32_t pj = prev[r];
+    int64_t tau = 0;
+    for (int32_t i = 0; i < d; ++i) {
+      const int64_t t = (int64_t)x[i] - (int64_t)C[(int64_t)pj * d + i];
+      tau += t * t;
+    }
+    const float tauf = (float)tau;
+    int32_t best = pj;
+    int64_t bd = tau;
+    for (int32_t j = 0; j < k; ++j) {
+      if (j == pj) continue;
+      const uint8_t *c = C + (int64_t)j * d;
+      int64_t p = 0;
+      int32_t i = 0, alive = 1;
+      for (int32_t D = d_front; D < d; D += step) {
+        for (; i < D; ++i) {
+          const int64_t t = (int64_t)x[i] - (int64_t)c[i];
+          p += t * t;
+        }
+        const int first = D == d_front;
+        tested += first;
+        const float lim = tauf * (float)orc_prune_factor(D, d, eps0);
+        if ((float)p > lim) {
+          alive = 0;
+          break;
+        }
+        passed += first;
+      }
+      if (!alive) continue;
+      for (; i < d; ++i) {
+        const int64_t t = (int64_t)x[i] - (int64_t)c[i];
+        p += t * t;
+      }
+      ++full;
+      if (p < bd || (p == bd && j < best)) {
+        bd = p;
+        best = j;
+      }
+    }
+    a[r] = best;
+    if (dist) dist[r] = bd;
+  }
+  if (counters) {
+    counters[0] = tested;
+    counters[1] = passed;
+    counters[2] = full;
+  }
+}
+
 void orc_sign1_prep(const float *C, int32_t k, int32_t d, const float *m, int32_t d0, int8_t *q,
                     float *sigma, int32_t *T, int32_t *Q, float *u) {
   const int32_t dt = d - d0;

@@ -137,6 +137,29 @@ void orc_update_sign1(const float *front, const uint32_t *bits, const float *alp
 void orc_sign1_decode(const uint32_t *bits, const float *alpha, int64_t n, int32_t d, int32_t d0,
                       const float *m, float *out, int64_t ldo);
 
+/* ---- Dimension pruning (Sec. 3.1 SuperKMeans; ADSampling test) ----------- */
+
+/* Factor of the ADSampling test at a checkpoint after D of d dims: a candidate
+   whose squared distance over the first D dims is p is dropped when
+   p > tau * r, r = (1 + eps0 / sqrt(D))^2 * D / d, tau = the squared distance to
+   the point's previous centroid (the current best). */
+double orc_prune_factor(int32_t D, int32_t d, double eps0);
+
+/* One pruned STEP 2: for every point, best = prev[r] at distance tau; every other
+   centroid j is tested at the checkpoints d_front, d_front + step, ... (< d) on
+   its partial squared distance and, if never dropped, compared on its full
+   distance (smaller wins, ties to the smaller index).  fp32 points: sums and the
+   test in fp64.  SQ8 codes: exact integer sums, test (float)p > (float)tau *
+   (float)r.  dist: the winning squared distance.  counters (nullable, int64[3]):
+   candidates tested at d_front, candidates that passed it, candidates compared on
+   the full distance. */
+void orc_assign_pruned_f32(const float *X, int64_t n, int32_t d, const float *C, int32_t k, const int32_t *prev,
+                           double eps0, int32_t d_front, int32_t step, int32_t *a, double *dist,
+                           int64_t *counters);
+void orc_assign_pruned_sq8(const uint8_t *X, int64_t n, int32_t d, const uint8_t *C, int32_t k,
+                           const int32_t *prev, double eps0, int32_t d_front, int32_t step, int32_t *a,
+                           int64_t *dist, int64_t *counters);
+
 /* ---- Objective ---------------------------------------------------------- */
 
 /* Sum over points of ||x - c_{a(x)}||^2 in fp64 (fp32 inputs). */

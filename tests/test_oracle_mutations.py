@@ -42,6 +42,14 @@ MUTATIONS = {
                             "fmaf(by, Ax, (sx * sy) * (float)dot)"),
     "lvq4_16_levels": ("const float s = hi > lo ? (hi - lo) / 15.0f : 1.0f;",
                        "const float s = hi > lo ? (hi - lo) / 16.0f : 1.0f;"),
+    "prune_factor_not_squared": ("return g * g * (double)D / (double)d;", "return g * (double)D / (double)d;"),
+    "prune_factor_inverted": ("return g * g * (double)D / (double)d;", "return g * g * (double)d / (double)D;"),
+    "prune_test_not_strict": ("if (p > tau * orc_prune_factor(D, d, eps0)) {", "if (p >= tau * orc_prune_factor(D, d, eps0)) {"),
+    "prune_sq8_test_not_strict": ("if ((float)p > lim) {", "if ((float)p >= lim) {"),
+    "prune_previous_centroid_dropped": ("    int32_t best = pj;\n    double bd = tau;", "    int32_t best = pj;\n    double bd = 1e300;"),
+    "prune_ties_to_larger": ("if (p < bd || (p == bd && j < best)) {", "if (p < bd || (p == bd && j > best)) {"),
+    "prune_first_checkpoint_skipped": ("for (int32_t D = d_front; D < d; D += step) { /* checkpoints */",
+                                       "for (int32_t D = d_front + step; D < d; D += step) { /* checkpoints */"),
 }
 
 # mistakes in the Python driver (hierarchical k-means)

@@ -842,3 +842,126 @@ def test_hier_one_fine_cluster_per_meso_cluster(orc):
     np.testing.assert_array_equal(a, am)
     for j in range(5):
         np.testing.assert_allclose(C[j], X[am == j].astype(np.float64).mean(0), rtol=1e-6, atol=1e-6)
+
+
+# --------------------------------------------------------------------------
+# Dimension pruning inside STEP 2 (Sec. 3.1 SuperKMeans, ADSampling test)
+
+def test_prune_hand_example(orc):
+    g = load_golden("prune_adsampling.json")
+    d, D0, step, eps0 = g["d"], g["d_front"], g["step"], g["eps0"]
+    for D, lim in g["thresholds_tau8"].items():
+        assert abs(8.0 * orc.prune_factor(int(D), d, eps0) - lim) <= 1e-12 * lim
+    for fmt in ("f32", "sq8"):
+        e = g[fmt]
+        if fmt == "f32":
+            P = {"fmt": "f32", "X": np.array(e["points"], np.float32)}
+            C = np.array(e["centroids"], np.float32)
+        else:
+            P = {"fmt": "sq8", "codes": np.array(e["points"], np.uint8)}
+            C = np.array(e["centroids"], np.uint8)
+        a, dist, cnt = orc.assign_pruned(P, C, np.array(e["prev"], np.int32), eps0, D0, step)
+        assert a.tolist() == e["assign"], fmt
+        assert dist.tolist() == e["dist"], fmt
+        assert cnt.tolist() == e["counters"], fmt
+    a_exact, _ = orc.assign_f32(np.array(g["f32"]["points"], np.float32), np.array(g["f32"]["centroids"], np.float32))
+    assert a_exact.tolist() == g["f32"]["exact_nearest"]
+
+
+def _prune_numpy(Xd, Cd, prev, eps0, D0, step, sq8):
+    """The pruned assignment evaluated with numpy: prefix sums of the squared
+    differences (cumsum), the survivor matrix over all checkpoints, then the argmin of
+    the full distance over the survivors and the previous centroid."""
+    n, d = Xd.shape
+    k = len(Cd)
+    sq = (Xd[:, None, :] - Cd[None, :, :]) ** 2
+    pre = np.cumsum(sq, axis=2)
+    full = pre[:, :, -1]
+    tau = full[np.arange(n), prev]
+    alive = np.ones((n, k), bool)
+    alive[np.arange(n), prev] = False
+    cps = list(range(D0, d, step))
+    tested = passed = 0
+    for m, D in enumerate(cps):
+        g = (1.0 + eps0 / np.sqrt(D)) ** 2 * D / d
+        if sq8:
+            keep = pre[:, :, D - 1].astype(np.float32) <= (tau.astype(np.float32)[:, None] * np.float32(g))
+        else:
+            keep = pre[:, :, D - 1] <= tau[:, None] * g
+        if m == 0:
+            tested = int(alive.sum())
+            passed = int((alive & keep).sum())
+        alive &= keep
+    cand = alive.copy()
+    cand[np.arange(n), prev] = True
+    score = np.where(cand, full, np.inf)
+    a = score.argmin(1)
+    return a, score[np.arange(n), a], [tested, passed, int(alive.sum())]
+
+
+@settings(max_examples=40, deadline=None)
+@given(n=st.integers(1, 30), d=st.sampled_from([8, 16, 40, 64]), k=st.integers(1, 9),
+       seed=st.integers(0, 2**31 - 1), sq8=st.booleans())
+def test_prune_brute_force(orc, n, d, k, seed, sq8):
+    rng = np.random.default_rng(seed)
+    D0, step = max(1, d // 8), max(1, d // 4)
+    prev = rng.integers(0, k, n).astype(np.int32)
+    if sq8:
+        X = rng.integers(0, 256, (n, d)).astype(np.uint8)
+        C = rng.integers(0, 256, (k, d)).astype(np.uint8)
+        C[k // 2] = C[0]  # equal centroids: ties to the smaller index
+        P = {"fmt": "sq8", "codes": X}
+        Xd, Cd = X.astype(np.int64), C.astype(np.int64)
+    else:
+        X = rng.standard_normal((n, d)).astype(np.float32)
+        C = (X[rng.integers(0, n, k)] + 0.7 * rng.standard_normal((k, d))).astype(np.float32)
+        P = {"fmt": "f32", "X": X}
+        Xd, Cd = X.astype(np.float64), C.astype(np.float64)
+    eps0 = float(rng.uniform(0.2, 3.0))
+    a, dist, cnt = orc.assign_pruned(P, C, prev, eps0, D0, step)
+    a2, dist2, cnt2 = _prune_numpy(Xd, Cd, prev, eps0, D0, step, sq8)
+    np.testing.assert_array_equal(a, a2)
+    np.testing.assert_array_equal(dist, dist2.astype(np.float64))
+    assert cnt.tolist() == cnt2
+    # never worse than the previous centroid
+    assert (dist <= ((Xd - Cd[prev]) ** 2).sum(1) + 1e-9).all()
+
+
+@pytest.mark.parametrize("fmt", ["f32", "sq8"])
+def test_prune_with_huge_eps_is_exact_assignment(orc, fmt):
+    rng = np.random.default_rng(81)
+    X = rng.standard_normal((300, 64)).astype(np.float32)
+    C = X[rng.choice(300, 17, replace=False)].copy()
+    C[5] = C[2]
+    if fmt == "f32":
+        P = {"fmt": "f32", "X": X}
+    else:
+        lo, hi = orc.sq8_fit(X)
+        P = {"fmt": "sq8", "codes": orc.sq8_encode(X, lo, hi)}
+        C = orc.sq8_encode(C, lo, hi)
+    prev = rng.integers(0, 17, 300).astype(np.int32)
+    a, dist, cnt = orc.assign_pruned(P, C, prev, 1e12)
+    a_ex, dist_ex = orc.assign(P, C)
+    np.testing.assert_array_equal(a, a_ex)
+    np.testing.assert_allclose(dist, dist_ex, rtol=1e-12)
+    assert cnt[0] == cnt[1] == cnt[2] == 300 * 16
+
+
+def test_prune_on_rotated_mixture_keeps_the_partition(orc):
+    """On randomly rotated, unit-normalised clustered data the test drops most
+    candidates at d' and the pruned Lloyd ends at (nearly) the exact partition."""
+    import synth
+    rng = np.random.default_rng(83)
+    d, n, comps = 256, 3000, 24
+    mu = rng.standard_normal((comps, d))
+    X = mu[rng.integers(0, comps, n)] + 0.35 * rng.standard_normal((n, d))
+    X /= np.linalg.norm(X, axis=1, keepdims=True)
+    X = (X @ synth.random_rotation(d, 4)).astype(np.float32)
+    P = {"fmt": "f32", "X": X}
+    idx = rng.choice(n, comps, replace=False)
+    C, a, J, cnt = orc.fit_pruned(P, comps, 6, idx)
+    C2, a2, J2 = orc.fit(P, comps, 6, idx)
+    assert (a == a2).mean() >= 0.995
+    assert cnt[1] <= 0.2 * cnt[0]
+    assert cnt[2] <= cnt[1]
+    assert abs(J[-1] - J2[-1]) <= 1e-3 * J2[-1]
