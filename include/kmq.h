@@ -250,6 +250,48 @@ km_status kmeans_fit(const km_points *P, int32_t k, int32_t iters, const int64_t
                      int32_t *assign, double *objective, int32_t policy, km_fit_stats *stats,
                      km_stream stream);
 
+/* Dimension pruning inside STEP 2 (Sec. 3.1 SuperKMeans, ADSampling test). */
+typedef struct km_prune {
+  double eps0;     /* ADSampling's epsilon_0 (> 0); 2.1 is the usual value */
+  int32_t d_front; /* d', the dims of the first test; 0 = 12.5 % of d rounded up to 32 (at most d) */
+  int32_t reserved; /* must be 0 */
+} km_prune;
+
+/*
+ * kmeans_assign_pruned -- one STEP 2 with dimension pruning (Sec. 3.1 "SuperKMeans";
+ * the ADSampling hypothesis test).  For every point, best = prev[i] at squared
+ * distance tau; every other centroid j is tested at the checkpoints D = d',
+ * d' + 64, d' + 128, ... (D < d) on its partial squared distance p(D) over the
+ * first D dims and dropped when p(D) > tau * r(D), r(D) = (1 + eps0 / sqrt(D))^2
+ * D / d; centroids never dropped are compared on the full distance (smaller wins,
+ * ties to the smaller index).  Meant for points under a random orthogonal
+ * rotation (the test assumes variance spread evenly over the dims); the result
+ * can differ from the exact nearest centroid when the test drops it.
+ *   P: KM_F32 (fp32 sums; r(D) rounded to fp32) or KM_SQ8 (exact integer distances
+ *   in code space, the test on (float)p(D) > (float)tau * (float)r(D)); d <= d' + 2048,
+ *   d' <= 256, d' % 4 == 0 (F32) or % 16 == 0 (SQ8).  C as in kmeans_assign.
+ *   prev: int32[n], the previous assignment (values in [0, k)); may be the same
+ *   array as assign.  dist (nullable): DEVICE double[n], the winning squared distance.
+ *   objective (nullable): DEVICE double[1], sum of dist.
+ *   counters (nullable, HOST uint64[3]): candidates tested at d', candidates that
+ *   passed d', candidates compared on the full distance; the call then waits for
+ *   the stream.
+ */
+km_status kmeans_assign_pruned(const km_points *P, const void *C, int32_t k, const int32_t *prev, int32_t *assign,
+                               double *dist, double *objective, const km_prune *pr, uint64_t *counters,
+                               km_stream stream);
+
+/*
+ * kmeans_fit_pruned -- kmeans_fit whose assignment passes after the first one are
+ * kmeans_assign_pruned from the previous assignment (SuperKMeans: the first pass
+ * is a full one).  Arguments as in kmeans_fit; pr as in kmeans_assign_pruned;
+ * counters (nullable, HOST uint64[3]) summed over the pruned passes (the call then
+ * waits for the stream).
+ */
+km_status kmeans_fit_pruned(const km_points *P, int32_t k, int32_t iters, const int64_t *init_idx, void *C,
+                            int32_t *assign, double *objective, int32_t policy, const km_prune *pr,
+                            km_fit_stats *stats, uint64_t *counters, km_stream stream);
+
 /* kmeans_fine() flags */
 #define KM_FINE_C_GIVEN 1 /* C holds the initial fine centroids; otherwise they are taken from the points */
 

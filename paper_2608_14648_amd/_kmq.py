@@ -22,7 +22,8 @@ KM_Q_FIT_PARAMS = 1
 KM_FINE_C_GIVEN = 1
 STATUS = {0: "KM_OK", -1: "KM_EINVAL", -2: "KM_EUNSUPPORTED", -3: "KM_ENOMEM", -4: "KM_EDEVICE"}
 EXPORTS = ("quantize", "rabitq_encode", "pca_fit_cov", "pca_project", "kmeans_assign", "kmeans_update",
-           "kmeans_fit", "kmeans_fine", "kmeans_fit_hier", "kmeans_cost", "km_last_error", "km_release")
+           "kmeans_fit", "kmeans_fine", "kmeans_fit_hier", "kmeans_assign_pruned", "kmeans_fit_pruned", "kmeans_cost",
+           "km_last_error", "km_release")
 
 
 class KmqError(RuntimeError):
@@ -44,6 +45,10 @@ class KmFitStats(ct.Structure):
 
     def as_dict(self):
         return {f: getattr(self, f) for f, _ in self._fields_}
+
+
+class KmPrune(ct.Structure):
+    _fields_ = [("eps0", ct.c_double), ("d_front", ct.c_int32), ("reserved", ct.c_int32)]
 
 
 class KmHierParams(ct.Structure):
@@ -74,6 +79,9 @@ def lib():
             "kmeans_fine": [ct.POINTER(KmPoints), vp, i32, i32, i32, i32, vp, vp, vp, vp, i32, vp],
             "kmeans_fit_hier": [ct.POINTER(KmPoints), i32, ct.POINTER(KmHierParams), vp, vp, vp, vp, vp, vp, i32,
                                 ct.POINTER(KmFitStats), vp, vp],
+            "kmeans_assign_pruned": [ct.POINTER(KmPoints), vp, i32, vp, vp, vp, vp, ct.POINTER(KmPrune), vp, vp],
+            "kmeans_fit_pruned": [ct.POINTER(KmPoints), i32, i32, vp, vp, vp, vp, i32, ct.POINTER(KmPrune),
+                                  ct.POINTER(KmFitStats), vp, vp],
             "kmeans_cost": [vp, i64, i32, i64, vp, i32, vp, vp, vp],
             "km_release": [],
         }
@@ -363,6 +371,48 @@ def kmeans_fit(P: Points, k: int, iters: int, init_idx=None, C: torch.Tensor | N
     _check(lib().kmeans_fit(P.ref, k, iters, idx_p, _ptr(C), _ptr(a), _ptr(obj), policy,
                             ct.byref(stats) if stats is not None else None, _stream()))
     return C, a, obj
+
+
+def kmeans_assign_pruned(P: Points, C: torch.Tensor, prev: torch.Tensor, eps0: float = 2.1, d_front: int = 0,
+                         dist: bool = True, objective: bool = False, counters: bool = False):
+    """One pruned STEP 2 from the previous assignment `prev` (fp32 or SQ8 points).
+    Returns (assign, dist double[n] or None, objective double[1] or None,
+    counters numpy uint64[3] or None)."""
+    k = _check_C(P, C)
+    _dev(prev, torch.int32, "prev", 1)
+    a = torch.empty(P.n, dtype=torch.int32, device=P.device)
+    dd = torch.empty(P.n, dtype=torch.float64, device=P.device) if dist else None
+    obj = torch.empty(1, dtype=torch.float64, device=P.device) if objective else None
+    cnt = np.zeros(3, dtype=np.uint64) if counters else None
+    pr = KmPrune(eps0, d_front, 0)
+    _check(lib().kmeans_assign_pruned(P.ref, _ptr(C), k, _ptr(prev), _ptr(a), _ptr(dd), _ptr(obj), ct.byref(pr),
+                                      cnt.ctypes.data_as(ct.c_void_p) if counters else None, _stream()))
+    return a, dd, obj, cnt
+
+
+def kmeans_fit_pruned(P: Points, k: int, iters: int, init_idx=None, C: torch.Tensor | None = None,
+                      policy: int = KM_EMPTY_SPLIT, eps0: float = 2.1, d_front: int = 0, objective: bool = True,
+                      stats: KmFitStats | None = None, counters: bool = False):
+    """Lloyd with dimension pruning in every assignment pass after the first.
+    Returns (C, assign, objective double[iters+1] or None, counters numpy uint64[3] or None)."""
+    if C is None:
+        C = torch.empty((k, P.d), dtype=P.centroid_dtype(), device=P.device)
+    else:
+        _check_C(P, C)
+    a = torch.empty(P.n, dtype=torch.int32, device=P.device)
+    obj = torch.empty(iters + 1, dtype=torch.float64, device=P.device) if objective else None
+    idx_p = None
+    if init_idx is not None:
+        idx = np.ascontiguousarray(np.asarray(init_idx, dtype=np.int64))
+        if idx.shape != (k,):
+            raise ValueError("init_idx must hold k indices")
+        idx_p = idx.ctypes.data_as(ct.c_void_p)
+    cnt = np.zeros(3, dtype=np.uint64) if counters else None
+    pr = KmPrune(eps0, d_front, 0)
+    _check(lib().kmeans_fit_pruned(P.ref, k, iters, idx_p, _ptr(C), _ptr(a), _ptr(obj), policy, ct.byref(pr),
+                                   ct.byref(stats) if stats is not None else None,
+                                   cnt.ctypes.data_as(ct.c_void_p) if counters else None, _stream()))
+    return C, a, obj, cnt
 
 
 def kmeans_fine(P: Points, meso_assign: torch.Tensor, k_meso: int, k: int, iters: int,

@@ -17,7 +17,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libkmq.so")
 BUILD = os.path.join(HERE, "_build")
-SOURCES = ["api.hip", "assign.hip", "update.hip", "quantize.hip", "pca.hip", "hier.hip"]
+SOURCES = ["api.hip", "assign.hip", "update.hip", "quantize.hip", "pca.hip", "hier.hip", "skm.hip"]
 ARCH = os.environ.get("KMQ_OFFLOAD_ARCH", "gfx950")
 
 CFLAGS = [

@@ -615,6 +615,137 @@ km_status kmeans_fit(const km_points *P, int32_t k, int32_t iters, const int64_t
   return KM_OK;
 }
 
+static km_status check_prune(const Points &p, const km_prune *pr, int *D0) {
+  KMQ_CHECK(pr != nullptr, KM_EINVAL, "pruning parameters are NULL");
+  KMQ_CHECK(p.fmt == KM_F32 || p.fmt == KM_SQ8, KM_EUNSUPPORTED,
+            "dimension pruning is implemented for fp32 and SQ8 points (fmt = %d)", p.fmt);
+  KMQ_CHECK(pr->reserved == 0, KM_EINVAL, "reserved field must be 0");
+  KMQ_CHECK(pr->eps0 > 0.0, KM_EINVAL, "eps0 must be > 0");
+  const int d0 = pr->d_front ? pr->d_front : prune_front_default(p.d);
+  const int g = p.fmt == KM_F32 ? 4 : 16;
+  KMQ_CHECK(d0 >= 1 && d0 <= p.d && d0 % g == 0, KM_EINVAL,
+            "d_front = %d must lie in [1, d] and be a multiple of %d", d0, g);
+  KMQ_CHECK(d0 <= 256 && p.d - d0 <= 2048, KM_EUNSUPPORTED,
+            "pruning supports d_front <= 256 and d - d_front <= 2048 (d_front = %d, d = %d)", d0, p.d);
+  *D0 = d0;
+  return KM_OK;
+}
+
+km_status kmeans_assign_pruned(const km_points *P, const void *C, int32_t k, const int32_t *prev, int32_t *assign,
+                               double *dist, double *objective, const km_prune *pr, uint64_t *counters,
+                               km_stream stream) {
+  g_err[0] = 0;
+  Points p;
+  km_status st = check_points(P, &p);
+  if (st != KM_OK) return st;
+  st = check_centroids(p, C, k);
+  if (st != KM_OK) return st;
+  KMQ_CHECK(prev != nullptr && assign != nullptr, KM_EINVAL, "prev or assign is NULL");
+  int D0 = 0;
+  st = check_prune(p, pr, &D0);
+  if (st != KM_OK) return st;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const size_t b_pr = al(pruned_bytes(p, k));
+  Scratch ws(s);
+  st = ws.alloc(b_pr + al(3 * sizeof(unsigned long long)));
+  if (st != KM_OK) return st;
+  unsigned long long *cnt = counters ? reinterpret_cast<unsigned long long *>(ws.get() + b_pr) : nullptr;
+  if (cnt) {
+    st = launch_zero_counters(cnt, s);
+    if (st != KM_OK) return st;
+  }
+  st = launch_assign_pruned(p, C, k, prev, assign, dist, objective, pr->eps0, D0, cnt, ws.get(), s);
+  if (st != KM_OK) return st;
+  if (cnt) {
+    KMQ_HIP(hipMemcpyAsync(counters, cnt, 3 * sizeof(unsigned long long), hipMemcpyDeviceToHost, s));
+    KMQ_HIP(hipStreamSynchronize(s));
+  }
+  return KM_OK;
+}
+
+km_status kmeans_fit_pruned(const km_points *P, int32_t k, int32_t iters, const int64_t *init_idx, void *C,
+                            int32_t *assign, double *objective, int32_t policy, const km_prune *pr,
+                            km_fit_stats *stats, uint64_t *counters, km_stream stream) {
+  g_err[0] = 0;
+  Points p;
+  km_status st = check_points(P, &p);
+  if (st != KM_OK) return st;
+  st = check_centroids(p, C, k);
+  if (st != KM_OK) return st;
+  KMQ_CHECK(assign != nullptr, KM_EINVAL, "assign is NULL");
+  KMQ_CHECK(k <= p.n, KM_EINVAL, "k = %d exceeds n = %lld", k, (long long)p.n);
+  KMQ_CHECK(iters >= 0, KM_EINVAL, "iters = %d must be >= 0", iters);
+  KMQ_CHECK(policy == KM_EMPTY_SPLIT || policy == KM_EMPTY_KEEP, KM_EINVAL, "unknown empty-cluster policy %d", policy);
+  int D0 = 0;
+  st = check_prune(p, pr, &D0);
+  if (st != KM_OK) return st;
+  if (init_idx) {
+    st = check_init_idx(init_idx, k, p.n);
+    if (st != KM_OK) return st;
+  }
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const size_t b_prep = al(prep_bytes(p, k));
+  const size_t b_upd = al(std::max(update_bytes(p, k), p.raw ? update_bytes(raw_points(p), k) : (size_t)0));
+  const size_t b_score = objective ? al(sizeof(float) * (size_t)p.n) : 0;
+  const size_t b_xc = objective ? al(sizeof(float) * (size_t)p.n) : 0;
+  const size_t b_part = objective ? al(sizeof(double) * (size_t)objective_blocks(p.n)) : 0;
+  const size_t b_idx = init_idx ? al(sizeof(int64_t) * (size_t)k) : 0;
+  const size_t b_pr = al(pruned_bytes(p, k));
+  const size_t b_cnt = al(3 * sizeof(unsigned long long));
+  Scratch ws(s);
+  st = ws.alloc(b_prep + b_upd + b_score + b_xc + b_part + b_idx + b_pr + b_cnt);
+  if (st != KM_OK) return st;
+  uint8_t *w = ws.get();
+  uint8_t *wprep = w;
+  uint8_t *wupd = w + b_prep;
+  float *sc = objective ? reinterpret_cast<float *>(wupd + b_upd) : nullptr;
+  float *xc = reinterpret_cast<float *>(wupd + b_upd + b_score);
+  double *part = reinterpret_cast<double *>(wupd + b_upd + b_score + b_xc);
+  int64_t *didx = reinterpret_cast<int64_t *>(wupd + b_upd + b_score + b_xc + b_part);
+  uint8_t *wpr = wupd + b_upd + b_score + b_xc + b_part + b_idx;
+  unsigned long long *cnt = counters ? reinterpret_cast<unsigned long long *>(wpr + b_pr) : nullptr;
+  try {
+    StageClock clk(stats != nullptr, s);
+    if (cnt) KMQ_STAGE(clk, kStOther, launch_zero_counters(cnt, s));
+    if (init_idx) {
+      KMQ_HIP(hipMemcpyAsync(didx, init_idx, sizeof(int64_t) * (size_t)k, hipMemcpyHostToDevice, s));
+      KMQ_STAGE(clk, kStOther, launch_gather_init(p, didx, k, C, s));
+    }
+    // the first pass is a full assignment
+    CentroidPrep cp;
+    KMQ_STAGE(clk, kStPrep, launch_prep(p, C, k, wprep, &cp, s));
+    KMQ_STAGE(clk, kStAssign, launch_assign(p, C, cp, k, assign, sc, s));
+    if (objective) {
+      KMQ_STAGE(clk, kStOther, launch_xconst(p, xc, s));
+      KMQ_STAGE(clk, kStOther, launch_objective(p, xc, sc, p.n, objective, part, objective_blocks(p.n), s));
+    }
+    for (int it = 1; it <= iters; ++it) {
+      if (p.raw && it == iters) {  // last update from the raw rows (Sec. 4.1)
+        KMQ_STAGE(clk, kStUpdate, launch_update(raw_points(p), assign, k, C, nullptr, policy, wupd, s));
+      } else {
+        KMQ_STAGE(clk, kStUpdate, launch_update(p, assign, k, C, nullptr, policy, wupd, s));
+      }
+      KMQ_STAGE(clk, kStAssign,
+                launch_assign_pruned(p, C, k, assign, assign, nullptr, objective ? objective + it : nullptr,
+                                     pr->eps0, D0, cnt, wpr, s));
+    }
+    if (stats) {
+      st = clk.collect(stats);
+      if (st != KM_OK) return st;
+      stats->assign_passes = iters + 1;
+      stats->updates = iters;
+    }
+    if (cnt) {
+      KMQ_HIP(hipMemcpyAsync(counters, cnt, 3 * sizeof(unsigned long long), hipMemcpyDeviceToHost, s));
+      KMQ_HIP(hipStreamSynchronize(s));
+    }
+  } catch (const std::bad_alloc &) {
+    set_error("host allocation failed");
+    return KM_ENOMEM;
+  }
+  return KM_OK;
+}
+
 km_status kmeans_fine(const km_points *P, const int32_t *meso_assign, int32_t k_meso, int32_t k, int32_t iters,
                       int32_t flags, void *C, int32_t *assign, int32_t *k_fine, double *objective, int32_t policy,
                       km_stream stream) {

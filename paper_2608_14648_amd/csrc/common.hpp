@@ -109,6 +109,15 @@ Points slice_points(const Points &P, int64_t start, int64_t count);
 km_status launch_scatter_assign(const int *perm, const int32_t *a_perm, int64_t nsel, int64_t n, int32_t *assign,
                                 hipStream_t s);
 
+// skm.hip: dimension pruning inside STEP 2
+double prune_factor(int D, int d, double eps0);
+int prune_front_default(int d);
+size_t pruned_bytes(const Points &P, int k);
+km_status launch_assign_pruned(const Points &P, const void *C, int k, const int32_t *prev, int32_t *assign,
+                               double *dist, double *objective, double eps0, int D0,
+                               unsigned long long *cnt, void *ws, hipStream_t s);
+km_status launch_zero_counters(unsigned long long *c, hipStream_t s);
+
 // quantize.hip
 size_t quantize_bytes(int64_t n, int d, int fmt);
 km_status launch_quantize(const float *X, int64_t n, int d, int64_t ldx, int fmt, void *codes,

@@ -242,3 +242,46 @@ def test_hierarchical_argument_checks(kmq):
     args[2], args[3] = ct.byref(hp0), oob
     assert L.kmeans_fit_hier(*args) == -1
     assert "outside" in L.km_last_error().decode()
+
+
+def test_pruned_argument_checks(kmq):
+    """kmeans_assign_pruned / kmeans_fit_pruned reject bad arguments on the host."""
+    L = kmq.lib()
+    P = _pts(kmq, d=768, ld=768)
+    pr = kmq.KmPrune(2.1, 0, 0)
+    ok = [ct.byref(P), FAKE, 4, FAKE, FAKE, None, None, ct.byref(pr), None, None]
+    cases = [(3, None, -1, "NULL"), (7, None, -1, "NULL")]
+    for i, v, code, msg in cases:
+        args = list(ok)
+        args[i] = v
+        assert L.kmeans_assign_pruned(*args) == code, msg
+        assert msg in L.km_last_error().decode()
+    for params, code, msg in [((0.0, 0, 0), -1, "eps0"), ((2.1, 0, 1), -1, "reserved"), ((2.1, 6, 0), -1, "d_front"),
+                              ((2.1, 512, 0), -2, "d_front"), ((2.1, 800, 0), -1, "d_front")]:
+        pr2 = kmq.KmPrune(*params)
+        args = list(ok)
+        args[7] = ct.byref(pr2)
+        assert L.kmeans_assign_pruned(*args) == code, msg
+        assert msg in L.km_last_error().decode(), (msg, L.km_last_error())
+    # formats other than fp32 / SQ8, and rows too long after d'
+    P1 = _pts(kmq, fmt=3, d=128, alpha=0x2000, center=0x3000)
+    args = list(ok)
+    args[0] = ct.byref(P1)
+    assert L.kmeans_assign_pruned(*args) == -2
+    Pw = _pts(kmq, d=4096, ld=4096)
+    args = list(ok)
+    args[0] = ct.byref(Pw)
+    assert L.kmeans_assign_pruned(*args) == -2
+    # SQ8: d' must be a multiple of 16
+    Ps = _pts(kmq, fmt=2, d=256, ld=256)
+    pr3 = kmq.KmPrune(2.1, 40, 0)
+    args = list(ok)
+    args[0], args[7] = ct.byref(Ps), ct.byref(pr3)
+    assert L.kmeans_assign_pruned(*args) == -1
+    # the fit: k > n, negative iterations, policy
+    fit_ok = [ct.byref(P), 4, 3, None, FAKE, FAKE, None, 0, ct.byref(pr), None, None, None]
+    for i, v, msg in [(1, 101, "exceeds"), (2, -1, "iters"), (7, 4, "policy"), (8, None, "NULL")]:
+        args = list(fit_ok)
+        args[i] = v
+        assert L.kmeans_fit_pruned(*args) == -1, msg
+        assert msg in L.km_last_error().decode(), (msg, L.km_last_error())
