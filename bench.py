@@ -18,7 +18,9 @@ through the paper's RabitQ pipeline (random rotation, SQ4 centroid codes with
 bias, last update from the raw rotated rows); --workload 8 runs the default
 workload's data as LVQ4 codes; --workload 9 runs hierarchical k-means (meso,
 then fine clustering inside each meso-cluster) on the 10M x 1024 data with
-k = 4 sqrt(N), fp32 and SQ8, and reports fits per second.
+k = 4 sqrt(N), fp32 and SQ8, and reports fits per second; --workload 10 runs
+the default workload's data under a random rotation with dimension pruning in
+the assignment passes (fp32 and SQ8).
 
 After the timed region, `quality` reports each final partition's full-precision
 cost (raw-vector member means), its cluster-size spread and, for the compressed
@@ -410,6 +412,73 @@ def workload_hier(cfg, torch, km, args):
     return step, finish, None, quality
 
 
+def workload_pruned(cfg, torch, km, args):
+    """The 1M x 768, k=1000 mixture under a random rotation, clustered with dimension
+    pruning in every assignment pass after the first (SuperKMeans with the ADSampling
+    test, eps0 = 2.1, d' = 96), as fp32 vectors and as SQ8 codes of the rotated
+    vectors.  One step: rotation (projection with an orthogonal matrix), pruned fp32
+    fit, SQ8 encode, pruned SQ8 fit, full-precision partition costs."""
+    spec = cfg["spec"] if args.n is None else cfg["spec"].with_n(args.n)
+    k, T = cfg["k"], cfg["iters"]
+    import synth
+    log(f"generating {spec.n} x {spec.d} mixture")
+    X = upload(spec, torch)
+    idx = synth.init_indices(spec.n, k)
+    R = torch.from_numpy(synth.random_rotation(spec.d, 11)).cuda()
+    zero = torch.zeros(spec.d, dtype=torch.float32, device="cuda")
+    Y = torch.empty_like(X)
+    P32 = km.points_f32(X)
+    mu = torch.empty((k, spec.d), dtype=torch.float32, device="cuda")
+    res = {}
+
+    def step(timer):
+        km.pca_project(X, zero, R, out=Y)
+        st32, st8 = km.KmFitStats(), km.KmFitStats()
+        C, a, J, c32 = km.kmeans_fit_pruned(km.points_f32(Y), k, T, idx, stats=st32, counters=True)
+        codes, _ = km.quantize_sq8(Y)
+        C8, a8, J8, c8 = km.kmeans_fit_pruned(km.points_sq8(codes), k, T, idx, stats=st8, counters=True)
+        costs = {}
+        for name, aa in (("f32", a), ("sq8", a8)):  # rotation keeps distances: cost on the raw rows
+            km.kmeans_update(P32, aa, mu, km.KM_EMPTY_KEEP, counts=False)
+            costs[name] = km.kmeans_cost(X, mu, aa)
+        if timer is not None:
+            timer.add("f32", st32)
+            timer.add("sq8", st8)
+            res.update(c32=c32, c8=c8, codes=codes)
+        return {"a": a, "a8": a8, "costs": costs}, J
+
+    def finish(out, timer, elapsed, K):
+        s32, s8 = timer.stats["f32"], timer.stats["sq8"]
+        pruned_passes = T  # per fit, after the full first pass
+
+        def frac(c):
+            c = c.astype(np.float64)
+            return {"front_pass": c[1] / max(1.0, c[0]), "full_distance": c[2] / max(1.0, c[0]),
+                    "candidates_tested_per_pass": c[0] / pruned_passes}
+        return {"value": 2 * T * K / elapsed, "unit": "Lloyd iters/s", "dtype": "f32+i8",
+                "config": {"workload": f"gmm{spec.n // 1000000}m_d{spec.d}_k{k}_pruned_f32_sq8", "N": spec.n,
+                           "d": spec.d, "k": k, "iters": T, "formats": ["f32", "sq8"], "eps0": 2.1,
+                           "d_front": 32 * ((spec.d + 255) // 256), "rotation": "random orthogonal"},
+                "partition_cost": {f: float(v.item()) for f, v in out["costs"].items()},
+                "survivors": {"f32": frac(res["c32"]), "sq8": frac(res["c8"])},
+                "stages": {"f32": stage_summary(s32), "sq8": stage_summary(s8)}}
+
+    def quality(out):
+        log("quality: exact fp32 and SQ8 fits on the rotated rows (outside the timed region)")
+        st, st8 = km.KmFitStats(), km.KmFitStats()
+        _, a_ex, _ = km.kmeans_fit(km.points_f32(Y), k, T, idx, objective=False, stats=st)
+        _, a8_ex, _ = km.kmeans_fit(km.points_sq8(res["codes"]), k, T, idx, objective=False, stats=st8)
+        q = {"f32_exact": partition_stats(km, X, a_ex, mu), "sq8_exact": partition_stats(km, X, a8_ex, mu),
+             "f32_pruned": partition_stats(km, X, out["a"], mu), "sq8_pruned": partition_stats(km, X, out["a8"], mu)}
+        q["objective_ratio_f32_pruned_vs_exact"] = q["f32_pruned"]["cost"] / q["f32_exact"]["cost"]
+        q["objective_ratio_sq8_pruned_vs_f32_exact"] = q["sq8_pruned"]["cost"] / q["f32_exact"]["cost"]
+        q["exact_assign_ms_per_pass"] = {"f32": st.assign_ms / st.assign_passes,
+                                         "sq8": st8.assign_ms / st8.assign_passes}
+        return q
+
+    return step, finish, None, quality
+
+
 def workload_sign1(cfg, torch, km, args):
     spec = cfg["spec"] if args.n is None else cfg["spec"].with_n(args.n)
     k, T = cfg["k"], cfg["iters"]
@@ -612,8 +681,9 @@ def workload_c1(cfg, torch, km, args):
 
 
 WORKLOADS = {1: workload_c1, 2: workload_c2, 3: workload_sign1, 4: workload_pca, 5: workload_hybrid,
-             6: workload_bf16, 7: workload_rabitq, 8: workload_lvq4, 9: workload_hier}
-CONFIG_OF = {6: 2, 7: 3, 8: 2, 9: 4}  # measurement-only workloads and the configuration whose data they use
+             6: workload_bf16, 7: workload_rabitq, 8: workload_lvq4, 9: workload_hier,
+             10: workload_pruned}
+CONFIG_OF = {6: 2, 7: 3, 8: 2, 9: 4, 10: 2}  # measurement-only workloads and the configuration whose data they use
 
 
 def main():

@@ -6,14 +6,16 @@
 // every 64 dims; the survivors are compared on the full distance.
 //
 //   front norms  ||x'||^2 of the points and ||c'||^2 of the centroids over d'
-//   tau          one wave per point: distance to the previous centroid, summed
-//                in the same 64-dim chunks as the refinement below
+//   tau          one wave per point: distance to the previous centroid (16-byte
+//                loads per lane)
 //   front        MFMA tile kernel (128 points x 128 centroids, fp32 or int8):
 //                p(d') = ||x'||^2 + ||c'||^2 - 2 <x', c'> for every pair, the test
-//                at d', one survivor bit per pair ([ceil(k/32)][n] words)
-//   refine       one wave per point, lanes over 64 consecutive dims: every
-//                survivor's distance grows chunk by chunk with the test after each
-//                chunk; the last chunk gives the full distance
+//                at d', one survivor bit per pair; each point's bits are one
+//                row of W4 words (W4 = ceil(k/128) * 4), written 16 bytes per tile
+//   refine       one wave per point, lanes over 64 consecutive dims: the point's
+//                mask row is read with one load, then every survivor's row is
+//                loaded whole and its distance grows chunk by chunk with the test
+//                after each chunk; the last chunk gives the full distance
 //
 // SQ8 codes: exact integer distances, the test in fp32 on (float)p and
 // (float)tau; fp32 points: fp32 sums.
@@ -44,14 +46,14 @@ struct SkmArgs {
   const void *xn;    // point front norms (float / int)
   const void *cn;    // centroid front norms (float / int)
   int D0;            // front dims d'
-  int W;             // words per point in the survivor mask
-  uint32_t *mask;    // [W][n]
+  int W4;            // words per point row of the survivor mask (multiple of 4)
+  uint32_t *mask;    // [n][W4]
   int front_test;    // d' < d: the first checkpoint is inside the row
   float r0;          // r(d')
   float rt[kMaxTail];  // r(d' + 64 (t + 1)) for the checkpoints inside the row
   int32_t *assign;
   double *dist;
-  unsigned long long *cnt;  // nullable: tested at d', passed d', compared in full
+  unsigned long long *cnt;  // nullable: per-workgroup (front: 2 per group) / per-wave (refine) partial counts
 };
 
 template <int FMT>
@@ -92,47 +94,49 @@ __global__ __launch_bounds__(256) void skm_norm_kernel(const uint8_t *rows, int6
   if (lane == 0) static_cast<Val<FMT> *>(out)[r] = s;
 }
 
-// Squared distance of a point row x to a centroid row c, summed in the chunk
-// order of the refinement: 64-dim chunks of [0, D0), then of [D0, d).
-template <int FMT>
-__device__ __forceinline__ Val<FMT> chunked_dist(const uint8_t *x, const uint8_t *c, int D0, int d, int lane) {
-  Val<FMT> acc = 0;
-  for (int b = 0; b < D0; b += 64) {
-    const int i = b + lane;
-    Val<FMT> t = 0;
-    if (i < D0) {
-      t = elem<FMT>(x, i) - elem<FMT>(c, i);
-      t = t * t;
-    }
-    acc += wave_sum(t);
-  }
-  for (int b = D0; b < d; b += 64) {
-    const int i = b + lane;
-    Val<FMT> t = 0;
-    if (i < d) {
-      t = elem<FMT>(x, i) - elem<FMT>(c, i);
-      t = t * t;
-    }
-    acc += wave_sum(t);
-  }
-  return acc;
-}
-
 template <int FMT>
 __global__ __launch_bounds__(256) void skm_tau_kernel(SkmArgs A, void *tau) {
   const int lane = threadIdx.x & 63;
   const int64_t p = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (p >= A.n) return;
   const int j = min(max(A.prev[p], 0), A.k - 1);
-  const size_t esz = FMT == KM_F32 ? 4 : 1;
-  const Val<FMT> t = chunked_dist<FMT>(A.X + p * A.xld, A.C + (int64_t)j * A.d * esz, A.D0, A.d, lane);
-  if (lane == 0) static_cast<Val<FMT> *>(tau)[p] = t;
+  Val<FMT> acc = 0;
+  if constexpr (FMT == KM_F32) {  // d % 4 == 0
+    const float *x = reinterpret_cast<const float *>(A.X + p * A.xld);
+    const float *c = reinterpret_cast<const float *>(A.C) + (int64_t)j * A.d;
+    for (int i = 4 * lane; i < A.d; i += 256) {
+      const f32x4 xv = *reinterpret_cast<const f32x4 *>(x + i);
+      const f32x4 cv = *reinterpret_cast<const f32x4 *>(c + i);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float t = xv[e] - cv[e];
+        acc += t * t;
+      }
+    }
+  } else {  // d % 16 == 0
+    const uint8_t *x = A.X + p * A.xld;
+    const uint8_t *c = A.C + (int64_t)j * A.d;
+    for (int i = 16 * lane; i < A.d; i += 1024) {
+      const uint4 xv = *reinterpret_cast<const uint4 *>(x + i);
+      const uint4 cv = *reinterpret_cast<const uint4 *>(c + i);
+      const uint32_t xs[4] = {xv.x, xv.y, xv.z, xv.w}, cs[4] = {cv.x, cv.y, cv.z, cv.w};
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int t = (int)((xs[e >> 2] >> (8 * (e & 3))) & 255u) - (int)((cs[e >> 2] >> (8 * (e & 3))) & 255u);
+        acc += t * t;
+      }
+    }
+  }
+  acc = wave_sum(acc);
+  if (lane == 0) static_cast<Val<FMT> *>(tau)[p] = acc;
 }
 
 // ---- front: all pairs over d' dims on the matrix cores, the test at d' -------
 template <int FMT>
 __global__ __launch_bounds__(256) void skm_front_kernel(SkmArgs A) {
   __shared__ __align__(16) uint8_t lds[2][2][kFTile];  // [buffer][centroids, points]
+  __shared__ Val<FMT> cnl[kFT];                       // front norms of the tile's centroids
+  __shared__ __align__(16) uint32_t mrow[kFT][4];     // the tile's 4 mask words of each point
   constexpr bool F = FMT == KM_F32;
   constexpr int esz = F ? 4 : 1;
   using Acc = typename std::conditional<F, f32x16, i32x16>::type;
@@ -144,7 +148,10 @@ __global__ __launch_bounds__(256) void skm_front_kernel(SkmArgs A) {
   const int64_t id = blockIdx.x;
   const int64_t pt = ((id >> 3) / nct) * 8 + (id & 7);
   const int ct = (int)((id >> 3) % nct);
-  if (pt >= npt) return;
+  if (pt >= npt) {
+    if (A.cnt && t == 0) A.cnt[2 * id] = A.cnt[2 * id + 1] = 0ull;
+    return;
+  }
   const int64_t p0 = pt * kFT;
   const int c0 = ct * kFT;
   const int bytes = A.D0 * esz;
@@ -189,6 +196,7 @@ __global__ __launch_bounds__(256) void skm_front_kernel(SkmArgs A) {
     }
   };
 
+  if (t < kFT) cnl[t] = static_cast<const Val<FMT> *>(A.cn)[min(c0 + t, A.k - 1)];
   load(0);
   store(0, 0);
   __syncthreads();
@@ -246,14 +254,14 @@ __global__ __launch_bounds__(256) void skm_front_kernel(SkmArgs A) {
         const int off = 8 * (v >> 2) + 4 * h + (v & 3);
         const int j = jb + off;
         const bool cand = p < A.n && j < A.k && j != pj;
-        const int jc = min(j, A.k - 1);
         bool keep = true;
         if (A.front_test) {
+          const Val<FMT> cnj = cnl[wc * 64 + cb * 32 + off];
           if constexpr (F) {
-            const float pd = fmaf(-2.0f, acc[cb][pb][v], xn + static_cast<const float *>(A.cn)[jc]);
+            const float pd = fmaf(-2.0f, acc[cb][pb][v], xn + cnj);
             keep = !(pd > lim);
           } else {
-            const int pd = xn + static_cast<const int *>(A.cn)[jc] - 2 * acc[cb][pb][v];
+            const int pd = xn + cnj - 2 * acc[cb][pb][v];
             keep = !((float)pd > lim);
           }
         }
@@ -263,98 +271,165 @@ __global__ __launch_bounds__(256) void skm_front_kernel(SkmArgs A) {
         passed += A.front_test && bit;
       }
       m |= __shfl_xor(m, 32);
-      if (h == 0 && p < A.n && jb < A.k) A.mask[(int64_t)(jb >> 5) * A.n + p] = m;
+      if (h == 0) mrow[wp * 64 + pb * 32 + r][wc * 2 + cb] = m;
     }
   }
-  if (A.cnt) {
+  __syncthreads();
+  if (t < kFT && p0 + t < A.n)  // words 4 ct .. 4 ct + 3 of the point's row (rows padded to W4 words)
+    *reinterpret_cast<uint4 *>(A.mask + (p0 + t) * A.W4 + 4 * ct) = *reinterpret_cast<const uint4 *>(mrow[t]);
+  if (A.cnt) {  // per-workgroup partial counts (summed later in a fixed order)
+    __shared__ unsigned long long cw[4][2];
     tested = wave_sum(tested);
     passed = wave_sum(passed);
     if (lane == 0) {
-      atomicAdd(A.cnt, tested);
-      atomicAdd(A.cnt + 1, passed);
+      cw[w][0] = tested;
+      cw[w][1] = passed;
+    }
+    __syncthreads();
+    if (t == 0) {
+      A.cnt[2 * id] = cw[0][0] + cw[1][0] + cw[2][0] + cw[3][0];
+      A.cnt[2 * id + 1] = cw[0][1] + cw[1][1] + cw[2][1] + cw[3][1];
     }
   }
 }
 
 // ---- refinement of the survivors: one wave per point ---------------------------
+// The point's mask row is read first; a point without survivors keeps its previous
+// centroid without touching its row.  Survivors are taken in groups of kGroup
+// (ascending index): chunk by chunk, the group's loads and reductions are
+// independent of each other, and every survivor stops at its first failed
+// checkpoint.
+constexpr int kGroup = 8;
+
 template <int FMT>
 __global__ __launch_bounds__(256) void skm_refine_kernel(SkmArgs A) {
   constexpr bool F = FMT == KM_F32;
   constexpr int esz = F ? 4 : 1;
   const int lane = threadIdx.x & 63;
-  const int64_t p = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (p >= A.n) return;
+  const int64_t wid = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int64_t nw = (int64_t)gridDim.x * 4;
   const int d = A.d, D0 = A.D0;
   const int nf = (D0 + 63) >> 6, nt = (d - D0 + 63) >> 6;
-  const uint8_t *x = A.X + p * A.xld;
-  Val<FMT> xf[kMaxFront], xt[kMaxTail];
-#pragma unroll
-  for (int m = 0; m < kMaxFront; ++m) {
-    const int i = 64 * m + lane;
-    xf[m] = (m < nf && i < D0) ? elem<FMT>(x, i) : (Val<FMT>)0;
-  }
-#pragma unroll
-  for (int m = 0; m < kMaxTail; ++m) {
-    const int i = D0 + 64 * m + lane;
-    xt[m] = (m < nt && i < d) ? elem<FMT>(x, i) : (Val<FMT>)0;
-  }
-  const int pj = min(max(A.prev[p], 0), A.k - 1);
-  const Val<FMT> tau = static_cast<const Val<FMT> *>(A.tau)[p];
-  const float tauf = (float)tau;
-  Val<FMT> bd = tau;
-  int best = pj;
   unsigned long long full = 0;
-  for (int wi = 0; wi < A.W; ++wi) {
-    uint32_t bits = A.mask[(int64_t)wi * A.n + p];
-    while (bits) {
-      const int j = wi * 32 + __ffs(bits) - 1;
-      bits &= bits - 1;
-      const uint8_t *c = A.C + (int64_t)j * d * esz;
-      Val<FMT> acc = 0;
+  for (int64_t p = wid; p < A.n; p += nw) {  // waves stride over the points
+    const int pj = min(max(A.prev[p], 0), A.k - 1);
+    const Val<FMT> tau = static_cast<const Val<FMT> *>(A.tau)[p];
+    const float tauf = (float)tau;
+    Val<FMT> bd = tau;
+    int best = pj;
+    const uint8_t *x = A.X + p * A.xld;
+    const uint32_t *mrow = A.mask + p * A.W4;
+    for (int w0 = 0; w0 < A.W4; w0 += 64) {  // 64 mask words (2048 centroids) per load
+      const uint32_t wv = w0 + lane < A.W4 ? mrow[w0 + lane] : 0u;
+      uint64_t nz = __ballot(wv != 0u);
+      uint32_t bits = 0u;
+      int wbase = 0;
+      while (nz || bits) {
+        // the next group of survivors, in ascending index
+        int jg[kGroup];
+        int ng = 0;
 #pragma unroll
-      for (int m = 0; m < kMaxFront; ++m) {
-        if (m < nf) {
-          const int i = 64 * m + lane;
-          Val<FMT> t = 0;
-          if (i < D0) {
-            t = xf[m] - elem<FMT>(c, i);
-            t = t * t;
+        for (int g = 0; g < kGroup; ++g) {
+          jg[g] = 0;
+          if (!bits && nz) {
+            const int wl = __ffsll((unsigned long long)nz) - 1;
+            nz &= nz - 1;
+            bits = __shfl(wv, wl);
+            wbase = (w0 + wl) * 32;
           }
-          acc += wave_sum(t);
+          if (bits) {
+            jg[g] = wbase + __ffs(bits) - 1;
+            bits &= bits - 1;
+            ng = g + 1;
+          }
         }
-      }
-      bool alive = true;
+        Val<FMT> acc[kGroup];
+        uint32_t alive = (1u << ng) - 1u;
 #pragma unroll
-      for (int m = 0; m < kMaxTail; ++m) {
-        if (m < nt && alive) {
-          const int i = D0 + 64 * m + lane;
-          Val<FMT> t = 0;
-          if (i < d) {
-            t = xt[m] - elem<FMT>(c, i);
-            t = t * t;
+        for (int g = 0; g < kGroup; ++g) acc[g] = 0;
+#pragma unroll
+        for (int m = 0; m < kMaxFront; ++m) {
+          if (m < nf) {
+            const int i = 64 * m + lane;
+            const Val<FMT> xv = i < D0 ? elem<FMT>(x, i) : (Val<FMT>)0;
+            Val<FMT> cv[kGroup];
+#pragma unroll
+            for (int g = 0; g < kGroup; ++g)
+              cv[g] = (g < ng && i < D0) ? elem<FMT>(A.C + (int64_t)jg[g] * d * esz, i) : xv;
+#pragma unroll
+            for (int g = 0; g < kGroup; ++g) {
+              if (g < ng) {
+                const Val<FMT> t = xv - cv[g];
+                acc[g] += wave_sum(t * t);
+              }
+            }
           }
-          acc += wave_sum(t);
-          if (D0 + 64 * (m + 1) < d && (float)acc > tauf * A.rt[m]) alive = false;  // checkpoint inside the row
         }
-      }
-      if (alive) {
-        ++full;
-        if (acc < bd || (acc == bd && j < best)) {
-          bd = acc;
-          best = j;
+#pragma unroll
+        for (int m = 0; m < kMaxTail; ++m) {
+          if (m < nt && alive) {
+            const int i = D0 + 64 * m + lane;
+            const Val<FMT> xv = i < d ? elem<FMT>(x, i) : (Val<FMT>)0;
+            Val<FMT> cv[kGroup];
+#pragma unroll
+            for (int g = 0; g < kGroup; ++g)
+              cv[g] = ((alive >> g) & 1u) && i < d ? elem<FMT>(A.C + (int64_t)jg[g] * d * esz, i) : xv;
+            const bool inside = D0 + 64 * (m + 1) < d;  // a checkpoint inside the row
+#pragma unroll
+            for (int g = 0; g < kGroup; ++g) {
+              if ((alive >> g) & 1u) {
+                const Val<FMT> t = xv - cv[g];
+                acc[g] += wave_sum(t * t);
+                if (inside && (float)acc[g] > tauf * A.rt[m]) alive &= ~(1u << g);
+              }
+            }
+          }
+        }
+#pragma unroll
+        for (int g = 0; g < kGroup; ++g) {
+          if ((alive >> g) & 1u) {  // compared on the full distance, in ascending index
+            ++full;
+            if (acc[g] < bd || (acc[g] == bd && jg[g] < best)) {
+              bd = acc[g];
+              best = jg[g];
+            }
+          }
         }
       }
     }
+    if (lane == 0) {
+      A.assign[p] = best;
+      A.dist[p] = (double)bd;
+    }
   }
-  if (lane == 0) {
-    A.assign[p] = best;
-    A.dist[p] = (double)bd;
-    if (A.cnt) atomicAdd(A.cnt + 2, full);
-  }
+  if (A.cnt && lane == 0) A.cnt[wid] = full;
 }
 
 __global__ __launch_bounds__(256) void skm_zero_kernel(unsigned long long *c) {
   if (threadIdx.x < 3) c[threadIdx.x] = 0ull;
+}
+
+// adds the partial counts of one pass to the running totals (one block, fixed order)
+__global__ __launch_bounds__(256) void skm_count_kernel(const unsigned long long *front, int64_t nfront,
+                                                        const unsigned long long *refine, int64_t nrefine,
+                                                        unsigned long long *cnt) {
+  __shared__ unsigned long long sh[3][256];
+  unsigned long long a = 0, b = 0, c = 0;
+  for (int64_t i = threadIdx.x; i < nfront; i += 256) {
+    a += front[2 * i];
+    b += front[2 * i + 1];
+  }
+  for (int64_t i = threadIdx.x; i < nrefine; i += 256) c += refine[i];
+  sh[0][threadIdx.x] = a;
+  sh[1][threadIdx.x] = b;
+  sh[2][threadIdx.x] = c;
+  __syncthreads();
+  for (int st = 128; st > 0; st >>= 1) {
+    if (threadIdx.x < st)
+      for (int q = 0; q < 3; ++q) sh[q][threadIdx.x] += sh[q][threadIdx.x + st];
+    __syncthreads();
+  }
+  if (threadIdx.x < 3) cnt[threadIdx.x] += sh[threadIdx.x][0];
 }
 
 // fixed-order sum of doubles: per-block partials, then one block
@@ -376,6 +451,9 @@ __global__ __launch_bounds__(256) void skm_final_kernel(const double *part, int 
 }
 
 constexpr int kSumBlocks = 1024;
+constexpr int kRefineBlocks = 4096;  // 16384 waves striding over the points
+
+int64_t front_blocks(int64_t n, int k) { return cdiv(cdiv(n, kFT), 8) * 8 * cdiv(k, kFT); }
 
 size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
 
@@ -390,9 +468,9 @@ int prune_front_default(int d) { return std::min(d, 32 * ((d + 255) / 256)); }
 
 size_t pruned_bytes(const Points &P, int k) {
   const size_t n = (size_t)P.n;
-  const size_t W = (size_t)cdiv(k, 32);
-  return al256(4 * n) + al256(4 * n) + al256(4 * (size_t)k) + al256(4 * W * n) + al256(8 * n) +
-         al256(8 * kSumBlocks);
+  const size_t W4 = 4 * (size_t)cdiv(k, kFT);
+  return al256(4 * n) + al256(4 * n) + al256(4 * (size_t)k) + al256(4 * W4 * n) + al256(8 * n) +
+         al256(8 * kSumBlocks) + al256(16 * (size_t)front_blocks(P.n, k)) + al256(8 * 4 * (size_t)kRefineBlocks);
 }
 
 km_status launch_assign_pruned(const Points &P, const void *C, int k, const int32_t *prev, int32_t *assign,
@@ -400,7 +478,7 @@ km_status launch_assign_pruned(const Points &P, const void *C, int k, const int3
                                unsigned long long *cnt, void *ws, hipStream_t s) {
   const int64_t n = P.n;
   const int d = P.d;
-  const int W = (int)cdiv(k, 32);
+  const int W4 = 4 * (int)cdiv(k, kFT);
   uint8_t *w = static_cast<uint8_t *>(ws);
   void *tau = w;
   w += al256(4 * (size_t)n);
@@ -409,10 +487,14 @@ km_status launch_assign_pruned(const Points &P, const void *C, int k, const int3
   void *cn = w;
   w += al256(4 * (size_t)k);
   uint32_t *mask = reinterpret_cast<uint32_t *>(w);
-  w += al256(4 * (size_t)W * (size_t)n);
+  w += al256(4 * (size_t)W4 * (size_t)n);
   double *dscratch = reinterpret_cast<double *>(w);
   w += al256(8 * (size_t)n);
   double *part = reinterpret_cast<double *>(w);
+  w += al256(8 * kSumBlocks);
+  unsigned long long *cfront = reinterpret_cast<unsigned long long *>(w);
+  w += al256(16 * (size_t)front_blocks(n, k));
+  unsigned long long *crefine = reinterpret_cast<unsigned long long *>(w);
 
   SkmArgs A{};
   A.n = n;
@@ -426,7 +508,7 @@ km_status launch_assign_pruned(const Points &P, const void *C, int k, const int3
   A.xn = xn;
   A.cn = cn;
   A.D0 = D0;
-  A.W = W;
+  A.W4 = W4;
   A.mask = mask;
   A.front_test = D0 < d;
   A.r0 = (float)prune_factor(D0, d, eps0);
@@ -436,29 +518,37 @@ km_status launch_assign_pruned(const Points &P, const void *C, int k, const int3
   }
   A.assign = assign;
   A.dist = dist ? dist : dscratch;
-  A.cnt = cnt;
+  A.cnt = nullptr;
 
   const dim3 rows_grid((unsigned)cdiv(n, 4));
-  const int64_t npt = cdiv(n, kFT);
-  const dim3 front_grid((unsigned)(cdiv(npt, 8) * 8 * cdiv(k, kFT)));
+  const int64_t nfb = front_blocks(n, k);
+  const dim3 front_grid((unsigned)nfb);
+  const unsigned nrb = (unsigned)std::min<int64_t>(kRefineBlocks, cdiv(n, 4));
+  const dim3 refine_grid(nrb);
+  SkmArgs Af = A, Ar = A;  // counts go to per-group / per-wave partials
+  if (cnt) {
+    Af.cnt = cfront;
+    Ar.cnt = crefine;
+  }
   const size_t cld = P.fmt == KM_F32 ? 4 * (size_t)d : (size_t)d;
   if (P.fmt == KM_F32) {
     hipLaunchKernelGGL(skm_norm_kernel<KM_F32>, rows_grid, dim3(256), 0, s, A.X, A.xld, n, D0, xn);
     hipLaunchKernelGGL(skm_norm_kernel<KM_F32>, dim3((unsigned)cdiv(k, 4)), dim3(256), 0, s, A.C, (int64_t)cld,
                        (int64_t)k, D0, cn);
     hipLaunchKernelGGL(skm_tau_kernel<KM_F32>, rows_grid, dim3(256), 0, s, A, tau);
-    hipLaunchKernelGGL(skm_front_kernel<KM_F32>, front_grid, dim3(256), 0, s, A);
-    hipLaunchKernelGGL(skm_refine_kernel<KM_F32>, rows_grid, dim3(256), 0, s, A);
+    hipLaunchKernelGGL(skm_front_kernel<KM_F32>, front_grid, dim3(256), 0, s, Af);
+    hipLaunchKernelGGL(skm_refine_kernel<KM_F32>, refine_grid, dim3(256), 0, s, Ar);
   } else if (P.fmt == KM_SQ8) {
     hipLaunchKernelGGL(skm_norm_kernel<KM_SQ8>, rows_grid, dim3(256), 0, s, A.X, A.xld, n, D0, xn);
     hipLaunchKernelGGL(skm_norm_kernel<KM_SQ8>, dim3((unsigned)cdiv(k, 4)), dim3(256), 0, s, A.C, (int64_t)cld,
                        (int64_t)k, D0, cn);
     hipLaunchKernelGGL(skm_tau_kernel<KM_SQ8>, rows_grid, dim3(256), 0, s, A, tau);
-    hipLaunchKernelGGL(skm_front_kernel<KM_SQ8>, front_grid, dim3(256), 0, s, A);
-    hipLaunchKernelGGL(skm_refine_kernel<KM_SQ8>, rows_grid, dim3(256), 0, s, A);
+    hipLaunchKernelGGL(skm_front_kernel<KM_SQ8>, front_grid, dim3(256), 0, s, Af);
+    hipLaunchKernelGGL(skm_refine_kernel<KM_SQ8>, refine_grid, dim3(256), 0, s, Ar);
   } else {
     return KM_EUNSUPPORTED;
   }
+  if (cnt) hipLaunchKernelGGL(skm_count_kernel, dim3(1), dim3(256), 0, s, cfront, nfb, crefine, (int64_t)nrb * 4, cnt);
   KMQ_LAUNCH_CHECK("pruned assignment");
   if (objective) {
     const int nb = (int)std::min<int64_t>(kSumBlocks, std::max<int64_t>(1, cdiv(n, 256)));
