@@ -269,7 +269,7 @@ typedef struct km_prune {
  * can differ from the exact nearest centroid when the test drops it.
  *   P: KM_F32 (fp32 sums; r(D) rounded to fp32) or KM_SQ8 (exact integer distances
  *   in code space, the test on (float)p(D) > (float)tau * (float)r(D)); d <= d' + 2048,
- *   d' <= 256, d' % 4 == 0 (F32) or % 16 == 0 (SQ8).  C as in kmeans_assign.
+ *   d' <= 256, d and d' multiples of 8 (F32) or of 16 (SQ8).  C as in kmeans_assign.
  *   prev: int32[n], the previous assignment (values in [0, k)); may be the same
  *   array as assign.  dist (nullable): DEVICE double[n], the winning squared distance.
  *   objective (nullable): DEVICE double[1], sum of dist.

@@ -622,7 +622,8 @@ static km_status check_prune(const Points &p, const km_prune *pr, int *D0) {
   KMQ_CHECK(pr->reserved == 0, KM_EINVAL, "reserved field must be 0");
   KMQ_CHECK(pr->eps0 > 0.0, KM_EINVAL, "eps0 must be > 0");
   const int d0 = pr->d_front ? pr->d_front : prune_front_default(p.d);
-  const int g = p.fmt == KM_F32 ? 4 : 16;
+  const int g = p.fmt == KM_F32 ? 8 : 16;  // the refinement reads 8 dims per lane
+  KMQ_CHECK(p.d % g == 0, KM_EUNSUPPORTED, "pruning needs d %% %d == 0 (d = %d)", g, p.d);
   KMQ_CHECK(d0 >= 1 && d0 <= p.d && d0 % g == 0, KM_EINVAL,
             "d_front = %d must lie in [1, d] and be a multiple of %d", d0, g);
   KMQ_CHECK(d0 <= 256 && p.d - d0 <= 2048, KM_EUNSUPPORTED,

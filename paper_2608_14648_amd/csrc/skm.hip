@@ -132,30 +132,37 @@ __global__ __launch_bounds__(256) void skm_tau_kernel(SkmArgs A, void *tau) {
 }
 
 // ---- front: all pairs over d' dims on the matrix cores, the test at d' -------
+// One workgroup per 128-point tile walks every 128-centroid tile: the (tile,
+// chunk) steps form one pipeline (the next step's rows are loaded into registers
+// while the current one runs on the matrix cores), and after a tile's last chunk
+// its survivor bits are written, 16 bytes per point.
 template <int FMT>
-__global__ __launch_bounds__(256) void skm_front_kernel(SkmArgs A) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void skm_front_kernel(SkmArgs A) {
   __shared__ __align__(16) uint8_t lds[2][2][kFTile];  // [buffer][centroids, points]
-  __shared__ Val<FMT> cnl[kFT];                       // front norms of the tile's centroids
+  __shared__ Val<FMT> cnl[2][kFT];                    // front norms of a tile's centroids (by tile parity)
   __shared__ __align__(16) uint32_t mrow[kFT][4];     // the tile's 4 mask words of each point
   constexpr bool F = FMT == KM_F32;
   constexpr int esz = F ? 4 : 1;
   using Acc = typename std::conditional<F, f32x16, i32x16>::type;
   const int t = threadIdx.x, lane = t & 63, w = t >> 6, r = lane & 31, h = lane >> 5;
   const int wc = w & 1, wp = w >> 1;
-  // the centroid tiles of one point tile run on one XCD (ids are dealt round-robin)
-  const int64_t npt = cdiv(A.n, kFT);
+  const int64_t p0 = (int64_t)blockIdx.x * kFT;
   const int nct = (int)cdiv(A.k, kFT);
-  const int64_t id = blockIdx.x;
-  const int64_t pt = ((id >> 3) / nct) * 8 + (id & 7);
-  const int ct = (int)((id >> 3) % nct);
-  if (pt >= npt) {
-    if (A.cnt && t == 0) A.cnt[2 * id] = A.cnt[2 * id + 1] = 0ull;
-    return;
-  }
-  const int64_t p0 = pt * kFT;
-  const int c0 = ct * kFT;
   const int bytes = A.D0 * esz;
   const int nch = (bytes + kFRow - 1) / kFRow;
+  const int total = nct * nch;
+
+  // this lane's two points: previous centroid, front norm, threshold tau r(d')
+  int pj[2];
+  Val<FMT> xn[2];
+  float lim[2];
+#pragma unroll
+  for (int pb = 0; pb < 2; ++pb) {
+    const int64_t pc = min<int64_t>(p0 + wp * 64 + pb * 32 + r, A.n - 1);
+    pj[pb] = A.prev[pc];
+    xn[pb] = static_cast<const Val<FMT> *>(A.xn)[pc];
+    lim[pb] = (F ? static_cast<const float *>(A.tau)[pc] : (float)static_cast<const int *>(A.tau)[pc]) * A.r0;
+  }
 
   Acc acc[2][2];
 #pragma unroll
@@ -166,7 +173,9 @@ __global__ __launch_bounds__(256) void skm_front_kernel(SkmArgs A) {
       for (int v = 0; v < 16; ++v) acc[cb][pb][v] = 0;
 
   uint4 rc[4], rp[4];
-  auto load = [&](int ch) {
+  Val<FMT> cnv = 0;
+  auto load = [&](int ct, int ch) {
+    const int c0 = ct * kFT;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int idx = t + 256 * i;
@@ -178,8 +187,9 @@ __global__ __launch_bounds__(256) void skm_front_kernel(SkmArgs A) {
       rc[i] = ok ? *reinterpret_cast<const uint4 *>(A.C + crow * A.d * esz + b) : make_uint4(0, 0, 0, 0);
       rp[i] = ok ? *reinterpret_cast<const uint4 *>(A.X + prow * A.xld + b) : make_uint4(0, 0, 0, 0);
     }
+    if (ch == 0 && t < kFT) cnv = static_cast<const Val<FMT> *>(A.cn)[min(c0 + t, A.k - 1)];
   };
-  auto store = [&](int ch, int buf) {
+  auto store = [&](int ct, int ch, int buf) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int idx = t + 256 * i;
@@ -194,15 +204,19 @@ __global__ __launch_bounds__(256) void skm_front_kernel(SkmArgs A) {
       *reinterpret_cast<uint4 *>(&lds[buf][0][row * kFStride + 16 * col]) = vc;
       *reinterpret_cast<uint4 *>(&lds[buf][1][row * kFStride + 16 * col]) = vp;
     }
+    if (ch == 0 && t < kFT) cnl[ct & 1][t] = cnv;
   };
 
-  if (t < kFT) cnl[t] = static_cast<const Val<FMT> *>(A.cn)[min(c0 + t, A.k - 1)];
-  load(0);
-  store(0, 0);
+  unsigned tested = 0, passed = 0;  // per lane; at most 64 per tile
+  load(0, 0);
+  store(0, 0, 0);
   __syncthreads();
-  for (int ch = 0; ch < nch; ++ch) {
-    const int buf = ch & 1;
-    if (ch + 1 < nch) load(ch + 1);
+  for (int q = 0; q < total; ++q) {
+    const int ct = q / nch, ch = q - ct * nch;
+    const int buf = q & 1;
+    const bool has_next = q + 1 < total;
+    const int ct_n = ch + 1 == nch ? ct + 1 : ct, ch_n = ch + 1 == nch ? 0 : ch + 1;
+    if (has_next) load(ct_n, ch_n);
     const uint8_t *cbuf = lds[buf][0];
     const uint8_t *pbuf = lds[buf][1];
 #pragma unroll
@@ -231,85 +245,123 @@ __global__ __launch_bounds__(256) void skm_front_kernel(SkmArgs A) {
           }
         }
     }
-    if (ch + 1 < nch) store(ch + 1, buf ^ 1);
+    if (has_next) store(ct_n, ch_n, buf ^ 1);
     __syncthreads();
-  }
-
-  // epilogue: lane (r, h) holds centroid rows 8 (v >> 2) + 4 h + (v & 3) of each
-  // 32 x 32 block for point column r
-  unsigned long long tested = 0, passed = 0;
+    if (ch + 1 < nch) continue;
+    // epilogue of tile ct: lane (r, h) holds centroid rows 8 (v >> 2) + 4 h + (v & 3)
+    // of each 32 x 32 block for point column r; the threshold test per pair, the
+    // validity (j < k, j != previous centroid, point in range) per 32-bit word
+    const int c0 = ct * kFT;
+    const Val<FMT> *cnt_ = cnl[ct & 1];
 #pragma unroll
-  for (int pb = 0; pb < 2; ++pb) {
-    const int64_t p = p0 + wp * 64 + pb * 32 + r;
-    const int64_t pc = min<int64_t>(p, A.n - 1);
-    const int pj = A.prev[pc];
-    const Val<FMT> xn = static_cast<const Val<FMT> *>(A.xn)[pc];
-    const float lim = (F ? static_cast<const float *>(A.tau)[pc] : (float)static_cast<const int *>(A.tau)[pc]) * A.r0;
+    for (int pb = 0; pb < 2; ++pb) {
+      const int64_t p = p0 + wp * 64 + pb * 32 + r;
 #pragma unroll
-    for (int cb = 0; cb < 2; ++cb) {
-      const int jb = c0 + wc * 64 + cb * 32;  // first centroid of the block (multiple of 32)
-      uint32_t m = 0;
+      for (int cb = 0; cb < 2; ++cb) {
+        const int jb = c0 + wc * 64 + cb * 32;  // first centroid of the block (multiple of 32)
+        uint32_t m = 0;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int off = 8 * (v >> 2) + 4 * h + (v & 3);
-        const int j = jb + off;
-        const bool cand = p < A.n && j < A.k && j != pj;
-        bool keep = true;
-        if (A.front_test) {
-          const Val<FMT> cnj = cnl[wc * 64 + cb * 32 + off];
+        for (int v = 0; v < 16; ++v) {
+          const int off = 8 * (v >> 2) + 4 * h + (v & 3);
+          const Val<FMT> cnj = cnt_[wc * 64 + cb * 32 + off];
+          bool keep;
           if constexpr (F) {
-            const float pd = fmaf(-2.0f, acc[cb][pb][v], xn + cnj);
-            keep = !(pd > lim);
+            const float pd = fmaf(-2.0f, acc[cb][pb][v], xn[pb] + cnj);
+            keep = !(pd > lim[pb]);
           } else {
-            const int pd = xn + cnj - 2 * acc[cb][pb][v];
-            keep = !((float)pd > lim);
+            const int pd = xn[pb] + cnj - 2 * acc[cb][pb][v];
+            keep = !((float)pd > lim[pb]);
+          }
+          m |= keep ? (1u << off) : 0u;
+          acc[cb][pb][v] = 0;
+        }
+        m |= __shfl_xor(m, 32);
+        const int nvalid = A.k - jb;
+        uint32_t valid = (p < A.n && nvalid > 0) ? (nvalid >= 32 ? 0xFFFFFFFFu : (1u << nvalid) - 1u) : 0u;
+        const int rel = pj[pb] - jb;
+        if (rel >= 0 && rel < 32) valid &= ~(1u << rel);
+        m = A.front_test ? (m & valid) : valid;
+        if (h == 0) {
+          mrow[wp * 64 + pb * 32 + r][wc * 2 + cb] = m;
+          if (A.front_test) {
+            tested += (unsigned)__popc(valid);
+            passed += (unsigned)__popc(m);
           }
         }
-        const bool bit = cand && keep;
-        m |= (bit ? 1u : 0u) << off;
-        tested += A.front_test && cand;
-        passed += A.front_test && bit;
       }
-      m |= __shfl_xor(m, 32);
-      if (h == 0) mrow[wp * 64 + pb * 32 + r][wc * 2 + cb] = m;
     }
+    __syncthreads();
+    if (t < kFT && p0 + t < A.n)  // words 4 ct .. 4 ct + 3 of the point's row (rows padded to W4 words)
+      *reinterpret_cast<uint4 *>(A.mask + (p0 + t) * A.W4 + 4 * ct) = *reinterpret_cast<const uint4 *>(mrow[t]);
   }
-  __syncthreads();
-  if (t < kFT && p0 + t < A.n)  // words 4 ct .. 4 ct + 3 of the point's row (rows padded to W4 words)
-    *reinterpret_cast<uint4 *>(A.mask + (p0 + t) * A.W4 + 4 * ct) = *reinterpret_cast<const uint4 *>(mrow[t]);
   if (A.cnt) {  // per-workgroup partial counts (summed later in a fixed order)
     __shared__ unsigned long long cw[4][2];
-    tested = wave_sum(tested);
-    passed = wave_sum(passed);
+    const unsigned long long tw = wave_sum((unsigned long long)tested);
+    const unsigned long long pw = wave_sum((unsigned long long)passed);
     if (lane == 0) {
-      cw[w][0] = tested;
-      cw[w][1] = passed;
+      cw[w][0] = tw;
+      cw[w][1] = pw;
     }
     __syncthreads();
     if (t == 0) {
-      A.cnt[2 * id] = cw[0][0] + cw[1][0] + cw[2][0] + cw[3][0];
-      A.cnt[2 * id + 1] = cw[0][1] + cw[1][1] + cw[2][1] + cw[3][1];
+      A.cnt[2 * blockIdx.x] = cw[0][0] + cw[1][0] + cw[2][0] + cw[3][0];
+      A.cnt[2 * blockIdx.x + 1] = cw[0][1] + cw[1][1] + cw[2][1] + cw[3][1];
     }
   }
 }
 
 // ---- refinement of the survivors: one wave per point ---------------------------
 // The point's mask row is read first; a point without survivors keeps its previous
-// centroid without touching its row.  Survivors are taken in groups of kGroup
-// (ascending index): chunk by chunk, the group's loads and reductions are
-// independent of each other, and every survivor stops at its first failed
-// checkpoint.
+// centroid without touching its row.  Survivors are taken in groups of 8
+// (ascending index), one survivor per 8 lanes: in each 64-dim chunk a lane sums
+// 8 consecutive dims, the 8 lanes of a survivor add their sums, and every
+// survivor stops at its first failed checkpoint.
 constexpr int kGroup = 8;
 
 template <int FMT>
+__device__ __forceinline__ Val<FMT> sq8dims(const uint8_t *x, const uint8_t *c, int i, int lim) {
+  // sum over the 8 dims [i, i + 8) below lim of (x - c)^2; i and lim are multiples of 8
+  Val<FMT> s = 0;
+  if (i < lim) {
+    if constexpr (FMT == KM_F32) {
+      const f32x4 x0 = *reinterpret_cast<const f32x4 *>(x + 4 * i), x1 = *reinterpret_cast<const f32x4 *>(x + 4 * i + 16);
+      const f32x4 c0 = *reinterpret_cast<const f32x4 *>(c + 4 * i), c1 = *reinterpret_cast<const f32x4 *>(c + 4 * i + 16);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float t0 = x0[e] - c0[e], t1 = x1[e] - c1[e];
+        s += t0 * t0;
+        s += t1 * t1;
+      }
+    } else {
+      const uint2 xv = *reinterpret_cast<const uint2 *>(x + i), cv = *reinterpret_cast<const uint2 *>(c + i);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t xw = e < 4 ? xv.x : xv.y, cw = e < 4 ? cv.x : cv.y;
+        const int t = (int)((xw >> (8 * (e & 3))) & 255u) - (int)((cw >> (8 * (e & 3))) & 255u);
+        s += t * t;
+      }
+    }
+  }
+  return s;
+}
+
+// sum over the 8 lanes of a survivor; every lane of the group gets the first lane's result
+template <typename T>
+__device__ __forceinline__ T group8_sum(T v, int lane) {
+  v += __shfl_xor(v, 4);
+  v += __shfl_xor(v, 2);
+  v += __shfl_xor(v, 1);
+  return __shfl(v, lane & ~7);
+}
+
+template <int FMT>
 __global__ __launch_bounds__(256) void skm_refine_kernel(SkmArgs A) {
-  constexpr bool F = FMT == KM_F32;
-  constexpr int esz = F ? 4 : 1;
+  constexpr int esz = FMT == KM_F32 ? 4 : 1;
   const int lane = threadIdx.x & 63;
+  const int gl = lane >> 3, u = lane & 7;  // survivor slot, sub-lane
   const int64_t wid = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int64_t nw = (int64_t)gridDim.x * 4;
   const int d = A.d, D0 = A.D0;
-  const int nf = (D0 + 63) >> 6, nt = (d - D0 + 63) >> 6;
   unsigned long long full = 0;
   for (int64_t p = wid; p < A.n; p += nw) {  // waves stride over the points
     const int pj = min(max(A.prev[p], 0), A.k - 1);
@@ -325,12 +377,10 @@ __global__ __launch_bounds__(256) void skm_refine_kernel(SkmArgs A) {
       uint32_t bits = 0u;
       int wbase = 0;
       while (nz || bits) {
-        // the next group of survivors, in ascending index
-        int jg[kGroup];
-        int ng = 0;
+        // the next group of survivors, in ascending index; slot gl of this lane
+        int jl = 0, ng = 0;
 #pragma unroll
         for (int g = 0; g < kGroup; ++g) {
-          jg[g] = 0;
           if (!bits && nz) {
             const int wl = __ffsll((unsigned long long)nz) - 1;
             nz &= nz - 1;
@@ -338,60 +388,33 @@ __global__ __launch_bounds__(256) void skm_refine_kernel(SkmArgs A) {
             wbase = (w0 + wl) * 32;
           }
           if (bits) {
-            jg[g] = wbase + __ffs(bits) - 1;
+            const int j = wbase + __ffs(bits) - 1;
             bits &= bits - 1;
+            if (g == gl) jl = j;
             ng = g + 1;
           }
         }
-        Val<FMT> acc[kGroup];
-        uint32_t alive = (1u << ng) - 1u;
-#pragma unroll
-        for (int g = 0; g < kGroup; ++g) acc[g] = 0;
-#pragma unroll
-        for (int m = 0; m < kMaxFront; ++m) {
-          if (m < nf) {
-            const int i = 64 * m + lane;
-            const Val<FMT> xv = i < D0 ? elem<FMT>(x, i) : (Val<FMT>)0;
-            Val<FMT> cv[kGroup];
-#pragma unroll
-            for (int g = 0; g < kGroup; ++g)
-              cv[g] = (g < ng && i < D0) ? elem<FMT>(A.C + (int64_t)jg[g] * d * esz, i) : xv;
-#pragma unroll
-            for (int g = 0; g < kGroup; ++g) {
-              if (g < ng) {
-                const Val<FMT> t = xv - cv[g];
-                acc[g] += wave_sum(t * t);
-              }
-            }
-          }
+        const bool mine = gl < ng;
+        const uint8_t *c = A.C + (int64_t)jl * d * esz;
+        Val<FMT> acc = 0;
+        for (int b = 0; b < D0; b += 64) acc += group8_sum(mine ? sq8dims<FMT>(x, c, b + 8 * u, D0) : (Val<FMT>)0, lane);
+        bool alive = mine;
+        for (int m = 0, b = D0; b < d; ++m, b += 64) {
+          if (!__ballot(alive)) break;
+          acc += group8_sum(alive ? sq8dims<FMT>(x, c, b + 8 * u, d) : (Val<FMT>)0, lane);
+          if (b + 64 < d && alive && (float)acc > tauf * A.rt[m]) alive = false;  // checkpoint inside the row
         }
-#pragma unroll
-        for (int m = 0; m < kMaxTail; ++m) {
-          if (m < nt && alive) {
-            const int i = D0 + 64 * m + lane;
-            const Val<FMT> xv = i < d ? elem<FMT>(x, i) : (Val<FMT>)0;
-            Val<FMT> cv[kGroup];
-#pragma unroll
-            for (int g = 0; g < kGroup; ++g)
-              cv[g] = ((alive >> g) & 1u) && i < d ? elem<FMT>(A.C + (int64_t)jg[g] * d * esz, i) : xv;
-            const bool inside = D0 + 64 * (m + 1) < d;  // a checkpoint inside the row
-#pragma unroll
-            for (int g = 0; g < kGroup; ++g) {
-              if ((alive >> g) & 1u) {
-                const Val<FMT> t = xv - cv[g];
-                acc[g] += wave_sum(t * t);
-                if (inside && (float)acc[g] > tauf * A.rt[m]) alive &= ~(1u << g);
-              }
-            }
-          }
-        }
+        // survivors reaching the full distance, compared in ascending index
+        const uint64_t am = __ballot(alive && u == 0);
 #pragma unroll
         for (int g = 0; g < kGroup; ++g) {
-          if ((alive >> g) & 1u) {  // compared on the full distance, in ascending index
+          if ((am >> (8 * g)) & 1ull) {
+            const Val<FMT> v = __shfl(acc, 8 * g);
+            const int j = __shfl(jl, 8 * g);
             ++full;
-            if (acc[g] < bd || (acc[g] == bd && jg[g] < best)) {
-              bd = acc[g];
-              best = jg[g];
+            if (v < bd || (v == bd && j < best)) {
+              bd = v;
+              best = j;
             }
           }
         }
@@ -453,7 +476,10 @@ __global__ __launch_bounds__(256) void skm_final_kernel(const double *part, int 
 constexpr int kSumBlocks = 1024;
 constexpr int kRefineBlocks = 4096;  // 16384 waves striding over the points
 
-int64_t front_blocks(int64_t n, int k) { return cdiv(cdiv(n, kFT), 8) * 8 * cdiv(k, kFT); }
+int64_t front_blocks(int64_t n, int k) {
+  (void)k;
+  return cdiv(n, kFT);
+}
 
 size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
 

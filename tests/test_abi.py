@@ -257,6 +257,7 @@ def test_pruned_argument_checks(kmq):
         assert L.kmeans_assign_pruned(*args) == code, msg
         assert msg in L.km_last_error().decode()
     for params, code, msg in [((0.0, 0, 0), -1, "eps0"), ((2.1, 0, 1), -1, "reserved"), ((2.1, 6, 0), -1, "d_front"),
+                              ((2.1, 36, 0), -1, "d_front"),
                               ((2.1, 512, 0), -2, "d_front"), ((2.1, 800, 0), -1, "d_front")]:
         pr2 = kmq.KmPrune(*params)
         args = list(ok)
@@ -271,6 +272,11 @@ def test_pruned_argument_checks(kmq):
     Pw = _pts(kmq, d=4096, ld=4096)
     args = list(ok)
     args[0] = ct.byref(Pw)
+    assert L.kmeans_assign_pruned(*args) == -2
+    # fp32 rows must hold whole groups of 8 dims
+    P8 = _pts(kmq, d=132, ld=132)
+    args = list(ok)
+    args[0] = ct.byref(P8)
     assert L.kmeans_assign_pruned(*args) == -2
     # SQ8: d' must be a multiple of 16
     Ps = _pts(kmq, fmt=2, d=256, ld=256)

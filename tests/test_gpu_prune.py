@@ -134,21 +134,21 @@ def check_f32_against_oracle(X, C, prev, a, a_o, eps0, D0, label):
     return len(mis)
 
 
-F32_SHAPES = [(1, 32, 1), (5, 64, 3), (300, 96, 17), (1000, 128, 64), (2049, 256, 130), (517, 768, 257),
-              (700, 1024, 300), (300, 2048, 40)]
+F32_SHAPES = [(1, 32, 1, 0), (5, 64, 3, 0), (300, 96, 17, 0), (1000, 128, 64, 0), (2049, 256, 130, 0),
+              (517, 768, 257, 0), (517, 768, 257, 40), (700, 1024, 300, 0), (300, 2048, 40, 0), (400, 136, 50, 8)]
 
 
-@pytest.mark.parametrize("n,d,k", F32_SHAPES)
-def test_assign_pruned_f32(km, torch, n, d, k):
-    say(f"pruned f32 n={n} d={d} k={k}")
+@pytest.mark.parametrize("n,d,k,d_front", F32_SHAPES)
+def test_assign_pruned_f32(km, torch, n, d, k, d_front):
+    say(f"pruned f32 n={n} d={d} k={k} d_front={d_front}")
     X = rotated_blobs(n, d, max(2, k // 2), seed=n + d + k + 1)
     rng = np.random.default_rng(n + k + 1)
     C = (X[rng.integers(0, n, k)] + 0.05 * rng.standard_normal((k, d))).astype(np.float32)
     prev = rng.integers(0, k, n).astype(np.int32)
-    D0 = orc.prune_front_dims(d)
-    a_o, dist_o, cnt_o = orc.assign_pruned({"fmt": "f32", "X": X}, C, prev, 2.1)
+    D0 = d_front or orc.prune_front_dims(d)
+    a_o, dist_o, cnt_o = orc.assign_pruned({"fmt": "f32", "X": X}, C, prev, 2.1, d_front)
     a, dist, obj, cnt = km.kmeans_assign_pruned(km.points_f32(to_dev(X, torch)), to_dev(C, torch),
-                                                to_dev(prev, torch), 2.1, objective=True, counters=True)
+                                                to_dev(prev, torch), 2.1, d_front, objective=True, counters=True)
     torch.cuda.synchronize()
     a, dist = host(a), host(dist)
     nmis = check_f32_against_oracle(X, C, prev, a, a_o, 2.1, D0, f"n={n} d={d} k={k}")
