@@ -4,9 +4,10 @@
 //               (LDS-privatised histogram), stored cluster-major [k][nblk].
 //   2. scan     exclusive scan of that table: entry (j, b) is where block b's
 //               first member of cluster j goes in the cluster-sorted order.
-//   3. scatter  stable counting sort: points are ranked inside each wave by a
-//               match loop over equal cluster ids and the four waves take
-//               their slots in order, so members stay in point order.
+//   3. scatter  stable counting sort: points are ranked inside each wave among
+//               the lanes with the same cluster id (found with one ballot per
+//               id bit) and the four waves take their slots in order, so
+//               members stay in point order.
 //   4. segsum   fixed-size chunks (<= 512 members, never crossing a cluster)
 //               are summed by one workgroup per (chunk, column slice): each
 //               wave adds every 4th member's slice of the row (coalesced
@@ -212,24 +213,24 @@ __global__ __launch_bounds__(256) void scatter_kernel(const int32_t *assign, int
     __syncthreads();
   }
   const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  const int nbits = k > 1 ? 32 - __clz(k - 1) : 0;  // bits of a cluster id
   for (int64_t base = lo; base < hi; base += 256) {
     const int64_t p = base + t;
     int a = p < hi ? assign[p] : -1;
     const bool valid = a >= 0 && a < k;
-    // rank among equal ids in this wave (lanes below), group size, group leader
+    // lanes holding the same id: one ballot per id bit; then the rank among them
+    // (lanes below), their number and their first lane
+    uint64_t peers = __ballot(valid);
+    for (int ib = 0; ib < nbits; ++ib) {
+      const bool bit = (a >> ib) & 1;
+      const uint64_t ones = __ballot(valid && bit);
+      peers &= bit ? ones : ~ones;
+    }
     int rank = 0, cnt = 0, leader = 0;
-    uint64_t todo = __ballot(valid);
-    while (todo) {
-      const int ld = __ffsll((unsigned long long)todo) - 1;
-      const int v = __shfl(a, ld);
-      const bool mine = valid && a == v;
-      const uint64_t m = __ballot(mine);
-      if (mine) {
-        rank = __popcll(m & lt_mask);
-        cnt = __popcll(m);
-        leader = ld;
-      }
-      todo &= ~m;
+    if (valid) {
+      rank = __popcll(peers & lt_mask);
+      cnt = __popcll(peers);
+      leader = __ffsll((unsigned long long)peers) - 1;
     }
     for (int w = 0; w < 4; ++w) {
       __syncthreads();
