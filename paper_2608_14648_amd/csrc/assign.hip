@@ -940,88 +940,154 @@ __global__ __launch_bounds__(k8Threads, 1) void assign_i8_kernel(AssignArgs A) {
 }
 
 // ---- 1-bit assignment with the points' bits resident in LDS ----------------------
-// A workgroup (8 waves) owns 512 points.  Their code words are loaded once and kept
-// in LDS transposed, word-major ([word][point]), so the 32 lanes of a wave that
-// read the same word of 32 consecutive points hit 32 consecutive banks.  At each
-// MFMA the lane widens its 16 bits (one half-word) to 16 {0,1} bytes in
-// registers.  The centroids' int8 residual codes stream through LDS in stages of
-// 128 centroids x 128 bytes; every wave multiplies its 64 points by all 128
-// centroids of the tile (4 x 2 blocks of 32 x 32 x 32), so no cross-wave merge is
-// needed and the workgroup sweeps the centroids once per 512 points.
-constexpr int kBT = 512;            // threads (8 waves)
-constexpr int kBTP = 512;           // points per workgroup
-constexpr int kBTC = 128;           // centroids per tile
-constexpr int kBMaxWords = 40;      // d - d0 <= 1280 dims for the resident codes
-constexpr int kBStageBytes = kBTC * kLdsStride;
+// A workgroup of NW waves owns 64 NW points.  Their code words are loaded once and
+// kept in LDS transposed, word-major ([word][point]), so the 32 lanes of a wave that
+// read the same word of 32 consecutive points hit 32 consecutive banks.  At load time
+// the bits of each word are regrouped: bit 16h + 4q + j (dimension 4q + j of half h,
+// i.e. byte j of operand register q for the lanes of half h) moves to bit 8j + 4h + q.
+// Widening a half-word to 16 bytes then costs one shift and one mask per register
+// instead of an extract, a multiply and a mask.  The centroids' int8 residual codes
+// stream through LDS in stages of 128 centroids x 128 bytes, copied by direct
+// global-to-LDS loads (no register staging): each load instruction of a wave fills
+// 64 consecutive 16-byte slots, and the lane that fills slot p of row R fetches
+// chunk p ^ (R & 7) of that row, so chunk c sits in slot c ^ (R & 7) and the 8 lanes
+// of one MFMA operand read hit 8 different bank groups.  Every wave multiplies its
+// 64 points by all 128 centroids of the tile (4 x 2 blocks of 32 x 32 x 32), so no
+// cross-wave merge is needed.
+//
+// Two shapes: 4 waves and 256 points with up to 1024 resident dimensions (69 KB of
+// LDS, two workgroups per CU, so one workgroup's epilogue runs under the other's
+// MFMAs), and 8 waves and 512 points with up to 1280 dimensions (one per CU).
+constexpr int kBTC = 128;  // centroids per tile
+constexpr int kBStageBytes = kBTC * kRowBytes;
+constexpr int kBWordsSmall = 32;  // 4-wave shape: d - d0 <= 1024
+constexpr int kBWordsLarge = 40;  // 8-wave shape: d - d0 <= 1280
 
-__device__ __forceinline__ i32x4 widen16(uint32_t hb) {
-  return i32x4{(int)spread4(hb & 15u), (int)spread4((hb >> 4) & 15u), (int)spread4((hb >> 8) & 15u),
-               (int)spread4((hb >> 12) & 15u)};
+__device__ __forceinline__ uint32_t regroup_bits(uint32_t w) {
+  uint32_t o = 0;
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) o |= spread4((w >> (16 * h + 4 * q)) & 15u) << (4 * h + q);
+  return o;
 }
+
+// x: a regrouped word shifted right by 4h.  Register q takes bit 8j + q of x as
+// byte j with the value 0 or 2, so the products sum to 2D; seeded with -T the
+// accumulator ends at 2D - T.
+__device__ __forceinline__ i32x4 widen_regrouped2(uint32_t x) {
+  constexpr uint32_t M2 = 0x02020202u;
+  return i32x4{(int)((x << 1) & M2), (int)(x & M2), (int)((x >> 1) & M2), (int)((x >> 2) & M2)};
+}
+
+// Direct copy of 16 bytes per lane from global memory into LDS: the wave's 64 lanes
+// fill 1 KB at LDS byte address lds (wave-uniform) in lane order.  Written as
+// inline assembly so that the compiler, which cannot tell the destination from the
+// LDS the MFMA loop reads, does not wait for the copy before every LDS read; the
+// caller waits (vmcnt) before the barrier that publishes the data.  M0 is set and
+// used inside the statement.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void lds_copy16(const void *src, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds) : "memory", "m0");
+}
+// the same from a wave-uniform base plus a 32-bit per-lane byte offset
+__device__ __forceinline__ void lds_copy16(const void *base, uint32_t off, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "s"(lds)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
 
 // FMT: KM_SIGN1 (symmetric int8 centroid codes) or KM_RABITQ (SQ4 centroid codes
 // with bias; the epilogue also needs each point's number of set bits).
-template <int FMT>
-__global__ __launch_bounds__(kBT, 1) void assign_bits_kernel(AssignArgs A) {
-  __shared__ uint32_t bitsT[kBMaxWords * kBTP];  // 80 KB
-  __shared__ __align__(16) uint8_t cst[2][kBStageBytes];
-  __shared__ float cparl[2][4 * kBTC];
-  __shared__ int popl[kBTP];
+template <int FMT, int NW, int MAXW>
+__global__ __launch_bounds__(64 * NW, 8 / NW) void assign_bits_kernel(AssignArgs A) {
+  constexpr int NT = 64 * NW;         // threads
+  constexpr int TP = 64 * NW;         // points per workgroup
+  constexpr int CPT = kBTC * 8 / NT;  // 16-byte centroid chunks per thread and stage
+  static_assert(CPT * NT == kBTC * 8 && NT >= kBTC, "stage split");
+  static_assert(MAXW % 4 == 0, "whole stages of resident words");
+  __shared__ uint32_t bitsT[MAXW * TP];
+  // two stage buffers as separate arrays: stage it reads one while the copies of
+  // stage it + 1 fill the other, and each access names its array statically
+  __shared__ __align__(16) uint8_t cst0[kBStageBytes];
+  __shared__ __align__(16) uint8_t cst1[kBStageBytes];
+  __shared__ __align__(16) float cparl[2][4 * kBTC];
+  __shared__ int popl[TP];
   const int t = threadIdx.x;
-  const int lane = t & 63, wave = t >> 6;
+  const int lane = t & 63, wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int r = lane & 31, h = lane >> 5;
-  const int64_t p0 = (int64_t)blockIdx.x * kBTP;
+  const int64_t p0 = (int64_t)blockIdx.x * TP;
   const int W = A.di / 32;  // words of the 1-bit part
   const int S = (A.di + kRowBytes - 1) / kRowBytes;
   const int nct = (A.k + kBTC - 1) / kBTC;
   const int total = nct * S;
-  const int prmax = (int)min<int64_t>(A.n - 1 - p0, kBTP - 1);
+  const int prmax = (int)min<int64_t>(A.n - 1 - p0, TP - 1);
 
-  // resident codes: thread t loads point t's words (and counts its set bits)
+  // resident codes: thread t loads point t's words, regroups them and counts set
+  // bits; words past the last one up to the stage boundary are zero, so the chunks
+  // that a partial last stage copies from past the dimensions contribute nothing
   {
     const uint32_t *row = A.pbits + (p0 + min(t, prmax)) * A.pbw + A.pbw0;
     int pc = 0;
     for (int w = 0; w < W; ++w) {
       const uint32_t v = row[w];
-      bitsT[w * kBTP + t] = v;
+      bitsT[w * TP + t] = regroup_bits(v);
       pc += __popc(v);
     }
+    for (int w = W; w < 4 * S; ++w) bitsT[w * TP + t] = 0u;
     popl[t] = pc;
   }
   float al[2];
 #pragma unroll
   for (int pb = 0; pb < 2; ++pb) al[pb] = A.alpha[p0 + min(wave * 64 + pb * 32 + r, prmax)];
 
-  // centroid stage loads: 128 rows x 8 chunks of 16 B = 2 chunks per thread
-  uint4 cr[2];
-  float cpv[4] = {0.f, 0.f, 0.f, 0.f};
-  auto load = [&](int ct, int s) {
-    const int64_t c0 = (int64_t)ct * kBTC;
-    const int crmax = (int)min<int64_t>(A.k - 1 - c0, kBTC - 1);
-    const int8_t *cbase = A.ci8 + c0 * A.cild;
+  // centroid stage loads: 128 rows x 8 chunks of 16 B straight into LDS buffer dst.
+  // A chunk past the last dimension repeats chunk 0 of its row: the resident point
+  // words are zero there.  The tile constants hold the negated code sum and, past
+  // the last centroid, u = +inf: such a score is +inf and never wins, so the
+  // epilogue needs no bounds test.  Their loads go out before the copies, so that
+  // waiting for them never waits for the copies.  Within a full stage of a full
+  // tile a lane's source is a fixed offset (coff) from the stage's first byte.
+  uint32_t coff[CPT];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int cidx = t + kBT * i;
-      const int row = cidx >> 3, col = cidx & 7;
-      const int b = kRowBytes * s + 16 * col;
-      cr[i] = *reinterpret_cast<const uint4 *>(cbase + (uint32_t)(min(row, crmax) * (int)A.cild + (b < A.di ? b : 0)));
-    }
+  for (int i = 0; i < CPT; ++i) {
+    const int slot = (i * NW + wave) * 64 + lane;
+    const int row = slot >> 3;
+    coff[i] = (uint32_t)(row * (int)A.cild + 16 * ((slot & 7) ^ (row & 7)));
+  }
+  float cpv[4] = {0.f, 0.f, 0.f, 0.f};
+  auto load = [&](int ct, int s, uint8_t *dst) {
+    const int c0 = ct * kBTC;
+    const int crmax = min(A.k - 1 - c0, kBTC - 1);
     if (s == 0 && t < kBTC) {
-      const int64_t j = c0 + min(t, crmax);
-      cpv[0] = __int_as_float(A.cp.qsum[j]);
-      cpv[1] = A.cp.u[j];
+      const int j = c0 + min(t, crmax);
+      cpv[0] = __int_as_float(-A.cp.qsum[j]);
+      cpv[1] = t <= crmax ? A.cp.u[j] : INFINITY;
       cpv[2] = A.cp.sig2[j];
       if (FMT == KM_RABITQ) cpv[3] = A.cp.cn[j];
     }
-  };
-  auto store = [&](int ct, int s, uint8_t *buf) {
+    const int8_t *cbase = A.ci8 + (int64_t)c0 * A.cild;
+    if (crmax == kBTC - 1 && kRowBytes * (s + 1) <= A.di) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int cidx = t + kBT * i;
-      const int row = cidx >> 3, col = cidx & 7;
-      const bool ok = kRowBytes * s + 16 * col < A.di;
-      *reinterpret_cast<uint4 *>(buf + row * kLdsStride + 16 * col) = mask4(cr[i], ok);
+      for (int i = 0; i < CPT; ++i)
+        lds_copy16(cbase + kRowBytes * s, coff[i],
+                   (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t *)(dst + (i * NW + wave) * 1024));
+    } else {
+#pragma unroll
+      for (int i = 0; i < CPT; ++i) {
+        const int slot = (i * NW + wave) * 64 + lane;
+        const int row = slot >> 3;
+        const int b = kRowBytes * s + 16 * ((slot & 7) ^ (row & 7));
+        lds_copy16(cbase + (uint32_t)(min(row, crmax) * (int)A.cild + (b < A.di ? b : 0)),
+                   (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t *)(dst + (i * NW + wave) * 1024));
+      }
     }
+  };
+  // completes a load: waits for this wave's copies (the barrier that follows makes
+  // the whole stage visible) and stores the tile constants
+  auto store = [&](int ct, int s) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     if (s == 0 && t < kBTC) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) cparl[ct & 1][q * kBTC + t] = cpv[q];
@@ -1031,68 +1097,75 @@ __global__ __launch_bounds__(kBT, 1) void assign_bits_kernel(AssignArgs A) {
   float best[2] = {INFINITY, INFINITY};
   int bidx[2] = {INT_MAX, INT_MAX};
 
-  load(0, 0);
-  store(0, 0, cst[0]);
+  load(0, 0, cst0);
+  store(0, 0);
   __syncthreads();
   int pop[2] = {0, 0};
   if (FMT == KM_RABITQ) {
 #pragma unroll
     for (int pb = 0; pb < 2; ++pb) pop[pb] = popl[wave * 64 + pb * 32 + r];
   }
+  const uint32_t hsh = 4u * (uint32_t)h;
 
-  for (int ct = 0; ct < nct; ++ct) {
-    i32x16 acc[4][2];
+  i32x16 acc[4][2];
+  // one stage of MFMAs; in a tile's first stage the first products take their
+  // accumulator seed, -T of the row, from the tile constants instead of acc
+  auto mfma_stage = [&](int ct, int s, const uint8_t *buf, auto first) {
+    constexpr bool kFirst = decltype(first)::value;
+    i32x16 seed[4];
+    if constexpr (kFirst) {
+      const float *cp = cparl[ct & 1];
 #pragma unroll
-    for (int a = 0; a < 4; ++a)
+      for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
-      for (int b = 0; b < 2; ++b)
+        for (int m = 0; m < 4; ++m) {
+          const int4 v = *reinterpret_cast<const int4 *>(cp + cb * 32 + 8 * m + 4 * h);
+          seed[cb][4 * m] = v.x;
+          seed[cb][4 * m + 1] = v.y;
+          seed[cb][4 * m + 2] = v.z;
+          seed[cb][4 * m + 3] = v.w;
+        }
+    }
 #pragma unroll
-        for (int i = 0; i < 16; ++i) acc[a][b][i] = 0;
-    for (int s = 0; s < S; ++s) {
-      const int it = ct * S + s;
-      const bool has_next = it + 1 < total;
-      const int s_n = (s + 1 == S) ? 0 : s + 1;
-      const int ct_n = (s + 1 == S) ? ct + 1 : ct;
-      if (has_next) load(ct_n, s_n);
-      const uint8_t *buf = cst[it & 1];
+    for (int g = 0; g < 4; ++g) {
+      const int w = 4 * s + g;
+      i32x4 bv[2];
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int w = min(4 * s + g, W - 1);  // past the end the centroid chunk is zero
-        i32x4 bv[2];
+      for (int pb = 0; pb < 2; ++pb) bv[pb] = widen_regrouped2(bitsT[w * TP + wave * 64 + pb * 32 + r] >> hsh);
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb) {
+        const uint4 av =
+            *reinterpret_cast<const uint4 *>(buf + (cb * 32 + r) * kRowBytes + 16 * ((2 * g + h) ^ (r & 7)));
+        const i32x4 a4 = {(int)av.x, (int)av.y, (int)av.z, (int)av.w};
 #pragma unroll
         for (int pb = 0; pb < 2; ++pb) {
-          const uint32_t word = bitsT[w * kBTP + wave * 64 + pb * 32 + r];
-          bv[pb] = widen16((word >> (16 * h)) & 0xFFFFu);
-        }
-#pragma unroll
-        for (int cb = 0; cb < 4; ++cb) {
-          const uint4 av = *reinterpret_cast<const uint4 *>(buf + (cb * 32 + r) * kLdsStride + 32 * g + 16 * h);
-          const i32x4 a4 = {(int)av.x, (int)av.y, (int)av.z, (int)av.w};
-#pragma unroll
-          for (int pb = 0; pb < 2; ++pb)
+          if (kFirst && g == 0)
+            acc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a4, bv[pb], seed[cb], 0, 0, 0);
+          else
             acc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a4, bv[pb], acc[cb][pb], 0, 0, 0);
         }
       }
-      if (has_next) store(ct_n, s_n, cst[(it + 1) & 1]);
-      __syncthreads();
     }
-    // epilogue: exact integer dot 2D - T, fp32 score in the fixed order of Eq. 4
-    const int64_t c0 = (int64_t)ct * kBTC;
+  };
+
+  // epilogue: acc holds the exact integer 2D - T; fp32 score in the fixed order of
+  // Eq. 4.  Rows are visited in increasing order, so a strict < keeps the smaller
+  // index on a tie; the tile-local row (without the half's offset 4h) is a constant.
+  auto epilogue = [&](int ct) {
     const float *cp = cparl[ct & 1];
+    int loc[2] = {-1, -1};
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const int crow = cb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
-        const int64_t j = c0 + crow;
-        const bool live = j < A.k;
-        const int qs = __float_as_int(cp[crow]);
+        const int cl = cb * 32 + 8 * (i >> 2) + (i & 3);
+        const int crow = cl + 4 * h;
         const float u = cp[kBTC + crow];
         const float s2 = cp[2 * kBTC + crow];
         const float bj = cp[3 * kBTC + crow];
 #pragma unroll
         for (int pb = 0; pb < 2; ++pb) {
-          const int sd = 2 * acc[cb][pb][i] - qs;
+          const int sd = acc[cb][pb][i];
           float sc;
           if constexpr (FMT == KM_RABITQ) {  // Eq. 4-5: fp32 in the oracle's order
             const float inner = fmaf(s2, (float)sd, bj * (float)(2 * pop[pb] - A.di));
@@ -1101,16 +1174,40 @@ __global__ __launch_bounds__(kBT, 1) void assign_bits_kernel(AssignArgs A) {
             const float v = al[pb] * s2;
             sc = fmaf(-v, (float)sd, u);
           }
-          if (live && sc < best[pb]) {
+          if (sc < best[pb]) {
             best[pb] = sc;
-            bidx[pb] = (int)j;
+            loc[pb] = cl;
           }
         }
       }
-    // the next tile's steps write tile ct + 2's constants into cparl[ct & 1]; with
-    // one stage per tile no other barrier would order that after these reads.
-    // (Unconditional: a branch here splits the loop and costs register spills.)
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb)
+      if (loc[pb] >= 0) bidx[pb] = ct * kBTC + loc[pb] + 4 * h;
+  };
+
+  // stage it = ct S + s reads buffer cur while the copies of stage it + 1 fill nxt
+  auto step = [&](int it, const uint8_t *cur, uint8_t *nxt) {
+    const int ct = it / S, s = it - ct * S;
+    const bool has_next = it + 1 < total;
+    const int s_n = (s + 1 == S) ? 0 : s + 1;
+    const int ct_n = (s + 1 == S) ? ct + 1 : ct;
+    if (has_next) load(ct_n, s_n, nxt);
+    if (s == 0)
+      mfma_stage(ct, s, cur, std::true_type{});
+    else
+      mfma_stage(ct, s, cur, std::false_type{});
+    if (has_next) store(ct_n, s_n);
     __syncthreads();
+    if (s == S - 1) {
+      epilogue(ct);
+      // the next tile's steps write tile ct + 2's constants into cparl[ct & 1]; with
+      // one stage per tile no other barrier would order that after these reads
+      __syncthreads();
+    }
+  };
+  for (int it = 0; it < total; it += 2) {
+    step(it, cst0, cst1);
+    if (it + 1 < total) step(it + 1, cst1, cst0);
   }
 #pragma unroll
   for (int pb = 0; pb < 2; ++pb) {
@@ -1537,8 +1634,10 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
     A.di = P.d - d0;
   }
   if constexpr (FMT == KM_SIGN1 || FMT == KM_RABITQ) {
-    if (P.d <= 32 * kBMaxWords) {
-      hipLaunchKernelGGL(assign_bits_kernel<FMT>, dim3((unsigned)cdiv(P.n, kBTP)), dim3(kBT), 0, s, A);
+    if (P.d <= 32 * kBWordsSmall) {
+      hipLaunchKernelGGL((assign_bits_kernel<FMT, 4, kBWordsSmall>), dim3((unsigned)cdiv(P.n, 256)), dim3(256), 0, s, A);
+    } else if (P.d <= 32 * kBWordsLarge) {
+      hipLaunchKernelGGL((assign_bits_kernel<FMT, 8, kBWordsLarge>), dim3((unsigned)cdiv(P.n, 512)), dim3(512), 0, s, A);
     } else {
       hipLaunchKernelGGL(assign_i8_kernel<FMT>, dim3((unsigned)cdiv(P.n, kT8)), dim3(k8Threads), 0, s, A);
     }
