@@ -86,6 +86,12 @@ __device__ __forceinline__ unsigned long long score_key(float sc, int idx) {
   return ((unsigned long long)u << 32) | (uint32_t)idx;
 }
 
+// the same for an exact int32 score: the sign bit flipped is an order-preserving
+// unsigned image
+__device__ __forceinline__ unsigned long long int_score_key(int sc, int idx) {
+  return ((unsigned long long)((uint32_t)sc ^ 0x80000000u) << 32) | (uint32_t)idx;
+}
+
 __device__ __forceinline__ float key_score(unsigned long long key) {
   uint32_t u = (uint32_t)(key >> 32);
   u = (u & 0x80000000u) ? (u & 0x7fffffffu) : ~u;
@@ -578,13 +584,14 @@ __global__ __launch_bounds__(256) void keys_init_kernel(unsigned long long *keys
   if (p < n) keys[p] = ~0ull;
 }
 
+template <bool INT>
 __global__ __launch_bounds__(256) void keys_unpack_kernel(const unsigned long long *keys, int64_t n, int32_t *assign,
                                                           float *score, int aoff) {
   const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (p >= n) return;
   const unsigned long long key = keys[p];
   assign[p] = (int32_t)(uint32_t)key + aoff;
-  if (score) score[p] = key_score(key);
+  if (score) score[p] = INT ? (float)(int)((uint32_t)(key >> 32) ^ 0x80000000u) : key_score(key);
 }
 
 // ---- int8 / bf16 assignment with 256 x 256 workgroup tiles -------------------
@@ -866,7 +873,7 @@ __global__ __launch_bounds__(k8Threads, 1) void assign_i8_kernel(AssignArgs A) {
           for (int pb = 0; pb < k8PB; ++pb) {
             score_t sc;
             if constexpr (FMT == KM_SQ8) {
-              sc = __float_as_int(q4[e]) - 2 * acc[cb][pb][i];
+              sc = -__float_as_int(q4[e]) - 2 * acc[cb][pb][i];  // the constant is -||c~||^2
             } else if constexpr (FMT == KM_BF16) {
               sc = fmaf(-2.0f, acc[cb][pb][i], q4[e]);  // ||c||^2 - 2<x,c>
             } else if constexpr (FMT == KM_LVQ4) {  // Eq. 2 without N_x, fp32 in the oracle's order
@@ -986,6 +993,8 @@ __device__ __forceinline__ i32x4 widen_regrouped2(uint32_t x) {
 // LDS the MFMA loop reads, does not wait for the copy before every LDS read; the
 // caller waits (vmcnt) before the barrier that publishes the data.  M0 is set and
 // used inside the statement.
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
+
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void lds_copy16(const void *src, uint32_t lds) {
@@ -1225,6 +1234,278 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void assign_bits_kernel(AssignArgs
   }
 }
 
+// ---- SQ8 / bf16 assignment with direct global-to-LDS stages -------------------
+// The same 256 x 256 workgroup tile and wave split as above (8 waves: 2 centroid
+// halves x 4 point quarters, 128 centroids x 64 points each), with the operand
+// traffic moved off the vector units: every stage (256 centroid rows and 256 point
+// rows of 128 bytes) is copied straight from global memory into LDS, 16 bytes per
+// lane, with the XOR slot layout of the 1-bit kernel (chunk c of row R in slot
+// c ^ (R & 7)), so nothing passes through registers and the MFMA operand reads are
+// free of bank conflicts.  SQ8 centroid codes arrive already recentred to int8
+// (code - 128, written by the centroid preparation); the point codes are recentred
+// in registers after the LDS read (one XOR per register).  Chunks past the last
+// dimension are zero-filled by ordinary LDS stores from the lanes that skip their
+// copy.  Rows past the last centroid repeat the last centroid, codes and constant,
+// so their scores tie with it exactly and lose on the index: the epilogue is
+// branch-free and needs no bounds test.
+//
+// With ngroups > 1 the workgroup (pt, g) sweeps centroid tiles g, g + ngroups, ...
+// of point tile pt; the ngroups workgroups of a point tile are consecutive among
+// the workgroups of one XCD, so their concurrent reads of the point rows share that
+// XCD's L2, and they merge through 64-bit (score, index) keys.
+constexpr int kQT = 256;                            // centroids and points per tile
+constexpr int kQThreads = 512;                      // 8 waves
+constexpr int kQStageBytes = 2 * kQT * kRowBytes;   // 64 KB: centroid rows, then point rows
+constexpr int kQMaxDimSQ8 = 8192;                   // |2<x~,c~> - ||c~||^2| < 2^31
+
+template <int FMT>
+__global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A) {
+  constexpr bool BF = FMT == KM_BF16;
+  static_assert(FMT == KM_SQ8 || FMT == KM_BF16, "SQ8 or bf16 points");
+  // SQ8 maximises the key 2D - ||c~||^2 (= -score, exact in int32); bf16 minimises
+  // the score ||c||^2 - 2<x,c> (fp32)
+  typedef typename std::conditional<BF, float, int>::type key_t;
+  __shared__ __align__(16) uint8_t qst0[kQStageBytes];
+  __shared__ __align__(16) uint8_t qst1[kQStageBytes];
+  __shared__ __align__(16) float cparl[2][kQT];
+  const int t = threadIdx.x;
+  const int lane = t & 63, wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int r = lane & 31, h = lane >> 5;
+  const int wc = wave & 1, wp = wave >> 1;
+  const int NG = A.ngroups;
+  int64_t pt = blockIdx.x;
+  int g = 0;
+  if (NG > 1) {
+    const int64_t l = blockIdx.x >> 3;
+    pt = (l / NG) * 8 + (blockIdx.x & 7);
+    g = (int)(l % NG);
+    if (pt >= A.n_ptiles) return;  // whole workgroup, before any barrier
+  }
+  const int64_t p0 = pt * kQT;
+  const int S = (A.di + kRowBytes - 1) / kRowBytes;
+  const int nct = (A.k + kQT - 1) / kQT;
+  const int nmy = (nct - g + NG - 1) / NG;  // centroid tiles of this workgroup (>= 1: NG <= nct)
+  const int total = nmy * S;
+  const int prmax = (int)min<int64_t>(A.n - 1 - p0, kQT - 1);
+  const uint8_t *pbase = A.pi8 + p0 * A.pild;
+
+  // copy i (0..7) of a wave fills slots (8 i + wave) 64 .. + 63 of the stage: rows
+  // 0..255 are centroids, 256..511 points.  A lane's source is the stage's first
+  // byte plus a 32-bit offset: point rows are clamped into the data once, centroid
+  // rows only in a last, partial centroid tile.  In a partial last stage the lanes
+  // whose chunk lies past the dimensions store zeros instead of copying.
+  uint32_t soff[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int slot = (i * 8 + wave) * 64 + lane;
+    const int row = slot >> 3;
+    const int chunk = (slot & 7) ^ (row & 7);
+    soff[i] = i < 4 ? (uint32_t)(row * (int)A.cild + 16 * chunk)
+                    : (uint32_t)(min(row - kQT, prmax) * (int)A.pild + 16 * chunk);
+  }
+  float cpv = 0.f;
+  auto load = [&](int ct, int s, uint8_t *dst) {
+    const int c0 = (g + ct * NG) * kQT;
+    const int crmax = min(A.k - 1 - c0, kQT - 1);
+    if (s == 0 && t < kQT) {
+      const int j = c0 + min(t, crmax);
+      cpv = BF ? A.cp.cn[j] : __int_as_float(A.cp.qsum[j]);  // SQ8: -||c~||^2
+    }
+    const int8_t *cbase = A.ci8 + (int64_t)c0 * A.cild + kRowBytes * s;
+    const uint8_t *psrc = pbase + kRowBytes * s;
+    const bool full_stage = kRowBytes * (s + 1) <= A.di;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int slot = (i * 8 + wave) * 64 + lane;
+      const int row = slot >> 3;
+      const int chunk = (slot & 7) ^ (row & 7);
+      uint32_t off = soff[i];
+      if (i < 4 && crmax < kQT - 1) off = (uint32_t)(min(row, crmax) * (int)A.cild + 16 * chunk);
+      const void *base = i < 4 ? (const void *)cbase : (const void *)psrc;
+      lds_u8 *wdst = (lds_u8 *)dst + (i * 8 + wave) * 1024;
+      const uint32_t lds = (uint32_t)(size_t)wdst;
+      if (full_stage) {
+        lds_copy16(base, off, lds);
+      } else if (kRowBytes * s + 16 * chunk < A.di) {
+        lds_copy16(base, off, lds);
+      } else {
+        __attribute__((address_space(3))) uint32_t *z = (__attribute__((address_space(3))) uint32_t *)(wdst + 16 * lane);
+        z[0] = z[1] = z[2] = z[3] = 0u;
+      }
+    }
+  };
+  auto store = [&](int ct, int s) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    if (s == 0 && t < kQT) cparl[ct & 1][t] = cpv;
+  };
+
+  Acc8<BF> acc[4][k8PB];
+  // one stage of 4 steps of 32 dimensions; a scheduling barrier per step keeps the
+  // compiler from hoisting the 24 operand reads of the stage, which would spill the
+  // accumulators (the other wave of the SIMD covers the read latency)
+  auto mfma_stage = [&](const uint8_t *buf, auto first) {
+    constexpr bool kFirst = decltype(first)::value;
+    uint4 av[1][4], bv[1][k8PB];
+    auto read = [&](int g, int slot) {
+      const int so = 16 * ((2 * g + h) ^ (r & 7));
+#pragma unroll
+      for (int pb = 0; pb < k8PB; ++pb)
+        bv[slot][pb] = *reinterpret_cast<const uint4 *>(buf + (kQT + wp * 32 * k8PB + pb * 32 + r) * kRowBytes + so);
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb)
+        av[slot][cb] = *reinterpret_cast<const uint4 *>(buf + (wc * 128 + cb * 32 + r) * kRowBytes + so);
+    };
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      constexpr int cur = 0;
+      read(g, 0);
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+        for (int pb = 0; pb < k8PB; ++pb) {
+          Acc8<BF> cin;
+          if (kFirst && g == 0) {
+#pragma unroll
+            for (int i = 0; i < 16; ++i) cin[i] = 0;
+          } else {
+            cin = acc[cb][pb];
+          }
+          if constexpr (BF) {
+            acc[cb][pb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                __builtin_bit_cast(bf16x8, av[cur][cb]), __builtin_bit_cast(bf16x8, bv[cur][pb]), cin, 0, 0, 0);
+          } else {
+            const uint4 bq = flip4(bv[cur][pb]);  // point codes recentred to int8
+            const i32x4 a4 = {(int)av[cur][cb].x, (int)av[cur][cb].y, (int)av[cur][cb].z, (int)av[cur][cb].w};
+            const i32x4 b4 = {(int)bq.x, (int)bq.y, (int)bq.z, (int)bq.w};
+            acc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a4, b4, cin, 0, 0, 0);
+          }
+        }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  key_t best[k8PB];
+  int bidx[k8PB];
+#pragma unroll
+  for (int pb = 0; pb < k8PB; ++pb) {
+    best[pb] = BF ? (key_t)INFINITY : (key_t)INT_MIN;
+    bidx[pb] = INT_MAX;
+  }
+  // rows ascend with (cb, i) in a lane, so the strict comparison keeps the smallest
+  // index among ties; the tile-local row without the wave's and half's offsets is a
+  // constant here
+  auto epilogue = [&](int ct) {
+    const float *cp = cparl[ct & 1];
+    int loc[k8PB] = {-1, -1};
+    // one 32-row block at a time (a scheduling barrier per block keeps the compiler
+    // from loading every constant and accumulator at once); constants 4 at a time
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) {
+#pragma unroll
+      for (int i4 = 0; i4 < 4; ++i4) {
+        const f32x4 cq4 = *reinterpret_cast<const f32x4 *>(cp + wc * 128 + cb * 32 + 8 * i4 + 4 * h);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int i = 4 * i4 + e;
+          const int cl = cb * 32 + 8 * i4 + e;
+#pragma unroll
+          for (int pb = 0; pb < k8PB; ++pb) {
+            if constexpr (BF) {
+              const float sc = fmaf(-2.0f, acc[cb][pb][i], cq4[e]);  // ||c||^2 - 2<x,c>
+              if (sc < best[pb]) {
+                best[pb] = sc;
+                loc[pb] = cl;
+              }
+            } else {
+              const int key = 2 * acc[cb][pb][i] + __float_as_int(cq4[e]);  // 2<x~,c~> - ||c~||^2
+              if (key > best[pb]) {
+                best[pb] = key;
+                loc[pb] = cl;
+              }
+            }
+          }
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int pb = 0; pb < k8PB; ++pb)
+      if (loc[pb] >= 0) bidx[pb] = (g + ct * NG) * kQT + wc * 128 + loc[pb] + 4 * h;
+  };
+
+  load(0, 0, qst0);
+  store(0, 0);
+  __syncthreads();
+  auto step = [&](int it, const uint8_t *cur, uint8_t *nxt) {
+    const int ct = it / S, s = it - ct * S;
+    const bool has_next = it + 1 < total;
+    const int s_n = (s + 1 == S) ? 0 : s + 1;
+    const int ct_n = (s + 1 == S) ? ct + 1 : ct;
+    if (has_next) load(ct_n, s_n, nxt);
+    if (s == 0)
+      mfma_stage(cur, std::true_type{});
+    else
+      mfma_stage(cur, std::false_type{});
+    if (has_next) store(ct_n, s_n);
+    __syncthreads();
+    if (s == S - 1) {
+      epilogue(ct);
+      // the next tile's steps write tile ct + 2's constants into cparl[ct & 1]
+      __syncthreads();
+    }
+  };
+  for (int it = 0; it < total; it += 2) {
+    step(it, qst0, qst1);
+    if (it + 1 < total) step(it + 1, qst1, qst0);
+  }
+
+  // merges in the key order (SQ8: exact integers), smaller index on ties; the
+  // stored score is the key for bf16 and the negated key (||c~||^2 - 2<x~,c~>) for SQ8
+  auto better = [](key_t o, int oi, key_t b, int bi) {
+    return (BF ? o < b : o > b) || (o == b && oi < bi);
+  };
+#pragma unroll
+  for (int pb = 0; pb < k8PB; ++pb) {
+    const key_t os = __shfl_xor(best[pb], 32);
+    const int oi = __shfl_xor(bidx[pb], 32);
+    if (better(os, oi, best[pb], bidx[pb])) {
+      best[pb] = os;
+      bidx[pb] = oi;
+    }
+  }
+  key_t *ms = reinterpret_cast<key_t *>(qst0);
+  int *mi = reinterpret_cast<int *>(qst0 + kQT * sizeof(key_t));
+  if (wc == 1 && h == 0) {
+#pragma unroll
+    for (int pb = 0; pb < k8PB; ++pb) {
+      ms[wp * 32 * k8PB + pb * 32 + r] = best[pb];
+      mi[wp * 32 * k8PB + pb * 32 + r] = bidx[pb];
+    }
+  }
+  __syncthreads();
+  if (wc == 0 && h == 0) {
+#pragma unroll
+    for (int pb = 0; pb < k8PB; ++pb) {
+      const int pc = wp * 32 * k8PB + pb * 32 + r;
+      const key_t os = ms[pc];
+      const int oi = mi[pc];
+      if (better(os, oi, best[pb], bidx[pb])) {
+        best[pb] = os;
+        bidx[pb] = oi;
+      }
+      const int64_t p = p0 + pc;
+      if (p < A.n) {
+        if (A.keys) {
+          atomicMin(A.keys + p, BF ? score_key((float)best[pb], bidx[pb]) : int_score_key(-(int)best[pb], bidx[pb]));
+        } else {
+          A.assign[p] = bidx[pb] + A.aoff;
+          if (A.score) A.score[p] = BF ? (float)best[pb] : (float)(-(int)best[pb]);
+        }
+      }
+    }
+  }
+}
+
 // ---- centroid preparation: one workgroup per centroid ----------------------
 
 template <int FMT>
@@ -1256,11 +1537,12 @@ __global__ __launch_bounds__(256) void prep_kernel(const void *Cv, int k, int d,
     s = block_sum_f64(s, shd);
     if (t == 0) cn[j] = (float)s;
   }
-  if (FMT == KM_SQ8) {
+  if (FMT == KM_SQ8) {  // recentred int8 codes (code - 128) and their squared norm
     const uint8_t *c = static_cast<const uint8_t *>(Cv) + (int64_t)j * d;
     int s = 0;
     for (int i = t; i < d; i += 256) {
       const int v = (int)c[i] - 128;
+      q[(int64_t)j * d + i] = (int8_t)v;
       s += v * v;
     }
     shi[t] = s;
@@ -1269,7 +1551,7 @@ __global__ __launch_bounds__(256) void prep_kernel(const void *Cv, int k, int d,
       if (t < st) shi[t] += shi[t + st];
       __syncthreads();
     }
-    if (t == 0) qsum[j] = shi[0];
+    if (t == 0) qsum[j] = -shi[0];  // negated: the assignment maximises 2<x~,c~> - ||c~||^2
   }
   if (FMT == KM_LVQ4) {  // LVQ4 of the centroid (Sec. 3.1 LVQ): b = min, s = range / 15, S, Q, N
     const float *c = static_cast<const float *>(Cv) + (int64_t)j * d;
@@ -1574,10 +1856,16 @@ constexpr int kObjBlocks = 1024;
 
 // Centroid-tile groups of the fp32 kernel: up to 8 workgroups share a point tile,
 // each scanning every 8th centroid tile.
+// centroid-tile groups of the SQ8 / bf16 kernel
+static int q8_groups(int k) { return (int)std::min<int64_t>(2, cdiv(k, kQT)); }
+
 int assign_groups(const Points &P, int k) {
-  if (P.fmt != KM_F32 && P.fmt != KM_HYBRID) return 1;
-  constexpr int TC = Geo<Blocking<KM_F32>::CB, Blocking<KM_F32>::PB>::TC;
-  return (int)std::min<int64_t>(8, cdiv(k, TC));
+  if (P.fmt == KM_F32 || P.fmt == KM_HYBRID) {
+    constexpr int TC = Geo<Blocking<KM_F32>::CB, Blocking<KM_F32>::PB>::TC;
+    return (int)std::min<int64_t>(8, cdiv(k, TC));
+  }
+  if (P.fmt == KM_BF16 || (P.fmt == KM_SQ8 && P.d <= kQMaxDimSQ8)) return q8_groups(k);
+  return 1;
 }
 
 template <int FMT>
@@ -1598,10 +1886,10 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
     A.cf = static_cast<const float *>(C);
     A.cfld = P.d;
     A.df = P.d;
-  } else if (FMT == KM_SQ8) {
+  } else if (FMT == KM_SQ8) {  // recentred centroid codes for the direct-copy kernel
     A.pi8 = static_cast<const uint8_t *>(P.data);
     A.pild = P.ld;
-    A.ci8 = static_cast<const int8_t *>(C);
+    A.ci8 = P.d <= kQMaxDimSQ8 ? cp.q : static_cast<const int8_t *>(C);
     A.cild = P.d;
     A.di = P.d;
   } else if (FMT == KM_LVQ4) {  // packed 4-bit point codes, unpacked centroid codes
@@ -1641,7 +1929,25 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
     } else {
       hipLaunchKernelGGL(assign_i8_kernel<FMT>, dim3((unsigned)cdiv(P.n, kT8)), dim3(k8Threads), 0, s, A);
     }
-  } else if constexpr (FMT == KM_SQ8 || FMT == KM_BF16 || FMT == KM_LVQ4) {
+  } else if constexpr (FMT == KM_SQ8 || FMT == KM_BF16) {
+    if (FMT == KM_BF16 || P.d <= kQMaxDimSQ8) {
+      const int64_t npt = cdiv(P.n, kQT);
+      const int ng = assign_groups(P, k);
+      A.n_ptiles = npt;
+      if (ng > 1) {
+        const dim3 gp((unsigned)cdiv(P.n, 256));
+        A.ngroups = ng;
+        A.keys = cp.keys;
+        hipLaunchKernelGGL(keys_init_kernel, gp, dim3(256), 0, s, cp.keys, P.n);
+        hipLaunchKernelGGL(assign_q8_kernel<FMT>, dim3((unsigned)(cdiv(npt, 8) * 8 * ng)), dim3(kQThreads), 0, s, A);
+        hipLaunchKernelGGL(keys_unpack_kernel<FMT == KM_SQ8>, gp, dim3(256), 0, s, cp.keys, P.n, assign, score, aoff);
+      } else {
+        hipLaunchKernelGGL(assign_q8_kernel<FMT>, dim3((unsigned)npt), dim3(kQThreads), 0, s, A);
+      }
+    } else {
+      hipLaunchKernelGGL(assign_i8_kernel<FMT>, dim3((unsigned)cdiv(P.n, kT8)), dim3(k8Threads), 0, s, A);
+    }
+  } else if constexpr (FMT == KM_LVQ4) {
     hipLaunchKernelGGL(assign_i8_kernel<FMT>, dim3((unsigned)cdiv(P.n, kT8)), dim3(k8Threads), 0, s, A);
   } else {
     constexpr int TP = Geo<Blocking<FMT>::CB, Blocking<FMT>::PB>::TP;
@@ -1654,7 +1960,7 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
       A.keys = cp.keys;
       hipLaunchKernelGGL(keys_init_kernel, gp, dim3(256), 0, s, cp.keys, P.n);
       hipLaunchKernelGGL(assign_kernel<FMT>, dim3((unsigned)(cdiv(npt, 8) * 8 * ng)), dim3(kThreads), 0, s, A);
-      hipLaunchKernelGGL(keys_unpack_kernel, gp, dim3(256), 0, s, cp.keys, P.n, assign, score, aoff);
+      hipLaunchKernelGGL(keys_unpack_kernel<false>, gp, dim3(256), 0, s, cp.keys, P.n, assign, score, aoff);
     } else {
       hipLaunchKernelGGL(assign_kernel<FMT>, dim3((unsigned)npt), dim3(kThreads), 0, s, A);
     }
@@ -1669,7 +1975,7 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
 static size_t prep_codes_bytes(const Points &P, int k) {
   const int d0 = P.fmt == KM_HYBRID ? P.d_front : 0;
   if (is_bits_fmt(P.fmt)) return (size_t)k * (size_t)(P.d - d0);
-  if (P.fmt == KM_LVQ4) return (size_t)k * (size_t)P.d;
+  if (P.fmt == KM_LVQ4 || P.fmt == KM_SQ8) return (size_t)k * (size_t)P.d;
   if (P.fmt == KM_BF16) return 2 * (size_t)k * (size_t)P.d;
   return 0;
 }
@@ -1756,7 +2062,7 @@ CentroidPrep prep_slice(const Points &P, const CentroidPrep &cp, int off, int64_
   r.sig2 = cp.sig2 + off;
   const int d0 = P.fmt == KM_HYBRID ? P.d_front : 0;
   if (is_bits_fmt(P.fmt)) r.q = cp.q + (int64_t)off * (P.d - d0);
-  if (P.fmt == KM_LVQ4) r.q = cp.q + (int64_t)off * P.d;
+  if (P.fmt == KM_LVQ4 || P.fmt == KM_SQ8) r.q = cp.q + (int64_t)off * P.d;
   if (P.fmt == KM_BF16) {
     r.cb = cp.cb + (int64_t)off * P.d;
     r.q = reinterpret_cast<const int8_t *>(r.cb);

@@ -41,12 +41,12 @@ __host__ __device__ constexpr bool is_bits_fmt(int fmt) {
 // Per-centroid data rebuilt before each assignment pass.
 struct CentroidPrep {
   const float *cn;     // F32/HYBRID/BF16: ||c'||^2 over the fp32 dims; RABITQ, LVQ4: bias b
-  const int *qsum;     // SQ8: ||c~||^2 ; SIGN1/HYBRID/RABITQ: T_j = sum q ; LVQ4: S_j = sum of codes
+  const int *qsum;     // SQ8: -||c~||^2 ; SIGN1/HYBRID/RABITQ: T_j = sum q ; LVQ4: S_j = sum of codes
   const float *u;      // SIGN1/HYBRID: (sigma*sigma)*Q ; RABITQ: ||c||^2 ; LVQ4: N_j
   const float *sig2;   // SIGN1/HYBRID: 2*sigma ; RABITQ, LVQ4: scale s
   const int8_t *q;     // SIGN1/HYBRID: int8 residual codes, k x dt ; RABITQ, LVQ4: codes 0..15, k x d
   const uint16_t *cb;  // BF16: centroids rounded to bfloat16, k x d
-  unsigned long long *keys;  // F32/HYBRID with centroid-tile groups: per-point (score, index) keys
+  unsigned long long *keys;  // centroid-tile groups (F32/HYBRID/SQ8/BF16): per-point (score, index) keys
 };
 
 // Host-side error plumbing.
