@@ -1856,15 +1856,20 @@ constexpr int kObjBlocks = 1024;
 
 // Centroid-tile groups of the fp32 kernel: up to 8 workgroups share a point tile,
 // each scanning every 8th centroid tile.
-// centroid-tile groups of the SQ8 / bf16 kernel
-static int q8_groups(int k) { return (int)std::min<int64_t>(2, cdiv(k, kQT)); }
+// centroid-tile groups of the SQ8 / bf16 kernel: only to fill the GPU (two
+// workgroups per CU) when the point tiles alone do not; shared point reads give
+// no measurable gain at a million points
+static int q8_groups(int64_t n, int k) {
+  const int64_t npt = cdiv(n, kQT);
+  return (int)std::min<int64_t>(std::min<int64_t>(8, cdiv(k, kQT)), std::max<int64_t>(1, cdiv(2 * 256, npt)));
+}
 
 int assign_groups(const Points &P, int k) {
   if (P.fmt == KM_F32 || P.fmt == KM_HYBRID) {
     constexpr int TC = Geo<Blocking<KM_F32>::CB, Blocking<KM_F32>::PB>::TC;
     return (int)std::min<int64_t>(8, cdiv(k, TC));
   }
-  if (P.fmt == KM_BF16 || (P.fmt == KM_SQ8 && P.d <= kQMaxDimSQ8)) return q8_groups(k);
+  if (P.fmt == KM_BF16 || (P.fmt == KM_SQ8 && P.d <= kQMaxDimSQ8)) return q8_groups(P.n, k);
   return 1;
 }
 

@@ -70,22 +70,44 @@ def test_assign_f32(km, torch, n, d, k):
     assert abs(J - dist_o.sum()) <= OBJ_REL * dist_o.sum() + 1e-3
 
 
-@pytest.mark.parametrize("fmt", ["f32", "hybrid"])
+@pytest.mark.parametrize("fmt", ["f32", "hybrid", "sq8", "bf16"])
 def test_assign_ties_across_centroid_groups(km, torch, fmt):
-    """k = 1100 spreads the centroid tiles over 8 workgroups per point tile; copies
-    of centroids 5 and 130 placed in other groups' tiles must never win."""
+    """k = 1100 spreads the centroid tiles over several workgroups per point tile
+    (8 for fp32 / hybrid with 128-centroid tiles, 5 for SQ8 / bf16 with 256-centroid
+    tiles at this n), merged through (score, index) keys; copies of centroids 5 and
+    130 placed in other groups' tiles must never win."""
     n, d, k = 3000, 96, 1100
     X = blobs(n, d, 40, seed=17)
     C = X[pick(n, k, 17)].copy()
-    C[900] = C[5]    # tile 7 vs tile 0
-    C[1050] = C[130]  # tile 8 vs tile 1
+    C[900] = C[5]    # tile 7 vs tile 0 (fp32 tiles; 3 vs 0 of 256)
+    C[1050] = C[130]  # tile 8 vs tile 1 (4 vs 0 of 256)
     C[640] = C[5]
+    if fmt == "sq8":  # exact integer scores: bit-exact against the oracle
+        lo, hi = orc.sq8_fit(X)
+        codes, Cq = orc.sq8_encode(X, lo, hi), orc.sq8_encode(C, lo, hi)
+        a_o, dist_o = orc.assign_sq8(codes, Cq)
+        a, sc, _ = km.kmeans_assign(km.points_sq8(to_dev(codes, torch)), to_dev(Cq, torch), score=True)
+        torch.cuda.synchronize()
+        a = host(a)
+        np.testing.assert_array_equal(a, a_o)
+        sq = (Cq.astype(np.int64) - 128)
+        exp_sc = (sq[a] ** 2).sum(1) - 2 * (sq[a] * (codes.astype(np.int64) - 128)).sum(1)
+        np.testing.assert_array_equal(host(sc).astype(np.int64), exp_sc)
+    elif fmt == "bf16":
+        codes = orc.bf16_round(X)
+        a_o, _ = orc.assign_bf16(codes, C)
+        Pb = km.points_bf16(to_dev(codes.view(np.int16), torch).view(torch.bfloat16))
+        a, _, _ = km.kmeans_assign(Pb, to_dev(C, torch), score=False)
+        a = host(a)
+        Xb = orc.bf16_decode(codes).astype(np.float64)
+        Cb = orc.bf16_decode(orc.bf16_round(C)).astype(np.float64)
+        assert_fp_assign(a, a_o, f32_dist(Xb, Cb), "bf16 groups")
     if fmt == "f32":
         a_o, _ = orc.assign_f32(X, C)
         a, _, _ = km.kmeans_assign(km.points_f32(to_dev(X, torch)), to_dev(C, torch), score=False)
         a = host(a)
         assert_fp_assign(a, a_o, f32_dist(X, C), "f32 groups")
-    else:
+    elif fmt == "hybrid":
         d0 = 32
         m = orc.col_mean(X)
         bits, alpha = orc.sign1_encode(X, m, d0)
@@ -95,7 +117,7 @@ def test_assign_ties_across_centroid_groups(km, torch, fmt):
                              to_dev(m, torch), d)
         a, _, _ = km.kmeans_assign(P, to_dev(C, torch), score=False)
         a = host(a)
-    if fmt == "f32":  # each centroid is a data point, which picks it (or an equal copy)
+    if fmt in ("f32", "sq8", "bf16"):  # each centroid is a data point, which picks it (or an equal copy)
         assert (a == 5).any() and (a == 130).any()
     assert not np.isin(a, [640, 900, 1050]).any()
 
