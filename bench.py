@@ -286,7 +286,7 @@ def workload_bf16(cfg, torch, km, args):
                            "formats": ["bf16"]},
                 "distances_per_s": (T + 1) * spec.n * k * K / elapsed,
                 "partition_cost": {"bf16": float(out["bf16"].item())},
-                "roofline": {"bound": "mfma", "kernel": "assign_i8_kernel<bf16>", "achieved": ach,
+                "roofline": {"bound": "mfma", "kernel": "assign_q8_kernel<bf16>", "achieved": ach,
                              "peak": PEAK["bf16_mfma_tflops"], "unit": "TFLOP/s",
                              "frac": ach / PEAK["bf16_mfma_tflops"], "traffic": None, "avg_launch_ms": a_ms},
                 "stages": {"bf16": stage_summary(s)}}
@@ -513,7 +513,7 @@ def workload_sign1(cfg, torch, km, args):
                            "formats": ["sign1"]},
                 "distances_per_s": (T + 1) * spec.n * k * K / elapsed,
                 "partition_cost": {"sign1": float(out["sign1"].item())},
-                "roofline": {"bound": "mfma", "kernel": "assign_kernel<1-bit>", "achieved": ach,
+                "roofline": {"bound": "mfma", "kernel": "assign_bits_kernel<sign1>", "achieved": ach,
                              "peak": PEAK["int8_mfma_tops"], "unit": "TOP/s", "frac": ach / PEAK["int8_mfma_tops"],
                              "traffic": None, "avg_launch_ms": a_ms},
                 "stages": {"sign1": stage_summary(s)}}
