@@ -533,8 +533,23 @@ static km_status fine_impl(const Points &p, const int32_t *meso, int k_meso, int
   const size_t b_part = objective ? al(sizeof(double) * (size_t)objective_blocks(N)) : 0;
   const size_t b_idx = al(sizeof(int64_t) * (size_t)k);
   const size_t b_seg = al(sizeof(int) * 2 * (size_t)k);
+  // fp32, SQ8 and bf16: one assignment launch per pass over all meso-clusters
+  // (segment and tile tables); other formats launch per meso-cluster
+  const int seg_rows = assign_segment_rows(p);
+  std::vector<int4> segs;
+  std::vector<int2> tiles;
+  if (seg_rows > 0) {
+    for (int i = 0; i < k_meso; ++i) {
+      if (n_i[i] == 0) continue;
+      const int si = (int)segs.size();
+      segs.push_back(make_int4((int)start[i], (int)n_i[i], (int)off[i], kf[i]));
+      for (int64_t tt = 0; tt * seg_rows < n_i[i]; ++tt) tiles.push_back(make_int2(si, (int)tt));
+    }
+  }
+  const size_t b_segs = al(sizeof(int4) * segs.size());
+  const size_t b_tiles = al(sizeof(int2) * tiles.size());
   Scratch ws(s);
-  st = ws.alloc(b_perm + b_prep + b_upd + b_a + b_score + b_xc + b_part + b_idx + b_seg);
+  st = ws.alloc(b_perm + b_prep + b_upd + b_a + b_score + b_xc + b_part + b_idx + b_seg + b_segs + b_tiles);
   if (st != KM_OK) return st;
   uint8_t *w = ws.get();
   uint8_t *wperm = w;
@@ -546,7 +561,13 @@ static km_status fine_impl(const Points &p, const int32_t *meso, int k_meso, int
   double *part = reinterpret_cast<double *>(wupd + b_upd + b_a + b_score + b_xc);
   int64_t *didx = reinterpret_cast<int64_t *>(wupd + b_upd + b_a + b_score + b_xc + b_part);
   int *dseg = reinterpret_cast<int *>(wupd + b_upd + b_a + b_score + b_xc + b_part + b_idx);
+  int4 *dsegs = reinterpret_cast<int4 *>(reinterpret_cast<uint8_t *>(dseg) + b_seg);
+  int2 *dtiles = reinterpret_cast<int2 *>(reinterpret_cast<uint8_t *>(dsegs) + b_segs);
   KMQ_STAGE(clk, kStOther, launch_permute_points(p, so.perm, N, wperm, &q, s));
+  if (!segs.empty()) {
+    KMQ_HIP(hipMemcpyAsync(dsegs, segs.data(), sizeof(int4) * segs.size(), hipMemcpyHostToDevice, s));
+    KMQ_HIP(hipMemcpyAsync(dtiles, tiles.data(), sizeof(int2) * tiles.size(), hipMemcpyHostToDevice, s));
+  }
   KMQ_HIP(hipMemcpyAsync(dseg, seg.data(), sizeof(int) * seg.size(), hipMemcpyHostToDevice, s));
   if (!c_given) {
     KMQ_HIP(hipMemcpyAsync(didx, idx.data(), sizeof(int64_t) * (size_t)k, hipMemcpyHostToDevice, s));
@@ -558,7 +579,11 @@ static km_status fine_impl(const Points &p, const int32_t *meso, int k_meso, int
     KMQ_STAGE(clk, kStPrep, launch_prep(q, C, k, wprep, &cp, s));
     st = clk.begin(kStAssign);
     if (st != KM_OK) return st;
-    for (int i = 0; i < k_meso; ++i) {  // each meso-cluster against its own fine centroids
+    if (!segs.empty()) {  // every meso-cluster against its own fine centroids, one launch
+      st = launch_assign_segments(q, C, cp, dsegs, dtiles, (int64_t)tiles.size(), ap, sc, s);
+      if (st != KM_OK) return st;
+    }
+    for (int i = 0; seg_rows == 0 && i < k_meso; ++i) {  // the same, one launch per meso-cluster
       if (n_i[i] == 0) continue;
       st = launch_assign(slice_points(q, start[i], n_i[i]), static_cast<const uint8_t *>(C) + off[i] * crow,
                          prep_slice(q, cp, (int)off[i], start[i]), kf[i], ap + start[i],

@@ -74,6 +74,11 @@ struct AssignArgs {
   int ngroups;
   int64_t n_ptiles;
   unsigned long long *keys;
+  // segmented launch (fp32): workgroup b takes point tile tiles[b].y of segment
+  // tiles[b].x; segment i is rows [segs[i].x, + segs[i].y) against centroids
+  // [segs[i].z, + segs[i].w) (indices into the full centroid and prepared arrays)
+  const int4 *segs;
+  const int2 *tiles;
 };
 
 // (score, index) as one 64-bit key whose unsigned order is the lexicographic
@@ -354,10 +359,27 @@ struct Blocking {
   static constexpr int MINB = 2;
 };
 
-template <int FMT>
-__global__ __launch_bounds__(kThreads, Blocking<FMT>::MINB) void assign_kernel(AssignArgs A) {
+template <int FMT, bool SEG = false>
+__global__ __launch_bounds__(kThreads, Blocking<FMT>::MINB) void assign_kernel(AssignArgs A0) {
   constexpr int CB = Blocking<FMT>::CB, PB = Blocking<FMT>::PB;
   typedef Geo<CB, PB> G;
+  // a segmented launch narrows the arguments to this workgroup's segment
+  AssignArgs A = A0;
+  int64_t seg_p0 = 0;  // first row of this workgroup's point tile (segmented launch)
+  if constexpr (SEG) {
+    const int2 ts = A0.tiles[blockIdx.x];
+    const int4 sg = A0.segs[ts.x];
+    seg_p0 = (int64_t)sg.x + (int64_t)ts.y * G::TP;
+    A.n = (int64_t)sg.x + sg.y;
+    A.k = sg.w;
+    A.cf = A0.cf + (int64_t)sg.z * A0.cfld;
+    A.cp.cn = A0.cp.cn + sg.z;
+    A.cp.qsum = A0.cp.qsum + sg.z;
+    A.cp.u = A0.cp.u + sg.z;
+    A.cp.sig2 = A0.cp.sig2 + sg.z;
+    A.aoff = A0.aoff + sg.z;
+    A.ngroups = 1;
+  }
   __shared__ __align__(16) uint8_t lds[2 * G::STAGE];
   __shared__ __align__(16) float cparl[2][4 * G::TC];
   typedef typename std::conditional<Cfg<FMT>::kIntScore, int, float>::type score_t;
@@ -379,7 +401,7 @@ __global__ __launch_bounds__(kThreads, Blocking<FMT>::MINB) void assign_kernel(A
     g = (int)(l % NG);
     if (pt >= A.n_ptiles) return;  // whole workgroup, before any barrier
   }
-  const int64_t p0 = pt * G::TP;
+  const int64_t p0 = SEG ? seg_p0 : pt * G::TP;
 
   const int SF = Cfg<FMT>::kFp ? (A.df + 31) / 32 : 0;
   const int SI = Cfg<FMT>::kInt ? (A.di + kRowBytes - 1) / kRowBytes : 0;
@@ -1258,9 +1280,24 @@ constexpr int kQThreads = 512;                      // 8 waves
 constexpr int kQStageBytes = 2 * kQT * kRowBytes;   // 64 KB: centroid rows, then point rows
 constexpr int kQMaxDimSQ8 = 8192;                   // |2<x~,c~> - ||c~||^2| < 2^31
 
-template <int FMT>
-__global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A) {
+template <int FMT, bool SEG = false>
+__global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) {
   constexpr bool BF = FMT == KM_BF16;
+  // a segmented launch narrows the arguments to this workgroup's segment
+  AssignArgs A = A0;
+  int64_t seg_p0 = 0;  // first row of this workgroup's point tile (segmented launch)
+  if constexpr (SEG) {
+    const int2 ts = A0.tiles[blockIdx.x];
+    const int4 sg = A0.segs[ts.x];
+    seg_p0 = (int64_t)sg.x + (int64_t)ts.y * kQT;
+    A.n = (int64_t)sg.x + sg.y;
+    A.k = sg.w;
+    A.ci8 = A0.ci8 + (int64_t)sg.z * A0.cild;
+    A.cp.cn = A0.cp.cn + sg.z;
+    A.cp.qsum = A0.cp.qsum + sg.z;
+    A.aoff = A0.aoff + sg.z;
+    A.ngroups = 1;
+  }
   static_assert(FMT == KM_SQ8 || FMT == KM_BF16, "SQ8 or bf16 points");
   // SQ8 maximises the key 2D - ||c~||^2 (= -score, exact in int32); bf16 minimises
   // the score ||c||^2 - 2<x,c> (fp32)
@@ -1281,7 +1318,7 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A) {
     g = (int)(l % NG);
     if (pt >= A.n_ptiles) return;  // whole workgroup, before any barrier
   }
-  const int64_t p0 = pt * kQT;
+  const int64_t p0 = SEG ? seg_p0 : pt * kQT;
   const int S = (A.di + kRowBytes - 1) / kRowBytes;
   const int nct = (A.k + kQT - 1) / kQT;
   const int nmy = (nct - g + NG - 1) / NG;  // centroid tiles of this workgroup (>= 1: NG <= nct)
@@ -2057,6 +2094,50 @@ km_status launch_assign(const Points &P, const void *C, const CentroidPrep &cp, 
     case KM_LVQ4: return launch_assign_t<KM_LVQ4>(P, C, cp, k, assign, score, s, aoff);
     default: return KM_EUNSUPPORTED;
   }
+}
+
+int assign_segment_rows(const Points &P) {
+  if (P.fmt == KM_F32) return Geo<Blocking<KM_F32>::CB, Blocking<KM_F32>::PB>::TP;
+  if (P.fmt == KM_BF16 || (P.fmt == KM_SQ8 && P.d <= kQMaxDimSQ8)) return kQT;
+  return 0;
+}
+
+km_status launch_assign_segments(const Points &P, const void *C, const CentroidPrep &cp, const int4 *segs,
+                                 const int2 *tiles, int64_t ntiles, int32_t *assign, float *score, hipStream_t s) {
+  if (assign_segment_rows(P) == 0) return KM_EUNSUPPORTED;
+  if (ntiles == 0) return KM_OK;
+  AssignArgs A{};
+  A.ngroups = 1;
+  A.n = P.n;
+  A.assign = assign;
+  A.score = score;
+  A.cp = cp;
+  A.segs = segs;
+  A.tiles = tiles;
+  if (P.fmt == KM_F32) {
+    A.pf = static_cast<const float *>(P.data);
+    A.pfld = P.ld;
+    A.cf = static_cast<const float *>(C);
+    A.cfld = P.d;
+    A.df = P.d;
+    hipLaunchKernelGGL((assign_kernel<KM_F32, true>), dim3((unsigned)ntiles), dim3(kThreads), 0, s, A);
+  } else if (P.fmt == KM_SQ8) {  // recentred centroid codes from the preparation
+    A.pi8 = static_cast<const uint8_t *>(P.data);
+    A.pild = P.ld;
+    A.ci8 = cp.q;
+    A.cild = P.d;
+    A.di = P.d;
+    hipLaunchKernelGGL((assign_q8_kernel<KM_SQ8, true>), dim3((unsigned)ntiles), dim3(kQThreads), 0, s, A);
+  } else {  // bfloat16 rows as bytes
+    A.pi8 = static_cast<const uint8_t *>(P.data);
+    A.pild = 2 * P.ld;
+    A.ci8 = reinterpret_cast<const int8_t *>(cp.cb);
+    A.cild = 2 * (int64_t)P.d;
+    A.di = 2 * P.d;
+    hipLaunchKernelGGL((assign_q8_kernel<KM_BF16, true>), dim3((unsigned)ntiles), dim3(kQThreads), 0, s, A);
+  }
+  KMQ_LAUNCH_CHECK("assign kernel (segments)");
+  return KM_OK;
 }
 
 CentroidPrep prep_slice(const Points &P, const CentroidPrep &cp, int off, int64_t pstart) {

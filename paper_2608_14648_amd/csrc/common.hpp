@@ -74,6 +74,15 @@ km_status launch_prep(const Points &P, const void *C, int k, void *ws_prep, Cent
                       hipStream_t s);
 size_t prep_bytes(const Points &P, int k);
 // aoff is added to every stored centroid index (C and cp may be a slice of a larger set)
+// One launch for many (row range, centroid range) segments of fp32, SQ8 or bf16
+// points: segment i is rows [segs[i].x, + segs[i].y) against centroids
+// [segs[i].z, + segs[i].w) of C and of the prepared constants; workgroup b takes
+// point tile tiles[b].y of segment tiles[b].x (tiles of assign_segment_rows(P) rows;
+// 0 = not supported for these points).  assign and score are indexed by absolute
+// row; centroid indices are absolute.
+int assign_segment_rows(const Points &P);
+km_status launch_assign_segments(const Points &P, const void *C, const CentroidPrep &cp, const int4 *segs,
+                                 const int2 *tiles, int64_t ntiles, int32_t *assign, float *score, hipStream_t s);
 km_status launch_assign(const Points &P, const void *C, const CentroidPrep &cp, int k, int32_t *assign,
                         float *score, hipStream_t s, int aoff = 0);
 // cp restricted to centroids [off, ...) and, for the per-point keys, to points [pstart, ...)
