@@ -382,7 +382,7 @@ def workload_hier(cfg, torch, km, args):
                 "ms_per_fit": {"f32": float(res["ph32"].sum()), "sq8": float(res["ph8"].sum())},
                 "phase_ms": {"f32": {"meso": res["ph32"][0], "fine": res["ph32"][1]},
                              "sq8": {"meso": res["ph8"][0], "fine": res["ph8"][1]}},
-                "roofline": {"bound": "mfma", "kernel": "assign_kernel<fp32> (meso and per-meso fine launches)",
+                "roofline": {"bound": "mfma", "kernel": "assign_kernel<fp32> (meso launches and segmented fine launches)",
                              "achieved": ach, "peak": PEAK["fp32_mfma_tflops"], "unit": "TFLOP/s",
                              "frac": ach / PEAK["fp32_mfma_tflops"], "traffic": None,
                              "algorithmic_flop_per_fit": flop / K},
