@@ -21,29 +21,60 @@ __global__ __launch_bounds__(256) void colminmax_partial_kernel(const float *X, 
                                                                 float *pmin, float *pmax) {
   const int64_t r0 = (int64_t)blockIdx.x * kRowsPerBlock;
   const int64_t r1 = min<int64_t>(n, r0 + kRowsPerBlock);
+  auto fold = [](f32x4 &mn, f32x4 &mx, const f32x4 v) {
+    mn.x = fminf(mn.x, v.x); mn.y = fminf(mn.y, v.y); mn.z = fminf(mn.z, v.z); mn.w = fminf(mn.w, v.w);
+    mx.x = fmaxf(mx.x, v.x); mx.y = fmaxf(mx.y, v.y); mx.z = fmaxf(mx.z, v.z); mx.w = fmaxf(mx.w, v.w);
+  };
   for (int g = threadIdx.x; g < d / 4; g += 256) {
-    f32x4 mn = *reinterpret_cast<const f32x4 *>(X + r0 * ldx + 4 * g);
-    f32x4 mx = mn;
-    for (int64_t r = r0 + 1; r < r1; ++r) {
-      const f32x4 v = *reinterpret_cast<const f32x4 *>(X + r * ldx + 4 * g);
-      mn.x = fminf(mn.x, v.x); mn.y = fminf(mn.y, v.y); mn.z = fminf(mn.z, v.z); mn.w = fminf(mn.w, v.w);
-      mx.x = fmaxf(mx.x, v.x); mx.y = fmaxf(mx.y, v.y); mx.z = fmaxf(mx.z, v.z); mx.w = fmaxf(mx.w, v.w);
+    // four independent running extrema keep four row loads in flight per thread
+    // (min and max are exact in any order)
+    const f32x4 first = *reinterpret_cast<const f32x4 *>(X + r0 * ldx + 4 * g);
+    f32x4 mn[4] = {first, first, first, first}, mx[4] = {first, first, first, first};
+    int64_t r = r0 + 1;
+    for (; r + 3 < r1; r += 4) {
+      f32x4 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const f32x4 *>(X + (r + u) * ldx + 4 * g);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) fold(mn[u], mx[u], v[u]);
     }
-    *reinterpret_cast<f32x4 *>(pmin + (int64_t)blockIdx.x * d + 4 * g) = mn;
-    *reinterpret_cast<f32x4 *>(pmax + (int64_t)blockIdx.x * d + 4 * g) = mx;
+    for (; r < r1; ++r) fold(mn[0], mx[0], *reinterpret_cast<const f32x4 *>(X + r * ldx + 4 * g));
+#pragma unroll
+    for (int u = 1; u < 4; ++u) {
+      fold(mn[0], mx[0], mn[u]);
+      fold(mn[0], mx[0], mx[u]);
+    }
+    *reinterpret_cast<f32x4 *>(pmin + (int64_t)blockIdx.x * d + 4 * g) = mn[0];
+    *reinterpret_cast<f32x4 *>(pmax + (int64_t)blockIdx.x * d + 4 * g) = mx[0];
   }
 }
 
-__global__ void colminmax_final_kernel(const float *pmin, const float *pmax, int nb, int d, float *lo, float *hi) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= d) return;
-  float mn = pmin[i], mx = pmax[i];
-  for (int b = 1; b < nb; ++b) {
+// one workgroup per column: strided partial extrema, then a tree (min and max are
+// exact in any order)
+__global__ __launch_bounds__(256) void colminmax_final_kernel(const float *pmin, const float *pmax, int nb, int d,
+                                                              float *lo, float *hi) {
+  __shared__ float smn[256], smx[256];
+  const int i = blockIdx.x;
+  const int t = threadIdx.x;
+  float mn = INFINITY, mx = -INFINITY;
+  for (int b = t; b < nb; b += 256) {
     mn = fminf(mn, pmin[(int64_t)b * d + i]);
     mx = fmaxf(mx, pmax[(int64_t)b * d + i]);
   }
-  lo[i] = mn;
-  hi[i] = mx;
+  smn[t] = mn;
+  smx[t] = mx;
+  __syncthreads();
+  for (int st = 128; st > 0; st >>= 1) {
+    if (t < st) {
+      smn[t] = fminf(smn[t], smn[t + st]);
+      smx[t] = fmaxf(smx[t], smx[t + st]);
+    }
+    __syncthreads();
+  }
+  if (t == 0) {
+    lo[i] = smn[0];
+    hi[i] = smx[0];
+  }
 }
 
 __global__ __launch_bounds__(256) void colsum_partial_kernel(const float *X, int64_t n, int d, int64_t ldx,
@@ -296,7 +327,7 @@ km_status launch_quantize(const float *X, int64_t n, int d, int64_t ldx, int fmt
     float *inv = pmax + (size_t)nb * d;
     if (flags & KM_Q_FIT_PARAMS) {
       hipLaunchKernelGGL(colminmax_partial_kernel, dim3(nb), dim3(256), 0, s, X, n, d, ldx, pmin, pmax);
-      hipLaunchKernelGGL(colminmax_final_kernel, gd, dim3(256), 0, s, pmin, pmax, nb, d, lo, hi);
+      hipLaunchKernelGGL(colminmax_final_kernel, dim3((unsigned)d), dim3(256), 0, s, pmin, pmax, nb, d, lo, hi);
     }
     hipLaunchKernelGGL(sq8_inv_kernel, gd, dim3(256), 0, s, lo, hi, d, inv);
     const int64_t work = n * (d / 16);
