@@ -1275,21 +1275,28 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void assign_bits_kernel(AssignArgs
 // of point tile pt; the ngroups workgroups of a point tile are consecutive among
 // the workgroups of one XCD, so their concurrent reads of the point rows share that
 // XCD's L2, and they merge through 64-bit (score, index) keys.
-constexpr int kQT = 256;                            // centroids and points per tile
+constexpr int kQT = 256;                            // points per workgroup (and centroids per tile, CB = 4)
 constexpr int kQThreads = 512;                      // 8 waves
-constexpr int kQStageBytes = 2 * kQT * kRowBytes;   // 64 KB: centroid rows, then point rows
 constexpr int kQMaxDimSQ8 = 8192;                   // |2<x~,c~> - ||c~||^2| < 2^31
 
-template <int FMT, bool SEG = false>
+// CB: 32 x 32 centroid blocks per wave, 4 (256-centroid tiles) or 2 (128-centroid
+// tiles, for k <= 128, where a 256-centroid tile would be mostly padding)
+template <int FMT, bool SEG = false, int CB = 4>
 __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) {
   constexpr bool BF = FMT == KM_BF16;
+  static_assert(CB == 2 || CB == 4, "128- or 256-centroid tiles");
+  constexpr int TC = 64 * CB;                       // centroids per tile
+  constexpr int TP = kQT;                           // points per workgroup
+  constexpr int NCC = TC / 64;                      // centroid copies per thread and stage
+  constexpr int NCOPY = (TC + TP) / 64;             // all copies per thread and stage
+  constexpr int STAGE = (TC + TP) * kRowBytes;      // centroid rows, then point rows
   // a segmented launch narrows the arguments to this workgroup's segment
   AssignArgs A = A0;
   int64_t seg_p0 = 0;  // first row of this workgroup's point tile (segmented launch)
   if constexpr (SEG) {
     const int2 ts = A0.tiles[blockIdx.x];
     const int4 sg = A0.segs[ts.x];
-    seg_p0 = (int64_t)sg.x + (int64_t)ts.y * kQT;
+    seg_p0 = (int64_t)sg.x + (int64_t)ts.y * TP;
     A.n = (int64_t)sg.x + sg.y;
     A.k = sg.w;
     A.ci8 = A0.ci8 + (int64_t)sg.z * A0.cild;
@@ -1302,9 +1309,9 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
   // SQ8 maximises the key 2D - ||c~||^2 (= -score, exact in int32); bf16 minimises
   // the score ||c||^2 - 2<x,c> (fp32)
   typedef typename std::conditional<BF, float, int>::type key_t;
-  __shared__ __align__(16) uint8_t qst0[kQStageBytes];
-  __shared__ __align__(16) uint8_t qst1[kQStageBytes];
-  __shared__ __align__(16) float cparl[2][kQT];
+  __shared__ __align__(16) uint8_t qst0[STAGE];
+  __shared__ __align__(16) uint8_t qst1[STAGE];
+  __shared__ __align__(16) float cparl[2][TC];
   const int t = threadIdx.x;
   const int lane = t & 63, wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int r = lane & 31, h = lane >> 5;
@@ -1318,33 +1325,33 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
     g = (int)(l % NG);
     if (pt >= A.n_ptiles) return;  // whole workgroup, before any barrier
   }
-  const int64_t p0 = SEG ? seg_p0 : pt * kQT;
+  const int64_t p0 = SEG ? seg_p0 : pt * TP;
   const int S = (A.di + kRowBytes - 1) / kRowBytes;
-  const int nct = (A.k + kQT - 1) / kQT;
+  const int nct = (A.k + TC - 1) / TC;
   const int nmy = (nct - g + NG - 1) / NG;  // centroid tiles of this workgroup (>= 1: NG <= nct)
   const int total = nmy * S;
-  const int prmax = (int)min<int64_t>(A.n - 1 - p0, kQT - 1);
+  const int prmax = (int)min<int64_t>(A.n - 1 - p0, TP - 1);
   const uint8_t *pbase = A.pi8 + p0 * A.pild;
 
-  // copy i (0..7) of a wave fills slots (8 i + wave) 64 .. + 63 of the stage: rows
-  // 0..255 are centroids, 256..511 points.  A lane's source is the stage's first
+  // copy i (0 .. NCOPY - 1) of a wave fills slots (8 i + wave) 64 .. + 63 of the
+  // stage: rows 0 .. TC - 1 are centroids, the next TP rows points.  A lane's source is the stage's first
   // byte plus a 32-bit offset: point rows are clamped into the data once, centroid
   // rows only in a last, partial centroid tile.  In a partial last stage the lanes
   // whose chunk lies past the dimensions store zeros instead of copying.
-  uint32_t soff[8];
+  uint32_t soff[NCOPY];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
+  for (int i = 0; i < NCOPY; ++i) {
     const int slot = (i * 8 + wave) * 64 + lane;
     const int row = slot >> 3;
     const int chunk = (slot & 7) ^ (row & 7);
-    soff[i] = i < 4 ? (uint32_t)(row * (int)A.cild + 16 * chunk)
-                    : (uint32_t)(min(row - kQT, prmax) * (int)A.pild + 16 * chunk);
+    soff[i] = i < NCC ? (uint32_t)(row * (int)A.cild + 16 * chunk)
+                      : (uint32_t)(min(row - TC, prmax) * (int)A.pild + 16 * chunk);
   }
   float cpv = 0.f;
   auto load = [&](int ct, int s, uint8_t *dst) {
-    const int c0 = (g + ct * NG) * kQT;
-    const int crmax = min(A.k - 1 - c0, kQT - 1);
-    if (s == 0 && t < kQT) {
+    const int c0 = (g + ct * NG) * TC;
+    const int crmax = min(A.k - 1 - c0, TC - 1);
+    if (s == 0 && t < TC) {
       const int j = c0 + min(t, crmax);
       cpv = BF ? A.cp.cn[j] : __int_as_float(A.cp.qsum[j]);  // SQ8: -||c~||^2
     }
@@ -1352,13 +1359,13 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
     const uint8_t *psrc = pbase + kRowBytes * s;
     const bool full_stage = kRowBytes * (s + 1) <= A.di;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < NCOPY; ++i) {
       const int slot = (i * 8 + wave) * 64 + lane;
       const int row = slot >> 3;
       const int chunk = (slot & 7) ^ (row & 7);
       uint32_t off = soff[i];
-      if (i < 4 && crmax < kQT - 1) off = (uint32_t)(min(row, crmax) * (int)A.cild + 16 * chunk);
-      const void *base = i < 4 ? (const void *)cbase : (const void *)psrc;
+      if (i < NCC && crmax < TC - 1) off = (uint32_t)(min(row, crmax) * (int)A.cild + 16 * chunk);
+      const void *base = i < NCC ? (const void *)cbase : (const void *)psrc;
       lds_u8 *wdst = (lds_u8 *)dst + (i * 8 + wave) * 1024;
       const uint32_t lds = (uint32_t)(size_t)wdst;
       if (full_stage) {
@@ -1373,31 +1380,31 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
   };
   auto store = [&](int ct, int s) {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    if (s == 0 && t < kQT) cparl[ct & 1][t] = cpv;
+    if (s == 0 && t < TC) cparl[ct & 1][t] = cpv;
   };
 
-  Acc8<BF> acc[4][k8PB];
+  Acc8<BF> acc[CB][k8PB];
   // one stage of 4 steps of 32 dimensions; a scheduling barrier per step keeps the
   // compiler from hoisting the 24 operand reads of the stage, which would spill the
   // accumulators (the other wave of the SIMD covers the read latency)
   auto mfma_stage = [&](const uint8_t *buf, auto first) {
     constexpr bool kFirst = decltype(first)::value;
-    uint4 av[1][4], bv[1][k8PB];
+    uint4 av[1][CB], bv[1][k8PB];
     auto read = [&](int g, int slot) {
       const int so = 16 * ((2 * g + h) ^ (r & 7));
 #pragma unroll
       for (int pb = 0; pb < k8PB; ++pb)
-        bv[slot][pb] = *reinterpret_cast<const uint4 *>(buf + (kQT + wp * 32 * k8PB + pb * 32 + r) * kRowBytes + so);
+        bv[slot][pb] = *reinterpret_cast<const uint4 *>(buf + (TC + wp * 32 * k8PB + pb * 32 + r) * kRowBytes + so);
 #pragma unroll
-      for (int cb = 0; cb < 4; ++cb)
-        av[slot][cb] = *reinterpret_cast<const uint4 *>(buf + (wc * 128 + cb * 32 + r) * kRowBytes + so);
+      for (int cb = 0; cb < CB; ++cb)
+        av[slot][cb] = *reinterpret_cast<const uint4 *>(buf + (wc * 32 * CB + cb * 32 + r) * kRowBytes + so);
     };
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       constexpr int cur = 0;
       read(g, 0);
 #pragma unroll
-      for (int cb = 0; cb < 4; ++cb)
+      for (int cb = 0; cb < CB; ++cb)
 #pragma unroll
         for (int pb = 0; pb < k8PB; ++pb) {
           Acc8<BF> cin;
@@ -1437,10 +1444,10 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
     // one 32-row block at a time (a scheduling barrier per block keeps the compiler
     // from loading every constant and accumulator at once); constants 4 at a time
 #pragma unroll
-    for (int cb = 0; cb < 4; ++cb) {
+    for (int cb = 0; cb < CB; ++cb) {
 #pragma unroll
       for (int i4 = 0; i4 < 4; ++i4) {
-        const f32x4 cq4 = *reinterpret_cast<const f32x4 *>(cp + wc * 128 + cb * 32 + 8 * i4 + 4 * h);
+        const f32x4 cq4 = *reinterpret_cast<const f32x4 *>(cp + wc * 32 * CB + cb * 32 + 8 * i4 + 4 * h);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int i = 4 * i4 + e;
@@ -1467,7 +1474,7 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
     }
 #pragma unroll
     for (int pb = 0; pb < k8PB; ++pb)
-      if (loc[pb] >= 0) bidx[pb] = (g + ct * NG) * kQT + wc * 128 + loc[pb] + 4 * h;
+      if (loc[pb] >= 0) bidx[pb] = (g + ct * NG) * TC + wc * 32 * CB + loc[pb] + 4 * h;
   };
 
   load(0, 0, qst0);
@@ -1511,7 +1518,7 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
     }
   }
   key_t *ms = reinterpret_cast<key_t *>(qst0);
-  int *mi = reinterpret_cast<int *>(qst0 + kQT * sizeof(key_t));
+  int *mi = reinterpret_cast<int *>(qst0 + TP * sizeof(key_t));
   if (wc == 1 && h == 0) {
 #pragma unroll
     for (int pb = 0; pb < k8PB; ++pb) {
@@ -1896,9 +1903,13 @@ constexpr int kObjBlocks = 1024;
 // centroid-tile groups of the SQ8 / bf16 kernel: only to fill the GPU (two
 // workgroups per CU) when the point tiles alone do not; shared point reads give
 // no measurable gain at a million points
+// centroids per tile of the SQ8 / bf16 kernel: 128 when k fits, else 256
+static int q8_tile_centroids(int k) { return k <= 128 ? 128 : 256; }
+
 static int q8_groups(int64_t n, int k) {
   const int64_t npt = cdiv(n, kQT);
-  return (int)std::min<int64_t>(std::min<int64_t>(8, cdiv(k, kQT)), std::max<int64_t>(1, cdiv(2 * 256, npt)));
+  return (int)std::min<int64_t>(std::min<int64_t>(8, cdiv(k, q8_tile_centroids(k))),
+                                std::max<int64_t>(1, cdiv(2 * 256, npt)));
 }
 
 int assign_groups(const Points &P, int k) {
@@ -1981,10 +1992,15 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
         A.ngroups = ng;
         A.keys = cp.keys;
         hipLaunchKernelGGL(keys_init_kernel, gp, dim3(256), 0, s, cp.keys, P.n);
-        hipLaunchKernelGGL(assign_q8_kernel<FMT>, dim3((unsigned)(cdiv(npt, 8) * 8 * ng)), dim3(kQThreads), 0, s, A);
+      }
+      const dim3 grid((unsigned)(ng > 1 ? cdiv(npt, 8) * 8 * ng : npt));
+      if (q8_tile_centroids(k) == 128)
+        hipLaunchKernelGGL((assign_q8_kernel<FMT, false, 2>), grid, dim3(kQThreads), 0, s, A);
+      else
+        hipLaunchKernelGGL((assign_q8_kernel<FMT, false, 4>), grid, dim3(kQThreads), 0, s, A);
+      if (ng > 1) {
+        const dim3 gp((unsigned)cdiv(P.n, 256));
         hipLaunchKernelGGL(keys_unpack_kernel<FMT == KM_SQ8>, gp, dim3(256), 0, s, cp.keys, P.n, assign, score, aoff);
-      } else {
-        hipLaunchKernelGGL(assign_q8_kernel<FMT>, dim3((unsigned)npt), dim3(kQThreads), 0, s, A);
       }
     } else {
       hipLaunchKernelGGL(assign_i8_kernel<FMT>, dim3((unsigned)cdiv(P.n, kT8)), dim3(k8Threads), 0, s, A);
@@ -2103,7 +2119,8 @@ int assign_segment_rows(const Points &P) {
 }
 
 km_status launch_assign_segments(const Points &P, const void *C, const CentroidPrep &cp, const int4 *segs,
-                                 const int2 *tiles, int64_t ntiles, int32_t *assign, float *score, hipStream_t s) {
+                                 const int2 *tiles, int64_t ntiles, int kmax, int32_t *assign, float *score,
+                                 hipStream_t s) {
   if (assign_segment_rows(P) == 0) return KM_EUNSUPPORTED;
   if (ntiles == 0) return KM_OK;
   AssignArgs A{};
@@ -2127,14 +2144,20 @@ km_status launch_assign_segments(const Points &P, const void *C, const CentroidP
     A.ci8 = cp.q;
     A.cild = P.d;
     A.di = P.d;
-    hipLaunchKernelGGL((assign_q8_kernel<KM_SQ8, true>), dim3((unsigned)ntiles), dim3(kQThreads), 0, s, A);
+    if (q8_tile_centroids(kmax) == 128)
+      hipLaunchKernelGGL((assign_q8_kernel<KM_SQ8, true, 2>), dim3((unsigned)ntiles), dim3(kQThreads), 0, s, A);
+    else
+      hipLaunchKernelGGL((assign_q8_kernel<KM_SQ8, true, 4>), dim3((unsigned)ntiles), dim3(kQThreads), 0, s, A);
   } else {  // bfloat16 rows as bytes
     A.pi8 = static_cast<const uint8_t *>(P.data);
     A.pild = 2 * P.ld;
     A.ci8 = reinterpret_cast<const int8_t *>(cp.cb);
     A.cild = 2 * (int64_t)P.d;
     A.di = 2 * P.d;
-    hipLaunchKernelGGL((assign_q8_kernel<KM_BF16, true>), dim3((unsigned)ntiles), dim3(kQThreads), 0, s, A);
+    if (q8_tile_centroids(kmax) == 128)
+      hipLaunchKernelGGL((assign_q8_kernel<KM_BF16, true, 2>), dim3((unsigned)ntiles), dim3(kQThreads), 0, s, A);
+    else
+      hipLaunchKernelGGL((assign_q8_kernel<KM_BF16, true, 4>), dim3((unsigned)ntiles), dim3(kQThreads), 0, s, A);
   }
   KMQ_LAUNCH_CHECK("assign kernel (segments)");
   return KM_OK;

@@ -79,10 +79,11 @@ size_t prep_bytes(const Points &P, int k);
 // [segs[i].z, + segs[i].w) of C and of the prepared constants; workgroup b takes
 // point tile tiles[b].y of segment tiles[b].x (tiles of assign_segment_rows(P) rows;
 // 0 = not supported for these points).  assign and score are indexed by absolute
-// row; centroid indices are absolute.
+// row; centroid indices are absolute.  kmax: the largest segment's centroid count.
 int assign_segment_rows(const Points &P);
 km_status launch_assign_segments(const Points &P, const void *C, const CentroidPrep &cp, const int4 *segs,
-                                 const int2 *tiles, int64_t ntiles, int32_t *assign, float *score, hipStream_t s);
+                                 const int2 *tiles, int64_t ntiles, int kmax, int32_t *assign, float *score,
+                                 hipStream_t s);
 km_status launch_assign(const Points &P, const void *C, const CentroidPrep &cp, int k, int32_t *assign,
                         float *score, hipStream_t s, int aoff = 0);
 // cp restricted to centroids [off, ...) and, for the per-point keys, to points [pstart, ...)
