@@ -175,7 +175,8 @@ def sign1_inputs(n, d, k, seed, d0=0):
 # d > 1280 takes the 256 x 256 int8 kernel instead of the resident-bits one
 @pytest.mark.parametrize("n,d,k", [(1, 32, 1), (5, 64, 3), (300, 96, 3), (1000, 128, 64), (2049, 256, 130),
                                    (517, 1024, 257), (700, 160, 129), (130, 64, 300), (700, 64, 600),
-                                   (300, 1536, 70), (700, 2048, 300), (1, 1312, 3)])
+                                   (300, 1536, 70), (700, 2048, 300), (1, 1312, 3), (600, 1152, 140),
+                                   (300, 1280, 70)])
 def test_assign_sign1_bit_exact(km, torch, n, d, k):
     say(f"assign sign1 n={n} d={d} k={k}")
     X, m, bits, alpha, C = sign1_inputs(n, d, k, seed=n + d + k)

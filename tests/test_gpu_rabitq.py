@@ -77,7 +77,7 @@ def pick(n, k, seed):
 # d <= 1280 runs the resident-bits kernel, d > 1280 the 256 x 256 int8 kernel
 @pytest.mark.parametrize("n,d,k", [(1, 32, 1), (5, 64, 3), (300, 96, 3), (1000, 128, 64), (2049, 256, 130),
                                    (517, 1024, 257), (130, 64, 300), (700, 64, 600), (300, 1536, 70),
-                                   (700, 2048, 300)])
+                                   (700, 2048, 300), (600, 1152, 140), (300, 1280, 70)])
 def test_assign_rabitq_bit_exact(km, torch, n, d, k):
     say(f"assign rabitq n={n} d={d} k={k}")
     X = blobs(n, d, max(2, k), seed=n + d + k)
