@@ -979,8 +979,10 @@ __global__ __launch_bounds__(k8Threads, 1) void assign_i8_kernel(AssignArgs A) {
 // stream through LDS in stages of 128 centroids x 128 bytes, copied by direct
 // global-to-LDS loads (no register staging): each load instruction of a wave fills
 // 64 consecutive 16-byte slots, and the lane that fills slot p of row R fetches
-// chunk p ^ (R & 7) of that row, so chunk c sits in slot c ^ (R & 7) and the 8 lanes
-// of one MFMA operand read hit 8 different bank groups.  Every wave multiplies its
+// chunk p ^ ((R >> 1) & 7) of that row, so chunk c sits in slot c ^ ((R >> 1) & 7):
+// the 16 lanes that an LDS cycle serves read 16 rows, and each half of them (even and
+// odd rows, 64 banks apart by the 128-byte row) hits 8 different slots, so an MFMA
+// operand read has no bank conflicts.  Every wave multiplies its
 // 64 points by all 128 centroids of the tile (4 x 2 blocks of 32 x 32 x 32), so no
 // cross-wave merge is needed.
 //
@@ -1085,7 +1087,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void assign_bits_kernel(AssignArgs
   for (int i = 0; i < CPT; ++i) {
     const int slot = (i * NW + wave) * 64 + lane;
     const int row = slot >> 3;
-    coff[i] = (uint32_t)(row * (int)A.cild + 16 * ((slot & 7) ^ (row & 7)));
+    coff[i] = (uint32_t)(row * (int)A.cild + 16 * ((slot & 7) ^ ((row >> 1) & 7)));
   }
   float cpv[4] = {0.f, 0.f, 0.f, 0.f};
   auto load = [&](int ct, int s, uint8_t *dst) {
@@ -1109,7 +1111,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void assign_bits_kernel(AssignArgs
       for (int i = 0; i < CPT; ++i) {
         const int slot = (i * NW + wave) * 64 + lane;
         const int row = slot >> 3;
-        const int b = kRowBytes * s + 16 * ((slot & 7) ^ (row & 7));
+        const int b = kRowBytes * s + 16 * ((slot & 7) ^ ((row >> 1) & 7));
         lds_copy16(cbase + (uint32_t)(min(row, crmax) * (int)A.cild + (b < A.di ? b : 0)),
                    (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t *)(dst + (i * NW + wave) * 1024));
       }
@@ -1166,7 +1168,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void assign_bits_kernel(AssignArgs
 #pragma unroll
       for (int cb = 0; cb < 4; ++cb) {
         const uint4 av =
-            *reinterpret_cast<const uint4 *>(buf + (cb * 32 + r) * kRowBytes + 16 * ((2 * g + h) ^ (r & 7)));
+            *reinterpret_cast<const uint4 *>(buf + (cb * 32 + r) * kRowBytes + 16 * ((2 * g + h) ^ ((r >> 1) & 7)));
         const i32x4 a4 = {(int)av.x, (int)av.y, (int)av.z, (int)av.w};
 #pragma unroll
         for (int pb = 0; pb < 2; ++pb) {
@@ -1262,8 +1264,8 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void assign_bits_kernel(AssignArgs
 // traffic moved off the vector units: every stage (256 centroid rows and 256 point
 // rows of 128 bytes) is copied straight from global memory into LDS, 16 bytes per
 // lane, with the XOR slot layout of the 1-bit kernel (chunk c of row R in slot
-// c ^ (R & 7)), so nothing passes through registers and the MFMA operand reads are
-// free of bank conflicts.  SQ8 centroid codes arrive already recentred to int8
+// c ^ ((R >> 1) & 7)), so nothing passes through registers and the MFMA operand
+// reads are free of bank conflicts.  SQ8 centroid codes arrive already recentred to int8
 // (code - 128, written by the centroid preparation); the point codes are recentred
 // in registers after the LDS read (one XOR per register).  Chunks past the last
 // dimension are zero-filled by ordinary LDS stores from the lanes that skip their
@@ -1343,7 +1345,7 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
   for (int i = 0; i < NCOPY; ++i) {
     const int slot = (i * 8 + wave) * 64 + lane;
     const int row = slot >> 3;
-    const int chunk = (slot & 7) ^ (row & 7);
+    const int chunk = (slot & 7) ^ ((row >> 1) & 7);
     soff[i] = i < NCC ? (uint32_t)(row * (int)A.cild + 16 * chunk)
                       : (uint32_t)(min(row - TC, prmax) * (int)A.pild + 16 * chunk);
   }
@@ -1362,7 +1364,7 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
     for (int i = 0; i < NCOPY; ++i) {
       const int slot = (i * 8 + wave) * 64 + lane;
       const int row = slot >> 3;
-      const int chunk = (slot & 7) ^ (row & 7);
+      const int chunk = (slot & 7) ^ ((row >> 1) & 7);
       uint32_t off = soff[i];
       if (i < NCC && crmax < TC - 1) off = (uint32_t)(min(row, crmax) * (int)A.cild + 16 * chunk);
       const void *base = i < NCC ? (const void *)cbase : (const void *)psrc;
@@ -1391,7 +1393,7 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
     constexpr bool kFirst = decltype(first)::value;
     uint4 av[1][CB], bv[1][k8PB];
     auto read = [&](int g, int slot) {
-      const int so = 16 * ((2 * g + h) ^ (r & 7));
+      const int so = 16 * ((2 * g + h) ^ ((r >> 1) & 7));
 #pragma unroll
       for (int pb = 0; pb < k8PB; ++pb)
         bv[slot][pb] = *reinterpret_cast<const uint4 *>(buf + (TC + wp * 32 * k8PB + pb * 32 + r) * kRowBytes + so);
