@@ -1280,10 +1280,21 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void assign_bits_kernel(AssignArgs
 constexpr int kQT = 256;                            // points per workgroup (and centroids per tile, CB = 4)
 constexpr int kQThreads = 512;                      // 8 waves
 constexpr int kQMaxDimSQ8 = 8192;                   // |2<x~,c~> - ||c~||^2| < 2^31
+constexpr int kQPackMaxDim = 1024;                  // SQ8 packed selection keys (below)
 
 // CB: 32 x 32 centroid blocks per wave, 4 (256-centroid tiles) or 2 (128-centroid
 // tiles, for k <= 128, where a 256-centroid tile would be mostly padding)
-template <int FMT, bool SEG = false, int CB = 4>
+//
+// PK (SQ8 with d <= kQPackMaxDim): the key 2<x~,c~> - ||c~||^2 of every code pair
+// lies in [-48896 d, 16384 d] (codes in [-128, 127]: the key is ||x~||^2 - ||x~ - c~||^2),
+// so key + 16256 d lies within +-32640 d < 2^25 and leaves the low 6 bits of an int32
+// for a row id that is unique among the 64 rows one lane scans per tile.  The
+// centroid constant of a row becomes E = ((-||c~||^2 + 16256 d) << 6) + 63 - id, and
+// the packed key of a pair, ((2<x~,c~> - ||c~||^2 + 16256 d) << 6) + 63 - id =
+// (acc << 7) + E (modulo 2^32, exact since the result is in range), orders pairs by
+// key and then by the smaller id: one shift-add and one max per pair select the
+// tile's winner instead of a compare and two selects.
+template <int FMT, bool SEG = false, int CB = 4, bool PK = false>
 __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) {
   constexpr bool BF = FMT == KM_BF16;
   static_assert(CB == 2 || CB == 4, "128- or 256-centroid tiles");
@@ -1308,6 +1319,7 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
     A.ngroups = 1;
   }
   static_assert(FMT == KM_SQ8 || FMT == KM_BF16, "SQ8 or bf16 points");
+  static_assert(!PK || FMT == KM_SQ8, "packed keys are integer keys");
   // SQ8 maximises the key 2D - ||c~||^2 (= -score, exact in int32); bf16 minimises
   // the score ||c||^2 - 2<x,c> (fp32)
   typedef typename std::conditional<BF, float, int>::type key_t;
@@ -1334,6 +1346,7 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
   const int total = nmy * S;
   const int prmax = (int)min<int64_t>(A.n - 1 - p0, TP - 1);
   const uint8_t *pbase = A.pi8 + p0 * A.pild;
+  const int pk_off = PK ? 16256 * A.di : 0;  // recentres the packed keys
 
   // copy i (0 .. NCOPY - 1) of a wave fills slots (8 i + wave) 64 .. + 63 of the
   // stage: rows 0 .. TC - 1 are centroids, the next TP rows points.  A lane's source is the stage's first
@@ -1356,6 +1369,11 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
     if (s == 0 && t < TC) {
       const int j = c0 + min(t, crmax);
       cpv = BF ? A.cp.cn[j] : __int_as_float(A.cp.qsum[j]);  // SQ8: -||c~||^2
+      if constexpr (PK) {
+        const int rr = t & (32 * CB - 1);  // row within the wave's centroid half
+        const int id = (rr >> 5) * 16 + ((rr >> 3) & 3) * 4 + (rr & 3);
+        cpv = __int_as_float((int)(((uint32_t)(A.cp.qsum[j] + pk_off) << 6) + (uint32_t)(63 - id)));
+      }
     }
     const int8_t *cbase = A.ci8 + (int64_t)c0 * A.cild + kRowBytes * s;
     const uint8_t *psrc = pbase + kRowBytes * s;
@@ -1442,6 +1460,33 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
   // constant here
   auto epilogue = [&](int ct) {
     const float *cp = cparl[ct & 1];
+    if constexpr (PK) {
+      int tk[k8PB] = {INT_MIN, INT_MIN};  // the tile's best packed key per point block
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb) {
+#pragma unroll
+        for (int i4 = 0; i4 < 4; ++i4) {
+          const f32x4 e4 = *reinterpret_cast<const f32x4 *>(cp + wc * 32 * CB + cb * 32 + 8 * i4 + 4 * h);
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+#pragma unroll
+            for (int pb = 0; pb < k8PB; ++pb)
+              tk[pb] = max(tk[pb], (int)(((uint32_t)acc[cb][pb][4 * i4 + e] << 7) + (uint32_t)__float_as_int(e4[e])));
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      // tiles ascend, so the strict comparison keeps the earlier tile on ties
+#pragma unroll
+      for (int pb = 0; pb < k8PB; ++pb) {
+        const int ks = tk[pb] >> 6;  // key + 16256 d
+        if (ks > best[pb]) {
+          const int id = 63 - (tk[pb] & 63);
+          best[pb] = ks;
+          bidx[pb] = (g + ct * NG) * TC + wc * 32 * CB + (id >> 4) * 32 + ((id >> 2) & 3) * 8 + 4 * h + (id & 3);
+        }
+      }
+      return;
+    }
     int loc[k8PB] = {-1, -1};
     // one 32-row block at a time (a scheduling barrier per block keeps the compiler
     // from loading every constant and accumulator at once); constants 4 at a time
@@ -1503,6 +1548,10 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
   for (int it = 0; it < total; it += 2) {
     step(it, qst0, qst1);
     if (it + 1 < total) step(it + 1, qst1, qst0);
+  }
+  if constexpr (PK) {
+#pragma unroll
+    for (int pb = 0; pb < k8PB; ++pb) best[pb] -= pk_off;  // back to 2<x~,c~> - ||c~||^2
   }
 
   // merges in the key order (SQ8: exact integers), smaller index on ties; the
@@ -1996,10 +2045,18 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
         hipLaunchKernelGGL(keys_init_kernel, gp, dim3(256), 0, s, cp.keys, P.n);
       }
       const dim3 grid((unsigned)(ng > 1 ? cdiv(npt, 8) * 8 * ng : npt));
-      if (q8_tile_centroids(k) == 128)
-        hipLaunchKernelGGL((assign_q8_kernel<FMT, false, 2>), grid, dim3(kQThreads), 0, s, A);
-      else
-        hipLaunchKernelGGL((assign_q8_kernel<FMT, false, 4>), grid, dim3(kQThreads), 0, s, A);
+      const bool pk = FMT == KM_SQ8 && P.d <= kQPackMaxDim;
+      if (q8_tile_centroids(k) == 128) {
+        if (pk)
+          hipLaunchKernelGGL((assign_q8_kernel<FMT, false, 2, FMT == KM_SQ8>), grid, dim3(kQThreads), 0, s, A);
+        else
+          hipLaunchKernelGGL((assign_q8_kernel<FMT, false, 2>), grid, dim3(kQThreads), 0, s, A);
+      } else {
+        if (pk)
+          hipLaunchKernelGGL((assign_q8_kernel<FMT, false, 4, FMT == KM_SQ8>), grid, dim3(kQThreads), 0, s, A);
+        else
+          hipLaunchKernelGGL((assign_q8_kernel<FMT, false, 4>), grid, dim3(kQThreads), 0, s, A);
+      }
       if (ng > 1) {
         const dim3 gp((unsigned)cdiv(P.n, 256));
         hipLaunchKernelGGL(keys_unpack_kernel<FMT == KM_SQ8>, gp, dim3(256), 0, s, cp.keys, P.n, assign, score, aoff);
@@ -2146,10 +2203,19 @@ km_status launch_assign_segments(const Points &P, const void *C, const CentroidP
     A.ci8 = cp.q;
     A.cild = P.d;
     A.di = P.d;
-    if (q8_tile_centroids(kmax) == 128)
-      hipLaunchKernelGGL((assign_q8_kernel<KM_SQ8, true, 2>), dim3((unsigned)ntiles), dim3(kQThreads), 0, s, A);
-    else
-      hipLaunchKernelGGL((assign_q8_kernel<KM_SQ8, true, 4>), dim3((unsigned)ntiles), dim3(kQThreads), 0, s, A);
+    const dim3 grid((unsigned)ntiles);
+    const bool pk = P.d <= kQPackMaxDim;
+    if (q8_tile_centroids(kmax) == 128) {
+      if (pk)
+        hipLaunchKernelGGL((assign_q8_kernel<KM_SQ8, true, 2, true>), grid, dim3(kQThreads), 0, s, A);
+      else
+        hipLaunchKernelGGL((assign_q8_kernel<KM_SQ8, true, 2>), grid, dim3(kQThreads), 0, s, A);
+    } else {
+      if (pk)
+        hipLaunchKernelGGL((assign_q8_kernel<KM_SQ8, true, 4, true>), grid, dim3(kQThreads), 0, s, A);
+      else
+        hipLaunchKernelGGL((assign_q8_kernel<KM_SQ8, true, 4>), grid, dim3(kQThreads), 0, s, A);
+    }
   } else {  // bfloat16 rows as bytes
     A.pi8 = static_cast<const uint8_t *>(P.data);
     A.pild = 2 * P.ld;

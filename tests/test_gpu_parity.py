@@ -163,6 +163,35 @@ def test_assign_sq8_bit_exact(km, torch, n, d, k):
         assert abs(host(obj)[0] - dist_o.sum()) <= 2 ** -23 * dist_o.sum()
 
 
+# Codes at the ends of the range reach the extremes of the SQ8 key 2<x~,c~> - ||c~||^2
+# (-48896 d with x~ = 127, c~ = -128; 16384 d with x~ = c~ = -128).  d <= 1024 selects
+# with packed 32-bit keys whose range holds exactly at 1024 dimensions (1008: a partial
+# last stage); 1040 and 1104 take the unpacked selection; 128-centroid tiles for
+# k = 100, 256-centroid tiles merged across groups for k = 700.
+@pytest.mark.parametrize("n,d,k", [(600, 1024, 100), (1500, 1024, 700), (777, 1008, 300), (400, 1040, 260),
+                                   (300, 1104, 90)])
+def test_assign_sq8_extreme_codes(km, torch, n, d, k):
+    say(f"assign sq8 extreme codes n={n} d={d} k={k}")
+    rng = np.random.default_rng(n + d + k)
+    codes = rng.choice(np.array([0, 255], np.uint8), size=(n, d))
+    codes[0::7] = 255
+    codes[1::7] = 0
+    codes[2::7, : d // 2] = 0
+    C = rng.choice(np.array([0, 255], np.uint8), size=(k, d))
+    C[0::5] = 0
+    C[1::5] = 255
+    C[2::5] = codes[3]           # exact matches and ties
+    C[3::5, d // 3:] = 0
+    C[k - 1] = C[2]
+    a_o, dist_o = orc.assign_sq8(codes, C)
+    a, sc, _ = km.kmeans_assign(km.points_sq8(to_dev(codes, torch)), to_dev(C, torch), score=True)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(a), a_o)
+    xt = codes.astype(np.int64) - 128
+    exp = dist_o - (xt * xt).sum(1)
+    np.testing.assert_array_equal(host(sc), exp.astype(np.float32))
+
+
 def sign1_inputs(n, d, k, seed, d0=0):
     X = blobs(n, d, max(2, k), seed=seed, sigma=0.4, normalize=True)
     m = orc.col_mean(X)
