@@ -56,7 +56,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "Lloyd iters/s + point×centroid distances/s; objective ratio vs fp32 oracle"
 PEAK = {"fp32_mfma_tflops": 157.3, "bf16_mfma_tflops": 2500.0, "int8_mfma_tops": 5000.0, "hbm_gbs": 8000.0}
-COUNTERS = os.path.join(ROOT, "profiles", "counters__assign_kernel_fp32__gmm1m_d768_k1000.md")
+COUNTERS = os.path.join(ROOT, "profiles", "counters__assign_f32_kernel__gmm1m_d768_k1000.md")
 KERNEL_SOURCES = ("paper_2608_14648_amd/csrc/assign.hip", "paper_2608_14648_amd/csrc/common.hpp")
 COPY_PROBE_FLOATS = 256 << 20  # 1 GiB of fp32
 
@@ -205,7 +205,7 @@ def workload_c2(cfg, torch, km, args):
             "distances_per_s": 2 * (T + 1) * spec.n * k * K / elapsed,
             "objective_ratio_sq8_vs_f32": c8 / c32,
             "partition_cost": {"f32": c32, "sq8": c8},
-            "roofline": {"bound": "mfma", "kernel": "assign_kernel<fp32>", "achieved": achieved,
+            "roofline": {"bound": "mfma", "kernel": "assign_f32_kernel", "achieved": achieved,
                          "peak": PEAK["fp32_mfma_tflops"], "unit": "TFLOP/s",
                          "frac": achieved / PEAK["fp32_mfma_tflops"],
                          "traffic": counted_traffic(cfg["name"]) if args.n is None else None,
@@ -382,7 +382,7 @@ def workload_hier(cfg, torch, km, args):
                 "ms_per_fit": {"f32": float(res["ph32"].sum()), "sq8": float(res["ph8"].sum())},
                 "phase_ms": {"f32": {"meso": res["ph32"][0], "fine": res["ph32"][1]},
                              "sq8": {"meso": res["ph8"][0], "fine": res["ph8"][1]}},
-                "roofline": {"bound": "mfma", "kernel": "assign_kernel<fp32> (meso launches and segmented fine launches)",
+                "roofline": {"bound": "mfma", "kernel": "assign_f32_kernel (meso launches and segmented fine launches)",
                              "achieved": ach, "peak": PEAK["fp32_mfma_tflops"], "unit": "TFLOP/s",
                              "frac": ach / PEAK["fp32_mfma_tflops"], "traffic": None,
                              "algorithmic_flop_per_fit": flop / K},
@@ -602,7 +602,7 @@ def workload_pca(cfg, torch, km, args):
         return {"value": T * K / elapsed, "unit": "Lloyd iters/s", "dtype": "f32",
                 "config": {"workload": cfg["name"], "N": spec.n, "d": spec.d, "d_out": dout, "k": k, "iters": T},
                 "distances_per_s": (T + 1) * spec.n * k * K / elapsed,
-                "roofline": {"bound": "mfma", "kernel": "assign_kernel<fp32>", "achieved": ach,
+                "roofline": {"bound": "mfma", "kernel": "assign_f32_kernel", "achieved": ach,
                              "peak": PEAK["fp32_mfma_tflops"], "unit": "TFLOP/s",
                              "frac": ach / PEAK["fp32_mfma_tflops"], "traffic": None, "avg_launch_ms": a_ms},
                 "stages": {"pca": stage_summary(s)}}

@@ -538,16 +538,15 @@ static km_status fine_impl(const Points &p, const int32_t *meso, int k_meso, int
   const int seg_rows = assign_segment_rows(p);
   std::vector<int4> segs;
   std::vector<int2> tiles;
-  int kmax = 0;
   if (seg_rows > 0) {
     for (int i = 0; i < k_meso; ++i) {
       if (n_i[i] == 0) continue;
-      kmax = std::max(kmax, kf[i]);
       const int si = (int)segs.size();
       segs.push_back(make_int4((int)start[i], (int)n_i[i], (int)off[i], kf[i]));
       for (int64_t tt = 0; tt * seg_rows < n_i[i]; ++tt) tiles.push_back(make_int2(si, (int)tt));
     }
   }
+  const int tile_c = segs.empty() ? 256 : segment_tile_centroids(segs.data(), (int)segs.size(), seg_rows);
   const size_t b_segs = al(sizeof(int4) * segs.size());
   const size_t b_tiles = al(sizeof(int2) * tiles.size());
   Scratch ws(s);
@@ -582,7 +581,7 @@ static km_status fine_impl(const Points &p, const int32_t *meso, int k_meso, int
     st = clk.begin(kStAssign);
     if (st != KM_OK) return st;
     if (!segs.empty()) {  // every meso-cluster against its own fine centroids, one launch
-      st = launch_assign_segments(q, C, cp, dsegs, dtiles, (int64_t)tiles.size(), kmax, ap, sc, s);
+      st = launch_assign_segments(q, C, cp, dsegs, dtiles, (int64_t)tiles.size(), tile_c, ap, sc, s);
       if (st != KM_OK) return st;
     }
     for (int i = 0; seg_rows == 0 && i < k_meso; ++i) {  // the same, one launch per meso-cluster

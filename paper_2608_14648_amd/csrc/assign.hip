@@ -359,27 +359,10 @@ struct Blocking {
   static constexpr int MINB = 2;
 };
 
-template <int FMT, bool SEG = false>
-__global__ __launch_bounds__(kThreads, Blocking<FMT>::MINB) void assign_kernel(AssignArgs A0) {
+template <int FMT>
+__global__ __launch_bounds__(kThreads, Blocking<FMT>::MINB) void assign_kernel(AssignArgs A) {
   constexpr int CB = Blocking<FMT>::CB, PB = Blocking<FMT>::PB;
   typedef Geo<CB, PB> G;
-  // a segmented launch narrows the arguments to this workgroup's segment
-  AssignArgs A = A0;
-  int64_t seg_p0 = 0;  // first row of this workgroup's point tile (segmented launch)
-  if constexpr (SEG) {
-    const int2 ts = A0.tiles[blockIdx.x];
-    const int4 sg = A0.segs[ts.x];
-    seg_p0 = (int64_t)sg.x + (int64_t)ts.y * G::TP;
-    A.n = (int64_t)sg.x + sg.y;
-    A.k = sg.w;
-    A.cf = A0.cf + (int64_t)sg.z * A0.cfld;
-    A.cp.cn = A0.cp.cn + sg.z;
-    A.cp.qsum = A0.cp.qsum + sg.z;
-    A.cp.u = A0.cp.u + sg.z;
-    A.cp.sig2 = A0.cp.sig2 + sg.z;
-    A.aoff = A0.aoff + sg.z;
-    A.ngroups = 1;
-  }
   __shared__ __align__(16) uint8_t lds[2 * G::STAGE];
   __shared__ __align__(16) float cparl[2][4 * G::TC];
   typedef typename std::conditional<Cfg<FMT>::kIntScore, int, float>::type score_t;
@@ -401,7 +384,7 @@ __global__ __launch_bounds__(kThreads, Blocking<FMT>::MINB) void assign_kernel(A
     g = (int)(l % NG);
     if (pt >= A.n_ptiles) return;  // whole workgroup, before any barrier
   }
-  const int64_t p0 = SEG ? seg_p0 : pt * G::TP;
+  const int64_t p0 = pt * G::TP;
 
   const int SF = Cfg<FMT>::kFp ? (A.df + 31) / 32 : 0;
   const int SI = Cfg<FMT>::kInt ? (A.di + kRowBytes - 1) / kRowBytes : 0;
@@ -1601,6 +1584,262 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
   }
 }
 
+// ---- fp32 assignment with direct global-to-LDS stages -------------------------
+// The SQ8 / bf16 kernel's workgroup shape on fp32 rows: 8 waves, a 256-point tile
+// against centroid tiles of TC = 64 CB (256, or 128 when k <= 128), each wave
+// CB x 2 blocks of v_mfma_f32_32x32x2_f32 (128 centroids x 64 points for CB = 4),
+// stages of 32 dimensions (128 bytes of every row) copied straight from global
+// memory into LDS in the conflict-free slot layout (chunk c of row R in slot
+// c ^ ((R >> 1) & 7)), two stage buffers, one workgroup per CU.  Per flop it moves
+// half the stage bytes of a 128 x 128 tile, and moving stage bytes (by any route)
+// is what costs matrix-core time here.  The copies of stage it+1 are spread over
+// stage it's four 8-dimension steps, between the operand reads (double-buffered)
+// and the MFMAs; full stages take a branch-free path, and in the last, partial
+// stage of a tile the lanes whose chunk lies past the dimensions store zeros
+// instead of copying (rows hold d % 4 == 0 floats, so a chunk is wholly in or out).
+// Rows past the last centroid read the last centroid's row (clamped) with an
+// infinite norm, so they never win.  Groups (ngroups > 1) and the per-point merge
+// are those of the other kernels: (score, index) keys through a 64-bit atomicMin.
+template <bool SEG = false, int CB = 4>
+__global__ __launch_bounds__(kQThreads, 1) void assign_f32_kernel(AssignArgs A0) {
+  static_assert(CB == 2 || CB == 4, "128- or 256-centroid tiles");
+  constexpr int TC = 64 * CB, TP = kQT, PB = k8PB;
+  constexpr int NCC = TC / 64;           // centroid copies per thread and stage
+  constexpr int NCOPY = (TC + TP) / 64;  // all copies per thread and stage
+  constexpr int STAGE = (TC + TP) * kRowBytes;
+  AssignArgs A = A0;
+  int64_t seg_p0 = 0;  // first row of this workgroup's point tile (segmented launch)
+  if constexpr (SEG) {
+    const int2 ts = A0.tiles[blockIdx.x];
+    const int4 sg = A0.segs[ts.x];
+    seg_p0 = (int64_t)sg.x + (int64_t)ts.y * TP;
+    A.n = (int64_t)sg.x + sg.y;
+    A.k = sg.w;
+    A.cf = A0.cf + (int64_t)sg.z * A0.cfld;
+    A.cp.cn = A0.cp.cn + sg.z;
+    A.aoff = A0.aoff + sg.z;
+    A.ngroups = 1;
+  }
+  __shared__ __align__(16) uint8_t fst0[STAGE];
+  __shared__ __align__(16) uint8_t fst1[STAGE];
+  __shared__ __align__(16) float cnl[2][TC];
+  const int t = threadIdx.x;
+  const int lane = t & 63, wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int r = lane & 31, h = lane >> 5;
+  const int wc = wave & 1, wp = wave >> 1;
+  const int NG = A.ngroups;
+  int64_t pt = blockIdx.x;
+  int g = 0;
+  if (NG > 1) {
+    const int64_t l = blockIdx.x >> 3;
+    pt = (l / NG) * 8 + (blockIdx.x & 7);
+    g = (int)(l % NG);
+    if (pt >= A.n_ptiles) return;  // whole workgroup, before any barrier
+  }
+  const int64_t p0 = SEG ? seg_p0 : pt * TP;
+  const int S = (A.df + 31) / 32;
+  const int nct = (A.k + TC - 1) / TC;
+  const int nmy = (nct - g + NG - 1) / NG;  // centroid tiles of this workgroup (>= 1: NG <= nct)
+  const int total = nmy * S;
+  const int prmax = (int)min<int64_t>(A.n - 1 - p0, TP - 1);
+  const float *pbase = A.pf + p0 * A.pfld;
+
+  // copy i of a wave fills slots (8 i + wave) 64 .. + 63 of the stage: rows 0 .. TC - 1
+  // are centroids, the next TP rows points.  Byte offsets from the stage's first
+  // float: point rows clamped into the data once, centroid rows of a full tile here
+  // and of a last, partial tile at copy time.
+  uint32_t soff[NCOPY];
+#pragma unroll
+  for (int i = 0; i < NCOPY; ++i) {
+    const int slot = (i * 8 + wave) * 64 + lane;
+    const int row = slot >> 3;
+    const int chunk = (slot & 7) ^ ((row >> 1) & 7);
+    soff[i] = i < NCC ? (uint32_t)(row * (int)A.cfld * 4 + 16 * chunk)
+                      : (uint32_t)(min(row - TC, prmax) * (int)A.pfld * 4 + 16 * chunk);
+  }
+  // the stage being copied: tile c0, stage cs, into buffer cdst
+  int c0c = 0, crmax = 0, cs = 0;
+  bool cfull = true;
+  uint8_t *cdst = fst0;
+  float cnv = 0.f;  // the next tile's norm for row t, stored once the copies have landed
+  auto begin_copies = [&](int ct, int s, uint8_t *dst) {
+    c0c = (g + ct * NG) * TC;
+    crmax = min(A.k - 1 - c0c, TC - 1);
+    cs = s;
+    cdst = dst;
+    cfull = 32 * (s + 1) <= A.df;
+    if (s == 0 && t < TC) cnv = t <= crmax ? A.cp.cn[c0c + t] : INFINITY;
+  };
+  auto copy = [&](int i) {
+    const int slot = (i * 8 + wave) * 64 + lane;
+    const int row = slot >> 3;
+    const int chunk = (slot & 7) ^ ((row >> 1) & 7);
+    uint32_t off = soff[i];
+    if (i < NCC && crmax < TC - 1) off = (uint32_t)(min(row, crmax) * (int)A.cfld * 4 + 16 * chunk);
+    const void *base = i < NCC ? (const void *)(A.cf + (int64_t)c0c * A.cfld + 32 * cs) : (const void *)(pbase + 32 * cs);
+    lds_u8 *wdst = (lds_u8 *)cdst + (i * 8 + wave) * 1024;
+    if (cfull) {
+      lds_copy16(base, off, (uint32_t)(size_t)wdst);
+    } else if (32 * cs + 4 * chunk < A.df) {
+      lds_copy16(base, off, (uint32_t)(size_t)wdst);
+    } else {
+      __attribute__((address_space(3))) uint32_t *z = (__attribute__((address_space(3))) uint32_t *)(wdst + 16 * lane);
+      z[0] = z[1] = z[2] = z[3] = 0u;
+    }
+  };
+  auto land = [&](int ct, int s) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    if (s == 0 && t < TC) cnl[ct & 1][t] = cnv;
+  };
+
+  f32x16 acc[CB][PB];
+  // one stage: four steps of 8 dimensions (4 k-pairs per MFMA block); the operand
+  // reads of step gg+1 and the copies of the next stage go out before step gg's MFMAs
+  auto mfma_stage = [&](const uint8_t *buf, bool copying) {
+    uint4 av[2][CB], bv[2][PB];
+    auto read = [&](int gg, int set) {
+      const int so = 16 * ((2 * gg + h) ^ ((r >> 1) & 7));
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb)
+        bv[set][pb] = *reinterpret_cast<const uint4 *>(buf + (TC + wp * 32 * PB + pb * 32 + r) * kRowBytes + so);
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb)
+        av[set][cb] = *reinterpret_cast<const uint4 *>(buf + (wc * 32 * CB + cb * 32 + r) * kRowBytes + so);
+    };
+    read(0, 0);
+#pragma unroll
+    for (int gg = 0; gg < 4; ++gg) {
+      const int cur = gg & 1;
+      if (gg + 1 < 4) read(gg + 1, cur ^ 1);
+      __builtin_amdgcn_sched_barrier(0);
+      if (copying) {
+#pragma unroll
+        for (int i = gg * NCOPY / 4; i < (gg + 1) * NCOPY / 4; ++i) copy(i);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+          for (int pb = 0; pb < PB; ++pb)
+            acc[cb][pb] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(av[cur][cb][e]),
+                                                              __uint_as_float(bv[cur][pb][e]), acc[cb][pb], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  // scores ||c||^2 - 2<x,c> and running argmin, lane-local and branch-free; rows
+  // ascend with (cb, i) in a lane, so the strict comparison keeps the smallest
+  // index among equal scores
+  float best[PB];
+  int bidx[PB];
+#pragma unroll
+  for (int pb = 0; pb < PB; ++pb) {
+    best[pb] = INFINITY;
+    bidx[pb] = INT_MAX;
+  }
+  auto epilogue = [&](int ct) {
+    const float *cp = cnl[ct & 1];
+    const int c0 = (g + ct * NG) * TC;
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) {
+      const int crow0 = wc * 32 * CB + cb * 32 + 4 * h;
+#pragma unroll
+      for (int i4 = 0; i4 < 4; ++i4) {
+        const f32x4 cn4 = *reinterpret_cast<const f32x4 *>(&cp[crow0 + 8 * i4]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int j = c0 + crow0 + 8 * i4 + e;
+#pragma unroll
+          for (int pb = 0; pb < PB; ++pb) {
+            const float sc = fmaf(-2.0f, acc[cb][pb][4 * i4 + e], cn4[e]);
+            const bool take = sc < best[pb];
+            best[pb] = take ? sc : best[pb];
+            bidx[pb] = take ? j : bidx[pb];
+          }
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  begin_copies(0, 0, fst0);
+#pragma unroll
+  for (int i = 0; i < NCOPY; ++i) copy(i);
+  land(0, 0);
+  __syncthreads();
+  auto step = [&](int it, const uint8_t *cur, uint8_t *nxt) {
+    const int ct = it / S, s = it - ct * S;
+    const bool has_next = it + 1 < total;
+    const int s_n = (s + 1 == S) ? 0 : s + 1;
+    const int ct_n = (s + 1 == S) ? ct + 1 : ct;
+    if (s == 0) {
+#pragma unroll
+      for (int a = 0; a < CB; ++a)
+#pragma unroll
+        for (int b = 0; b < PB; ++b)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) acc[a][b][i] = 0.f;
+    }
+    if (has_next) begin_copies(ct_n, s_n, nxt);
+    mfma_stage(cur, has_next);
+    if (has_next) land(ct_n, s_n);
+    __syncthreads();
+    if (s == S - 1) {
+      epilogue(ct);
+      // the next tile's steps write tile ct + 2's norms into cnl[ct & 1]
+      __syncthreads();
+    }
+  };
+  for (int it = 0; it < total; it += 2) {
+    step(it, fst0, fst1);
+    if (it + 1 < total) step(it + 1, fst1, fst0);
+  }
+
+  // merge the two lane halves (rows 4h..), then the two centroid halves
+#pragma unroll
+  for (int pb = 0; pb < PB; ++pb) {
+    const float os = __shfl_xor(best[pb], 32);
+    const int oi = __shfl_xor(bidx[pb], 32);
+    if (os < best[pb] || (os == best[pb] && oi < bidx[pb])) {
+      best[pb] = os;
+      bidx[pb] = oi;
+    }
+  }
+  float *ms = reinterpret_cast<float *>(fst0);
+  int *mi = reinterpret_cast<int *>(fst0 + TP * sizeof(float));
+  if (wc == 1 && h == 0) {
+#pragma unroll
+    for (int pb = 0; pb < PB; ++pb) {
+      ms[wp * 32 * PB + pb * 32 + r] = best[pb];
+      mi[wp * 32 * PB + pb * 32 + r] = bidx[pb];
+    }
+  }
+  __syncthreads();
+  if (wc == 0 && h == 0) {
+#pragma unroll
+    for (int pb = 0; pb < PB; ++pb) {
+      const int pc = wp * 32 * PB + pb * 32 + r;
+      const float os = ms[pc];
+      const int oi = mi[pc];
+      if (os < best[pb] || (os == best[pb] && oi < bidx[pb])) {
+        best[pb] = os;
+        bidx[pb] = oi;
+      }
+      const int64_t p = p0 + pc;
+      if (p < A.n) {
+        if (A.keys) {
+          atomicMin(A.keys + p, score_key(best[pb], bidx[pb]));
+        } else {
+          A.assign[p] = bidx[pb] + A.aoff;
+          if (A.score) A.score[p] = best[pb];
+        }
+      }
+    }
+  }
+}
+
 // ---- centroid preparation: one workgroup per centroid ----------------------
 
 template <int FMT>
@@ -1949,13 +2188,34 @@ __global__ __launch_bounds__(256) void cost_kernel(const float *X, int64_t n, in
 
 constexpr int kObjBlocks = 1024;
 
-// Centroid-tile groups of the fp32 kernel: up to 8 workgroups share a point tile,
-// each scanning every 8th centroid tile.
+// Centroid-tile groups of the hybrid kernel: up to 8 workgroups share a point
+// tile, each scanning every 8th centroid tile.
 // centroid-tile groups of the SQ8 / bf16 kernel: only to fill the GPU (two
 // workgroups per CU) when the point tiles alone do not; shared point reads give
 // no measurable gain at a million points
-// centroids per tile of the SQ8 / bf16 kernel: 128 when k fits, else 256
+// centroids per tile of the 8-wave kernels (fp32, SQ8, bf16): 128 when k fits, else 256
 static int q8_tile_centroids(int k) { return k <= 128 ? 128 : 256; }
+
+// Centroid-tile groups of the fp32 kernel (one workgroup per CU, long-lived
+// workgroups): the group count g that minimises the rounds of workgroups over the
+// CUs times the centroid tiles of the busiest group, ceil(npt g / CUs) ceil(nct / g),
+// i.e. the partly filled last round (1M points: 3907 point tiles = 15.3 rounds
+// alone, 30.5 with g = 2); the smallest such g, since each group adds a key merge.
+static int f32_groups(int64_t n, int k) {
+  const int64_t npt = cdiv(n, kQT);
+  const int nct = (int)cdiv(k, q8_tile_centroids(k));
+  const int64_t cus = cu_count();
+  int best_g = 1;
+  int64_t best = -1;
+  for (int g = 1; g <= std::min(8, nct); ++g) {
+    const int64_t cost = cdiv(npt * g, cus) * cdiv(nct, g);
+    if (best < 0 || cost < best) {
+      best = cost;
+      best_g = g;
+    }
+  }
+  return best_g;
+}
 
 static int q8_groups(int64_t n, int k) {
   const int64_t npt = cdiv(n, kQT);
@@ -1964,7 +2224,8 @@ static int q8_groups(int64_t n, int k) {
 }
 
 int assign_groups(const Points &P, int k) {
-  if (P.fmt == KM_F32 || P.fmt == KM_HYBRID) {
+  if (P.fmt == KM_F32) return f32_groups(P.n, k);
+  if (P.fmt == KM_HYBRID) {
     constexpr int TC = Geo<Blocking<KM_F32>::CB, Blocking<KM_F32>::PB>::TC;
     return (int)std::min<int64_t>(8, cdiv(k, TC));
   }
@@ -2066,6 +2327,25 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
     }
   } else if constexpr (FMT == KM_LVQ4) {
     hipLaunchKernelGGL(assign_i8_kernel<FMT>, dim3((unsigned)cdiv(P.n, kT8)), dim3(k8Threads), 0, s, A);
+  } else if constexpr (FMT == KM_F32) {
+    const int64_t npt = cdiv(P.n, kQT);
+    const int ng = assign_groups(P, k);
+    A.n_ptiles = npt;
+    if (ng > 1) {
+      const dim3 gp((unsigned)cdiv(P.n, 256));
+      A.ngroups = ng;
+      A.keys = cp.keys;
+      hipLaunchKernelGGL(keys_init_kernel, gp, dim3(256), 0, s, cp.keys, P.n);
+    }
+    const dim3 grid((unsigned)(ng > 1 ? cdiv(npt, 8) * 8 * ng : npt));
+    if (q8_tile_centroids(k) == 128)
+      hipLaunchKernelGGL((assign_f32_kernel<false, 2>), grid, dim3(kQThreads), 0, s, A);
+    else
+      hipLaunchKernelGGL((assign_f32_kernel<false, 4>), grid, dim3(kQThreads), 0, s, A);
+    if (ng > 1) {
+      const dim3 gp((unsigned)cdiv(P.n, 256));
+      hipLaunchKernelGGL(keys_unpack_kernel<false>, gp, dim3(256), 0, s, cp.keys, P.n, assign, score, aoff);
+    }
   } else {
     constexpr int TP = Geo<Blocking<FMT>::CB, Blocking<FMT>::PB>::TP;
     const int64_t npt = cdiv(P.n, TP);
@@ -2171,14 +2451,24 @@ km_status launch_assign(const Points &P, const void *C, const CentroidPrep &cp, 
   }
 }
 
+int segment_tile_centroids(const int4 *segs, int nseg, int seg_rows) {
+  int64_t w128 = 0, w256 = 0;
+  for (int i = 0; i < nseg; ++i) {
+    const int64_t nt = cdiv(segs[i].y, seg_rows);
+    w128 += nt * cdiv(segs[i].w, 128) * 128;
+    w256 += nt * cdiv(segs[i].w, 256) * 256;
+  }
+  return w128 < w256 ? 128 : 256;
+}
+
 int assign_segment_rows(const Points &P) {
-  if (P.fmt == KM_F32) return Geo<Blocking<KM_F32>::CB, Blocking<KM_F32>::PB>::TP;
+  if (P.fmt == KM_F32) return kQT;
   if (P.fmt == KM_BF16 || (P.fmt == KM_SQ8 && P.d <= kQMaxDimSQ8)) return kQT;
   return 0;
 }
 
 km_status launch_assign_segments(const Points &P, const void *C, const CentroidPrep &cp, const int4 *segs,
-                                 const int2 *tiles, int64_t ntiles, int kmax, int32_t *assign, float *score,
+                                 const int2 *tiles, int64_t ntiles, int tile_c, int32_t *assign, float *score,
                                  hipStream_t s) {
   if (assign_segment_rows(P) == 0) return KM_EUNSUPPORTED;
   if (ntiles == 0) return KM_OK;
@@ -2196,7 +2486,10 @@ km_status launch_assign_segments(const Points &P, const void *C, const CentroidP
     A.cf = static_cast<const float *>(C);
     A.cfld = P.d;
     A.df = P.d;
-    hipLaunchKernelGGL((assign_kernel<KM_F32, true>), dim3((unsigned)ntiles), dim3(kThreads), 0, s, A);
+    if (tile_c == 128)
+      hipLaunchKernelGGL((assign_f32_kernel<true, 2>), dim3((unsigned)ntiles), dim3(kQThreads), 0, s, A);
+    else
+      hipLaunchKernelGGL((assign_f32_kernel<true, 4>), dim3((unsigned)ntiles), dim3(kQThreads), 0, s, A);
   } else if (P.fmt == KM_SQ8) {  // recentred centroid codes from the preparation
     A.pi8 = static_cast<const uint8_t *>(P.data);
     A.pild = P.ld;
@@ -2205,7 +2498,7 @@ km_status launch_assign_segments(const Points &P, const void *C, const CentroidP
     A.di = P.d;
     const dim3 grid((unsigned)ntiles);
     const bool pk = P.d <= kQPackMaxDim;
-    if (q8_tile_centroids(kmax) == 128) {
+    if (tile_c == 128) {
       if (pk)
         hipLaunchKernelGGL((assign_q8_kernel<KM_SQ8, true, 2, true>), grid, dim3(kQThreads), 0, s, A);
       else
@@ -2222,7 +2515,7 @@ km_status launch_assign_segments(const Points &P, const void *C, const CentroidP
     A.ci8 = reinterpret_cast<const int8_t *>(cp.cb);
     A.cild = 2 * (int64_t)P.d;
     A.di = 2 * P.d;
-    if (q8_tile_centroids(kmax) == 128)
+    if (tile_c == 128)
       hipLaunchKernelGGL((assign_q8_kernel<KM_BF16, true, 2>), dim3((unsigned)ntiles), dim3(kQThreads), 0, s, A);
     else
       hipLaunchKernelGGL((assign_q8_kernel<KM_BF16, true, 4>), dim3((unsigned)ntiles), dim3(kQThreads), 0, s, A);

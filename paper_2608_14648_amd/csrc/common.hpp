@@ -69,6 +69,9 @@ __host__ __device__ static inline int64_t cdiv(int64_t a, int64_t b) { return (a
 
 // ---- launchers implemented in the kernel sources ---------------------------
 
+// pca.hip: compute units of the current device (256 if the query fails)
+int cu_count();
+
 // assign.hip
 km_status launch_prep(const Points &P, const void *C, int k, void *ws_prep, CentroidPrep *out,
                       hipStream_t s);
@@ -79,10 +82,14 @@ size_t prep_bytes(const Points &P, int k);
 // [segs[i].z, + segs[i].w) of C and of the prepared constants; workgroup b takes
 // point tile tiles[b].y of segment tiles[b].x (tiles of assign_segment_rows(P) rows;
 // 0 = not supported for these points).  assign and score are indexed by absolute
-// row; centroid indices are absolute.  kmax: the largest segment's centroid count.
+// row; centroid indices are absolute.  tile_c: centroids per tile (128 or 256), from
+// segment_tile_centroids over the host copy of segs.
 int assign_segment_rows(const Points &P);
+// 128 or 256: the tile size with the smaller padded work, the sum over segments of
+// point tiles x centroid rows rounded up to the tile (256 on ties)
+int segment_tile_centroids(const int4 *segs, int nseg, int seg_rows);
 km_status launch_assign_segments(const Points &P, const void *C, const CentroidPrep &cp, const int4 *segs,
-                                 const int2 *tiles, int64_t ntiles, int kmax, int32_t *assign, float *score,
+                                 const int2 *tiles, int64_t ntiles, int tile_c, int32_t *assign, float *score,
                                  hipStream_t s);
 km_status launch_assign(const Points &P, const void *C, const CentroidPrep &cp, int k, int32_t *assign,
                         float *score, hipStream_t s, int aoff = 0);

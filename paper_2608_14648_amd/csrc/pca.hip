@@ -269,19 +269,6 @@ struct CovPlan {
   int64_t rows_per_split;
 };
 
-int cu_count() {
-  static int cus = 0;
-  if (cus == 0) {
-    int dev = 0, v = 0;
-    if (hipGetDevice(&dev) == hipSuccess && hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
-        v > 0)
-      cus = v;
-    else
-      cus = 256;
-  }
-  return cus;
-}
-
 // One covariance workgroup fills a CU (LDS), so the number of (tile, split)
 // workgroups is kept just under a whole number of passes over the CUs.
 CovPlan cov_plan(int64_t n, int d) {
@@ -298,6 +285,19 @@ CovPlan cov_plan(int64_t n, int d) {
 }
 
 }  // namespace
+
+int cu_count() {
+  static int cus = 0;
+  if (cus == 0) {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) == hipSuccess && hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        v > 0)
+      cus = v;
+    else
+      cus = 256;
+  }
+  return cus;
+}
 
 size_t pca_cov_bytes(int64_t n, int d) {
   const CovPlan p = cov_plan(n, d);
