@@ -2190,18 +2190,16 @@ constexpr int kObjBlocks = 1024;
 
 // Centroid-tile groups of the hybrid kernel: up to 8 workgroups share a point
 // tile, each scanning every 8th centroid tile.
-// centroid-tile groups of the SQ8 / bf16 kernel: only to fill the GPU (two
-// workgroups per CU) when the point tiles alone do not; shared point reads give
-// no measurable gain at a million points
 // centroids per tile of the 8-wave kernels (fp32, SQ8, bf16): 128 when k fits, else 256
 static int q8_tile_centroids(int k) { return k <= 128 ? 128 : 256; }
 
-// Centroid-tile groups of the fp32 kernel (one workgroup per CU, long-lived
+// Centroid-tile groups of the 8-wave kernels (one workgroup per CU, long-lived
 // workgroups): the group count g that minimises the rounds of workgroups over the
-// CUs times the centroid tiles of the busiest group, ceil(npt g / CUs) ceil(nct / g),
-// i.e. the partly filled last round (1M points: 3907 point tiles = 15.3 rounds
-// alone, 30.5 with g = 2); the smallest such g, since each group adds a key merge.
-static int f32_groups(int64_t n, int k) {
+// CUs times the centroid tiles of the busiest group, ceil(npt g / CUs) ceil(nct / g).
+// This fills the GPU when the point tiles alone do not, and shortens the partly
+// filled last round (1M points: 3907 point tiles = 15.3 rounds alone, 30.5 with
+// g = 2); the smallest such g, since each group adds a key merge.
+static int tile_groups(int64_t n, int k) {
   const int64_t npt = cdiv(n, kQT);
   const int nct = (int)cdiv(k, q8_tile_centroids(k));
   const int64_t cus = cu_count();
@@ -2217,19 +2215,13 @@ static int f32_groups(int64_t n, int k) {
   return best_g;
 }
 
-static int q8_groups(int64_t n, int k) {
-  const int64_t npt = cdiv(n, kQT);
-  return (int)std::min<int64_t>(std::min<int64_t>(8, cdiv(k, q8_tile_centroids(k))),
-                                std::max<int64_t>(1, cdiv(2 * 256, npt)));
-}
-
 int assign_groups(const Points &P, int k) {
-  if (P.fmt == KM_F32) return f32_groups(P.n, k);
+  if (P.fmt == KM_F32) return tile_groups(P.n, k);
   if (P.fmt == KM_HYBRID) {
     constexpr int TC = Geo<Blocking<KM_F32>::CB, Blocking<KM_F32>::PB>::TC;
     return (int)std::min<int64_t>(8, cdiv(k, TC));
   }
-  if (P.fmt == KM_BF16 || (P.fmt == KM_SQ8 && P.d <= kQMaxDimSQ8)) return q8_groups(P.n, k);
+  if (P.fmt == KM_BF16 || (P.fmt == KM_SQ8 && P.d <= kQMaxDimSQ8)) return tile_groups(P.n, k);
   return 1;
 }
 
