@@ -165,17 +165,38 @@ __global__ __launch_bounds__(256) void bf16_encode_kernel(const float *X, int64_
 // LVQ4: one wave per row.  Pass 1: the row's min and max (float4 per lane, wave
 // reductions); pass 2: codes, two per byte, and the exact sums S and Q of the codes;
 // lane 0 writes (s, b, A, N) with the fp32 expressions of the format definition.
+// NV > 0: rows of at most 256 NV dims stay in registers between the passes (NV
+// float4 per lane, all loads in flight at once), so a row is read once; NV = 0
+// reads it again for pass 2.
+template <int NV>
 __global__ __launch_bounds__(256) void lvq4_encode_kernel(const float *X, int64_t n, int d, int64_t ldx,
                                                           uint8_t *codes, float *par) {
   const int lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= n) return;
   const float *x = X + row * ldx;
+  constexpr int R = NV > 0 ? NV : 1;
+  f32x4 v[R];
   float lo = INFINITY, hi = -INFINITY;
-  for (int i = 4 * lane; i < d; i += 256) {
-    const f32x4 v = *reinterpret_cast<const f32x4 *>(x + i);
-    lo = fminf(fminf(lo, v[0]), fminf(fminf(v[1], v[2]), v[3]));
-    hi = fmaxf(fmaxf(hi, v[0]), fmaxf(fmaxf(v[1], v[2]), v[3]));
+  if constexpr (NV > 0) {
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      const int i = 4 * lane + 256 * j;  // d % 32 == 0: a float4 is wholly in or out
+      v[j] = i < d ? *reinterpret_cast<const f32x4 *>(x + i) : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      if (4 * lane + 256 * j < d) {
+        lo = fminf(fminf(lo, v[j][0]), fminf(fminf(v[j][1], v[j][2]), v[j][3]));
+        hi = fmaxf(fmaxf(hi, v[j][0]), fmaxf(fmaxf(v[j][1], v[j][2]), v[j][3]));
+      }
+    }
+  } else {
+    for (int i = 4 * lane; i < d; i += 256) {
+      const f32x4 w = *reinterpret_cast<const f32x4 *>(x + i);
+      lo = fminf(fminf(lo, w[0]), fminf(fminf(w[1], w[2]), w[3]));
+      hi = fmaxf(fmaxf(hi, w[0]), fmaxf(fmaxf(w[1], w[2]), w[3]));
+    }
   }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) {
@@ -185,16 +206,22 @@ __global__ __launch_bounds__(256) void lvq4_encode_kernel(const float *X, int64_
   const float s = hi > lo ? (hi - lo) / 15.0f : 1.0f;
   int S = 0, Q = 0;
   uint8_t *out = codes + row * (int64_t)(d / 2);
-  for (int i = 4 * lane; i < d; i += 256) {  // d % 32 == 0: a float4 is wholly in or out
-    const f32x4 v = *reinterpret_cast<const f32x4 *>(x + i);
+  auto encode4 = [&](const f32x4 &w, int i) {
     int c[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      c[e] = (int)fminf(fmaxf(rintf((v[e] - lo) / s), 0.0f), 15.0f);
+      c[e] = (int)fminf(fmaxf(rintf((w[e] - lo) / s), 0.0f), 15.0f);
       S += c[e];
       Q += c[e] * c[e];
     }
     *reinterpret_cast<uint16_t *>(out + i / 2) = (uint16_t)(c[0] | (c[1] << 4) | (c[2] << 8) | (c[3] << 12));
+  };
+  if constexpr (NV > 0) {
+#pragma unroll
+    for (int j = 0; j < NV; ++j)
+      if (4 * lane + 256 * j < d) encode4(v[j], 4 * lane + 256 * j);
+  } else {
+    for (int i = 4 * lane; i < d; i += 256) encode4(*reinterpret_cast<const f32x4 *>(x + i), i);
   }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) {
@@ -338,8 +365,14 @@ km_status launch_quantize(const float *X, int64_t n, int d, int64_t ldx, int fmt
     return KM_OK;
   }
   if (fmt == KM_LVQ4) {
-    hipLaunchKernelGGL(lvq4_encode_kernel, dim3((unsigned)cdiv(n, 4)), dim3(256), 0, s, X, n, d, ldx,
-                       static_cast<uint8_t *>(codes), params);
+    const dim3 g((unsigned)cdiv(n, 4));
+    uint8_t *c8 = static_cast<uint8_t *>(codes);
+    if (d <= 1024)
+      hipLaunchKernelGGL(lvq4_encode_kernel<4>, g, dim3(256), 0, s, X, n, d, ldx, c8, params);
+    else if (d <= 2048)
+      hipLaunchKernelGGL(lvq4_encode_kernel<8>, g, dim3(256), 0, s, X, n, d, ldx, c8, params);
+    else
+      hipLaunchKernelGGL(lvq4_encode_kernel<0>, g, dim3(256), 0, s, X, n, d, ldx, c8, params);
     KMQ_LAUNCH_CHECK("quantize lvq4");
     return KM_OK;
   }

@@ -47,7 +47,10 @@ def encode(X):
     return codes, orc.lvq4_pack(codes), par
 
 
-@pytest.mark.parametrize("n,d", [(1, 32), (3, 64), (1000, 128), (3001, 768), (257, 1536)])
+# rows of up to 1024 and 2048 dims stay in registers between the two passes (the
+# limits: 1024, 2048); 2080 reads the row twice
+@pytest.mark.parametrize("n,d", [(1, 32), (3, 64), (1000, 128), (3001, 768), (200, 1024), (257, 1536), (100, 2048),
+                                 (60, 2080)])
 def test_quantize_lvq4_bit_exact(km, torch, n, d):
     say(f"quantize lvq4 n={n} d={d}")
     X = blobs(n, d, 5, seed=n + d, normalize=False)
