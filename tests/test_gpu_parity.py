@@ -220,8 +220,11 @@ def test_assign_sign1_bit_exact(km, torch, n, d, k):
     assert abs(host(obj)[0] - dist_o.sum()) <= 1e-5 * dist_o.sum() + 1e-6
 
 
+# (700, 256, 128, 300): one tail stage; (300, 1280, 512, 1100): a 768-dim tail and
+# centroid-tile groups
 @pytest.mark.parametrize("n,d,d0,k", [(300, 64, 32, 3), (1000, 128, 32, 64), (2049, 256, 96, 130),
-                                      (517, 1024, 384, 257), (50, 96, 64, 7), (600, 128, 32, 1100)])
+                                      (517, 1024, 384, 257), (700, 256, 128, 300), (1000, 384, 128, 64),
+                                      (300, 1280, 512, 1100), (50, 96, 64, 7), (600, 128, 32, 1100)])
 def test_assign_hybrid(km, torch, n, d, d0, k):
     say(f"assign hybrid n={n} d={d} d0={d0} k={k}")
     X, m, bits, alpha, C = sign1_inputs(n, d, k, seed=n + d + k + d0, d0=d0)
