@@ -1346,10 +1346,11 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
                       : (uint32_t)(min(row - TC, prmax) * (int)A.pild + 16 * chunk);
   }
   float cpv = 0.f;
-  auto load = [&](int ct, int s, uint8_t *dst) {
+  // the next stage's tile constant for row t (loaded with its tile's first stage)
+  auto load_constant = [&](int ct) {
     const int c0 = (g + ct * NG) * TC;
     const int crmax = min(A.k - 1 - c0, TC - 1);
-    if (s == 0 && t < TC) {
+    if (t < TC) {
       const int j = c0 + min(t, crmax);
       cpv = BF ? A.cp.cn[j] : __int_as_float(A.cp.qsum[j]);  // SQ8: -||c~||^2
       if constexpr (PK) {
@@ -1358,33 +1359,48 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
         cpv = __int_as_float((int)(((uint32_t)(A.cp.qsum[j] + pk_off) << 6) + (uint32_t)(63 - id)));
       }
     }
+  };
+  // copy i of stage s of tile ct into buffer dst
+  auto load_one = [&](int ct, int s, uint8_t *dst, int i) {
+    const int c0 = (g + ct * NG) * TC;
+    const int crmax = min(A.k - 1 - c0, TC - 1);
     const int8_t *cbase = A.ci8 + (int64_t)c0 * A.cild + kRowBytes * s;
     const uint8_t *psrc = pbase + kRowBytes * s;
     const bool full_stage = kRowBytes * (s + 1) <= A.di;
-#pragma unroll
-    for (int i = 0; i < NCOPY; ++i) {
-      const int slot = (i * 8 + wave) * 64 + lane;
-      const int row = slot >> 3;
-      const int chunk = (slot & 7) ^ ((row >> 1) & 7);
-      uint32_t off = soff[i];
-      if (i < NCC && crmax < TC - 1) off = (uint32_t)(min(row, crmax) * (int)A.cild + 16 * chunk);
-      const void *base = i < NCC ? (const void *)cbase : (const void *)psrc;
-      lds_u8 *wdst = (lds_u8 *)dst + (i * 8 + wave) * 1024;
-      const uint32_t lds = (uint32_t)(size_t)wdst;
-      if (full_stage) {
-        lds_copy16(base, off, lds);
-      } else if (kRowBytes * s + 16 * chunk < A.di) {
-        lds_copy16(base, off, lds);
-      } else {
-        __attribute__((address_space(3))) uint32_t *z = (__attribute__((address_space(3))) uint32_t *)(wdst + 16 * lane);
-        z[0] = z[1] = z[2] = z[3] = 0u;
-      }
+    const int slot = (i * 8 + wave) * 64 + lane;
+    const int row = slot >> 3;
+    const int chunk = (slot & 7) ^ ((row >> 1) & 7);
+    uint32_t off = soff[i];
+    if (i < NCC && crmax < TC - 1) off = (uint32_t)(min(row, crmax) * (int)A.cild + 16 * chunk);
+    const void *base = i < NCC ? (const void *)cbase : (const void *)psrc;
+    lds_u8 *wdst = (lds_u8 *)dst + (i * 8 + wave) * 1024;
+    const uint32_t lds = (uint32_t)(size_t)wdst;
+    if (full_stage) {
+      lds_copy16(base, off, lds);
+    } else if (kRowBytes * s + 16 * chunk < A.di) {
+      lds_copy16(base, off, lds);
+    } else {
+      __attribute__((address_space(3))) uint32_t *z = (__attribute__((address_space(3))) uint32_t *)(wdst + 16 * lane);
+      z[0] = z[1] = z[2] = z[3] = 0u;
     }
+  };
+  auto load = [&](int ct, int s, uint8_t *dst) {
+    if (s == 0) load_constant(ct);
+#pragma unroll
+    for (int i = 0; i < NCOPY; ++i) load_one(ct, s, dst, i);
   };
   auto store = [&](int ct, int s) {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     if (s == 0 && t < TC) cparl[ct & 1][t] = cpv;
   };
+
+  // SQ8 with packed keys spreads the next stage's copies over the stage's four
+  // steps (5 % faster at 1M x 768); the instances with more live registers (bf16,
+  // unpacked SQ8) issue them all before the MFMAs, as spreading them there spills
+  constexpr bool SPREAD = PK;
+  int sp_ct = 0, sp_s = 0;
+  uint8_t *sp_dst = nullptr;
+  bool sp_on = false;
 
   Acc8<BF> acc[CB][k8PB];
   // one stage of 4 steps of 32 dimensions; a scheduling barrier per step keeps the
@@ -1406,6 +1422,10 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
     for (int g = 0; g < 4; ++g) {
       constexpr int cur = 0;
       read(g, 0);
+      if (SPREAD && sp_on) {
+#pragma unroll
+        for (int i = g * NCOPY / 4; i < (g + 1) * NCOPY / 4; ++i) load_one(sp_ct, sp_s, sp_dst, i);
+      }
 #pragma unroll
       for (int cb = 0; cb < CB; ++cb)
 #pragma unroll
@@ -1515,7 +1535,15 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
     const bool has_next = it + 1 < total;
     const int s_n = (s + 1 == S) ? 0 : s + 1;
     const int ct_n = (s + 1 == S) ? ct + 1 : ct;
-    if (has_next) load(ct_n, s_n, nxt);
+    if constexpr (SPREAD) {
+      sp_on = has_next;
+      sp_ct = ct_n;
+      sp_s = s_n;
+      sp_dst = nxt;
+      if (has_next && s_n == 0) load_constant(ct_n);
+    } else {
+      if (has_next) load(ct_n, s_n, nxt);
+    }
     if (s == 0)
       mfma_stage(cur, std::true_type{});
     else
