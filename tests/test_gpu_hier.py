@@ -218,6 +218,25 @@ def test_fine_fp_formats_lockstep(km, torch, fmt, d):
     assert compared >= 2
 
 
+def test_fine_f32_large_segments(km, torch):
+    """Meso-clusters of ~200 fine centroids (128 < k_i <= 256): the segmented launch
+    takes 256-centroid tiles.  From the oracle's STEP-1 centroids, the fine
+    assignment within the fp tolerance and its objective within OBJ_REL."""
+    n, d, k_meso, k = 6000, 64, 4, 800
+    X = blobs(n, d, 24, seed=31)
+    Po, Pg = formats(km, torch, "f32", X)
+    am = meso_labels(n, k_meso, seed=32)
+    amd = to_dev(am, torch)
+    C0_o, _, kf_o, _ = orc.fit_fine(Po, am, k_meso, k, 0)
+    assert all(128 < kf_o[i] <= 256 for i in range(k_meso))
+    _, a_o, _, J_o = orc.fit_fine(Po, am, k_meso, k, 0, C0=C0_o)
+    _, a, kf, obj = km.kmeans_fine(Pg, amd, k_meso, k, 0, C=to_dev(C0_o, torch), objective=True)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(kf, kf_o)
+    assert_fp_assign(host(a), a_o, fp_d_of("f32", Po, C0_o), "f32 large segments")
+    assert abs(host(obj)[0] - J_o[-1]) <= OBJ_REL * abs(J_o[-1])
+
+
 def test_hier_pipeline_is_its_phases(km, torch):
     """kmeans_fit_hier equals, bit for bit, its phases called one by one (kmeans_fit for
     MESO, kmeans_fine, kmeans_fit from the fine centroids for REFINE); the fine phase
