@@ -135,10 +135,12 @@ def test_assign_f32_strided_rows(km, torch):
     assert_fp_assign(host(a), a_o, f32_dist(X, C), "f32 strided")
 
 
-# (700, 16, 900): 4 centroid-tile groups merged through exact integer keys;
-# (300, 8208, 20): rows beyond 8192 dims take the register-staged int8 kernel
+# (700, 16, 900): 4 centroid-tile groups merged through exact integer keys; (500, 32, 2100):
+# 9 tiles over 5 groups (uneven); (300, 8208, 20): rows beyond 8192 dims take the
+# register-staged int8 kernel
 @pytest.mark.parametrize("n,d,k", [(1, 16, 1), (5, 16, 3), (300, 32, 3), (1000, 128, 64), (2049, 96, 130),
-                                   (517, 768, 257), (130, 48, 300), (700, 16, 900), (300, 8208, 20)])
+                                   (517, 768, 257), (130, 48, 300), (700, 16, 900), (500, 32, 2100),
+                                   (300, 8208, 20)])
 def test_assign_sq8_bit_exact(km, torch, n, d, k):
     say(f"assign sq8 n={n} d={d} k={k}")
     rng = np.random.default_rng(n * 7 + d + k)
