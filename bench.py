@@ -701,8 +701,9 @@ def main():
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path (the sharding design is "
-              "described in DESIGN.md); run with --gpus 1", file=sys.stderr)
+        print("bench.py measures one GPU only: the library has no multi-GPU path (points would be sharded "
+              "by rows, one shard per GPU, with an all-reduce of the per-cluster sums); run with --gpus 1",
+              file=sys.stderr)
         sys.exit(2)
 
     import torch
