@@ -1395,8 +1395,8 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
   };
 
   // SQ8 with packed keys spreads the next stage's copies over the stage's four
-  // steps (5 % faster at 1M x 768); the instances with more live registers (bf16,
-  // unpacked SQ8) issue them all before the MFMAs, as spreading them there spills
+  // steps (5 % faster at 1M x 768); unpacked SQ8 issues them all before the MFMAs
+  // (spreading them there spills), and so does bf16 (spreading them gained nothing)
   constexpr bool SPREAD = PK;
   int sp_ct = 0, sp_s = 0;
   uint8_t *sp_dst = nullptr;
@@ -1431,11 +1431,11 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
 #pragma unroll
         for (int pb = 0; pb < k8PB; ++pb) {
           Acc8<BF> cin;
-          if (kFirst && g == 0) {
+          if (!BF && kFirst && g == 0) {
 #pragma unroll
             for (int i = 0; i < 16; ++i) cin[i] = 0;
           } else {
-            cin = acc[cb][pb];
+            cin = acc[cb][pb];  // bf16: the tile's seeds -||c||^2 / 2 at its first step
           }
           if constexpr (BF) {
             acc[cb][pb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
@@ -1455,7 +1455,7 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
   int bidx[k8PB];
 #pragma unroll
   for (int pb = 0; pb < k8PB; ++pb) {
-    best[pb] = BF ? (key_t)INFINITY : (key_t)INT_MIN;
+    best[pb] = BF ? (key_t)-INFINITY : (key_t)INT_MIN;
     bidx[pb] = INT_MAX;
   }
   // rows ascend with (cb, i) in a lane, so the strict comparison keeps the smallest
@@ -1505,8 +1505,8 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
 #pragma unroll
           for (int pb = 0; pb < k8PB; ++pb) {
             if constexpr (BF) {
-              const float sc = fmaf(-2.0f, acc[cb][pb][i], cq4[e]);  // ||c||^2 - 2<x,c>
-              if (sc < best[pb]) {
+              const float sc = acc[cb][pb][i];  // <x,c> - ||c||^2 / 2 = -(||c||^2 - 2<x,c>) / 2
+              if (sc > best[pb]) {
                 best[pb] = sc;
                 loc[pb] = cl;
               }
@@ -1544,6 +1544,21 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
     } else {
       if (has_next) load(ct_n, s_n, nxt);
     }
+    if (BF && s == 0) {
+      // bf16: the accumulators start at -||c||^2 / 2 of their row (exact halving),
+      // so they end at <x,c> - ||c||^2 / 2 and the epilogue only keeps the largest
+      const float *cp = cparl[ct & 1];
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+          const f32x4 v = *reinterpret_cast<const f32x4 *>(cp + wc * 32 * CB + cb * 32 + 8 * m + 4 * h);
+#pragma unroll
+          for (int pb = 0; pb < k8PB; ++pb)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc[cb][pb][4 * m + e] = -0.5f * v[e];
+        }
+    }
     if (s == 0)
       mfma_stage(cur, std::true_type{});
     else
@@ -1563,6 +1578,10 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
   if constexpr (PK) {
 #pragma unroll
     for (int pb = 0; pb < k8PB; ++pb) best[pb] -= pk_off;  // back to 2<x~,c~> - ||c~||^2
+  }
+  if constexpr (BF) {
+#pragma unroll
+    for (int pb = 0; pb < k8PB; ++pb) best[pb] = -2.0f * best[pb];  // the score ||c||^2 - 2<x,c>
   }
 
   // merges in the key order (SQ8: exact integers), smaller index on ties; the
