@@ -50,9 +50,12 @@ MUTATIONS = {
     "prune_ties_to_larger": ("if (p < bd || (p == bd && j < best)) {", "if (p < bd || (p == bd && j > best)) {"),
     "prune_first_checkpoint_skipped": ("for (int32_t D = d_front; D < d; D += step) { /* checkpoints */",
                                        "for (int32_t D = d_front + step; D < d; D += step) { /* checkpoints */"),
+    "hybrid_front_row_stride_d": ("(double)front[r * d0 + i]", "(double)front[r * d + i]"),
+    "hybrid_front_adds_m": ("C[(int64_t)j * d + i] = i < d0 ? Z[(int64_t)j * d + i] : m[i] + Z[(int64_t)j * d + i];",
+                            "C[(int64_t)j * d + i] = m[i] + Z[(int64_t)j * d + i];"),
 }
 
-# mistakes in the Python driver (hierarchical k-means)
+# mistakes in the Python driver (hierarchical k-means, hybrid initialisation and update)
 PY_MUTATIONS = {
     "fine_init_first_members": ("(np.arange(k_i, dtype=np.int64) * n_i) // k_i", "np.arange(k_i, dtype=np.int64)"),
     "fine_offsets_without_leading_zero": ("off = np.concatenate([[0], np.cumsum(k_i)])", "off = np.cumsum(k_i)"),
@@ -60,6 +63,10 @@ PY_MUTATIONS = {
     "fine_share_by_n_not_n_minus_1": ("w = v - 1 if v > 0 else 0", "w = v"),
     "refine_skipped": ("    if iters_refine > 0:\n        C, a, Jr", "    if iters_refine > 1:\n        C, a, Jr"),
     "meso_count_floor": ("return max(1, r + 1 if k - r * r > r else r)", "return max(1, r)"),
+    "hybrid_init_front_not_copied": ('C[:, :d0] = P["front"][idx]', "C[:, :d0] = 0.0"),
+    "hybrid_init_tail_without_m": ('C = sign1_decode(P["bits"][idx], P["alpha"][idx], P["d"], P["m"], d0)',
+                                   'C = sign1_decode(P["bits"][idx], P["alpha"][idx], P["d"], np.zeros(P["d"], np.float32), d0)'),
+    "hybrid_update_without_front": ('policy, front=P["front"], d0=P["d0"])', 'policy)'),
 }
 
 PINS = [name for name in dir(pins) if name.startswith("test_")]

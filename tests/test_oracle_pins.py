@@ -431,13 +431,176 @@ def test_update_sign1_bruteforce(orc, n, w, k, seed):
     a = rng.integers(0, k, n).astype(np.int32)
     C0 = rng.standard_normal((k, d)).astype(np.float32)
     C, cnt = orc.update_sign1(bits, alpha, d, m, a, k, C0, orc.EMPTY_KEEP)
-    dec = orc.sign1_decode(bits, alpha, d, m).astype(np.float64)  # m + alpha(2b-1)
+    dec = m.astype(np.float64) + alpha[:, None].astype(np.float64) * (2 * _unpack_bits(bits, d) - 1)  # m + alpha(2b-1)
     for j in range(k):
         if (a == j).any():
             # fused decode-average == average of decoded points (m is common)
             np.testing.assert_allclose(C[j], dec[a == j].mean(0), rtol=1e-5, atol=1e-6)
         else:
             np.testing.assert_array_equal(C[j], C0[j])
+
+
+def _unpack_bits(bits, d):
+    """{0, 1} matrix (n x d) of LSB-first uint32 sign words, by numpy shifts."""
+    n = bits.shape[0]
+    return ((bits[:, :, None] >> np.arange(32, dtype=np.uint32)) & 1).reshape(n, d).astype(np.int64)
+
+
+def _padded_front(front, d):
+    """The front rows (n x d0) as the leading rows of a larger contiguous buffer
+    whose other rows hold 1e6: a read with the row stride of the whole vector
+    stays inside memory and returns values far from every real one."""
+    n, d0 = front.shape
+    buf = np.full((n * (d // d0 + 1) + 1, d0), 1e6, np.float32)
+    buf[:n] = front
+    return buf[:n]
+
+
+def _split_reference(Z, cnt):
+    """Empty-cluster rule (Sec. 2.3 STEP 3 reading): ascending empty j, donor the
+    largest working count (first on ties), halves of the donor's count."""
+    k, d = Z.shape
+    Z = Z.copy()
+    work = cnt.copy()
+    fresh = cnt > 0
+    p = np.where(np.arange(d) % 2 == 0, 1.0, -1.0)
+    for j in range(k):
+        if cnt[j] != 0:
+            continue
+        b = int(np.argmax(work))
+        if work[b] < 2:
+            continue
+        Z[j] = Z[b] * (1.0 + EPS * p)
+        Z[b] = Z[b] * (1.0 - EPS * p)
+        work[j] = work[b] // 2
+        work[b] -= work[j]
+        fresh[j] = True
+    return Z, fresh
+
+
+def _golden_rows(g, part, rows, d, d0):
+    out = np.empty((rows, d), np.float64)
+    even = np.arange(d) % 2 == 0
+    for r in range(rows):
+        out[r, :d0] = np.where(even[:d0], part["front_even"][r], part["front_odd"][r])
+        out[r, d0:] = np.where(even[d0:], part["tail_even"][r], part["tail_odd"][r])
+    return out
+
+
+def _golden_hybrid_inputs(g):
+    d, d0 = g["d"], g["d0"]
+    n = len(g["alpha"])
+    front = np.repeat(np.array(g["front_value"], np.float32)[:, None], d0, axis=1)
+    bits = np.array(g["words"], np.uint32)
+    alpha = np.array(g["alpha"], np.float32)
+    m = np.concatenate([np.full(d0, g["m_front"]), np.full(d - d0, g["m_tail"])]).astype(np.float32)
+    C_old = np.repeat(np.array(g["C_old_value"], np.float32)[:, None], d, axis=1)
+    return n, d, d0, front, bits, alpha, m, C_old
+
+
+def test_update_hybrid_example(orc):
+    g = load_golden("hybrid_update.json")
+    n, d, d0, front, bits, alpha, m, C_old = _golden_hybrid_inputs(g)
+    a = np.array(g["assign"], np.int32)
+    for policy, key in ((orc.EMPTY_KEEP, "keep"), (orc.EMPTY_SPLIT, "split")):
+        C, cnt = orc.update_sign1(bits, alpha, d, m, a, g["k"], C_old, policy,
+                                  front=_padded_front(front, d), d0=d0)
+        np.testing.assert_array_equal(C, _golden_rows(g, g[key], g["k"], d, d0).astype(np.float32), err_msg=key)
+        assert cnt.tolist() == g["counts"]
+
+
+def test_init_hybrid_example(orc):
+    g = load_golden("hybrid_update.json")
+    n, d, d0, front, bits, alpha, m, _ = _golden_hybrid_inputs(g)
+    P = {"fmt": "hybrid", "front": front, "bits": bits, "alpha": alpha, "m": m, "d": d, "d0": d0}
+    C = orc.init_centroids(P, g["init_idx"])
+    np.testing.assert_array_equal(C, _golden_rows(g, g["init"], len(g["init_idx"]), d, d0).astype(np.float32))
+
+
+@settings(max_examples=40, deadline=None)
+@given(n=st.integers(1, 40), shape=st.sampled_from([(64, 32), (128, 32), (416, 384), (448, 384)]),
+       k=st.integers(1, 6), split=st.booleans(), seed=st.integers(0, 2**31 - 1))
+def test_update_hybrid_bruteforce(orc, n, shape, k, split, seed):
+    d, d0 = shape
+    rng = np.random.default_rng(seed)
+    front = rng.standard_normal((n, d0)).astype(np.float32)
+    bits = rng.integers(0, 2**32, (n, d // 32), dtype=np.uint64).astype(np.uint32)
+    alpha = rng.uniform(0.05, 2.0, n).astype(np.float32)
+    m = (rng.standard_normal(d) * 0.5).astype(np.float32)
+    a = rng.integers(0, max(1, k - (seed % 3)), n).astype(np.int32)  # some draws leave clusters empty
+    C0 = rng.standard_normal((k, d)).astype(np.float32)
+    policy = orc.EMPTY_SPLIT if split else orc.EMPTY_KEEP
+    C, cnt = orc.update_sign1(bits, alpha, d, m, a, k, C0, policy, front=_padded_front(front, d), d0=d0)
+    # clustering-space members: front values, and tail residuals alpha (2b - 1)
+    V = np.concatenate([front.astype(np.float64),
+                        alpha[:, None].astype(np.float64) * (2 * _unpack_bits(bits, d)[:, d0:] - 1)], axis=1)
+    counts = np.bincount(a, minlength=k)
+    Z = np.zeros((k, d))
+    for j in range(k):
+        if counts[j]:
+            Z[j] = V[a == j].mean(0)
+    fresh = counts > 0
+    if split:
+        Z, fresh = _split_reference(Z, counts)
+    expect = C0.astype(np.float64).copy()
+    for j in range(k):
+        if fresh[j]:
+            expect[j, :d0] = Z[j, :d0]
+            expect[j, d0:] = m[d0:].astype(np.float64) + Z[j, d0:]
+    np.testing.assert_allclose(C, expect, rtol=1e-6, atol=1e-6)
+    assert cnt.tolist() == counts.tolist()
+
+
+@settings(max_examples=20, deadline=None)
+@given(n=st.integers(1, 30), shape=st.sampled_from([(64, 32), (416, 384)]), seed=st.integers(0, 2**31 - 1))
+def test_init_hybrid_bruteforce(orc, n, shape, seed):
+    d, d0 = shape
+    rng = np.random.default_rng(seed)
+    front = rng.standard_normal((n, d0)).astype(np.float32)
+    bits = rng.integers(0, 2**32, (n, d // 32), dtype=np.uint64).astype(np.uint32)
+    alpha = rng.uniform(0.05, 2.0, n).astype(np.float32)
+    m = (rng.standard_normal(d) * 0.5).astype(np.float32)
+    idx = rng.permutation(n)[: max(1, n // 2)]
+    P = {"fmt": "hybrid", "front": front, "bits": bits, "alpha": alpha, "m": m, "d": d, "d0": d0}
+    C = orc.init_centroids(P, idx)
+    sgn = 2 * _unpack_bits(bits, d)[:, d0:] - 1
+    np.testing.assert_array_equal(C[:, :d0], front[idx])
+    np.testing.assert_allclose(C[:, d0:], m[d0:].astype(np.float64) + alpha[idx, None].astype(np.float64) * sgn[idx],
+                               rtol=1e-7, atol=1e-7)
+
+
+def test_hybrid_fit_with_constant_tail_is_front_lloyd(orc):
+    # every row's tail equals the column mean: residuals are zero, so alpha = 0, the
+    # tail adds nothing to any distance and every centroid's tail stays m; the
+    # hybrid fit is then plain Lloyd on the front dims (numpy, fp64)
+    rng = np.random.default_rng(31)
+    n, d, d0, k, T = 300, 96, 32, 5, 6
+    centers = rng.standard_normal((k, d0)) * 3
+    Xf = (centers[rng.integers(0, k, n)] + rng.standard_normal((n, d0)) * 0.5).astype(np.float32)
+    tail = rng.standard_normal(d - d0).astype(np.float32)
+    X = np.concatenate([Xf, np.repeat(tail[None], n, axis=0)], axis=1)
+    m = orc.col_mean(X)
+    assert np.array_equal(m[d0:], tail)
+    bits, alpha = orc.sign1_encode(X, m, d0)
+    assert (alpha == 0).all()
+    idx = rng.choice(n, k, replace=False)
+    P = {"fmt": "hybrid", "front": _padded_front(Xf, d), "bits": bits, "alpha": alpha, "m": m, "d": d, "d0": d0}
+    C, a, J = orc.fit(P, k, T, idx)
+    Cr = Xf[idx].astype(np.float64)
+    Xd = Xf.astype(np.float64)
+    Jr = []
+    for t in range(T + 1):
+        D = ((Xd[:, None, :] - Cr[None]) ** 2).sum(-1)
+        ar = D.argmin(1)
+        Jr.append(D.min(1).sum())
+        if t < T:
+            for j in range(k):
+                if (ar == j).any():
+                    Cr[j] = Xd[ar == j].mean(0)
+    np.testing.assert_array_equal(a, ar)
+    np.testing.assert_allclose(C[:, :d0], Cr, rtol=1e-5, atol=1e-6)
+    np.testing.assert_array_equal(C[:, d0:], np.repeat(tail[None], k, axis=0))
+    np.testing.assert_allclose(J, Jr, rtol=1e-6)
 
 
 def test_col_mean_and_sq8_fit_special_cases(orc):
