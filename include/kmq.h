@@ -199,6 +199,26 @@ km_status kmeans_assign(const km_points *P, const void *C, int32_t k, int32_t *a
                         double *objective, km_stream stream);
 
 /*
+ * kmeans_assign_noalloc -- kmeans_assign for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation.  Same arguments, checks, kernels and results as kmeans_assign; its
+ * scratch (centroid preparation, the (score, index) keys of the centroid-tile
+ * groups, objective partials) lives in a static device array of 64 MiB that the
+ * library holds on every device it runs on until the process ends, so the call
+ * makes no allocation of any kind.
+ *   KM_EINVAL when the call would need more than 64 MiB of scratch: about
+ *   16 bytes per point with the objective, 8 without (fp32, bfloat16 and SQ8
+ *   points in centroid-tile groups), plus the prepared centroids (k x d bytes for
+ *   SQ8 and the 1-bit formats, 2 k d for bfloat16) and 16 k bytes.
+ *   Every call on one device shares that device's array, which keeps the last
+ *   call's contents: calls that overlap on one device (on different streams, or
+ *   from different threads without ordering) race and give undefined results.
+ *   Calls on different devices do not share it.
+ */
+km_status kmeans_assign_noalloc(const km_points *P, const void *C, int32_t k, int32_t *assign, float *score,
+                                double *objective, km_stream stream);
+
+/*
  * kmeans_update -- STEP 3 (Sec. 2.3): each centroid becomes the mean of its
  * members, in the clustering space:
  *   KM_F32: fp32 mean; KM_BF16: fp32 mean of the stored bfloat16 values;

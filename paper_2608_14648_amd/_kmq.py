@@ -21,7 +21,8 @@ KM_EMPTY_SPLIT, KM_EMPTY_KEEP = 0, 1
 KM_Q_FIT_PARAMS = 1
 KM_FINE_C_GIVEN = 1
 STATUS = {0: "KM_OK", -1: "KM_EINVAL", -2: "KM_EUNSUPPORTED", -3: "KM_ENOMEM", -4: "KM_EDEVICE"}
-EXPORTS = ("quantize", "rabitq_encode", "pca_fit_cov", "pca_project", "kmeans_assign", "kmeans_update",
+EXPORTS = ("quantize", "rabitq_encode", "pca_fit_cov", "pca_project", "kmeans_assign", "kmeans_assign_noalloc",
+           "kmeans_update",
            "kmeans_fit", "kmeans_fine", "kmeans_fit_hier", "kmeans_assign_pruned", "kmeans_fit_pruned", "kmeans_cost",
            "km_last_error", "km_release")
 
@@ -74,6 +75,7 @@ def lib():
             "pca_fit_cov": [vp, i64, i32, vp, vp, vp],
             "pca_project": [vp, i64, i32, vp, vp, i32, vp, vp],
             "kmeans_assign": [ct.POINTER(KmPoints), vp, i32, vp, vp, vp, vp],
+            "kmeans_assign_noalloc": [ct.POINTER(KmPoints), vp, i32, vp, vp, vp, vp],
             "kmeans_update": [ct.POINTER(KmPoints), vp, i32, vp, vp, i32, vp],
             "kmeans_fit": [ct.POINTER(KmPoints), i32, i32, vp, vp, vp, vp, i32, ct.POINTER(KmFitStats), vp],
             "kmeans_fine": [ct.POINTER(KmPoints), vp, i32, i32, i32, i32, vp, vp, vp, vp, i32, vp],
@@ -338,6 +340,24 @@ def kmeans_assign(P: Points, C: torch.Tensor, score: bool = True, objective: boo
     obj = torch.empty(1, dtype=torch.float64, device=P.device) if objective else None
     _check(lib().kmeans_assign(P.ref, _ptr(C), k, _ptr(a), _ptr(sc), _ptr(obj), _stream()))
     return a, sc, obj
+
+
+def kmeans_assign_noalloc(P: Points, C: torch.Tensor, assign: torch.Tensor, score: torch.Tensor | None = None,
+                          objective: torch.Tensor | None = None):
+    """kmeans_assign into caller-given outputs, with the library's static scratch:
+    assign int32[n], score float[n] or None, objective double[1] or None (device
+    tensors).  The library allocates nothing for this call."""
+    k = _check_C(P, C)
+    _dev(assign, torch.int32, "assign", 1)
+    if score is not None:
+        _dev(score, torch.float32, "score", 1)
+    if objective is not None:
+        _dev(objective, torch.float64, "objective", 1)
+    if assign.shape[0] != P.n or (score is not None and score.shape[0] != P.n) or \
+            (objective is not None and objective.shape[0] != 1):
+        raise ValueError("assign and score must hold n values, objective one")
+    _check(lib().kmeans_assign_noalloc(P.ref, _ptr(C), k, _ptr(assign), _ptr(score), _ptr(objective), _stream()))
+    return assign, score, objective
 
 
 def kmeans_update(P: Points, assign: torch.Tensor, C: torch.Tensor, policy: int = KM_EMPTY_SPLIT,

@@ -86,6 +86,30 @@ class Scratch {
 
 static size_t al(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Scratch of kmeans_assign_noalloc: one file-scope array per device, for the
+// life of the process.  Its name is a host-side stand-in in host code; the
+// device address is taken once per device with hipGetSymbolAddress and only
+// that address is handed to kernels.
+constexpr size_t kStaticScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) uint8_t scratch[kStaticScratchBytes];
+
+static km_status static_scratch(uint8_t **out) {
+  static std::mutex mu;
+  static void *addr[64] = {nullptr};
+  int dev = 0;
+  KMQ_HIP(hipGetDevice(&dev));
+  KMQ_CHECK(dev >= 0 && dev < 64, KM_EDEVICE, "device index %d outside [0, 64)", dev);
+  std::lock_guard<std::mutex> g(mu);
+  if (addr[dev] == nullptr) {
+    void *p = nullptr;
+    hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    addr[dev] = p;
+  }
+  *out = static_cast<uint8_t *>(addr[dev]);
+  return KM_OK;
+}
+
 static km_status check_points(const km_points *P, Points *out) {
   KMQ_CHECK(P != nullptr, KM_EINVAL, "points descriptor is NULL");
   const int fmt = P->fmt;
@@ -276,30 +300,44 @@ km_status rabitq_encode(const float *X, int64_t n, int32_t d, int64_t ldx, const
   return launch_rabitq_encode(X, n, d, ldx, P, m, bits, alpha, Y, flags, ws.get(), s);
 }
 
-km_status kmeans_assign(const km_points *P, const void *C, int32_t k, int32_t *assign, float *score,
-                        double *objective, km_stream stream) {
-  g_err[0] = 0;
-  Points p;
-  km_status st = check_points(P, &p);
+}  // extern "C"
+
+namespace kmq {
+// scratch layout of one assignment call: centroid preparation | scores when the
+// caller gives none but wants the objective | point-only terms | objective partials
+struct AssignScratch {
+  size_t b_prep, b_score, b_xc, b_part;
+  size_t total() const { return b_prep + b_score + b_xc + b_part; }
+};
+
+static AssignScratch assign_scratch(const Points &p, int k, const float *score, const double *objective) {
+  AssignScratch a;
+  a.b_prep = al(prep_bytes(p, k));
+  a.b_score = objective != nullptr && score == nullptr ? al(sizeof(float) * (size_t)p.n) : 0;
+  a.b_xc = objective ? al(sizeof(float) * (size_t)p.n) : 0;
+  a.b_part = objective ? al(sizeof(double) * (size_t)objective_blocks(p.n)) : 0;
+  return a;
+}
+
+static km_status check_assign_args(const km_points *P, const void *C, int32_t k, const int32_t *assign, Points *p) {
+  km_status st = check_points(P, p);
   if (st != KM_OK) return st;
-  st = check_centroids(p, C, k);
+  st = check_centroids(*p, C, k);
   if (st != KM_OK) return st;
   KMQ_CHECK(assign != nullptr, KM_EINVAL, "assign is NULL");
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  const size_t b_prep = al(prep_bytes(p, k));
-  const bool need_score = objective != nullptr && score == nullptr;
-  const size_t b_score = need_score ? al(sizeof(float) * (size_t)p.n) : 0;
-  const size_t b_xc = objective ? al(sizeof(float) * (size_t)p.n) : 0;
-  const size_t b_part = objective ? al(sizeof(double) * (size_t)objective_blocks(p.n)) : 0;
-  Scratch ws(s);
-  st = ws.alloc(b_prep + b_score + b_xc + b_part);
-  if (st != KM_OK) return st;
-  uint8_t *w = ws.get();
+  return KM_OK;
+}
+
+// the launches of one assignment call on the scratch at w (layout as above)
+static km_status assign_on(const Points &p, const void *C, int32_t k, int32_t *assign, float *score,
+                           double *objective, const AssignScratch &a, uint8_t *w, hipStream_t s) {
+  const size_t b_prep = a.b_prep, b_score = a.b_score, b_xc = a.b_xc;
+  const bool need_score = b_score != 0;
   float *sc = need_score ? reinterpret_cast<float *>(w + b_prep) : score;
   float *xc = reinterpret_cast<float *>(w + b_prep + b_score);
   double *part = reinterpret_cast<double *>(w + b_prep + b_score + b_xc);
   CentroidPrep cp;
-  st = launch_prep(p, C, k, w, &cp, s);
+  km_status st = launch_prep(p, C, k, w, &cp, s);
   if (st != KM_OK) return st;
   st = launch_assign(p, C, cp, k, assign, sc, s);
   if (st != KM_OK) return st;
@@ -309,6 +347,39 @@ km_status kmeans_assign(const km_points *P, const void *C, int32_t k, int32_t *a
     st = launch_objective(p, xc, sc, p.n, objective, part, objective_blocks(p.n), s);
   }
   return st;
+}
+}  // namespace kmq
+
+extern "C" {
+
+km_status kmeans_assign(const km_points *P, const void *C, int32_t k, int32_t *assign, float *score,
+                        double *objective, km_stream stream) {
+  g_err[0] = 0;
+  Points p;
+  km_status st = check_assign_args(P, C, k, assign, &p);
+  if (st != KM_OK) return st;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const AssignScratch a = assign_scratch(p, k, score, objective);
+  Scratch ws(s);
+  st = ws.alloc(a.total());
+  if (st != KM_OK) return st;
+  return assign_on(p, C, k, assign, score, objective, a, ws.get(), s);
+}
+
+km_status kmeans_assign_noalloc(const km_points *P, const void *C, int32_t k, int32_t *assign, float *score,
+                                double *objective, km_stream stream) {
+  g_err[0] = 0;
+  Points p;
+  km_status st = check_assign_args(P, C, k, assign, &p);
+  if (st != KM_OK) return st;
+  const AssignScratch a = assign_scratch(p, k, score, objective);
+  KMQ_CHECK(a.total() <= kStaticScratchBytes, KM_EINVAL,
+            "kmeans_assign_noalloc needs %zu bytes of scratch for n = %lld, k = %d; its static buffer holds %zu",
+            a.total(), (long long)p.n, k, kStaticScratchBytes);
+  uint8_t *w = nullptr;
+  st = static_scratch(&w);
+  if (st != KM_OK) return st;
+  return assign_on(p, C, k, assign, score, objective, a, w, reinterpret_cast<hipStream_t>(stream));
 }
 
 km_status kmeans_update(const km_points *P, const int32_t *assign, int32_t k, void *C, int64_t *counts, int32_t policy,
