@@ -2,6 +2,7 @@
 // call), stream-ordered scratch memory, and the Lloyd loop of Sec. 2.3.
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
@@ -63,6 +64,13 @@ class Scratch {
     if (p_) (void)hipFreeAsync(p_, s_);
   }
   km_status alloc(size_t bytes) {
+    // KMQ_FAIL_ALLOC=1 makes every scratch allocation fail before any HIP call:
+    // the failure path can be exercised on a machine without a GPU
+    const char *fail = getenv("KMQ_FAIL_ALLOC");
+    if (fail && fail[0] == '1') {
+      set_error("scratch allocation of %zu bytes failed: refused (KMQ_FAIL_ALLOC=1)", bytes);
+      return KM_ENOMEM;
+    }
     km_status st = prepare_pool();
     if (st != KM_OK) return st;
     hipError_t e = hipMallocAsync(&p_, std::max<size_t>(bytes, 256), s_);
@@ -136,6 +144,12 @@ static km_status check_points(const km_points *P, Points *out) {
   p.vparams = P->vparams;
   KMQ_CHECK((fmt == KM_LVQ4) == (P->vparams != nullptr), KM_EINVAL,
             "vparams must be given for LVQ4 points and only for them");
+  if (fmt == KM_F32 || fmt == KM_BF16 || fmt == KM_SQ8 || fmt == KM_LVQ4) {
+    // the assignment kernels address a tile of 256 rows with 32-bit offsets
+    const int64_t elem = fmt == KM_F32 ? 4 : fmt == KM_BF16 ? 2 : 1;
+    KMQ_CHECK(P->ld >= 0 && P->ld <= ((int64_t)1 << 31) / (256 * elem) - 1, KM_EINVAL,
+              "ld = %lld too large: 256 rows of ld elements must span less than 2^31 bytes", (long long)P->ld);
+  }
   if (P->raw) {
     KMQ_CHECK(fmt != KM_SQ8, KM_EINVAL, "raw rows are not allowed for SQ8 points (their centroids are codes)");
     KMQ_CHECK(P->d % 4 == 0 && P->raw_ld >= P->d && P->raw_ld % 4 == 0 && aligned16(P->raw), KM_EINVAL,

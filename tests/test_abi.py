@@ -6,6 +6,7 @@ import ctypes as ct
 import os
 import re
 import subprocess
+import sys
 
 import pytest
 
@@ -97,6 +98,10 @@ FAKE = ct.c_void_p(0x10000)  # never dereferenced: validation fails first
     (dict(fmt=6, d=128, ld=72, vparams=0x6000), -1, "ld % 16"),
     (dict(fmt=6, d=128, ld=64, vparams=0x6000, center=0x3000), -1, "no center"),
     (dict(fmt=6, d=128, ld=64, vparams=0x6004), -1, "vparams must be 16-byte"),
+    (dict(fmt=0, d=128, ld=1 << 21), -1, "too large"),
+    (dict(fmt=1, d=128, ld=1 << 22), -1, "too large"),
+    (dict(fmt=2, d=128, ld=1 << 23), -1, "too large"),
+    (dict(fmt=6, d=128, ld=1 << 23, vparams=0x6000), -1, "too large"),
 ])
 def test_points_validation(kmq, kw, status, msg):
     L = kmq.lib()
@@ -291,3 +296,31 @@ def test_pruned_argument_checks(kmq):
         args[i] = v
         assert L.kmeans_fit_pruned(*args) == -1, msg
         assert msg in L.km_last_error().decode(), (msg, L.km_last_error())
+
+
+def test_allocation_failure_is_reported(kmq):
+    # KMQ_FAIL_ALLOC=1 refuses every scratch allocation before any HIP call; a valid
+    # call then returns KM_ENOMEM with nothing launched (checked in a child process,
+    # since the library reads the variable on every allocation)
+    code = (
+        "import ctypes as ct, sys\n"
+        f"sys.path.insert(0, {ROOT!r})\n"
+        "from paper_2608_14648_amd import _kmq as k\n"
+        "L = k.lib()\n"
+        "P = k.KmPoints(k.KM_F32, 128, 100, ct.c_void_p(0x10000), 128, None, None, None, 0, 0, None, 0, None)\n"
+        "F = ct.c_void_p(0x10000)\n"
+        "st = [L.kmeans_assign(ct.byref(P), F, 4, F, None, None, None),\n"
+        "      L.kmeans_update(ct.byref(P), F, 4, F, None, 0, None),\n"
+        "      L.quantize(F, 100, 128, 128, k.KM_SQ8, F, F, None, 0, None, 1, None),\n"
+        "      L.pca_fit_cov(F, 100, 128, F, F, None)]\n"
+        "print(st, L.km_last_error().decode())\n"
+    )
+    env = dict(os.environ, KMQ_FAIL_ALLOC="1")
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, env=env, timeout=120)
+    assert r.returncode == 0, r.stderr
+    assert r.stdout.startswith("[-3, -3, -3, -3]"), r.stdout
+    assert "KMQ_FAIL_ALLOC" in r.stdout
+    # the noalloc entry point never allocates, so the variable cannot make it fail
+    # that way: it still validates its arguments on the host
+    L = kmq.lib()
+    assert L.kmeans_assign_noalloc(None, FAKE, 4, FAKE, None, None, None) == -1

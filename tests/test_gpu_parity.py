@@ -409,6 +409,11 @@ def test_pca_cov(km, torch, n, d):
     np.testing.assert_array_equal(c, c.T)
     err = np.linalg.norm(c - cov_o) / max(np.linalg.norm(cov_o), 1e-30)
     assert err <= 1e-5, err
+    # entry by entry, each against the scale of its own row and column: a wrong
+    # small off-diagonal entry cannot hide under the diagonal
+    sd = np.sqrt(np.clip(np.diag(cov_o), 0.0, None))
+    bad = np.abs(c - cov_o) > 2e-5 * np.outer(sd, sd) + 1e-12
+    assert not bad.any(), (int(bad.sum()), np.argwhere(bad)[:5].tolist())
 
 
 @pytest.mark.parametrize("n,d,dout", [(1, 4, 4), (5000, 64, 16), (3001, 256, 128), (2000, 1024, 256), (700, 96, 36)])
