@@ -1173,12 +1173,20 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void assign_bits_kernel(AssignArgs
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int cl = cb * 32 + 8 * (i >> 2) + (i & 3);
-        const int crow = cl + 4 * h;
-        const float u = cp[kBTC + crow];
-        const float s2 = cp[2 * kBTC + crow];
-        const float bj = cp[3 * kBTC + crow];
+      for (int i4 = 0; i4 < 4; ++i4) {
+        // the constants of 4 consecutive rows at a time
+        const int row0 = cb * 32 + 8 * i4 + 4 * h;
+        const f32x4 u4 = *reinterpret_cast<const f32x4 *>(cp + kBTC + row0);
+        const f32x4 s24 = *reinterpret_cast<const f32x4 *>(cp + 2 * kBTC + row0);
+        f32x4 bj4 = {0.f, 0.f, 0.f, 0.f};
+        if constexpr (FMT == KM_RABITQ) bj4 = *reinterpret_cast<const f32x4 *>(cp + 3 * kBTC + row0);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+        const int i = 4 * i4 + e;
+        const int cl = cb * 32 + 8 * i4 + e;
+        const float u = u4[e];
+        const float s2 = s24[e];
+        const float bj = bj4[e];
 #pragma unroll
         for (int pb = 0; pb < 2; ++pb) {
           const int sd = acc[cb][pb][i];
@@ -1195,16 +1203,15 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void assign_bits_kernel(AssignArgs
             loc[pb] = cl;
           }
         }
+        }
       }
 #pragma unroll
     for (int pb = 0; pb < 2; ++pb)
       if (loc[pb] >= 0) bidx[pb] = ct * kBTC + loc[pb] + 4 * h;
   };
 
-  // stage it = ct S + s reads buffer cur while the copies of stage it + 1 fill nxt
-  auto step = [&](int it, const uint8_t *cur, uint8_t *nxt) {
-    const int ct = it / S, s = it - ct * S;
-    const bool has_next = it + 1 < total;
+  // stage s of tile ct reads buffer cur while the copies of the next stage fill nxt
+  auto step = [&](int ct, int s, bool has_next, const uint8_t *cur, uint8_t *nxt) {
     const int s_n = (s + 1 == S) ? 0 : s + 1;
     const int ct_n = (s + 1 == S) ? ct + 1 : ct;
     if (has_next) load(ct_n, s_n, nxt);
@@ -1221,9 +1228,20 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void assign_bits_kernel(AssignArgs
       __syncthreads();
     }
   };
+  int cct = 0, cs = 0;  // tile and stage of the step about to run
+  auto advance = [&]() {
+    if (++cs == S) {
+      cs = 0;
+      ++cct;
+    }
+  };
   for (int it = 0; it < total; it += 2) {
-    step(it, cst0, cst1);
-    if (it + 1 < total) step(it + 1, cst1, cst0);
+    step(cct, cs, it + 1 < total, cst0, cst1);
+    advance();
+    if (it + 1 < total) {
+      step(cct, cs, it + 2 < total, cst1, cst0);
+      advance();
+    }
   }
 #pragma unroll
   for (int pb = 0; pb < 2; ++pb) {
@@ -1384,10 +1402,28 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
       z[0] = z[1] = z[2] = z[3] = 0u;
     }
   };
+  // The copies of one stage: its two source bases are computed once.  When the stage
+  // lies wholly inside the dimensions and its centroid tile is full, every copy is
+  // a plain one (a precomputed offset, no test); otherwise load_one handles the
+  // clamped rows and the zero-filled chunks.  A stage's plan is (ct, s, dst, cb, pb,
+  // plain), kept in scalar variables.
+  auto plan_cb = [&](int ct, int s) { return A.ci8 + (int64_t)((g + ct * NG) * TC) * A.cild + kRowBytes * s; };
+  auto plan_plain = [&](int ct, int s) { return kRowBytes * (s + 1) <= A.di && A.k - (g + ct * NG) * TC >= TC; };
+  // copies i0 .. i1 - 1 of a stage (constants once the callers' loops are unrolled)
+  auto copies = [&](int ct, int s, uint8_t *dst, const int8_t *cb, const uint8_t *pb, bool plain, int i0, int i1) {
+    if (plain) {
+#pragma unroll
+      for (int i = i0; i < i1; ++i)
+        lds_copy16(i < NCC ? (const void *)cb : (const void *)pb, soff[i],
+                   (uint32_t)(size_t)((lds_u8 *)dst + (i * 8 + wave) * 1024));
+    } else {
+#pragma unroll
+      for (int i = i0; i < i1; ++i) load_one(ct, s, dst, i);
+    }
+  };
   auto load = [&](int ct, int s, uint8_t *dst) {
     if (s == 0) load_constant(ct);
-#pragma unroll
-    for (int i = 0; i < NCOPY; ++i) load_one(ct, s, dst, i);
+    copies(ct, s, dst, plan_cb(ct, s), pbase + kRowBytes * s, plan_plain(ct, s), 0, NCOPY);
   };
   auto store = [&](int ct, int s) {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -1400,7 +1436,9 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
   constexpr bool SPREAD = PK;
   int sp_ct = 0, sp_s = 0;
   uint8_t *sp_dst = nullptr;
-  bool sp_on = false;
+  const int8_t *sp_cb = nullptr;
+  const uint8_t *sp_pb = nullptr;
+  bool sp_on = false, sp_plain = false;
 
   Acc8<BF> acc[CB][k8PB];
   // one stage of 4 steps of 32 dimensions; a scheduling barrier per step keeps the
@@ -1422,10 +1460,8 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
     for (int g = 0; g < 4; ++g) {
       constexpr int cur = 0;
       read(g, 0);
-      if (SPREAD && sp_on) {
-#pragma unroll
-        for (int i = g * NCOPY / 4; i < (g + 1) * NCOPY / 4; ++i) load_one(sp_ct, sp_s, sp_dst, i);
-      }
+      if (SPREAD && sp_on)
+        copies(sp_ct, sp_s, sp_dst, sp_cb, sp_pb, sp_plain, g * NCOPY / 4, (g + 1) * NCOPY / 4);
 #pragma unroll
       for (int cb = 0; cb < CB; ++cb)
 #pragma unroll
@@ -1530,9 +1566,8 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
   load(0, 0, qst0);
   store(0, 0);
   __syncthreads();
-  auto step = [&](int it, const uint8_t *cur, uint8_t *nxt) {
-    const int ct = it / S, s = it - ct * S;
-    const bool has_next = it + 1 < total;
+  // stage s of tile ct reads buffer cur while the copies of the next stage fill nxt
+  auto step = [&](int ct, int s, bool has_next, const uint8_t *cur, uint8_t *nxt) {
     const int s_n = (s + 1 == S) ? 0 : s + 1;
     const int ct_n = (s + 1 == S) ? ct + 1 : ct;
     if constexpr (SPREAD) {
@@ -1540,6 +1575,9 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
       sp_ct = ct_n;
       sp_s = s_n;
       sp_dst = nxt;
+      sp_cb = plan_cb(ct_n, s_n);
+      sp_pb = pbase + kRowBytes * s_n;
+      sp_plain = plan_plain(ct_n, s_n);
       if (has_next && s_n == 0) load_constant(ct_n);
     } else {
       if (has_next) load(ct_n, s_n, nxt);
@@ -1571,9 +1609,20 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
       __syncthreads();
     }
   };
+  int cct = 0, cs = 0;  // tile and stage of the step about to run
+  auto advance = [&]() {
+    if (++cs == S) {
+      cs = 0;
+      ++cct;
+    }
+  };
   for (int it = 0; it < total; it += 2) {
-    step(it, qst0, qst1);
-    if (it + 1 < total) step(it + 1, qst1, qst0);
+    step(cct, cs, it + 1 < total, qst0, qst1);
+    advance();
+    if (it + 1 < total) {
+      step(cct, cs, it + 2 < total, qst1, qst0);
+      advance();
+    }
   }
   if constexpr (PK) {
 #pragma unroll
@@ -1816,9 +1865,8 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_f32_kernel(AssignArgs A0)
   for (int i = 0; i < NCOPY; ++i) copy(i);
   land(0, 0);
   __syncthreads();
-  auto step = [&](int it, const uint8_t *cur, uint8_t *nxt) {
-    const int ct = it / S, s = it - ct * S;
-    const bool has_next = it + 1 < total;
+  // stage s of tile ct reads buffer cur while the copies of the next stage fill nxt
+  auto step = [&](int ct, int s, bool has_next, const uint8_t *cur, uint8_t *nxt) {
     const int s_n = (s + 1 == S) ? 0 : s + 1;
     const int ct_n = (s + 1 == S) ? ct + 1 : ct;
     if (s == 0) {
@@ -1839,9 +1887,20 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_f32_kernel(AssignArgs A0)
       __syncthreads();
     }
   };
+  int cur_t = 0, cur_s = 0;  // tile and stage of the step about to run
+  auto advance = [&]() {
+    if (++cur_s == S) {
+      cur_s = 0;
+      ++cur_t;
+    }
+  };
   for (int it = 0; it < total; it += 2) {
-    step(it, fst0, fst1);
-    if (it + 1 < total) step(it + 1, fst1, fst0);
+    step(cur_t, cur_s, it + 1 < total, fst0, fst1);
+    advance();
+    if (it + 1 < total) {
+      step(cur_t, cur_s, it + 2 < total, fst1, fst0);
+      advance();
+    }
   }
 
   // merge the two lane halves (rows 4h..), then the two centroid halves
