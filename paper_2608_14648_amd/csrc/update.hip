@@ -2,8 +2,11 @@
 //
 //   1. hist     per block of points (about 1024 blocks), member counts of every cluster
 //               (LDS-privatised histogram), stored cluster-major [k][nblk].
-//   2. scan     exclusive scan of that table: entry (j, b) is where block b's
-//               first member of cluster j goes in the cluster-sorted order.
+//   2. scan     exclusive scan of that table (block sums, then each block's
+//               scan plus the sum of the blocks before it): entry (j, b) is where
+//               block b's first member of cluster j goes in the cluster-sorted
+//               order; one workgroup then derives every cluster's count, start
+//               and chunk offset.
 //   3. scatter  stable counting sort: points are ranked inside each wave among
 //               the lanes with the same cluster id (found with one ballot per
 //               id bit) and the four waves take their slots in order, so
@@ -157,28 +160,19 @@ __global__ __launch_bounds__(256) void scan_reduce_kernel(const int *x, int64_t 
   if (threadIdx.x == 0) bsum[blockIdx.x] = sh[0];
 }
 
-// Single-workgroup exclusive scan of n ints in place (each thread a contiguous run).
-// mode 1 scans ceil(x / kChunk) instead of x.  *total receives the grand total.
-__global__ __launch_bounds__(256) void scan_single_kernel(const int *in, int *out, int n, int *total, int mode) {
+// Exclusive scan of block b's segment plus the sum of the segments before it, which
+// the block adds up itself from the segment sums (a few thousand at most); the last
+// block also writes the grand total.
+__global__ __launch_bounds__(256) void scan_down_kernel(int *x, int64_t L, const int *bsum, int *total) {
   __shared__ int sh[256];
-  const int t = threadIdx.x;
-  const int per = (n + 255) / 256;
-  const int lo = min(n, t * per), hi = min(n, lo + per);
-  int s = 0;
-  for (int i = lo; i < hi; ++i) s += mode ? (in[i] + kChunk - 1) / kChunk : in[i];
-  int tot;
-  int run = block_excl_scan_int(s, sh, &tot);
-  for (int i = lo; i < hi; ++i) {
-    const int v = mode ? (in[i] + kChunk - 1) / kChunk : in[i];
-    out[i] = run;
-    run += v;
-  }
-  if (t == 0 && total) *total = tot;
-}
-
-__global__ __launch_bounds__(256) void scan_down_kernel(int *x, int64_t L, const int *bsum) {
-  __shared__ int sh[256];
-  const int64_t base = (int64_t)blockIdx.x * kScanSeg + (int64_t)threadIdx.x * 16;
+  __shared__ int pre[4];
+  const int b = blockIdx.x, t = threadIdx.x;
+  int ps = 0;
+  for (int i = t; i < b; i += 256) ps += bsum[i];
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) ps += __shfl_xor(ps, o);
+  if ((t & 63) == 0) pre[t >> 6] = ps;
+  const int64_t base = (int64_t)b * kScanSeg + (int64_t)t * 16;
   int v[16];
   int s = 0;
 #pragma unroll
@@ -186,7 +180,11 @@ __global__ __launch_bounds__(256) void scan_down_kernel(int *x, int64_t L, const
     v[e] = base + e < L ? x[base + e] : 0;
     s += v[e];
   }
-  int run = block_excl_scan_int(s, sh, nullptr) + bsum[blockIdx.x];
+  int tot;
+  int run = block_excl_scan_int(s, sh, &tot);  // its barriers also publish pre[]
+  const int prefix = pre[0] + pre[1] + pre[2] + pre[3];
+  run += prefix;
+  if (t == 0 && b == gridDim.x - 1) *total = prefix + tot;
 #pragma unroll
   for (int e = 0; e < 16; ++e) {
     if (base + e < L) x[base + e] = run;
@@ -194,14 +192,29 @@ __global__ __launch_bounds__(256) void scan_down_kernel(int *x, int64_t L, const
   }
 }
 
-// counts and start offsets of each cluster from the scanned table
-__global__ void counts_kernel(const int *offs, int nblk, int k, const int *total, int *cnt, int *cstart) {
-  const int j = blockIdx.x * 256 + threadIdx.x;
-  if (j >= k) return;
-  const int s = offs[(int64_t)j * nblk];
-  const int e = j + 1 < k ? offs[(int64_t)(j + 1) * nblk] : total[0];
-  cnt[j] = e - s;
-  cstart[j] = s;
+// counts and start offsets of each cluster from the scanned table, and the exclusive
+// scan of their chunk counts ceil(cnt / kChunk) (one workgroup; choff[k] = all chunks)
+__global__ __launch_bounds__(256) void counts_kernel(const int *offs, int nblk, int k, const int *total, int *cnt,
+                                                     int *cstart, int *choff) {
+  __shared__ int sh[256];
+  const int t = threadIdx.x;
+  const int per = (k + 255) / 256;
+  const int lo = min(k, t * per), hi = min(k, lo + per);
+  int sum = 0;
+  for (int j = lo; j < hi; ++j) {
+    const int s0 = offs[(int64_t)j * nblk];
+    const int e0 = j + 1 < k ? offs[(int64_t)(j + 1) * nblk] : total[0];
+    cnt[j] = e0 - s0;
+    cstart[j] = s0;
+    sum += (e0 - s0 + kChunk - 1) / kChunk;
+  }
+  int tot;
+  int run = block_excl_scan_int(sum, sh, &tot);
+  for (int j = lo; j < hi; ++j) {
+    choff[j] = run;
+    run += (cnt[j] + kChunk - 1) / kChunk;
+  }
+  if (t == 0) choff[k] = tot;
 }
 
 // ---- 3. stable scatter -------------------------------------------------------
@@ -585,7 +598,21 @@ __global__ __launch_bounds__(256) void segsum_sq8_kernel(const uint8_t *codes, i
   }
 }
 
-// ---- 5. finalize ---------------------------------------------------------------
+// ---- 5. finalize (and compose) ---------------------------------------------------
+// The new centroid in the original space from its clustering-space value z: on the
+// 1-bit dims (col >= d_bits of a 1-bit format) m + z, the centre m being NULL (0)
+// for RabitQ's residual space; elsewhere z.
+struct Compose {
+  float *C;
+  const float *m;
+  int d_bits;
+  int bits;
+  int64_t *counts;
+  __device__ float operator()(int col, float z) const {
+    return bits && col >= d_bits ? (m ? m[col] : 0.0f) + z : z;
+  }
+};
+
 // Columns from d_bits on hold, per chunk, W as an exact integer sum of the scaled
 // alphas q over the set bits; partialA the chunk's sum of q and partialM its
 // largest alpha, which fixes the scale s = partialM / (2^23 - 1).  The mean decoded
@@ -593,11 +620,14 @@ __global__ __launch_bounds__(256) void segsum_sq8_kernel(const uint8_t *codes, i
 __global__ __launch_bounds__(256) void finalize_f32_kernel(const float *partial, int dp, const int *cnt,
                                                            const int *choff, float *Z, uint8_t *fresh,
                                                            const uint32_t *partialA, const float *partialM,
-                                                           int d_bits) {
+                                                           int d_bits, Compose cm) {
   const int j = blockIdx.x;
   const int col = blockIdx.y * 256 + threadIdx.x;
   const int nj = cnt[j];
-  if (blockIdx.y == 0 && threadIdx.x == 0) fresh[j] = nj > 0;
+  if (blockIdx.y == 0 && threadIdx.x == 0) {
+    fresh[j] = nj > 0;
+    if (cm.counts) cm.counts[j] = nj;
+  }
   if (nj == 0 || col >= dp) return;
   double s = 0.0;
   if (partialA && col >= d_bits) {
@@ -612,20 +642,28 @@ __global__ __launch_bounds__(256) void finalize_f32_kernel(const float *partial,
   } else {
     for (int c = choff[j]; c < choff[j + 1]; ++c) s += (double)partial[(int64_t)c * dp + col];
   }
-  Z[(int64_t)j * dp + col] = (float)(s / (double)nj);
+  const float z = (float)(s / (double)nj);
+  Z[(int64_t)j * dp + col] = z;
+  cm.C[(int64_t)j * dp + col] = cm(col, z);
 }
 
 __global__ __launch_bounds__(256) void finalize_sq8_kernel(const int *partial, int d, const int *cnt,
-                                                           const int *choff, uint8_t *Z, uint8_t *fresh) {
+                                                           const int *choff, uint8_t *Z, uint8_t *fresh, uint8_t *C,
+                                                           int64_t *counts) {
   const int j = blockIdx.x;
   const int col = blockIdx.y * 256 + threadIdx.x;
   const int nj = cnt[j];
-  if (blockIdx.y == 0 && threadIdx.x == 0) fresh[j] = nj > 0;
+  if (blockIdx.y == 0 && threadIdx.x == 0) {
+    fresh[j] = nj > 0;
+    if (counts) counts[j] = nj;
+  }
   if (nj == 0 || col >= d) return;
   int64_t S = 0;
   for (int c = choff[j]; c < choff[j + 1]; ++c) S += partial[(int64_t)c * d + col];
   // mean of the codes rounded half up: floor((2S + n) / (2n))
-  Z[(int64_t)j * d + col] = (uint8_t)((2 * S + nj) / (2 * (int64_t)nj));
+  const uint8_t z = (uint8_t)((2 * S + nj) / (2 * (int64_t)nj));
+  Z[(int64_t)j * d + col] = z;
+  C[(int64_t)j * d + col] = z;
 }
 
 // ---- 6. empty-cluster split (one workgroup) -----------------------------------
@@ -635,7 +673,7 @@ __global__ __launch_bounds__(256) void finalize_sq8_kernel(const int *partial, i
 template <bool CODES>
 __global__ __launch_bounds__(256) void split_kernel(void *Zv, int k, int dp, const int *cnt, int64_t *cntw,
                                                     uint8_t *fresh, int *empties, const int *seg_lo,
-                                                    const int *seg_hi) {
+                                                    const int *seg_hi, Compose cm) {
   __shared__ int64_t sv[256];
   __shared__ int si[256];
   __shared__ int shs[256];
@@ -686,21 +724,29 @@ __global__ __launch_bounds__(256) void split_kernel(void *Zv, int k, int dp, con
     const int64_t nb = sv[0];
     __syncthreads();
     if (nb < 2) continue;  // uniform
+    // the two rows change in Z and, composed, in C (finalize composed the others)
     if (CODES) {
       uint8_t *Z = static_cast<uint8_t *>(Zv);
+      uint8_t *C = reinterpret_cast<uint8_t *>(cm.C);
       for (int i = t; i < dp; i += 256) {
         const int v = Z[(int64_t)b * dp + i];
         const int p = (i & 1) ? -1 : 1;
-        Z[(int64_t)j * dp + i] = (uint8_t)min(255, max(0, v + p));
-        Z[(int64_t)b * dp + i] = (uint8_t)min(255, max(0, v - p));
+        const uint8_t zj = (uint8_t)min(255, max(0, v + p)), zb = (uint8_t)min(255, max(0, v - p));
+        Z[(int64_t)j * dp + i] = zj;
+        Z[(int64_t)b * dp + i] = zb;
+        C[(int64_t)j * dp + i] = zj;
+        C[(int64_t)b * dp + i] = zb;
       }
     } else {
       float *Z = static_cast<float *>(Zv);
       for (int i = t; i < dp; i += 256) {
         const float v = Z[(int64_t)b * dp + i];
         const bool even = (i & 1) == 0;
-        Z[(int64_t)j * dp + i] = v * (even ? up : dn);
-        Z[(int64_t)b * dp + i] = v * (even ? dn : up);
+        const float zj = v * (even ? up : dn), zb = v * (even ? dn : up);
+        Z[(int64_t)j * dp + i] = zj;
+        Z[(int64_t)b * dp + i] = zb;
+        cm.C[(int64_t)j * dp + i] = cm(i, zj);
+        cm.C[(int64_t)b * dp + i] = cm(i, zb);
       }
     }
     __syncthreads();
@@ -711,25 +757,6 @@ __global__ __launch_bounds__(256) void split_kernel(void *Zv, int k, int dp, con
       fresh[j] = 1;
     }
     __syncthreads();
-  }
-}
-
-// ---- 7. compose -----------------------------------------------------------------
-template <int FMT>
-__global__ __launch_bounds__(256) void compose_kernel(const void *Zv, int k, int d, int d0, const float *m,
-                                                      const uint8_t *fresh, const int *cnt, void *Cv,
-                                                      int64_t *counts) {
-  const int j = blockIdx.x;
-  const int col = blockIdx.y * 256 + threadIdx.x;
-  if (counts && blockIdx.y == 0 && threadIdx.x == 0) counts[j] = cnt[j];
-  if (!fresh[j] || col >= d) return;
-  if (FMT == KM_SQ8) {
-    static_cast<uint8_t *>(Cv)[(int64_t)j * d + col] = static_cast<const uint8_t *>(Zv)[(int64_t)j * d + col];
-  } else {
-    const float z = static_cast<const float *>(Zv)[(int64_t)j * d + col];
-    const bool bitdim = (FMT == KM_SIGN1 || FMT == KM_HYBRID) && col >= d0;
-    // (RabitQ centroids live in the rotated residual space: centre 0, composed as SIGN1 with m = NULL)
-    static_cast<float *>(Cv)[(int64_t)j * d + col] = bitdim ? (m ? m[col] : 0.0f) + z : z;
   }
 }
 
@@ -749,11 +776,8 @@ static km_status launch_sort(const int32_t *assign, int64_t n, int k, const UpdW
   hipLaunchKernelGGL(hist_kernel, dim3(w.nblk), dim3(256), lds_bytes, s, assign, n, k, w.nblk, w.ppb, w.offs,
                      (int)lds);
   hipLaunchKernelGGL(scan_reduce_kernel, dim3(w.nsb), dim3(256), 0, s, w.offs, w.L, w.bsum);
-  hipLaunchKernelGGL(scan_single_kernel, dim3(1), dim3(256), 0, s, w.bsum, w.bsum, w.nsb, w.total, 0);
-  hipLaunchKernelGGL(scan_down_kernel, dim3(w.nsb), dim3(256), 0, s, w.offs, w.L, w.bsum);
-  hipLaunchKernelGGL(counts_kernel, dim3((unsigned)cdiv(k, 256)), dim3(256), 0, s, w.offs, w.nblk, k, w.total, w.cnt,
-                     w.cstart);
-  hipLaunchKernelGGL(scan_single_kernel, dim3(1), dim3(256), 0, s, w.cnt, w.choff, k, w.choff + k, 1);
+  hipLaunchKernelGGL(scan_down_kernel, dim3(w.nsb), dim3(256), 0, s, w.offs, w.L, w.bsum, w.total);
+  hipLaunchKernelGGL(counts_kernel, dim3(1), dim3(256), 0, s, w.offs, w.nblk, k, w.total, w.cnt, w.cstart, w.choff);
   hipLaunchKernelGGL(scatter_kernel, dim3(w.nblk), dim3(256), lds_bytes, s, assign, n, k, w.nblk, w.ppb, w.offs,
                      (int)lds, w.perm);
   KMQ_LAUNCH_CHECK("update: sort");
@@ -788,12 +812,19 @@ km_status launch_update(const Points &P, const int32_t *assign, int k, void *C, 
   if (sst != KM_OK) return sst;
 
   const int d = P.d;
+  Compose cm;
+  cm.C = static_cast<float *>(C);
+  cm.m = P.center;
+  cm.d_bits = P.fmt == KM_HYBRID ? P.d_front : 0;
+  cm.bits = is_bits_fmt(P.fmt);
+  cm.counts = counts;
   if (P.fmt == KM_SQ8) {
     hipLaunchKernelGGL(segsum_sq8_kernel, dim3(w.maxchunks, (unsigned)cdiv(d, 1024)), dim3(256), 0, s,
                        static_cast<const uint8_t *>(P.data), P.ld, d, w.perm, w.cnt, w.cstart, w.choff, k,
                        static_cast<int *>(w.partial));
     hipLaunchKernelGGL(finalize_sq8_kernel, dim3(k, (unsigned)cdiv(d, 256)), dim3(256), 0, s,
-                       static_cast<const int *>(w.partial), d, w.cnt, w.choff, static_cast<uint8_t *>(w.Z), w.fresh);
+                       static_cast<const int *>(w.partial), d, w.cnt, w.choff, static_cast<uint8_t *>(w.Z), w.fresh,
+                       static_cast<uint8_t *>(C), counts);
   } else {
     int df = 0;
     const float *F = nullptr;
@@ -828,29 +859,17 @@ km_status launch_update(const Points &P, const int32_t *assign, int k, void *C, 
     }
     hipLaunchKernelGGL(finalize_f32_kernel, dim3(k, (unsigned)cdiv(w.dp, 256)), dim3(256), 0, s,
                        static_cast<const float *>(w.partial), w.dp, w.cnt, w.choff, static_cast<float *>(w.Z),
-                       w.fresh, is_bits_fmt(P.fmt) ? w.partialA : nullptr, w.partialM, d_bits);
+                       w.fresh, is_bits_fmt(P.fmt) ? w.partialA : nullptr, w.partialM, d_bits, cm);
   }
   KMQ_LAUNCH_CHECK("update: segmented sums");
 
   if (policy == KM_EMPTY_SPLIT) {
     if (P.fmt == KM_SQ8)
       hipLaunchKernelGGL(split_kernel<true>, dim3(1), dim3(256), 0, s, w.Z, k, w.dp, w.cnt, w.cntw, w.fresh,
-                         w.empties, seg_lo, seg_hi);
+                         w.empties, seg_lo, seg_hi, cm);
     else
       hipLaunchKernelGGL(split_kernel<false>, dim3(1), dim3(256), 0, s, w.Z, k, w.dp, w.cnt, w.cntw, w.fresh,
-                         w.empties, seg_lo, seg_hi);
-  }
-  const dim3 g(k, (unsigned)cdiv(d, 256));
-  const int d0 = P.fmt == KM_HYBRID ? P.d_front : 0;
-  switch (P.fmt) {
-    case KM_F32:
-    case KM_LVQ4:
-    case KM_BF16: hipLaunchKernelGGL(compose_kernel<KM_F32>, g, dim3(256), 0, s, w.Z, k, d, d0, P.center, w.fresh, w.cnt, C, counts); break;
-    case KM_SQ8: hipLaunchKernelGGL(compose_kernel<KM_SQ8>, g, dim3(256), 0, s, w.Z, k, d, d0, P.center, w.fresh, w.cnt, C, counts); break;
-    case KM_SIGN1:
-    case KM_RABITQ: hipLaunchKernelGGL(compose_kernel<KM_SIGN1>, g, dim3(256), 0, s, w.Z, k, d, d0, P.center, w.fresh, w.cnt, C, counts); break;
-    case KM_HYBRID: hipLaunchKernelGGL(compose_kernel<KM_HYBRID>, g, dim3(256), 0, s, w.Z, k, d, d0, P.center, w.fresh, w.cnt, C, counts); break;
-    default: return KM_EUNSUPPORTED;
+                         w.empties, seg_lo, seg_hi, cm);
   }
   KMQ_LAUNCH_CHECK("update: split/compose");
   return KM_OK;
