@@ -517,8 +517,8 @@ def wl_c5(cfg, torch, km, args):
                      "format": "hybrid (fp32 front + 1-bit tail)"},
                     distances_per_s=(T + 1) * spec.n * k * K / elapsed,
                     partition_cost=float(out["cost"].item()),
-                    roofline=dict(roofline(cfg["name"], s, 2.0 * spec.n * k * d0, "fp32", "assign_kernel<hybrid>",
-                                           "assign_kernel<hybrid>"),
+                    roofline=dict(roofline(cfg["name"], s, 2.0 * spec.n * k * d0, "fp32", "assign_hyb_kernel",
+                                           "assign_hyb_kernel"),
                                   work="2 d_front operations per (point, centroid) pair on fp32 MFMA (the front "
                                        "contraction; the 1-bit tail's int8 work rides in the same launch)"),
                     update_hbm=update_hbm(s, spec.n * (4 * d0 + (spec.d - d0) // 8 + 8),

@@ -1946,6 +1946,363 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_f32_kernel(AssignArgs A0)
   }
 }
 
+// ---- hybrid assignment (fp32 front + 1-bit tail) with direct global-to-LDS stages ---
+// The fp32 kernel's shape (8 waves, a 256-point tile against 256-centroid tiles,
+// 4 x 2 blocks per wave, one workgroup per CU) on the segment decomposition of the
+// squared distance (Sec. 3.1 SuperKMeans).  Per centroid tile the tail comes first:
+// int8 stages of the centroids' residual codes (128 bytes of every row per stage,
+// copied straight into LDS in the conflict-free slot layout) against the points'
+// tail bits, which stay resident in LDS for the whole workgroup, regrouped at load
+// so that widening a half-word to {0, 2} bytes costs a shift and a mask per
+// register.  Seeded with -T the integer accumulators end at 2D - T; that becomes the
+// 1-bit score ts = fmaf(-(alpha 2 sigma), 2D - T, sigma^2 Q) in fp32 (Eq. 4, the
+// order the oracle uses), the same registers then start the fp32 front at -ts/2, and
+// the front's fp32 stages follow, so the epilogue's ||c'||^2 - 2 acc is
+// ||c'||^2 - 2<x',c'> + ts.  The copies of the next stage, of either kind, are spread
+// over the current stage's four steps.
+constexpr int kHybMaxTW = 20;  // resident tail words per point (640 tail dims)
+
+template <int CB = 4>
+__global__ __launch_bounds__(kQThreads, 1) void assign_hyb_kernel(AssignArgs A) {
+  static_assert(CB == 2 || CB == 4, "128- or 256-centroid tiles");
+  constexpr int TC = 64 * CB, TP = kQT, PB = k8PB;
+  constexpr int NCC = TC / 64;           // centroid copies per thread and stage
+  constexpr int NCOPY = (TC + TP) / 64;  // all copies per thread of a front stage
+  constexpr int STAGE = (TC + TP) * kRowBytes;
+  __shared__ __align__(16) uint8_t fst0[STAGE];
+  __shared__ __align__(16) uint8_t fst1[STAGE];
+  __shared__ __align__(16) float cnl[2][4][TC];  // per tile: ||c'||^2, -T (int bits), sigma^2 Q, 2 sigma
+  __shared__ uint32_t bitsT[kHybMaxTW * TP];
+  __shared__ float alp[TP];  // the points' alpha
+  const int t = threadIdx.x;
+  const int lane = t & 63, wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int r = lane & 31, h = lane >> 5;
+  const int wc = wave & 1, wp = wave >> 1;
+  const int NG = A.ngroups;
+  int64_t pt = blockIdx.x;
+  int g = 0;
+  if (NG > 1) {
+    const int64_t l = blockIdx.x >> 3;
+    pt = (l / NG) * 8 + (blockIdx.x & 7);
+    g = (int)(l % NG);
+    if (pt >= A.n_ptiles) return;  // whole workgroup, before any barrier
+  }
+  const int64_t p0 = pt * TP;
+  const int SI = (A.di + kRowBytes - 1) / kRowBytes;  // tail stages
+  const int SF = (A.df + 31) / 32;                    // front stages
+  const int S = SI + SF;
+  const int nct = (A.k + TC - 1) / TC;
+  const int nmy = (nct - g + NG - 1) / NG;
+  const int total = nmy * S;
+  const int prmax = (int)min<int64_t>(A.n - 1 - p0, TP - 1);
+  const float *pbase = A.pf + p0 * A.pfld;
+
+  // resident tail bits, word-major, regrouped; words past the tail up to the last
+  // stage's end are zero (the codes there are zero-filled too)
+  {
+    const int TW = A.di / 32;
+    for (int e = t; e < 4 * SI * TP; e += kQThreads) {
+      const int w = e / TP, pp = e - w * TP;
+      uint32_t v = 0u;
+      if (w < TW) v = regroup_bits(A.pbits[(p0 + min(pp, prmax)) * A.pbw + A.pbw0 + w]);
+      bitsT[w * TP + pp] = v;
+    }
+  }
+  if (t < TP) alp[t] = A.alpha[p0 + min(t, prmax)];
+
+  // the stage being copied: tile c0c, stage cs of the tile, into buffer cdst
+  int c0c = 0, crmax = 0, cs = 0;
+  bool cfull = true, ctail = true;
+  uint8_t *cdst = fst0;
+  auto begin_copies = [&](int ct, int s, uint8_t *dst) {
+    c0c = (g + ct * NG) * TC;
+    crmax = min(A.k - 1 - c0c, TC - 1);
+    cs = s;
+    cdst = dst;
+    ctail = s < SI;
+    cfull = ctail ? kRowBytes * (s + 1) <= A.di : 32 * (s - SI + 1) <= A.df;
+  };
+  // copy i of a wave fills slots (8 i + wave) 64 .. + 63 of the stage: in a tail
+  // stage rows 0 .. TC - 1 of centroid codes, in a front stage TC fp32 centroid rows
+  // and then TP point rows; rows past the last centroid or point are clamped
+  auto copy = [&](int i) {
+    if (ctail && i >= NCC) return;  // a tail stage copies centroid codes only
+    const int slot = (i * 8 + wave) * 64 + lane;
+    const int row = slot >> 3;
+    const int chunk = (slot & 7) ^ ((row >> 1) & 7);
+    uint32_t off;
+    const void *base;
+    bool inside;
+    if (ctail) {
+      off = (uint32_t)(min(row, crmax) * (int)A.cild + 16 * chunk);
+      base = A.ci8 + (int64_t)c0c * A.cild + kRowBytes * cs;
+      inside = kRowBytes * cs + 16 * chunk < A.di;
+    } else {
+      const int sf = cs - SI;
+      if (i < NCC) {
+        off = (uint32_t)(min(row, crmax) * (int)A.cfld * 4 + 16 * chunk);
+        base = A.cf + (int64_t)c0c * A.cfld + 32 * sf;
+      } else {
+        off = (uint32_t)(min(row - TC, prmax) * (int)A.pfld * 4 + 16 * chunk);
+        base = pbase + 32 * sf;
+      }
+      inside = 32 * sf + 4 * chunk < A.df;
+    }
+    lds_u8 *wdst = (lds_u8 *)cdst + (i * 8 + wave) * 1024;
+    if (cfull || inside) {
+      lds_copy16(base, off, (uint32_t)(size_t)wdst);
+    } else {
+      __attribute__((address_space(3))) uint32_t *z = (__attribute__((address_space(3))) uint32_t *)(wdst + 16 * lane);
+      z[0] = z[1] = z[2] = z[3] = 0u;
+    }
+  };
+  auto land = [&]() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); };
+  // a tile's constants for row t: loaded during the first (tail) stage of the tile
+  // before (the prologue for the first tile), where few registers are live, and
+  // stored once that stage's copies have landed
+  float cv[4] = {0.f, 0.f, 0.f, 0.f};
+  auto load_consts = [&](int ct) {
+    if (t < TC) {
+      const int c0 = (g + ct * NG) * TC;
+      const int j = c0 + min(t, A.k - 1 - c0);
+      cv[0] = t <= A.k - 1 - c0 ? A.cp.cn[j] : INFINITY;
+      cv[1] = __int_as_float(-A.cp.qsum[j]);
+      cv[2] = A.cp.u[j];
+      cv[3] = A.cp.sig2[j];
+    }
+  };
+  auto store_consts = [&](int ct) {
+    if (t < TC) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) cnl[ct & 1][q][t] = cv[q];
+    }
+  };
+
+  f32x16 acc[CB][PB];  // the tail's int32 2D - T (bit patterns), then the fp32 front
+  // one tail stage: four steps of 32 dims (one int8 MFMA per block and step)
+  // a tile's accumulators start at -T of their row
+  auto seed = [&](int ct) {
+    const float *cp = cnl[ct & 1][1];
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        const f32x4 v = *reinterpret_cast<const f32x4 *>(cp + wc * 32 * CB + cb * 32 + 8 * m + 4 * h);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+          for (int pb = 0; pb < PB; ++pb) acc[cb][pb][4 * m + e] = v[e];
+      }
+  };
+  auto tail_stage = [&](int s, const uint8_t *buf, bool copying) {
+    const uint32_t hsh = 4u * (uint32_t)h;
+#pragma unroll
+    for (int gg = 0; gg < 4; ++gg) {
+      uint4 av[CB];
+      i32x4 bv[PB];
+      const int so = 16 * ((2 * gg + h) ^ ((r >> 1) & 7));
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb)
+        av[cb] = *reinterpret_cast<const uint4 *>(buf + (wc * 32 * CB + cb * 32 + r) * kRowBytes + so);
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb) bv[pb] = widen_regrouped2(bitsT[(4 * s + gg) * TP + wp * 64 + pb * 32 + r] >> hsh);
+      __builtin_amdgcn_sched_barrier(0);
+      if (copying) {
+#pragma unroll
+        for (int i = gg * NCOPY / 4; i < (gg + 1) * NCOPY / 4; ++i) copy(i);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb) {
+        const i32x4 a4 = {(int)av[cb].x, (int)av[cb].y, (int)av[cb].z, (int)av[cb].w};
+#pragma unroll
+        for (int pb = 0; pb < PB; ++pb)
+          acc[cb][pb] = __builtin_bit_cast(
+              f32x16, __builtin_amdgcn_mfma_i32_32x32x32_i8(a4, bv[pb], __builtin_bit_cast(i32x16, acc[cb][pb]), 0, 0, 0));
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  // the tail's 2D - T to the fp32 seed -ts/2 of the front
+  auto fold_tail = [&](int ct) {
+    const float *cu = cnl[ct & 1][2];
+    const float *c2 = cnl[ct & 1][3];
+    float al[PB];
+#pragma unroll
+    for (int pb = 0; pb < PB; ++pb) al[pb] = alp[wp * 64 + pb * 32 + r];
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        const int row0 = wc * 32 * CB + cb * 32 + 8 * m + 4 * h;
+        const f32x4 u4 = *reinterpret_cast<const f32x4 *>(cu + row0);
+        const f32x4 s4 = *reinterpret_cast<const f32x4 *>(c2 + row0);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+          for (int pb = 0; pb < PB; ++pb) {
+            const int sd = __float_as_int(acc[cb][pb][4 * m + e]);
+            const float ts = fmaf(-(al[pb] * s4[e]), (float)sd, u4[e]);
+            acc[cb][pb][4 * m + e] = -0.5f * ts;
+          }
+      }
+  };
+  // one front stage: four steps of 8 dims (4 k-pairs per MFMA block), operand reads
+  // double-buffered
+  auto front_stage = [&](const uint8_t *buf, bool copying) {
+    uint4 av[2][CB], bv[2][PB];
+    auto read = [&](int gg, int set) {
+      const int so = 16 * ((2 * gg + h) ^ ((r >> 1) & 7));
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb)
+        bv[set][pb] = *reinterpret_cast<const uint4 *>(buf + (TC + wp * 32 * PB + pb * 32 + r) * kRowBytes + so);
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb)
+        av[set][cb] = *reinterpret_cast<const uint4 *>(buf + (wc * 32 * CB + cb * 32 + r) * kRowBytes + so);
+    };
+    read(0, 0);
+#pragma unroll
+    for (int gg = 0; gg < 4; ++gg) {
+      const int cur = gg & 1;
+      if (gg + 1 < 4) read(gg + 1, cur ^ 1);
+      __builtin_amdgcn_sched_barrier(0);
+      if (copying) {
+#pragma unroll
+        for (int i = gg * NCOPY / 4; i < (gg + 1) * NCOPY / 4; ++i) copy(i);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+          for (int pb = 0; pb < PB; ++pb)
+            acc[cb][pb] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(av[cur][cb][e]),
+                                                              __uint_as_float(bv[cur][pb][e]), acc[cb][pb], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  float best[PB];
+  int bidx[PB];
+#pragma unroll
+  for (int pb = 0; pb < PB; ++pb) {
+    best[pb] = INFINITY;
+    bidx[pb] = INT_MAX;
+  }
+  auto epilogue = [&](int ct) {
+    const float *cp = cnl[ct & 1][0];
+    const int c0 = (g + ct * NG) * TC;
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) {
+      const int crow0 = wc * 32 * CB + cb * 32 + 4 * h;
+#pragma unroll
+      for (int i4 = 0; i4 < 4; ++i4) {
+        const f32x4 cn4 = *reinterpret_cast<const f32x4 *>(&cp[crow0 + 8 * i4]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int j = c0 + crow0 + 8 * i4 + e;
+#pragma unroll
+          for (int pb = 0; pb < PB; ++pb) {
+            const float sc = fmaf(-2.0f, acc[cb][pb][4 * i4 + e], cn4[e]);
+            const bool take = sc < best[pb];
+            best[pb] = take ? sc : best[pb];
+            bidx[pb] = take ? j : bidx[pb];
+          }
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  load_consts(0);
+  begin_copies(0, 0, fst0);
+#pragma unroll
+  for (int i = 0; i < NCOPY; ++i) copy(i);
+  land();
+  store_consts(0);
+  __syncthreads();  // also publishes the resident bits and alpha
+  // Per tile: the tail stages, the fold, the front stages, the scores.  Stage gi of
+  // the workgroup's sequence reads buffer gi & 1 while the copies of stage gi + 1
+  // fill the other one.  The tail and front stages run in loops of their own (one
+  // loop with a branch between the two kinds of MFMA stage makes the register
+  // allocator keep a second copy of the accumulators).  A tile's first stage is a
+  // tail stage and never the last stage (S >= 2): its copies land and the next
+  // tile's constants wait with them.
+  int gi = 0;
+  for (int ct = 0; ct < nmy; ++ct) {
+    seed(ct);
+    for (int s = 0; s < SI; ++s, ++gi) {
+      const uint8_t *cur = (gi & 1) ? fst1 : fst0;
+      uint8_t *nxt = (gi & 1) ? fst0 : fst1;
+      begin_copies(ct, s + 1, nxt);  // s + 1 <= SI < S
+      const bool consts = s == 0 && ct + 1 < nmy;
+      if (consts) load_consts(ct + 1);
+      tail_stage(s, cur, true);
+      land();
+      // cnl[(ct + 1) & 1] held tile ct - 1's constants, last read before the barrier
+      // that closed that tile
+      if (consts) store_consts(ct + 1);
+      __syncthreads();
+    }
+    fold_tail(ct);
+    for (int s = SI; s < S; ++s, ++gi) {
+      const uint8_t *cur = (gi & 1) ? fst1 : fst0;
+      uint8_t *nxt = (gi & 1) ? fst0 : fst1;
+      const bool has_next = gi + 1 < total;
+      if (has_next) begin_copies(s + 1 == S ? ct + 1 : ct, s + 1 == S ? 0 : s + 1, nxt);
+      front_stage(cur, has_next);
+      if (has_next) land();
+      __syncthreads();
+    }
+    epilogue(ct);
+    // the next tile's first stage writes tile ct + 2's constants into cnl[ct & 1]
+    __syncthreads();
+  }
+
+  // merge the two lane halves (rows 4h..), then the two centroid halves
+#pragma unroll
+  for (int pb = 0; pb < PB; ++pb) {
+    const float os = __shfl_xor(best[pb], 32);
+    const int oi = __shfl_xor(bidx[pb], 32);
+    if (os < best[pb] || (os == best[pb] && oi < bidx[pb])) {
+      best[pb] = os;
+      bidx[pb] = oi;
+    }
+  }
+  float *ms = reinterpret_cast<float *>(fst0);
+  int *mi = reinterpret_cast<int *>(fst0 + TP * sizeof(float));
+  if (wc == 1 && h == 0) {
+#pragma unroll
+    for (int pb = 0; pb < PB; ++pb) {
+      ms[wp * 32 * PB + pb * 32 + r] = best[pb];
+      mi[wp * 32 * PB + pb * 32 + r] = bidx[pb];
+    }
+  }
+  __syncthreads();
+  if (wc == 0 && h == 0) {
+#pragma unroll
+    for (int pb = 0; pb < PB; ++pb) {
+      const int pc = wp * 32 * PB + pb * 32 + r;
+      const float os = ms[pc];
+      const int oi = mi[pc];
+      if (os < best[pb] || (os == best[pb] && oi < bidx[pb])) {
+        best[pb] = os;
+        bidx[pb] = oi;
+      }
+      const int64_t p = p0 + pc;
+      if (p < A.n) {
+        if (A.keys) {
+          atomicMin(A.keys + p, score_key(best[pb], bidx[pb]));
+        } else {
+          A.assign[p] = bidx[pb] + A.aoff;
+          if (A.score) A.score[p] = best[pb];
+        }
+      }
+    }
+  }
+}
+
 // ---- centroid preparation: one workgroup per centroid ----------------------
 
 template <int FMT>
@@ -2321,8 +2678,11 @@ static int tile_groups(int64_t n, int k) {
   return best_g;
 }
 
+// hybrid points whose tail words fit the direct-copy kernel's resident LDS array
+static bool hyb_direct(const Points &P) { return P.fmt == KM_HYBRID && P.d - P.d_front <= 32 * kHybMaxTW; }
+
 int assign_groups(const Points &P, int k) {
-  if (P.fmt == KM_F32) return tile_groups(P.n, k);
+  if (P.fmt == KM_F32 || hyb_direct(P)) return tile_groups(P.n, k);
   if (P.fmt == KM_HYBRID) {
     constexpr int TC = Geo<Blocking<KM_F32>::CB, Blocking<KM_F32>::PB>::TC;
     return (int)std::min<int64_t>(8, cdiv(k, TC));
@@ -2440,6 +2800,25 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
       hipLaunchKernelGGL((assign_f32_kernel<false, 2>), grid, dim3(kQThreads), 0, s, A);
     else
       hipLaunchKernelGGL((assign_f32_kernel<false, 4>), grid, dim3(kQThreads), 0, s, A);
+    if (ng > 1) {
+      const dim3 gp((unsigned)cdiv(P.n, 256));
+      hipLaunchKernelGGL(keys_unpack_kernel<false>, gp, dim3(256), 0, s, cp.keys, P.n, assign, score, aoff);
+    }
+  } else if (FMT == KM_HYBRID && hyb_direct(P)) {
+    const int64_t npt = cdiv(P.n, kQT);
+    const int ng = assign_groups(P, k);
+    A.n_ptiles = npt;
+    if (ng > 1) {
+      const dim3 gp((unsigned)cdiv(P.n, 256));
+      A.ngroups = ng;
+      A.keys = cp.keys;
+      hipLaunchKernelGGL(keys_init_kernel, gp, dim3(256), 0, s, cp.keys, P.n);
+    }
+    const dim3 grid((unsigned)(ng > 1 ? cdiv(npt, 8) * 8 * ng : npt));
+    if (q8_tile_centroids(k) == 128)
+      hipLaunchKernelGGL((assign_hyb_kernel<2>), grid, dim3(kQThreads), 0, s, A);
+    else
+      hipLaunchKernelGGL((assign_hyb_kernel<4>), grid, dim3(kQThreads), 0, s, A);
     if (ng > 1) {
       const dim3 gp((unsigned)cdiv(P.n, 256));
       hipLaunchKernelGGL(keys_unpack_kernel<false>, gp, dim3(256), 0, s, cp.keys, P.n, assign, score, aoff);

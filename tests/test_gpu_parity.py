@@ -72,15 +72,14 @@ def test_assign_f32(km, torch, n, d, k):
 
 @pytest.mark.parametrize("fmt", ["f32", "hybrid", "sq8", "bf16"])
 def test_assign_ties_across_centroid_groups(km, torch, fmt):
-    """k = 1100 spreads the centroid tiles over several workgroups per point tile
-    (8 for the hybrid with 128-centroid tiles, 5 for fp32, SQ8 and bf16 with
-    256-centroid tiles at this n), merged through (score, index) keys; copies of
-    centroids 5 and 130 placed in other groups' tiles must never win."""
+    """k = 1100 spreads the five 256-centroid tiles over five workgroups per point
+    tile at this n, merged through (score, index) keys; copies of centroids 5 and
+    130 placed in other groups' tiles must never win."""
     n, d, k = 3000, 96, 1100
     X = blobs(n, d, 40, seed=17)
     C = X[pick(n, k, 17)].copy()
-    C[900] = C[5]    # tile 7 vs tile 0 (128-centroid tiles; 3 vs 0 of 256)
-    C[1050] = C[130]  # tile 8 vs tile 1 (4 vs 0 of 256)
+    C[900] = C[5]    # tile 3 vs tile 0
+    C[1050] = C[130]  # tile 4 vs tile 0
     C[640] = C[5]
     if fmt == "sq8":  # exact integer scores: bit-exact against the oracle
         lo, hi = orc.sq8_fit(X)
