@@ -4,9 +4,9 @@
 //
 // Covariance: the d x d output is cut into 256 x 256 tiles (upper triangle only,
 // mirrored at the end) and the n rows are split across workgroups.  Each stage
-// stages 32 rows x 256 columns of both column blocks in LDS, centred on load.
+// copies 32 rows x 256 columns of both column blocks into LDS, centred when read.
 // The fp32 accumulators are added into a per-workgroup fp64 partial tile every
-// 2048 rows, and the partial tiles are folded in split order.
+// 8192 rows, and the partial tiles are folded in split order.
 // Projection: 128 points x 128 outputs per workgroup, 32 dims per stage; the
 // point rows are centred on load and W is pre-transposed so both MFMA operands
 // are read as 16 contiguous bytes per lane (k permuted identically on both).
@@ -21,7 +21,7 @@ constexpr int kT = 128;           // projection tile
 constexpr int kCT = 256;          // covariance output tile
 constexpr int kCovRows = 32;      // rows per covariance stage
 constexpr int kCovStride = kCT + 4;
-constexpr int kFlushStages = 64;  // 2048 rows per fp32 accumulation run
+constexpr int kFlushStages = 256;  // 8192 rows per fp32 accumulation run
 
 __device__ __forceinline__ void tile_ij(int t, int T, int &ti, int &tj) {
   // enumerate the upper triangle row by row
@@ -33,15 +33,41 @@ __device__ __forceinline__ void tile_ij(int t, int T, int &ti, int &tj) {
   tj = ti + t;
 }
 
-// One workgroup per (256 x 256 output tile, run of rows).  Each wave owns a
-// 128 x 128 quarter as 4 x 4 blocks of 32 x 32 (fp32 MFMA, rows are the
-// contraction index, read column-wise from row-major LDS tiles).  Every 2048 rows
-// the fp32 accumulators are added into this workgroup's own fp64 partial tile
-// in global memory (read-modify-write, no other workgroup touches it).
-__global__ __launch_bounds__(256, 1) void cov_kernel(const float *X, int64_t n, int d, const float *mean, int T,
-                                                     int ntiles, int64_t rows_per_split, double *partial) {
-  __shared__ float Ai[2][kCovRows * kCovStride];
-  __shared__ float Aj[2][kCovRows * kCovStride];
+// Direct copy of 16 bytes per lane from global memory into LDS: the wave's 64 lanes
+// fill 1 KB at LDS byte address lds (wave-uniform) in lane order, from a
+// wave-uniform base plus a 32-bit per-lane byte offset.  Inline assembly, so that
+// the compiler does not wait for the copy before the LDS reads of the other stage
+// buffer; the caller waits (vmcnt) before the barrier that publishes the data.
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void lds_copy16(const void *base, uint32_t off, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "s"(lds)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// One workgroup per (256 x 256 output tile, run of rows): 8 waves, two per SIMD,
+// each owning 128 x 64 of the tile as 4 x 2 blocks of 32 x 32 (fp32 MFMA; rows are
+// the contraction index, read column-wise from row-major LDS stages).  A stage is
+// 32 rows of both 256-column blocks, copied straight from global memory into LDS,
+// one 1 KB row-block per wave instruction (rows padded to 260 floats); the rows
+// are centred when the MFMA operands are read (x - mean in fp32, the same operand
+// a centring copy would store).  Rows past the end of the run are filled with the
+// mean itself, so their centred values are exactly zero; columns past d are
+// zero-filled and their outputs dropped by the reduction.  The copies of stage
+// st + 1 go out during stage st's four steps.  Every 8192 rows the fp32
+// accumulators are added into this workgroup's own fp64 partial tile in global
+// memory (read-modify-write, no other workgroup touches it); the fold is a
+// synchronous read-modify-write of 128 values per lane, so shorter runs cost
+// (2048 rows: 7 % slower).
+constexpr int kCovThreads = 512;
+
+__global__ __launch_bounds__(kCovThreads, 1) void cov_kernel(const float *X, int64_t n, int d, const float *mean, int T,
+                                                             int ntiles, int64_t rows_per_split, double *partial) {
+  constexpr int BS = kCovRows * kCovStride;  // floats of one column block of a stage
+  __shared__ __align__(16) float stA0[2 * BS];
+  __shared__ __align__(16) float stA1[2 * BS];
   const int tile = blockIdx.x % ntiles;
   const int split = blockIdx.x / ntiles;
   int ti, tj;
@@ -49,96 +75,123 @@ __global__ __launch_bounds__(256, 1) void cov_kernel(const float *X, int64_t n, 
   const int i0 = ti * kCT, j0 = tj * kCT;
   const int64_t rb = (int64_t)split * rows_per_split;
   const int64_t re = min<int64_t>(n, rb + rows_per_split);
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int t = threadIdx.x, lane = t & 63, wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int r = lane & 31, h = lane >> 5;
   const int wi = wave & 1, wj = wave >> 1;
   double *out = partial + ((int64_t)split * ntiles + tile) * (kCT * kCT);
-
   const int nst = (int)cdiv(max<int64_t>(re - rb, 0), kCovRows);
-  f32x4 ri[8], rj[8];
-  auto load = [&](int st) {
+
+  // the means of this lane's operand columns
+  float mi[4], mj[2];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int idx = t + 256 * q;
-      const int row = idx >> 6, c4 = idx & 63;
-      const int64_t gr = rb + (int64_t)st * kCovRows + row;
-      const bool rok = gr < re;
-      const int64_t grc = rok ? gr : rb;
-      const int ci = i0 + 4 * c4, cj = j0 + 4 * c4;
-      const bool iok = rok && ci < d, jok = rok && cj < d;
-      ri[q] = *reinterpret_cast<const f32x4 *>(X + grc * d + (iok ? ci : 0));
-      rj[q] = *reinterpret_cast<const f32x4 *>(X + grc * d + (jok ? cj : 0));
+  for (int cb = 0; cb < 4; ++cb) mi[cb] = mean[min(i0 + wi * 128 + cb * 32 + r, d - 1)];
+#pragma unroll
+  for (int pb = 0; pb < 2; ++pb) mj[pb] = mean[min(j0 + wj * 64 + pb * 32 + r, d - 1)];
+
+  // the fill of a row past the run: the means of this lane's four columns of each
+  // block (zeros past d), held in registers so that no load the compiler tracks
+  // sits among the copies
+  f32x4 fill[2];
+#pragma unroll
+  for (int blk = 0; blk < 2; ++blk) {
+    const int col = (blk ? j0 : i0) + 4 * lane;
+    fill[blk] = col < d ? *reinterpret_cast<const f32x4 *>(mean + col) : f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  // copy q (0 .. 7) of wave w: row-block c = 8 q + w, column block c >> 5, row c & 31
+  auto copy = [&](int st, float *dst, int q) {
+    const int c = 8 * q + wave;
+    const int blk = c >> 5, row = c & 31;
+    const int col = (blk ? j0 : i0) + 4 * lane;
+    float *w = dst + blk * BS + row * kCovStride;
+    const int64_t gr = rb + (int64_t)st * kCovRows + row;
+    if (gr < re && col < d) {
+      lds_copy16(X + gr * d + (blk ? j0 : i0), (uint32_t)(16 * lane), (uint32_t)(size_t)(lds_u8 *)(w));
+    } else {
+      // a row past the run holds the mean (centred: zero); a column past d zeros
+      *reinterpret_cast<f32x4 *>(w + 4 * lane) = gr >= re ? fill[blk] : f32x4{0.f, 0.f, 0.f, 0.f};
     }
   };
-  // centring and zero-fill happen when the stage is written to LDS, one stage
-  // after the loads were issued
-  auto store = [&](int st, int buf) {
+  auto land = [&]() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); };
+
+  f32x16 acc[4][2];
+  // one stage: 16 row pairs in 4 steps of 4; the operand reads of step g + 1 and
+  // two of the next stage's copies go out before step g's MFMAs
+  auto mfma_stage = [&](const float *buf, bool copying, int st_n, float *nxt) {
+    const float *A = buf;
+    const float *B = buf + BS;
+    float av[2][4][4], bv[2][4][2];
+    auto read = [&](int g, int set) {
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int idx = t + 256 * q;
-      const int row = idx >> 6, c4 = idx & 63;
-      const int64_t gr = rb + (int64_t)st * kCovRows + row;
-      const bool rok = gr < re;
-      const int ci = i0 + 4 * c4, cj = j0 + 4 * c4;
-      const bool iok = rok && ci < d, jok = rok && cj < d;
-      const f32x4 mi = *reinterpret_cast<const f32x4 *>(mean + (ci < d ? ci : 0));
-      const f32x4 mj = *reinterpret_cast<const f32x4 *>(mean + (cj < d ? cj : 0));
-      const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-      *reinterpret_cast<f32x4 *>(&Ai[buf][row * kCovStride + 4 * c4]) = iok ? ri[q] - mi : z;
-      *reinterpret_cast<f32x4 *>(&Aj[buf][row * kCovStride + 4 * c4]) = jok ? rj[q] - mj : z;
+      for (int pp = 0; pp < 4; ++pp) {
+        const int row = 2 * (4 * g + pp) + h;
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) av[set][pp][cb] = A[row * kCovStride + wi * 128 + cb * 32 + r] - mi[cb];
+#pragma unroll
+        for (int pb = 0; pb < 2; ++pb) bv[set][pp][pb] = B[row * kCovStride + wj * 64 + pb * 32 + r] - mj[pb];
+      }
+    };
+    read(0, 0);
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int cur = g & 1;
+      if (g + 1 < 4) read(g + 1, cur ^ 1);
+      __builtin_amdgcn_sched_barrier(0);
+      if (copying) {
+        copy(st_n, nxt, 2 * g);
+        copy(st_n, nxt, 2 * g + 1);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int pp = 0; pp < 4; ++pp)
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+          for (int pb = 0; pb < 2; ++pb)
+            acc[cb][pb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[cur][pp][cb], bv[cur][pp][pb], acc[cb][pb], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
 
   if (nst > 0) {
-    load(0);
-    store(0, 0);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) copy(0, stA0, q);
+    land();
   }
   __syncthreads();
   const int nrun = (nst + kFlushStages - 1) / kFlushStages;
   for (int run = 0; run < nrun; ++run) {
-    f32x16 acc[4][4];
 #pragma unroll
     for (int a = 0; a < 4; ++a)
 #pragma unroll
-      for (int b = 0; b < 4; ++b)
+      for (int b = 0; b < 2; ++b)
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.f;
     const int st1 = min(nst, (run + 1) * kFlushStages);
     for (int st = run * kFlushStages; st < st1; ++st) {
       const bool nxt = st + 1 < nst;
-      if (nxt) load(st + 1);
-      const float *A = Ai[st & 1];
-      const float *B = Aj[st & 1];
-#pragma unroll 4
-      for (int p = 0; p < kCovRows / 2; ++p) {
-        float a[4], b[4];
-#pragma unroll
-        for (int cb = 0; cb < 4; ++cb) a[cb] = A[(2 * p + h) * kCovStride + wi * 128 + cb * 32 + r];
-#pragma unroll
-        for (int pb = 0; pb < 4; ++pb) b[pb] = B[(2 * p + h) * kCovStride + wj * 128 + pb * 32 + r];
-#pragma unroll
-        for (int cb = 0; cb < 4; ++cb)
-#pragma unroll
-          for (int pb = 0; pb < 4; ++pb)
-            acc[cb][pb] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[cb], b[pb], acc[cb][pb], 0, 0, 0);
-      }
-      if (nxt) store(st + 1, (st + 1) & 1);
+      mfma_stage((st & 1) ? stA1 : stA0, nxt, st + 1, (st & 1) ? stA0 : stA1);
+      if (nxt) land();
       __syncthreads();
     }
+    // the lane's offset passes through an empty asm statement so that the element
+    // addresses are formed here, not hoisted out of the run loop (they would hold
+    // 128 register pairs for the whole loop); the pointer itself stays a global one
+    // (a flat access here would make every LDS wait of the stage loop wait for
+    // the copies too)
+    int boff = (wi * 128 + 4 * h) * kCT + wj * 64 + r;
+    asm volatile("" : "+v"(boff));
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
-      for (int pb = 0; pb < 4; ++pb)
+      for (int pb = 0; pb < 2; ++pb)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const int il = wi * 128 + cb * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
-          const int jl = wj * 128 + pb * 32 + r;
-          double *o = out + il * kCT + jl;
+          double *o = out + boff + (cb * 32 + 8 * (v >> 2) + (v & 3)) * kCT + pb * 32;
           *o = (run == 0 ? 0.0 : *o) + (double)acc[cb][pb][v];
         }
   }
   if (nrun == 0) {  // no rows: the partial tile is zero
-    for (int e = t; e < kCT * kCT; e += 256) out[e] = 0.0;
+    for (int e = t; e < kCT * kCT; e += kCovThreads) out[e] = 0.0;
   }
 }
 
@@ -310,7 +363,7 @@ km_status launch_pca_cov(const float *X, int64_t n, int d, float *mean, float *c
   void *mws = static_cast<uint8_t *>(ws) + (((size_t)p.nsplit * p.ntiles * kCT * kCT * sizeof(double) + 255) & ~(size_t)255);
   km_status st = launch_colmean(X, n, d, d, mean, mws, s);
   if (st != KM_OK) return st;
-  hipLaunchKernelGGL(cov_kernel, dim3(p.ntiles * p.nsplit), dim3(256), 0, s, X, n, d, mean, p.T, p.ntiles,
+  hipLaunchKernelGGL(cov_kernel, dim3(p.ntiles * p.nsplit), dim3(kCovThreads), 0, s, X, n, d, mean, p.T, p.ntiles,
                      p.rows_per_split, partial);
   hipLaunchKernelGGL(cov_reduce_kernel, dim3(p.ntiles, 16), dim3(256), 0, s, partial, p.ntiles, p.nsplit, p.T, d, n,
                      cov);

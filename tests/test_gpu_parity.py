@@ -395,7 +395,10 @@ def test_quantize_sign1(km, torch, n, d, d0):
 
 # --------------------------------------------------------------------------- PCA
 
-@pytest.mark.parametrize("n,d", [(1, 4), (5000, 64), (20001, 256), (3000, 132)])
+# (30001, 520): three column blocks (six tiles, a partial one), eight row splits
+# with a partial last stage each; the fold of several fp32 runs per split is
+# covered at full size (10M x 1024) by test_c4_pca_full_size
+@pytest.mark.parametrize("n,d", [(1, 4), (5000, 64), (20001, 256), (3000, 132), (30001, 520)])
 def test_pca_cov(km, torch, n, d):
     say(f"pca cov n={n} d={d}")
     lam = np.arange(1, d + 1) ** -0.5
