@@ -59,6 +59,7 @@ import sys
 import time
 
 import numpy as np
+import scipy.linalg
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
@@ -436,9 +437,12 @@ def wl_c4(cfg, torch, km, args):
 
     def step(timer):
         mean, cov = km.pca_fit_cov(X)
-        cov_h = cov.double().cpu().numpy()  # waits for the covariance
+        cov_h = cov.cpu().numpy()  # waits for the covariance
         t0 = time.perf_counter()
-        w, V = np.linalg.eigh(cov_h)  # host eigensolve of the d x d covariance
+        # host eigensolve of the d x d covariance in its own precision (fp32),
+        # LAPACK's divide and conquer
+        w, V = scipy.linalg.eigh(cov_h, driver="evd", check_finite=False)
+        w = w.astype(np.float64)
         order = np.argsort(w)[::-1][:dout]
         W = torch.from_numpy(np.ascontiguousarray(V[:, order], dtype=np.float32)).cuda()
         if timer is not None:
