@@ -621,17 +621,22 @@ static km_status fine_impl(const Points &p, const int32_t *meso, int k_meso, int
   // fp32, SQ8 and bf16: one assignment launch per pass over all meso-clusters
   // (segment and tile tables); other formats launch per meso-cluster
   const int seg_rows = assign_segment_rows(p);
+  // point tiles of the segments with 128-centroid tiles first (n128 of them), then
+  // those with 256-centroid tiles: one launch each
   std::vector<int4> segs;
   std::vector<int2> tiles;
+  int64_t n128 = 0;
   if (seg_rows > 0) {
-    for (int i = 0; i < k_meso; ++i) {
-      if (n_i[i] == 0) continue;
-      const int si = (int)segs.size();
-      segs.push_back(make_int4((int)start[i], (int)n_i[i], (int)off[i], kf[i]));
-      for (int64_t tt = 0; tt * seg_rows < n_i[i]; ++tt) tiles.push_back(make_int2(si, (int)tt));
+    for (int i = 0; i < k_meso; ++i)
+      if (n_i[i] > 0) segs.push_back(make_int4((int)start[i], (int)n_i[i], (int)off[i], kf[i]));
+    for (int cls = 128; cls <= 256; cls += 128) {
+      for (int si = 0; si < (int)segs.size(); ++si) {
+        if (segment_tile_centroids(segs[si].w) != cls) continue;
+        for (int64_t tt = 0; tt * seg_rows < segs[si].y; ++tt) tiles.push_back(make_int2(si, (int)tt));
+      }
+      if (cls == 128) n128 = (int64_t)tiles.size();
     }
   }
-  const int tile_c = segs.empty() ? 256 : segment_tile_centroids(segs.data(), (int)segs.size(), seg_rows);
   const size_t b_segs = al(sizeof(int4) * segs.size());
   const size_t b_tiles = al(sizeof(int2) * tiles.size());
   Scratch ws(s);
@@ -665,8 +670,10 @@ static km_status fine_impl(const Points &p, const int32_t *meso, int k_meso, int
     KMQ_STAGE(clk, kStPrep, launch_prep(q, C, k, wprep, &cp, s));
     st = clk.begin(kStAssign);
     if (st != KM_OK) return st;
-    if (!segs.empty()) {  // every meso-cluster against its own fine centroids, one launch
-      st = launch_assign_segments(q, C, cp, dsegs, dtiles, (int64_t)tiles.size(), tile_c, ap, sc, s);
+    if (!segs.empty()) {  // every meso-cluster against its own fine centroids, one launch per tile size
+      st = launch_assign_segments(q, C, cp, dsegs, dtiles, n128, 128, ap, sc, s);
+      if (st != KM_OK) return st;
+      st = launch_assign_segments(q, C, cp, dsegs, dtiles + n128, (int64_t)tiles.size() - n128, 256, ap, sc, s);
       if (st != KM_OK) return st;
     }
     for (int i = 0; seg_rows == 0 && i < k_meso; ++i) {  // the same, one launch per meso-cluster

@@ -2928,15 +2928,7 @@ km_status launch_assign(const Points &P, const void *C, const CentroidPrep &cp, 
   }
 }
 
-int segment_tile_centroids(const int4 *segs, int nseg, int seg_rows) {
-  int64_t w128 = 0, w256 = 0;
-  for (int i = 0; i < nseg; ++i) {
-    const int64_t nt = cdiv(segs[i].y, seg_rows);
-    w128 += nt * cdiv(segs[i].w, 128) * 128;
-    w256 += nt * cdiv(segs[i].w, 256) * 256;
-  }
-  return w128 < w256 ? 128 : 256;
-}
+int segment_tile_centroids(int k_seg) { return k_seg <= 128 ? 128 : 256; }
 
 int assign_segment_rows(const Points &P) {
   if (P.fmt == KM_F32) return kQT;

@@ -82,12 +82,12 @@ size_t prep_bytes(const Points &P, int k);
 // [segs[i].z, + segs[i].w) of C and of the prepared constants; workgroup b takes
 // point tile tiles[b].y of segment tiles[b].x (tiles of assign_segment_rows(P) rows;
 // 0 = not supported for these points).  assign and score are indexed by absolute
-// row; centroid indices are absolute.  tile_c: centroids per tile (128 or 256), from
-// segment_tile_centroids over the host copy of segs.
+// row; centroid indices are absolute.  tile_c: centroids per tile (128 or 256) of
+// every segment of the launch (segment_tile_centroids picks it per segment).
 int assign_segment_rows(const Points &P);
-// 128 or 256: the tile size with the smaller padded work, the sum over segments of
-// point tiles x centroid rows rounded up to the tile (256 on ties)
-int segment_tile_centroids(const int4 *segs, int nseg, int seg_rows);
+// 128 for a segment of at most 128 centroids, else 256: the 256-centroid kernel
+// does more MFMA work per stage, which outweighs its extra padding from 129 on
+int segment_tile_centroids(int k_seg);
 km_status launch_assign_segments(const Points &P, const void *C, const CentroidPrep &cp, const int4 *segs,
                                  const int2 *tiles, int64_t ntiles, int tile_c, int32_t *assign, float *score,
                                  hipStream_t s);

@@ -88,7 +88,8 @@ def meso_labels(n, k_meso, seed, empty=None, invalid=0):
 
 
 # (n, d, k_meso, k, iters, empty meso-cluster, invalid ids); d = 1040 selects without
-# packed keys (128- and 256-centroid segment tiles)
+# packed keys; (700, 16, 5, 700) has meso-clusters on both sides of 128 fine
+# centroids, so one pass runs both segment launches (128- and 256-centroid tiles)
 SQ8_CASES = [(1, 16, 1, 1, 2, None, 0), (300, 16, 1, 17, 3, None, 0), (1000, 32, 4, 20, 3, None, 0),
              (5000, 64, 10, 100, 4, 3, 20), (3001, 768, 32, 1000, 2, None, 0), (2000, 48, 7, 7, 2, None, 0),
              (700, 16, 5, 700, 1, None, 0), (400, 1040, 3, 300, 1, None, 0), (600, 1040, 2, 400, 1, None, 0)]
