@@ -224,7 +224,7 @@ constexpr int kPStride = 32 + 4;  // floats per LDS row of a projection stage
 // Workgroups are numbered so that the output tiles of one point tile land on the
 // same XCD one after another (consecutive ids are spread over the 8 XCDs), so the
 // point rows come from HBM once and from that XCD's L2 for the other tiles.
-__global__ __launch_bounds__(256) void project_kernel(const float *X, int64_t n, int d, int64_t ldx,
+__global__ __launch_bounds__(256) void project_staged_kernel(const float *X, int64_t n, int d, int64_t ldx,
                                                       const float *mean, const float *Wt, int d_out, float *Y,
                                                       int n_ptiles, int n_otiles) {
   __shared__ float Xs[2][kT * kPStride];
@@ -322,6 +322,147 @@ struct CovPlan {
   int64_t rows_per_split;
 };
 
+// Projection, direct-copy design (d <= kProjMaxD, ldx % 4 == 0, 256 rows of X
+// within 2 GB): the 8-wave shape of the fp32 assignment kernel with the points as
+// the first MFMA operand and the rows of W^T as the second, so a lane's outputs
+// are consecutive output dims of one point and the stores are coalesced.  A
+// workgroup computes 256 points x 256 outputs; stages of 32 dims (128 bytes of
+// every row: 256 point rows, then 256 rows of W^T) are copied straight from global
+// memory into LDS in the XOR slot layout (chunk c of row R in slot c ^ ((R >> 1) &
+// 7)), two stage buffers, one workgroup per CU.  The mean sits in LDS (zero past
+// d) and the point operands are centred as they are read (x - mean in fp32, the
+// value a centring copy would store).  Chunks past d are zero-filled; rows past n
+// or d_out are clamped to the last one and their outputs are not stored.
+constexpr int kProjMaxD = 4096;
+constexpr int kPT = 256;  // points and outputs per workgroup
+
+__global__ __launch_bounds__(512, 1) void project_kernel(const float *X, int64_t n, int d, int64_t ldx,
+                                                         const float *mean, const float *Wt, int d_out, float *Y,
+                                                         int n_ptiles, int n_otiles) {
+  constexpr int NCP = kPT / 64;            // point copies per thread and stage
+  constexpr int NCOPY = 2 * kPT / 64;      // all copies per thread and stage
+  constexpr int STAGE = 2 * kPT * 128;     // bytes: point rows, then W^T rows
+  __shared__ __align__(16) uint8_t pst0[STAGE];
+  __shared__ __align__(16) uint8_t pst1[STAGE];
+  __shared__ __align__(16) float msh[kProjMaxD + 32];
+  // workgroup ids, tiles and bases are wave-uniform: computed in 32 bits and
+  // pinned to scalar registers (the copies take their bases there)
+  const int b = (int)blockIdx.x;
+  const int group = __builtin_amdgcn_readfirstlane(b / (8 * n_otiles));  // 8 point tiles per group
+  const int rem = __builtin_amdgcn_readfirstlane(b % (8 * n_otiles));
+  const int ptile = group * 8 + rem % 8;
+  const int otile = rem / 8;
+  if (ptile >= n_ptiles) return;  // whole workgroup, before any barrier
+  const int64_t p0 = (int64_t)ptile * kPT;
+  const int o0 = otile * kPT;
+  const int t = threadIdx.x, lane = t & 63, wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int r = lane & 31, h = lane >> 5;
+  const int wc = wave & 1, wp = wave >> 1;  // 128-point half, 64-output quarter
+  const int prmax = (int)min<int64_t>(n - 1 - p0, kPT - 1);
+  const int ormax = min(d_out - 1 - o0, kPT - 1);
+  const int S = (d + 31) / 32;
+  for (int i = t; i < 32 * S; i += 512) msh[i] = i < d ? mean[i] : 0.f;
+  const float *xbase = X + p0 * ldx;
+  const float *wbase = Wt + (int64_t)o0 * d;
+
+  // copy i of a wave fills slots (8 i + wave) 64 .. + 63: rows 0 .. 255 are points,
+  // rows 256 .. 511 rows of W^T; byte offsets from the stage's first dim
+  uint32_t soff[NCOPY];
+#pragma unroll
+  for (int i = 0; i < NCOPY; ++i) {
+    const int slot = (i * 8 + wave) * 64 + lane;
+    const int row = slot >> 3;
+    const int chunk = (slot & 7) ^ ((row >> 1) & 7);
+    soff[i] = i < NCP ? (uint32_t)(min(row, prmax) * (int)ldx * 4 + 16 * chunk)
+                      : (uint32_t)(min(row - kPT, ormax) * d * 4 + 16 * chunk);
+  }
+  auto copy = [&](int st, uint8_t *dst, int i) {
+    const int slot = (i * 8 + wave) * 64 + lane;
+    const int row = slot >> 3;
+    const int chunk = (slot & 7) ^ ((row >> 1) & 7);
+    lds_u8 *w = (lds_u8 *)dst + (i * 8 + wave) * 1024;
+    // the stage's first dim of the points or of W^T, pinned to scalar registers
+    const float *src = (i < NCP ? xbase : wbase) + 32 * st;
+    const uint64_t su = (uint64_t)(size_t)src;
+    const void *base = (const void *)(size_t)(((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(su >> 32)) << 32) |
+                                              (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)su));
+    if (32 * st + 4 * chunk < d) {
+      lds_copy16(base, soff[i], (uint32_t)(size_t)w);
+    } else {
+      __attribute__((address_space(3))) uint32_t *z = (__attribute__((address_space(3))) uint32_t *)(w + 16 * lane);
+      z[0] = z[1] = z[2] = z[3] = 0u;
+    }
+  };
+  auto land = [&]() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); };
+
+  f32x16 acc[4][2];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[a][c][v] = 0.f;
+  // one stage: four steps of 8 dims; the operand reads of step g + 1 and two of
+  // the next stage's copies go out before step g's MFMAs
+  auto mfma_stage = [&](int st, const uint8_t *buf, bool copying, uint8_t *nxt) {
+    f32x4 av[2][4], bv[2][2];
+    auto read = [&](int g, int set) {
+      const int so = 16 * ((2 * g + h) ^ ((r >> 1) & 7));
+      const f32x4 m4 = *reinterpret_cast<const f32x4 *>(&msh[32 * st + 8 * g + 4 * h]);
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb)
+        av[set][cb] = *reinterpret_cast<const f32x4 *>(buf + (wc * 128 + cb * 32 + r) * 128 + so) - m4;
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb)
+        bv[set][pb] = *reinterpret_cast<const f32x4 *>(buf + (kPT + wp * 64 + pb * 32 + r) * 128 + so);
+    };
+    read(0, 0);
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int cur = g & 1;
+      if (g + 1 < 4) read(g + 1, cur ^ 1);
+      __builtin_amdgcn_sched_barrier(0);
+      if (copying) {
+        copy(st + 1, nxt, 2 * g);
+        copy(st + 1, nxt, 2 * g + 1);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+          for (int pb = 0; pb < 2; ++pb)
+            acc[cb][pb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[cur][cb][e], bv[cur][pb][e], acc[cb][pb], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+#pragma unroll
+  for (int i = 0; i < NCOPY; ++i) copy(0, pst0, i);
+  land();
+  __syncthreads();  // also publishes the mean
+  for (int st = 0; st < S; ++st) {
+    const bool nxt = st + 1 < S;
+    mfma_stage(st, (st & 1) ? pst1 : pst0, nxt, (st & 1) ? pst0 : pst1);
+    if (nxt) land();
+    __syncthreads();
+  }
+  // lane (r, h) of block (cb, pb) holds points wc 128 + cb 32 + 8 i4 + 4 h + e of
+  // output wp 64 + pb 32 + r
+#pragma unroll
+  for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb) {
+      const int o = o0 + wp * 64 + pb * 32 + r;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int64_t p = p0 + wc * 128 + cb * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
+        if (p < n && o < d_out) Y[p * d_out + o] = acc[cb][pb][v];
+      }
+    }
+}
+
 // One covariance workgroup fills a CU (LDS), so the number of (tile, split)
 // workgroups is kept just under a whole number of passes over the CUs.
 CovPlan cov_plan(int64_t n, int d) {
@@ -378,10 +519,17 @@ km_status launch_pca_project(const float *X, int64_t n, int d, int64_t ldx, cons
   float *Wt = static_cast<float *>(ws);
   const int64_t e = (int64_t)d * d_out;
   hipLaunchKernelGGL(transpose_kernel, dim3((unsigned)cdiv(e, 256)), dim3(256), 0, s, W, d, d_out, Wt);
-  const int n_ptiles = (int)cdiv(n, kT), n_otiles = (int)cdiv(d_out, kT);
-  const int64_t nblk = cdiv(n_ptiles, 8) * 8 * n_otiles;
-  hipLaunchKernelGGL(project_kernel, dim3((unsigned)nblk), dim3(256), 0, s, X, n, d, ldx, mean, Wt, d_out, Y,
-                     n_ptiles, n_otiles);
+  if (d <= kProjMaxD && ldx % 4 == 0 && (int64_t)kPT * ldx * 4 < ((int64_t)1 << 31)) {
+    const int n_ptiles = (int)cdiv(n, kPT), n_otiles = (int)cdiv(d_out, kPT);
+    const int64_t nblk = cdiv(n_ptiles, 8) * 8 * n_otiles;
+    hipLaunchKernelGGL(project_kernel, dim3((unsigned)nblk), dim3(512), 0, s, X, n, d, ldx, mean, Wt, d_out, Y,
+                       n_ptiles, n_otiles);
+  } else {
+    const int n_ptiles = (int)cdiv(n, kT), n_otiles = (int)cdiv(d_out, kT);
+    const int64_t nblk = cdiv(n_ptiles, 8) * 8 * n_otiles;
+    hipLaunchKernelGGL(project_staged_kernel, dim3((unsigned)nblk), dim3(256), 0, s, X, n, d, ldx, mean, Wt, d_out,
+                       Y, n_ptiles, n_otiles);
+  }
   KMQ_LAUNCH_CHECK("pca_project");
   return KM_OK;
 }
