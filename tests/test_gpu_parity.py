@@ -433,6 +433,23 @@ def test_pca_project(km, torch, n, d, dout):
     np.testing.assert_allclose(Yh, Y_o, rtol=0, atol=2e-5 * scale)
 
 
+# (1500, 1024, 300): two output tiles, the second partial; (257, 36, 40): one
+# partial stage and a partial output tile; (300, 4100, 8): past the direct-copy
+# kernel's 4096 dims, the register-staged kernel.  W is a seeded orthonormal basis
+# (an input), so no eigensolve of a large covariance is needed.
+@pytest.mark.parametrize("n,d,dout", [(1500, 1024, 300), (257, 36, 40), (300, 4100, 8)])
+def test_pca_project_shapes(km, torch, n, d, dout):
+    say(f"pca project shapes n={n} d={d} dout={dout}")
+    X = blobs(n, d, 5, seed=n + d + dout) + np.float32(0.25)
+    mean = X.astype(np.float64).mean(0).astype(np.float32)
+    W = np.linalg.qr(np.random.default_rng(d + dout).standard_normal((d, dout)))[0].astype(np.float32)
+    Y_o = orc.project(X, mean, W)
+    Y = km.pca_project(to_dev(X, torch), to_dev(mean, torch), to_dev(W, torch))
+    torch.cuda.synchronize()
+    scale = np.abs(Y_o).max() + 1e-30
+    np.testing.assert_allclose(host(Y), Y_o, rtol=0, atol=2e-5 * scale)
+
+
 # --------------------------------------------------------------------------- Lloyd
 
 def test_fit_f32_lockstep_config1(km, torch):
