@@ -807,6 +807,25 @@ def wl_hier(fmt):
             vanilla_ms = 1e3 * (11 * (t1 - t0) + 10 * (t2 - t1))
             q["vanilla_f32_T10_ms_estimate"] = vanilla_ms
             q["speedup_vs_vanilla_f32"] = vanilla_ms / float(res["ph"].sum())
+            # Sec. 4.4 taken literally: round(sqrt(n_i)) fine clusters per meso-cluster
+            # (the same meso partition: the meso phase is deterministic), C sized to their sum
+            n_i = torch.bincount(res["am"].long(), minlength=kmeso).cpu().numpy().astype(np.int64)
+            r = np.floor(np.sqrt(n_i.astype(np.float64))).astype(np.int64)
+            r -= (r * r > n_i)
+            r += ((r + 1) * (r + 1) <= n_i)
+            cap = int(np.where(n_i > 0, np.where(n_i - r * r > r, r + 1, r), 0).sum())
+            log(f"quality: the paper's literal fine counts ({cap} fine clusters), outside the timed region")
+            P = P32 if fmt == "f32" else km.points_sq8(km.quantize_sq8(X)[0])
+            C2, a2, kf2, _, ph2 = km.kmeans_fit_hier(P, cap, init, Tm, Tf, 0, k_meso=kmeso, objective=False,
+                                                     phases=True, sqrt_rule=True)
+            mu2 = torch.empty((len(C2), spec.d), dtype=torch.float32, device="cuda")
+            lit = partition_stats(km, X, a2, mu2)
+            lit.update(k_fine_total=int(kf2.sum()), ms_per_fit=float(ph2.sum()),
+                       phase_ms={"meso": float(ph2[0]), "fine": float(ph2[1])})
+            lit["meso_sizes"] = {"min": int(n_i.min()), "max": int(n_i.max()),
+                                 "cv": float(n_i.std() / max(n_i.mean(), 1e-30))}
+            q["sqrt_rule"] = lit
+            q["objective_ratio_sqrt_rule_vs_reading"] = lit["cost"] / q[fmt]["cost"]
             return q
 
         return step, finish, cpu_baseline, quality

@@ -314,6 +314,7 @@ km_status kmeans_fit_pruned(const km_points *P, int32_t k, int32_t iters, const 
 
 /* kmeans_fine() flags */
 #define KM_FINE_C_GIVEN 1 /* C holds the initial fine centroids; otherwise they are taken from the points */
+#define KM_FINE_SQRT 2    /* the paper's fine counts, k_i = round(sqrt(n_i)) (see kmeans_fine) */
 
 /*
  * kmeans_fine -- FINE-CLUSTERING of hierarchical k-means (Sec. 4.4, Table 7):
@@ -327,6 +328,10 @@ km_status kmeans_fit_pruned(const km_points *P, int32_t k, int32_t iters, const 
  *     the smaller meso index).  Fine centroid j of meso-cluster i is centroid
  *     off_i + j of C, off_i = k_0 + ... + k_{i-1}.  KM_EINVAL unless m <= k <= the
  *     number of points with a valid meso id.
+ *   With flags & KM_FINE_SQRT, the counts of Sec. 4.4 taken literally: k_i = the
+ *     integer nearest to sqrt(n_i) for every non-empty meso-cluster (their sum is
+ *     set by the data); k is then the capacity of C: KM_EINVAL if the k_i sum to
+ *     more, and the rows of C past their sum are left as they are.
  *   STEP 1 (unless flags has KM_FINE_C_GIVEN): centroid off_i + j = the member of
  *     meso-cluster i at position floor(j n_i / k_i) in ascending point order.
  *   Then `iters` x (STEP 2 against the point's own meso-cluster's centroids, STEP 3
@@ -348,6 +353,8 @@ typedef struct km_hier_params {
   int32_t iters_meso;   /* Lloyd iterations of MESO-CLUSTERING */
   int32_t iters_fine;   /* Lloyd iterations inside every meso-cluster */
   int32_t iters_refine; /* vanilla Lloyd iterations over all points and all k centroids afterwards; 0 = none */
+  int32_t flags;        /* KM_FINE_SQRT: the paper's fine counts; k is then the capacity of C and the refinement
+                           runs on the fine centroids made (their number is the sum of k_fine) */
 } km_hier_params;
 
 /*

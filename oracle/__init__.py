@@ -484,6 +484,8 @@ def fit(P: dict, k: int, iters: int, init_idx, policy: int = EMPTY_SPLIT, C0=Non
     those instead of the compressed points (the raw-vector last iteration of
     Sec. 4.1 that removes the outward bias of decoded 1-bit codes)."""
     C = init_centroids(P, init_idx) if C0 is None else np.array(C0, copy=True)
+    if len(C) != k:
+        raise ValueError(f"{len(C)} initial centroids for k = {k}")
     J = []
     for t in range(iters):
         a, dist = assign(P, C)
@@ -554,23 +556,48 @@ def fine_counts(n_meso, k: int):
     return np.asarray(ks, dtype=np.int32)
 
 
+def fine_counts_sqrt(n_meso):
+    """Fine clusters per meso-cluster as Sec. 4.4 states them: the integer nearest to
+    sqrt(n_i) for every non-empty meso-cluster (0 for an empty one).  Exact integer
+    arithmetic: r = floor(sqrt(v)), and r + 1 when v - r^2 > r (sqrt(v) > r + 1/2
+    exactly then, since (r + 1/2)^2 = r^2 + r + 1/4); never a tie.  1 <= k_i <= n_i."""
+    out = []
+    for v in (int(x) for x in n_meso):
+        if v <= 0:
+            out.append(0)
+            continue
+        r = 0
+        while (r + 1) * (r + 1) <= v:
+            r += 1
+        out.append(r + 1 if v - r * r > r else r)
+    return np.asarray(out, dtype=np.int32)
+
+
 def fine_init_positions(n_i: int, k_i: int):
     """Initial fine centroids of a meso-cluster: its members (ascending point index)
     at positions floor(j n_i / k_i), j = 0 .. k_i - 1 (distinct since k_i <= n_i)."""
     return (np.arange(k_i, dtype=np.int64) * n_i) // k_i
 
 
-def fit_fine(P: dict, a_meso, k_meso: int, k: int, iters: int, policy: int = EMPTY_SPLIT, C0=None):
+def fit_fine(P: dict, a_meso, k_meso: int, k: int, iters: int, policy: int = EMPTY_SPLIT, C0=None,
+             sqrt_rule: bool = False):
     """FINE-CLUSTERING: Lloyd (T = iters) inside every meso-cluster i on its members,
-    with k_i fine centroids; fine centroid j of meso-cluster i is global centroid
-    off_i + j, off_i = k_0 + ... + k_{i-1}.  C0 (optional, k rows) replaces the
-    initial centroids.  Returns (C, a, k_i, J) with J[t] the in-space objective of
-    pass t summed over the meso-clusters; points with a meso id outside [0, k_meso)
-    get -1."""
+    with k_i fine centroids (fine_counts; with sqrt_rule fine_counts_sqrt, k then
+    being an upper bound on their sum); fine centroid j of meso-cluster i is global
+    centroid off_i + j, off_i = k_0 + ... + k_{i-1}.  C0 (optional, sum k_i rows)
+    replaces the initial centroids.  Returns (C, a, k_i, J) with C holding sum k_i
+    rows and J[t] the in-space objective of pass t summed over the meso-clusters;
+    points with a meso id outside [0, k_meso) get -1."""
     a_meso = np.asarray(a_meso, dtype=np.int64)
     valid = (a_meso >= 0) & (a_meso < k_meso)
     n_i = np.bincount(a_meso[valid], minlength=k_meso)
-    k_i = fine_counts(n_i, k)
+    if sqrt_rule:
+        k_i = fine_counts_sqrt(n_i)
+        if int(k_i.sum()) > k:
+            raise ValueError("the fine counts exceed k")
+        k = int(k_i.sum())
+    else:
+        k_i = fine_counts(n_i, k)
     off = np.concatenate([[0], np.cumsum(k_i)])
     a = np.full(len(a_meso), -1, dtype=np.int32)
     C = None
@@ -591,20 +618,20 @@ def fit_fine(P: dict, a_meso, k_meso: int, k: int, iters: int, policy: int = EMP
 
 
 def fit_hier(P: dict, k: int, iters_meso: int, iters_fine: int, iters_refine: int, init_meso,
-             k_meso: int = 0, policy: int = EMPTY_SPLIT):
+             k_meso: int = 0, policy: int = EMPTY_SPLIT, sqrt_rule: bool = False):
     """Hierarchical k-means.  MESO: Lloyd with k_meso (default meso_count(k))
-    centroids on all points from the rows init_meso; FINE: fit_fine; REFINE:
-    iters_refine vanilla Lloyd iterations over all points with all k centroids
-    (then a final assignment), the last update from P["raw"] if given.  Meso and
-    fine use the compressed points only.  Returns (C, a, J, info) with J the
-    in-space objective of the returned partition."""
+    centroids on all points from the rows init_meso; FINE: fit_fine (sqrt_rule as
+    there); REFINE: iters_refine vanilla Lloyd iterations over all points with all
+    the fine centroids (then a final assignment), the last update from P["raw"] if
+    given.  Meso and fine use the compressed points only.  Returns (C, a, J, info)
+    with J the in-space objective of the returned partition."""
     km = k_meso if k_meso else meso_count(k)
     Pc = subset(P, slice(None))
     Cm, am, Jm = fit(Pc, km, iters_meso, init_meso, policy)
-    C, a, k_i, Jf = fit_fine(Pc, am, km, k, iters_fine, policy)
+    C, a, k_i, Jf = fit_fine(Pc, am, km, k, iters_fine, policy, sqrt_rule=sqrt_rule)
     J = float(Jf[-1])
     if iters_refine > 0:
-        C, a, Jr = fit(P, k, iters_refine, None, policy, C0=C)
+        C, a, Jr = fit(P, len(C), iters_refine, None, policy, C0=C)
         J = float(Jr[-1])
     return C, a, J, {"k_meso": km, "C_meso": Cm, "a_meso": am, "J_meso": Jm, "k_fine": k_i, "J_fine": Jf}
 

@@ -20,6 +20,7 @@ KM_F32, KM_BF16, KM_SQ8, KM_SIGN1, KM_HYBRID, KM_RABITQ, KM_LVQ4 = 0, 1, 2, 3, 4
 KM_EMPTY_SPLIT, KM_EMPTY_KEEP = 0, 1
 KM_Q_FIT_PARAMS = 1
 KM_FINE_C_GIVEN = 1
+KM_FINE_SQRT = 2
 STATUS = {0: "KM_OK", -1: "KM_EINVAL", -2: "KM_EUNSUPPORTED", -3: "KM_ENOMEM", -4: "KM_EDEVICE"}
 EXPORTS = ("quantize", "rabitq_encode", "pca_fit_cov", "pca_project", "kmeans_assign", "kmeans_assign_noalloc",
            "kmeans_update",
@@ -54,7 +55,7 @@ class KmPrune(ct.Structure):
 
 class KmHierParams(ct.Structure):
     _fields_ = [("k_meso", ct.c_int32), ("iters_meso", ct.c_int32), ("iters_fine", ct.c_int32),
-                ("iters_refine", ct.c_int32)]
+                ("iters_refine", ct.c_int32), ("flags", ct.c_int32)]
 
 
 _lib = None
@@ -436,9 +437,12 @@ def kmeans_fit_pruned(P: Points, k: int, iters: int, init_idx=None, C: torch.Ten
 
 
 def kmeans_fine(P: Points, meso_assign: torch.Tensor, k_meso: int, k: int, iters: int,
-                C: torch.Tensor | None = None, policy: int = KM_EMPTY_SPLIT, objective: bool = False):
+                C: torch.Tensor | None = None, policy: int = KM_EMPTY_SPLIT, objective: bool = False,
+                sqrt_rule: bool = False):
     """FINE-CLUSTERING inside each meso-cluster (hierarchical k-means).  C given: the
     initial fine centroids (k rows); otherwise they are taken from the points.
+    sqrt_rule: k_i = round(sqrt(n_i)) (the paper's counts), k being the capacity of C;
+    the returned C then holds the k_fine.sum() fine centroids made.
     Returns (C, assign int32[n], k_fine numpy int32[k_meso], objective double[1] or None)."""
     _dev(meso_assign, torch.int32, "meso_assign", 1)
     if meso_assign.shape[0] != P.n:
@@ -453,16 +457,21 @@ def kmeans_fine(P: Points, meso_assign: torch.Tensor, k_meso: int, k: int, iters
     a = torch.empty(P.n, dtype=torch.int32, device=P.device)
     kf = np.zeros(k_meso, dtype=np.int32)
     obj = torch.empty(1, dtype=torch.float64, device=P.device) if objective else None
+    if sqrt_rule:
+        flags |= KM_FINE_SQRT
     _check(lib().kmeans_fine(P.ref, _ptr(meso_assign), k_meso, k, iters, flags, _ptr(C), _ptr(a),
                              kf.ctypes.data_as(ct.c_void_p), _ptr(obj), policy, _stream()))
-    return C, a, kf, obj
+    return (C[:int(kf.sum())] if sqrt_rule else C), a, kf, obj
 
 
 def kmeans_fit_hier(P: Points, k: int, init_meso, iters_meso: int, iters_fine: int, iters_refine: int = 0,
                     k_meso: int = 0, policy: int = KM_EMPTY_SPLIT, objective: bool = True,
-                    stats: KmFitStats | None = None, phases: bool = False, meso: bool = False):
+                    stats: KmFitStats | None = None, phases: bool = False, meso: bool = False,
+                    sqrt_rule: bool = False):
     """Hierarchical k-means: meso Lloyd with k_meso (0 = round(sqrt(k))) centroids from
     the rows init_meso, Lloyd inside every meso-cluster, optional vanilla refinement.
+    sqrt_rule: the paper's fine counts round(sqrt(n_i)); k is then the capacity of C
+    and the returned C holds the k_fine.sum() centroids made.
     Returns (C, assign, k_fine numpy int32[k_meso], objective double[1] or None,
     phase times [meso, fine, refine] in ms or None); with meso=True the meso
     assignment (int32[n]) is appended."""
@@ -470,7 +479,7 @@ def kmeans_fit_hier(P: Points, k: int, init_meso, iters_meso: int, iters_fine: i
     km = k_meso if k_meso else len(idx)
     if idx.ndim != 1 or len(idx) != km:
         raise ValueError("init_meso must hold k_meso indices")
-    hp = KmHierParams(k_meso, iters_meso, iters_fine, iters_refine)
+    hp = KmHierParams(k_meso, iters_meso, iters_fine, iters_refine, KM_FINE_SQRT if sqrt_rule else 0)
     C = torch.empty((k, P.d), dtype=P.centroid_dtype(), device=P.device)
     a = torch.empty(P.n, dtype=torch.int32, device=P.device)
     kf = np.zeros(len(idx), dtype=np.int32)
@@ -481,6 +490,8 @@ def kmeans_fit_hier(P: Points, k: int, init_meso, iters_meso: int, iters_fine: i
                                  kf.ctypes.data_as(ct.c_void_p), _ptr(obj), policy,
                                  ct.byref(stats) if stats is not None else None,
                                  ph.ctypes.data_as(ct.c_void_p) if phases else None, _stream()))
+    if sqrt_rule:
+        C = C[:int(kf.sum())]
     return (C, a, kf, obj, ph, am) if meso else (C, a, kf, obj, ph)
 
 

@@ -6,6 +6,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <cmath>
 #include <mutex>
 #include <new>
 #include <vector>
@@ -567,9 +568,27 @@ static std::vector<int> fine_counts(const std::vector<int64_t> &n_i, int k) {
   return ks;
 }
 
-// FINE-CLUSTERING (Sec. 4.4) on validated arguments.
+// The paper's fine counts (Sec. 4.4): the integer nearest to sqrt(n_i) for every
+// non-empty meso-cluster (never a tie for integer n_i; at least 1 and at most n_i).
+static std::vector<int> fine_counts_sqrt(const std::vector<int64_t> &n_i) {
+  std::vector<int> ks(n_i.size(), 0);
+  for (size_t i = 0; i < n_i.size(); ++i) {
+    const int64_t v = n_i[i];
+    if (v <= 0) continue;
+    int64_t r = (int64_t)std::sqrt((double)v);
+    while (r * r > v) --r;
+    while ((r + 1) * (r + 1) <= v) ++r;
+    ks[i] = (int)(v - r * r > r ? r + 1 : r);
+  }
+  return ks;
+}
+
+// FINE-CLUSTERING (Sec. 4.4) on validated arguments.  sqrt_rule: the paper's fine
+// counts, k being the capacity of C; *k_used (nullable) receives the number of fine
+// centroids.
 static km_status fine_impl(const Points &p, const int32_t *meso, int k_meso, int k, int iters, bool c_given,
-                           void *C, int32_t *assign, int32_t *k_fine, double *objective, int policy, StageClock &clk,
+                           bool sqrt_rule, int *k_used, void *C, int32_t *assign, int32_t *k_fine, double *objective,
+                           int policy, StageClock &clk,
                            hipStream_t s) {
   km_status st;
   // meso-cluster order of the points (stable) and the meso-cluster sizes
@@ -588,10 +607,21 @@ static km_status fine_impl(const Points &p, const int32_t *meso, int k_meso, int
     m += v > 0;
   }
   KMQ_CHECK(N >= 1, KM_EINVAL, "no point has a meso-cluster id in [0, %d)", k_meso);
-  KMQ_CHECK(m <= k && k <= N, KM_EINVAL,
-            "k = %d must lie between the number of non-empty meso-clusters (%lld) and the number of points with a "
-            "meso-cluster (%lld)", k, (long long)m, (long long)N);
-  const std::vector<int> kf = fine_counts(n_i, k);
+  std::vector<int> kf;
+  if (sqrt_rule) {
+    kf = fine_counts_sqrt(n_i);
+    int64_t kt = 0;
+    for (int v : kf) kt += v;
+    KMQ_CHECK(kt <= k, KM_EINVAL, "the fine counts sum to %lld, more than the %d centroids C holds", (long long)kt,
+              k);
+    k = (int)kt;  // the rest of C is left as it is
+  } else {
+    KMQ_CHECK(m <= k && k <= N, KM_EINVAL,
+              "k = %d must lie between the number of non-empty meso-clusters (%lld) and the number of points with a "
+              "meso-cluster (%lld)", k, (long long)m, (long long)N);
+    kf = fine_counts(n_i, k);
+  }
+  if (k_used) *k_used = k;
   std::vector<int64_t> start(k_meso), off(k_meso + 1, 0);
   for (int i = 0, acc = 0; i < k_meso; ++i) {
     start[i] = acc;
@@ -877,13 +907,13 @@ km_status kmeans_fine(const km_points *P, const int32_t *meso_assign, int32_t k_
   KMQ_CHECK(meso_assign != nullptr && assign != nullptr, KM_EINVAL, "meso_assign or assign is NULL");
   KMQ_CHECK(k_meso >= 1, KM_EINVAL, "k_meso = %d must be >= 1", k_meso);
   KMQ_CHECK(iters >= 0, KM_EINVAL, "iters = %d must be >= 0", iters);
-  KMQ_CHECK((flags & ~KM_FINE_C_GIVEN) == 0, KM_EINVAL, "unknown flags 0x%x", flags);
+  KMQ_CHECK((flags & ~(KM_FINE_C_GIVEN | KM_FINE_SQRT)) == 0, KM_EINVAL, "unknown flags 0x%x", flags);
   KMQ_CHECK(policy == KM_EMPTY_SPLIT || policy == KM_EMPTY_KEEP, KM_EINVAL, "unknown empty-cluster policy %d", policy);
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   try {
     StageClock clk(false, s);
-    return fine_impl(p, meso_assign, k_meso, k, iters, (flags & KM_FINE_C_GIVEN) != 0, C, assign, k_fine, objective,
-                     policy, clk, s);
+    return fine_impl(p, meso_assign, k_meso, k, iters, (flags & KM_FINE_C_GIVEN) != 0, (flags & KM_FINE_SQRT) != 0,
+                     nullptr, C, assign, k_fine, objective, policy, clk, s);
   } catch (const std::bad_alloc &) {
     set_error("host allocation failed");
     return KM_ENOMEM;
@@ -906,6 +936,7 @@ km_status kmeans_fit_hier(const km_points *P, int32_t k, const km_hier_params *h
   KMQ_CHECK(km >= 1 && km <= k, KM_EINVAL, "k_meso = %d must lie in [1, k]", km);
   KMQ_CHECK(hp->iters_meso >= 0 && hp->iters_fine >= 0 && hp->iters_refine >= 0, KM_EINVAL,
             "iteration counts must be >= 0");
+  KMQ_CHECK((hp->flags & ~KM_FINE_SQRT) == 0, KM_EINVAL, "unknown hierarchical flags 0x%x", hp->flags);
   KMQ_CHECK(policy == KM_EMPTY_SPLIT || policy == KM_EMPTY_KEEP, KM_EINVAL, "unknown empty-cluster policy %d", policy);
   st = check_init_idx(init_meso, km, p.n);
   if (st != KM_OK) return st;
@@ -939,12 +970,13 @@ km_status kmeans_fit_hier(const km_points *P, int32_t k, const km_hier_params *h
     st = fit_impl(pc, km, hp->iters_meso, init_meso, Cm, am, nullptr, policy, clk, s);
     if (st != KM_OK) return st;
     if (phase_ms) KMQ_HIP(hipEventRecord(ev[1], s));
-    st = fine_impl(pc, am, km, k, hp->iters_fine, false, C, assign, k_fine, R > 0 ? nullptr : objective, policy, clk,
-                   s);
+    int kt = k;  // fine centroids made (fewer than k under the paper's counts)
+    st = fine_impl(pc, am, km, k, hp->iters_fine, false, (hp->flags & KM_FINE_SQRT) != 0, &kt, C, assign, k_fine,
+                   R > 0 ? nullptr : objective, policy, clk, s);
     if (st != KM_OK) return st;
     if (phase_ms) KMQ_HIP(hipEventRecord(ev[2], s));
     if (R > 0) {
-      st = fit_impl(p, k, R, nullptr, C, assign, objective ? objr : nullptr, policy, clk, s);
+      st = fit_impl(p, kt, R, nullptr, C, assign, objective ? objr : nullptr, policy, clk, s);
       if (st != KM_OK) return st;
       if (objective) KMQ_HIP(hipMemcpyAsync(objective, objr + R, sizeof(double), hipMemcpyDeviceToDevice, s));
     }

@@ -213,7 +213,7 @@ def test_hierarchical_argument_checks(kmq):
         (ok[:1] + (None,) + ok[2:], "NULL"),
         (ok[:2] + (0,) + ok[3:], "k_meso"),
         (ok[:4] + (-1,) + ok[5:], "iters"),
-        (ok[:5] + (2,) + ok[6:], "flags"),
+        (ok[:5] + (4,) + ok[6:], "flags"),  # 1 and 2 (KM_FINE_C_GIVEN, KM_FINE_SQRT) are known
         (ok[:10] + (5,) + ok[11:], "policy"),
         (ok[:6] + (None,) + ok[7:], "centroids"),
         (ok[:7] + (None,) + ok[8:], "NULL"),
@@ -229,7 +229,8 @@ def test_hierarchical_argument_checks(kmq):
         args[i] = v
         assert L.kmeans_fit_hier(*args) == -1, msg
         assert msg in L.km_last_error().decode(), (msg, L.km_last_error())
-    for params, msg in [((11, 2, 2, 0), "k_meso"), ((3, -1, 2, 0), "iteration"), ((3, 2, 2, -2), "iteration")]:
+    for params, msg in [((11, 2, 2, 0), "k_meso"), ((3, -1, 2, 0), "iteration"), ((3, 2, 2, -2), "iteration"),
+                        ((3, 2, 2, 0, 4), "flags")]:
         hp2 = kmq.KmHierParams(*params)
         args = list(base)
         args[2] = ct.byref(hp2)

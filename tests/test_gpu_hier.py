@@ -130,6 +130,53 @@ def test_hier_sq8_bit_exact(km, torch, refine):
     assert (ph[:2] > 0).all() and (ph >= 0).all()
 
 
+@pytest.mark.parametrize("n,k_meso,cap", [(5000, 10, 300), (3000, 3, 95)])
+def test_fine_sq8_sqrt_rule_bit_exact(km, torch, n, k_meso, cap):
+    """The paper's fine counts (round(sqrt(n_i)) per meso-cluster) with C's capacity
+    above or at their sum; a meso-cluster is left empty in the first case."""
+    say(f"fine sq8 sqrt rule n={n} k_meso={k_meso}")
+    X = blobs(n, 64, 30, seed=n + 91)
+    Po, Pg = formats(km, torch, "sq8", X)
+    am = meso_labels(n, k_meso, seed=n + 92, empty=3 if k_meso > 3 else None)
+    C_o, a_o, kf_o, J_o = orc.fit_fine(Po, am, k_meso, cap, 3, sqrt_rule=True)
+    assert kf_o.sum() <= cap
+    C, a, kf, obj = km.kmeans_fine(Pg, to_dev(am, torch), k_meso, cap, 3, objective=True, sqrt_rule=True)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(kf, kf_o)
+    np.testing.assert_array_equal(host(a), a_o)
+    np.testing.assert_array_equal(host(C), C_o)
+    assert host(obj)[0] == J_o[-1]
+
+
+def test_fine_sqrt_rule_rejects_a_short_c(km, torch):
+    n, k_meso = 2000, 4
+    X = blobs(n, 32, 10, seed=93)
+    Po, Pg = formats(km, torch, "sq8", X)
+    am = meso_labels(n, k_meso, seed=94)
+    need = int(orc.fine_counts_sqrt(np.bincount(am, minlength=k_meso)).sum())
+    with pytest.raises(RuntimeError, match="fine counts sum"):
+        km.kmeans_fine(Pg, to_dev(am, torch), k_meso, need - 1, 1, sqrt_rule=True)
+
+
+def test_hier_sq8_sqrt_rule_bit_exact(km, torch):
+    """The whole pipeline with the paper's fine counts and a refinement over the fine
+    centroids made."""
+    import synth
+    spec = synth.config(2)["spec"].with_n(20000)
+    X = synth.make_points(spec)
+    Po, Pg = formats(km, torch, "sq8", X)
+    k = 1000  # C's capacity: 32 meso-clusters of ~625 points take ~25 fine centroids each
+    init = synth.init_indices(len(X), orc.meso_count(k))
+    say("hier sq8 sqrt rule")
+    C_o, a_o, J_o, info = orc.fit_hier(Po, k, 3, 2, 1, init, sqrt_rule=True)
+    C, a, kf, obj, ph = km.kmeans_fit_hier(Pg, k, init, 3, 2, 1, sqrt_rule=True)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(kf, info["k_fine"])
+    np.testing.assert_array_equal(host(a), a_o)
+    np.testing.assert_array_equal(host(C), C_o)
+    assert host(obj)[0] == J_o
+
+
 @pytest.mark.parametrize("fmt,d", [("sign1", 128), ("rabitq", 256), ("lvq4", 96), ("sign1", 1536)])
 def test_fine_integer_formats_lockstep(km, torch, fmt, d):
     """Assignments bit-exact against the same fine centroids (STEP 1 gather exact as

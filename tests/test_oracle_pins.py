@@ -877,6 +877,45 @@ def test_hier_meso_count_and_fine_counts_hand_examples(orc):
         assert orc.fine_counts(case["n"], case["k"]).tolist() == case["k_fine"], case
 
 
+def test_fine_counts_sqrt_rule(orc):
+    """The paper's fine counts: hand values, then for every n up to 20000 the count is
+    the unique integer within 1/2 of sqrt(n) (floating point decides nothing here:
+    (c - 1/2)^2 < n < (c + 1/2)^2 in integers is 4c^2 - 4c + 1 < 4n < 4c^2 + 4c + 1)."""
+    g = load_golden("hier_fine_counts.json")["sqrt_rule"]
+    assert orc.fine_counts_sqrt(g["n"]).tolist() == g["k_fine"]
+    ks = orc.fine_counts_sqrt(range(20001))
+    assert ks[0] == 0
+    for v in range(1, 20001):
+        c = int(ks[v])
+        assert 1 <= c <= v and 4 * c * c - 4 * c + 1 < 4 * v < 4 * c * c + 4 * c + 1, (v, c)
+
+
+def test_fine_sqrt_rule_fit(orc):
+    """fit_fine with the paper's counts: k_i = fine_counts_sqrt(n_i), C holds their sum,
+    each meso-cluster's points keep to its own segment of centroids, and a larger k
+    than needed changes nothing; fit_hier refines over the fine centroids made."""
+    X = _blob_rows(500, 8, 83)
+    a_meso = np.random.default_rng(84).integers(0, 4, 500).astype(np.int32)
+    a_meso[a_meso == 2] = 3  # an empty meso-cluster
+    P = {"fmt": "f32", "X": X}
+    n_i = np.bincount(a_meso, minlength=4)
+    C, a, ks, J = orc.fit_fine(P, a_meso, 4, 60, 2, sqrt_rule=True)
+    assert ks.tolist() == orc.fine_counts_sqrt(n_i).tolist() and ks[2] == 0 and len(C) == ks.sum()
+    off = np.concatenate([[0], np.cumsum(ks)])
+    np.testing.assert_array_equal(np.searchsorted(off, a, side="right") - 1, a_meso)
+    C2, a2, ks2, J2 = orc.fit_fine(P, a_meso, 4, int(ks.sum()), 2, sqrt_rule=True)
+    np.testing.assert_array_equal(C, C2)
+    np.testing.assert_array_equal(a, a2)
+    with pytest.raises(ValueError):
+        orc.fit_fine(P, a_meso, 4, int(ks.sum()) - 1, 2, sqrt_rule=True)
+    init = np.random.default_rng(85).choice(500, 4, replace=False)
+    Ch, ah, Jh, info = orc.fit_hier(P, 64, 2, 2, 1, init, k_meso=4, sqrt_rule=True)
+    assert len(Ch) == info["k_fine"].sum() and info["k_fine"].tolist() == orc.fine_counts_sqrt(
+        np.bincount(info["a_meso"], minlength=info["k_meso"])).tolist()
+    a_exp, d = _nearest(X, Ch, list(range(len(Ch))))
+    np.testing.assert_array_equal(ah, a_exp)
+
+
 @settings(max_examples=200, deadline=None)
 @given(n=st.lists(st.integers(0, 40), min_size=1, max_size=12), seed=st.integers(0, 10 ** 6))
 def test_fine_counts_properties(orc, n, seed):
