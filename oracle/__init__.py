@@ -16,7 +16,8 @@ import os
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(HERE, "libkmq_oracle.so")
+# KMQ_ORACLE_LIB names another build of kmq_oracle.c (a sanitizer build in the tests)
+_LIB_PATH = os.environ.get("KMQ_ORACLE_LIB") or os.path.join(HERE, "libkmq_oracle.so")
 _lib = None
 
 EMPTY_SPLIT = 0
@@ -36,6 +37,14 @@ _i32 = ct.c_int32
 
 def _null(dtype):
     return np.ctypeslib.ndpointer(dtype, flags="C_CONTIGUOUS")
+
+
+def _centroid_rows(C, k: int, d: int):
+    """The update writes k rows of d values into C: refuse a C of another shape
+    before the C code can run past it."""
+    if C.shape != (k, d):
+        raise ValueError(f"centroids of shape {C.shape} for k = {k}, d = {d}")
+    return C
 
 
 def lib():
@@ -348,7 +357,7 @@ def assign_hybrid(front, bits, alpha, C, m, d0: int):
 def update_f32(X, a, k: int, C_old, policy: int = EMPTY_SPLIT):
     X = _c(X, np.float32)
     n, d = X.shape
-    C = np.array(C_old, dtype=np.float32, copy=True, order="C")
+    C = _centroid_rows(np.array(C_old, dtype=np.float32, copy=True, order="C"), k, d)
     counts = np.empty(k, np.int64)
     lib().orc_update_f32(X, n, d, d, _c(a, np.int32), k, C, counts, policy)
     return C, counts
@@ -362,7 +371,7 @@ def update_bf16(codes, a, k: int, C_old, policy: int = EMPTY_SPLIT):
 def update_lvq4(codes, par, a, k: int, C_old, policy: int = EMPTY_SPLIT):
     codes = _c(codes, np.uint8)
     n, d = codes.shape
-    C = np.array(C_old, dtype=np.float32, copy=True, order="C")
+    C = _centroid_rows(np.array(C_old, dtype=np.float32, copy=True, order="C"), k, d)
     counts = np.empty(k, np.int64)
     lib().orc_update_lvq4(codes, _c(par, np.float32), n, d, _c(a, np.int32), k, C, counts, policy)
     return C, counts
@@ -371,7 +380,7 @@ def update_lvq4(codes, par, a, k: int, C_old, policy: int = EMPTY_SPLIT):
 def update_sq8(codes, a, k: int, C_old, policy: int = EMPTY_SPLIT):
     codes = _c(codes, np.uint8)
     n, d = codes.shape
-    C = np.array(C_old, dtype=np.uint8, copy=True, order="C")
+    C = _centroid_rows(np.array(C_old, dtype=np.uint8, copy=True, order="C"), k, d)
     counts = np.empty(k, np.int64)
     lib().orc_update_sq8(codes, n, d, _c(a, np.int32), k, C, counts, policy)
     return C, counts
@@ -380,7 +389,7 @@ def update_sq8(codes, a, k: int, C_old, policy: int = EMPTY_SPLIT):
 def update_sign1(bits, alpha, d: int, m, a, k: int, C_old, policy: int = EMPTY_SPLIT, front=None, d0: int = 0):
     bits = _c(bits, np.uint32)
     n = bits.shape[0]
-    C = np.array(C_old, dtype=np.float32, copy=True, order="C")
+    C = _centroid_rows(np.array(C_old, dtype=np.float32, copy=True, order="C"), k, d)
     counts = np.empty(k, np.int64)
     fp = None
     if d0 > 0:
