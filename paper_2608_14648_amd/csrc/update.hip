@@ -55,7 +55,8 @@ struct UpdWs {
   int *perm;     // [n]
   void *partial; // [maxchunks * dp] float or int
   uint32_t *partialA; // [maxchunks] 1-bit formats: sum of the scaled alphas per chunk
-  float *partialM;    // [maxchunks] 1-bit formats: largest alpha per chunk
+  float *partialM;    // [maxchunks] 1-bit formats: largest alpha per chunk; LVQ4: largest scale
+  double *partialB;   // [maxchunks] LVQ4: sum of the biases per chunk
   void *Z;       // [k * dp] float or uint8
   uint8_t *fresh;  // [k]
   int64_t *cntw;   // [k]
@@ -89,6 +90,7 @@ UpdWs carve(const Points &P, int k, void *base, size_t *bytes_out) {
   w.partial = take(sizeof(float) * (size_t)w.maxchunks * (size_t)w.dp);
   w.partialA = (uint32_t *)take(sizeof(uint32_t) * (size_t)w.maxchunks);
   w.partialM = (float *)take(sizeof(float) * (size_t)w.maxchunks);
+  w.partialB = (double *)take(sizeof(double) * (size_t)w.maxchunks);
   w.Z = take(sizeof(float) * (size_t)k * (size_t)w.dp);
   w.fresh = (uint8_t *)take((size_t)k);
   w.cntw = (int64_t *)take(sizeof(int64_t) * (size_t)k);
@@ -369,69 +371,6 @@ __global__ __launch_bounds__(256) void segsum_bf16_kernel(const uint16_t *X, int
   }
 }
 
-// LVQ4 rows: one slice of 1024 dims (512 packed bytes) per workgroup; lane = 16
-// dims from 8 packed bytes, each decoded as fmaf(s, code, b) and summed in fp32
-__global__ __launch_bounds__(256) void segsum_lvq4_kernel(const uint8_t *codes, int64_t ld, const float *vparams,
-                                                          int d, const int *perm, const int *cnt, const int *cstart,
-                                                          const int *choff, int k, float *partial, int dp) {
-  __shared__ float red[4][64 * 17];
-  const int c = blockIdx.x;
-  if (c >= choff[k]) return;
-  const int j = find_cluster(choff, k, c);
-  const int ci = c - choff[j];
-  const int m0 = cstart[j] + ci * kChunk;
-  const int m1 = cstart[j] + min(cnt[j], (ci + 1) * kChunk);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int col = blockIdx.y * 1024 + 16 * lane;
-  const bool ok = col < d;  // d % 32 == 0: 16 dims are wholly in or out
-  const int bo = (ok ? col : 0) / 2;
-  float acc[16];
-#pragma unroll
-  for (int e = 0; e < 16; ++e) acc[e] = 0.f;
-  auto add = [&](float sx, float bx, uint2 w) {
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const uint32_t byte = ((e < 4 ? w.x : w.y) >> (8 * (e & 3))) & 255u;
-      acc[2 * e] += fmaf(sx, (float)(byte & 15u), bx);
-      acc[2 * e + 1] += fmaf(sx, (float)(byte >> 4), bx);
-    }
-  };
-  int m = m0 + wave;
-  for (; m + 28 < m1; m += 32) {
-    int pp[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) pp[e] = perm[m + 4 * e];
-    f32x4 vp[8];
-    uint2 ww[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      vp[e] = *reinterpret_cast<const f32x4 *>(vparams + 4 * (int64_t)pp[e]);
-      ww[e] = *reinterpret_cast<const uint2 *>(codes + (int64_t)pp[e] * ld + bo);
-    }
-#pragma unroll
-    for (int e = 0; e < 8; ++e) add(vp[e][0], vp[e][1], ww[e]);
-  }
-  for (; m < m1; m += 4) {
-    const int p = perm[m];
-    add(vparams[4 * (int64_t)p], vparams[4 * (int64_t)p + 1],
-        *reinterpret_cast<const uint2 *>(codes + (int64_t)p * ld + bo));
-  }
-#pragma unroll
-  for (int e = 0; e < 16; ++e) red[wave][lane * 17 + e] = acc[e];
-  __syncthreads();
-  if (wave == 0 && ok) {
-    float *out = partial + (int64_t)c * dp + col;
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      float t = red[0][lane * 17 + e];
-      t += red[1][lane * 17 + e];
-      t += red[2][lane * 17 + e];
-      t += red[3][lane * 17 + e];
-      out[e] = t;
-    }
-  }
-}
-
 // 1-bit rows: one slice of 1024 tail dims per workgroup; lane = 16 dims (half a
 // word).  Only W = sum of alpha over the members whose bit is set is accumulated
 // per dim (finalize forms the mean decoded residual (2W - A)/n with A = sum of
@@ -540,6 +479,124 @@ __global__ __launch_bounds__(256) void segsum_bits_kernel(const uint32_t *bits, 
   }
 }
 
+// LVQ4 rows: one slice of 1024 dims (512 packed bytes) per workgroup; lane = 16
+// dims from 8 packed bytes.  A member decodes to s x + b per dim (x its 4-bit
+// code); the bias part is summed once per member (B = sum of b, in fp64) and the
+// scaled codes in exact integers, as for the 1-bit rows: the chunk's scales become
+// 19-bit integers q = rint(s / u), u = (largest scale of the chunk) / (2^19 - 1), so
+// a dim costs a bit-field extract and a 24-bit multiply-add, and no sum can wrap
+// (at most 512 members: 512 * 15 * (2^19 - 1) < 2^32).  The fold forms
+// sum over chunks of u W + B in fp64.
+constexpr double kLvqSteps = 524287.0;  // 2^19 - 1
+
+__global__ __launch_bounds__(256) void segsum_lvq4_kernel(const uint8_t *codes, int64_t ld, const float *vparams,
+                                                          int d, const int *perm, const int *cnt, const int *cstart,
+                                                          const int *choff, int k, uint32_t *partial, float *partialM,
+                                                          double *partialB, int dp) {
+  __shared__ int sperm[kChunk];
+  __shared__ uint32_t sq[kChunk];
+  __shared__ uint32_t red[4][64 * 17];
+  __shared__ float smax[4];
+  __shared__ double sbias[4];
+  const int c = blockIdx.x;
+  if (c >= choff[k]) return;
+  const int j = find_cluster(choff, k, c);
+  const int ci = c - choff[j];
+  const int m0 = cstart[j] + ci * kChunk;
+  const int len = min(cnt[j], (ci + 1) * kChunk) - ci * kChunk;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  // the chunk's member ids and scales (two per thread), its largest scale and its
+  // bias sum (fixed-order reductions)
+  float sv[2] = {0.f, 0.f};
+  float mx = 0.f;
+  double bs = 0.0;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int i = t + 256 * h;
+    if (i < len) {
+      const int p = perm[m0 + i];
+      sperm[i] = p;
+      const float2 sb = *reinterpret_cast<const float2 *>(vparams + 4 * (int64_t)p);
+      sv[h] = sb.x;
+      mx = fmaxf(mx, sb.x);
+      bs += (double)sb.y;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    mx = fmaxf(mx, __shfl_xor(mx, o));
+    bs += __shfl_xor(bs, o);
+  }
+  if (lane == 0) {
+    smax[wave] = mx;
+    sbias[wave] = bs;
+  }
+  __syncthreads();
+  const float smx = fmaxf(fmaxf(smax[0], smax[1]), fmaxf(smax[2], smax[3]));
+  const double inv_u = smx > 0.f ? kLvqSteps / (double)smx : 0.0;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int i = t + 256 * h;
+    if (i < len) sq[i] = (uint32_t)rint((double)sv[h] * inv_u);
+  }
+  if (t == 0 && blockIdx.y == 0) {
+    partialM[c] = smx;
+    partialB[c] = ((sbias[0] + sbias[1]) + sbias[2]) + sbias[3];
+  }
+  __syncthreads();
+  const int col = blockIdx.y * 1024 + 16 * lane;
+  const bool ok = col < d;  // d % 32 == 0: 16 dims are wholly in or out
+  const int bo = (ok ? col : 0) / 2;
+  uint32_t acc[16];
+#pragma unroll
+  for (int e = 0; e < 16; ++e) acc[e] = 0u;
+  // nibble 2e of the lane's 8 bytes is dim col + 2e (low nibble first)
+  auto add = [&](uint32_t q, uint2 w) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e)
+      acc[e] = mad_u24(__builtin_amdgcn_ubfe(e < 8 ? w.x : w.y, 4 * (e & 7), 4), q, acc[e]);
+  };
+  // lane adds the members m, m + 4, m + 8, ... of the chunk, 8 at a time, with the
+  // next 8 rows' loads in flight while the current ones are added (the last
+  // round's look-ahead rereads the chunk's last row and is not used)
+  uint32_t qq[8];
+  uint2 ww[8];
+  auto fetch = [&](int mb) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int i = min(mb + 4 * e, len - 1);
+      qq[e] = sq[i];
+      ww[e] = *reinterpret_cast<const uint2 *>(codes + (int64_t)sperm[i] * ld + bo);
+    }
+  };
+  const int rounds = len - 28 > wave ? (len - 28 - wave + 31) / 32 : 0;  // m + 28 < len
+  if (rounds > 0) fetch(wave);
+  for (int r = 0; r < rounds; ++r) {
+    uint32_t q0[8];
+    uint2 w0[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      q0[e] = qq[e];
+      w0[e] = ww[e];
+    }
+    fetch(wave + 32 * (r + 1));
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) add(q0[e], w0[e]);
+  }
+  for (int m = wave + 32 * rounds; m < len; m += 4)
+    add(sq[m], *reinterpret_cast<const uint2 *>(codes + (int64_t)sperm[m] * ld + bo));
+#pragma unroll
+  for (int e = 0; e < 16; ++e) red[wave][lane * 17 + e] = acc[e];
+  __syncthreads();
+  if (wave == 0 && ok) {
+    uint32_t *out = partial + (int64_t)c * dp + col;
+#pragma unroll
+    for (int e = 0; e < 16; ++e)
+      out[e] = red[0][lane * 17 + e] + red[1][lane * 17 + e] + red[2][lane * 17 + e] + red[3][lane * 17 + e];
+  }
+}
+
 // SQ8 codes: one slice of 1024 bytes (16 per lane) per workgroup, exact int32 sums
 __global__ __launch_bounds__(256) void segsum_sq8_kernel(const uint8_t *codes, int64_t ld, int d, const int *perm,
                                                          const int *cnt, const int *cstart, const int *choff, int k,
@@ -616,11 +673,14 @@ struct Compose {
 // Columns from d_bits on hold, per chunk, W as an exact integer sum of the scaled
 // alphas q over the set bits; partialA the chunk's sum of q and partialM its
 // largest alpha, which fixes the scale s = partialM / (2^23 - 1).  The mean decoded
-// residual is (2W - A)/n with W and A scaled back by each chunk's s.
+// residual is (2W - A)/n with W and A scaled back by each chunk's s.  LVQ4
+// (partialB set): W is the chunk's exact sum of its scaled scales times the codes,
+// partialM its largest scale and partialB its bias sum; the mean is the sum over
+// chunks of (partialM / (2^19 - 1)) W + partialB, over n.
 __global__ __launch_bounds__(256) void finalize_f32_kernel(const float *partial, int dp, const int *cnt,
                                                            const int *choff, float *Z, uint8_t *fresh,
                                                            const uint32_t *partialA, const float *partialM,
-                                                           int d_bits, Compose cm) {
+                                                           const double *partialB, int d_bits, Compose cm) {
   const int j = blockIdx.x;
   const int col = blockIdx.y * 256 + threadIdx.x;
   const int nj = cnt[j];
@@ -639,6 +699,10 @@ __global__ __launch_bounds__(256) void finalize_f32_kernel(const float *partial,
       a += sc * (double)partialA[c];
     }
     s = 2.0 * s - a;
+  } else if (partialB) {
+    const uint32_t *pu = reinterpret_cast<const uint32_t *>(partial);
+    for (int c = choff[j]; c < choff[j + 1]; ++c)
+      s += (double)partialM[c] / kLvqSteps * (double)pu[(int64_t)c * dp + col] + partialB[c];
   } else {
     for (int c = choff[j]; c < choff[j + 1]; ++c) s += (double)partial[(int64_t)c * dp + col];
   }
@@ -841,7 +905,7 @@ km_status launch_update(const Points &P, const int32_t *assign, int k, void *C, 
     if (P.fmt == KM_LVQ4)
       hipLaunchKernelGGL(segsum_lvq4_kernel, dim3(w.maxchunks, (unsigned)cdiv(d, 1024)), dim3(256), 0, s,
                          static_cast<const uint8_t *>(P.data), P.ld, P.vparams, d, w.perm, w.cnt, w.cstart, w.choff,
-                         k, static_cast<float *>(w.partial), w.dp);
+                         k, static_cast<uint32_t *>(w.partial), w.partialM, w.partialB, w.dp);
     if (P.fmt == KM_BF16)
       hipLaunchKernelGGL(segsum_bf16_kernel, dim3(w.maxchunks, (unsigned)cdiv(d, 512)), dim3(256), 0, s,
                          static_cast<const uint16_t *>(P.data), P.ld, d, w.perm, w.cnt, w.cstart, w.choff, k,
@@ -859,7 +923,8 @@ km_status launch_update(const Points &P, const int32_t *assign, int k, void *C, 
     }
     hipLaunchKernelGGL(finalize_f32_kernel, dim3(k, (unsigned)cdiv(w.dp, 256)), dim3(256), 0, s,
                        static_cast<const float *>(w.partial), w.dp, w.cnt, w.choff, static_cast<float *>(w.Z),
-                       w.fresh, is_bits_fmt(P.fmt) ? w.partialA : nullptr, w.partialM, d_bits, cm);
+                       w.fresh, is_bits_fmt(P.fmt) ? w.partialA : nullptr, w.partialM,
+                       P.fmt == KM_LVQ4 ? w.partialB : nullptr, d_bits, cm);
   }
   KMQ_LAUNCH_CHECK("update: segmented sums");
 
