@@ -1261,7 +1261,8 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void assign_bits_kernel(AssignArgs
 
 // ---- SQ8 / bf16 assignment with direct global-to-LDS stages -------------------
 // The same 256 x 256 workgroup tile and wave split as above (8 waves: 2 centroid
-// halves x 4 point quarters, 128 centroids x 64 points each), with the operand
+// halves x 4 point quarters, 128 centroids x 64 points each; bf16 uses 16 waves, NWC
+// below), with the operand
 // traffic moved off the vector units: every stage (256 centroid rows and 256 point
 // rows of 128 bytes) is copied straight from global memory into LDS, 16 bytes per
 // lane, with the XOR slot layout of the 1-bit kernel (chunk c of row R in slot
@@ -1280,11 +1281,21 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void assign_bits_kernel(AssignArgs
 // XCD's L2, and they merge through 64-bit (score, index) keys.
 constexpr int kQT = 256;                            // points per workgroup (and centroids per tile, CB = 4)
 constexpr int kQThreads = 512;                      // 8 waves
+constexpr int kQWideThreads = 1024;                 // 16 waves (bf16, 256-centroid tiles)
 constexpr int kQMaxDimSQ8 = 8192;                   // |2<x~,c~> - ||c~||^2| < 2^31
 constexpr int kQPackMaxDim = 1024;                  // SQ8 packed selection keys (below)
 
 // CB: 32 x 32 centroid blocks per wave, 4 (256-centroid tiles) or 2 (128-centroid
 // tiles, for k <= 128, where a 256-centroid tile would be mostly padding)
+//
+// NWC: waves along the centroids.  2 is the shape above; 4 (bf16 only, with CB = 2)
+// makes 16 waves of 64 centroids x 64 points on the same 256 x 256 tile.  A wave's
+// direct copies complete one after another, so a stage's 64 copy instructions
+// spread over 16 waves (4 each) take half the time they take over 8; the LDS
+// operand reads grow by a third (each wave reads 4 operand blocks per step for 4
+// MFMAs instead of 6 for 8).  Its 128-register budget leaves no room to keep the
+// copy offsets, which are recomputed at each copy.  SQ8 spills at that budget and
+// keeps the 8-wave shape.
 //
 // PK (SQ8 with d <= kQPackMaxDim): the key 2<x~,c~> - ||c~||^2 of every code pair
 // lies in [-48896 d, 16384 d] (codes in [-128, 127]: the key is ||x~||^2 - ||x~ - c~||^2),
@@ -1295,14 +1306,17 @@ constexpr int kQPackMaxDim = 1024;                  // SQ8 packed selection keys
 // (acc << 7) + E (modulo 2^32, exact since the result is in range), orders pairs by
 // key and then by the smaller id: one shift-add and one max per pair select the
 // tile's winner instead of a compare and two selects.
-template <int FMT, bool SEG = false, int CB = 4, bool PK = false>
-__global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) {
+template <int FMT, bool SEG = false, int CB = 4, bool PK = false, int NWC = 2>
+__global__ __launch_bounds__(256 * NWC, 1) void assign_q8_kernel(AssignArgs A0) {
   constexpr bool BF = FMT == KM_BF16;
-  static_assert(CB == 2 || CB == 4, "128- or 256-centroid tiles");
-  constexpr int TC = 64 * CB;                       // centroids per tile
+  static_assert(CB == 2 || CB == 4, "64 or 128 centroids per wave");
+  static_assert(NWC == 2 || NWC == 4, "2 or 4 waves along the centroids");
+  constexpr int NW = 4 * NWC;                       // waves: NWC centroid groups x 4 point quarters
+  constexpr int TC = 32 * CB * NWC;                 // centroids per tile
   constexpr int TP = kQT;                           // points per workgroup
-  constexpr int NCC = TC / 64;                      // centroid copies per thread and stage
-  constexpr int NCOPY = (TC + TP) / 64;             // all copies per thread and stage
+  constexpr int NCC = TC / (8 * NW);                // centroid copies per thread and stage
+  constexpr int NCOPY = (TC + TP) / (8 * NW);       // all copies per thread and stage
+  static_assert(NWC == 2 || (BF && CB == 2), "16 waves: bf16 with 64 centroids per wave (SQ8 spills there)");
   constexpr int STAGE = (TC + TP) * kRowBytes;      // centroid rows, then point rows
   // a segmented launch narrows the arguments to this workgroup's segment
   AssignArgs A = A0;
@@ -1330,7 +1344,7 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
   const int t = threadIdx.x;
   const int lane = t & 63, wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int r = lane & 31, h = lane >> 5;
-  const int wc = wave & 1, wp = wave >> 1;
+  const int wc = wave % NWC, wp = wave / NWC;
   const int NG = A.ngroups;
   int64_t pt = blockIdx.x;
   int g = 0;
@@ -1349,20 +1363,35 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
   const uint8_t *pbase = A.pi8 + p0 * A.pild;
   const int pk_off = PK ? 16256 * A.di : 0;  // recentres the packed keys
 
-  // copy i (0 .. NCOPY - 1) of a wave fills slots (8 i + wave) 64 .. + 63 of the
+  // copy i (0 .. NCOPY - 1) of a wave fills slots (NW i + wave) 64 .. + 63 of the
   // stage: rows 0 .. TC - 1 are centroids, the next TP rows points.  A lane's source is the stage's first
   // byte plus a 32-bit offset: point rows are clamped into the data once, centroid
   // rows only in a last, partial centroid tile.  In a partial last stage the lanes
   // whose chunk lies past the dimensions store zeros instead of copying.
-  uint32_t soff[NCOPY];
-#pragma unroll
-  for (int i = 0; i < NCOPY; ++i) {
-    const int slot = (i * 8 + wave) * 64 + lane;
+  auto source_offset = [&](int i) {
+    const int slot = (i * NW + wave) * 64 + lane;
     const int row = slot >> 3;
     const int chunk = (slot & 7) ^ ((row >> 1) & 7);
-    soff[i] = i < NCC ? (uint32_t)(row * (int)A.cild + 16 * chunk)
-                      : (uint32_t)(min(row - TC, prmax) * (int)A.pild + 16 * chunk);
+    return i < NCC ? (uint32_t)(row * (int)A.cild + 16 * chunk)
+                   : (uint32_t)(min(row - TC, prmax) * (int)A.pild + 16 * chunk);
+  };
+  // 16 waves have no registers to spare: their offsets are recomputed at each copy
+  // (a few vector instructions) and laundered so that the compiler keeps them there
+  constexpr bool kKeepOffsets = NWC == 2;
+  uint32_t soff[kKeepOffsets ? NCOPY : 1];
+  if constexpr (kKeepOffsets) {
+#pragma unroll
+    for (int i = 0; i < NCOPY; ++i) soff[i] = source_offset(i);
   }
+  auto offset_of = [&](int i) {
+    if constexpr (kKeepOffsets) {
+      return soff[i];
+    } else {
+      uint32_t o = source_offset(i);
+      asm volatile("" : "+v"(o));
+      return o;
+    }
+  };
   float cpv = 0.f;
   // the next stage's tile constant for row t (loaded with its tile's first stage)
   auto load_constant = [&](int ct) {
@@ -1372,7 +1401,7 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
       const int j = c0 + min(t, crmax);
       cpv = BF ? A.cp.cn[j] : __int_as_float(A.cp.qsum[j]);  // SQ8: -||c~||^2
       if constexpr (PK) {
-        const int rr = t & (32 * CB - 1);  // row within the wave's centroid half
+        const int rr = t & (32 * CB - 1);  // row within its wave's centroid group
         const int id = (rr >> 5) * 16 + ((rr >> 3) & 3) * 4 + (rr & 3);
         cpv = __int_as_float((int)(((uint32_t)(A.cp.qsum[j] + pk_off) << 6) + (uint32_t)(63 - id)));
       }
@@ -1385,13 +1414,13 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
     const int8_t *cbase = A.ci8 + (int64_t)c0 * A.cild + kRowBytes * s;
     const uint8_t *psrc = pbase + kRowBytes * s;
     const bool full_stage = kRowBytes * (s + 1) <= A.di;
-    const int slot = (i * 8 + wave) * 64 + lane;
+    const int slot = (i * NW + wave) * 64 + lane;
     const int row = slot >> 3;
     const int chunk = (slot & 7) ^ ((row >> 1) & 7);
-    uint32_t off = soff[i];
+    uint32_t off = offset_of(i);
     if (i < NCC && crmax < TC - 1) off = (uint32_t)(min(row, crmax) * (int)A.cild + 16 * chunk);
     const void *base = i < NCC ? (const void *)cbase : (const void *)psrc;
-    lds_u8 *wdst = (lds_u8 *)dst + (i * 8 + wave) * 1024;
+    lds_u8 *wdst = (lds_u8 *)dst + (i * NW + wave) * 1024;
     const uint32_t lds = (uint32_t)(size_t)wdst;
     if (full_stage) {
       lds_copy16(base, off, lds);
@@ -1414,8 +1443,8 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
     if (plain) {
 #pragma unroll
       for (int i = i0; i < i1; ++i)
-        lds_copy16(i < NCC ? (const void *)cb : (const void *)pb, soff[i],
-                   (uint32_t)(size_t)((lds_u8 *)dst + (i * 8 + wave) * 1024));
+        lds_copy16(i < NCC ? (const void *)cb : (const void *)pb, offset_of(i),
+                   (uint32_t)(size_t)((lds_u8 *)dst + (i * NW + wave) * 1024));
     } else {
 #pragma unroll
       for (int i = i0; i < i1; ++i) load_one(ct, s, dst, i);
@@ -1647,13 +1676,14 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
       bidx[pb] = oi;
     }
   }
+  // centroid groups 1 .. NWC - 1 hand their per-point winners to group 0 through LDS
   key_t *ms = reinterpret_cast<key_t *>(qst0);
-  int *mi = reinterpret_cast<int *>(qst0 + TP * sizeof(key_t));
-  if (wc == 1 && h == 0) {
+  int *mi = reinterpret_cast<int *>(qst0 + (NWC - 1) * TP * sizeof(key_t));
+  if (wc > 0 && h == 0) {
 #pragma unroll
     for (int pb = 0; pb < k8PB; ++pb) {
-      ms[wp * 32 * k8PB + pb * 32 + r] = best[pb];
-      mi[wp * 32 * k8PB + pb * 32 + r] = bidx[pb];
+      ms[(wc - 1) * TP + wp * 32 * k8PB + pb * 32 + r] = best[pb];
+      mi[(wc - 1) * TP + wp * 32 * k8PB + pb * 32 + r] = bidx[pb];
     }
   }
   __syncthreads();
@@ -1661,11 +1691,14 @@ __global__ __launch_bounds__(kQThreads, 1) void assign_q8_kernel(AssignArgs A0) 
 #pragma unroll
     for (int pb = 0; pb < k8PB; ++pb) {
       const int pc = wp * 32 * k8PB + pb * 32 + r;
-      const key_t os = ms[pc];
-      const int oi = mi[pc];
-      if (better(os, oi, best[pb], bidx[pb])) {
-        best[pb] = os;
-        bidx[pb] = oi;
+#pragma unroll
+      for (int o = 0; o < NWC - 1; ++o) {
+        const key_t os = ms[o * TP + pc];
+        const int oi = mi[o * TP + pc];
+        if (better(os, oi, best[pb], bidx[pb])) {
+          best[pb] = os;
+          bidx[pb] = oi;
+        }
       }
       const int64_t p = p0 + pc;
       if (p < A.n) {
@@ -2770,9 +2803,12 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
           hipLaunchKernelGGL((assign_q8_kernel<FMT, false, 2, FMT == KM_SQ8>), grid, dim3(kQThreads), 0, s, A);
         else
           hipLaunchKernelGGL((assign_q8_kernel<FMT, false, 2>), grid, dim3(kQThreads), 0, s, A);
+      } else if constexpr (FMT == KM_BF16) {
+        // 16 waves of 64 x 64: half the direct copies per wave of the 8-wave shape
+        hipLaunchKernelGGL((assign_q8_kernel<FMT, false, 2, false, 4>), grid, dim3(kQWideThreads), 0, s, A);
       } else {
         if (pk)
-          hipLaunchKernelGGL((assign_q8_kernel<FMT, false, 4, FMT == KM_SQ8>), grid, dim3(kQThreads), 0, s, A);
+          hipLaunchKernelGGL((assign_q8_kernel<FMT, false, 4, true>), grid, dim3(kQThreads), 0, s, A);
         else
           hipLaunchKernelGGL((assign_q8_kernel<FMT, false, 4>), grid, dim3(kQThreads), 0, s, A);
       }
@@ -2987,7 +3023,8 @@ km_status launch_assign_segments(const Points &P, const void *C, const CentroidP
     if (tile_c == 128)
       hipLaunchKernelGGL((assign_q8_kernel<KM_BF16, true, 2>), dim3((unsigned)ntiles), dim3(kQThreads), 0, s, A);
     else
-      hipLaunchKernelGGL((assign_q8_kernel<KM_BF16, true, 4>), dim3((unsigned)ntiles), dim3(kQThreads), 0, s, A);
+      hipLaunchKernelGGL((assign_q8_kernel<KM_BF16, true, 2, false, 4>), dim3((unsigned)ntiles), dim3(kQWideThreads), 0,
+                         s, A);
   }
   KMQ_LAUNCH_CHECK("assign kernel (segments)");
   return KM_OK;
