@@ -267,13 +267,15 @@ def test_fine_fp_formats_lockstep(km, torch, fmt, d):
     assert compared >= 2
 
 
-def test_fine_f32_large_segments(km, torch):
+@pytest.mark.parametrize("fmt", ["f32", "bf16"])
+def test_fine_large_segments(km, torch, fmt):
     """Meso-clusters of ~200 fine centroids (128 < k_i <= 256): the segmented launch
-    takes 256-centroid tiles.  From the oracle's STEP-1 centroids, the fine
-    assignment within the fp tolerance and its objective within OBJ_REL."""
+    takes 256-centroid tiles (bf16: the 16-wave kernel).  From the oracle's STEP-1
+    centroids, the fine assignment within the fp tolerance and its objective within
+    OBJ_REL."""
     n, d, k_meso, k = 6000, 64, 4, 800
     X = blobs(n, d, 24, seed=31)
-    Po, Pg = formats(km, torch, "f32", X)
+    Po, Pg = formats(km, torch, fmt, X)
     am = meso_labels(n, k_meso, seed=32)
     amd = to_dev(am, torch)
     C0_o, _, kf_o, _ = orc.fit_fine(Po, am, k_meso, k, 0)
@@ -282,7 +284,7 @@ def test_fine_f32_large_segments(km, torch):
     _, a, kf, obj = km.kmeans_fine(Pg, amd, k_meso, k, 0, C=to_dev(C0_o, torch), objective=True)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(kf, kf_o)
-    assert_fp_assign(host(a), a_o, fp_d_of("f32", Po, C0_o), "f32 large segments")
+    assert_fp_assign(host(a), a_o, fp_d_of(fmt, Po, C0_o), f"{fmt} large segments")
     assert abs(host(obj)[0] - J_o[-1]) <= OBJ_REL * abs(J_o[-1])
 
 
