@@ -665,7 +665,8 @@ __device__ __forceinline__ void load_stage8(const AssignArgs &A, int s, int64_t 
   }
   if (s == 0) {  // per-centroid constants: threads t < kT8 (the others load a valid duplicate)
     const int64_t j = min<int64_t>(c0 + (t & (kT8 - 1)), A.k - 1);
-    R.cpar[1] = FMT == KM_BF16 ? A.cp.cn[j] : __int_as_float(A.cp.qsum[j]);
+    // LVQ4: the code sum as the float value the epilogue multiplies (exact: |sum| <= 15 d)
+    R.cpar[1] = FMT == KM_BF16 ? A.cp.cn[j] : FMT == KM_LVQ4 ? (float)A.cp.qsum[j] : __int_as_float(A.cp.qsum[j]);
     if (FMT == KM_SIGN1 || FMT == KM_RABITQ || FMT == KM_LVQ4) {
       R.cpar[2] = A.cp.u[j];
       R.cpar[3] = A.cp.sig2[j];
@@ -883,8 +884,7 @@ __global__ __launch_bounds__(k8Threads, 1) void assign_i8_kernel(AssignArgs A) {
               sc = fmaf(-2.0f, acc[cb][pb][i], q4[e]);  // ||c||^2 - 2<x,c>
             } else if constexpr (FMT == KM_LVQ4) {  // Eq. 2 without N_x, fp32 in the oracle's order
               const float sy = s4[e];
-              const float tt = fmaf(vp[pb][1] * sy, (float)__float_as_int(q4[e]),
-                                    fmaf(b4[e], vp[pb][2], (vp[pb][0] * sy) * (float)acc[cb][pb][i]));
+              const float tt = fmaf(vp[pb][1] * sy, q4[e], fmaf(b4[e], vp[pb][2], (vp[pb][0] * sy) * (float)acc[cb][pb][i]));
               sc = fmaf(-2.0f, tt, u4[e]);
             } else if constexpr (FMT == KM_RABITQ) {  // Eq. 4-5, fp32 in the oracle's order
               const int sd = 2 * acc[cb][pb][i] - __float_as_int(q4[e]);
@@ -895,7 +895,9 @@ __global__ __launch_bounds__(k8Threads, 1) void assign_i8_kernel(AssignArgs A) {
               const float v = al[pb] * s4[e];
               sc = fmaf(-v, (float)sd, u4[e]);
             }
-            const bool take = live && sc < best[pb];
+            // LVQ4: rows past the last centroid repeat it (clamped rows and constants), so
+            // they tie with it exactly and lose on the index in the merges; no bound test
+            const bool take = (FMT == KM_LVQ4 || live) && sc < best[pb];
             best[pb] = take ? sc : best[pb];
             bidx[pb] = take ? j : bidx[pb];
           }
