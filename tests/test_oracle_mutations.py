@@ -67,6 +67,10 @@ PY_MUTATIONS = {
     "hybrid_init_tail_without_m": ('C = sign1_decode(P["bits"][idx], P["alpha"][idx], P["d"], P["m"], d0)',
                                    'C = sign1_decode(P["bits"][idx], P["alpha"][idx], P["d"], np.zeros(P["d"], np.float32), d0)'),
     "hybrid_update_without_front": ('policy, front=P["front"], d0=P["d0"])', 'policy)'),
+    "sqrt_rule_rounds_down": ("out.append(r + 1 if v - r * r > r else r)", "out.append(r)"),
+    "sqrt_rule_rounds_half_down": ("out.append(r + 1 if v - r * r > r else r)",
+                                   "out.append(r + 1 if v - r * r > r + 1 else r)"),
+    "sqrt_rule_empty_gets_one": ("        if v <= 0:\n            out.append(0)", "        if v <= 0:\n            out.append(1)"),
 }
 
 PINS = [name for name in dir(pins) if name.startswith("test_")]
