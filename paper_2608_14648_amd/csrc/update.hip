@@ -34,7 +34,7 @@
 namespace kmq {
 namespace {
 
-constexpr int kHistBlocks = 1024;  // target number of histogram / scatter blocks
+constexpr int kHistBlocks = 512;   // target number of histogram / scatter blocks
 constexpr int kChunk = 512;        // members per segmented-sum chunk
 constexpr int kLdsCursorMax = 16384;
 constexpr int kScanSeg = 4096;     // elements per scan block (256 threads x 16)
