@@ -3,7 +3,7 @@ times, checked on sampled outputs the oracle computes one by one (or through
 properties that hold at any size).  Inputs come from the seeded generator or
 from the oracle, never from the HIP path.
 
-Workloads: 1M x 768 (fp32 and SQ8, k = 1000), 1M x 1024 1-bit (k = 1024),
+Workloads: 1M x 768 (fp32, SQ8, bfloat16 and LVQ4, k = 1000), 1M x 1024 1-bit (k = 1024),
 10M x 1024 -> PCA 256 (k = 4096) and 10M x 1024 fp32-front-384 + 1-bit (k = 4096).
 """
 import numpy as np
@@ -129,6 +129,94 @@ def test_c2_sq8_quantize_assign_sampled(km, torch, c2):
         members = np.nonzero(a == j)[0]
         mj, _ = orc.update_sq8(codes_o[members], np.zeros(len(members), np.int32), 1, C[j:j + 1], orc.EMPTY_KEEP)
         np.testing.assert_array_equal(Cn[j], mj[0])
+
+
+def _bf16_dev(codes, torch):
+    return to_dev(codes.view(np.int16), torch).view(torch.bfloat16)
+
+
+@pytest.mark.timeout(300)
+def test_c2_bf16_sampled(km, torch, c2):
+    """The bfloat16 workload (1M x 768, k = 1000, the 16-wave assignment kernel):
+    encoding bit-exact on sampled rows; the assignment of sampled rows within the
+    fp tolerance against the oracle and the in-space objective within OBJ_REL; the
+    counts exact and sampled clusters' means within the centroid tolerance."""
+    cfg, X, Xd = c2
+    import synth
+    k = cfg["k"]
+    say("c2 bf16 encode")
+    got = km.quantize_bf16(Xd)
+    torch.cuda.synchronize()
+    codes_o = orc.bf16_round(X)
+    rows = sample_rows(len(X), 4)
+    np.testing.assert_array_equal(host(got.view(torch.int16))[rows].view(np.uint16), codes_o[rows])
+    del got
+    idx = synth.init_indices(len(X), k)
+    C = np.ascontiguousarray(X[idx])
+    P = km.points_bf16(_bf16_dev(codes_o, torch))
+    say("c2 bf16 assign")
+    a, _, obj = km.kmeans_assign(P, to_dev(C, torch), score=False, objective=True)
+    torch.cuda.synchronize()
+    a = host(a)
+    Cb = orc.bf16_decode(orc.bf16_round(C))
+    a_o, _ = orc.assign_bf16(codes_o[rows], C)
+    assert_fp_assign(a[rows], a_o, f32_dist(orc.bf16_decode(codes_o[rows]), Cb), "c2 bf16 sampled")
+    J_o = orc.cost_f32(orc.bf16_decode(codes_o), Cb, a)
+    assert abs(host(obj)[0] - J_o) <= OBJ_REL * J_o
+    say("c2 bf16 update")
+    Cd = to_dev(C, torch)
+    _, cnt = km.kmeans_update(P, to_dev(a, torch), Cd)
+    torch.cuda.synchronize()
+    cnt = host(cnt)
+    np.testing.assert_array_equal(cnt, np.bincount(a, minlength=k))
+    Cn = host(Cd)
+    for j in np.random.default_rng(5).choice(np.nonzero(cnt)[0], 25, replace=False):
+        members = np.nonzero(a == j)[0]
+        mj, _ = orc.update_bf16(codes_o[members], np.zeros(len(members), np.int32), 1, C[j:j + 1], orc.EMPTY_KEEP)
+        assert_centroids(Cn[j:j + 1], mj, f"bf16 cluster {j}")
+
+
+@pytest.mark.timeout(300)
+def test_c2_lvq4_sampled(km, torch, c2):
+    """The LVQ4 workload (1M x 768, k = 1000): codes and per-vector parameters
+    bit-exact on sampled rows; assignments and scores of sampled rows bit-exact
+    against the oracle; the counts exact and sampled clusters' decoded means within
+    the centroid tolerance."""
+    cfg, X, Xd = c2
+    import synth
+    k = cfg["k"]
+    say("c2 lvq4 encode")
+    packed, par = km.quantize_lvq4(Xd)
+    torch.cuda.synchronize()
+    rows = sample_rows(len(X), 6)
+    codes_o, par_o = orc.lvq4_encode(X[rows])
+    np.testing.assert_array_equal(host(packed)[rows], orc.lvq4_pack(codes_o))
+    np.testing.assert_array_equal(host(par)[rows], par_o)
+    idx = synth.init_indices(len(X), k)
+    C = np.ascontiguousarray(X[idx])
+    P = km.points_lvq4(packed, par, X.shape[1])
+    say("c2 lvq4 assign")
+    a, sc, _ = km.kmeans_assign(P, to_dev(C, torch), score=True)
+    torch.cuda.synchronize()
+    a, sc = host(a), host(sc)
+    a_o, sc_o, _ = orc.assign_lvq4(codes_o, par_o, C)
+    np.testing.assert_array_equal(a[rows], a_o)
+    np.testing.assert_array_equal(sc[rows], sc_o)
+    say("c2 lvq4 update")
+    Cd = to_dev(C, torch)
+    _, cnt = km.kmeans_update(P, to_dev(a, torch), Cd)
+    torch.cuda.synchronize()
+    cnt = host(cnt)
+    np.testing.assert_array_equal(cnt, np.bincount(a, minlength=k))
+    Cn = host(Cd)
+    pk, pp = host(packed), host(par)
+    for j in np.random.default_rng(7).choice(np.nonzero(cnt)[0], 25, replace=False):
+        members = np.nonzero(a == j)[0]
+        cj, pj = orc.lvq4_encode(X[members])
+        mj, _ = orc.update_lvq4(cj, pj, np.zeros(len(members), np.int32), 1, C[j:j + 1], orc.EMPTY_KEEP)
+        np.testing.assert_array_equal(pk[members], orc.lvq4_pack(cj))
+        np.testing.assert_array_equal(pp[members], pj)
+        assert_centroids(Cn[j:j + 1], mj, f"lvq4 cluster {j}")
 
 
 def test_c2_fit_descends(km, torch, c2):
