@@ -3,7 +3,7 @@ times, checked on sampled outputs the oracle computes one by one (or through
 properties that hold at any size).  Inputs come from the seeded generator or
 from the oracle, never from the HIP path.
 
-Workloads: 1M x 768 (fp32, SQ8, bfloat16 and LVQ4, k = 1000), 1M x 1024 1-bit (k = 1024),
+Workloads: 1M x 768 (fp32, SQ8, bfloat16 and LVQ4, k = 1000), 1M x 1024 1-bit and RabitQ (k = 1024),
 10M x 1024 -> PCA 256 (k = 4096) and 10M x 1024 fp32-front-384 + 1-bit (k = 4096).
 """
 import numpy as np
@@ -275,6 +275,59 @@ def test_c3_sign1_sampled(km, torch, c3):
         mj, _ = orc.update_sign1(bits_o[members], alpha_o[members], d, m_o, np.zeros(len(members), np.int32), 1,
                                  C[j:j + 1], orc.EMPTY_KEEP)
         assert_centroids(Cn[j:j + 1], mj, f"cluster {j}")
+
+
+@pytest.mark.timeout(300)
+def test_c3_rabitq_sampled(km, torch, c3):
+    """The RabitQ workload (1M x 1024, k = 1024): the GPU rotation and encoding of
+    sampled rows against the oracle's (signs may differ only within rounding of 0);
+    then, on oracle-encoded codes of every point (the codes of the centred rows; the
+    assignment kernel does not depend on how they were rotated), the assignments and
+    scores of sampled rows bit-exact, the counts exact and sampled clusters' means
+    within the centroid tolerance."""
+    cfg, X, Xd = c3
+    import synth
+    k, d = cfg["k"], cfg["spec"].d
+    say("c3 rabitq encode")
+    m_o = orc.col_mean(X)
+    Rot = synth.random_rotation(d, 21)
+    bits_g, _, alpha_g, Yg = km.rabitq_encode(Xd, to_dev(Rot, torch), center=to_dev(m_o, torch), want_rotated=True)
+    torch.cuda.synchronize()
+    rows = sample_rows(len(X), 8)
+    Y = orc.project(X[rows], m_o, Rot)
+    bits_o, alpha_o = orc.sign1_encode(Y, np.zeros(d, np.float32), 0)
+    rn = np.linalg.norm(X[rows].astype(np.float64) - m_o.astype(np.float64), axis=1, keepdims=True)
+    assert (np.abs(host(Yg)[rows].astype(np.float64) - Y) <= 2e-6 * rn + 1e-12).all()
+    diff = unpack_bits(host(bits_g)[rows].view(np.uint32), d) != unpack_bits(bits_o, d)
+    scale = np.abs(Y).max(1, keepdims=True) + 1e-30
+    assert (np.abs(Y)[diff] <= 1e-5 * np.broadcast_to(scale, Y.shape)[diff]).all()
+    np.testing.assert_allclose(host(alpha_g)[rows], alpha_o, rtol=2e-5, atol=1e-7)
+    del bits_g, alpha_g, Yg
+    # assignment and update on oracle codes of all points
+    bits_a, alpha_a = orc.sign1_encode(X, m_o)
+    Po = {"fmt": "rabitq", "bits": bits_a, "alpha": alpha_a, "d": d}
+    idx = synth.init_indices(len(X), k)
+    C = np.ascontiguousarray(X[idx] - m_o)
+    P = km.points_rabitq(to_dev(bits_a.view(np.int32), torch), to_dev(alpha_a, torch), d)
+    say("c3 rabitq assign")
+    a, sc, _ = km.kmeans_assign(P, to_dev(C, torch), score=True)
+    torch.cuda.synchronize()
+    a, sc = host(a), host(sc)
+    a_o, sc_o, _ = orc.assign_rabitq(bits_a[rows], alpha_a[rows], C)
+    np.testing.assert_array_equal(a[rows], a_o)
+    np.testing.assert_array_equal(sc[rows], sc_o)
+    say("c3 rabitq update")
+    Cd = to_dev(C, torch)
+    _, cnt = km.kmeans_update(P, to_dev(a, torch), Cd)
+    torch.cuda.synchronize()
+    cnt = host(cnt)
+    np.testing.assert_array_equal(cnt, np.bincount(a, minlength=k))
+    Cn = host(Cd)
+    for j in np.random.default_rng(9).choice(np.nonzero(cnt)[0], 20, replace=False):
+        members = np.nonzero(a == j)[0]
+        Pj = {"fmt": "rabitq", "bits": bits_a[members], "alpha": alpha_a[members], "d": d}
+        mj, _ = orc.update(Pj, np.zeros(len(members), np.int32), 1, C[j:j + 1], orc.EMPTY_KEEP)
+        assert_centroids(Cn[j:j + 1], mj, f"rabitq cluster {j}")
 
 
 # --------------------------------------------------------------------------- 10M x 1024
