@@ -3,7 +3,8 @@ times, checked on sampled outputs the oracle computes one by one (or through
 properties that hold at any size).  Inputs come from the seeded generator or
 from the oracle, never from the HIP path.
 
-Workloads: 1M x 768 (fp32, SQ8, bfloat16 and LVQ4, k = 1000), 1M x 1024 1-bit and RabitQ (k = 1024),
+Workloads: 1M x 768 (fp32, SQ8, bfloat16, LVQ4 and a pruned SQ8 pass, k = 1000), 1M x 1024 1-bit and
+RabitQ (k = 1024),
 10M x 1024 -> PCA 256 (k = 4096) and 10M x 1024 fp32-front-384 + 1-bit (k = 4096).
 """
 import numpy as np
@@ -217,6 +218,29 @@ def test_c2_lvq4_sampled(km, torch, c2):
         np.testing.assert_array_equal(pk[members], orc.lvq4_pack(cj))
         np.testing.assert_array_equal(pp[members], pj)
         assert_centroids(Cn[j:j + 1], mj, f"lvq4 cluster {j}")
+
+
+@pytest.mark.timeout(300)
+def test_c2_pruned_sq8_sampled(km, torch, c2):
+    """One pruned SQ8 pass of the pruning workload's size (1M x 768, k = 1000, front
+    96 dims = 12.5 %, eps0 = 2.1) from a seeded previous assignment: the assignment
+    and distance of sampled rows bit-exact against the oracle's pruned pass (a row's
+    result depends only on the row, its previous centroid and the centroids)."""
+    cfg, X, Xd = c2
+    import synth
+    k, d = cfg["k"], X.shape[1]
+    lo, hi = orc.sq8_fit(X)
+    codes_o = orc.sq8_encode(X, lo, hi)
+    C = np.ascontiguousarray(codes_o[synth.init_indices(len(X), k)])
+    prev = np.random.default_rng(11).integers(0, k, len(X)).astype(np.int32)
+    say("c2 pruned sq8 pass")
+    a, dist, _, _ = km.kmeans_assign_pruned(km.points_sq8(to_dev(codes_o, torch)), to_dev(C, torch),
+                                            to_dev(prev, torch), 2.1, d // 8)
+    torch.cuda.synchronize()
+    rows = sample_rows(len(X), 10)
+    a_o, dist_o, _ = orc.assign_pruned({"fmt": "sq8", "codes": codes_o[rows]}, C, prev[rows], 2.1, d // 8)
+    np.testing.assert_array_equal(host(a)[rows], a_o)
+    np.testing.assert_array_equal(host(dist)[rows], dist_o)
 
 
 def test_c2_fit_descends(km, torch, c2):
