@@ -5,7 +5,8 @@ from the oracle, never from the HIP path.
 
 Workloads: 1M x 768 (fp32, SQ8, bfloat16, LVQ4 and a pruned SQ8 pass, k = 1000), 1M x 1024 1-bit and
 RabitQ (k = 1024),
-10M x 1024 -> PCA 256 (k = 4096) and 10M x 1024 fp32-front-384 + 1-bit (k = 4096).
+10M x 1024 -> PCA 256 (k = 4096), 10M x 1024 fp32-front-384 + 1-bit (k = 4096) and the
+hierarchical FINE phase on 10M x 1024 SQ8 codes (k = 12649).
 """
 import numpy as np
 import pytest
@@ -363,6 +364,42 @@ def c45(torch):
     X = generate(cfg["spec"])
     Xd = to_dev(X, torch)
     return cfg, X, Xd
+
+
+@pytest.mark.timeout(600)
+def test_hier_sq8_fine_full_size(km, torch, c45):
+    """The hierarchical workload's FINE phase at its size (10M x 1024 SQ8 codes, 112
+    meso-clusters from seeded labels, k = 12649 fine centroids; the segmented launches
+    bench.py times): the fine counts exact, the STEP-1 fine centroids (members of each
+    meso-cluster at the strided positions) exact, and the fine assignment of sampled
+    rows bit-exact against the nearest centroid of their own meso-cluster's segment."""
+    cfg, X, Xd = c45
+    n = len(X)
+    k_meso, k = 112, 12649
+    say("hier fine: oracle SQ8 codes")
+    lo, hi = orc.sq8_fit(X)
+    codes_o = orc.sq8_encode(X, lo, hi)
+    am = np.random.default_rng(12).integers(0, k_meso, n).astype(np.int32)
+    say("hier fine: GPU fine phase")
+    C, a, kf, _ = km.kmeans_fine(km.points_sq8(to_dev(codes_o, torch)), to_dev(am, torch), k_meso, k, 0)
+    torch.cuda.synchronize()
+    n_i = np.bincount(am, minlength=k_meso)
+    kf_o = orc.fine_counts(n_i, k)
+    np.testing.assert_array_equal(kf, kf_o)
+    off = np.concatenate([[0], np.cumsum(kf_o)])
+    start = np.concatenate([[0], np.cumsum(n_i)])
+    order = np.argsort(am, kind="stable")
+    C_o = np.empty((k, X.shape[1]), np.uint8)
+    for i in range(k_meso):
+        members = order[start[i]:start[i + 1]]
+        C_o[off[i]:off[i + 1]] = codes_o[members[orc.fine_init_positions(int(n_i[i]), int(kf_o[i]))]]
+    np.testing.assert_array_equal(host(C), C_o)
+    a = host(a)
+    rows = sample_rows(n, 14)
+    for i in np.unique(am[rows]):
+        ri = rows[am[rows] == i]
+        a_o, _ = orc.assign_sq8(codes_o[ri], C_o[off[i]:off[i + 1]])
+        np.testing.assert_array_equal(a[ri], a_o + off[i])
 
 
 @pytest.mark.timeout(600)
