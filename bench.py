@@ -625,8 +625,8 @@ def wl_lvq4(cfg, torch, km, args):
                     {"workload": wname, "N": spec.n, "d": spec.d, "k": k, "iters": T, "format": "lvq4"},
                     distances_per_s=(T + 1) * spec.n * k * K / elapsed,
                     partition_cost=float(out["cost"].item()),
-                    roofline=roofline(wname, s, 2.0 * spec.n * k * spec.d, "int8", "assign_i8_kernel<lvq4>",
-                                      "assign_i8_kernel<lvq4>"),
+                    roofline=roofline(wname, s, 2.0 * spec.n * k * spec.d, "int8", "assign_q8_kernel<lvq4>",
+                                      "assign_q8_kernel<lvq4>"),
                     update_hbm=update_hbm(s, spec.n * (spec.d // 2 + 20), "d/2+20 per point"),
                     stages={"lvq4": stage_summary(s)})
 

@@ -600,7 +600,8 @@ __global__ __launch_bounds__(256) void keys_unpack_kernel(const unsigned long lo
 }
 
 // ---- int8 / bf16 assignment with 256 x 256 workgroup tiles -------------------
-// SQ8, bf16 and (wide) 1-bit points.  An int8 or bf16 MFMA is 16-32x denser than
+// Register-staged stages; the direct-copy kernels below replace it except for SQ8
+// beyond 8192 dimensions and 1-bit points beyond 1280.  An int8 or bf16 MFMA is 16-32x denser than
 // the fp32 one, so operand bandwidth decides the tiling: the workgroup owns 256
 // centroids x 256 points per stage (a quarter of the L2 bytes per MFMA of a 128
 // tile) and each of its 8 waves 128 centroids x 64 points (4 x 2 blocks of
@@ -618,11 +619,6 @@ struct Stage8 {
   uint4 p[4];
   float cpar[4];
 };
-
-// 4 packed 4-bit codes (a half-word) -> 4 bytes holding the codes (nibble k -> byte k)
-__device__ __forceinline__ uint32_t spread_nib(uint32_t h) {
-  return (h & 0x000Fu) | ((h & 0x00F0u) << 4) | ((h & 0x0F00u) << 8) | ((h & 0xF000u) << 12);
-}
 
 template <int FMT>
 __device__ __forceinline__ void load_stage8(const AssignArgs &A, int s, int64_t c0, int64_t p0, Stage8 &R) {
@@ -644,16 +640,6 @@ __device__ __forceinline__ void load_stage8(const AssignArgs &A, int s, int64_t 
     if (FMT == KM_SQ8 || FMT == KM_BF16)
       R.p[i] = *reinterpret_cast<const uint4 *>(pbase8 + (uint32_t)(min(row, prmax) * (int)A.pild + bc));
   }
-  if (FMT == KM_LVQ4) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {  // 256 rows x 4 chunks of 16 packed bytes (32 dims) per stage
-      const int w = t + k8Threads * i;
-      const int row = w >> 2, qc = w & 3;
-      const int dim = kRowBytes * s + 32 * qc;
-      const int bp = dim < A.di ? dim / 2 : 0;
-      R.p[i] = *reinterpret_cast<const uint4 *>(pbase8 + (uint32_t)(min(row, prmax) * (int)A.pild + bp));
-    }
-  }
   if (FMT == KM_SIGN1 || FMT == KM_RABITQ) {
 #pragma unroll
     for (int i = 0; i < 2; ++i) {  // 256 rows x 4 words
@@ -665,13 +651,12 @@ __device__ __forceinline__ void load_stage8(const AssignArgs &A, int s, int64_t 
   }
   if (s == 0) {  // per-centroid constants: threads t < kT8 (the others load a valid duplicate)
     const int64_t j = min<int64_t>(c0 + (t & (kT8 - 1)), A.k - 1);
-    // LVQ4: the code sum as the float value the epilogue multiplies (exact: |sum| <= 15 d)
-    R.cpar[1] = FMT == KM_BF16 ? A.cp.cn[j] : FMT == KM_LVQ4 ? (float)A.cp.qsum[j] : __int_as_float(A.cp.qsum[j]);
-    if (FMT == KM_SIGN1 || FMT == KM_RABITQ || FMT == KM_LVQ4) {
+    R.cpar[1] = FMT == KM_BF16 ? A.cp.cn[j] : __int_as_float(A.cp.qsum[j]);
+    if (FMT == KM_SIGN1 || FMT == KM_RABITQ) {
       R.cpar[2] = A.cp.u[j];
       R.cpar[3] = A.cp.sig2[j];
     }
-    if (FMT == KM_RABITQ || FMT == KM_LVQ4) R.cpar[0] = A.cp.cn[j];
+    if (FMT == KM_RABITQ) R.cpar[0] = A.cp.cn[j];
   }
 }
 
@@ -692,23 +677,6 @@ __device__ __forceinline__ void store_stage8(const AssignArgs &A, int s, const S
       *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 16 * col) = mask4(flip4(R.p[i]), ok);
     if (FMT == KM_BF16) *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 16 * col) = mask4(R.p[i], ok);
   }
-  if (FMT == KM_LVQ4) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int w = t + k8Threads * i;
-      const int row = w >> 2, qc = w & 3;
-      const bool ok = kRowBytes * s + 32 * qc < A.di;
-      const uint4 v = R.p[i];
-      *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 32 * qc) =
-          mask4(make_uint4(spread_nib(v.x & 0xFFFFu), spread_nib(v.x >> 16), spread_nib(v.y & 0xFFFFu),
-                           spread_nib(v.y >> 16)),
-                ok);
-      *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 32 * qc + 16) =
-          mask4(make_uint4(spread_nib(v.z & 0xFFFFu), spread_nib(v.z >> 16), spread_nib(v.w & 0xFFFFu),
-                           spread_nib(v.w >> 16)),
-                ok);
-    }
-  }
   if (FMT == KM_SIGN1 || FMT == KM_RABITQ) {
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
@@ -725,7 +693,7 @@ __device__ __forceinline__ void store_stage8(const AssignArgs &A, int s, const S
   }
   if (s == 0 && t < kT8) {
 #pragma unroll
-    for (int q = (FMT == KM_RABITQ || FMT == KM_LVQ4 ? 0 : 1); q < 4; ++q) cpar[q * kT8 + t] = R.cpar[q];
+    for (int q = (FMT == KM_RABITQ ? 0 : 1); q < 4; ++q) cpar[q * kT8 + t] = R.cpar[q];
   }
 }
 
@@ -795,13 +763,6 @@ __global__ __launch_bounds__(k8Threads, 1) void assign_i8_kernel(AssignArgs A) {
 
   float al[k8PB] = {};
   int pop[k8PB] = {};
-  f32x4 vp[k8PB] = {};  // LVQ4: (s, b, A, N) of the lane's points
-  if (FMT == KM_LVQ4) {
-#pragma unroll
-    for (int pb = 0; pb < k8PB; ++pb)
-      vp[pb] = *reinterpret_cast<const f32x4 *>(
-          A.vparams + 4 * min<int64_t>(p0 + wp * 32 * k8PB + pb * 32 + r, A.n - 1));
-  }
   if (FMT == KM_SIGN1 || FMT == KM_RABITQ) {
 #pragma unroll
     for (int pb = 0; pb < k8PB; ++pb) {
@@ -865,11 +826,7 @@ __global__ __launch_bounds__(k8Threads, 1) void assign_i8_kernel(AssignArgs A) {
           u4 = *reinterpret_cast<const f32x4 *>(&cp[2 * kT8 + cr]);
           s4 = *reinterpret_cast<const f32x4 *>(&cp[3 * kT8 + cr]);
         }
-        if constexpr (FMT == KM_RABITQ || FMT == KM_LVQ4) b4 = *reinterpret_cast<const f32x4 *>(&cp[cr]);
-        if constexpr (FMT == KM_LVQ4) {
-          u4 = *reinterpret_cast<const f32x4 *>(&cp[2 * kT8 + cr]);
-          s4 = *reinterpret_cast<const f32x4 *>(&cp[3 * kT8 + cr]);
-        }
+        if constexpr (FMT == KM_RABITQ) b4 = *reinterpret_cast<const f32x4 *>(&cp[cr]);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int i = 4 * i4 + e;
@@ -882,10 +839,6 @@ __global__ __launch_bounds__(k8Threads, 1) void assign_i8_kernel(AssignArgs A) {
               sc = -__float_as_int(q4[e]) - 2 * acc[cb][pb][i];  // the constant is -||c~||^2
             } else if constexpr (FMT == KM_BF16) {
               sc = fmaf(-2.0f, acc[cb][pb][i], q4[e]);  // ||c||^2 - 2<x,c>
-            } else if constexpr (FMT == KM_LVQ4) {  // Eq. 2 without N_x, fp32 in the oracle's order
-              const float sy = s4[e];
-              const float tt = fmaf(vp[pb][1] * sy, q4[e], fmaf(b4[e], vp[pb][2], (vp[pb][0] * sy) * (float)acc[cb][pb][i]));
-              sc = fmaf(-2.0f, tt, u4[e]);
             } else if constexpr (FMT == KM_RABITQ) {  // Eq. 4-5, fp32 in the oracle's order
               const int sd = 2 * acc[cb][pb][i] - __float_as_int(q4[e]);
               const float inner = fmaf(s4[e], (float)sd, b4[e] * (float)(2 * pop[pb] - A.di));
@@ -895,9 +848,7 @@ __global__ __launch_bounds__(k8Threads, 1) void assign_i8_kernel(AssignArgs A) {
               const float v = al[pb] * s4[e];
               sc = fmaf(-v, (float)sd, u4[e]);
             }
-            // LVQ4: rows past the last centroid repeat it (clamped rows and constants), so
-            // they tie with it exactly and lose on the index in the merges; no bound test
-            const bool take = (FMT == KM_LVQ4 || live) && sc < best[pb];
+            const bool take = live && sc < best[pb];
             best[pb] = take ? sc : best[pb];
             bidx[pb] = take ? j : bidx[pb];
           }
@@ -1261,7 +1212,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void assign_bits_kernel(AssignArgs
   }
 }
 
-// ---- SQ8 / bf16 assignment with direct global-to-LDS stages -------------------
+// ---- SQ8 / bf16 / LVQ4 assignment with direct global-to-LDS stages ------------
 // The same 256 x 256 workgroup tile and wave split as above (8 waves: 2 centroid
 // halves x 4 point quarters, 128 centroids x 64 points each; bf16 uses 16 waves, NWC
 // below), with the operand
@@ -1276,6 +1227,13 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void assign_bits_kernel(AssignArgs
 // copy.  Rows past the last centroid repeat the last centroid, codes and constant,
 // so their scores tie with it exactly and lose on the index: the epilogue is
 // branch-free and needs no bounds test.
+//
+// LVQ4 points stay packed (4 bits per dimension) through the copies, so a stage
+// moves 64 bytes per point row; the MFMA operand is unpacked after the LDS read
+// (low nibbles, then high nibbles of each word: two masks and a shift), and the
+// centroid preparation writes the int8 centroid codes in that same order. The
+// epilogue evaluates Eq. 2 per pair from the point's (s, b, A) and the centroid's
+// (b, S, N, s).
 //
 // With ngroups > 1 the workgroup (pt, g) sweeps centroid tiles g, g + ngroups, ...
 // of point tile pt; the ngroups workgroups of a point tile are consecutive among
@@ -1311,15 +1269,19 @@ constexpr int kQPackMaxDim = 1024;                  // SQ8 packed selection keys
 template <int FMT, bool SEG = false, int CB = 4, bool PK = false, int NWC = 2>
 __global__ __launch_bounds__(256 * NWC, 1) void assign_q8_kernel(AssignArgs A0) {
   constexpr bool BF = FMT == KM_BF16;
+  constexpr bool LV = FMT == KM_LVQ4;
   static_assert(CB == 2 || CB == 4, "64 or 128 centroids per wave");
   static_assert(NWC == 2 || NWC == 4, "2 or 4 waves along the centroids");
   constexpr int NW = 4 * NWC;                       // waves: NWC centroid groups x 4 point quarters
   constexpr int TC = 32 * CB * NWC;                 // centroids per tile
   constexpr int TP = kQT;                           // points per workgroup
+  constexpr int PRB = LV ? kRowBytes / 2 : kRowBytes;  // point bytes per row and stage (LVQ4: packed)
   constexpr int NCC = TC / (8 * NW);                // centroid copies per thread and stage
-  constexpr int NCOPY = (TC + TP) / (8 * NW);       // all copies per thread and stage
+  constexpr int NCOPY = NCC + TP * PRB / (1024 * NW);  // all copies per thread and stage
+  constexpr int NCONST = LV ? 4 : 1;                // per-centroid constants of the epilogue
   static_assert(NWC == 2 || (BF && CB == 2), "16 waves: bf16 with 64 centroids per wave (SQ8 spills there)");
-  constexpr int STAGE = (TC + TP) * kRowBytes;      // centroid rows, then point rows
+  static_assert(!LV || (!SEG && NWC == 2), "LVQ4: unsegmented, 8 waves");
+  constexpr int STAGE = TC * kRowBytes + TP * PRB;  // centroid rows, then point rows
   // a segmented launch narrows the arguments to this workgroup's segment
   AssignArgs A = A0;
   int64_t seg_p0 = 0;  // first row of this workgroup's point tile (segmented launch)
@@ -1335,14 +1297,14 @@ __global__ __launch_bounds__(256 * NWC, 1) void assign_q8_kernel(AssignArgs A0) 
     A.aoff = A0.aoff + sg.z;
     A.ngroups = 1;
   }
-  static_assert(FMT == KM_SQ8 || FMT == KM_BF16, "SQ8 or bf16 points");
+  static_assert(FMT == KM_SQ8 || FMT == KM_BF16 || LV, "SQ8, bf16 or LVQ4 points");
   static_assert(!PK || FMT == KM_SQ8, "packed keys are integer keys");
-  // SQ8 maximises the key 2D - ||c~||^2 (= -score, exact in int32); bf16 minimises
-  // the score ||c||^2 - 2<x,c> (fp32)
-  typedef typename std::conditional<BF, float, int>::type key_t;
+  // SQ8 maximises the key 2D - ||c~||^2 (= -score, exact in int32); bf16 and LVQ4
+  // minimise their fp32 scores
+  typedef typename std::conditional<BF || LV, float, int>::type key_t;
   __shared__ __align__(16) uint8_t qst0[STAGE];
   __shared__ __align__(16) uint8_t qst1[STAGE];
-  __shared__ __align__(16) float cparl[2][TC];
+  __shared__ __align__(16) float cparl[2][NCONST * TC];
   const int t = threadIdx.x;
   const int lane = t & 63, wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int r = lane & 31, h = lane >> 5;
@@ -1370,16 +1332,31 @@ __global__ __launch_bounds__(256 * NWC, 1) void assign_q8_kernel(AssignArgs A0) 
   // byte plus a 32-bit offset: point rows are clamped into the data once, centroid
   // rows only in a last, partial centroid tile.  In a partial last stage the lanes
   // whose chunk lies past the dimensions store zeros instead of copying.
+  //
+  // LVQ4 point rows hold a stage's 128 dimensions in 64 packed bytes (4 chunks of
+  // 32 dimensions): chunk c of point row R sits in slot c ^ ((R >> 2) & 3), so the
+  // 16 lanes that read one chunk each of 16 consecutive rows hit 64 distinct banks.
+  auto point_slot = [&](int i, int &row, int &chunk) {  // LVQ4 point copies (i >= NCC)
+    const int slot = ((i - NCC) * NW + wave) * 64 + lane;
+    row = slot >> 2;
+    chunk = (slot & 3) ^ ((row >> 2) & 3);
+  };
   auto source_offset = [&](int i) {
+    if (LV && i >= NCC) {
+      int row, chunk;
+      point_slot(i, row, chunk);
+      return (uint32_t)(min(row, prmax) * (int)A.pild + 16 * chunk);
+    }
     const int slot = (i * NW + wave) * 64 + lane;
     const int row = slot >> 3;
     const int chunk = (slot & 7) ^ ((row >> 1) & 7);
     return i < NCC ? (uint32_t)(row * (int)A.cild + 16 * chunk)
                    : (uint32_t)(min(row - TC, prmax) * (int)A.pild + 16 * chunk);
   };
-  // 16 waves have no registers to spare: their offsets are recomputed at each copy
-  // (a few vector instructions) and laundered so that the compiler keeps them there
-  constexpr bool kKeepOffsets = NWC == 2;
+  // 16 waves (and LVQ4, whose epilogue needs the point and centroid constants) have
+  // no registers to spare: their offsets are recomputed at each copy (a few vector
+  // instructions) and laundered so that the compiler keeps them there
+  constexpr bool kKeepOffsets = NWC == 2 && !LV;
   uint32_t soff[kKeepOffsets ? NCOPY : 1];
   if constexpr (kKeepOffsets) {
 #pragma unroll
@@ -1395,6 +1372,7 @@ __global__ __launch_bounds__(256 * NWC, 1) void assign_q8_kernel(AssignArgs A0) 
     }
   };
   float cpv = 0.f;
+  float cpx[3] = {0.f, 0.f, 0.f};  // LVQ4: the other three constants of row t
   // the next stage's tile constant for row t (loaded with its tile's first stage)
   auto load_constant = [&](int ct) {
     const int c0 = (g + ct * NG) * TC;
@@ -1402,6 +1380,12 @@ __global__ __launch_bounds__(256 * NWC, 1) void assign_q8_kernel(AssignArgs A0) 
     if (t < TC) {
       const int j = c0 + min(t, crmax);
       cpv = BF ? A.cp.cn[j] : __int_as_float(A.cp.qsum[j]);  // SQ8: -||c~||^2
+      if constexpr (LV) {  // b_y, S_y (the code sum as the float the epilogue multiplies), N_y, s_y
+        cpv = A.cp.cn[j];
+        cpx[0] = (float)A.cp.qsum[j];
+        cpx[1] = A.cp.u[j];
+        cpx[2] = A.cp.sig2[j];
+      }
       if constexpr (PK) {
         const int rr = t & (32 * CB - 1);  // row within its wave's centroid group
         const int id = (rr >> 5) * 16 + ((rr >> 3) & 3) * 4 + (rr & 3);
@@ -1414,11 +1398,17 @@ __global__ __launch_bounds__(256 * NWC, 1) void assign_q8_kernel(AssignArgs A0) 
     const int c0 = (g + ct * NG) * TC;
     const int crmax = min(A.k - 1 - c0, TC - 1);
     const int8_t *cbase = A.ci8 + (int64_t)c0 * A.cild + kRowBytes * s;
-    const uint8_t *psrc = pbase + kRowBytes * s;
+    const uint8_t *psrc = pbase + PRB * s;
     const bool full_stage = kRowBytes * (s + 1) <= A.di;
     const int slot = (i * NW + wave) * 64 + lane;
-    const int row = slot >> 3;
-    const int chunk = (slot & 7) ^ ((row >> 1) & 7);
+    int row = slot >> 3;
+    int chunk = (slot & 7) ^ ((row >> 1) & 7);
+    // the chunk's first dimension (LVQ4 point chunks hold 32 dimensions)
+    int dim0 = kRowBytes * s + 16 * chunk;
+    if (LV && i >= NCC) {
+      point_slot(i, row, chunk);
+      dim0 = kRowBytes * s + 32 * chunk;
+    }
     uint32_t off = offset_of(i);
     if (i < NCC && crmax < TC - 1) off = (uint32_t)(min(row, crmax) * (int)A.cild + 16 * chunk);
     const void *base = i < NCC ? (const void *)cbase : (const void *)psrc;
@@ -1426,7 +1416,7 @@ __global__ __launch_bounds__(256 * NWC, 1) void assign_q8_kernel(AssignArgs A0) 
     const uint32_t lds = (uint32_t)(size_t)wdst;
     if (full_stage) {
       lds_copy16(base, off, lds);
-    } else if (kRowBytes * s + 16 * chunk < A.di) {
+    } else if (dim0 < A.di) {
       lds_copy16(base, off, lds);
     } else {
       __attribute__((address_space(3))) uint32_t *z = (__attribute__((address_space(3))) uint32_t *)(wdst + 16 * lane);
@@ -1454,16 +1444,23 @@ __global__ __launch_bounds__(256 * NWC, 1) void assign_q8_kernel(AssignArgs A0) 
   };
   auto load = [&](int ct, int s, uint8_t *dst) {
     if (s == 0) load_constant(ct);
-    copies(ct, s, dst, plan_cb(ct, s), pbase + kRowBytes * s, plan_plain(ct, s), 0, NCOPY);
+    copies(ct, s, dst, plan_cb(ct, s), pbase + PRB * s, plan_plain(ct, s), 0, NCOPY);
   };
   auto store = [&](int ct, int s) {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    if (s == 0 && t < TC) cparl[ct & 1][t] = cpv;
+    if (s == 0 && t < TC) {
+      cparl[ct & 1][t] = cpv;
+      if constexpr (LV) {
+#pragma unroll
+        for (int q = 0; q < 3; ++q) cparl[ct & 1][(q + 1) * TC + t] = cpx[q];
+      }
+    }
   };
 
   // SQ8 with packed keys spreads the next stage's copies over the stage's four
-  // steps (5 % faster at 1M x 768); unpacked SQ8 issues them all before the MFMAs
-  // (spreading them there spills), and so does bf16 (spreading them gained nothing)
+  // steps (5 % faster at 1M x 768); unpacked SQ8 and LVQ4 issue them all before the
+  // MFMAs (spreading them there spills: LVQ4 ran 15 % slower), and so does bf16
+  // (spreading them gained nothing)
   constexpr bool SPREAD = PK;
   int sp_ct = 0, sp_s = 0;
   uint8_t *sp_dst = nullptr;
@@ -1478,11 +1475,22 @@ __global__ __launch_bounds__(256 * NWC, 1) void assign_q8_kernel(AssignArgs A0) 
   auto mfma_stage = [&](const uint8_t *buf, auto first) {
     constexpr bool kFirst = decltype(first)::value;
     uint4 av[1][CB], bv[1][k8PB];
+    // LVQ4: step g = 2j + e of a stage multiplies dimensions 16 (4j + 2h + e) .. + 15
+    // in lane half h: one read of packed point chunk 2j + h serves steps 2j and 2j + 1
+    // (8 bytes each), and the centroid operand is int8 chunk 4j + 2h + e of its row
     auto read = [&](int g, int slot) {
-      const int so = 16 * ((2 * g + h) ^ ((r >> 1) & 7));
+      const int ca = LV ? 2 * g - (g & 1) + 2 * h : 2 * g + h;
+      const int so = 16 * (ca ^ ((r >> 1) & 7));
+      if constexpr (LV) {
+        const int sp = 16 * (((g & ~1) + h) ^ ((r >> 2) & 3));
 #pragma unroll
-      for (int pb = 0; pb < k8PB; ++pb)
-        bv[slot][pb] = *reinterpret_cast<const uint4 *>(buf + (TC + wp * 32 * k8PB + pb * 32 + r) * kRowBytes + so);
+        for (int pb = 0; pb < k8PB; ++pb)
+          bv[slot][pb] = *reinterpret_cast<const uint4 *>(buf + TC * kRowBytes + (wp * 32 * k8PB + pb * 32 + r) * PRB + sp);
+      } else {
+#pragma unroll
+        for (int pb = 0; pb < k8PB; ++pb)
+          bv[slot][pb] = *reinterpret_cast<const uint4 *>(buf + (TC + wp * 32 * k8PB + pb * 32 + r) * kRowBytes + so);
+      }
 #pragma unroll
       for (int cb = 0; cb < CB; ++cb)
         av[slot][cb] = *reinterpret_cast<const uint4 *>(buf + (wc * 32 * CB + cb * 32 + r) * kRowBytes + so);
@@ -1507,6 +1515,15 @@ __global__ __launch_bounds__(256 * NWC, 1) void assign_q8_kernel(AssignArgs A0) 
           if constexpr (BF) {
             acc[cb][pb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                 __builtin_bit_cast(bf16x8, av[cur][cb]), __builtin_bit_cast(bf16x8, bv[cur][pb]), cin, 0, 0, 0);
+          } else if constexpr (LV) {
+            // 16 packed codes -> 16 bytes: the low nibbles of a word (even dimensions)
+            // then its high nibbles (odd ones), the order of the centroid codes
+            const uint32_t w0 = (g & 1) ? bv[cur][pb].z : bv[cur][pb].x;
+            const uint32_t w1 = (g & 1) ? bv[cur][pb].w : bv[cur][pb].y;
+            constexpr uint32_t M = 0x0F0F0F0Fu;
+            const i32x4 a4 = {(int)av[cur][cb].x, (int)av[cur][cb].y, (int)av[cur][cb].z, (int)av[cur][cb].w};
+            const i32x4 b4 = {(int)(w0 & M), (int)((w0 >> 4) & M), (int)(w1 & M), (int)((w1 >> 4) & M)};
+            acc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a4, b4, cin, 0, 0, 0);
           } else {
             const uint4 bq = flip4(bv[cur][pb]);  // point codes recentred to int8
             const i32x4 a4 = {(int)av[cur][cb].x, (int)av[cur][cb].y, (int)av[cur][cb].z, (int)av[cur][cb].w};
@@ -1522,14 +1539,56 @@ __global__ __launch_bounds__(256 * NWC, 1) void assign_q8_kernel(AssignArgs A0) 
   int bidx[k8PB];
 #pragma unroll
   for (int pb = 0; pb < k8PB; ++pb) {
-    best[pb] = BF ? (key_t)-INFINITY : (key_t)INT_MIN;
+    best[pb] = LV ? (key_t)INFINITY : BF ? (key_t)-INFINITY : (key_t)INT_MIN;
     bidx[pb] = INT_MAX;
+  }
+  f32x4 vp[k8PB] = {};  // LVQ4: (s, b, A, N) of the lane's points
+  if constexpr (LV) {
+#pragma unroll
+    for (int pb = 0; pb < k8PB; ++pb)
+      vp[pb] = *reinterpret_cast<const f32x4 *>(A.vparams + 4 * (p0 + min(wp * 32 * k8PB + pb * 32 + r, prmax)));
   }
   // rows ascend with (cb, i) in a lane, so the strict comparison keeps the smallest
   // index among ties; the tile-local row without the wave's and half's offsets is a
   // constant here
   auto epilogue = [&](int ct) {
     const float *cp = cparl[ct & 1];
+    if constexpr (LV) {  // Eq. 2 without N_x, fp32 in the oracle's order
+      int loc[k8PB] = {-1, -1};
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb) {
+#pragma unroll
+        for (int i4 = 0; i4 < 4; ++i4) {
+          const int cr = wc * 32 * CB + cb * 32 + 8 * i4 + 4 * h;
+          const f32x4 b4 = *reinterpret_cast<const f32x4 *>(cp + cr);           // b_y
+          const f32x4 q4 = *reinterpret_cast<const f32x4 *>(cp + TC + cr);      // S_y
+          const f32x4 u4 = *reinterpret_cast<const f32x4 *>(cp + 2 * TC + cr);  // N_y
+          const f32x4 s4 = *reinterpret_cast<const f32x4 *>(cp + 3 * TC + cr);  // s_y
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int i = 4 * i4 + e;
+            const int cl = cb * 32 + 8 * i4 + e;
+#pragma unroll
+            for (int pb = 0; pb < k8PB; ++pb) {
+              const float sy = s4[e];
+              const float tt =
+                  fmaf(vp[pb][1] * sy, q4[e], fmaf(b4[e], vp[pb][2], (vp[pb][0] * sy) * (float)acc[cb][pb][i]));
+              const float sc = fmaf(-2.0f, tt, u4[e]);
+              if (sc < best[pb]) {
+                best[pb] = sc;
+                loc[pb] = cl;
+              }
+            }
+          }
+          // four rows at a time: their 16 constants, not a block's 64, in registers
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+#pragma unroll
+      for (int pb = 0; pb < k8PB; ++pb)
+        if (loc[pb] >= 0) bidx[pb] = (g + ct * NG) * TC + wc * 32 * CB + loc[pb] + 4 * h;
+      return;
+    }
     if constexpr (PK) {
       int tk[k8PB] = {INT_MIN, INT_MIN};  // the tile's best packed key per point block
 #pragma unroll
@@ -1607,7 +1666,7 @@ __global__ __launch_bounds__(256 * NWC, 1) void assign_q8_kernel(AssignArgs A0) 
       sp_s = s_n;
       sp_dst = nxt;
       sp_cb = plan_cb(ct_n, s_n);
-      sp_pb = pbase + kRowBytes * s_n;
+      sp_pb = pbase + PRB * s_n;
       sp_plain = plan_plain(ct_n, s_n);
       if (has_next && s_n == 0) load_constant(ct_n);
     } else {
@@ -1665,9 +1724,10 @@ __global__ __launch_bounds__(256 * NWC, 1) void assign_q8_kernel(AssignArgs A0) 
   }
 
   // merges in the key order (SQ8: exact integers), smaller index on ties; the
-  // stored score is the key for bf16 and the negated key (||c~||^2 - 2<x~,c~>) for SQ8
+  // stored score is the key for bf16 and LVQ4 and the negated key (||c~||^2 - 2<x~,c~>)
+  // for SQ8
   auto better = [](key_t o, int oi, key_t b, int bi) {
-    return (BF ? o < b : o > b) || (o == b && oi < bi);
+    return (BF || LV ? o < b : o > b) || (o == b && oi < bi);
   };
 #pragma unroll
   for (int pb = 0; pb < k8PB; ++pb) {
@@ -1705,10 +1765,11 @@ __global__ __launch_bounds__(256 * NWC, 1) void assign_q8_kernel(AssignArgs A0) 
       const int64_t p = p0 + pc;
       if (p < A.n) {
         if (A.keys) {
-          atomicMin(A.keys + p, BF ? score_key((float)best[pb], bidx[pb]) : int_score_key(-(int)best[pb], bidx[pb]));
+          atomicMin(A.keys + p,
+                    BF || LV ? score_key((float)best[pb], bidx[pb]) : int_score_key(-(int)best[pb], bidx[pb]));
         } else {
           A.assign[p] = bidx[pb] + A.aoff;
-          if (A.score) A.score[p] = BF ? (float)best[pb] : (float)(-(int)best[pb]);
+          if (A.score) A.score[p] = BF || LV ? (float)best[pb] : (float)(-(int)best[pb]);
         }
       }
     }
@@ -2411,7 +2472,9 @@ __global__ __launch_bounds__(256) void prep_kernel(const void *Cv, int k, int d,
     int ts = 0, tq = 0;
     for (int i = t; i < d; i += 256) {
       const int v = (int)fminf(fmaxf(rintf((c[i] - lo) / sc), 0.f), 15.f);
-      q[(int64_t)j * d + i] = (int8_t)v;
+      // within each 8 dimensions the even ones first, then the odd ones: the byte
+      // order in which the assignment unpacks the points' packed codes
+      q[(int64_t)j * d + (i & ~7) + ((i & 1) << 2) + ((i >> 1) & 3)] = (int8_t)v;
       ts += v;
       tq += v * v;
     }
@@ -2722,7 +2785,7 @@ int assign_groups(const Points &P, int k) {
     constexpr int TC = Geo<Blocking<KM_F32>::CB, Blocking<KM_F32>::PB>::TC;
     return (int)std::min<int64_t>(8, cdiv(k, TC));
   }
-  if (P.fmt == KM_BF16 || (P.fmt == KM_SQ8 && P.d <= kQMaxDimSQ8)) return tile_groups(P.n, k);
+  if (P.fmt == KM_BF16 || P.fmt == KM_LVQ4 || (P.fmt == KM_SQ8 && P.d <= kQMaxDimSQ8)) return tile_groups(P.n, k);
   return 1;
 }
 
@@ -2787,8 +2850,8 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
     } else {
       hipLaunchKernelGGL(assign_i8_kernel<FMT>, dim3((unsigned)cdiv(P.n, kT8)), dim3(k8Threads), 0, s, A);
     }
-  } else if constexpr (FMT == KM_SQ8 || FMT == KM_BF16) {
-    if (FMT == KM_BF16 || P.d <= kQMaxDimSQ8) {
+  } else if constexpr (FMT == KM_SQ8 || FMT == KM_BF16 || FMT == KM_LVQ4) {
+    if (FMT != KM_SQ8 || P.d <= kQMaxDimSQ8) {
       const int64_t npt = cdiv(P.n, kQT);
       const int ng = assign_groups(P, k);
       A.n_ptiles = npt;
@@ -2810,7 +2873,7 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
         hipLaunchKernelGGL((assign_q8_kernel<FMT, false, 2, false, 4>), grid, dim3(kQWideThreads), 0, s, A);
       } else {
         if (pk)
-          hipLaunchKernelGGL((assign_q8_kernel<FMT, false, 4, true>), grid, dim3(kQThreads), 0, s, A);
+          hipLaunchKernelGGL((assign_q8_kernel<FMT, false, 4, FMT == KM_SQ8>), grid, dim3(kQThreads), 0, s, A);
         else
           hipLaunchKernelGGL((assign_q8_kernel<FMT, false, 4>), grid, dim3(kQThreads), 0, s, A);
       }
@@ -2818,11 +2881,9 @@ km_status launch_assign_t(const Points &P, const void *C, const CentroidPrep &cp
         const dim3 gp((unsigned)cdiv(P.n, 256));
         hipLaunchKernelGGL(keys_unpack_kernel<FMT == KM_SQ8>, gp, dim3(256), 0, s, cp.keys, P.n, assign, score, aoff);
       }
-    } else {
+    } else if constexpr (FMT == KM_SQ8) {
       hipLaunchKernelGGL(assign_i8_kernel<FMT>, dim3((unsigned)cdiv(P.n, kT8)), dim3(k8Threads), 0, s, A);
     }
-  } else if constexpr (FMT == KM_LVQ4) {
-    hipLaunchKernelGGL(assign_i8_kernel<FMT>, dim3((unsigned)cdiv(P.n, kT8)), dim3(k8Threads), 0, s, A);
   } else if constexpr (FMT == KM_F32) {
     const int64_t npt = cdiv(P.n, kQT);
     const int ng = assign_groups(P, k);
