@@ -651,6 +651,10 @@ static km_status fine_impl(const Points &p, const int32_t *meso, int k_meso, int
   // fp32, SQ8 and bf16: one assignment launch per pass over all meso-clusters
   // (segment and tile tables); other formats launch per meso-cluster
   const int seg_rows = assign_segment_rows(p);
+  // a per-meso-cluster launch may split its few point tiles' centroid tiles over
+  // groups (merging through per-point keys) where the launch over all N points
+  // would not, and then the preparation sized for N holds no keys: give them room
+  const size_t b_keys = seg_rows == 0 ? al(sizeof(unsigned long long) * (size_t)N) : 0;
   // point tiles of the segments with 128-centroid tiles first (n128 of them), then
   // those with 256-centroid tiles: one launch each
   std::vector<int4> segs;
@@ -670,7 +674,7 @@ static km_status fine_impl(const Points &p, const int32_t *meso, int k_meso, int
   const size_t b_segs = al(sizeof(int4) * segs.size());
   const size_t b_tiles = al(sizeof(int2) * tiles.size());
   Scratch ws(s);
-  st = ws.alloc(b_perm + b_prep + b_upd + b_a + b_score + b_xc + b_part + b_idx + b_seg + b_segs + b_tiles);
+  st = ws.alloc(b_perm + b_prep + b_upd + b_a + b_score + b_xc + b_part + b_idx + b_seg + b_segs + b_tiles + b_keys);
   if (st != KM_OK) return st;
   uint8_t *w = ws.get();
   uint8_t *wperm = w;
@@ -684,6 +688,7 @@ static km_status fine_impl(const Points &p, const int32_t *meso, int k_meso, int
   int *dseg = reinterpret_cast<int *>(wupd + b_upd + b_a + b_score + b_xc + b_part + b_idx);
   int4 *dsegs = reinterpret_cast<int4 *>(reinterpret_cast<uint8_t *>(dseg) + b_seg);
   int2 *dtiles = reinterpret_cast<int2 *>(reinterpret_cast<uint8_t *>(dsegs) + b_segs);
+  auto *keys = b_keys ? reinterpret_cast<unsigned long long *>(reinterpret_cast<uint8_t *>(dtiles) + b_tiles) : nullptr;
   KMQ_STAGE(clk, kStOther, launch_permute_points(p, so.perm, N, wperm, &q, s));
   if (!segs.empty()) {
     KMQ_HIP(hipMemcpyAsync(dsegs, segs.data(), sizeof(int4) * segs.size(), hipMemcpyHostToDevice, s));
@@ -698,6 +703,7 @@ static km_status fine_impl(const Points &p, const int32_t *meso, int k_meso, int
   CentroidPrep cp;
   for (int it = 0; it <= iters; ++it) {
     KMQ_STAGE(clk, kStPrep, launch_prep(q, C, k, wprep, &cp, s));
+    if (cp.keys == nullptr) cp.keys = keys;
     st = clk.begin(kStAssign);
     if (st != KM_OK) return st;
     if (!segs.empty()) {  // every meso-cluster against its own fine centroids, one launch per tile size

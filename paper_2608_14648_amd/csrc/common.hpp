@@ -44,9 +44,10 @@ struct CentroidPrep {
   const int *qsum;     // SQ8: -||c~||^2 ; SIGN1/HYBRID/RABITQ: T_j = sum q ; LVQ4: S_j = sum of codes
   const float *u;      // SIGN1/HYBRID: (sigma*sigma)*Q ; RABITQ: ||c||^2 ; LVQ4: N_j
   const float *sig2;   // SIGN1/HYBRID: 2*sigma ; RABITQ, LVQ4: scale s
-  const int8_t *q;     // SIGN1/HYBRID: int8 residual codes, k x dt ; RABITQ, LVQ4: codes 0..15, k x d
+  const int8_t *q;     // SIGN1/HYBRID: int8 residual codes, k x dt ; RABITQ: codes 0..15, k x d ; LVQ4: codes
+                       // 0..15, k x d, each 8 dims ordered 0 2 4 6 1 3 5 7 (the unpacked point order)
   const uint16_t *cb;  // BF16: centroids rounded to bfloat16, k x d
-  unsigned long long *keys;  // centroid-tile groups (F32/HYBRID/SQ8/BF16): per-point (score, index) keys
+  unsigned long long *keys;  // centroid-tile groups (F32/HYBRID/SQ8/BF16/LVQ4): per-point (score, index) keys
 };
 
 // Host-side error plumbing.
