@@ -599,9 +599,9 @@ __global__ __launch_bounds__(256) void keys_unpack_kernel(const unsigned long lo
   if (score) score[p] = INT ? (float)(int)((uint32_t)(key >> 32) ^ 0x80000000u) : key_score(key);
 }
 
-// ---- int8 / bf16 assignment with 256 x 256 workgroup tiles -------------------
+// ---- int8 assignment with 256 x 256 workgroup tiles ---------------------------
 // Register-staged stages; the direct-copy kernels below replace it except for SQ8
-// beyond 8192 dimensions and 1-bit points beyond 1280.  An int8 or bf16 MFMA is 16-32x denser than
+// beyond 8192 dimensions and 1-bit points beyond 1280.  An int8 MFMA is 16-32x denser than
 // the fp32 one, so operand bandwidth decides the tiling: the workgroup owns 256
 // centroids x 256 points per stage (a quarter of the L2 bytes per MFMA of a 128
 // tile) and each of its 8 waves 128 centroids x 64 points (4 x 2 blocks of
@@ -637,7 +637,7 @@ __device__ __forceinline__ void load_stage8(const AssignArgs &A, int s, int64_t 
     const int b = b0 + 16 * col;
     const int bc = b < A.di ? b : 0;
     R.c[i] = *reinterpret_cast<const uint4 *>(cbase + (uint32_t)(min(row, crmax) * (int)A.cild + bc));
-    if (FMT == KM_SQ8 || FMT == KM_BF16)
+    if (FMT == KM_SQ8)
       R.p[i] = *reinterpret_cast<const uint4 *>(pbase8 + (uint32_t)(min(row, prmax) * (int)A.pild + bc));
   }
   if (FMT == KM_SIGN1 || FMT == KM_RABITQ) {
@@ -651,7 +651,7 @@ __device__ __forceinline__ void load_stage8(const AssignArgs &A, int s, int64_t 
   }
   if (s == 0) {  // per-centroid constants: threads t < kT8 (the others load a valid duplicate)
     const int64_t j = min<int64_t>(c0 + (t & (kT8 - 1)), A.k - 1);
-    R.cpar[1] = FMT == KM_BF16 ? A.cp.cn[j] : __int_as_float(A.cp.qsum[j]);
+    R.cpar[1] = __int_as_float(A.cp.qsum[j]);
     if (FMT == KM_SIGN1 || FMT == KM_RABITQ) {
       R.cpar[2] = A.cp.u[j];
       R.cpar[3] = A.cp.sig2[j];
@@ -675,7 +675,6 @@ __device__ __forceinline__ void store_stage8(const AssignArgs &A, int s, const S
     *reinterpret_cast<uint4 *>(ct + row * kLdsStride + 16 * col) = mask4(cv, ok);
     if (FMT == KM_SQ8)
       *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 16 * col) = mask4(flip4(R.p[i]), ok);
-    if (FMT == KM_BF16) *reinterpret_cast<uint4 *>(pt + row * kLdsStride + 16 * col) = mask4(R.p[i], ok);
   }
   if (FMT == KM_SIGN1 || FMT == KM_RABITQ) {
 #pragma unroll
@@ -704,9 +703,8 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 template <bool BF>
 using Acc8 = typename std::conditional<BF, f32x16, i32x16>::type;
 
-template <bool BF>
 __device__ __forceinline__ void mfma_stage8(const uint8_t *cbuf, const uint8_t *pbuf, int wc, int wp, int r, int h,
-                                            Acc8<BF> (&acc)[4][k8PB]) {
+                                            i32x16 (&acc)[4][k8PB]) {
   uint4 av[2][4], bv[2][k8PB];
 #pragma unroll
   for (int cb = 0; cb < 4; ++cb)
@@ -731,22 +729,16 @@ __device__ __forceinline__ void mfma_stage8(const uint8_t *cbuf, const uint8_t *
     for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
       for (int pb = 0; pb < k8PB; ++pb) {
-        const Acc8<BF> cin = acc[cb][pb];
-        if constexpr (BF) {
-          const bf16x8 a8 = __builtin_bit_cast(bf16x8, av[cur][cb]);
-          const bf16x8 b8 = __builtin_bit_cast(bf16x8, bv[cur][pb]);
-          acc[cb][pb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a8, b8, cin, 0, 0, 0);
-        } else {
-          const i32x4 a4 = {(int)av[cur][cb].x, (int)av[cur][cb].y, (int)av[cur][cb].z, (int)av[cur][cb].w};
-          const i32x4 b4 = {(int)bv[cur][pb].x, (int)bv[cur][pb].y, (int)bv[cur][pb].z, (int)bv[cur][pb].w};
-          acc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a4, b4, cin, 0, 0, 0);
-        }
+        const i32x4 a4 = {(int)av[cur][cb].x, (int)av[cur][cb].y, (int)av[cur][cb].z, (int)av[cur][cb].w};
+        const i32x4 b4 = {(int)bv[cur][pb].x, (int)bv[cur][pb].y, (int)bv[cur][pb].z, (int)bv[cur][pb].w};
+        acc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a4, b4, acc[cb][pb], 0, 0, 0);
       }
   }
 }
 
 template <int FMT>
 __global__ __launch_bounds__(k8Threads, 1) void assign_i8_kernel(AssignArgs A) {
+  static_assert(FMT == KM_SQ8 || FMT == KM_SIGN1 || FMT == KM_RABITQ, "int8 formats beyond the direct-copy kernels");
   __shared__ __align__(16) uint8_t lds[2 * kStageBytes8];
   __shared__ __align__(16) float cparl[2][4 * kT8];
   typedef typename std::conditional<FMT == KM_SQ8, int, float>::type score_t;
@@ -774,8 +766,7 @@ __global__ __launch_bounds__(k8Threads, 1) void assign_i8_kernel(AssignArgs A) {
       }
     }
   }
-  constexpr bool BF = FMT == KM_BF16;
-  Acc8<BF> acc[4][k8PB];
+  i32x16 acc[4][k8PB];
 #pragma unroll
   for (int a = 0; a < 4; ++a)
 #pragma unroll
@@ -804,7 +795,7 @@ __global__ __launch_bounds__(k8Threads, 1) void assign_i8_kernel(AssignArgs A) {
       const int ct_n = (s + 1 == S) ? ct + 1 : ct;
       if (has_next) load_stage8<FMT>(A, s_n, (int64_t)ct_n * kT8, p0, R);
       const uint8_t *buf = lds + (it & 1) * kStageBytes8;
-      mfma_stage8<BF>(buf, buf + kTileBytes8, wc, wp, r, h, acc);
+      mfma_stage8(buf, buf + kTileBytes8, wc, wp, r, h, acc);
       if (has_next) store_stage8<FMT>(A, s_n, R, lds + ((it + 1) & 1) * kStageBytes8, cparl[ct_n & 1]);
       __syncthreads();
     }
@@ -837,8 +828,6 @@ __global__ __launch_bounds__(k8Threads, 1) void assign_i8_kernel(AssignArgs A) {
             score_t sc;
             if constexpr (FMT == KM_SQ8) {
               sc = -__float_as_int(q4[e]) - 2 * acc[cb][pb][i];  // the constant is -||c~||^2
-            } else if constexpr (FMT == KM_BF16) {
-              sc = fmaf(-2.0f, acc[cb][pb][i], q4[e]);  // ||c||^2 - 2<x,c>
             } else if constexpr (FMT == KM_RABITQ) {  // Eq. 4-5, fp32 in the oracle's order
               const int sd = 2 * acc[cb][pb][i] - __float_as_int(q4[e]);
               const float inner = fmaf(s4[e], (float)sd, b4[e] * (float)(2 * pop[pb] - A.di));
@@ -1334,8 +1323,11 @@ __global__ __launch_bounds__(256 * NWC, 1) void assign_q8_kernel(AssignArgs A0) 
   // whose chunk lies past the dimensions store zeros instead of copying.
   //
   // LVQ4 point rows hold a stage's 128 dimensions in 64 packed bytes (4 chunks of
-  // 32 dimensions): chunk c of point row R sits in slot c ^ ((R >> 2) & 3), so the
-  // 16 lanes that read one chunk each of 16 consecutive rows hit 64 distinct banks.
+  // 32 dimensions): chunk c of point row R sits in slot c ^ ((R >> 2) & 3), which
+  // spreads the 16 rows that 16 lanes read over 16 distinct 16-byte bank groups if
+  // an LDS cycle serves 16 lanes as it does for the 128-byte rows; the counters
+  // still show two passes per read (a 2-way conflict on these reads only, worth
+  // about 1 % of the kernel; other placements tried cost more in registers).
   auto point_slot = [&](int i, int &row, int &chunk) {  // LVQ4 point copies (i >= NCC)
     const int slot = ((i - NCC) * NW + wave) * 64 + lane;
     row = slot >> 2;
