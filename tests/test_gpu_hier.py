@@ -207,26 +207,31 @@ def test_fine_integer_formats_lockstep(km, torch, fmt, d):
         C_start = C1_o
 
 
-def test_fine_per_cluster_launch_groups(km, torch):
+@pytest.mark.parametrize("fmt,d", [("lvq4", 32), ("hybrid", 128)])
+def test_fine_per_cluster_launch_groups(km, torch, fmt, d):
     """Per-meso-cluster launches (every format but fp32, SQ8 and bf16) whose centroid
     tiles split over groups while the launch over all points would not: 131072
     points and k = 1028 take one group on a 256-CU device (five 256-centroid tiles;
     two groups' rounds tie with one), but each of the four meso-clusters of 32768
     points and 257 fine centroids takes two, so the fine phase must supply the
-    per-point merge keys that the preparation for all points leaves out.  LVQ4,
-    bit-exact against the oracle."""
-    n, d, k_meso, k = 131072, 32, 4, 1028
+    per-point merge keys that the preparation for all points leaves out.  LVQ4
+    bit-exact against the oracle; the hybrid (32-dim front, 96-dim 1-bit tail: the
+    direct-copy hybrid kernel) within the fp tolerance."""
+    n, k_meso, k = 131072, 4, 1028
     X = blobs(n, d, 64, seed=7)
-    Po, Pg = formats(km, torch, "lvq4", X)
+    Po, Pg = formats(km, torch, fmt, X)
     am = np.repeat(np.arange(k_meso, dtype=np.int32), n // k_meso)
-    say("fine lvq4 per-cluster launch groups")
+    say(f"fine {fmt} per-cluster launch groups")
     C0_o, a0_o, kf_o, _ = orc.fit_fine(Po, am, k_meso, k, 0)
     C0, a0, kf, _ = km.kmeans_fine(Pg, to_dev(am, torch), k_meso, k, 0)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(kf, kf_o)
     assert (np.asarray(kf) == k // k_meso).all()
     np.testing.assert_array_equal(host(C0), C0_o)
-    np.testing.assert_array_equal(host(a0), a0_o)
+    if fmt == "lvq4":
+        np.testing.assert_array_equal(host(a0), a0_o)
+    else:
+        assert_fp_assign(host(a0), a0_o, hybrid_d_of(Po, C0_o), f"{fmt} per-cluster groups")
 
 
 def hybrid_d_of(Po, C):
