@@ -2,7 +2,7 @@
 allocate, with its scratch in the library's static device array.  Checked
 through the C ABI against kmeans_assign on the same inputs, on two calls in a
 row (the second with fewer points, so the static array still holds the first
-call's contents), in fp32, SQ8, bfloat16 and 1-bit formats, with the objective.
+call's contents), in fp32, SQ8, bfloat16, LVQ4 and 1-bit formats, with the objective.
 """
 import numpy as np
 import pytest
@@ -27,11 +27,14 @@ def _inputs(torch, km, fmt, n):
         return km.points_sq8(codes), codes[idx].contiguous()
     if fmt == "bf16":
         return km.points_bf16(km.quantize_bf16(X)), X[idx].contiguous()
+    if fmt == "lvq4":
+        codes, par = km.quantize_lvq4(X)
+        return km.points_lvq4(codes, par, spec.d), X[idx].contiguous()
     bits, m, alpha, _ = km.quantize_sign1(X)
     return km.points_sign1(bits, alpha, m, spec.d), X[idx].contiguous()
 
 
-@pytest.mark.parametrize("fmt", ["f32", "sq8", "bf16", "sign1"])
+@pytest.mark.parametrize("fmt", ["f32", "sq8", "bf16", "lvq4", "sign1"])
 def test_noalloc_matches_kmeans_assign(fmt):
     torch = torch_cuda()
     import paper_2608_14648_amd as km
