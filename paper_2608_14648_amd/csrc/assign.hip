@@ -1468,8 +1468,10 @@ __global__ __launch_bounds__(256 * NWC, 1) void assign_q8_kernel(AssignArgs A0) 
     constexpr bool kFirst = decltype(first)::value;
     uint4 av[1][CB], bv[1][k8PB];
     // LVQ4: step g = 2j + e of a stage multiplies dimensions 16 (4j + 2h + e) .. + 15
-    // in lane half h: one read of packed point chunk 2j + h serves steps 2j and 2j + 1
-    // (8 bytes each), and the centroid operand is int8 chunk 4j + 2h + e of its row
+    // in lane half h: packed point chunk 2j + h holds the point operands of steps 2j
+    // and 2j + 1 (8 bytes each; each step reads it again, which keeps fewer registers
+    // live than holding it across the pair), and the centroid operand is int8 chunk
+    // 4j + 2h + e of its row
     auto read = [&](int g, int slot) {
       const int ca = LV ? 2 * g - (g & 1) + 2 * h : 2 * g + h;
       const int so = 16 * (ca ^ ((r >> 1) & 7));
