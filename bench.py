@@ -871,12 +871,25 @@ def wl_pruned(fmt):
         def finish(out, timer, elapsed, K):
             s = timer.stats[fmt]
             c = res["cnt"].astype(np.float64)
+            # the MFMA work of the assignment passes of one fit: the first, full pass,
+            # then T pruned passes (the d'-dim front on every pair, the full distance on
+            # the survivors), against the whole assignment stage's time (front, tau and
+            # refinement kernels alike)
+            d_front = 32 * ((spec.d + 255) // 256)
+            work = K * (2.0 * spec.n * k * spec.d + T * 2.0 * spec.n * k * d_front + 2.0 * spec.d * c[2])
+            ach = work / (s["assign_ms"] * 1e-3) / 1e12
+            peak = "fp32" if fmt == "f32" else "int8"
             return line(T * K / elapsed, "Lloyd iters/s", "f32" if fmt == "f32" else "u8",
                         {"workload": wname, "N": spec.n, "d": spec.d, "k": k, "iters": T, "format": fmt,
                          "eps0": 2.1, "d_front": 32 * ((spec.d + 255) // 256), "rotation": "random orthogonal"},
                         partition_cost=float(out["cost"].item()),
                         survivors={"front_pass": c[1] / max(1.0, c[0]), "full_distance": c[2] / max(1.0, c[0]),
                                    "candidates_tested_per_pass": c[0] / T},
+                        roofline={"bound": "mfma", "kernel": "all assignment launches (first full pass, then the "
+                                  "pruned front, threshold and refinement kernels)",
+                                  "achieved": ach, "peak": PEAK[peak], "unit": PEAK_UNIT[peak],
+                                  "frac": ach / PEAK[peak], "traffic": None,
+                                  "algorithmic_work_per_fit": work / K},
                         stages={fmt: stage_summary(s)})
 
         def cpu_baseline():
