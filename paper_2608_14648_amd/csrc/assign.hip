@@ -1291,11 +1291,12 @@ __global__ __launch_bounds__(256 * NWC, 1) void assign_q8_kernel(AssignArgs A0) 
   // SQ8 maximises the key 2D - ||c~||^2 (= -score, exact in int32); bf16 and LVQ4
   // minimise their fp32 scores
   typedef typename std::conditional<BF || LV, float, int>::type key_t;
-  // SQ8 on 128-centroid tiles (k <= 128, and the hierarchical phases' small
-  // centroid sets): a stage carries only ~1000 MFMA cycles per SIMD against a copy
-  // latency of a microsecond or more, so three stage buffers (3 x 48 KB) keep the
-  // copies two stages ahead; 17 % faster on a 2M x 1024, k = 112 pass
-  constexpr bool TRI = FMT == KM_SQ8 && CB == 2;
+  // 128-centroid tiles of the 8-wave shape (k <= 128, and the hierarchical phases'
+  // small centroid sets): a stage carries only ~1000 MFMA cycles per SIMD (SQ8)
+  // against a copy latency of a microsecond or more, so three stage buffers (3 x 48
+  // KB; LVQ4 3 x 32 KB) keep the copies two stages ahead; SQ8 17 % faster on a
+  // 2M x 1024, k = 112 pass
+  constexpr bool TRI = CB == 2 && NWC == 2;
   __shared__ __align__(16) uint8_t qst0[STAGE];
   __shared__ __align__(16) uint8_t qst1[STAGE];
   __shared__ __align__(16) uint8_t qst2[TRI ? STAGE : 16];
@@ -1653,6 +1654,21 @@ __global__ __launch_bounds__(256 * NWC, 1) void assign_q8_kernel(AssignArgs A0) 
       if (loc[pb] >= 0) bidx[pb] = (g + ct * NG) * TC + wc * 32 * CB + loc[pb] + 4 * h;
   };
 
+  // bf16: the accumulators start at -||c||^2 / 2 of their row (exact halving), so
+  // they end at <x,c> - ||c||^2 / 2 and the epilogue only keeps the largest
+  auto seed = [&](int ct) {
+    const float *cp = cparl[ct & 1];
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        const f32x4 v = *reinterpret_cast<const f32x4 *>(cp + wc * 32 * CB + cb * 32 + 8 * m + 4 * h);
+#pragma unroll
+        for (int pb = 0; pb < k8PB; ++pb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[cb][pb][4 * m + e] = -0.5f * v[e];
+      }
+  };
   if constexpr (TRI) {
     // stage j (tile j / S, stage j % S) lives in buffer j % 3.  Step it issues the
     // copies of stage it + 2, then waits until at most NCOPY of its own copies are in
@@ -1667,8 +1683,7 @@ __global__ __launch_bounds__(256 * NWC, 1) void assign_q8_kernel(AssignArgs A0) 
     };
     auto set_constants = [&](int ct) {
       load_constant(ct);
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      if (t < TC) cparl[ct & 1][t] = cpv;
+      store(ct, 0);  // waits for every copy in flight, then writes the tile's constants
     };
     set_constants(0);
     issue(0);
@@ -1682,6 +1697,7 @@ __global__ __launch_bounds__(256 * NWC, 1) void assign_q8_kernel(AssignArgs A0) 
     for (int it = 0; it < total; ++it) {
       const int ct = it / S, s = it % S;
       if (it + 2 < total) issue(it + 2);
+      if (BF && s == 0) seed(ct);
       if (s == 0)
         mfma_stage(buf_of(it), std::true_type{});
       else
@@ -1717,21 +1733,7 @@ __global__ __launch_bounds__(256 * NWC, 1) void assign_q8_kernel(AssignArgs A0) 
     } else {
       if (has_next) load(ct_n, s_n, nxt);
     }
-    if (BF && s == 0) {
-      // bf16: the accumulators start at -||c||^2 / 2 of their row (exact halving),
-      // so they end at <x,c> - ||c||^2 / 2 and the epilogue only keeps the largest
-      const float *cp = cparl[ct & 1];
-#pragma unroll
-      for (int cb = 0; cb < CB; ++cb)
-#pragma unroll
-        for (int m = 0; m < 4; ++m) {
-          const f32x4 v = *reinterpret_cast<const f32x4 *>(cp + wc * 32 * CB + cb * 32 + 8 * m + 4 * h);
-#pragma unroll
-          for (int pb = 0; pb < k8PB; ++pb)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) acc[cb][pb][4 * m + e] = -0.5f * v[e];
-        }
-    }
+    if (BF && s == 0) seed(ct);
     if (s == 0)
       mfma_stage(cur, std::true_type{});
     else
